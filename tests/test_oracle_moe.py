@@ -1,0 +1,162 @@
+"""Pins of the MoE parts of the oracle: the slow MoE stream against a library
+MoE decoder, and the expert-cache simulation against a textbook LRU and
+against the special cases the policy fixes."""
+from collections import OrderedDict
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import Oracle, KVCache, simulate_expert_cache
+
+MOE = synth.ModelConfig("moe_pin", n_layers=3, d_model=64, n_heads=2, head_dim=32, ffn=0, vocab=50, rank=4,
+                        wdtype="f32", kvdtype="f64", n_experts=8, top_k=2, expert_ffn=32, seed=21)
+
+
+def _qwen2moe(cfg, w):
+    """HuggingFace Qwen2-MoE with its extras disabled (zero q/k/v biases, zero
+    shared expert, no top-k renormalisation): softmax router over all experts,
+    top-k, combine with the raw probabilities."""
+    from transformers import Qwen2MoeConfig, Qwen2MoeForCausalLM
+    c = Qwen2MoeConfig(vocab_size=cfg.vocab, hidden_size=cfg.d_model, intermediate_size=cfg.expert_ffn,
+                       moe_intermediate_size=cfg.expert_ffn, shared_expert_intermediate_size=cfg.expert_ffn,
+                       num_hidden_layers=cfg.n_layers, num_attention_heads=cfg.n_heads,
+                       num_key_value_heads=cfg.n_heads, num_experts=cfg.n_experts, num_experts_per_tok=cfg.top_k,
+                       norm_topk_prob=False, decoder_sparse_step=1, mlp_only_layers=[], tie_word_embeddings=False,
+                       rms_norm_eps=cfg.rms_eps, rope_theta=cfg.rope_theta, max_position_embeddings=1024)
+    c._attn_implementation = "eager"
+    c._experts_implementation = "eager"   # the per-expert loop (the grouped kernel has no float64)
+    m = Qwen2MoeForCausalLM(c).double().eval()
+    sd = {k: torch.zeros_like(v) for k, v in m.state_dict().items()}
+    T = lambda a: torch.tensor(np.asarray(a, np.float64))
+    sd["model.embed_tokens.weight"] = T(w["embed"])
+    sd["model.norm.weight"] = T(w["final_norm"])
+    sd["lm_head.weight"] = T(w["lm_head"])
+    for l in range(cfg.n_layers):
+        p = f"model.layers.{l}."
+        for nm, key in (("wq", "q_proj"), ("wk", "k_proj"), ("wv", "v_proj"), ("wo", "o_proj")):
+            sd[p + f"self_attn.{key}.weight"] = T(w[f"L{l}.{nm}"])
+        sd[p + "input_layernorm.weight"] = T(w[f"L{l}.attn_norm"])
+        sd[p + "post_attention_layernorm.weight"] = T(w[f"L{l}.mlp_norm"])
+        sd[p + "mlp.gate.weight"] = T(w[f"L{l}.router"])
+        sd[p + "mlp.experts.gate_up_proj"] = T(np.stack([np.concatenate([w[f"L{l}.E{e}.wg"], w[f"L{l}.E{e}.wu"]])
+                                                         for e in range(cfg.n_experts)]))
+        sd[p + "mlp.experts.down_proj"] = T(np.stack([w[f"L{l}.E{e}.wd"] for e in range(cfg.n_experts)]))
+    m.load_state_dict(sd, strict=True)
+    return m
+
+
+def test_moe_slow_stream_matches_library_moe_decoder():
+    cfg = MOE
+    w = synth.make_weights(cfg, threads=4)
+    ids = list(synth.prompt_ids(cfg, 10))
+    with torch.no_grad():
+        ref = _qwen2moe(cfg, w)(torch.tensor([ids])).logits[0].numpy()
+    got = Oracle(cfg, w).slow_chunk(ids, 0, KVCache(cfg, 16))
+    # the library evaluates rotary angles and router softmax in float32
+    np.testing.assert_allclose(got, ref, rtol=1e-5, atol=2e-6)
+
+
+def test_moe_dual_step_slow_logits_equal_chunk_forward():
+    cfg = MOE
+    w = synth.make_weights(cfg, threads=4)
+    orc = Oracle(cfg, w)
+    ids = list(synth.prompt_ids(cfg, 7))
+    full = orc.slow_chunk(ids, 0, KVCache(cfg, 16))
+    c = KVCache(cfg, 16)
+    orc.slow_chunk(ids[:-1], 0, c)
+    r = orc.decode_step(ids[-1], len(ids) - 1, c, mode="off")
+    np.testing.assert_allclose(r.logits, full[-1], rtol=1e-12, atol=1e-13)
+    # predictions exist exactly for layers 2i+2, 2i+3 below N
+    assert (r.pred_experts[:2] == -1).all() and (r.pred_experts[2:] >= 0).all()
+
+
+def test_zero_adapters_predict_from_slow_state():
+    """With zero adapters p == h, so the prediction for layer l' is the top-k
+    of router l' applied to the slow state after layer (l'-2)//2."""
+    cfg = MOE.replace(n_layers=4)
+    w = synth.make_weights(cfg, threads=4, adapter_scale=0.0)
+    orc = Oracle(cfg, w)
+    ids = list(synth.prompt_ids(cfg, 4))
+    c = KVCache(cfg, 8)
+    orc.slow_chunk(ids[:-1], 0, c)
+    r = orc.decode_step(ids[-1], len(ids) - 1, c, mode="off")
+    # slow state after layer 0 == a 1-layer model's final residual; recompute with a truncated oracle
+    sub = synth.make_weights(cfg.replace(n_layers=1), threads=4, adapter_scale=0.0)
+    o1 = Oracle(cfg.replace(n_layers=1), sub)
+    c1 = KVCache(cfg.replace(n_layers=1), 8)
+    o1.slow_chunk(ids[:-1], 0, c1)
+    r1 = o1.decode_step(ids[-1], len(ids) - 1, c1, mode="off")
+    for lp in (2, 3):
+        z = orc.router_logits(lp, r1.h)
+        np.testing.assert_array_equal(r.pred_experts[lp], np.lexsort((np.arange(cfg.n_experts), -z))[:cfg.top_k])
+
+
+# ---------------------------------------------------------------------------
+# Expert cache simulation
+# ---------------------------------------------------------------------------
+
+def _textbook_lru(trace, E, C):
+    """OrderedDict LRU per layer, warm start 0..C-1 (0 oldest); within a layer
+    step the resident experts are touched first, then the missing ones are loaded."""
+    T, N, K = trace.shape
+    caches = [OrderedDict((e, None) for e in range(C)) for _ in range(N)]
+    hits = misses = 0
+    for t in range(T):
+        for l in range(N):
+            od = caches[l]
+            need = [int(e) for e in trace[t, l]]
+            for e in need:
+                if e in od:
+                    od.move_to_end(e)
+                    hits += 1
+            for e in need:
+                if e not in od:
+                    misses += 1
+                    od.popitem(last=False)
+                    od[e] = None
+    return hits, misses
+
+
+@pytest.mark.parametrize("E,K,C", [(8, 2, 2), (8, 2, 3), (16, 4, 6), (64, 8, 16)])
+def test_cache_sim_without_prediction_is_textbook_lru(E, K, C):
+    rng = np.random.default_rng(E * 100 + C)
+    T, N = 40, 5
+    # skewed expert popularity so that both hits and misses occur
+    pop = rng.dirichlet(np.ones(E) * 0.3)
+    trace = np.stack([[rng.choice(E, K, replace=False, p=pop) for _ in range(N)] for _ in range(T)])
+    st = simulate_expert_cache(trace, None, E, C)
+    h, m = _textbook_lru(trace, E, C)
+    assert (st.hits, st.misses) == (h, m)
+    assert st.loads == m and st.prefetch_issued == 0
+
+
+def test_cache_sim_special_cases():
+    rng = np.random.default_rng(5)
+    E, K, N, T = 16, 4, 8, 30
+    trace = np.stack([[rng.choice(E, K, replace=False) for _ in range(N)] for _ in range(T)])
+    # every expert resident: all hits, nothing moves
+    st = simulate_expert_cache(trace, trace, E, E)
+    assert st.misses == 0 and st.hits == T * N * K and st.loads == 0
+    # a perfect predictor: every predicted layer (l >= 2) hits
+    pred = trace.copy()
+    pred[:, :2] = -1
+    st = simulate_expert_cache(trace, pred, E, K)
+    assert st.per_layer_misses[2:] == [0] * (N - 2)
+    assert st.pred_correct == st.pred_total == T * (N - 2) * K
+    assert st.prefetch_used + st.prefetch_wasted <= st.prefetch_issued
+    # C < K is rejected
+    with pytest.raises(ValueError):
+        simulate_expert_cache(trace, None, E, K - 1)
+
+
+def test_cache_sim_worked_example():
+    """Hand-worked trace: E=4, K=1, C=2, one layer."""
+    trace = np.array([[[2]], [[0]], [[2]], [[1]], [[3]], [[1]]])
+    # start: resident {0 (oldest), 1}
+    # t0 need 2: miss, evict 0 -> {1, 2}; t1 need 0: miss, evict 1 -> {2, 0};
+    # t2 need 2: hit -> {0, 2}; t3 need 1: miss, evict 0 -> {2, 1};
+    # t4 need 3: miss, evict 2 -> {1, 3}; t5 need 1: hit
+    st = simulate_expert_cache(trace, None, 4, 2)
+    assert (st.hits, st.misses) == (2, 4)
