@@ -1,0 +1,195 @@
+/*
+ * m2r2.h — C ABI of the MI355X (gfx950) decode path of M2R2, "Mixture of
+ * Multi-Rate Residuals" (arXiv 2502.02040).
+ *
+ * The library runs the autoregressive decode step of a pre-norm decoder-only
+ * transformer that carries, in one forward pass, the slow residual stream h
+ * (the base model, Eq. 1) and the accelerated residual stream p (Eq. 2):
+ * every projection of a layer is streamed from HBM once and applied to both
+ * rows; the fast row adds rank-r accelerator adapters (Sec. 2.2) and attends
+ * to the slow row's KV cache plus its own key/value (the shared cache of
+ * Sec. 2.2); at every layer the cosine between the fast state entering and
+ * leaving the layer is computed as the exit signal (the directional shift of
+ * Sec. 2.1), and at exit gates the fast row is either re-initialised from the
+ * slow row (Fig. 3 caption) or, in exit mode, emits the token (Eq. 4).
+ * On top of the step: self-speculative drafting from the fast stream and
+ * parallel verification on the slow stream (Sec. 2.3.2).
+ *
+ * Conventions (all entry points):
+ *  - Memory: the caller owns every buffer.  Pointers named *_d are device
+ *    pointers, *_h host pointers.  Weights are borrowed for the lifetime of a
+ *    context; activations, KV pages and outputs for the duration of a call.
+ *    The library never allocates device memory: all scratch lives in the
+ *    workspace passed to m2r2_create.
+ *  - Layout: matrices are row-major [d_out][d_in] (the reduction dimension is
+ *    contiguous).  Adapter factors are A [rank][d_in] and B [d_out][rank]; the
+ *    adapter adds (x A^T) B^T to the projection of x.  Matrices and adapters
+ *    are stored in the configured weight dtype; norm gains are always float32.
+ *  - KV cache: paged, slow stream only.  K and V pages are
+ *    [n_layers][num_blocks][n_heads][block_size][head_dim] in the configured
+ *    KV dtype; block_table is [batch][max_blocks_per_seq] int32 (physical
+ *    block of each logical block, shared by all layers).  Positions outside a
+ *    sequence's block table are not read or written (a sticky device error
+ *    bit is set instead).
+ *  - Streams: every call that takes a hipStream_t only enqueues work on it
+ *    (no host synchronisation), so a sequence of calls can be captured into a
+ *    HIP graph.  One context must not be used on two streams at once.
+ *  - Errors: no exception or abort crosses the ABI.  Arguments are checked
+ *    before anything is enqueued; on failure the call returns a negative
+ *    m2r2_status and m2r2_last_error() (thread-local) describes it.  A launch
+ *    failure reported by HIP returns M2R2_E_HIP.
+ */
+#ifndef M2R2_H_
+#define M2R2_H_
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define M2R2_API __attribute__((visibility("default")))
+
+typedef enum {
+  M2R2_OK = 0,
+  M2R2_E_INVALID = -1,      /* NULL pointer, bad enum, bad pointer alignment */
+  M2R2_E_SHAPE = -2,        /* a size is out of the supported range */
+  M2R2_E_DTYPE = -3,        /* unsupported dtype combination */
+  M2R2_E_NOMEM = -4,        /* workspace smaller than m2r2_workspace_size() */
+  M2R2_E_HIP = -5,          /* a HIP runtime call failed */
+  M2R2_E_STATE = -6,        /* call not valid in the context's current state */
+  M2R2_E_UNSUPPORTED = -7   /* valid request this build does not implement */
+} m2r2_status;
+
+typedef enum { M2R2_F32 = 0, M2R2_BF16 = 1 } m2r2_dtype;
+
+/* Exit handling at gates (Fig. 3 caption; Eq. 4).
+ *  OFF:     no gate is evaluated; p is never re-initialised.
+ *  OBSERVE: at each gate b the signal of layer b-1 is compared with tau; the
+ *           first gate with signal >= tau is recorded as the exit boundary,
+ *           and p <- h at every gate (the full-depth slow token is emitted).
+ *  EXIT:    as OBSERVE, but a sequence whose signal reaches tau at a gate
+ *           stops there: its token comes from the final norm and LM head on
+ *           p at the gate, and the KV entries of its remaining layers are
+ *           projected from the slow state h at the gate. */
+typedef enum { M2R2_EXIT_OFF = 0, M2R2_EXIT_OBSERVE = 1, M2R2_EXIT_EXIT = 2 } m2r2_exit_mode;
+
+typedef struct {
+  int32_t n_layers, d_model, n_heads, head_dim, ffn, vocab, rank;
+  int32_t wdtype;           /* m2r2_dtype of matrices, embeddings, adapters */
+  int32_t kvdtype;          /* m2r2_dtype of the KV pages */
+  float rms_eps;            /* RMSNorm epsilon */
+  float rope_theta;         /* rotate-half RoPE base */
+} m2r2_config;
+
+/* Per-layer device pointers.  Any adapter pointer may be NULL (adapter
+ * absent: that projection of the fast row equals the slow one). */
+typedef struct {
+  const float* attn_norm;   /* [d] */
+  const void* wq;           /* [H*hd][d] */
+  const void* wk;           /* [H*hd][d] */
+  const void* wv;           /* [H*hd][d] */
+  const void* wo;           /* [d][H*hd] */
+  const float* mlp_norm;    /* [d] */
+  const void* wg;           /* [ffn][d]  gate */
+  const void* wu;           /* [ffn][d]  up */
+  const void* wd;           /* [d][ffn]  down */
+  /* accelerator adapters, index 0..6 = q, k, v, o, gate, up, down */
+  const void* A[7];
+  const void* B[7];
+} m2r2_layer_weights;
+
+typedef struct {
+  const void* embed;                 /* [vocab][d] */
+  const float* final_norm;           /* [d] */
+  const void* lm_head;               /* [vocab][d] */
+  const m2r2_layer_weights* layers;  /* host array of n_layers entries, copied by m2r2_create */
+} m2r2_weights;
+
+typedef struct {
+  void* k_pages;                 /* device, see layout above */
+  void* v_pages;
+  const int32_t* block_table_d;  /* [batch][max_blocks_per_seq] */
+  int32_t* seq_lens_d;           /* [batch]: written with the number of valid cache positions */
+  int32_t num_blocks, block_size, max_blocks_per_seq;
+} m2r2_kv;
+
+typedef struct {
+  const int32_t* gates_h;   /* host array of gate boundaries b in [1, n_layers-1] */
+  int32_t n_gates;
+  float tau;                /* exit iff signal >= tau */
+  int32_t mode;             /* m2r2_exit_mode */
+} m2r2_exit;
+
+typedef struct {
+  int32_t* next_token_d;    /* [batch] required: greedy token (lowest id on ties) */
+  int32_t* exit_boundary_d; /* [batch] optional: first gate whose signal >= tau, n_layers if none */
+  float* signal_d;          /* [batch][n_layers] optional: cos(p entering, p leaving) per layer */
+  float* logits_d;          /* [batch][vocab] optional: logits of the emitted row */
+  float* h_out_d;           /* [batch][d] optional: slow row fed to the head (gate state on exit) */
+  float* p_out_d;           /* [batch][d] optional: fast row at the end of the step */
+  int32_t advance;          /* nonzero: positions_d[b] += 1 at the end of the step */
+} m2r2_step_out;
+
+typedef struct m2r2_ctx m2r2_ctx;
+
+/* Workspace bytes a context needs for up to max_batch sequences, chunks of
+ * up to max_chunk rows (verification/prefill) and max_ctx cache positions per
+ * sequence.  max_batch <= 8, max_chunk <= 16. */
+M2R2_API m2r2_status m2r2_workspace_size(const m2r2_config* cfg, int32_t max_batch, int32_t max_chunk,
+                                         int32_t max_ctx, size_t* bytes_out);
+
+/* Create a context.  `workspace` is device memory of at least the size above,
+ * 256-byte aligned, owned by the caller and used exclusively by this context;
+ * it is initialised here (synchronously on the null stream).  Requirements:
+ * d_model, H*head_dim and ffn multiples of 32 (bf16) or 16 (f32); head_dim
+ * even and <= 128; rank <= 32. */
+M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, int32_t max_batch,
+                                 int32_t max_chunk, int32_t max_ctx, void* workspace, size_t ws_bytes,
+                                 m2r2_ctx** out);
+M2R2_API void m2r2_destroy(m2r2_ctx* ctx);
+
+/* One dual-stream decode step (Eq. 1 and Eq. 2 with the shared KV cache,
+ * Sec. 2.2) for `batch` sequences.  tokens_d[b] is the input token of
+ * sequence b and positions_d[b] its position t; the cache must hold t valid
+ * positions.  The slow row's key/value at t are written to the cache and
+ * seq_lens_d[b] is set to t+1.  `dual` = 0 runs the slow row alone (plain
+ * decoding on the same kernels; exit settings are then ignored).
+ * tokens_d may alias out->next_token_d. */
+M2R2_API m2r2_status m2r2_decode_step(m2r2_ctx* ctx, int32_t batch, int32_t dual, const int32_t* tokens_d,
+                                      int32_t* positions_d, const m2r2_kv* kv, const m2r2_exit* ex,
+                                      const m2r2_step_out* out, hipStream_t stream);
+
+/* Self-speculative draft (Sec. 2.3.2): gamma greedy tokens from the fast row
+ * alone, run through layers 0..exit_layer-1 (a fast stream at rate
+ * n_layers/exit_layer), then the final norm and LM head.  Batch 1.  The first
+ * draft consumes last_token_d[0] at position positions_d[0] = t; draft j is at
+ * position t+j.  The fast row's key/value at those positions are written to
+ * cache positions t..t+gamma-1 of layers < exit_layer, where later drafts read
+ * them; m2r2_verify overwrites them.  Writes drafts_d[0..gamma). */
+M2R2_API m2r2_status m2r2_draft(m2r2_ctx* ctx, const int32_t* last_token_d, const int32_t* positions_d,
+                                int32_t exit_layer, int32_t gamma, const m2r2_kv* kv, int32_t* drafts_d,
+                                hipStream_t stream);
+
+/* Parallel verification on the slow stream (Sec. 2.3.2) of a chunk of n
+ * tokens chunk_d[0..n) at positions t..t+n-1 (t = positions_d[0]), causal,
+ * batch 1.  Writes the cache at those positions and targets_d[i] = greedy
+ * token after chunk row i.  If n_accepted_d is not NULL, the chunk is
+ * [last, d_1..d_{n-1}] and n_accepted_d[0] = largest j with
+ * d_1..d_j == targets_d[0..j); seq_lens_d[0] = t + j + 1; if
+ * bonus_token_d is not NULL it receives targets_d[j]; positions_d[0] is
+ * advanced by j + 1.  If n_accepted_d is NULL (prefill) every row is kept:
+ * seq_lens_d[0] = t + n and positions_d[0] is advanced by n.  1 <= n <= max_chunk. */
+M2R2_API m2r2_status m2r2_verify(m2r2_ctx* ctx, const int32_t* chunk_d, int32_t n, int32_t* positions_d,
+                                 const m2r2_kv* kv, int32_t* targets_d, int32_t* n_accepted_d,
+                                 int32_t* bonus_token_d, hipStream_t stream);
+
+/* Description of the last error on this thread ("" if none). */
+M2R2_API const char* m2r2_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* M2R2_H_ */

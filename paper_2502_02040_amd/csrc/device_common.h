@@ -1,0 +1,112 @@
+// Device-side building blocks shared by the decode kernels (gfx950).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+namespace m2r2 {
+
+constexpr int kMaxRows = 16;     // rows of one GEMV (an MFMA tile is 16 rows high)
+constexpr int kMaxSeq = 16;
+constexpr int kMaxRank = 32;
+constexpr int kMaxHeadDim = 128;
+
+// ----------------------------------------------------------------------------
+// bfloat16 <-> float32
+// ----------------------------------------------------------------------------
+__device__ __forceinline__ float bf16lo(uint32_t v) { return __uint_as_float(v << 16); }
+__device__ __forceinline__ float bf16hi(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// Round to nearest even (inputs are finite).
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+__device__ __forceinline__ float round_bf16(float f) { return __uint_as_float(f32_to_bf16_bits(f) << 16); }
+
+// Split 8 floats into bf16 hi + lo parts (x ~= hi + lo with 16 significant bits).
+__device__ __forceinline__ void split_hi_lo(const float (&x)[8], bf16x8_t& hi, bf16x8_t& lo) {
+  u32x4_t h, l;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    uint32_t a = f32_to_bf16_bits(x[2 * i]), b = f32_to_bf16_bits(x[2 * i + 1]);
+    float ra = x[2 * i] - __uint_as_float(a << 16), rb = x[2 * i + 1] - __uint_as_float(b << 16);
+    h[i] = a | (b << 16);
+    l[i] = f32_to_bf16_bits(ra) | (f32_to_bf16_bits(rb) << 16);
+  }
+  hi = __builtin_bit_cast(bf16x8_t, h);
+  lo = __builtin_bit_cast(bf16x8_t, l);
+}
+
+// ----------------------------------------------------------------------------
+// Loads
+// ----------------------------------------------------------------------------
+__device__ __forceinline__ u32x4_t ld_stream(const void* p) {
+  // weights are read exactly once per step: non-temporal hint
+  return __builtin_nontemporal_load((const u32x4_t*)p);
+}
+__device__ __forceinline__ float4 ld4(const float* p) { return *(const float4*)p; }
+
+// ----------------------------------------------------------------------------
+// Wave reductions (64 lanes)
+// ----------------------------------------------------------------------------
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+// Block-wide sum of one value per thread; `red` holds blockDim/64 floats.
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  v = wave_sum(v);
+  __syncthreads();
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  float s = 0.f;
+  for (int i = 0; i < nw; ++i) s += red[i];
+  return s;
+}
+__device__ __forceinline__ float block_max(float v, float* red) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  v = wave_max(v);
+  __syncthreads();
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  float s = -INFINITY;
+  for (int i = 0; i < nw; ++i) s = fmaxf(s, red[i]);
+  return s;
+}
+
+// Arrival counter for "the last workgroup finishes the job" patterns.  Every
+// thread's prior global writes are released before the increment; the
+// workgroup that observes `total-1` resets the counter (for the next launch)
+// and acquires everyone else's writes.  Returns true in that workgroup.
+__device__ __forceinline__ bool arrive_last(uint32_t* counter, uint32_t total, int* flag_lds) {
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t old = atomicAdd(counter, 1u);
+    int last = (old == total - 1);
+    if (last) atomicExch(counter, 0u);
+    *flag_lds = last;
+  }
+  __syncthreads();
+  const bool last = *flag_lds != 0;
+  if (last) __threadfence();
+  return last;
+}
+
+__device__ __forceinline__ float silu(float x) { return x / (1.f + __expf(-x)); }
+
+}  // namespace m2r2

@@ -1,0 +1,58 @@
+"""The C ABI library loads, exports what include/m2r2.h declares, and rejects
+bad arguments before touching a device (no GPU needed)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import synth
+from paper_2502_02040_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "m2r2.h")).read()
+    return set(re.findall(r"M2R2_API\s+[\w\s\*]+?\b(m2r2_\w+)\s*\(", src))
+
+
+def test_header_declarations_match_binding():
+    assert _declared() == set(binding.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = binding.lib()
+    for name in _declared():
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", binding.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\bT (m2r2_\w+)", out))
+    assert exported == _declared()
+
+
+def test_workspace_size_and_validation():
+    cfg = synth.CONFIGS["phi3"]
+    n = binding.workspace_size(cfg, 1, 16, 1536)
+    assert 0 < n < 1 << 30
+    assert binding.workspace_size(cfg, 8, 16, 4352) >= n
+    with pytest.raises(binding.M2R2Error) as e:
+        binding.workspace_size(cfg.replace(head_dim=80), 1, 16, 1024)
+    assert e.value.status == -7
+    with pytest.raises(binding.M2R2Error) as e:
+        binding.workspace_size(cfg, 9, 16, 1024)
+    assert e.value.status == -2
+    with pytest.raises(binding.M2R2Error) as e:
+        binding.workspace_size(cfg.replace(d_model=3000), 1, 16, 1024)
+    assert e.value.status == -2
+
+
+def test_null_arguments_are_rejected():
+    lib = binding.lib()
+    assert lib.m2r2_decode_step(None, 1, 1, None, None, None, None, None, None) == -1
+    assert b"ctx" in lib.m2r2_last_error()
+    assert lib.m2r2_verify(None, None, 1, None, None, None, None, None, None) == -1
+    assert lib.m2r2_draft(None, None, None, 1, 1, None, None, None) == -1
+    cfg = binding.make_config(synth.CONFIGS["tiny"])
+    out = ctypes.c_void_p()
+    assert lib.m2r2_create(ctypes.byref(cfg), None, 1, 16, 128, None, 0, ctypes.byref(out)) == -1

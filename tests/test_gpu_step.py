@@ -1,0 +1,168 @@
+"""GPU parity of the dual-stream decode step, the chunked slow forward and the
+self-speculative draft/verify, through the C ABI, against the CPU oracle.
+
+Inputs are the seeded synthetic weights and prompts of synth; the paged
+cache uses a shuffled block table.  Sizes: the tiny float32 decoder (2
+layers, d 256, 4 heads x 64) and a small bfloat16 decoder (3 layers, d 192,
+2 heads x 96, ffn 320: tiles of 16 rows leave ragged tails in the LM head,
+vocab 1000)."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from tests.gpu_harness import Pair, Tally, rel, token_decidable
+
+pytestmark = pytest.mark.gpu
+
+CASES = ["tiny", "small_bf16"]
+
+
+def _decode_run(name, *, mode, tau, gates, n_steps, adapter_scale=1.0, block_size=16, prompt_len=16):
+    cfg = synth.CONFIGS[name]
+    w = synth.make_weights(cfg, adapter_scale=adapter_scale)
+    pair = Pair(cfg, w, max_ctx=prompt_len + n_steps + 8, block_size=block_size, table_seed=3)
+    t = Tally()
+    prompt = list(synth.prompt_ids(cfg, prompt_len))
+    tok = pair.prefill(prompt, tally=t)
+    pair.check_cache(0, 0, prompt_len, t, "prefill")
+    dev = pair.dev
+    N = cfg.n_layers
+    tok_d = torch.tensor([tok], dtype=torch.int32, device=dev)
+    pos_d = torch.tensor([prompt_len], dtype=torch.int32, device=dev)
+    nxt = torch.zeros(1, dtype=torch.int32, device=dev)
+    exb = torch.zeros(1, dtype=torch.int32, device=dev)
+    sig = torch.zeros(N, dtype=torch.float32, device=dev)
+    logits = torch.zeros(cfg.vocab, dtype=torch.float32, device=dev)
+    h_out = torch.zeros(cfg.d_model, dtype=torch.float32, device=dev)
+    p_out = torch.zeros(cfg.d_model, dtype=torch.float32, device=dev)
+    exits = 0
+    for step in range(n_steps):
+        pos = prompt_len + step
+        pair.model.decode_step(tok_d, pos_d, pair.kv.desc(), gates=gates, tau=tau, mode=mode, next_token=nxt,
+                               exit_boundary=exb, signal=sig, logits=logits, h_out=h_out, p_out=p_out, advance=True)
+        torch.cuda.synchronize()
+        r = pair.orc.decode_step(int(tok_d.item()), pos, pair.caches[0], gates=gates, tau=tau, mode=mode)
+        assert int(pos_d.item()) == pos + 1 and int(pair.kv.seq_lens[0].item()) == pos + 1
+        got_sig = sig.cpu().numpy()
+        ambiguous = any(abs(r.signal[b - 1] - tau) <= pair.tol for b in gates if b - 1 < N)
+        if not ambiguous:
+            assert int(exb.item()) == r.exit_boundary, f"step {step}: exit boundary"
+            t.rel(logits.cpu().numpy(), r.logits, pair.tol, f"step {step} logits")
+            t.rel(h_out.cpu().numpy(), r.h, pair.tol, f"step {step} h")
+            t.rel(p_out.cpu().numpy(), r.p, pair.tol, f"step {step} p")
+            ran = [l for l in range(N) if not (mode == "exit" and r.exit_boundary < N and l >= r.exit_boundary)]
+            assert np.max(np.abs(got_sig[ran] - r.signal[ran])) <= pair.tol, f"step {step} signal"
+            t.token(int(nxt.item()), r.logits, pair.tol, f"step {step} token")
+            pair.check_cache(0, pos, pos + 1, t, f"step {step}")
+            exits += r.exit_boundary < N
+        else:
+            t.skipped += 1
+            break   # the two sides may now hold different caches
+        tok_d.copy_(nxt)
+    return t, exits
+
+
+@pytest.mark.parametrize("name", CASES)
+def test_dual_step_observe(name):
+    """OBSERVE mode at every interior boundary: slow token, fast state,
+    per-layer signal and the paged cache match the oracle step by step."""
+    cfg = synth.CONFIGS[name]
+    gates = list(range(1, cfg.n_layers))
+    t, _ = _decode_run(name, mode="observe", tau=0.9, gates=gates, n_steps=12)
+    assert t.compared >= 6
+
+
+@pytest.mark.parametrize("name", CASES)
+@pytest.mark.parametrize("tau", [-1.0, 0.5])
+def test_dual_step_exit(name, tau):
+    """EXIT mode: the token comes from the fast row at the gate and the
+    skipped layers' cache entries are projected from the slow row."""
+    t, exits = _decode_run(name, mode="exit", tau=tau, gates=[1], n_steps=8)
+    if tau < 0:
+        assert exits == 8
+
+
+def test_zero_adapters_fast_row_tracks_slow_row():
+    """P1 on the GPU: zero adapters, no gates -> p == h within tolerance."""
+    t, _ = _decode_run("tiny", mode="off", tau=2.0, gates=[], n_steps=4, adapter_scale=0.0)
+
+
+@pytest.mark.parametrize("block_size", [1, 16, 64])
+def test_block_size_and_table_invariance(block_size):
+    """P8: results do not depend on the block size or the block-table permutation."""
+    _decode_run("tiny", mode="observe", tau=0.9, gates=[1], n_steps=4, block_size=block_size)
+
+
+@pytest.mark.parametrize("name", CASES)
+def test_single_stream_step(name):
+    """dual = 0: the slow row alone (plain decoding on the same kernels)."""
+    cfg = synth.CONFIGS[name]
+    w = synth.make_weights(cfg)
+    pair = Pair(cfg, w, max_ctx=40)
+    t = Tally()
+    prompt = list(synth.prompt_ids(cfg, 9))
+    tok = pair.prefill(prompt, tally=t)
+    dev = pair.dev
+    tok_d = torch.tensor([tok], dtype=torch.int32, device=dev)
+    pos_d = torch.tensor([len(prompt)], dtype=torch.int32, device=dev)
+    nxt = torch.zeros(1, dtype=torch.int32, device=dev)
+    logits = torch.zeros(cfg.vocab, dtype=torch.float32, device=dev)
+    for step in range(6):
+        pos = len(prompt) + step
+        pair.model.decode_step(tok_d, pos_d, pair.kv.desc(), dual=False, next_token=nxt, logits=logits, advance=True)
+        torch.cuda.synchronize()
+        ref = pair.orc.slow_chunk([int(tok_d.item())], pos, pair.caches[0])[0]
+        t.rel(logits.cpu().numpy(), ref, pair.tol, f"step {step}")
+        t.token(int(nxt.item()), ref, pair.tol)
+        pair.check_cache(0, pos, pos + 1, t)
+        tok_d.copy_(nxt)
+
+
+@pytest.mark.parametrize("name", CASES)
+@pytest.mark.parametrize("gamma,exit_layer", [(3, 1), (4, 2)])
+def test_draft_and_verify(name, gamma, exit_layer):
+    """Draft from the fast row exiting at `exit_layer`, verify on the slow
+    stream: drafts, targets and the acceptance bookkeeping match the oracle."""
+    cfg = synth.CONFIGS[name]
+    if exit_layer > cfg.n_layers:
+        pytest.skip("exit layer beyond depth")
+    w = synth.make_weights(cfg)
+    pair = Pair(cfg, w, max_ctx=64)
+    t = Tally()
+    prompt = list(synth.prompt_ids(cfg, 11))
+    tok = pair.prefill(prompt, tally=t)
+    dev = pair.dev
+    buf = torch.zeros(gamma + 1, dtype=torch.int32, device=dev)   # [last, d1..d_gamma]
+    buf[0] = tok
+    pos_d = torch.tensor([len(prompt)], dtype=torch.int32, device=dev)
+    targets = torch.zeros(gamma + 1, dtype=torch.int32, device=dev)
+    n_acc = torch.zeros(1, dtype=torch.int32, device=dev)
+    pos = len(prompt)
+    for rnd in range(4):
+        last = int(buf[0].item())
+        pair.model.draft(buf[0:1], pos_d, exit_layer, gamma, pair.kv.desc(), buf[1:])
+        torch.cuda.synchronize()
+        drafts = buf[1:].cpu().numpy().tolist()
+        # oracle drafts from the same state, compared while unambiguous
+        ref_d = pair.orc.draft(last, pos, pair.caches[0], exit_layer, gamma)
+        for j in range(gamma):
+            if drafts[j] != ref_d[j]:
+                break
+            t.compared += 1
+        # draft cache entries (fast k/v of layers < exit_layer at pos..pos+gamma-1) are scratch: not compared
+        pair.model.verify(buf, gamma + 1, pos_d, pair.kv.desc(), targets, n_accepted=n_acc, bonus=buf[0:1])
+        torch.cuda.synchronize()
+        tg = targets.cpu().numpy().tolist()
+        ref = pair.orc.slow_chunk([last] + drafts, pos, pair.caches[0])
+        for i in range(gamma + 1):
+            t.token(tg[i], ref[i], pair.tol, f"round {rnd} target {i}")
+        j = 0
+        while j < gamma and drafts[j] == tg[j]:
+            j += 1
+        assert int(n_acc.item()) == j
+        assert int(buf[0].item()) == tg[j]
+        assert int(pos_d.item()) == pos + j + 1 == int(pair.kv.seq_lens[0].item())
+        pair.check_cache(0, pos, pos + j + 1, t, f"round {rnd}")
+        pos += j + 1
+    assert t.compared > 0
