@@ -30,6 +30,7 @@ justification in the design notes of the repository):
 from __future__ import annotations
 
 import dataclasses
+import math
 from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
@@ -68,7 +69,7 @@ def rope(x: np.ndarray, pos, theta: float) -> np.ndarray:
 def attend(q: np.ndarray, K: np.ndarray, V: np.ndarray) -> np.ndarray:
     """Single-query multi-head attention: q [H, hd], K/V [T, H, hd] -> [H, hd]."""
     hd = q.shape[-1]
-    s = np.einsum("hd,thd->ht", q, K) / np.sqrt(hd)
+    s = np.einsum("hd,thd->ht", q, K) / math.sqrt(hd)   # a Python float keeps q's precision
     s = s - s.max(axis=-1, keepdims=True)
     w = np.exp(s)
     w = w / w.sum(axis=-1, keepdims=True)
