@@ -17,10 +17,15 @@
  *
  * Conventions (all entry points):
  *  - Memory: the caller owns every buffer.  Pointers named *_d are device
- *    pointers, *_h host pointers.  Weights are borrowed for the lifetime of a
- *    context; activations, KV pages and outputs for the duration of a call.
- *    The library never allocates device memory: all scratch lives in the
- *    workspace passed to m2r2_create.
+ *    pointers, *_h host pointers.  The library never allocates device memory:
+ *    the workspace passed to m2r2_create holds a tile-packed copy of every
+ *    projection matrix (so that each wave's 16-byte loads form 1 KB contiguous
+ *    blocks that are exactly MFMA operands) and all scratch.  The row-major
+ *    projection matrices (wq, wk, wv, wo, wg, wu, wd, the LM head) and the
+ *    q/k/v adapter-down factors A[0..2] are read only during m2r2_create and
+ *    may be freed afterwards; the embedding, norm gains and the remaining
+ *    adapter factors are borrowed for the lifetime of the context.
+ *    Activations, KV pages and outputs are borrowed for the duration of a call.
  *  - Layout: matrices are row-major [d_out][d_in] (the reduction dimension is
  *    contiguous).  Adapter factors are A [rank][d_in] and B [d_out][rank]; the
  *    adapter adds (x A^T) B^T to the projection of x.  Matrices and adapters
@@ -135,15 +140,17 @@ typedef struct {
 
 typedef struct m2r2_ctx m2r2_ctx;
 
-/* Workspace bytes a context needs for up to max_batch sequences, chunks of
- * up to max_chunk rows (verification/prefill) and max_ctx cache positions per
- * sequence.  max_batch <= 8, max_chunk <= 16. */
+/* Workspace bytes a context needs (packed weights plus scratch) for up to
+ * max_batch sequences, chunks of up to max_chunk rows (verification/prefill)
+ * and max_ctx cache positions per sequence.  max_batch <= 8, max_chunk <= 16. */
 M2R2_API m2r2_status m2r2_workspace_size(const m2r2_config* cfg, int32_t max_batch, int32_t max_chunk,
                                          int32_t max_ctx, size_t* bytes_out);
 
 /* Create a context.  `workspace` is device memory of at least the size above,
  * 256-byte aligned, owned by the caller and used exclusively by this context;
- * it is initialised here (synchronously on the null stream).  Requirements:
+ * it is initialised here, including packing the projection matrices
+ * (synchronously, on the null stream).  Weight pointers must be 16-byte
+ * aligned.  Requirements:
  * d_model, H*head_dim and ffn multiples of 32 (bf16) or 16 (f32); head_dim
  * even and <= 128; rank <= 32. */
 M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, int32_t max_batch,
@@ -185,6 +192,24 @@ M2R2_API m2r2_status m2r2_draft(m2r2_ctx* ctx, const int32_t* last_token_d, cons
 M2R2_API m2r2_status m2r2_verify(m2r2_ctx* ctx, const int32_t* chunk_d, int32_t n, int32_t* positions_d,
                                  const m2r2_kv* kv, int32_t* targets_d, int32_t* n_accepted_d,
                                  int32_t* bonus_token_d, hipStream_t stream);
+
+/* Kernel timing for measurement.  Kernel classes of one decode pass:
+ * 0 qkv, 1 attention, 2 output projection, 3 gate/up, 4 down, 5 LM head,
+ * 6 embedding, 7 attention merge.  m2r2_timing_enable(ctx, k) starts a new record: every
+ * launch of class k made by later calls is bracketed by a pair of HIP events
+ * recorded on the call's stream (up to 1024 launches; record with direct
+ * launches: events recorded inside a captured graph cannot be timed).
+ * m2r2_timing_read waits for the recorded events and returns the summed
+ * kernel milliseconds and the launch count of the record.  k = -1 stops
+ * recording.  Events are host-side objects created by the library (no device
+ * memory). */
+M2R2_API m2r2_status m2r2_timing_enable(m2r2_ctx* ctx, int32_t kernel_class);
+M2R2_API m2r2_status m2r2_timing_read(m2r2_ctx* ctx, double* ms_sum, int32_t* launches);
+
+/* Sticky device error bits set by kernels since the context was created
+ * (1: token id out of range, 2: cache position outside the block table,
+ * 4: context longer than the workspace was sized for); waits for `stream`. */
+M2R2_API m2r2_status m2r2_device_errors(m2r2_ctx* ctx, hipStream_t stream, int32_t* bits);
 
 /* Description of the last error on this thread ("" if none). */
 M2R2_API const char* m2r2_last_error(void);

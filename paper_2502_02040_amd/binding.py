@@ -22,7 +22,8 @@ MODES = {"off": EXIT_OFF, "observe": EXIT_OBSERVE, "exit": EXIT_EXIT}
 PROJ = ("q", "k", "v", "o", "g", "u", "d")
 
 EXPORTS = ("m2r2_workspace_size", "m2r2_create", "m2r2_destroy", "m2r2_decode_step", "m2r2_draft", "m2r2_verify",
-           "m2r2_last_error")
+           "m2r2_timing_enable", "m2r2_timing_read", "m2r2_device_errors", "m2r2_last_error")
+KERNEL_CLASSES = {"qkv": 0, "attn": 1, "oproj": 2, "gateup": 3, "down": 4, "head": 5, "embed": 6, "attn_merge": 7}
 
 
 class Config(ctypes.Structure):
@@ -76,8 +77,12 @@ def lib() -> ctypes.CDLL:
         L.m2r2_draft.argtypes = [c_void_p, c_void_p, c_void_p, c_int32, c_int32, POINTER(KV), c_void_p, c_void_p]
         L.m2r2_verify.argtypes = [c_void_p, c_void_p, c_int32, c_void_p, POINTER(KV), c_void_p, c_void_p, c_void_p,
                                   c_void_p]
+        L.m2r2_timing_enable.argtypes = [c_void_p, c_int32]
+        L.m2r2_timing_read.argtypes = [c_void_p, POINTER(ctypes.c_double), POINTER(c_int32)]
+        L.m2r2_device_errors.argtypes = [c_void_p, c_void_p, POINTER(c_int32)]
         L.m2r2_last_error.restype = ctypes.c_char_p
-        for f in ("m2r2_workspace_size", "m2r2_create", "m2r2_decode_step", "m2r2_draft", "m2r2_verify"):
+        for f in ("m2r2_workspace_size", "m2r2_create", "m2r2_decode_step", "m2r2_draft", "m2r2_verify",
+                  "m2r2_timing_enable", "m2r2_timing_read", "m2r2_device_errors"):
             getattr(L, f).restype = c_int32
         _lib = L
     return _lib
@@ -187,19 +192,28 @@ class Model:
             self._keep.append(t)
             return t.data_ptr()
 
+        # projection matrices (and the q/k/v adapter-down factors) are read by
+        # m2r2_create only: it packs them into the workspace
+        self._transient = []
+
+        def up_t(name):
+            t = torch.from_numpy(np.ascontiguousarray(weights[name], dtype=np.float32)).to(device=device, dtype=wdt)
+            self._transient.append(t)
+            return t.data_ptr()
+
         self._layers = (LayerWeights * cfg.n_layers)()
         for l in range(cfg.n_layers):
             p = f"L{l}."
             L = self._layers[l]
             L.attn_norm = up(p + "attn_norm", torch.float32)
             L.mlp_norm = up(p + "mlp_norm", torch.float32)
-            L.wq, L.wk, L.wv, L.wo = up(p + "wq"), up(p + "wk"), up(p + "wv"), up(p + "wo")
-            L.wg, L.wu, L.wd = up(p + "wg"), up(p + "wu"), up(p + "wd")
+            L.wq, L.wk, L.wv, L.wo = up_t(p + "wq"), up_t(p + "wk"), up_t(p + "wv"), up_t(p + "wo")
+            L.wg, L.wu, L.wd = up_t(p + "wg"), up_t(p + "wu"), up_t(p + "wd")
             for i, pr in enumerate(PROJ):
                 if p + f"A_{pr}" in weights:
-                    L.A[i] = up(p + f"A_{pr}")
+                    L.A[i] = up_t(p + f"A_{pr}") if i < 3 else up(p + f"A_{pr}")
                     L.B[i] = up(p + f"B_{pr}")
-        self._w = Weights(up("embed"), up("final_norm", torch.float32), up("lm_head"), self._layers)
+        self._w = Weights(up("embed"), up("final_norm", torch.float32), up_t("lm_head"), self._layers)
         self.ws_bytes = workspace_size(cfg, max_batch, max_chunk, max_ctx)
         self.workspace = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=device)
         base = self.workspace.data_ptr()
@@ -207,6 +221,8 @@ class Model:
         self._ctx = c_void_p()
         _check(lib().m2r2_create(ctypes.byref(make_config(cfg)), ctypes.byref(self._w), max_batch, max_chunk, max_ctx,
                                  ws_ptr, self.ws_bytes, ctypes.byref(self._ctx)), "m2r2_create")
+        torch.cuda.synchronize()
+        self._transient = []   # packed copies live in the workspace
 
     def __del__(self):
         try:
@@ -236,3 +252,18 @@ class Model:
     def verify(self, chunk, n: int, positions, kv: KV, targets, n_accepted=None, bonus=None, *, stream=None) -> None:
         _check(lib().m2r2_verify(self._ctx, chunk.data_ptr(), n, positions.data_ptr(), ctypes.byref(kv),
                                  targets.data_ptr(), _ptr(n_accepted), _ptr(bonus), _stream(stream)), "m2r2_verify")
+
+    def timing_enable(self, kernel: Optional[str]) -> None:
+        _check(lib().m2r2_timing_enable(self._ctx, -1 if kernel is None else KERNEL_CLASSES[kernel]),
+               "m2r2_timing_enable")
+
+    def timing_read(self):
+        """(summed kernel milliseconds, launches) of the current record."""
+        ms, n = ctypes.c_double(0.0), c_int32(0)
+        _check(lib().m2r2_timing_read(self._ctx, ctypes.byref(ms), ctypes.byref(n)), "m2r2_timing_read")
+        return ms.value, n.value
+
+    def device_errors(self, stream=None) -> int:
+        bits = c_int32(0)
+        _check(lib().m2r2_device_errors(self._ctx, _stream(stream), ctypes.byref(bits)), "m2r2_device_errors")
+        return bits.value

@@ -88,23 +88,39 @@ __device__ __forceinline__ float block_max(float v, float* red) {
   return s;
 }
 
-// Arrival counter for "the last workgroup finishes the job" patterns.  Every
-// thread's prior global writes are released before the increment; the
-// workgroup that observes `total-1` resets the counter (for the next launch)
-// and acquires everyone else's writes.  Returns true in that workgroup.
+// Device-coherent (agent scope) stores and loads.  Data that one workgroup
+// hands to another workgroup of the same kernel goes through these: they are
+// performed at the device coherence point (sc1), so no L2 write-back or
+// invalidate is needed; a release/acquire fence at agent scope per workgroup
+// would flush the L2 and costs an order of magnitude more than the kernel.
+__device__ __forceinline__ void st_agent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_agent(int* p, int v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_agent(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int ld_agent(const int* p) {
+  return __hip_atomic_load(const_cast<int*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Arrival counter for "the last workgroup finishes the job": every thread
+// waits until its st_agent stores are complete, then one thread counts the
+// workgroup in.  The workgroup that observes `total-1` resets the counter (for
+// the next launch) and may read the others' st_agent data with ld_agent.
 __device__ __forceinline__ bool arrive_last(uint32_t* counter, uint32_t total, int* flag_lds) {
-  __threadfence();
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (threadIdx.x == 0) {
-    uint32_t old = atomicAdd(counter, 1u);
-    int last = (old == total - 1);
-    if (last) atomicExch(counter, 0u);
+    const uint32_t old = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int last = (old == total - 1);
+    if (last) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     *flag_lds = last;
   }
   __syncthreads();
-  const bool last = *flag_lds != 0;
-  if (last) __threadfence();
-  return last;
+  return *flag_lds != 0;
 }
 
 __device__ __forceinline__ float silu(float x) { return x / (1.f + __expf(-x)); }

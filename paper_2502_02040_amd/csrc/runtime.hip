@@ -39,17 +39,22 @@ constexpr int kPerMaxBase = kScoreCap;
 
 int per_max(int rows) { return (kPerMaxBase / std::max(rows, 1)) & ~15; }
 
-// Context splits of the attention for `nseq` sequences of `rows` rows each.
+// Context splits of the attention for `nseq` sequences of `rows` rows each:
+// about 256 workgroups in total (each streams its share of the cache with many
+// loads in flight), at least as many as the LDS score buffer requires.
 int choose_splits(int nseq, int rows, int H, int max_ctx) {
-  const int target = std::max(1, (1024 + nseq * H - 1) / (nseq * H));
-  const int useful = std::max(1, (max_ctx + 63) / 64);
+  const int target = std::max(1, (256 + nseq * H - 1) / (nseq * H));
+  const int useful = std::max(1, (max_ctx + 127) / 128);
   const int need = std::max(1, (max_ctx + per_max(rows) - 1) / per_max(rows));
   return std::max(need, std::min(target, useful));
 }
 
 struct Layout {
-  size_t X, PIN, QKV, O, ACT, part_d, part_o, part_gu, uo, att, att_cnt, lm_val, lm_idx, lm_cnt, exited, exitb,
-      reinit, err, sig, total;
+  size_t packed;                         // start of the packed projection matrices
+  std::vector<size_t> lay_off;           // per layer: pq pk pv pa po pg pu pd (8 offsets)
+  size_t lm;                             // packed LM head
+  size_t X, PIN, QKV, O, ACT, bin_d, bin_o, bin_gu, uo, att, att_cnt, lm_val, lm_idx, lm_cnt, exited, exitb,
+      reinit, err, sig, rope, total;
   int TD, TF, TV, S_max;
 };
 
@@ -73,16 +78,30 @@ Layout make_layout(const m2r2_config& c, int max_batch, int max_chunk, int max_c
     off += (bytes + 255) & ~(size_t)255;
     return o;
   };
+  const int wb = c.wdtype == M2R2_BF16;
+  L.packed = 0;
+  for (int l = 0; l < c.n_layers; ++l) {
+    L.lay_off.push_back(take(packed_bytes(qdim, d, wb)));
+    L.lay_off.push_back(take(packed_bytes(qdim, d, wb)));
+    L.lay_off.push_back(take(packed_bytes(qdim, d, wb)));
+    L.lay_off.push_back(take(packed_bytes(3 * r, d, wb)));
+    L.lay_off.push_back(take(packed_bytes(d, qdim, wb)));
+    L.lay_off.push_back(take(packed_bytes(c.ffn, d, wb)));
+    L.lay_off.push_back(take(packed_bytes(c.ffn, d, wb)));
+    L.lay_off.push_back(take(packed_bytes(d, c.ffn, wb)));
+  }
+  L.lm = take(packed_bytes(c.vocab, d, wb));
   L.X = take(sizeof(float) * kMaxRows * d);
   L.PIN = take(sizeof(float) * kMaxRows * d);
   L.QKV = take(sizeof(float) * kMaxRows * nqkv);
   L.O = take(sizeof(float) * kMaxRows * qdim);
   L.ACT = take(sizeof(float) * kMaxRows * std::max(c.ffn, 1));
-  L.part_d = take(sizeof(float) * L.TD * kMaxRows * 4);
-  L.part_o = take(sizeof(float) * L.TD * kMaxRows * (1 + 2 * r));
-  L.part_gu = take(sizeof(float) * L.TF * kMaxRows * std::max(r, 1));
+  L.bin_d = take(sizeof(float) * (c.n_layers + 1) * kBins * kMaxRows * 4);
+  L.bin_o = take(sizeof(float) * c.n_layers * kBins * kMaxRows * (1 + 2 * r));
+  L.bin_gu = take(sizeof(float) * c.n_layers * kBins * kMaxRows * std::max(r, 1));
   L.uo = take(sizeof(float) * kMaxRows * c.n_heads * std::max(r, 1));
-  L.att = take(sizeof(float) * (size_t)std::max(max_batch, 1) * c.n_heads * smax * kMaxRows * (c.head_dim + 2));
+  L.att = take(sizeof(float) * (size_t)std::max(max_batch, 1) * c.n_heads * (smax + 1) * kMaxRows *
+               (c.head_dim + 2 + r));
   L.att_cnt = take(sizeof(uint32_t) * kMaxSeq * c.n_heads);
   L.lm_val = take(sizeof(float) * L.TV * kMaxRows);
   L.lm_idx = take(sizeof(int) * L.TV * kMaxRows);
@@ -92,6 +111,7 @@ Layout make_layout(const m2r2_config& c, int max_batch, int max_chunk, int max_c
   L.reinit = take(sizeof(int) * c.n_layers * kMaxSeq);
   L.err = take(sizeof(int));
   L.sig = take(sizeof(float) * kMaxSeq * c.n_layers);
+  L.rope = take(sizeof(float) * 2 * (size_t)max_ctx * (c.head_dim / 2));
   L.total = off;
   return L;
 }
@@ -128,9 +148,13 @@ struct m2r2_ctx {
   std::vector<LayerPtrs> layers;
   const void* embed;
   const float* final_norm;
-  const void* lm_head;
+  const void* lm_head;   // packed
   int max_batch, max_chunk, max_ctx;
   WS ws;
+  // kernel timing (measurement only)
+  int timed_class = -1;
+  std::vector<hipEvent_t> ev;   // pairs
+  int ev_used = 0;
 };
 
 namespace {
@@ -150,7 +174,36 @@ KVPtrs kv_ptrs(const m2r2_kv* kv) {
                 kv->max_blocks_per_seq};
 }
 
-template <int WB, int KB, int HD>
+constexpr int kMaxTimed = 1024;
+
+// Launch `fn` bracketed by timing events when its class is being timed.
+template <class F>
+m2r2_status timed(m2r2_ctx* c, int cls, hipStream_t st, F&& fn) {
+  const bool on = c->timed_class == cls && c->ev_used < kMaxTimed;
+  if (on) {
+    if ((int)c->ev.size() < 2 * (c->ev_used + 1)) {
+      hipEvent_t a, b;
+      HIP_TRY(hipEventCreate(&a));
+      HIP_TRY(hipEventCreate(&b));
+      c->ev.push_back(a);
+      c->ev.push_back(b);
+    }
+    HIP_TRY(hipEventRecord(c->ev[2 * c->ev_used], st));
+  }
+  fn();
+  if (on) {
+    HIP_TRY(hipEventRecord(c->ev[2 * c->ev_used + 1], st));
+    ++c->ev_used;
+  }
+  return M2R2_OK;
+}
+
+#define TIMED(cls, launch)                                                   \
+  do {                                                                       \
+    if (m2r2_status s_ = timed(c, cls, st, [&]() { launch; })) return s_;   \
+  } while (0)
+
+template <int WB, int KB, int HD, int MT>
 m2r2_status run_layers_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPtrs& kv, int n_layers_run,
                          hipStream_t st) {
   const Dims& D = c->D;
@@ -159,34 +212,89 @@ m2r2_status run_layers_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const 
   for (int s = 0; s < rm.nseq; ++s) rows_per_seq = std::max(rows_per_seq, (int)rm.cnt[s]);
   const int S = choose_splits(rm.nseq, rows_per_seq, D.H, c->max_ctx);
   if (S > c->lay.S_max) return fail(M2R2_E_SHAPE, "attention splits exceed the workspace");
+  if (S + 1 > 64) return fail(M2R2_E_SHAPE, "context too long for the attention merge (max_ctx %d)", c->max_ctx);
   const size_t smem = attn_smem_bytes();
+  const size_t gl = gemv_lds_bytes(WB, MT);
   for (int l = 0; l < n_layers_run; ++l) {
     const LayerPtrs& L = c->layers[l];
-    k_qkv<WB><<<(nqkv + 15) / 16, kGemvThreads, 0, st>>>(D, L, rm, c->ws, io, l, l == 0 ? 1 : c->lay.TD);
-    k_attn<KB, HD><<<dim3(S, D.H, rm.nseq), kAttnThreads, smem, st>>>(D, L, rm, c->ws, io, kv, l, S);
-    k_oproj<WB><<<c->lay.TD, kGemvThreads, 0, st>>>(D, L, rm, c->ws, io, l);
-    k_gateup<WB><<<c->lay.TF, kGemvThreads, 0, st>>>(D, L, rm, c->ws, io, c->lay.TD);
-    k_down<WB><<<c->lay.TD, kGemvThreads, 0, st>>>(D, L, rm, c->ws, io, c->lay.TF);
+    TIMED(0, (k_qkv<WB, MT><<<3 * (D.qdim / 16) + (3 * D.r + 15) / 16, kGemvThreads, gl, st>>>(D, L, rm, c->ws, io, l)));
+    TIMED(1, (k_attn<KB, HD><<<dim3(S + 1, D.H, rm.nseq), kAttnThreads, smem, st>>>(D, L, rm, c->ws, io, kv, l, S)));
+    TIMED(7, (k_attn_merge<<<dim3(D.H, rm.nseq), kAttnThreads, 0, st>>>(D, rm, c->ws, S)));
+    TIMED(2, (k_oproj<WB, MT><<<c->lay.TD, kGemvThreads, gl, st>>>(D, L, rm, c->ws, io, l)));
+    TIMED(3, (k_gateup<WB, MT><<<c->lay.TF, kGemvThreads, gl, st>>>(D, L, rm, c->ws, io, l)));
+    TIMED(4, (k_down<WB, MT><<<c->lay.TD, kGemvThreads, gl, st>>>(D, L, rm, c->ws, io, l)));
   }
-  k_head<WB><<<c->lay.TV, kGemvThreads, 0, st>>>(D, c->lm_head, c->final_norm, rm, c->ws, io, kv,
-                                                 n_layers_run == 0 ? 1 : c->lay.TD, c->lay.TV);
+  TIMED(5, (k_head<WB, MT><<<c->lay.TV, kGemvThreads, gl, st>>>(D, c->lm_head, c->final_norm, rm, c->ws, io, kv,
+                                                            c->lay.TV, n_layers_run)));
   HIP_TRY(hipGetLastError());
   return M2R2_OK;
+}
+
+template <int WB, int KB, int HD>
+m2r2_status run_mt(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPtrs& kv, int nl, hipStream_t st) {
+  if (rm.M <= 2) return run_layers_t<WB, KB, HD, 2>(c, rm, io, kv, nl, st);
+  return run_layers_t<WB, KB, HD, 16>(c, rm, io, kv, nl, st);
 }
 
 template <int WB, int KB>
 m2r2_status run_hd(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPtrs& kv, int nl, hipStream_t st) {
   switch (c->D.hd) {
-    case 64: return run_layers_t<WB, KB, 64>(c, rm, io, kv, nl, st);
-    case 96: return run_layers_t<WB, KB, 96>(c, rm, io, kv, nl, st);
-    case 128: return run_layers_t<WB, KB, 128>(c, rm, io, kv, nl, st);
+    case 64: return run_mt<WB, KB, 64>(c, rm, io, kv, nl, st);
+    case 96: return run_mt<WB, KB, 96>(c, rm, io, kv, nl, st);
+    case 128: return run_mt<WB, KB, 128>(c, rm, io, kv, nl, st);
   }
   return fail(M2R2_E_UNSUPPORTED, "head_dim");
 }
 
+// Pack the projection matrices of every layer and the LM head into the
+// workspace (null stream).
+hipError_t pack_one(int wb, PackSrc src, int rows, int K, void* dst) {
+  const size_t chunks = (size_t)((rows + 15) / 16) * (K / (wb ? 32 : 16)) * 64;
+  const int grid = (int)std::min<size_t>(8192, (chunks + 255) / 256);
+  if (wb) k_pack<1><<<grid, 256>>>(src, rows, K, dst);
+  else k_pack<0><<<grid, 256>>>(src, rows, K, dst);
+  return hipGetLastError();
+}
+
+hipError_t pack_all(m2r2_ctx* c, const m2r2_weights* w, void* workspace) {
+  const m2r2_config& cf = c->cfg;
+  const int wb = cf.wdtype == M2R2_BF16, d = cf.d_model, q = cf.n_heads * cf.head_dim, r = cf.rank, F = cf.ffn;
+  char* b = (char*)workspace;
+  auto one = [](const void* p, int rows) { return PackSrc{{p, nullptr, nullptr}, {rows, 0, 0}}; };
+  hipError_t e = hipSuccess;
+  for (int l = 0; l < cf.n_layers && e == hipSuccess; ++l) {
+    const m2r2_layer_weights& L = w->layers[l];
+    const size_t* o = &c->lay.lay_off[8 * l];
+    e = pack_one(wb, one(L.wq, q), q, d, b + o[0]);
+    if (e == hipSuccess) e = pack_one(wb, one(L.wk, q), q, d, b + o[1]);
+    if (e == hipSuccess) e = pack_one(wb, one(L.wv, q), q, d, b + o[2]);
+    if (e == hipSuccess) e = pack_one(wb, PackSrc{{L.A[0], L.A[1], L.A[2]}, {r, r, r}}, 3 * r, d, b + o[3]);
+    if (e == hipSuccess) e = pack_one(wb, one(L.wo, d), d, q, b + o[4]);
+    if (e == hipSuccess) e = pack_one(wb, one(L.wg, F), F, d, b + o[5]);
+    if (e == hipSuccess) e = pack_one(wb, one(L.wu, F), F, d, b + o[6]);
+    if (e == hipSuccess) e = pack_one(wb, one(L.wd, d), d, F, b + o[7]);
+  }
+  if (e == hipSuccess) e = pack_one(wb, one(w->lm_head, cf.vocab), cf.vocab, d, b + c->lay.lm);
+  return e;
+}
+
+// Allow the GEMV kernels the dynamic LDS of 16-row staging (> 64 KB).
+template <int WB, int MT>
+hipError_t set_lds_limits() {
+  const int bytes = gemv_lds_bytes(WB, MT);
+  hipError_t e = hipSuccess;
+  const void* fns[] = {(const void*)k_qkv<WB, MT>, (const void*)k_oproj<WB, MT>, (const void*)k_gateup<WB, MT>,
+                       (const void*)k_down<WB, MT>, (const void*)k_head<WB, MT>};
+  for (const void* f : fns) {
+    hipError_t r = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (r != hipSuccess) e = r;
+  }
+  return e;
+}
+
 // Embedding, n_layers_run layers, head.
 m2r2_status run_pass(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPtrs& kv, int nl, hipStream_t st) {
-  k_embed<<<rm.M, 256, 0, st>>>(c->D, c->embed, rm, c->ws, io, 1);
+  TIMED(6, (k_embed<<<rm.M, 256, 0, st>>>(c->D, c->embed, rm, c->ws, io, 1)));
   HIP_TRY(hipGetLastError());
   const int wb = c->D.wbf16, kb = c->D.kvbf16;
   if (wb && kb) return run_hd<1, 1>(c, rm, io, kv, nl, st);
@@ -240,9 +348,11 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
     const void* ps[] = {L.wq, L.wk, L.wv, L.wo, L.wg, L.wu, L.wd, w->embed, w->lm_head};
     for (const void* p : ps)
       if (!aligned16(p)) return fail(M2R2_E_INVALID, "layer %d: weight not 16-byte aligned", l);
-    for (int a = 0; a < 7; ++a)
+    for (int a = 0; a < 7; ++a) {
       if ((L.A[a] == nullptr) != (L.B[a] == nullptr))
         return fail(M2R2_E_INVALID, "layer %d adapter %d: A and B must be both set or both NULL", l, a);
+      if (!aligned16(L.A[a])) return fail(M2R2_E_INVALID, "layer %d adapter %d: A not 16-byte aligned", l, a);
+    }
   }
   m2r2_ctx* c = new (std::nothrow) m2r2_ctx();
   if (!c) return fail(M2R2_E_NOMEM, "host allocation");
@@ -253,7 +363,7 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
   c->max_ctx = max_ctx;
   c->embed = w->embed;
   c->final_norm = w->final_norm;
-  c->lm_head = w->lm_head;
+  c->lm_head = (char*)workspace + lay.lm;
   Dims& D = c->D;
   D.n_layers = cfg->n_layers; D.d = cfg->d_model; D.H = cfg->n_heads; D.hd = cfg->head_dim;
   D.qdim = cfg->n_heads * cfg->head_dim; D.F = cfg->ffn; D.V = cfg->vocab; D.r = cfg->rank;
@@ -262,20 +372,44 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
   for (int l = 0; l < cfg->n_layers; ++l) {
     const m2r2_layer_weights& s = w->layers[l];
     LayerPtrs& L = c->layers[l];
-    L.attn_norm = s.attn_norm; L.wq = s.wq; L.wk = s.wk; L.wv = s.wv; L.wo = s.wo;
-    L.mlp_norm = s.mlp_norm; L.wg = s.wg; L.wu = s.wu; L.wd = s.wd;
+    L.attn_norm = s.attn_norm;
+    L.mlp_norm = s.mlp_norm;
+    char* wsb = (char*)workspace;
+    const size_t* o = &lay.lay_off[8 * l];
+    L.pq = wsb + o[0]; L.pk = wsb + o[1]; L.pv = wsb + o[2]; L.pa = wsb + o[3];
+    L.po = wsb + o[4]; L.pg = wsb + o[5]; L.pu = wsb + o[6]; L.pd = wsb + o[7];
     for (int a = 0; a < 7; ++a) { L.A[a] = s.A[a]; L.B[a] = s.B[a]; }
   }
   char* b = (char*)workspace;
   WS& ws = c->ws;
   ws.X = (float*)(b + lay.X); ws.PIN = (float*)(b + lay.PIN); ws.QKV = (float*)(b + lay.QKV);
-  ws.O = (float*)(b + lay.O); ws.ACT = (float*)(b + lay.ACT); ws.part_d = (float*)(b + lay.part_d);
-  ws.part_o = (float*)(b + lay.part_o); ws.part_gu = (float*)(b + lay.part_gu); ws.uo = (float*)(b + lay.uo);
+  ws.O = (float*)(b + lay.O); ws.ACT = (float*)(b + lay.ACT); ws.bin_d = (float*)(b + lay.bin_d);
+  ws.bin_o = (float*)(b + lay.bin_o); ws.bin_gu = (float*)(b + lay.bin_gu); ws.uo = (float*)(b + lay.uo);
   ws.att = (float*)(b + lay.att); ws.att_cnt = (uint32_t*)(b + lay.att_cnt); ws.lm_val = (float*)(b + lay.lm_val);
   ws.lm_idx = (int*)(b + lay.lm_idx); ws.lm_cnt = (uint32_t*)(b + lay.lm_cnt); ws.exited = (int*)(b + lay.exited);
   ws.exitb = (int*)(b + lay.exitb); ws.reinit = (int*)(b + lay.reinit); ws.err = (int*)(b + lay.err);
   ws.sig = (float*)(b + lay.sig);
+  ws.rope = (const float2*)(b + lay.rope);
+  ws.rope_len = max_ctx;
+
   hipError_t e = hipMemset(workspace, 0, lay.total);
+  if (e == hipSuccess) {
+    // RoPE table: angle pos * theta^(-2j/hd) evaluated in double precision
+    const int half = cfg->head_dim / 2;
+    std::vector<float> t((size_t)max_ctx * half * 2);
+    for (int pos = 0; pos < max_ctx; ++pos)
+      for (int j = 0; j < half; ++j) {
+        const double ang = (double)pos * std::pow((double)cfg->rope_theta, -2.0 * j / cfg->head_dim);
+        t[((size_t)pos * half + j) * 2] = (float)std::cos(ang);
+        t[((size_t)pos * half + j) * 2 + 1] = (float)std::sin(ang);
+      }
+    e = hipMemcpy(b + lay.rope, t.data(), t.size() * sizeof(float), hipMemcpyHostToDevice);
+  }
+  if (e == hipSuccess) e = pack_all(c, w, workspace);
+  if (e == hipSuccess) e = set_lds_limits<0, 2>();
+  if (e == hipSuccess) e = set_lds_limits<1, 2>();
+  if (e == hipSuccess) e = set_lds_limits<0, 16>();
+  if (e == hipSuccess) e = set_lds_limits<1, 16>();
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) {
     delete c;
@@ -285,7 +419,40 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
   return M2R2_OK;
 }
 
-M2R2_API void m2r2_destroy(m2r2_ctx* ctx) { delete ctx; }
+M2R2_API void m2r2_destroy(m2r2_ctx* ctx) {
+  if (!ctx) return;
+  for (hipEvent_t e : ctx->ev) (void)hipEventDestroy(e);
+  delete ctx;
+}
+
+M2R2_API m2r2_status m2r2_timing_enable(m2r2_ctx* c, int32_t kernel_class) {
+  if (!c) return fail(M2R2_E_INVALID, "ctx is NULL");
+  if (kernel_class < -1 || kernel_class > 7) return fail(M2R2_E_INVALID, "kernel class %d", kernel_class);
+  c->timed_class = kernel_class;
+  c->ev_used = 0;   // a new record
+  return M2R2_OK;
+}
+
+M2R2_API m2r2_status m2r2_timing_read(m2r2_ctx* c, double* ms_sum, int32_t* launches) {
+  if (!c || !ms_sum || !launches) return fail(M2R2_E_INVALID, "NULL argument");
+  double sum = 0.0;
+  for (int i = 0; i < c->ev_used; ++i) {
+    HIP_TRY(hipEventSynchronize(c->ev[2 * i + 1]));
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, c->ev[2 * i], c->ev[2 * i + 1]));
+    sum += ms;
+  }
+  *ms_sum = sum;
+  *launches = c->ev_used;
+  return M2R2_OK;
+}
+
+M2R2_API m2r2_status m2r2_device_errors(m2r2_ctx* c, hipStream_t stream, int32_t* bits) {
+  if (!c || !bits) return fail(M2R2_E_INVALID, "NULL argument");
+  HIP_TRY(hipMemcpyAsync(bits, c->ws.err, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
+  HIP_TRY(hipStreamSynchronize(stream));
+  return M2R2_OK;
+}
 
 M2R2_API m2r2_status m2r2_decode_step(m2r2_ctx* c, int32_t batch, int32_t dual, const int32_t* tokens_d,
                                       int32_t* positions_d, const m2r2_kv* kv, const m2r2_exit* ex,

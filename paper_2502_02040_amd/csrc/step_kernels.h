@@ -34,14 +34,26 @@ struct Dims {
   int wbf16, kvbf16;
 };
 
+// Projection matrices are read from a tile-packed copy (pack_index below):
+// pq/pk/pv/pa (q, k, v and the stacked adapter-down rows [A_q; A_k; A_v]),
+// po, pg, pu, pd.  Adapter factors and norms stay row-major.
 struct LayerPtrs {
   const float* attn_norm;
-  const void *wq, *wk, *wv, *wo;
   const float* mlp_norm;
-  const void *wg, *wu, *wd;
+  const void *pq, *pk, *pv, *pa, *po, *pg, *pu, *pd;
   const void* A[7];
   const void* B[7];
 };
+
+// Tile-packed weight layout.  A [rows][K] matrix is stored as 16-row tiles;
+// within a tile, K is cut into MFMA steps (32 bf16 or 16 f32 elements) and
+// each step is one 1 KB block holding, for lane l of a wave, the 16 bytes
+// row (l % 16), elements [step*KSTEP + EPL*(l/16), +EPL) -- exactly the B
+// operand of one MFMA, so each wave load is 1 KB contiguous.  Rows past the
+// end of the matrix are zero.
+__host__ __device__ constexpr size_t packed_bytes(int rows, int K, int wb) {
+  return (size_t)((rows + 15) / 16) * 16 * K * (wb ? 2 : 4);
+}
 
 // Row bookkeeping, passed by value.  Rows of one sequence are contiguous.
 struct RowMap {
@@ -72,9 +84,14 @@ struct WS {
   float* QKV;      // [16][nqkv]    q|k|v|u_q|u_k|u_v (already divided by rms)
   float* O;        // [16][qdim]    attention output
   float* ACT;      // [16][F]       SwiGLU activation
-  float* part_d;   // [TD][16][4]   per 16-row tile of d: sum x^2, sum pin*x, sum pin^2
-  float* part_o;   // [TD][16][1+2r] sum x^2, adapter-down partials of gate and up
-  float* part_gu;  // [TF][16][r]   adapter-down partials of down
+  // Row statistics and adapter-down projections are sums over a whole row,
+  // which the producing kernel holds in 16-row tiles.  Each workgroup adds its
+  // tile's share with float atomics into one of kBins bins of the layer; the
+  // consumer (the next kernel) sums the kBins bins.  Bins are zeroed by the
+  // embedding kernel at the start of every pass.
+  float* bin_d;    // [n_layers+1][kBins][16][4]   sum x^2, sum pin*x, sum pin^2 (entering layer l)
+  float* bin_o;    // [n_layers][kBins][16][1+2r]  sum x^2, adapter-down of gate and up
+  float* bin_gu;   // [n_layers][kBins][16][r]     adapter-down of down
   float* uo;       // [16][H][r]    adapter-down of o, per head
   float* att;      // [nseq][H][S][rows][hd+2] split partials
   uint32_t* att_cnt;  // [16][H] arrival counters
@@ -86,7 +103,22 @@ struct WS {
   int* reinit;     // [n_layers][16]
   int* err;        // sticky device error bits
   float* sig;      // [16][n_layers] scratch signal (copied to the caller's buffer if any)
+  const float2* rope;  // [rope_len][hd/2] (cos, sin), built in double precision on the host
+  int rope_len;
 };
+
+constexpr int kBins = 8;
+
+__device__ __forceinline__ float* bin_d_at(const WS& ws, int l, int b, int m) { return ws.bin_d + (((size_t)l * kBins + b) * kMaxRows + m) * 4; }
+__device__ __forceinline__ float* bin_o_at(const WS& ws, const Dims& D, int l, int b, int m) {
+  return ws.bin_o + (((size_t)l * kBins + b) * kMaxRows + m) * (1 + 2 * D.r);
+}
+__device__ __forceinline__ float* bin_gu_at(const WS& ws, const Dims& D, int l, int b, int m) {
+  return ws.bin_gu + (((size_t)l * kBins + b) * kMaxRows + m) * D.r;
+}
+__device__ __forceinline__ void add_agent(float* p, float v) {
+  __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 struct StepIO {
   const int* tokens;     // token array indexed by RowMap::tok
@@ -126,100 +158,165 @@ __device__ __forceinline__ int row_pos(const RowMap& rm, const StepIO& io, int m
 //
 // One workgroup of 8 waves owns a tile of 16 consecutive weight rows (two
 // tiles for the paired gate/up projection).  The waves split the reduction
-// dimension; each lane streams 16-byte pieces of one weight row with
-// non-temporal loads and the matching 8 (bf16) or 4 (f32) activations of up
-// to 16 rows.  bf16 weights: v_mfma_f32_16x16x32_bf16 with the fp32
-// activations split into bf16 hi + lo parts (two MFMAs, ~16 significant bits
-// of the activation).  f32 weights: four v_mfma_f32_16x16x4_f32 per 16-byte
-// piece (exact fp32 products).  Accumulation is fp32.  The 8 partial results
-// are summed through LDS.
+// dimension into contiguous ranges.  A wave walks its range in chunks of 8
+// K-steps: the weight pieces of the next chunk are already in flight (16-byte
+// non-temporal loads, one weight row per lane group) while the activations of
+// the current chunk (up to 16 rows, times the norm gain when there is one) are
+// copied from global memory into the wave's own LDS region in MFMA fragment
+// order.  bf16 weights: v_mfma_f32_16x16x32_bf16 with each fp32 activation
+// split into bf16 hi + lo parts (two MFMAs, 16 significant bits of the
+// activation).  f32 weights: four v_mfma_f32_16x16x4_f32 per 16-byte piece
+// (exact fp32 products).  Accumulation is fp32; the 8 per-wave results are
+// summed through LDS (gemv_reduce).
 // ============================================================================
 constexpr int kGemvWaves = 8;
 constexpr int kGemvThreads = kGemvWaves * 64;
-constexpr int kBatch = 8;   // K-steps whose weight loads are in flight per wave
+constexpr int kChunk = 8;   // K-steps per chunk
 
-struct XSrc {
-  const float* row;   // activation row of this lane's m (nullptr: zero)
-  const float* gain;  // per-k gain or nullptr
-};
-
-template <int WB>
-__device__ __forceinline__ void mfma_step(const u32x4_t w, const float* xr, const float* g, int k, int grp,
-                                          f32x4_t& acc) {
-  if constexpr (WB) {
-    float xv[8];
-    if (xr) {
-      float4 a = ld4(xr + k + 8 * grp), b = ld4(xr + k + 8 * grp + 4);
-      xv[0] = a.x; xv[1] = a.y; xv[2] = a.z; xv[3] = a.w; xv[4] = b.x; xv[5] = b.y; xv[6] = b.z; xv[7] = b.w;
-      if (g) {
-        float4 ga = ld4(g + k + 8 * grp), gb = ld4(g + k + 8 * grp + 4);
-        xv[0] *= ga.x; xv[1] *= ga.y; xv[2] *= ga.z; xv[3] *= ga.w;
-        xv[4] *= gb.x; xv[5] *= gb.y; xv[6] *= gb.z; xv[7] *= gb.w;
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) xv[i] = 0.f;
-    }
-    bf16x8_t hi, lo;
-    split_hi_lo(xv, hi, lo);
-    const bf16x8_t wb = __builtin_bit_cast(bf16x8_t, w);
-    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, wb, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, wb, acc, 0, 0, 0);
-  } else {
-    float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (xr) {
-      a = ld4(xr + k + 4 * grp);
-      if (g) {
-        float4 ga = ld4(g + k + 4 * grp);
-        a.x *= ga.x; a.y *= ga.y; a.z *= ga.z; a.w *= ga.w;
-      }
-    }
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, __uint_as_float(w[0]), acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, __uint_as_float(w[1]), acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, __uint_as_float(w[2]), acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, __uint_as_float(w[3]), acc, 0, 0, 0);
-  }
+// Dynamic LDS bytes of the activation staging for the row class MT.
+__host__ __device__ constexpr int gemv_lds_bytes(int wb, int MT) {
+  return kGemvWaves * MT * kChunk * (wb ? 32 * 4 : 16 * 4);
 }
 
-// Accumulate NT tiles over this wave's K range.  wrow[t]: this lane's weight
-// row of tile t (nullptr: row absent -> contributes 0).
-template <int WB, int NT>
-__device__ __forceinline__ void gemv_wave(const void* const (&wrow)[NT], XSrc xs, int K, f32x4_t (&acc)[NT]) {
-  constexpr int KSTEP = WB ? 32 : 16;
-  constexpr int EPL = WB ? 8 : 4;          // elements per lane per step
-  constexpr int ESZ = WB ? 2 : 4;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int grp = lane >> 4;
-  const int nsteps = K / KSTEP;
-  const int per = (nsteps + kGemvWaves - 1) / kGemvWaves;
-  const int s0 = wave * per;
-  const int s1 = min(nsteps, s0 + per);
+// 16-byte load through a global-address-space pointer (no flat access).
+typedef float f32x4v_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ float4 ldg4(const float* p) {
+  const f32x4v_t v = *(const __attribute__((address_space(1))) f32x4v_t*)(p);
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+
+// MT: row-count class (2 or 16) the code is unrolled for; M <= MT rows are live.
+// GAIN: activations are multiplied by a per-k gain while staged.
+template <int WB, int NT, int MT, bool GAIN>
+struct GemvWave {
+  static constexpr int KSTEP = WB ? 32 : 16;   // K per MFMA step
+  static constexpr int P = KSTEP / 4;          // float4 pieces per step and row
+  u32x4_t w[NT][kChunk];
+  const char* base[NT];   // this lane's 16 bytes of step 0 of each tile
+  int s0, s1;
+
+  __device__ __forceinline__ void load(int sb, u32x4_t (&dst)[NT][kChunk]) const {
 #pragma unroll
-  for (int t = 0; t < NT; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  for (int sb = s0; sb < s1; sb += kBatch) {
-    u32x4_t w[NT][kBatch];
+    for (int j = 0; j < kChunk; ++j) {
+      const int sj = min(sb + j, s1 - 1);   // steps past the range repeat a valid address; never used
 #pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      if (sb + j < s1) {
+      for (int t = 0; t < NT; ++t) dst[t][j] = ld_stream(base[t] + (size_t)sj * 1024);
+    }
+  }
+
+  // tile[t]: packed tile of NT.  Split the K steps over the waves and put the
+  // first chunk's loads in flight.
+  __device__ __forceinline__ void begin(const void* const (&tile)[NT], int K) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int nsteps = K / KSTEP;
+    const int per = (nsteps + kGemvWaves - 1) / kGemvWaves;
+    s0 = min(nsteps, wave * per);
+    s1 = min(nsteps, s0 + per);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) base[t] = (const char*)tile[t] + lane * 16;
+    load(s0, w);   // unconditional: clamped addresses are valid even for an empty range
+  }
+
+  // One chunk: activations of steps [sb, sb+kChunk) are loaded, then the
+  // weights of the following chunk are put in flight (into wnext), then the
+  // activations are staged in MFMA fragment order and the MFMAs consume wcur.
+  // Scheduling barriers keep that order so that waiting for the activations
+  // never waits for the prefetched weights.  All MT row slots are staged (rows
+  // >= M repeat row 0 and only feed output rows that are discarded); steps
+  // past the range are staged as zeros (they add 0 x repeated weights).
+  __device__ __forceinline__ void chunk(int sb, const float* const (&xr)[MT], const float* gain, char* my,
+                                        const u32x4_t (&wcur)[NT][kChunk], u32x4_t (&wnext)[NT][kChunk],
+                                        f32x4_t (&acc)[NT]) const {
+    const int lane = threadIdx.x & 63;
+    const int mr = lane & 15, grp = lane >> 4;
+    const int q = WB ? lane : (lane & 31);       // float4 piece of the chunk this lane stages
+    const int mread = mr < MT ? mr : MT - 1;
+    const int nst = min(kChunk, s1 - sb);
+    const bool live = q < nst * P;
+    const int kq = sb * KSTEP + 4 * (live ? q : 0);
+    float4 xv[MT];
+    float4 gv = make_float4(1.f, 1.f, 1.f, 1.f);
+    if constexpr (GAIN) gv = ldg4(gain + kq);
+#pragma unroll
+    for (int m = 0; m < MT; ++m) xv[m] = ldg4(xr[m] + kq);
+    __builtin_amdgcn_sched_barrier(0);
+    load(sb + kChunk, wnext);
+    __builtin_amdgcn_sched_barrier(0);
+    const int j = q / P, e = (q % P) * 4;
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      float4 v = xv[m];
+      v.x = live ? v.x * gv.x : 0.f;
+      v.y = live ? v.y * gv.y : 0.f;
+      v.z = live ? v.z * gv.z : 0.f;
+      v.w = live ? v.w * gv.w : 0.f;
+      if constexpr (WB) {
+        uint16_t* hi = (uint16_t*)my;
+        uint16_t* lo = hi + kChunk * MT * 32;
+        const float xs[4] = {v.x, v.y, v.z, v.w};
+        uint32_t h[4], l[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          h[i] = f32_to_bf16_bits(xs[i]);
+          l[i] = f32_to_bf16_bits(xs[i] - __uint_as_float(h[i] << 16));
+        }
+        const int o = (j * MT + m) * 32 + e;
+        *(uint2*)(hi + o) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+        *(uint2*)(lo + o) = make_uint2(l[0] | (l[1] << 16), l[2] | (l[3] << 16));
+      } else {
+        *(float4*)((float*)my + (j * MT + m) * 16 + e) = v;
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int jj = 0; jj < kChunk; ++jj) {
+      if constexpr (WB) {
+        const uint16_t* hi = (const uint16_t*)my;
+        const uint16_t* lo = hi + kChunk * MT * 32;
+        const int o = (jj * MT + mread) * 32 + 8 * grp;
+        const bf16x8_t a_hi = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(hi + o));
+        const bf16x8_t a_lo = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(lo + o));
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-          if (wrow[t])
-            w[t][j] = ld_stream((const char*)wrow[t] + ((size_t)(sb + j) * KSTEP + EPL * grp) * ESZ);
-          else
-            w[t][j] = u32x4_t{0u, 0u, 0u, 0u};
+          const bf16x8_t bw = __builtin_bit_cast(bf16x8_t, wcur[t][jj]);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_hi, bw, acc[t], 0, 0, 0);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_lo, bw, acc[t], 0, 0, 0);
+        }
+      } else {
+        const float4 a = *(const float4*)((const float*)my + (jj * MT + mread) * 16 + 4 * grp);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, __uint_as_float(wcur[t][jj][0]), acc[t], 0, 0, 0);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, __uint_as_float(wcur[t][jj][1]), acc[t], 0, 0, 0);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, __uint_as_float(wcur[t][jj][2]), acc[t], 0, 0, 0);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, __uint_as_float(wcur[t][jj][3]), acc[t], 0, 0, 0);
         }
       }
     }
+    __builtin_amdgcn_wave_barrier();
+  }
+
+  // Run the wave's K range.  xrow: M activation row pointers (LDS array);
+  // lds: the workgroup's dynamic staging area (gemv_lds_bytes(WB, MT)).
+  __device__ __forceinline__ void run(const float* const* xrow, const float* gain, int M, char* lds,
+                                      f32x4_t (&acc)[NT]) {
+    const int wave = threadIdx.x >> 6;
+    char* my = lds + wave * (MT * kChunk * KSTEP * 4);
+    const float* xr[MT];
 #pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      if (sb + j < s1) {
-        const int k = (sb + j) * KSTEP;
+    for (int m = 0; m < MT; ++m) xr[m] = xrow[m < M ? m : 0];
 #pragma unroll
-        for (int t = 0; t < NT; ++t) mfma_step<WB>(w[t][j], xs.row, xs.gain, k, grp, acc[t]);
-      }
+    for (int t = 0; t < NT; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    u32x4_t w2[NT][kChunk];
+    for (int sb = s0; sb < s1; sb += 2 * kChunk) {
+      chunk(sb, xr, gain, my, w, w2, acc);
+      if (sb + kChunk >= s1) break;
+      chunk(sb + kChunk, xr, gain, my, w2, w, acc);
     }
   }
-}
+};
 
 // Sum the per-wave accumulators into y[t][m][n] (LDS, NT x 16 x 16 floats).
 // red: LDS scratch of kGemvWaves * NT * 256 floats.
@@ -249,6 +346,99 @@ __device__ __forceinline__ float ld_w(const void* p, size_t i, int wb) {
   return wb ? bf16_to_f32(((const uint16_t*)p)[i]) : ((const float*)p)[i];
 }
 
+// sum_{j<r} W[row][j] * u[j] for a [rows][r] matrix (adapter B factors);
+// 16-byte loads when the row is 16-byte aligned.
+__device__ __forceinline__ float dot_row(const void* W, size_t row, int r, const float* u, int wb) {
+  float v = 0.f;
+  const size_t b = row * r;
+  if (wb && (r & 7) == 0) {
+    const u32x4_t* p = (const u32x4_t*)((const uint16_t*)W + b);
+    for (int j = 0; j < r; j += 8) {
+      const u32x4_t w = p[j / 8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v += bf16lo(w[i]) * u[j + 2 * i] + bf16hi(w[i]) * u[j + 2 * i + 1];
+    }
+    return v;
+  }
+  if (!wb && (r & 3) == 0) {
+    const float4* p = (const float4*)((const float*)W + b);
+    for (int j = 0; j < r; j += 4) {
+      const float4 w = p[j / 4];
+      v += w.x * u[j] + w.y * u[j + 1] + w.z * u[j + 2] + w.w * u[j + 3];
+    }
+    return v;
+  }
+#pragma unroll 8
+  for (int j = 0; j < r; ++j) v += ld_w(W, b + j, wb) * u[j];
+  return v;
+}
+
+// out[o] = sum_{t<n} src[t*stride + o] for o < n_out with every thread of the
+// block; the summation order depends only on (n, n_out, blockDim).  src is
+// read with device-coherent loads (it was written by other workgroups of the
+// same kernel).  `scratch` holds blockDim.x floats.  Ends with a barrier.
+__device__ void column_sums(const float* src, int n, int stride, int n_out, float* out, float* scratch) {
+  const int T = blockDim.x;
+  if (n_out >= T / 2) {
+    for (int o = threadIdx.x; o < n_out; o += T) {
+      float a = 0.f;
+#pragma unroll 8
+      for (int t = 0; t < n; ++t) a += ld_agent(src + (size_t)t * stride + o);
+      out[o] = a;
+    }
+    __syncthreads();
+    return;
+  }
+  const int G = T / n_out;
+  const int o = threadIdx.x % n_out, g = threadIdx.x / n_out;
+  float a = 0.f;
+  if (g < G) {
+#pragma unroll 8
+    for (int t = g; t < n; t += G) a += ld_agent(src + (size_t)t * stride + o);
+  }
+  scratch[threadIdx.x] = a;
+  __syncthreads();
+  if (threadIdx.x < n_out) {
+    float b = 0.f;
+    for (int gg = 0; gg < G; ++gg) b += scratch[gg * n_out + threadIdx.x];
+    out[threadIdx.x] = b;
+  }
+  __syncthreads();
+}
+
+// ============================================================================
+// Kernel: pack up to three stacked row-major matrices [rows_g][K] into the
+// tile-packed layout (one-time, at context creation).
+// ============================================================================
+struct PackSrc {
+  const void* p[3];
+  int rows[3];
+};
+
+template <int WB>
+__global__ __launch_bounds__(256) void k_pack(PackSrc src, int total_rows, int K, void* dst) {
+  constexpr int KSTEP = WB ? 32 : 16, EPL = WB ? 8 : 4, ESZ = WB ? 2 : 4;
+  const int S = K / KSTEP;
+  const size_t n = (size_t)((total_rows + 15) / 16) * S * 64;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+    const int l = (int)(i & 63);
+    const size_t ts = i >> 6;
+    const int s = (int)(ts % S);
+    const size_t t = ts / S;
+    int r = (int)(t * 16) + (l & 15);
+    const int col = s * KSTEP + EPL * (l >> 4);
+    u32x4_t v = {0u, 0u, 0u, 0u};
+    for (int g = 0; g < 3; ++g) {
+      if (r < src.rows[g]) {
+        if (src.p[g]) v = *(const u32x4_t*)((const char*)src.p[g] + ((size_t)r * K + col) * ESZ);
+        break;
+      }
+      r -= src.rows[g];
+    }
+    *(u32x4_t*)((char*)dst + i * 16) = v;
+  }
+}
+
 // ============================================================================
 // Kernel: embedding gather + per-step control initialisation.
 // grid = M rows, block = 256.
@@ -266,9 +456,23 @@ __global__ __launch_bounds__(256) void k_embed(Dims D, const void* embed, RowMap
     ws.PIN[m * D.d + i] = v;
     ss += v * v;
   }
-  ss = block_sum(ss, red);
+  // zero this row's bins of every layer
+  const int PO = 1 + 2 * D.r;
+  for (int i = threadIdx.x; i < (D.n_layers + 1) * kBins * 4; i += 256) {
+    const int l = i / (kBins * 4), b = (i / 4) % kBins;
+    bin_d_at(ws, l, b, m)[i % 4] = 0.f;
+  }
+  for (int i = threadIdx.x; i < D.n_layers * kBins * PO; i += 256) {
+    const int l = i / (kBins * PO), b = (i / PO) % kBins;
+    bin_o_at(ws, D, l, b, m)[i % PO] = 0.f;
+  }
+  for (int i = threadIdx.x; i < D.n_layers * kBins * D.r; i += 256) {
+    const int l = i / (kBins * D.r), b = (i / D.r) % kBins;
+    bin_gu_at(ws, D, l, b, m)[i % D.r] = 0.f;
+  }
+  ss = block_sum(ss, red);   // contains a barrier: the zeroing above is done
   if (threadIdx.x == 0) {
-    float* pd = ws.part_d + m * 4;
+    float* pd = bin_d_at(ws, 0, 0, m);
     pd[0] = ss; pd[1] = ss; pd[2] = ss; pd[3] = 0.f;
   }
   if (init_ctl && m == 0) {
@@ -308,38 +512,40 @@ __device__ void gate_logic(const Dims& D, const RowMap& rm, const WS& ws, const 
 // decision of the preceding boundary.  grid = tiles of 16 rows over
 // [Wq; Wk; Wv; Aq; Ak; Av], block = 512.
 // ============================================================================
-template <int WB>
-__global__ __launch_bounds__(kGemvThreads) void k_qkv(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int layer,
-                                                      int n_part) {
+template <int WB, int MT>
+__global__ __launch_bounds__(kGemvThreads) void k_qkv(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int layer) {
   __shared__ float red[kGemvWaves * 256];
   __shared__ float y[256];
   __shared__ float ssum[kMaxRows * 4];
   __shared__ int reinit_s[kMaxSeq], exited_s[kMaxSeq], exitb_s[kMaxSeq];
   __shared__ float sig_s[kMaxSeq];
   __shared__ float inv_rms[kMaxRows];
-  __shared__ int src_s[kMaxRows];
+  __shared__ const float* xrow_s[kMaxRows];
+  extern __shared__ __attribute__((aligned(16))) char dyn[];
   const int nq = D.qdim;
   const int nqkv = 3 * nq + 3 * D.r;
   const int n0 = blockIdx.x * 16;
   // this lane's weight row
   const int lane = threadIdx.x & 63;
-  const int n = n0 + (lane & 15);
-  const void* wrow[1] = {nullptr};
+  const void* wrow[1];
   {
-    const size_t esz = WB ? 2 : 4;
-    if (n < 3 * nq) {
-      const void* base = n < nq ? L.wq : (n < 2 * nq ? L.wk : L.wv);
-      wrow[0] = (const char*)base + (size_t)(n % nq) * D.d * esz;
-    } else if (n < nqkv) {
-      const int a = (n - 3 * nq) / D.r, j = (n - 3 * nq) % D.r;
-      if (L.A[a]) wrow[0] = (const char*)L.A[a] + (size_t)j * D.d * esz;
+    const int tq = nq / 16, b = blockIdx.x;
+    const size_t tb = (size_t)16 * D.d * (WB ? 2 : 4);   // bytes of one packed tile
+    if (b < 3 * tq) {
+      const void* base = b < tq ? L.pq : (b < 2 * tq ? L.pk : L.pv);
+      wrow[0] = (const char*)base + (size_t)(b % tq) * tb;
+    } else {
+      wrow[0] = (const char*)L.pa + (size_t)(b - 3 * tq) * tb;
     }
   }
-  // partial sums of the previous kernel -> per-row statistics
-  for (int e = threadIdx.x; e < rm.M * 4; e += kGemvThreads) {
-    float s = 0.f;
-    for (int t = 0; t < n_part; ++t) s += ws.part_d[(t * kMaxRows) * 4 + e];
-    ssum[e] = s;
+  GemvWave<WB, 1, MT, true> gw;
+  gw.begin(wrow, D.d);
+  // row statistics: sum of the bins filled by the previous kernel
+  if (threadIdx.x < rm.M * 4) {
+    float a = 0.f;
+#pragma unroll
+    for (int b = 0; b < kBins; ++b) a += bin_d_at(ws, layer, b, threadIdx.x >> 2)[threadIdx.x & 3];
+    ssum[threadIdx.x] = a;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -348,7 +554,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_qkv(Dims D, LayerPtrs L, RowMa
       const int s = rm.seq[m];
       int src = m;
       if (rm.fast[m] && reinit_s[s]) src = rm.slow_of[m];
-      src_s[m] = src;
+      xrow_s[m] = ws.X + (size_t)src * D.d;
       inv_rms[m] = rsqrtf(ssum[src * 4] / D.d + D.eps);
     }
   }
@@ -365,11 +571,8 @@ __global__ __launch_bounds__(kGemvThreads) void k_qkv(Dims D, LayerPtrs L, RowMa
   for (int s = 0; s < rm.nseq; ++s) all_exited &= exited_s[s] != 0;
   if (all_exited && (n0 < nq || n0 >= 3 * nq)) return;
 
-  XSrc xs{nullptr, L.attn_norm};
-  const int mrow = lane & 15;
-  if (mrow < rm.M) xs.row = ws.X + (size_t)src_s[mrow] * D.d;
   f32x4_t acc[1];
-  gemv_wave<WB, 1>(wrow, xs, D.d, acc);
+  gw.run(xrow_s, L.attn_norm, rm.M, dyn, acc);
   gemv_reduce<1>(acc, rm.M, red, y);
   for (int e = threadIdx.x; e < rm.M * 16; e += kGemvThreads) {
     const int m = e >> 4, nn = n0 + (e & 15);
@@ -392,10 +595,7 @@ __device__ __forceinline__ float proj_elem(const Dims& D, const LayerPtrs& L, co
   const float* row = ws.QKV + (size_t)m * nqkv;
   const int c = h * D.hd + d;
   float v = row[which * D.qdim + c];
-  if (rm.fast[m] && L.B[which] && L.A[which]) {
-    const float* u = row + 3 * D.qdim + which * D.r;
-    for (int j = 0; j < D.r; ++j) v += ld_w(L.B[which], (size_t)c * D.r + j, D.wbf16) * u[j];
-  }
+  if (rm.fast[m] && L.B[which] && L.A[which]) v += dot_row(L.B[which], c, D.r, row + 3 * D.qdim + which * D.r, D.wbf16);
   return v;
 }
 
@@ -411,9 +611,13 @@ __device__ void head_vectors(const Dims& D, const LayerPtrs& L, const RowMap& rm
   if (which < 2) {
     for (int e = threadIdx.x; e < R * half; e += kAttnThreads) {
       const int i = e / half, j = e % half;
-      const double pos = (double)row_pos(rm, io, first + i);
-      const double ang = pos * pow((double)D.theta, -2.0 * j / hd);
-      const float c = (float)cos(ang), s = (float)sin(ang);
+      int pos = row_pos(rm, io, first + i);
+      if (pos < 0 || pos >= ws.rope_len) {
+        atomicOr(ws.err, 8);
+        pos = 0;
+      }
+      const float2 cs = ws.rope[(size_t)pos * half + j];   // cos, sin of pos * theta^(-2j/hd)
+      const float c = cs.x, s = cs.y;
       const float a = out[i * hd + j], b = out[i * hd + j + half];
       out[i * hd + j] = a * c - b * s;
       out[i * hd + j + half] = b * c + a * s;
@@ -462,6 +666,20 @@ constexpr size_t attn_smem_bytes() {
   return (size_t)(3 * kMaxRows * kMaxHeadDim + kScoreCap + 8 * kMaxHeadDim) * sizeof(float);
 }
 
+// Attention partial of one (sequence, head, split) and row: running max m,
+// sum of exponentials l, unnormalised accumulator acc[hd] and the o-adapter
+// down-projection of acc (fast rows), r floats.  Layout of ws.att:
+// [seq][H][splits+1][16 rows][2 + hd + r]; split index `splits` holds the
+// rows' own keys.
+__device__ __forceinline__ float* att_part(const WS& ws, const Dims& D, int s, int h, int sp, int n_split, int i) {
+  const int stride = 2 + D.hd + D.r;
+  return ws.att + ((((size_t)s * D.H + h) * (n_split + 1) + sp) * kMaxRows + i) * stride;
+}
+
+// Kernel: attention over the shared cache, one context split per workgroup,
+// plus one workgroup per (sequence, head) for the rows' own keys and the cache
+// writes.  grid = (splits + 1, H, nseq), block = 256.  The partials are merged
+// by k_attn_merge.
 template <int KB, int HD>
 __global__ __launch_bounds__(kAttnThreads) void k_attn(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, KVPtrs kv,
                                                        int layer, int n_split) {
@@ -476,197 +694,260 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn(Dims D, LayerPtrs L, RowM
   float* sc = vx + kMaxRows * kMaxHeadDim; // [R][per] scores, then probabilities
   float* redp = sc + kScoreCap;            // [4 waves][2 rows][hd]
   __shared__ float rowm[kMaxRows], rowl[kMaxRows];
-  __shared__ int last_flag;
+  __shared__ float uacc_s[kMaxRows * kMaxRank];
 
   const int ctx = io.positions[s] + rm.pos_offset;
   const bool frozen = ws.exited[s] != 0;
+  const bool own = split == n_split;
 
-  // cache writes of this layer: rows flagged `wr` (slow rows; the fast row when drafting)
-  if (split == 0) {
-    bool any = false;
-    for (int i = 0; i < R; ++i) any |= rm.wr[first + i] != 0;
-    if (any) {
-      head_vectors(D, L, rm, ws, io, first, R, 1, h, kx);
-      head_vectors(D, L, rm, ws, io, first, R, 2, h, vx);
-      for (int e = threadIdx.x; e < R * hd; e += kAttnThreads) {
-        const int i = e / hd, d = e % hd;
-        if (!rm.wr[first + i]) continue;
+  if (own) {
+    // ---- the rows' own keys and the cache writes -------------------------------
+    head_vectors(D, L, rm, ws, io, first, R, 1, h, kx);
+    head_vectors(D, L, rm, ws, io, first, R, 2, h, vx);
+    for (int e = threadIdx.x; e < R * hd; e += kAttnThreads) {
+      const int i = e / hd, d = e % hd;
+      if (!rm.wr[first + i]) continue;
+      bool ok;
+      const size_t ix = kv_index(kv, D, layer, s, ctx + rm.idx[first + i], h, d, ok);
+      if (!ok) { atomicOr(ws.err, 2); continue; }
+      if (KB) {
+        ((uint16_t*)kv.k)[ix] = (uint16_t)f32_to_bf16_bits(kx[e]);
+        ((uint16_t*)kv.v)[ix] = (uint16_t)f32_to_bf16_bits(vx[e]);
+      } else {
+        ((float*)kv.k)[ix] = kx[e];
+        ((float*)kv.v)[ix] = vx[e];
+      }
+    }
+    if (frozen) return;   // exited sequence: only its cache entries are produced
+    head_vectors(D, L, rm, ws, io, first, R, 0, h, q);
+    // a slow row sees the chunk's slow rows up to itself (as stored in the
+    // cache); a fast row sees only its own exact key/value
+    float* ownsc = sc;   // [R][R]
+    for (int e = threadIdx.x; e < R * R; e += kAttnThreads) {
+      const int i = e / R, jj = e % R;
+      const int mi = first + i, mj = first + jj;
+      bool vis;
+      if (rm.fast[mi]) vis = (jj == i);
+      else vis = !rm.fast[mj] && rm.idx[mj] <= rm.idx[mi];
+      float p = -INFINITY;
+      if (vis) {
+        p = 0.f;
+        const bool rnd = !rm.fast[mi];
+        for (int d = 0; d < hd; ++d) {
+          const float kk = rnd ? kv_round(kx[jj * hd + d], KB) : kx[jj * hd + d];
+          p += q[i * hd + d] * kk;
+        }
+        p *= scale;
+      }
+      ownsc[e] = p;
+    }
+    __syncthreads();
+    if (threadIdx.x < R) {
+      const int i = threadIdx.x;
+      float mx = -INFINITY;
+      for (int jj = 0; jj < R; ++jj) mx = fmaxf(mx, ownsc[i * R + jj]);
+      float l = 0.f;
+      for (int jj = 0; jj < R; ++jj) {
+        const float v = ownsc[i * R + jj] == -INFINITY ? 0.f : __expf(ownsc[i * R + jj] - mx);
+        ownsc[i * R + jj] = v;
+        l += v;
+      }
+      rowm[i] = mx;
+      rowl[i] = l;
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < R * hd; e += kAttnThreads) {
+      const int i = e / hd, d = e % hd;
+      const bool rnd = !rm.fast[first + i];
+      float a = 0.f;
+      for (int jj = 0; jj < R; ++jj) {
+        const float w = ownsc[i * R + jj];
+        if (w != 0.f) a += w * (rnd ? kv_round(vx[jj * hd + d], KB) : vx[jj * hd + d]);
+      }
+      q[e] = a;   // acc of the own-key partial
+    }
+    __syncthreads();
+  } else {
+    // ---- this split's share of the cached context [0, ctx) -------------------
+    if (frozen) return;
+    head_vectors(D, L, rm, ws, io, first, R, 0, h, q);
+    const int per = ((ctx + n_split - 1) / n_split + 15) & ~15;
+    if (per * R > kScoreCap) {             // the host sizes splits so that this cannot happen
+      if (threadIdx.x == 0) atomicOr(ws.err, 4);
+      return;
+    }
+    const int t0 = min(ctx, split * per), t1 = min(ctx, t0 + per);
+    const int nt = t1 - t0;
+    const int sub = threadIdx.x & 3, slot = threadIdx.x >> 2;
+    const int d0 = sub * DPL;
+#pragma unroll 4
+    for (int j = slot; j < nt; j += kAttnThreads / 4) {
+      bool ok;
+      const size_t base = kv_index(kv, D, layer, s, t0 + j, h, d0, ok);
+      float kk[DPL];
+      kv_row_load<KB, HD>(kv.k, base, ok, kk);
+      for (int i = 0; i < R; ++i) {
+        float p = 0.f;
+#pragma unroll
+        for (int c = 0; c < DPL; ++c) p += q[i * hd + d0 + c] * kk[c];
+        p += __shfl_xor(p, 1);
+        p += __shfl_xor(p, 2);
+        if (sub == 0) sc[i * per + j] = p * scale;
+      }
+    }
+    __syncthreads();
+    {
+      const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+      for (int i = w; i < R; i += 4) {
+        float mx = -INFINITY;
+        for (int j = lane; j < nt; j += 64) mx = fmaxf(mx, sc[i * per + j]);
+        mx = wave_max(mx);
+        float l = 0.f;
+        for (int j = lane; j < nt; j += 64) {
+          const float e = __expf(sc[i * per + j] - mx);
+          sc[i * per + j] = e;
+          l += e;
+        }
+        l = wave_sum(l);
+        if (lane == 0) { rowm[i] = nt > 0 ? mx : -INFINITY; rowl[i] = nt > 0 ? l : 0.f; }
+      }
+    }
+    __syncthreads();
+    const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    for (int i0 = 0; i0 < R; i0 += 2) {
+      const bool two = i0 + 1 < R;
+      float acc0[DPL], acc1[DPL];
+#pragma unroll
+      for (int c = 0; c < DPL; ++c) { acc0[c] = 0.f; acc1[c] = 0.f; }
+#pragma unroll 4
+      for (int j = slot; j < nt; j += kAttnThreads / 4) {
         bool ok;
-        const size_t ix = kv_index(kv, D, layer, s, ctx + rm.idx[first + i], h, d, ok);
-        if (!ok) { atomicOr(ws.err, 2); continue; }
-        if (KB) {
-          ((uint16_t*)kv.k)[ix] = (uint16_t)f32_to_bf16_bits(kx[e]);
-          ((uint16_t*)kv.v)[ix] = (uint16_t)f32_to_bf16_bits(vx[e]);
-        } else {
-          ((float*)kv.k)[ix] = kx[e];
-          ((float*)kv.v)[ix] = vx[e];
+        const size_t base = kv_index(kv, D, layer, s, t0 + j, h, d0, ok);
+        float vv[DPL];
+        kv_row_load<KB, HD>(kv.v, base, ok, vv);
+        const float p0 = sc[i0 * per + j];
+        const float p1 = two ? sc[(i0 + 1) * per + j] : 0.f;
+#pragma unroll
+        for (int c = 0; c < DPL; ++c) { acc0[c] += p0 * vv[c]; acc1[c] += p1 * vv[c]; }
+      }
+#pragma unroll
+      for (int c = 0; c < DPL; ++c) {
+        float a = acc0[c], b = acc1[c];
+        a += __shfl_xor(a, 4); b += __shfl_xor(b, 4);
+        a += __shfl_xor(a, 8); b += __shfl_xor(b, 8);
+        a += __shfl_xor(a, 16); b += __shfl_xor(b, 16);
+        a += __shfl_xor(a, 32); b += __shfl_xor(b, 32);
+        acc0[c] = a; acc1[c] = b;
+      }
+      if (lane < 4) {
+#pragma unroll
+        for (int c = 0; c < DPL; ++c) {
+          redp[(wv * 2 + 0) * hd + d0 + c] = acc0[c];
+          redp[(wv * 2 + 1) * hd + d0 + c] = acc1[c];
+        }
+      }
+      __syncthreads();
+      for (int e = threadIdx.x; e < 2 * hd; e += kAttnThreads) {
+        const int a = e / hd, d = e % hd;
+        if (i0 + a < R) {
+          float v = 0.f;
+          for (int w = 0; w < 4; ++w) v += redp[(w * 2 + a) * hd + d];
+          q[(i0 + a) * hd + d] = v;   // q is no longer needed: reuse it for acc
         }
       }
       __syncthreads();
     }
   }
-  if (frozen) return;   // exited sequence: only its cache entries are produced
-
-  head_vectors(D, L, rm, ws, io, first, R, 0, h, q);
-
-  // ---- this split's share of the cached context [0, ctx) -------------------
-  const int per = ((ctx + n_split - 1) / n_split + 15) & ~15;
-  if (per * R > kScoreCap) {             // the host sizes splits so that this cannot happen
-    if (threadIdx.x == 0) atomicOr(ws.err, 4);
-    return;
-  }
-  const int t0 = min(ctx, split * per), t1 = min(ctx, t0 + per);
-  const int nt = t1 - t0;
-  const int sub = threadIdx.x & 3, slot = threadIdx.x >> 2;
-  const int d0 = sub * DPL;
-  for (int j = slot; j < nt; j += kAttnThreads / 4) {
-    bool ok;
-    const size_t base = kv_index(kv, D, layer, s, t0 + j, h, d0, ok);
-    float kk[DPL];
-    kv_row_load<KB, HD>(kv.k, base, ok, kk);
-    for (int i = 0; i < R; ++i) {
-      float p = 0.f;
-#pragma unroll
-      for (int c = 0; c < DPL; ++c) p += q[i * hd + d0 + c] * kk[c];
-      p += __shfl_xor(p, 1);
-      p += __shfl_xor(p, 2);
-      if (sub == 0) sc[i * per + j] = p * scale;
-    }
-  }
-  __syncthreads();
+  // ---- store the partial: m, l, acc, and A_o[:, head cols] . acc (fast rows) ----
   {
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    for (int i = w; i < R; i += 4) {
-      float mx = -INFINITY;
-      for (int j = lane; j < nt; j += 64) mx = fmaxf(mx, sc[i * per + j]);
-      mx = wave_max(mx);
-      float l = 0.f;
-      for (int j = lane; j < nt; j += 64) {
-        const float e = __expf(sc[i * per + j] - mx);
-        sc[i * per + j] = e;
-        l += e;
+    // A_o[j][h*hd + d] . acc_i[d]: 8 dims per thread, then a sum over hd/8 threads
+    constexpr int PCS = HD / 8;
+    float* up = redp;   // [R*r][PCS] partials (R*r*PCS <= 16*32*16 would overflow: rows done in groups)
+    for (int i0 = 0; i0 < R; ++i0) {
+      if (!rm.fast[first + i0] || !L.A[3]) {
+        for (int j = threadIdx.x; j < D.r; j += kAttnThreads) uacc_s[i0 * D.r + j] = 0.f;
+        continue;
       }
-      l = wave_sum(l);
-      if (lane == 0) { rowm[i] = mx; rowl[i] = l; }
+      for (int e = threadIdx.x; e < D.r * PCS; e += kAttnThreads) {
+        const int j = e / PCS, pc = e % PCS;
+        const size_t base = (size_t)j * D.qdim + h * hd + pc * 8;
+        float u = 0.f;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) u += ld_w(L.A[3], base + t, D.wbf16) * q[i0 * hd + pc * 8 + t];
+        up[e] = u;
+      }
+      __syncthreads();
+      for (int j = threadIdx.x; j < D.r; j += kAttnThreads) {
+        float u = 0.f;
+        for (int pc = 0; pc < PCS; ++pc) u += up[j * PCS + pc];
+        uacc_s[i0 * D.r + j] = u;
+      }
+      __syncthreads();
     }
   }
   __syncthreads();
-  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  float* attp = ws.att + ((((size_t)s * D.H + h) * n_split + split) * kMaxRows) * (hd + 2);
-  for (int i0 = 0; i0 < R; i0 += 2) {
-    const bool two = i0 + 1 < R;
-    float acc0[DPL], acc1[DPL];
-#pragma unroll
-    for (int c = 0; c < DPL; ++c) { acc0[c] = 0.f; acc1[c] = 0.f; }
-    for (int j = slot; j < nt; j += kAttnThreads / 4) {
-      bool ok;
-      const size_t base = kv_index(kv, D, layer, s, t0 + j, h, d0, ok);
-      float vv[DPL];
-      kv_row_load<KB, HD>(kv.v, base, ok, vv);
-      const float p0 = sc[i0 * per + j];
-      const float p1 = two ? sc[(i0 + 1) * per + j] : 0.f;
-#pragma unroll
-      for (int c = 0; c < DPL; ++c) { acc0[c] += p0 * vv[c]; acc1[c] += p1 * vv[c]; }
+  for (int i = 0; i < R; ++i) {
+    float* pp = att_part(ws, D, s, h, split, n_split, i);
+    for (int e = threadIdx.x; e < 2 + hd + D.r; e += kAttnThreads) {
+      float v;
+      if (e == 0) v = rowm[i];
+      else if (e == 1) v = rowl[i];
+      else if (e < 2 + hd) v = q[i * hd + e - 2];
+      else v = uacc_s[i * D.r + e - 2 - hd];
+      pp[e] = v;
     }
-#pragma unroll
-    for (int c = 0; c < DPL; ++c) {
-      float a = acc0[c], b = acc1[c];
-      a += __shfl_xor(a, 4); b += __shfl_xor(b, 4);
-      a += __shfl_xor(a, 8); b += __shfl_xor(b, 8);
-      a += __shfl_xor(a, 16); b += __shfl_xor(b, 16);
-      a += __shfl_xor(a, 32); b += __shfl_xor(b, 32);
-      acc0[c] = a; acc1[c] = b;
-    }
-    if (lane < 4) {
-#pragma unroll
-      for (int c = 0; c < DPL; ++c) {
-        redp[(wv * 2 + 0) * hd + d0 + c] = acc0[c];
-        redp[(wv * 2 + 1) * hd + d0 + c] = acc1[c];
-      }
-    }
-    __syncthreads();
-    for (int e = threadIdx.x; e < 2 * hd; e += kAttnThreads) {
-      const int a = e / hd, d = e % hd;
-      if (i0 + a < R) {
-        float v = 0.f;
-        for (int w = 0; w < 4; ++w) v += redp[(w * 2 + a) * hd + d];
-        attp[(size_t)(i0 + a) * (hd + 2) + 2 + d] = v;
-      }
-    }
-    __syncthreads();
   }
-  for (int i = threadIdx.x; i < R; i += kAttnThreads) {
-    attp[(size_t)i * (hd + 2)] = nt > 0 ? rowm[i] : -INFINITY;
-    attp[(size_t)i * (hd + 2) + 1] = nt > 0 ? rowl[i] : 0.f;
-  }
+}
 
-  // ---- the last split of this (sequence, head) merges ------------------------
-  if (!arrive_last(ws.att_cnt + s * D.H + h, n_split, &last_flag)) return;
-
-  head_vectors(D, L, rm, ws, io, first, R, 1, h, kx);
-  head_vectors(D, L, rm, ws, io, first, R, 2, h, vx);
-  // the rows' own keys: a slow row sees the chunk's slow rows up to itself (as
-  // stored in the cache); a fast row sees only its own exact key/value.
-  float* ownsc = sc;   // [R][R]
-  for (int e = threadIdx.x; e < R * R; e += kAttnThreads) {
-    const int i = e / R, jj = e % R;
-    const int mi = first + i, mj = first + jj;
-    bool vis;
-    if (rm.fast[mi]) vis = (jj == i);
-    else vis = !rm.fast[mj] && rm.idx[mj] <= rm.idx[mi];
-    float p = -INFINITY;
-    if (vis) {
-      p = 0.f;
-      const bool rnd = !rm.fast[mi];
-      for (int d = 0; d < hd; ++d) {
-        const float kk = rnd ? kv_round(kx[jj * hd + d], KB) : kx[jj * hd + d];
-        p += q[i * hd + d] * kk;
-      }
-      p *= scale;
-    }
-    ownsc[e] = p;
+// Kernel: merge the attention partials of one (sequence, head): the output o
+// of every row and, for fast rows, the o-adapter down-projection of that head.
+// grid = (H, nseq), block = 256.
+__global__ __launch_bounds__(kAttnThreads) void k_attn_merge(Dims D, RowMap rm, WS ws, int n_split) {
+  __shared__ float stat[kMaxRows * 64 * 2];   // m, l of every split (n_split + 1 <= 64)
+  __shared__ float wgt[kMaxRows * 64];
+  __shared__ float linv[kMaxRows];
+  const int h = blockIdx.x, s = blockIdx.y;
+  if (ws.exited[s]) return;
+  const int R = rm.cnt[s], first = rm.first[s];
+  const int S1 = n_split + 1;
+  for (int e = threadIdx.x; e < R * S1; e += kAttnThreads) {
+    const int i = e / S1, sp = e % S1;
+    const float* pp = att_part(ws, D, s, h, sp, n_split, i);
+    stat[(i * 64 + sp) * 2] = pp[0];
+    stat[(i * 64 + sp) * 2 + 1] = pp[1];
   }
   __syncthreads();
-  const float* att0 = ws.att + (((size_t)s * D.H + h) * n_split) * kMaxRows * (hd + 2);
-  for (int e = threadIdx.x; e < R * hd; e += kAttnThreads) {
-    const int i = e / hd, d = e % hd;
-    const int mi = first + i;
+  if (threadIdx.x < R) {
+    const int i = threadIdx.x;
     float M = -INFINITY;
-    for (int sp = 0; sp < n_split; ++sp) {
-      const float* pp = att0 + ((size_t)sp * kMaxRows + i) * (hd + 2);
-      if (pp[1] > 0.f) M = fmaxf(M, pp[0]);
+    for (int sp = 0; sp < S1; ++sp)
+      if (stat[(i * 64 + sp) * 2 + 1] > 0.f) M = fmaxf(M, stat[(i * 64 + sp) * 2]);
+    float Lsum = 0.f;
+    for (int sp = 0; sp < S1; ++sp) {
+      const float l = stat[(i * 64 + sp) * 2 + 1];
+      const float w = l > 0.f ? __expf(stat[(i * 64 + sp) * 2] - M) : 0.f;
+      wgt[i * 64 + sp] = w;
+      Lsum += w * l;
     }
-    for (int jj = 0; jj < R; ++jj) M = fmaxf(M, ownsc[i * R + jj]);
-    float Lsum = 0.f, o = 0.f;
-    for (int sp = 0; sp < n_split; ++sp) {
-      const float* pp = att0 + ((size_t)sp * kMaxRows + i) * (hd + 2);
-      if (pp[1] > 0.f) {
-        const float w = __expf(pp[0] - M);
-        Lsum += w * pp[1];
-        o += w * pp[2 + d];
-      }
-    }
-    const bool rnd = !rm.fast[mi];
-    for (int jj = 0; jj < R; ++jj) {
-      const float sj = ownsc[i * R + jj];
-      if (sj == -INFINITY) continue;
-      const float w = __expf(sj - M);
-      Lsum += w;
-      o += w * (rnd ? kv_round(vx[jj * hd + d], KB) : vx[jj * hd + d]);
-    }
-    o /= Lsum;
-    ws.O[(size_t)mi * D.qdim + h * hd + d] = o;
-    q[e] = o;   // keep for the o adapter-down
+    linv[i] = 1.f / Lsum;
   }
   __syncthreads();
-  // adapter-down of the o projection for fast rows: u_o[h] = A_o[:, head cols] . o_h
-  for (int e = threadIdx.x; e < R * D.r; e += kAttnThreads) {
-    const int i = e / D.r, j = e % D.r;
+  const int W = D.hd + D.r;
+  for (int e = threadIdx.x; e < R * W; e += kAttnThreads) {
+    const int i = e / W, c = e % W;
+    float v = 0.f;
+    for (int sp0 = 0; sp0 < S1; sp0 += 8) {
+      float part[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) part[u] = att_part(ws, D, s, h, min(sp0 + u, S1 - 1), n_split, i)[2 + c];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (sp0 + u < S1) v += wgt[i * 64 + sp0 + u] * part[u];
+    }
+    v *= linv[i];
     const int mi = first + i;
-    float u = 0.f;
-    if (rm.fast[mi] && L.A[3])
-      for (int d = 0; d < hd; ++d) u += ld_w(L.A[3], (size_t)j * D.qdim + h * hd + d, D.wbf16) * q[i * hd + d];
-    ws.uo[((size_t)mi * D.H + h) * D.r + j] = u;
+    if (c < D.hd) ws.O[(size_t)mi * D.qdim + h * D.hd + c] = v;
+    else ws.uo[((size_t)mi * D.H + h) * D.r + (c - D.hd)] = rm.fast[mi] ? v : 0.f;
   }
 }
 
@@ -674,30 +955,36 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn(Dims D, LayerPtrs L, RowM
 // Kernel: output projection + residual add (+ adapter on the fast row).
 // grid = d/16 tiles, block = 512.
 // ============================================================================
-template <int WB>
+template <int WB, int MT>
 __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int layer) {
   __shared__ float red[kGemvWaves * 256];
   __shared__ float y[256];
   __shared__ float uo_s[kMaxRows * kMaxRank];
   __shared__ float newx[256];
+  __shared__ const float* xrow_s[kMaxRows];
+  extern __shared__ __attribute__((aligned(16))) char dyn[];
   const int n0 = blockIdx.x * 16;
   const int lane = threadIdx.x & 63;
   const size_t esz = WB ? 2 : 4;
-  bool all_exited = true;
-  for (int s = 0; s < rm.nseq; ++s) all_exited &= ws.exited[s] != 0;
-  if (all_exited) return;
-  const void* wrow[1] = {(const char*)L.wo + (size_t)(n0 + (lane & 15)) * D.qdim * esz};
-  XSrc xs{nullptr, nullptr};
-  if ((lane & 15) < rm.M) xs.row = ws.O + (size_t)(lane & 15) * D.qdim;
+  if (io.mode == EX_EXIT) {
+    bool all_exited = true;
+    for (int s = 0; s < rm.nseq; ++s) all_exited &= ws.exited[s] != 0;
+    if (all_exited) return;
+  }
+  const void* wrow[1] = {(const char*)L.po + (size_t)blockIdx.x * 16 * D.qdim * esz};
+  GemvWave<WB, 1, MT, false> gw;
+  gw.begin(wrow, D.qdim);
+  if (threadIdx.x < rm.M) xrow_s[threadIdx.x] = ws.O + (size_t)threadIdx.x * D.qdim;
+  __syncthreads();
   f32x4_t acc[1];
-  gemv_wave<WB, 1>(wrow, xs, D.qdim, acc);
-  // adapter-down of o, summed over heads
-  for (int e = threadIdx.x; e < rm.M * D.r; e += kGemvThreads) {
-    const int m = e / D.r, j = e % D.r;
-    float u = 0.f;
-    if (rm.fast[m] && L.A[3])
-      for (int hh = 0; hh < D.H; ++hh) u += ws.uo[((size_t)m * D.H + hh) * D.r + j];
-    uo_s[e] = u;
+  gw.run(xrow_s, nullptr, rm.M, dyn, acc);
+  // adapter-down of o, summed over heads (uo is [16][H][r]: column sums over H
+  // with stride r per head, one column per (row, j))
+  if (L.A[3]) {
+    for (int e = threadIdx.x; e < rm.M * D.r; e += kGemvThreads) uo_s[e] = 0.f;
+    __syncthreads();
+    for (int m = 0; m < rm.M; ++m)
+      if (rm.fast[m]) column_sums(ws.uo + (size_t)m * D.H * D.r, D.H, D.r, D.r, uo_s + m * D.r, red);
   }
   gemv_reduce<1>(acc, rm.M, red, y);
   // epilogue: thread e -> (m, n) ; read everything first, write after a barrier
@@ -717,7 +1004,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
         pin = ri ? ws.X[(size_t)rm.slow_of[m] * D.d + nn] : xo;
         float ad = 0.f;
         if (L.B[3] && L.A[3])
-          for (int j = 0; j < D.r; ++j) ad += ld_w(L.B[3], (size_t)nn * D.r + j, D.wbf16) * uo_s[m * D.r + j];
+          ad = dot_row(L.B[3], nn, D.r, uo_s + m * D.r, D.wbf16);
         xnew = pin + y[e] + ad;
       } else {
         xnew = xo + y[e];
@@ -735,7 +1022,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
   // partial sums for the gate/up prologue: sum x^2 and the adapter-down of
   // gate and up (fast rows): sum_n A[j][n] g_mlp[n] x[n]
   const int PO = 1 + 2 * D.r;
-  float* po = ws.part_o + ((size_t)blockIdx.x * kMaxRows) * PO;
+  const int bin = blockIdx.x % kBins;
   for (int q = threadIdx.x; q < rm.M * PO; q += kGemvThreads) {
     const int mm = q / PO, c = q % PO;
     float v = 0.f;
@@ -748,7 +1035,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
         for (int i = 0; i < 16; ++i)
           v += ld_w(A, (size_t)j * D.d + n0 + i, D.wbf16) * L.mlp_norm[n0 + i] * newx[mm * 16 + i];
     }
-    po[(size_t)mm * PO + c] = v;
+    if (c == 0 || rm.fast[mm]) add_agent(bin_o_at(ws, D, layer, bin, mm) + c, v);
   }
 }
 
@@ -756,32 +1043,37 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
 // Kernel: gate/up projections (paired tiles), adapter-up, SwiGLU.
 // grid = F/16 tiles, block = 512.
 // ============================================================================
-template <int WB>
-__global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io,
-                                                         int n_part) {
+template <int WB, int MT>
+__global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int layer) {
   __shared__ float red[kGemvWaves * 512];
   __shared__ float y[512];
   __shared__ float stat[kMaxRows * (1 + 2 * kMaxRank)];
   __shared__ float inv_rms[kMaxRows];
   __shared__ float act[256];
+  __shared__ const float* xrow_s[kMaxRows];
+  extern __shared__ __attribute__((aligned(16))) char dyn[];
   const int n0 = blockIdx.x * 16;
   const int lane = threadIdx.x & 63;
   const size_t esz = WB ? 2 : 4;
-  bool all_exited = true;
-  for (int s = 0; s < rm.nseq; ++s) all_exited &= ws.exited[s] != 0;
-  if (all_exited) return;
-  const int n = n0 + (lane & 15);
-  const void* wrow[2] = {(const char*)L.wg + (size_t)n * D.d * esz, (const char*)L.wu + (size_t)n * D.d * esz};
-  XSrc xs{nullptr, L.mlp_norm};
-  if ((lane & 15) < rm.M) xs.row = ws.X + (size_t)(lane & 15) * D.d;
+  if (io.mode == EX_EXIT) {
+    bool all_exited = true;
+    for (int s = 0; s < rm.nseq; ++s) all_exited &= ws.exited[s] != 0;
+    if (all_exited) return;
+  }
+  const void* wrow[2] = {(const char*)L.pg + (size_t)blockIdx.x * 16 * D.d * esz,
+                         (const char*)L.pu + (size_t)blockIdx.x * 16 * D.d * esz};
+  GemvWave<WB, 2, MT, true> gw;
+  gw.begin(wrow, D.d);
+  if (threadIdx.x < rm.M) xrow_s[threadIdx.x] = ws.X + (size_t)threadIdx.x * D.d;
+  __syncthreads();
   f32x4_t acc[2];
-  gemv_wave<WB, 2>(wrow, xs, D.d, acc);
+  gw.run(xrow_s, L.mlp_norm, rm.M, dyn, acc);
   const int PO = 1 + 2 * D.r;
   for (int q = threadIdx.x; q < rm.M * PO; q += kGemvThreads) {
-    const int mm = q / PO, c = q % PO;
-    float v = 0.f;
-    for (int t = 0; t < n_part; ++t) v += ws.part_o[((size_t)t * kMaxRows + mm) * PO + c];
-    stat[q] = v;
+    float a = 0.f;
+#pragma unroll
+    for (int b = 0; b < kBins; ++b) a += bin_o_at(ws, D, layer, b, q / PO)[q % PO];
+    stat[q] = a;
   }
   __syncthreads();
   if (threadIdx.x < rm.M) inv_rms[threadIdx.x] = rsqrtf(stat[threadIdx.x * PO] / D.d + D.eps);
@@ -792,11 +1084,8 @@ __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, Ro
     const float ir = inv_rms[m];
     float g = y[e] * ir, u = y[256 + e] * ir;
     if (rm.fast[m]) {
-      if (L.B[4] && L.A[4])
-        for (int j = 0; j < D.r; ++j) g += ld_w(L.B[4], (size_t)nn * D.r + j, D.wbf16) * stat[m * PO + 1 + j] * ir;
-      if (L.B[5] && L.A[5])
-        for (int j = 0; j < D.r; ++j)
-          u += ld_w(L.B[5], (size_t)nn * D.r + j, D.wbf16) * stat[m * PO + 1 + D.r + j] * ir;
+      if (L.B[4] && L.A[4]) g += dot_row(L.B[4], nn, D.r, stat + m * PO + 1, D.wbf16) * ir;
+      if (L.B[5] && L.A[5]) u += dot_row(L.B[5], nn, D.r, stat + m * PO + 1 + D.r, D.wbf16) * ir;
     }
     const float a = silu(g) * u;
     ws.ACT[(size_t)m * D.F + nn] = a;
@@ -804,13 +1093,13 @@ __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, Ro
   }
   __syncthreads();
   // partials of the down adapter-down: sum_n A_d[j][n] a[n]
-  float* pg = ws.part_gu + ((size_t)blockIdx.x * kMaxRows) * D.r;
+  const int bin = blockIdx.x % kBins;
   for (int q = threadIdx.x; q < rm.M * D.r; q += kGemvThreads) {
     const int mm = q / D.r, j = q % D.r;
     float v = 0.f;
     if (rm.fast[mm] && L.A[6])
       for (int i = 0; i < 16; ++i) v += ld_w(L.A[6], (size_t)j * D.F + n0 + i, D.wbf16) * act[mm * 16 + i];
-    pg[(size_t)mm * D.r + j] = v;
+    if (rm.fast[mm] && L.A[6]) add_agent(bin_gu_at(ws, D, layer, bin, mm) + j, v);
   }
 }
 
@@ -818,31 +1107,37 @@ __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, Ro
 // Kernel: down projection + residual add (+ adapter), partial sums for the
 // next layer's norm and the exit signal.  grid = d/16 tiles, block = 512.
 // ============================================================================
-template <int WB>
-__global__ __launch_bounds__(kGemvThreads) void k_down(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int n_part) {
+template <int WB, int MT>
+__global__ __launch_bounds__(kGemvThreads) void k_down(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int layer) {
   __shared__ float red[kGemvWaves * 256];
   __shared__ float y[256];
   __shared__ float ud[kMaxRows * kMaxRank];
   __shared__ float newx[256], pin_s[256];
+  __shared__ const float* xrow_s[kMaxRows];
+  extern __shared__ __attribute__((aligned(16))) char dyn[];
   const int n0 = blockIdx.x * 16;
   const int lane = threadIdx.x & 63;
   const size_t esz = WB ? 2 : 4;
-  bool all_exited = true;
-  for (int s = 0; s < rm.nseq; ++s) all_exited &= ws.exited[s] != 0;
+  bool all_exited = false;
+  if (io.mode == EX_EXIT) {
+    all_exited = true;
+    for (int s = 0; s < rm.nseq; ++s) all_exited &= ws.exited[s] != 0;
+  }
   const int e = threadIdx.x;
   if (!all_exited) {
-    const void* wrow[1] = {(const char*)L.wd + (size_t)(n0 + (lane & 15)) * D.F * esz};
-    XSrc xs{nullptr, nullptr};
-    if ((lane & 15) < rm.M) xs.row = ws.ACT + (size_t)(lane & 15) * D.F;
-    f32x4_t acc[1];
-    gemv_wave<WB, 1>(wrow, xs, D.F, acc);
+    const void* wrow[1] = {(const char*)L.pd + (size_t)blockIdx.x * 16 * D.F * esz};
+    GemvWave<WB, 1, MT, false> gw;
+    gw.begin(wrow, D.F);
+    if (threadIdx.x < rm.M) xrow_s[threadIdx.x] = ws.ACT + (size_t)threadIdx.x * D.F;
     for (int q = threadIdx.x; q < rm.M * D.r; q += kGemvThreads) {
-      const int m = q / D.r, j = q % D.r;
-      float u = 0.f;
-      if (rm.fast[m] && L.A[6])
-        for (int t = 0; t < n_part; ++t) u += ws.part_gu[((size_t)t * kMaxRows + m) * D.r + j];
-      ud[q] = u;
+      float a = 0.f;
+#pragma unroll
+      for (int b = 0; b < kBins; ++b) a += bin_gu_at(ws, D, layer, b, q / D.r)[q % D.r];
+      ud[q] = a;
     }
+    __syncthreads();
+    f32x4_t acc[1];
+    gw.run(xrow_s, nullptr, rm.M, dyn, acc);
     gemv_reduce<1>(acc, rm.M, red, y);
   }
   if (e < rm.M * 16) {
@@ -852,15 +1147,14 @@ __global__ __launch_bounds__(kGemvThreads) void k_down(Dims D, LayerPtrs L, RowM
     float x = ws.X[(size_t)m * D.d + nn];
     if (!ex) {
       x += y[e];
-      if (rm.fast[m] && L.B[6] && L.A[6])
-        for (int j = 0; j < D.r; ++j) x += ld_w(L.B[6], (size_t)nn * D.r + j, D.wbf16) * ud[m * D.r + j];
+      if (rm.fast[m] && L.B[6] && L.A[6]) x += dot_row(L.B[6], nn, D.r, ud + m * D.r, D.wbf16);
       ws.X[(size_t)m * D.d + nn] = x;
     }
     newx[e] = x;
     pin_s[e] = rm.fast[m] ? ws.PIN[(size_t)m * D.d + nn] : 0.f;
   }
   __syncthreads();
-  float* pd = ws.part_d + ((size_t)blockIdx.x * kMaxRows) * 4;
+  const int bin = blockIdx.x % kBins;
   for (int q = threadIdx.x; q < rm.M * 4; q += kGemvThreads) {
     const int mm = q >> 2, c = q & 3;
     float v = 0.f;
@@ -868,7 +1162,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_down(Dims D, LayerPtrs L, RowM
       const float x = newx[mm * 16 + i], p = pin_s[mm * 16 + i];
       v += c == 0 ? x * x : (c == 1 ? p * x : (c == 2 ? p * p : 0.f));
     }
-    pd[q] = v;
+    if (c < 3) add_agent(bin_d_at(ws, layer + 1, bin, mm) + c, v);
   }
 }
 
@@ -877,9 +1171,9 @@ __global__ __launch_bounds__(kGemvThreads) void k_down(Dims D, LayerPtrs L, RowM
 // (tokens, exit bookkeeping, acceptance of a verified chunk).
 // grid = V/16 tiles, block = 512.
 // ============================================================================
-template <int WB>
+template <int WB, int MT>
 __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_head, const float* final_norm, RowMap rm,
-                                                       WS ws, StepIO io, KVPtrs kv, int n_part, int n_tiles) {
+                                                       WS ws, StepIO io, KVPtrs kv, int n_tiles, int n_layers_run) {
   __shared__ float red[kGemvWaves * 256];
   __shared__ float y[256];
   __shared__ float ssum[kMaxRows * 4];
@@ -887,15 +1181,19 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
   __shared__ int nh_s;
   __shared__ float inv_rms[kMaxRows];
   __shared__ int last_flag;
+  __shared__ const float* xrow_s[kMaxRows];
+  extern __shared__ __attribute__((aligned(16))) char dyn[];
   const int n0 = blockIdx.x * 16;
   const int lane = threadIdx.x & 63;
   const size_t esz = WB ? 2 : 4;
-  const int nrow = min(n0 + (lane & 15), D.V - 1);
-  const void* wrow[1] = {(const char*)lm_head + (size_t)nrow * D.d * esz};
+  const void* wrow[1] = {(const char*)lm_head + (size_t)blockIdx.x * 16 * D.d * esz};
+  GemvWave<WB, 1, MT, true> gw;
+  gw.begin(wrow, D.d);
   for (int q = threadIdx.x; q < rm.M * 4; q += kGemvThreads) {
-    float v = 0.f;
-    for (int t = 0; t < n_part; ++t) v += ws.part_d[((size_t)t * kMaxRows) * 4 + q];
-    ssum[q] = v;
+    float a = 0.f;
+#pragma unroll
+    for (int b = 0; b < kBins; ++b) a += bin_d_at(ws, n_layers_run, b, q >> 2)[q & 3];
+    ssum[q] = a;
   }
   if (threadIdx.x == 0) {
     // rows fed to the head
@@ -913,12 +1211,14 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
     nh_s = nh;
   }
   __syncthreads();
-  if (threadIdx.x < nh_s) inv_rms[threadIdx.x] = rsqrtf(ssum[hrow[threadIdx.x] * 4] / D.d + D.eps);
+  if (threadIdx.x < nh_s) {
+    inv_rms[threadIdx.x] = rsqrtf(ssum[hrow[threadIdx.x] * 4] / D.d + D.eps);
+    xrow_s[threadIdx.x] = ws.X + (size_t)hrow[threadIdx.x] * D.d;
+  }
+  __syncthreads();
   const int nh = nh_s;
-  XSrc xs{nullptr, final_norm};
-  if ((lane & 15) < nh) xs.row = ws.X + (size_t)hrow[lane & 15] * D.d;
   f32x4_t acc[1];
-  gemv_wave<WB, 1>(wrow, xs, D.d, acc);
+  gw.run(xrow_s, final_norm, nh, dyn, acc);
   gemv_reduce<1>(acc, nh, red, y);
   // logits and per-tile argmax (lowest index on ties)
   const int e = threadIdx.x;
@@ -936,8 +1236,8 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
       if (z2 > z || (z2 == z && i2 < idx)) { z = z2; idx = i2; }
     }
     if ((e & 15) == 0) {
-      ws.lm_val[(size_t)blockIdx.x * kMaxRows + k] = z;
-      ws.lm_idx[(size_t)blockIdx.x * kMaxRows + k] = idx;
+      st_agent(&ws.lm_val[(size_t)blockIdx.x * kMaxRows + k], z);
+      st_agent(&ws.lm_idx[(size_t)blockIdx.x * kMaxRows + k], idx);
     }
   }
   if (!arrive_last(ws.lm_cnt, n_tiles, &last_flag)) return;
@@ -949,8 +1249,8 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
     float bz = -INFINITY;
     int bi = 0x7fffffff;
     for (int t = lane; t < n_tiles; t += 64) {
-      const float z = ws.lm_val[(size_t)t * kMaxRows + k];
-      const int i = ws.lm_idx[(size_t)t * kMaxRows + k];
+      const float z = ld_agent(&ws.lm_val[(size_t)t * kMaxRows + k]);
+      const int i = ld_agent(&ws.lm_idx[(size_t)t * kMaxRows + k]);
       if (z > bz || (z == bz && i < bi)) { bz = z; bi = i; }
     }
 #pragma unroll
