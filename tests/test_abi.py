@@ -34,7 +34,10 @@ def test_library_exports_every_declared_symbol():
 def test_workspace_size_and_validation():
     cfg = synth.CONFIGS["phi3"]
     n = binding.workspace_size(cfg, 1, 16, 1536)
-    assert 0 < n < 1 << 30
+    # the workspace holds the tile-packed projection matrices (bf16) plus scratch
+    d, q, F, V, L = cfg.d_model, cfg.qdim, cfg.ffn, cfg.vocab, cfg.n_layers
+    packed = 2 * (L * (3 * q * d + 16 * d + d * q + 3 * F * d) + V * d)
+    assert packed < n < packed + (64 << 20)
     assert binding.workspace_size(cfg, 8, 16, 4352) >= n
     with pytest.raises(binding.M2R2Error) as e:
         binding.workspace_size(cfg.replace(head_dim=80), 1, 16, 1024)
