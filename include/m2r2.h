@@ -13,7 +13,10 @@
  * Sec. 2.1), and at exit gates the fast row is either re-initialised from the
  * slow row (Fig. 3 caption) or, in exit mode, emits the token (Eq. 4).
  * On top of the step: self-speculative drafting from the fast stream and
- * parallel verification on the slow stream (Sec. 2.3.2).
+ * parallel verification on the slow stream (Sec. 2.3.2), and, for
+ * mixture-of-experts models (Sec. 2.3.3), expert prediction from the fast
+ * stream driving ahead-of-time copies of expert weights from pinned host
+ * memory into a per-layer HBM expert cache.
  *
  * Conventions (all entry points):
  *  - Memory: the caller owns every buffer.  Pointers named *_d are device
@@ -38,7 +41,10 @@
  *    bit is set instead).
  *  - Streams: every call that takes a hipStream_t only enqueues work on it
  *    (no host synchronisation), so a sequence of calls can be captured into a
- *    HIP graph.  One context must not be used on two streams at once.
+ *    HIP graph -- except the decode step of a mixture-of-experts model, which
+ *    waits, layer by layer, for the router's choice before it can place the
+ *    expert copies (see m2r2_decode_step).  One context must not be used on
+ *    two streams at once.
  *  - Errors: no exception or abort crosses the ABI.  Arguments are checked
  *    before anything is enqueued; on failure the call returns a negative
  *    m2r2_status and m2r2_last_error() (thread-local) describes it.  A launch
@@ -87,6 +93,12 @@ typedef struct {
   int32_t kvdtype;          /* m2r2_dtype of the KV pages */
   float rms_eps;            /* RMSNorm epsilon */
   float rope_theta;         /* rotate-half RoPE base */
+  /* Mixture of experts (Sec. 2.3.3); n_experts = 0 for a dense model.  Every
+   * layer then has n_experts SwiGLU experts of width expert_ffn, top_k of
+   * which are chosen per token, and the HBM cache holds expert_slots experts
+   * per layer (top_k <= expert_slots <= n_experts; = n_experts keeps every
+   * expert resident). */
+  int32_t n_experts, top_k, expert_ffn, expert_slots;
 } m2r2_config;
 
 /* Per-layer device pointers.  Any adapter pointer may be NULL (adapter
@@ -104,6 +116,12 @@ typedef struct {
   /* accelerator adapters, index 0..6 = q, k, v, o, gate, up, down */
   const void* A[7];
   const void* B[7];
+  /* mixture-of-experts layers: wg, wu, wd and A/B[4..6] are NULL; the router
+   * and the fast row's MLP, which is the rank-r adapter alone (Sec. 2.3.3):
+   * MLP_fast(x) = (m A_m^T) B_m^T with m = rms(x) * mlp_norm */
+  const void* router;       /* [n_experts][d] */
+  const void* A_m;          /* [rank][d], may be NULL with B_m (fast MLP absent) */
+  const void* B_m;          /* [d][rank] */
 } m2r2_layer_weights;
 
 typedef struct {
@@ -111,6 +129,11 @@ typedef struct {
   const float* final_norm;           /* [d] */
   const void* lm_head;               /* [vocab][d] */
   const m2r2_layer_weights* layers;  /* host array of n_layers entries, copied by m2r2_create */
+  /* mixture of experts: pinned host memory (hipHostMalloc) holding every
+   * expert of every layer, expert e of layer l at byte offset
+   * (l * n_experts + e) * m2r2_expert_bytes(), each filled by
+   * m2r2_pack_expert.  Borrowed for the lifetime of the context. */
+  const void* experts_h;
 } m2r2_weights;
 
 typedef struct {
@@ -136,20 +159,31 @@ typedef struct {
   float* h_out_d;           /* [batch][d] optional: slow row fed to the head (gate state on exit) */
   float* p_out_d;           /* [batch][d] optional: fast row at the end of the step */
   int32_t advance;          /* nonzero: positions_d[b] += 1 at the end of the step */
+  /* mixture of experts, optional: [batch][n_layers][top_k] experts chosen by
+   * the slow row's router (descending probability, lowest id on ties; -1 for
+   * layers not run after an exit), and experts predicted for layer l from the
+   * fast row after layer (l-2)/2 (Sec. 2.3.3; -1 where no prediction) */
+  int32_t* slow_experts_d;
+  int32_t* pred_experts_d;
 } m2r2_step_out;
 
 typedef struct m2r2_ctx m2r2_ctx;
 
 /* Workspace bytes a context needs (packed weights plus scratch) for up to
  * max_batch sequences, chunks of up to max_chunk rows (verification/prefill)
- * and max_ctx cache positions per sequence.  max_batch <= 8, max_chunk <= 16. */
+ * and max_ctx cache positions per sequence.  max_batch <= 8, max_chunk <= 16.
+ * For a mixture-of-experts model it includes the HBM expert cache,
+ * n_layers * expert_slots * m2r2_expert_bytes() bytes, and the packed routers;
+ * such a model takes max_batch = 1. */
 M2R2_API m2r2_status m2r2_workspace_size(const m2r2_config* cfg, int32_t max_batch, int32_t max_chunk,
                                          int32_t max_ctx, size_t* bytes_out);
 
 /* Create a context.  `workspace` is device memory of at least the size above,
  * 256-byte aligned, owned by the caller and used exclusively by this context;
  * it is initialised here, including packing the projection matrices
- * (synchronously, on the null stream).  Weight pointers must be 16-byte
+ * (synchronously, on the null stream) and, for a mixture-of-experts model,
+ * the warm start of the expert cache (experts 0..expert_slots-1 of every
+ * layer copied from the host store).  Weight pointers must be 16-byte
  * aligned.  Requirements:
  * d_model, H*head_dim and ffn multiples of 32 (bf16) or 16 (f32); head_dim
  * even and <= 128; rank <= 32. */
@@ -164,7 +198,21 @@ M2R2_API void m2r2_destroy(m2r2_ctx* ctx);
  * positions.  The slow row's key/value at t are written to the cache and
  * seq_lens_d[b] is set to t+1.  `dual` = 0 runs the slow row alone (plain
  * decoding on the same kernels; exit settings are then ignored).
- * tokens_d may alias out->next_token_d. */
+ * tokens_d may alias out->next_token_d.
+ *
+ * Mixture-of-experts models (batch 1): in every layer the slow row's router
+ * picks top_k experts (softmax over all experts, unrenormalised weights) and
+ * the fast row, whose MLP is its adapter alone, predicts the experts of
+ * layers 2i+2 and 2i+3 from its state after layer i, each with that layer's
+ * norm gain and router (Sec. 2.3.3).  The call then waits until the routing
+ * of the layer is known on the host, makes every chosen expert resident in
+ * that layer's HBM cache (a miss is copied from the host store on the
+ * library's on-demand copy stream), makes `stream` wait for any copy still in
+ * flight, and runs the experts from their cache slots.  Under the
+ * M2R2_MOE_AHEAD_OF_TIME policy the predicted experts are then copied on the
+ * library's prefetch stream.  Cache replacement is least-recently-used, with
+ * the experts needed now and those predicted for the layer protected from
+ * eviction.  The call returns once the last layer's experts are enqueued. */
 M2R2_API m2r2_status m2r2_decode_step(m2r2_ctx* ctx, int32_t batch, int32_t dual, const int32_t* tokens_d,
                                       int32_t* positions_d, const m2r2_kv* kv, const m2r2_exit* ex,
                                       const m2r2_step_out* out, hipStream_t stream);
@@ -175,7 +223,8 @@ M2R2_API m2r2_status m2r2_decode_step(m2r2_ctx* ctx, int32_t batch, int32_t dual
  * draft consumes last_token_d[0] at position positions_d[0] = t; draft j is at
  * position t+j.  The fast row's key/value at those positions are written to
  * cache positions t..t+gamma-1 of layers < exit_layer, where later drafts read
- * them; m2r2_verify overwrites them.  Writes drafts_d[0..gamma). */
+ * them; m2r2_verify overwrites them.  Writes drafts_d[0..gamma).  Dense
+ * models only (M2R2_E_UNSUPPORTED for a mixture-of-experts model). */
 M2R2_API m2r2_status m2r2_draft(m2r2_ctx* ctx, const int32_t* last_token_d, const int32_t* positions_d,
                                 int32_t exit_layer, int32_t gamma, const m2r2_kv* kv, int32_t* drafts_d,
                                 hipStream_t stream);
@@ -188,14 +237,75 @@ M2R2_API m2r2_status m2r2_draft(m2r2_ctx* ctx, const int32_t* last_token_d, cons
  * d_1..d_j == targets_d[0..j); seq_lens_d[0] = t + j + 1; if
  * bonus_token_d is not NULL it receives targets_d[j]; positions_d[0] is
  * advanced by j + 1.  If n_accepted_d is NULL (prefill) every row is kept:
- * seq_lens_d[0] = t + n and positions_d[0] is advanced by n.  1 <= n <= max_chunk. */
+ * seq_lens_d[0] = t + n and positions_d[0] is advanced by n.  1 <= n <= max_chunk.
+ * Dense models only: a mixture-of-experts model is prefilled with slow-only
+ * decode steps (dual = 0). */
 M2R2_API m2r2_status m2r2_verify(m2r2_ctx* ctx, const int32_t* chunk_d, int32_t n, int32_t* positions_d,
                                  const m2r2_kv* kv, int32_t* targets_d, int32_t* n_accepted_d,
                                  int32_t* bonus_token_d, hipStream_t stream);
 
+/* ---- mixture of experts (Sec. 2.3.3) ----------------------------------- */
+
+typedef enum {
+  M2R2_MOE_ON_DEMAND = 0,      /* least-recently-used cache, misses loaded when routed */
+  M2R2_MOE_AHEAD_OF_TIME = 1   /* as above, plus copies of the fast stream's predictions */
+} m2r2_moe_policy;
+
+typedef struct {
+  int64_t hits, misses;             /* chosen experts resident (or in flight) / not, when routed */
+  int64_t prefetch_issued, prefetch_used, prefetch_wasted;   /* wasted: evicted before any use */
+  int64_t loads;                    /* host-to-device expert copies */
+  int64_t pred_correct, pred_total; /* |P ∩ S| and |P| over predicted layers (ahead-of-time policy) */
+  int64_t h2d_bytes;                /* bytes copied host to device */
+  int64_t copy_waits;               /* times the compute stream was made to wait for a copy */
+  int64_t host_wait_ns;             /* host time spent waiting for routing results */
+  int64_t layer_misses[128];        /* misses per layer */
+} m2r2_moe_counters;
+
+/* Bytes of one packed expert: gate [F_e][d], up [F_e][d] and down [d][F_e],
+ * each in the tile-packed layout the expert kernels read.  Requires
+ * expert_ffn a multiple of 32 (bf16) or 16 (f32). */
+M2R2_API m2r2_status m2r2_expert_bytes(const m2r2_config* cfg, size_t* bytes_out);
+
+/* Host-only: pack one expert's row-major gate, up ([F_e][d]) and down
+ * ([d][F_e]) matrices, in the weight dtype, into dst_h (m2r2_expert_bytes
+ * bytes of host memory).  No device work. */
+M2R2_API m2r2_status m2r2_pack_expert(const m2r2_config* cfg, const void* wg_h, const void* wu_h, const void* wd_h,
+                                      void* dst_h);
+
+/* Select the cache policy for later decode steps (default: ahead of time). */
+M2R2_API m2r2_status m2r2_moe_set_policy(m2r2_ctx* ctx, int32_t policy);
+
+/* Make experts ids_h[0..n) of `layer` resident or in flight (Sec. 2.3.3,
+ * Appendix B): a resident expert is marked as just used; a missing one
+ * replaces the least recently used expert not in ids_h and is copied from the
+ * host store on copy_stream (priority != 0: on the library's on-demand copy
+ * stream; NULL copy_stream: the library's prefetch stream).  Later decode
+ * steps wait for the copy before they use the slot.  Counts as prefetches. */
+M2R2_API m2r2_status m2r2_prefetch_experts(m2r2_ctx* ctx, int32_t layer, const int32_t* ids_h, int32_t n,
+                                           int32_t priority, hipStream_t copy_stream);
+
+/* Restore the warm start -- experts 0..slots-1 of every layer resident, expert
+ * 0 least recently used -- and zero the statistics.  Synchronous. */
+M2R2_API m2r2_status m2r2_moe_reset(m2r2_ctx* ctx);
+
+/* Counters since the last reset. */
+M2R2_API m2r2_status m2r2_moe_stats(m2r2_ctx* ctx, m2r2_moe_counters* out);
+
+/* Host-only replay of the cache policy on a routing trace, with no copies:
+ * slow_h[t][l][top_k] experts chosen at token t, layer l; pred_h (may be
+ * NULL) the same shape, predictions (-1 where none).  With prefetch != 0 the
+ * predictions for layers 2i+2, 2i+3 are applied after layer i as the
+ * ahead-of-time policy does.  Fills the counters of `out` (h2d_bytes,
+ * copy_waits and host_wait_ns are 0). */
+M2R2_API m2r2_status m2r2_expert_cache_replay(int32_t n_layers, int32_t n_experts, int32_t top_k, int32_t slots,
+                                              int32_t n_tokens, const int32_t* slow_h, const int32_t* pred_h,
+                                              int32_t prefetch, m2r2_moe_counters* out);
+
 /* Kernel timing for measurement.  Kernel classes of one decode pass:
  * 0 qkv, 1 attention, 2 output projection, 3 gate/up, 4 down, 5 LM head,
- * 6 embedding, 7 attention merge.  m2r2_timing_enable(ctx, k) starts a new record: every
+ * 6 embedding, 7 attention merge, 8 expert gate/up, 9 expert down, 10
+ * router and top-k.  m2r2_timing_enable(ctx, k) starts a new record: every
  * launch of class k made by later calls is bracketed by a pair of HIP events
  * recorded on the call's stream (up to 1024 launches; record with direct
  * launches: events recorded inside a captured graph cannot be timed).

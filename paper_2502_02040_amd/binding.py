@@ -22,25 +22,31 @@ MODES = {"off": EXIT_OFF, "observe": EXIT_OBSERVE, "exit": EXIT_EXIT}
 PROJ = ("q", "k", "v", "o", "g", "u", "d")
 
 EXPORTS = ("m2r2_workspace_size", "m2r2_create", "m2r2_destroy", "m2r2_decode_step", "m2r2_draft", "m2r2_verify",
-           "m2r2_timing_enable", "m2r2_timing_read", "m2r2_device_errors", "m2r2_last_error")
-KERNEL_CLASSES = {"qkv": 0, "attn": 1, "oproj": 2, "gateup": 3, "down": 4, "head": 5, "embed": 6, "attn_merge": 7}
+           "m2r2_timing_enable", "m2r2_timing_read", "m2r2_device_errors", "m2r2_last_error",
+           "m2r2_expert_bytes", "m2r2_pack_expert", "m2r2_moe_set_policy", "m2r2_prefetch_experts",
+           "m2r2_moe_reset", "m2r2_moe_stats", "m2r2_expert_cache_replay")
+KERNEL_CLASSES = {"qkv": 0, "attn": 1, "oproj": 2, "gateup": 3, "down": 4, "head": 5, "embed": 6, "attn_merge": 7,
+                  "expert_gateup": 8, "expert_down": 9, "router": 10}
+MOE_ON_DEMAND, MOE_AHEAD_OF_TIME = 0, 1
+POLICIES = {"on_demand": MOE_ON_DEMAND, "ahead_of_time": MOE_AHEAD_OF_TIME}
 
 
 class Config(ctypes.Structure):
     _fields_ = [("n_layers", c_int32), ("d_model", c_int32), ("n_heads", c_int32), ("head_dim", c_int32),
                 ("ffn", c_int32), ("vocab", c_int32), ("rank", c_int32), ("wdtype", c_int32), ("kvdtype", c_int32),
-                ("rms_eps", c_float), ("rope_theta", c_float)]
+                ("rms_eps", c_float), ("rope_theta", c_float), ("n_experts", c_int32), ("top_k", c_int32),
+                ("expert_ffn", c_int32), ("expert_slots", c_int32)]
 
 
 class LayerWeights(ctypes.Structure):
     _fields_ = [("attn_norm", c_void_p), ("wq", c_void_p), ("wk", c_void_p), ("wv", c_void_p), ("wo", c_void_p),
                 ("mlp_norm", c_void_p), ("wg", c_void_p), ("wu", c_void_p), ("wd", c_void_p),
-                ("A", c_void_p * 7), ("B", c_void_p * 7)]
+                ("A", c_void_p * 7), ("B", c_void_p * 7), ("router", c_void_p), ("A_m", c_void_p), ("B_m", c_void_p)]
 
 
 class Weights(ctypes.Structure):
     _fields_ = [("embed", c_void_p), ("final_norm", c_void_p), ("lm_head", c_void_p),
-                ("layers", POINTER(LayerWeights))]
+                ("layers", POINTER(LayerWeights)), ("experts_h", c_void_p)]
 
 
 class KV(ctypes.Structure):
@@ -54,7 +60,22 @@ class Exit(ctypes.Structure):
 
 class StepOut(ctypes.Structure):
     _fields_ = [("next_token_d", c_void_p), ("exit_boundary_d", c_void_p), ("signal_d", c_void_p),
-                ("logits_d", c_void_p), ("h_out_d", c_void_p), ("p_out_d", c_void_p), ("advance", c_int32)]
+                ("logits_d", c_void_p), ("h_out_d", c_void_p), ("p_out_d", c_void_p), ("advance", c_int32),
+                ("slow_experts_d", c_void_p), ("pred_experts_d", c_void_p)]
+
+
+_I64 = ctypes.c_int64
+COUNTER_FIELDS = ("hits", "misses", "prefetch_issued", "prefetch_used", "prefetch_wasted", "loads", "pred_correct",
+                  "pred_total", "h2d_bytes", "copy_waits", "host_wait_ns")
+
+
+class MoeCounters(ctypes.Structure):
+    _fields_ = [(f, _I64) for f in COUNTER_FIELDS] + [("layer_misses", _I64 * 128)]
+
+    def as_dict(self, n_layers: int) -> dict:
+        d = {f: int(getattr(self, f)) for f in COUNTER_FIELDS}
+        d["layer_misses"] = [int(self.layer_misses[i]) for i in range(n_layers)]
+        return d
 
 
 _lib = None
@@ -81,8 +102,18 @@ def lib() -> ctypes.CDLL:
         L.m2r2_timing_read.argtypes = [c_void_p, POINTER(ctypes.c_double), POINTER(c_int32)]
         L.m2r2_device_errors.argtypes = [c_void_p, c_void_p, POINTER(c_int32)]
         L.m2r2_last_error.restype = ctypes.c_char_p
+        L.m2r2_expert_bytes.argtypes = [POINTER(Config), POINTER(c_size_t)]
+        L.m2r2_pack_expert.argtypes = [POINTER(Config), c_void_p, c_void_p, c_void_p, c_void_p]
+        L.m2r2_moe_set_policy.argtypes = [c_void_p, c_int32]
+        L.m2r2_prefetch_experts.argtypes = [c_void_p, c_int32, POINTER(c_int32), c_int32, c_int32, c_void_p]
+        L.m2r2_moe_reset.argtypes = [c_void_p]
+        L.m2r2_moe_stats.argtypes = [c_void_p, POINTER(MoeCounters)]
+        L.m2r2_expert_cache_replay.argtypes = [c_int32, c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,
+                                               c_int32, POINTER(MoeCounters)]
         for f in ("m2r2_workspace_size", "m2r2_create", "m2r2_decode_step", "m2r2_draft", "m2r2_verify",
-                  "m2r2_timing_enable", "m2r2_timing_read", "m2r2_device_errors"):
+                  "m2r2_timing_enable", "m2r2_timing_read", "m2r2_device_errors", "m2r2_expert_bytes",
+                  "m2r2_pack_expert", "m2r2_moe_set_policy", "m2r2_prefetch_experts", "m2r2_moe_reset",
+                  "m2r2_moe_stats", "m2r2_expert_cache_replay"):
             getattr(L, f).restype = c_int32
         _lib = L
     return _lib
@@ -110,17 +141,68 @@ def _stream(stream) -> int:
     return s.cuda_stream
 
 
-def make_config(cfg) -> Config:
+def make_config(cfg, expert_slots: Optional[int] = None) -> Config:
+    slots = cfg.n_experts if expert_slots is None else expert_slots
     return Config(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.ffn, cfg.vocab, cfg.rank,
                   BF16 if cfg.wdtype == "bf16" else F32, BF16 if cfg.kvdtype == "bf16" else F32,
-                  cfg.rms_eps, cfg.rope_theta)
+                  cfg.rms_eps, cfg.rope_theta, cfg.n_experts, cfg.top_k, cfg.expert_ffn, slots)
 
 
-def workspace_size(cfg, max_batch: int, max_chunk: int, max_ctx: int) -> int:
+def workspace_size(cfg, max_batch: int, max_chunk: int, max_ctx: int, expert_slots: Optional[int] = None) -> int:
     n = c_size_t(0)
-    _check(lib().m2r2_workspace_size(ctypes.byref(make_config(cfg)), max_batch, max_chunk, max_ctx, ctypes.byref(n)),
-           "m2r2_workspace_size")
+    _check(lib().m2r2_workspace_size(ctypes.byref(make_config(cfg, expert_slots)), max_batch, max_chunk, max_ctx,
+                                     ctypes.byref(n)), "m2r2_workspace_size")
     return n.value
+
+
+def expert_bytes(cfg) -> int:
+    n = c_size_t(0)
+    _check(lib().m2r2_expert_bytes(ctypes.byref(make_config(cfg)), ctypes.byref(n)), "m2r2_expert_bytes")
+    return n.value
+
+
+def _host_matrix(a: np.ndarray, wdtype: str) -> np.ndarray:
+    """A weight matrix in its storage dtype (bf16 bit patterns or float32)."""
+    if wdtype == "bf16":
+        u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+        return ((u + (((u >> 16) & 1) + np.uint32(0x7FFF))) >> 16).astype(np.uint16)
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def pack_expert_store(cfg, expert_source, *, threads: int = 8):
+    """Pinned host tensor holding every expert of every layer in the packed
+    layout of the C library; ``expert_source(l, e)`` returns the row-major
+    (gate, up, down) matrices of expert e of layer l."""
+    import torch
+    from concurrent.futures import ThreadPoolExecutor
+    eb = expert_bytes(cfg)
+    store = torch.empty(cfg.n_layers * cfg.n_experts * eb, dtype=torch.uint8, pin_memory=True)
+    base = store.data_ptr()
+    c = make_config(cfg)
+
+    def one(le):
+        l, e = le
+        g, u, d = (_host_matrix(x, cfg.wdtype) for x in expert_source(l, e))
+        _check(lib().m2r2_pack_expert(ctypes.byref(c), g.ctypes.data, u.ctypes.data, d.ctypes.data,
+                                      base + (l * cfg.n_experts + e) * eb), "m2r2_pack_expert")
+
+    jobs = [(l, e) for l in range(cfg.n_layers) for e in range(cfg.n_experts)]
+    with ThreadPoolExecutor(threads) as ex:
+        list(ex.map(one, jobs))
+    return store
+
+
+def cache_replay(n_layers: int, n_experts: int, top_k: int, slots: int, slow: np.ndarray,
+                 pred: Optional[np.ndarray] = None, prefetch: bool = True) -> dict:
+    """Host-only replay of the library's expert-cache policy on a trace
+    ``slow[t][l][k]`` (and predictions of the same shape, -1 where none)."""
+    slow = np.ascontiguousarray(slow, dtype=np.int32)
+    pr = None if pred is None else np.ascontiguousarray(pred, dtype=np.int32)
+    out = MoeCounters()
+    _check(lib().m2r2_expert_cache_replay(n_layers, n_experts, top_k, slots, slow.shape[0], slow.ctypes.data,
+                                          None if pr is None else pr.ctypes.data, 1 if prefetch else 0,
+                                          ctypes.byref(out)), "m2r2_expert_cache_replay")
+    return out.as_dict(n_layers)
 
 
 class PagedKV:
@@ -179,9 +261,14 @@ class Model:
     """Weights resident in HBM plus a context of the C library."""
 
     def __init__(self, cfg, weights: Dict[str, np.ndarray], *, max_batch: int = 1, max_chunk: int = 16,
-                 max_ctx: int = 2048, device: str = "cuda"):
+                 max_ctx: int = 2048, device: str = "cuda", expert_slots: Optional[int] = None,
+                 expert_store=None, expert_source=None):
+        """For a mixture-of-experts ``cfg`` the experts live in pinned host
+        memory: ``expert_store`` (from pack_expert_store), else one is packed
+        from ``expert_source(l, e)`` or, by default, from ``weights``."""
         import torch
         self.cfg = cfg
+        self.expert_slots = cfg.n_experts if expert_slots is None else expert_slots
         self.device = device
         self.max_batch, self.max_chunk, self.max_ctx = max_batch, max_chunk, max_ctx
         wdt = torch.bfloat16 if cfg.wdtype == "bf16" else torch.float32
@@ -208,19 +295,35 @@ class Model:
             L.attn_norm = up(p + "attn_norm", torch.float32)
             L.mlp_norm = up(p + "mlp_norm", torch.float32)
             L.wq, L.wk, L.wv, L.wo = up_t(p + "wq"), up_t(p + "wk"), up_t(p + "wv"), up_t(p + "wo")
-            L.wg, L.wu, L.wd = up_t(p + "wg"), up_t(p + "wu"), up_t(p + "wd")
+            if cfg.is_moe:
+                L.router = up_t(p + "router")
+                if p + "A_m" in weights:
+                    L.A_m, L.B_m = up(p + "A_m"), up(p + "B_m")
+            else:
+                L.wg, L.wu, L.wd = up_t(p + "wg"), up_t(p + "wu"), up_t(p + "wd")
             for i, pr in enumerate(PROJ):
+                if cfg.is_moe and i >= 4:
+                    break
                 if p + f"A_{pr}" in weights:
                     L.A[i] = up_t(p + f"A_{pr}") if i < 3 else up(p + f"A_{pr}")
                     L.B[i] = up(p + f"B_{pr}")
-        self._w = Weights(up("embed"), up("final_norm", torch.float32), up_t("lm_head"), self._layers)
-        self.ws_bytes = workspace_size(cfg, max_batch, max_chunk, max_ctx)
+        self.expert_store = None
+        self.expert_bytes = expert_bytes(cfg) if cfg.is_moe else 0
+        if cfg.is_moe:
+            if expert_store is None:
+                src = expert_source or (lambda l, e: (weights[f"L{l}.E{e}.wg"], weights[f"L{l}.E{e}.wu"],
+                                                      weights[f"L{l}.E{e}.wd"]))
+                expert_store = pack_expert_store(cfg, src)
+            self.expert_store = expert_store
+        self._w = Weights(up("embed"), up("final_norm", torch.float32), up_t("lm_head"), self._layers,
+                          None if self.expert_store is None else self.expert_store.data_ptr())
+        self.ws_bytes = workspace_size(cfg, max_batch, max_chunk, max_ctx, self.expert_slots)
         self.workspace = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=device)
         base = self.workspace.data_ptr()
         ws_ptr = (base + 255) & ~255
         self._ctx = c_void_p()
-        _check(lib().m2r2_create(ctypes.byref(make_config(cfg)), ctypes.byref(self._w), max_batch, max_chunk, max_ctx,
-                                 ws_ptr, self.ws_bytes, ctypes.byref(self._ctx)), "m2r2_create")
+        _check(lib().m2r2_create(ctypes.byref(make_config(cfg, self.expert_slots)), ctypes.byref(self._w), max_batch,
+                                 max_chunk, max_ctx, ws_ptr, self.ws_bytes, ctypes.byref(self._ctx)), "m2r2_create")
         torch.cuda.synchronize()
         self._transient = []   # packed copies live in the workspace
 
@@ -235,11 +338,12 @@ class Model:
     # -- calls ------------------------------------------------------------------
     def decode_step(self, tokens, positions, kv: KV, *, dual: bool = True, gates: Sequence[int] = (),
                     tau: float = 2.0, mode: str = "observe", next_token=None, exit_boundary=None, signal=None,
-                    logits=None, h_out=None, p_out=None, advance: bool = False, stream=None) -> None:
+                    logits=None, h_out=None, p_out=None, advance: bool = False, slow_experts=None,
+                    pred_experts=None, stream=None) -> None:
         g = (c_int32 * max(1, len(gates)))(*gates)
         ex = Exit(ctypes.cast(g, POINTER(c_int32)), len(gates), tau, MODES[mode])
         out = StepOut(_ptr(next_token), _ptr(exit_boundary), _ptr(signal), _ptr(logits), _ptr(h_out), _ptr(p_out),
-                      1 if advance else 0)
+                      1 if advance else 0, _ptr(slow_experts), _ptr(pred_experts))
         B = tokens.numel()
         _check(lib().m2r2_decode_step(self._ctx, B, 1 if dual else 0, tokens.data_ptr(), positions.data_ptr(),
                                       ctypes.byref(kv), ctypes.byref(ex), ctypes.byref(out), _stream(stream)),
@@ -262,6 +366,24 @@ class Model:
         ms, n = ctypes.c_double(0.0), c_int32(0)
         _check(lib().m2r2_timing_read(self._ctx, ctypes.byref(ms), ctypes.byref(n)), "m2r2_timing_read")
         return ms.value, n.value
+
+    # -- mixture of experts --------------------------------------------------------
+    def moe_set_policy(self, policy: str) -> None:
+        _check(lib().m2r2_moe_set_policy(self._ctx, POLICIES[policy]), "m2r2_moe_set_policy")
+
+    def prefetch_experts(self, layer: int, ids: Sequence[int], *, priority: bool = False, stream=None) -> None:
+        a = (c_int32 * max(1, len(ids)))(*[int(i) for i in ids])
+        _check(lib().m2r2_prefetch_experts(self._ctx, layer, ctypes.cast(a, POINTER(c_int32)), len(ids),
+                                           1 if priority else 0, None if stream is None else stream.cuda_stream),
+               "m2r2_prefetch_experts")
+
+    def moe_reset(self) -> None:
+        _check(lib().m2r2_moe_reset(self._ctx), "m2r2_moe_reset")
+
+    def moe_stats(self) -> dict:
+        out = MoeCounters()
+        _check(lib().m2r2_moe_stats(self._ctx, ctypes.byref(out)), "m2r2_moe_stats")
+        return out.as_dict(self.cfg.n_layers)
 
     def device_errors(self, stream=None) -> int:
         bits = c_int32(0)

@@ -1,0 +1,272 @@
+// Mixture-of-experts kernels of the M2R2 decode step (Sec. 2.3.3): the
+// slow row is routed (softmax over all experts, top-k, unrenormalised
+// weights) and runs its k experts out of the HBM expert cache; the fast row's
+// MLP is a rank-r adapter; after layer i the fast row predicts the experts of
+// layers 2i+2 and 2i+3 with those layers' routers.
+#pragma once
+#include "step_kernels.h"
+
+namespace m2r2 {
+
+constexpr int kMaxExperts = 256;
+constexpr int kMaxTopK = 16;
+
+struct MoePtrs {
+  const float* logits;    // [3][E]: router logits of the slow row, predictions for 2i+2, 2i+3
+  int* sel;               // [3][kMaxTopK] chosen / predicted experts
+  float* prob;            // [kMaxTopK] router probabilities of the chosen experts
+  int* sel_host;          // mapped host memory: [3][kMaxTopK] + sequence word
+  float* act;             // [kMaxTopK][F_e] prob * silu(g) * u of each chosen expert
+};
+
+// Kernel: router logits.  rows [0, E) of `router` applied to the slow row
+// (gain g_mlp, rms from the bins of the o projection) -> out[0..E).  Also used
+// for the predictions: `row` selects the residual row, `gain` the target
+// layer's mlp norm, `stat_layer` the bins holding that row's sum of squares.
+// grid = ceil(E/16) (x n_tasks), block = 512.
+struct RouterTask {
+  const void* packed;     // packed router [E][d]
+  const float* gain;      // [d]
+  int row;                // residual row of X
+  int stat_kind;          // 0: bins of the o projection of stat_layer, 1: bins entering stat_layer
+  int stat_layer;
+  float* out;             // [E]
+};
+
+template <int WB>
+__global__ __launch_bounds__(kGemvThreads) void k_router(Dims D, int E, RouterTask t0, RouterTask t1, RouterTask t2,
+                                                         int n_tasks, WS ws) {
+  __shared__ float red[kGemvWaves * 256];
+  __shared__ float y[256];
+  __shared__ const float* xrow_s[kMaxRows];
+  __shared__ float inv_rms;
+  extern __shared__ __attribute__((aligned(16))) char dyn[];
+  const int tiles = (E + 15) / 16;
+  const int task = blockIdx.x / tiles, tile = blockIdx.x % tiles;
+  if (task >= n_tasks) return;
+  const RouterTask T = task == 0 ? t0 : (task == 1 ? t1 : t2);
+  const void* wrow[1] = {(const char*)T.packed + (size_t)tile * 16 * D.d * (WB ? 2 : 4)};
+  GemvWave<WB, 1, 2, true> gw;
+  gw.begin(wrow, D.d);
+  if (threadIdx.x == 0) {
+    xrow_s[0] = ws.X + (size_t)T.row * D.d;
+    float a = 0.f;
+    for (int b = 0; b < kBins; ++b)
+      a += T.stat_kind == 0 ? bin_o_at(ws, D, T.stat_layer, b, T.row)[0] : bin_d_at(ws, T.stat_layer, b, T.row)[0];
+    inv_rms = rsqrtf(a / D.d + D.eps);
+  }
+  __syncthreads();
+  f32x4_t acc[1];
+  gw.run(xrow_s, T.gain, 1, dyn, acc);
+  gemv_reduce<1>(acc, 1, red, y);
+  if (threadIdx.x < 16 && tile * 16 + (int)threadIdx.x < E) T.out[tile * 16 + threadIdx.x] = y[threadIdx.x] * inv_rms;
+}
+
+// Words of the mapped host block that k_topk fills.
+constexpr int kHostSeq = 3 * kMaxTopK;       // sequence number, written last
+constexpr int kHostExited = 3 * kMaxTopK + 1;
+constexpr int kHostWords = 64;
+
+// Kernel: top-k of up to three logit vectors (one workgroup).  Task 0 (if
+// `route`) is the slow row's routing: softmax over all experts, then the k
+// largest probabilities (ties to the lower id) and their unrenormalised
+// weights.  Tasks 1, 2 are predictions: top-k of the logits.  Nothing is
+// chosen once the sequence has exited.  The ids are also written to mapped
+// host memory, then `seq` with release semantics at system scope.
+__global__ __launch_bounds__(256) void k_topk(int E, int K, const float* logits, int route, int n_pred, MoePtrs mp,
+                                              WS ws, int* slow_out, int* pred_out, int seq) {
+  __shared__ float z[3][kMaxExperts];
+  __shared__ int chosen[3][kMaxTopK];
+  __shared__ float pr[kMaxTopK];
+  const bool exited = ws.exited[0] != 0;
+  if (exited) { route = 0; n_pred = 0; }
+  for (int e = threadIdx.x; e < 3 * E; e += 256) z[e / E][e % E] = logits[e];
+  __syncthreads();
+  if (threadIdx.x < 3) {
+    const int t = threadIdx.x;
+    const bool active = t == 0 ? route != 0 : (t - 1) < n_pred;
+    if (active) {
+      float mx = -INFINITY;
+      for (int e = 0; e < E; ++e) mx = fmaxf(mx, z[t][e]);
+      float sum = 0.f;
+      if (t == 0)
+        for (int e = 0; e < E; ++e) sum += __expf(z[t][e] - mx);
+      // selection by repeated arg-max (ties to the lower id); E and K are small
+      unsigned long long taken[kMaxExperts / 64] = {};
+      for (int k = 0; k < K; ++k) {
+        int bi = -1;
+        float bz = -INFINITY;
+        for (int e = 0; e < E; ++e) {
+          if ((taken[e >> 6] >> (e & 63)) & 1ull) continue;
+          if (bi < 0 || z[t][e] > bz) { bz = z[t][e]; bi = e; }
+        }
+        taken[bi >> 6] |= 1ull << (bi & 63);
+        chosen[t][k] = bi;
+        if (t == 0) pr[k] = __expf(bz - mx) / sum;
+      }
+    } else {
+      for (int k = 0; k < K; ++k) chosen[t][k] = -1;
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x < 3 * K) {
+    const int t = threadIdx.x / K, k = threadIdx.x % K;
+    const bool active = t == 0 ? route != 0 : (t - 1) < n_pred;
+    if (active) {
+      mp.sel[t * kMaxTopK + k] = chosen[t][k];
+      if (t == 0) mp.prob[k] = pr[k];
+      if (t == 0 && slow_out) slow_out[k] = chosen[t][k];
+      if (t > 0 && pred_out) pred_out[(t - 1) * K + k] = chosen[t][k];
+    }
+  }
+  if (threadIdx.x == 0 && mp.sel_host) {
+    for (int i = 0; i < 3 * K; ++i)
+      __hip_atomic_store(&mp.sel_host[(i / K) * kMaxTopK + i % K], chosen[i / K][i % K], __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_SYSTEM);
+    __hip_atomic_store(&mp.sel_host[kHostExited], exited ? 1 : 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    __hip_atomic_store(&mp.sel_host[kHostSeq], seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+  }
+}
+
+// Kernel: the fast row's MLP of a mixture-of-experts layer, the rank-r
+// adapter alone: p += (rms(p) * g_mlp . A_m^T) B_m^T, with the adapter-down
+// sums taken from the bins of the o projection; then the partial sums of
+// the next layer's norm and of the exit signal.  grid = ceil(d/256), block = 256.
+__global__ __launch_bounds__(256) void k_fast_mlp(Dims D, RowMap rm, LayerPtrs L, int layer, WS ws) {
+  __shared__ float um[kMaxRank];
+  __shared__ float red[4];
+  const int nn = blockIdx.x * 256 + threadIdx.x;
+  const int bin = blockIdx.x % kBins;
+  for (int m = 0; m < rm.M; ++m) {
+    if (!rm.fast[m]) continue;
+    const bool ex = ws.exited[rm.seq[m]] != 0;
+    if (threadIdx.x < D.r) {
+      float a = 0.f, ss = 0.f;
+      for (int b = 0; b < kBins; ++b) {
+        a += bin_o_at(ws, D, layer, b, m)[1 + threadIdx.x];
+        ss += bin_o_at(ws, D, layer, b, m)[0];
+      }
+      um[threadIdx.x] = a * rsqrtf(ss / D.d + D.eps);
+    }
+    __syncthreads();
+    float x = 0.f, p = 0.f;
+    if (nn < D.d) {
+      x = ws.X[(size_t)m * D.d + nn];
+      p = ws.PIN[(size_t)m * D.d + nn];
+      if (!ex && L.A[4] && L.B[4]) {
+        x += dot_row(L.B[4], nn, D.r, um, D.wbf16);
+        ws.X[(size_t)m * D.d + nn] = x;
+      }
+    }
+    const float s0 = block_sum(x * x, red);
+    const float s1 = block_sum(p * x, red);
+    const float s2 = block_sum(p * p, red);
+    if (threadIdx.x == 0) {
+      add_agent(bin_d_at(ws, layer + 1, bin, m) + 0, s0);
+      add_agent(bin_d_at(ws, layer + 1, bin, m) + 1, s1);
+      add_agent(bin_d_at(ws, layer + 1, bin, m) + 2, s2);
+    }
+    __syncthreads();
+  }
+}
+
+// Kernel: sum of squares of residual row `row` into the bins entering layer
+// `next` (a layer whose MLP is skipped after an exit leaves the slow row
+// unchanged; the cache entries of the following layers still normalise it).
+// grid = 1, block = 256.
+__global__ __launch_bounds__(256) void k_row_stats(Dims D, int row, int next, WS ws) {
+  __shared__ float red[4];
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < D.d; i += 256) {
+    const float x = ws.X[(size_t)row * D.d + i];
+    ss += x * x;
+  }
+  ss = block_sum(ss, red);
+  if (threadIdx.x == 0) add_agent(bin_d_at(ws, next, 0, row), ss);
+}
+
+// Slot pointers of the k chosen experts (packed gate, up and down matrices).
+struct ExpertSlots {
+  const void* w[kMaxTopK];   // start of the expert: gate [F_e][d], up [F_e][d], down [d][F_e], each packed
+};
+
+// Kernel: gate/up of the chosen experts for the slow row, SwiGLU, times the
+// router probability.  grid = K * F_e/16, block = 512.
+template <int WB>
+__global__ __launch_bounds__(kGemvThreads) void k_moe_gateup(Dims D, int Fe, int K, ExpertSlots es, int slow_row,
+                                                             const float* mlp_norm, int layer, MoePtrs mp, WS ws) {
+  __shared__ float red[kGemvWaves * 512];
+  __shared__ float y[512];
+  __shared__ const float* xrow_s[kMaxRows];
+  __shared__ float inv_rms;
+  extern __shared__ __attribute__((aligned(16))) char dyn[];
+  const int tiles = Fe / 16;
+  const int k = blockIdx.x / tiles, t = blockIdx.x % tiles;
+  const size_t esz = WB ? 2 : 4;
+  const char* base = (const char*)es.w[k];
+  const size_t mat = (size_t)Fe * D.d * esz;
+  const void* wrow[2] = {base + (size_t)t * 16 * D.d * esz, base + mat + (size_t)t * 16 * D.d * esz};
+  GemvWave<WB, 2, 2, true> gw;
+  gw.begin(wrow, D.d);
+  if (threadIdx.x == 0) {
+    xrow_s[0] = ws.X + (size_t)slow_row * D.d;
+    float a = 0.f;
+    for (int b = 0; b < kBins; ++b) a += bin_o_at(ws, D, layer, b, slow_row)[0];
+    inv_rms = rsqrtf(a / D.d + D.eps);
+  }
+  __syncthreads();
+  f32x4_t acc[2];
+  gw.run(xrow_s, mlp_norm, 1, dyn, acc);
+  gemv_reduce<2>(acc, 1, red, y);
+  if (threadIdx.x < 16) {
+    const float g = y[threadIdx.x] * inv_rms, u = y[256 + threadIdx.x] * inv_rms;
+    mp.act[(size_t)k * Fe + t * 16 + threadIdx.x] = mp.prob[k] * silu(g) * u;
+  }
+}
+
+// Kernel: down projections of the chosen experts summed into the slow row
+// (the K experts' matrices form one reduction of length K*F_e over the
+// probability-weighted activations), then the slow row's partial sums for the
+// next layer's norm.  grid = d/16, block = 512.
+template <int WB>
+__global__ __launch_bounds__(kGemvThreads) void k_moe_down(Dims D, int Fe, int K, ExpertSlots es, int slow_row,
+                                                           int layer, MoePtrs mp, WS ws) {
+  __shared__ float red[kGemvWaves * 256];
+  __shared__ float y[256];
+  __shared__ float newx[16];
+  __shared__ const float* xrow_s[kMaxRows];
+  __shared__ const char* segs[kMaxTopK];
+  extern __shared__ __attribute__((aligned(16))) char dyn[];
+  const int n0 = blockIdx.x * 16;
+  const size_t esz = WB ? 2 : 4;
+  const size_t mat = (size_t)Fe * D.d * esz;
+  if (threadIdx.x < K)
+    segs[threadIdx.x] = (const char*)es.w[threadIdx.x] + 2 * mat + (size_t)blockIdx.x * 16 * Fe * esz;
+  if (threadIdx.x == 0) xrow_s[0] = mp.act;
+  __syncthreads();
+  GemvWave<WB, 1, 2, false> gw;
+  gw.seg = segs;
+  gw.seg_steps = Fe / (WB ? 32 : 16);
+  const void* first[1] = {segs[0]};
+  gw.begin(first, K * Fe);
+  f32x4_t acc[1];
+  gw.run(xrow_s, nullptr, 1, dyn, acc);
+  gemv_reduce<1>(acc, 1, red, y);
+  if (threadIdx.x < 16) {
+    const int nn = n0 + threadIdx.x;
+    float x = ws.X[(size_t)slow_row * D.d + nn];
+    if (!ws.exited[0]) {
+      x += y[threadIdx.x];
+      ws.X[(size_t)slow_row * D.d + nn] = x;
+    }
+    newx[threadIdx.x] = x;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float v = 0.f;
+    for (int i = 0; i < 16; ++i) v += newx[i] * newx[i];
+    add_agent(bin_d_at(ws, layer + 1, blockIdx.x % kBins, slow_row), v);
+  }
+}
+
+}  // namespace m2r2

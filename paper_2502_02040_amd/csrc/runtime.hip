@@ -1,7 +1,10 @@
 // Host runtime and C ABI of the M2R2 decode path (see include/m2r2.h).
 #include <hip/hip_runtime.h>
 
+#include <immintrin.h>
+
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -10,7 +13,9 @@
 #include <string>
 #include <vector>
 
+#include "expert_cache.h"
 #include "m2r2.h"
+#include "moe_kernels.h"
 #include "step_kernels.h"
 
 using namespace m2r2;
@@ -55,8 +60,20 @@ struct Layout {
   size_t lm;                             // packed LM head
   size_t X, PIN, QKV, O, ACT, bin_d, bin_o, bin_gu, uo, att, att_cnt, lm_val, lm_idx, lm_cnt, exited, exitb,
       reinit, err, sig, rope, total;
+  // mixture of experts: router logits, choices, probabilities, activations,
+  // and the expert cache ([n_layers][slots] slots of expert_stride bytes)
+  size_t moe_logits, moe_sel, moe_prob, moe_act, moe_slots;
+  size_t expert_bytes, expert_stride;
   int TD, TF, TV, S_max;
 };
+
+bool is_moe(const m2r2_config& c) { return c.n_experts > 0; }
+
+// Packed gate + up ([F_e][d] each) + down ([d][F_e]).
+size_t expert_bytes_of(const m2r2_config& c) {
+  const int wb = c.wdtype == M2R2_BF16;
+  return 2 * packed_bytes(c.expert_ffn, c.d_model, wb) + packed_bytes(c.d_model, c.expert_ffn, wb);
+}
 
 Layout make_layout(const m2r2_config& c, int max_batch, int max_chunk, int max_ctx) {
   Layout L{};
@@ -80,15 +97,22 @@ Layout make_layout(const m2r2_config& c, int max_batch, int max_chunk, int max_c
   };
   const int wb = c.wdtype == M2R2_BF16;
   L.packed = 0;
+  const bool moe = is_moe(c);
   for (int l = 0; l < c.n_layers; ++l) {
     L.lay_off.push_back(take(packed_bytes(qdim, d, wb)));
     L.lay_off.push_back(take(packed_bytes(qdim, d, wb)));
     L.lay_off.push_back(take(packed_bytes(qdim, d, wb)));
     L.lay_off.push_back(take(packed_bytes(3 * r, d, wb)));
     L.lay_off.push_back(take(packed_bytes(d, qdim, wb)));
-    L.lay_off.push_back(take(packed_bytes(c.ffn, d, wb)));
-    L.lay_off.push_back(take(packed_bytes(c.ffn, d, wb)));
-    L.lay_off.push_back(take(packed_bytes(d, c.ffn, wb)));
+    if (moe) {   // slot 5: the router; 6, 7 unused
+      L.lay_off.push_back(take(packed_bytes(c.n_experts, d, wb)));
+      L.lay_off.push_back(0);
+      L.lay_off.push_back(0);
+    } else {
+      L.lay_off.push_back(take(packed_bytes(c.ffn, d, wb)));
+      L.lay_off.push_back(take(packed_bytes(c.ffn, d, wb)));
+      L.lay_off.push_back(take(packed_bytes(d, c.ffn, wb)));
+    }
   }
   L.lm = take(packed_bytes(c.vocab, d, wb));
   L.X = take(sizeof(float) * kMaxRows * d);
@@ -112,6 +136,15 @@ Layout make_layout(const m2r2_config& c, int max_batch, int max_chunk, int max_c
   L.err = take(sizeof(int));
   L.sig = take(sizeof(float) * kMaxSeq * c.n_layers);
   L.rope = take(sizeof(float) * 2 * (size_t)max_ctx * (c.head_dim / 2));
+  if (moe) {
+    L.moe_logits = take(sizeof(float) * 3 * c.n_experts);
+    L.moe_sel = take(sizeof(int) * 3 * kMaxTopK);
+    L.moe_prob = take(sizeof(float) * kMaxTopK);
+    L.moe_act = take(sizeof(float) * (size_t)c.top_k * c.expert_ffn);
+    L.expert_bytes = expert_bytes_of(c);
+    L.expert_stride = (L.expert_bytes + 255) & ~(size_t)255;
+    L.moe_slots = take(L.expert_stride * c.n_layers * c.expert_slots);
+  }
   L.total = off;
   return L;
 }
@@ -123,7 +156,19 @@ m2r2_status check_config(const m2r2_config* c, int max_batch, int max_chunk, int
   const int kstep = c->wdtype == M2R2_BF16 ? 32 : 16;
   if (c->n_layers < 1 || c->n_layers > 127) return fail(M2R2_E_SHAPE, "n_layers %d not in [1,127]", c->n_layers);
   if (c->d_model <= 0 || c->d_model % kstep) return fail(M2R2_E_SHAPE, "d_model %d not a multiple of %d", c->d_model, kstep);
-  if (c->ffn <= 0 || c->ffn % kstep) return fail(M2R2_E_SHAPE, "ffn %d not a multiple of %d", c->ffn, kstep);
+  if (c->n_experts < 0) return fail(M2R2_E_SHAPE, "n_experts %d", c->n_experts);
+  if (!is_moe(*c) && (c->ffn <= 0 || c->ffn % kstep))
+    return fail(M2R2_E_SHAPE, "ffn %d not a multiple of %d", c->ffn, kstep);
+  if (is_moe(*c)) {
+    if (c->n_experts > kMaxExperts) return fail(M2R2_E_SHAPE, "n_experts %d > %d", c->n_experts, kMaxExperts);
+    if (c->top_k < 1 || c->top_k > kMaxTopK || c->top_k > c->n_experts)
+      return fail(M2R2_E_SHAPE, "top_k %d not in [1, min(%d, n_experts)]", c->top_k, kMaxTopK);
+    if (c->expert_ffn <= 0 || c->expert_ffn % kstep)
+      return fail(M2R2_E_SHAPE, "expert_ffn %d not a multiple of %d", c->expert_ffn, kstep);
+    if (c->expert_slots < c->top_k || c->expert_slots > c->n_experts)
+      return fail(M2R2_E_SHAPE, "expert_slots %d not in [top_k, n_experts]", c->expert_slots);
+    if (max_batch != 1) return fail(M2R2_E_UNSUPPORTED, "mixture-of-experts decoding takes max_batch 1");
+  }
   if (c->head_dim != 64 && c->head_dim != 96 && c->head_dim != 128)
     return fail(M2R2_E_UNSUPPORTED, "head_dim %d (supported: 64, 96, 128)", c->head_dim);
   if (c->n_heads < 1 || (c->n_heads * c->head_dim) % kstep)
@@ -141,6 +186,27 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
 }  // namespace
 
+// Host side of the expert cache of a mixture-of-experts context.
+struct MoeState {
+  bool on = false;
+  int E = 0, K = 0, Fe = 0, C = 0;
+  size_t ebytes = 0, stride = 0;
+  const char* store_h = nullptr;   // pinned host store [n_layers][E][ebytes]
+  char* slots_d = nullptr;         // [n_layers][C][stride]
+  std::vector<const void*> router; // packed router per layer
+  MoePtrs mp{};
+  int* host_words = nullptr;       // mapped host block written by k_topk
+  int seq = 0;
+  int policy = M2R2_MOE_AHEAD_OF_TIME;
+  ExpertCachePolicy pol;
+  std::vector<hipEvent_t> slot_ev;   // [n_layers*C] last copy into the slot
+  std::vector<char> slot_pending;    // a copy was recorded and not yet seen complete
+  std::vector<hipEvent_t> layer_done;  // [n_layers] the layer's expert kernels, recorded on the compute stream
+  std::vector<char> layer_done_rec;
+  hipStream_t copy_demand = nullptr, copy_ahead = nullptr;
+  int64_t h2d_bytes = 0, copy_waits = 0, host_wait_ns = 0;
+};
+
 struct m2r2_ctx {
   m2r2_config cfg;
   Dims D;
@@ -155,6 +221,7 @@ struct m2r2_ctx {
   int timed_class = -1;
   std::vector<hipEvent_t> ev;   // pairs
   int ev_used = 0;
+  MoeState moe;
 };
 
 namespace {
@@ -270,6 +337,10 @@ hipError_t pack_all(m2r2_ctx* c, const m2r2_weights* w, void* workspace) {
     if (e == hipSuccess) e = pack_one(wb, one(L.wv, q), q, d, b + o[2]);
     if (e == hipSuccess) e = pack_one(wb, PackSrc{{L.A[0], L.A[1], L.A[2]}, {r, r, r}}, 3 * r, d, b + o[3]);
     if (e == hipSuccess) e = pack_one(wb, one(L.wo, d), d, q, b + o[4]);
+    if (is_moe(cf)) {
+      if (e == hipSuccess) e = pack_one(wb, one(L.router, cf.n_experts), cf.n_experts, d, b + o[5]);
+      continue;
+    }
     if (e == hipSuccess) e = pack_one(wb, one(L.wg, F), F, d, b + o[5]);
     if (e == hipSuccess) e = pack_one(wb, one(L.wu, F), F, d, b + o[6]);
     if (e == hipSuccess) e = pack_one(wb, one(L.wd, d), d, F, b + o[7]);
@@ -301,6 +372,216 @@ m2r2_status run_pass(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPt
   if (wb && !kb) return run_hd<1, 0>(c, rm, io, kv, nl, st);
   if (!wb && kb) return run_hd<0, 1>(c, rm, io, kv, nl, st);
   return run_hd<0, 0>(c, rm, io, kv, nl, st);
+}
+
+// ---- mixture of experts --------------------------------------------------------
+
+// Copy expert e of layer l from the host store into slot `slot` on copy
+// stream cs, after the layer's last expert kernels (the slot's previous
+// occupant may still be read) and after any earlier copy into the slot.
+hipError_t moe_copy(m2r2_ctx* c, int l, int slot, int e, hipStream_t cs) {
+  MoeState& M = c->moe;
+  const int i = l * M.C + slot;
+  hipError_t r = hipSuccess;
+  if (M.layer_done_rec[l]) r = hipStreamWaitEvent(cs, M.layer_done[l], 0);
+  if (r == hipSuccess && M.slot_pending[i]) r = hipStreamWaitEvent(cs, M.slot_ev[i], 0);
+  if (r == hipSuccess)
+    r = hipMemcpyAsync(M.slots_d + (size_t)i * M.stride, M.store_h + ((size_t)l * M.E + e) * M.ebytes, M.ebytes,
+                       hipMemcpyHostToDevice, cs);
+  if (r == hipSuccess) r = hipEventRecord(M.slot_ev[i], cs);
+  if (r == hipSuccess) {
+    M.slot_pending[i] = 1;
+    M.h2d_bytes += (int64_t)M.ebytes;
+  }
+  return r;
+}
+
+// Wait until k_topk has published sequence number `seq` in the mapped block.
+m2r2_status wait_routing(m2r2_ctx* c, int seq, hipStream_t st) {
+  using clk = std::chrono::steady_clock;
+  const auto t0 = clk::now();
+  int* w = &c->moe.host_words[kHostSeq];
+  uint64_t spins = 0;
+  while (__atomic_load_n(w, __ATOMIC_ACQUIRE) != seq) {
+    if ((++spins & 0xfff) == 0) {
+      const hipError_t q = hipStreamQuery(st);
+      if (q != hipSuccess && q != hipErrorNotReady) return fail(M2R2_E_HIP, "routing: %s", hipGetErrorString(q));
+      if (q == hipSuccess && __atomic_load_n(w, __ATOMIC_ACQUIRE) != seq)
+        return fail(M2R2_E_HIP, "routing result missing after the stream drained");
+      if (clk::now() - t0 > std::chrono::seconds(60)) return fail(M2R2_E_HIP, "timed out waiting for routing");
+    }
+    _mm_pause();
+  }
+  c->moe.host_wait_ns += std::chrono::duration_cast<std::chrono::nanoseconds>(clk::now() - t0).count();
+  return M2R2_OK;
+}
+
+// Dual-stream (or slow-only) pass of a mixture-of-experts model, batch 1:
+// rows 0 (slow) and 1 (fast).
+template <int WB, int KB, int HD>
+m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPtrs& kv, const m2r2_step_out* out,
+                      bool dual, hipStream_t st) {
+  constexpr int MT = 2;
+  const Dims& D = c->D;
+  MoeState& M = c->moe;
+  const int S = choose_splits(1, rm.M, D.H, c->max_ctx);
+  if (S > c->lay.S_max || S + 1 > 64) return fail(M2R2_E_SHAPE, "attention splits exceed the workspace");
+  const size_t smem = attn_smem_bytes();
+  const size_t gl = gemv_lds_bytes(WB, MT);
+  const bool ahead = dual && M.policy == M2R2_MOE_AHEAD_OF_TIME;
+  const bool want_pred = dual && (ahead || (out && out->pred_experts_d));
+  const int tiles = (M.E + 15) / 16;
+  float* logits = (float*)M.mp.logits;
+  std::vector<int> pslots, pexperts;
+  for (int l = 0; l < D.n_layers; ++l) {
+    const LayerPtrs& L = c->layers[l];
+    TIMED(0, (k_qkv<WB, MT><<<3 * (D.qdim / 16) + (3 * D.r + 15) / 16, kGemvThreads, gl, st>>>(D, L, rm, c->ws, io, l)));
+    TIMED(1, (k_attn<KB, HD><<<dim3(S + 1, D.H, 1), kAttnThreads, smem, st>>>(D, L, rm, c->ws, io, kv, l, S)));
+    TIMED(7, (k_attn_merge<<<dim3(D.H, 1), kAttnThreads, 0, st>>>(D, rm, c->ws, S)));
+    TIMED(2, (k_oproj<WB, MT><<<c->lay.TD, kGemvThreads, gl, st>>>(D, L, rm, c->ws, io, l)));
+    if (dual) TIMED(10, (k_fast_mlp<<<(D.d + 255) / 256, 256, 0, st>>>(D, rm, L, l, c->ws)));
+    // routing of the slow row, predictions for layers 2l+2 and 2l+3 from the fast row
+    RouterTask t[3] = {};
+    t[0] = RouterTask{M.router[l], L.mlp_norm, 0, 0, l, logits};
+    int n_pred = 0;
+    if (want_pred)
+      for (int lp = 2 * l + 2; lp <= 2 * l + 3 && lp < D.n_layers; ++lp, ++n_pred)
+        t[1 + n_pred] = RouterTask{M.router[lp], c->layers[lp].mlp_norm, 1, 1, l + 1, logits + (1 + n_pred) * M.E};
+    TIMED(10, (k_router<WB><<<tiles * (1 + n_pred), kGemvThreads, gl, st>>>(D, M.E, t[0], t[1], t[2], 1 + n_pred,
+                                                                          c->ws)));
+    int* slow_out = out->slow_experts_d ? out->slow_experts_d + l * M.K : nullptr;
+    int* pred_out = (out->pred_experts_d && n_pred) ? out->pred_experts_d + (2 * l + 2) * M.K : nullptr;
+    const int seq = ++M.seq;
+    TIMED(10, (k_topk<<<1, 256, 0, st>>>(M.E, M.K, logits, 1, n_pred, M.mp, c->ws, slow_out, pred_out, seq)));
+    HIP_TRY(hipGetLastError());
+    if (m2r2_status s = wait_routing(c, seq, st)) return s;
+    if (M.host_words[kHostExited]) {   // exited: no MLP for the remaining layers
+      TIMED(10, (k_row_stats<<<1, 256, 0, st>>>(D, 0, l + 1, c->ws)));
+      HIP_TRY(hipGetLastError());
+      continue;
+    }
+    int need[kMaxTopK], slot[kMaxTopK];
+    bool load[kMaxTopK];
+    for (int k = 0; k < M.K; ++k) {
+      need[k] = M.host_words[k];
+      if (need[k] < 0 || need[k] >= M.E) return fail(M2R2_E_HIP, "layer %d: router returned expert %d", l, need[k]);
+    }
+    M.pol.use(l, need, M.K, slot, load);
+    for (int k = 0; k < M.K; ++k)
+      if (load[k]) HIP_TRY(moe_copy(c, l, slot[k], need[k], M.copy_demand));
+    ExpertSlots es{};
+    for (int k = 0; k < M.K; ++k) {
+      const int i = l * M.C + slot[k];
+      if (M.slot_pending[i]) {
+        const hipError_t q = hipEventQuery(M.slot_ev[i]);
+        if (q == hipSuccess) {
+          M.slot_pending[i] = 0;
+        } else if (q == hipErrorNotReady) {
+          HIP_TRY(hipStreamWaitEvent(st, M.slot_ev[i], 0));
+          ++M.copy_waits;
+        } else {
+          return fail(M2R2_E_HIP, "expert copy: %s", hipGetErrorString(q));
+        }
+      }
+      es.w[k] = M.slots_d + (size_t)i * M.stride;
+    }
+    TIMED(8, (k_moe_gateup<WB><<<M.K * (M.Fe / 16), kGemvThreads, gl, st>>>(D, M.Fe, M.K, es, 0, L.mlp_norm, l, M.mp,
+                                                                           c->ws)));
+    TIMED(9, (k_moe_down<WB><<<c->lay.TD, kGemvThreads, gl, st>>>(D, M.Fe, M.K, es, 0, l, M.mp, c->ws)));
+    HIP_TRY(hipGetLastError());
+    HIP_TRY(hipEventRecord(M.layer_done[l], st));
+    M.layer_done_rec[l] = 1;
+    if (ahead) {
+      for (int j = 0; j < n_pred; ++j) {
+        pslots.clear();
+        pexperts.clear();
+        M.pol.predict(2 * l + 2 + j, M.host_words + (1 + j) * kMaxTopK, M.K, &pslots, &pexperts);
+        for (size_t q = 0; q < pslots.size(); ++q)
+          HIP_TRY(moe_copy(c, 2 * l + 2 + j, pslots[q], pexperts[q], M.copy_ahead));
+      }
+    }
+  }
+  TIMED(5, (k_head<WB, MT><<<c->lay.TV, kGemvThreads, gl, st>>>(D, c->lm_head, c->final_norm, rm, c->ws, io, kv,
+                                                            c->lay.TV, D.n_layers)));
+  HIP_TRY(hipGetLastError());
+  M.pol.end_token();
+  return M2R2_OK;
+}
+
+template <int WB, int KB>
+m2r2_status run_moe_hd(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPtrs& kv, const m2r2_step_out* out,
+                       bool dual, hipStream_t st) {
+  switch (c->D.hd) {
+    case 64: return run_moe_t<WB, KB, 64>(c, rm, io, kv, out, dual, st);
+    case 96: return run_moe_t<WB, KB, 96>(c, rm, io, kv, out, dual, st);
+    case 128: return run_moe_t<WB, KB, 128>(c, rm, io, kv, out, dual, st);
+  }
+  return fail(M2R2_E_UNSUPPORTED, "head_dim");
+}
+
+m2r2_status run_moe_pass(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPtrs& kv, const m2r2_step_out* out,
+                         bool dual, hipStream_t st) {
+  const int N = c->D.n_layers, K = c->moe.K;
+  if (out->slow_experts_d) HIP_TRY(hipMemsetAsync(out->slow_experts_d, 0xff, sizeof(int32_t) * N * K, st));
+  if (out->pred_experts_d) HIP_TRY(hipMemsetAsync(out->pred_experts_d, 0xff, sizeof(int32_t) * N * K, st));
+  TIMED(6, (k_embed<<<rm.M, 256, 0, st>>>(c->D, c->embed, rm, c->ws, io, 1)));
+  HIP_TRY(hipGetLastError());
+  const int wb = c->D.wbf16, kb = c->D.kvbf16;
+  if (wb && kb) return run_moe_hd<1, 1>(c, rm, io, kv, out, dual, st);
+  if (wb && !kb) return run_moe_hd<1, 0>(c, rm, io, kv, out, dual, st);
+  if (!wb && kb) return run_moe_hd<0, 1>(c, rm, io, kv, out, dual, st);
+  return run_moe_hd<0, 0>(c, rm, io, kv, out, dual, st);
+}
+
+template <int WB>
+hipError_t set_moe_lds_limits() {
+  const int bytes = gemv_lds_bytes(WB, 2);
+  hipError_t e = hipSuccess;
+  const void* fns[] = {(const void*)k_router<WB>, (const void*)k_moe_gateup<WB>, (const void*)k_moe_down<WB>};
+  for (const void* f : fns) {
+    hipError_t r = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (r != hipSuccess) e = r;
+  }
+  return e;
+}
+
+// Warm start of the expert cache: experts 0..C-1 in slots 0..C-1 of every
+// layer (synchronous).
+hipError_t moe_warm(m2r2_ctx* c) {
+  MoeState& M = c->moe;
+  hipError_t e = hipDeviceSynchronize();
+  M.pol.warm();
+  for (int l = 0; l < c->D.n_layers && e == hipSuccess; ++l)
+    for (int s = 0; s < M.C && e == hipSuccess; ++s)
+      e = hipMemcpyAsync(M.slots_d + ((size_t)l * M.C + s) * M.stride, M.store_h + ((size_t)l * M.E + s) * M.ebytes,
+                         M.ebytes, hipMemcpyHostToDevice, M.copy_demand);
+  if (e == hipSuccess) e = hipStreamSynchronize(M.copy_demand);
+  std::fill(M.slot_pending.begin(), M.slot_pending.end(), 0);
+  std::fill(M.layer_done_rec.begin(), M.layer_done_rec.end(), 0);
+  M.h2d_bytes = M.copy_waits = M.host_wait_ns = 0;
+  return e;
+}
+
+void fill_stats(const CacheCounters& k, m2r2_moe_counters* o) {
+  memset(o, 0, sizeof *o);
+  o->hits = k.hits; o->misses = k.misses; o->prefetch_issued = k.prefetch_issued; o->prefetch_used = k.prefetch_used;
+  o->prefetch_wasted = k.prefetch_wasted; o->loads = k.loads; o->pred_correct = k.pred_correct;
+  o->pred_total = k.pred_total;
+  for (size_t l = 0; l < k.layer_misses.size() && l < 128; ++l) o->layer_misses[l] = k.layer_misses[l];
+}
+
+void moe_release(MoeState& M) {
+  if (M.copy_demand) (void)hipStreamSynchronize(M.copy_demand);
+  if (M.copy_ahead) (void)hipStreamSynchronize(M.copy_ahead);
+  for (hipEvent_t e : M.slot_ev) (void)hipEventDestroy(e);
+  for (hipEvent_t e : M.layer_done) (void)hipEventDestroy(e);
+  M.slot_ev.clear();
+  M.layer_done.clear();
+  if (M.copy_demand) (void)hipStreamDestroy(M.copy_demand);
+  if (M.copy_ahead) (void)hipStreamDestroy(M.copy_ahead);
+  if (M.host_words) (void)hipHostFree(M.host_words);
+  M.copy_demand = M.copy_ahead = nullptr;
+  M.host_words = nullptr;
 }
 
 RowMap empty_rowmap() {
@@ -341,18 +622,26 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
   if (!workspace || ((uintptr_t)workspace & 255)) return fail(M2R2_E_INVALID, "workspace NULL or not 256-byte aligned");
   const Layout lay = make_layout(*cfg, max_batch, max_chunk, max_ctx);
   if (ws_bytes < lay.total) return fail(M2R2_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, lay.total);
+  const bool moe = is_moe(*cfg);
+  if (moe && !w->experts_h) return fail(M2R2_E_INVALID, "mixture of experts: experts_h is NULL");
   for (int l = 0; l < cfg->n_layers; ++l) {
     const m2r2_layer_weights& L = w->layers[l];
-    if (!L.attn_norm || !L.wq || !L.wk || !L.wv || !L.wo || !L.mlp_norm || !L.wg || !L.wu || !L.wd)
+    if (!L.attn_norm || !L.wq || !L.wk || !L.wv || !L.wo || !L.mlp_norm)
       return fail(M2R2_E_INVALID, "layer %d: a base weight pointer is NULL", l);
-    const void* ps[] = {L.wq, L.wk, L.wv, L.wo, L.wg, L.wu, L.wd, w->embed, w->lm_head};
+    if (!moe && (!L.wg || !L.wu || !L.wd)) return fail(M2R2_E_INVALID, "layer %d: an MLP weight pointer is NULL", l);
+    if (moe && !L.router) return fail(M2R2_E_INVALID, "layer %d: router is NULL", l);
+    const void* ps[] = {L.wq, L.wk, L.wv, L.wo, L.wg, L.wu, L.wd, L.router, w->embed, w->lm_head};
     for (const void* p : ps)
       if (!aligned16(p)) return fail(M2R2_E_INVALID, "layer %d: weight not 16-byte aligned", l);
     for (int a = 0; a < 7; ++a) {
       if ((L.A[a] == nullptr) != (L.B[a] == nullptr))
         return fail(M2R2_E_INVALID, "layer %d adapter %d: A and B must be both set or both NULL", l, a);
       if (!aligned16(L.A[a])) return fail(M2R2_E_INVALID, "layer %d adapter %d: A not 16-byte aligned", l, a);
+      if (moe && a >= 4 && L.A[a])
+        return fail(M2R2_E_INVALID, "layer %d: a mixture-of-experts layer takes A_m/B_m, not adapter %d", l, a);
     }
+    if ((L.A_m == nullptr) != (L.B_m == nullptr))
+      return fail(M2R2_E_INVALID, "layer %d: A_m and B_m must be both set or both NULL", l);
   }
   m2r2_ctx* c = new (std::nothrow) m2r2_ctx();
   if (!c) return fail(M2R2_E_NOMEM, "host allocation");
@@ -377,8 +666,17 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
     char* wsb = (char*)workspace;
     const size_t* o = &lay.lay_off[8 * l];
     L.pq = wsb + o[0]; L.pk = wsb + o[1]; L.pv = wsb + o[2]; L.pa = wsb + o[3];
-    L.po = wsb + o[4]; L.pg = wsb + o[5]; L.pu = wsb + o[6]; L.pd = wsb + o[7];
+    L.po = wsb + o[4];
     for (int a = 0; a < 7; ++a) { L.A[a] = s.A[a]; L.B[a] = s.B[a]; }
+    if (moe) {
+      // the fast MLP adapter rides in the gate slot: the o projection sums its
+      // adapter-down partials, the fast MLP kernel applies its up factor
+      L.pg = L.pu = L.pd = nullptr;
+      L.A[4] = s.A_m; L.B[4] = s.B_m;
+      c->moe.router.push_back(wsb + o[5]);
+    } else {
+      L.pg = wsb + o[5]; L.pu = wsb + o[6]; L.pd = wsb + o[7];
+    }
   }
   char* b = (char*)workspace;
   WS& ws = c->ws;
@@ -410,8 +708,46 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
   if (e == hipSuccess) e = set_lds_limits<1, 2>();
   if (e == hipSuccess) e = set_lds_limits<0, 16>();
   if (e == hipSuccess) e = set_lds_limits<1, 16>();
+  if (e == hipSuccess && moe) {
+    MoeState& M = c->moe;
+    M.on = true;
+    M.E = cfg->n_experts; M.K = cfg->top_k; M.Fe = cfg->expert_ffn; M.C = cfg->expert_slots;
+    M.ebytes = lay.expert_bytes;
+    M.stride = lay.expert_stride;
+    M.store_h = (const char*)w->experts_h;
+    M.slots_d = b + lay.moe_slots;
+    M.mp.logits = (const float*)(b + lay.moe_logits);
+    M.mp.sel = (int*)(b + lay.moe_sel);
+    M.mp.prob = (float*)(b + lay.moe_prob);
+    M.mp.act = (float*)(b + lay.moe_act);
+    e = hipHostMalloc((void**)&M.host_words, sizeof(int) * kHostWords, hipHostMallocMapped | hipHostMallocCoherent);
+    if (e == hipSuccess) {
+      memset(M.host_words, 0, sizeof(int) * kHostWords);
+      e = hipHostGetDevicePointer((void**)&M.mp.sel_host, M.host_words, 0);
+    }
+    if (e == hipSuccess) e = hipStreamCreateWithFlags(&M.copy_demand, hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipStreamCreateWithFlags(&M.copy_ahead, hipStreamNonBlocking);
+    const int n_ev = cfg->n_layers * M.C;
+    for (int i = 0; i < n_ev && e == hipSuccess; ++i) {
+      hipEvent_t ev;
+      e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+      if (e == hipSuccess) M.slot_ev.push_back(ev);
+    }
+    for (int l = 0; l < cfg->n_layers && e == hipSuccess; ++l) {
+      hipEvent_t ev;
+      e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+      if (e == hipSuccess) M.layer_done.push_back(ev);
+    }
+    M.slot_pending.assign(n_ev, 0);
+    M.layer_done_rec.assign(cfg->n_layers, 0);
+    M.pol.init(cfg->n_layers, M.E, M.C);
+    if (e == hipSuccess) e = set_moe_lds_limits<0>();
+    if (e == hipSuccess) e = set_moe_lds_limits<1>();
+    if (e == hipSuccess) e = moe_warm(c);
+  }
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) {
+    moe_release(c->moe);
     delete c;
     return fail(M2R2_E_HIP, "workspace init: %s", hipGetErrorString(e));
   }
@@ -422,12 +758,13 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
 M2R2_API void m2r2_destroy(m2r2_ctx* ctx) {
   if (!ctx) return;
   for (hipEvent_t e : ctx->ev) (void)hipEventDestroy(e);
+  moe_release(ctx->moe);
   delete ctx;
 }
 
 M2R2_API m2r2_status m2r2_timing_enable(m2r2_ctx* c, int32_t kernel_class) {
   if (!c) return fail(M2R2_E_INVALID, "ctx is NULL");
-  if (kernel_class < -1 || kernel_class > 7) return fail(M2R2_E_INVALID, "kernel class %d", kernel_class);
+  if (kernel_class < -1 || kernel_class > 10) return fail(M2R2_E_INVALID, "kernel class %d", kernel_class);
   c->timed_class = kernel_class;
   c->ev_used = 0;   // a new record
   return M2R2_OK;
@@ -498,6 +835,10 @@ M2R2_API m2r2_status m2r2_decode_step(m2r2_ctx* c, int32_t batch, int32_t dual, 
       rm.slow_of[m + 1] = m;
     }
   }
+  if (c->moe.on) {
+    if (batch != 1) return fail(M2R2_E_UNSUPPORTED, "mixture-of-experts decoding takes batch 1");
+    return run_moe_pass(c, rm, io, kv_ptrs(kv), out, dual != 0, stream);
+  }
   return run_pass(c, rm, io, kv_ptrs(kv), c->D.n_layers, stream);
 }
 
@@ -506,6 +847,7 @@ M2R2_API m2r2_status m2r2_draft(m2r2_ctx* c, const int32_t* last_token_d, const 
                                 hipStream_t stream) {
   if (!c) return fail(M2R2_E_INVALID, "ctx is NULL");
   if (!last_token_d || !positions_d || !drafts_d) return fail(M2R2_E_INVALID, "NULL token/position/drafts");
+  if (c->moe.on) return fail(M2R2_E_UNSUPPORTED, "drafting is implemented for dense models");
   if (exit_layer < 1 || exit_layer > c->D.n_layers) return fail(M2R2_E_SHAPE, "exit_layer %d", exit_layer);
   if (gamma < 1 || gamma > 64) return fail(M2R2_E_SHAPE, "gamma %d not in [1,64]", gamma);
   if (m2r2_status s = check_kv(c, kv)) return s;
@@ -530,6 +872,7 @@ M2R2_API m2r2_status m2r2_verify(m2r2_ctx* c, const int32_t* chunk_d, int32_t n,
                                  int32_t* bonus_token_d, hipStream_t stream) {
   if (!c) return fail(M2R2_E_INVALID, "ctx is NULL");
   if (!chunk_d || !positions_d || !targets_d) return fail(M2R2_E_INVALID, "NULL chunk/positions/targets");
+  if (c->moe.on) return fail(M2R2_E_UNSUPPORTED, "chunk verification is implemented for dense models");
   if (n < 1 || n > c->max_chunk) return fail(M2R2_E_SHAPE, "chunk %d not in [1,%d]", n, c->max_chunk);
   if (m2r2_status s = check_kv(c, kv)) return s;
   RowMap rm = empty_rowmap();
@@ -546,6 +889,119 @@ M2R2_API m2r2_status m2r2_verify(m2r2_ctx* c, const int32_t* chunk_d, int32_t n,
   io.n_chunk = n;
   io.mode = EX_OFF;
   return run_pass(c, rm, io, kv_ptrs(kv), c->D.n_layers, stream);
+}
+
+M2R2_API m2r2_status m2r2_expert_bytes(const m2r2_config* cfg, size_t* bytes_out) {
+  if (!cfg || !bytes_out) return fail(M2R2_E_INVALID, "NULL argument");
+  if (cfg->wdtype != M2R2_F32 && cfg->wdtype != M2R2_BF16) return fail(M2R2_E_DTYPE, "wdtype %d", cfg->wdtype);
+  const int kstep = cfg->wdtype == M2R2_BF16 ? 32 : 16;
+  if (!is_moe(*cfg)) return fail(M2R2_E_SHAPE, "not a mixture-of-experts config");
+  if (cfg->d_model <= 0 || cfg->d_model % kstep || cfg->expert_ffn <= 0 || cfg->expert_ffn % kstep)
+    return fail(M2R2_E_SHAPE, "d_model and expert_ffn must be positive multiples of %d", kstep);
+  *bytes_out = expert_bytes_of(*cfg);
+  return M2R2_OK;
+}
+
+M2R2_API m2r2_status m2r2_pack_expert(const m2r2_config* cfg, const void* wg_h, const void* wu_h, const void* wd_h,
+                                      void* dst_h) {
+  size_t total = 0;
+  if (m2r2_status st = m2r2_expert_bytes(cfg, &total)) return st;
+  if (!wg_h || !wu_h || !wd_h || !dst_h) return fail(M2R2_E_INVALID, "NULL matrix or destination");
+  const int wb = cfg->wdtype == M2R2_BF16, esz = wb ? 2 : 4, kstep = wb ? 32 : 16, epl = kstep / 4;
+  const int d = cfg->d_model, Fe = cfg->expert_ffn;
+  char* dst = (char*)dst_h;
+  // same tile-packed layout as the device packing kernel
+  auto pack = [&](const char* src, int rows, int K, char* out) {
+    const int S = K / kstep;
+    const int tiles = (rows + 15) / 16;
+    for (int t = 0; t < tiles; ++t)
+      for (int st = 0; st < S; ++st)
+        for (int l = 0; l < 64; ++l) {
+          const int r = t * 16 + (l & 15), col = st * kstep + epl * (l >> 4);
+          char* o = out + (((size_t)t * S + st) * 64 + l) * 16;
+          if (r < rows) memcpy(o, src + ((size_t)r * K + col) * esz, 16);
+          else memset(o, 0, 16);
+        }
+  };
+  const size_t mat = packed_bytes(Fe, d, wb);
+  pack((const char*)wg_h, Fe, d, dst);
+  pack((const char*)wu_h, Fe, d, dst + mat);
+  pack((const char*)wd_h, d, Fe, dst + 2 * mat);
+  return M2R2_OK;
+}
+
+M2R2_API m2r2_status m2r2_moe_set_policy(m2r2_ctx* c, int32_t policy) {
+  if (!c) return fail(M2R2_E_INVALID, "ctx is NULL");
+  if (!c->moe.on) return fail(M2R2_E_STATE, "not a mixture-of-experts context");
+  if (policy != M2R2_MOE_ON_DEMAND && policy != M2R2_MOE_AHEAD_OF_TIME) return fail(M2R2_E_INVALID, "policy %d", policy);
+  c->moe.policy = policy;
+  return M2R2_OK;
+}
+
+M2R2_API m2r2_status m2r2_prefetch_experts(m2r2_ctx* c, int32_t layer, const int32_t* ids_h, int32_t n,
+                                           int32_t priority, hipStream_t copy_stream) {
+  if (!c) return fail(M2R2_E_INVALID, "ctx is NULL");
+  MoeState& M = c->moe;
+  if (!M.on) return fail(M2R2_E_STATE, "not a mixture-of-experts context");
+  if (layer < 0 || layer >= c->D.n_layers) return fail(M2R2_E_SHAPE, "layer %d", layer);
+  if (n < 0 || n > M.C || (n > 0 && !ids_h)) return fail(M2R2_E_SHAPE, "n %d not in [0, slots]", n);
+  for (int i = 0; i < n; ++i) {
+    if (ids_h[i] >= M.E) return fail(M2R2_E_SHAPE, "expert id %d >= n_experts", ids_h[i]);
+    for (int j = 0; j < i; ++j)
+      if (ids_h[i] >= 0 && ids_h[i] == ids_h[j]) return fail(M2R2_E_INVALID, "expert %d listed twice", ids_h[i]);
+  }
+  hipStream_t cs = copy_stream ? copy_stream : (priority ? M.copy_demand : M.copy_ahead);
+  std::vector<int> slots, experts;
+  M.pol.predict(layer, ids_h, n, &slots, &experts);
+  for (size_t q = 0; q < slots.size(); ++q) HIP_TRY(moe_copy(c, layer, slots[q], experts[q], cs));
+  return M2R2_OK;
+}
+
+M2R2_API m2r2_status m2r2_moe_reset(m2r2_ctx* c) {
+  if (!c) return fail(M2R2_E_INVALID, "ctx is NULL");
+  if (!c->moe.on) return fail(M2R2_E_STATE, "not a mixture-of-experts context");
+  HIP_TRY(moe_warm(c));
+  return M2R2_OK;
+}
+
+M2R2_API m2r2_status m2r2_moe_stats(m2r2_ctx* c, m2r2_moe_counters* out) {
+  if (!c || !out) return fail(M2R2_E_INVALID, "NULL argument");
+  if (!c->moe.on) return fail(M2R2_E_STATE, "not a mixture-of-experts context");
+  fill_stats(c->moe.pol.counters(), out);
+  out->h2d_bytes = c->moe.h2d_bytes;
+  out->copy_waits = c->moe.copy_waits;
+  out->host_wait_ns = c->moe.host_wait_ns;
+  return M2R2_OK;
+}
+
+M2R2_API m2r2_status m2r2_expert_cache_replay(int32_t n_layers, int32_t n_experts, int32_t top_k, int32_t slots,
+                                              int32_t n_tokens, const int32_t* slow_h, const int32_t* pred_h,
+                                              int32_t prefetch, m2r2_moe_counters* out) {
+  if (!slow_h || !out) return fail(M2R2_E_INVALID, "NULL argument");
+  if (n_layers < 1 || n_layers > 127 || n_experts < 1 || top_k < 1 || top_k > kMaxTopK || n_tokens < 0)
+    return fail(M2R2_E_SHAPE, "sizes");
+  if (slots < top_k || slots > n_experts) return fail(M2R2_E_SHAPE, "need top_k <= slots <= n_experts");
+  const size_t per_tok = (size_t)n_layers * top_k;
+  for (size_t i = 0; i < per_tok * n_tokens; ++i) {
+    if (slow_h[i] < 0 || slow_h[i] >= n_experts) return fail(M2R2_E_SHAPE, "slow expert id %d", slow_h[i]);
+    if (pred_h && pred_h[i] >= n_experts) return fail(M2R2_E_SHAPE, "predicted expert id %d", pred_h[i]);
+  }
+  ExpertCachePolicy pol;
+  pol.init(n_layers, n_experts, slots);
+  int slot[kMaxTopK];
+  bool load[kMaxTopK];
+  std::vector<int> s1, e1;
+  for (int t = 0; t < n_tokens; ++t) {
+    for (int l = 0; l < n_layers; ++l) {
+      pol.use(l, slow_h + t * per_tok + l * top_k, top_k, slot, load);
+      if (prefetch && pred_h)
+        for (int lp = 2 * l + 2; lp <= 2 * l + 3 && lp < n_layers; ++lp)
+          pol.predict(lp, pred_h + t * per_tok + lp * top_k, top_k, &s1, &e1);
+    }
+    pol.end_token();
+  }
+  fill_stats(pol.counters(), out);
+  return M2R2_OK;
 }
 
 }  // extern "C"

@@ -194,13 +194,26 @@ struct GemvWave {
   u32x4_t w[NT][kChunk];
   const char* base[NT];   // this lane's 16 bytes of step 0 of each tile
   int s0, s1;
+  // segmented reduction (NT == 1): steps [k*seg_steps, (k+1)*seg_steps) come
+  // from the tile at seg[k] (the K experts of a mixture-of-experts layer)
+  const char* const* seg = nullptr;
+  int seg_steps = 0;
+
+  __device__ __forceinline__ const char* step_ptr(int t, int sj) const {
+    if (seg_steps) return seg[sj / seg_steps] + (size_t)(sj % seg_steps) * 1024 + (threadIdx.x & 63) * 16;
+    return base[t] + (size_t)sj * 1024;
+  }
+  __device__ __forceinline__ u32x4_t ld_step(int t, int sj) const {
+    // global-address-space load (the segment pointers come from LDS)
+    return __builtin_nontemporal_load((const __attribute__((address_space(1))) u32x4_t*)step_ptr(t, sj));
+  }
 
   __device__ __forceinline__ void load(int sb, u32x4_t (&dst)[NT][kChunk]) const {
 #pragma unroll
     for (int j = 0; j < kChunk; ++j) {
       const int sj = min(sb + j, s1 - 1);   // steps past the range repeat a valid address; never used
 #pragma unroll
-      for (int t = 0; t < NT; ++t) dst[t][j] = ld_stream(base[t] + (size_t)sj * 1024);
+      for (int t = 0; t < NT; ++t) dst[t][j] = ld_step(t, sj);
     }
   }
 

@@ -91,6 +91,9 @@ CONFIGS: Dict[str, ModelConfig] = {
                              wdtype="f32", kvdtype="f32", n_experts=8, top_k=2, expert_ffn=8, seed=13),
     "small_moe": ModelConfig("small_moe", n_layers=6, d_model=256, n_heads=2, head_dim=128, ffn=0, vocab=777,
                              rank=4, wdtype="bf16", kvdtype="bf16", n_experts=16, top_k=4, expert_ffn=96, seed=17),
+    "small_moe_f32": ModelConfig("small_moe_f32", n_layers=5, d_model=128, n_heads=2, head_dim=64, ffn=0,
+                                 vocab=300, rank=4, wdtype="f32", kvdtype="f32", n_experts=8, top_k=2,
+                                 expert_ffn=64, seed=19),
 }
 
 

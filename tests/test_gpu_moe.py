@@ -1,0 +1,189 @@
+"""GPU parity of the mixture-of-experts decode step (Sec. 2.3.3) through the
+C ABI against the CPU oracle: the slow row's routed experts, the fast row's
+adapter-only MLP and its expert predictions for layers 2i+2 and 2i+3, the
+hidden states, logits and cache; and the HBM expert cache's counters against
+the oracle's cache simulation replayed on the GPU's own routing trace.
+
+Sizes: a bfloat16 model with 6 layers, d 256, 2 heads x 128, 16 experts of
+width 96, top-4 (caches of 5 and 16 slots), and a float32 model with 5
+layers, d 128, 2 heads x 64, 8 experts of width 64, top-2."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import KVCache, Oracle, simulate_expert_cache
+from paper_2502_02040_amd import Model, PagedKV
+from tests.gpu_harness import Tally, shuffled_table, tol_of
+
+pytestmark = pytest.mark.gpu
+
+FIELDS = ("hits", "misses", "prefetch_issued", "prefetch_used", "prefetch_wasted", "loads", "pred_correct",
+          "pred_total")
+
+
+def topk_decidable(z, k, eps) -> bool:
+    """The k-th and (k+1)-th largest logits are further apart than the bound."""
+    s = np.sort(np.asarray(z, np.float64))[::-1]
+    return k >= len(s) or (s[k - 1] - s[k]) > 2 * eps * np.max(np.abs(s))
+
+
+class MoePair:
+    def __init__(self, name, *, slots, max_ctx=64, policy="ahead_of_time", weights=None):
+        cfg = synth.CONFIGS[name]
+        self.cfg = cfg
+        self.tol = tol_of(cfg)
+        self.w = weights if weights is not None else synth.make_weights(cfg)
+        self.model = Model(cfg, self.w, max_batch=1, max_chunk=16, max_ctx=max_ctx, expert_slots=slots)
+        self.model.moe_set_policy(policy)
+        self.kv = PagedKV(cfg, 1, max_ctx, block_size=16, block_table=shuffled_table(1, max_ctx, 16, 5))
+        self.orc = Oracle(cfg, self.w)
+        self.cache = KVCache(cfg, max_ctx)
+        self.dev = torch.device("cuda")
+        N, K = cfg.n_layers, cfg.top_k
+        self.slow = torch.zeros(N * K, dtype=torch.int32, device=self.dev)
+        self.pred = torch.zeros(N * K, dtype=torch.int32, device=self.dev)
+
+    def prefill(self, prompt, t: Tally):
+        """Slow-only decode steps on the GPU, the chunked slow forward in the oracle."""
+        ref = self.orc.slow_chunk(list(prompt), 0, self.cache)
+        pos = torch.zeros(1, dtype=torch.int32, device=self.dev)
+        nxt = torch.zeros(1, dtype=torch.int32, device=self.dev)
+        for i, tok in enumerate(prompt):
+            tk = torch.tensor([tok], dtype=torch.int32, device=self.dev)
+            self.model.decode_step(tk, pos, self.kv.desc(), dual=False, next_token=nxt, advance=True)
+            torch.cuda.synchronize()
+            t.token(int(nxt.item()), ref[i], self.tol, f"prefill row {i}")
+        for l in range(self.cfg.n_layers):
+            K, V = self.kv.read(0, l, 0, len(prompt))
+            t.rel(K, self.cache.K[l][:len(prompt)], self.tol, f"prefill K layer {l}")
+            t.rel(V, self.cache.V[l][:len(prompt)], self.tol, f"prefill V layer {l}")
+        return int(nxt.item())
+
+    def run(self, n_steps, *, mode="observe", gates=(), tau=2.0, prompt_len=12, check=True):
+        cfg, N, K = self.cfg, self.cfg.n_layers, self.cfg.top_k
+        t = Tally()
+        prompt = list(synth.prompt_ids(cfg, prompt_len))
+        tok = self.prefill(prompt, t)
+        self.model.moe_reset()
+        dev = self.dev
+        tok_d = torch.tensor([tok], dtype=torch.int32, device=dev)
+        pos_d = torch.tensor([prompt_len], dtype=torch.int32, device=dev)
+        nxt = torch.zeros(1, dtype=torch.int32, device=dev)
+        exb = torch.zeros(1, dtype=torch.int32, device=dev)
+        sig = torch.zeros(N, dtype=torch.float32, device=dev)
+        logits = torch.zeros(cfg.vocab, dtype=torch.float32, device=dev)
+        h_out = torch.zeros(cfg.d_model, dtype=torch.float32, device=dev)
+        p_out = torch.zeros(cfg.d_model, dtype=torch.float32, device=dev)
+        slow_tr, pred_tr, outs = [], [], []
+        for step in range(n_steps):
+            pos = prompt_len + step
+            self.model.decode_step(tok_d, pos_d, self.kv.desc(), gates=gates, tau=tau, mode=mode, next_token=nxt,
+                                   exit_boundary=exb, signal=sig, logits=logits, h_out=h_out, p_out=p_out,
+                                   advance=True, slow_experts=self.slow, pred_experts=self.pred)
+            torch.cuda.synchronize()
+            gs = self.slow.cpu().numpy().reshape(N, K)
+            gp = self.pred.cpu().numpy().reshape(N, K)
+            slow_tr.append(gs)
+            pred_tr.append(gp)
+            outs.append(logits.cpu().numpy().copy())
+            if not check:
+                tok_d.copy_(nxt)
+                continue
+            r = self.orc.decode_step(int(tok_d.item()), pos, self.cache, gates=gates, tau=tau, mode=mode)
+            # expert choices: compared where the router margin decides them
+            ran = r.slow_experts.shape[0]
+            for l in range(ran):
+                same = set(gs[l]) == set(r.slow_experts[l])
+                if topk_decidable(r.router_logits[l], K, self.tol):
+                    t.compared += 1
+                    assert same, f"step {step} layer {l}: slow experts"
+                else:
+                    t.skipped += 1
+                    if not same:   # a near tie went the other way: the two sides now differ
+                        return t, slow_tr, pred_tr, outs
+            assert np.all(gs[ran:] == -1), f"step {step}: layers after the exit report experts"
+            for l in range(N):
+                if r.pred_experts[l][0] < 0:
+                    assert np.all(gp[l] == -1), f"step {step} layer {l}: unexpected prediction"
+                elif topk_decidable(r.pred_logits[l], K, self.tol):
+                    t.compared += 1
+                    assert set(gp[l]) == set(r.pred_experts[l]), f"step {step} layer {l}: predicted experts"
+                else:
+                    t.skipped += 1
+            ambiguous = any(abs(r.signal[b - 1] - tau) <= self.tol for b in gates if b - 1 < N)
+            if ambiguous:
+                t.skipped += 1
+                break
+            assert int(exb.item()) == r.exit_boundary
+            t.rel(logits.cpu().numpy(), r.logits, self.tol, f"step {step} logits")
+            t.rel(h_out.cpu().numpy(), r.h, self.tol, f"step {step} h")
+            t.rel(p_out.cpu().numpy(), r.p, self.tol, f"step {step} p")
+            got_sig = sig.cpu().numpy()
+            lr = [l for l in range(N) if not (mode == "exit" and r.exit_boundary < N and l >= r.exit_boundary)]
+            assert np.max(np.abs(got_sig[lr] - r.signal[lr])) <= self.tol, f"step {step} signal"
+            t.token(int(nxt.item()), r.logits, self.tol, f"step {step} token")
+            for l in range(N):
+                K_, V_ = self.kv.read(0, l, pos, pos + 1)
+                t.rel(K_, self.cache.K[l][pos:pos + 1], self.tol, f"step {step} K layer {l}")
+                t.rel(V_, self.cache.V[l][pos:pos + 1], self.tol, f"step {step} V layer {l}")
+            tok_d.copy_(nxt)
+        return t, slow_tr, pred_tr, outs
+
+
+@pytest.mark.parametrize("name,slots", [("small_moe", 5), ("small_moe", 16), ("small_moe_f32", 3)])
+def test_moe_dual_step_observe(name, slots):
+    cfg = synth.CONFIGS[name]
+    p = MoePair(name, slots=slots)
+    t, *_ = p.run(10, mode="observe", gates=list(range(1, cfg.n_layers)), tau=0.9)
+    assert t.compared >= 12
+
+
+def test_moe_exit_mode_fills_skipped_layers():
+    p = MoePair("small_moe_f32", slots=4)
+    t, slow_tr, _, _ = p.run(6, mode="exit", gates=[2], tau=-1.0)
+    assert t.compared >= 4
+    assert all(np.all(s[2:] == -1) for s in slow_tr)
+
+
+@pytest.mark.parametrize("policy", ["ahead_of_time", "on_demand"])
+def test_expert_cache_counters_match_simulation(policy):
+    """The runtime's hits, misses, prefetches and prediction accuracy equal
+    the oracle's cache simulation replayed on the GPU's own routing trace."""
+    p = MoePair("small_moe", slots=5, policy=policy)
+    _, slow_tr, pred_tr, _ = p.run(16, check=False)
+    st = simulate_expert_cache(np.stack(slow_tr), np.stack(pred_tr), p.cfg.n_experts, 5,
+                               prefetch=policy == "ahead_of_time")
+    got = p.model.moe_stats()
+    for f in FIELDS:
+        assert got[f] == getattr(st, f), f"{f}: {got[f]} != {getattr(st, f)}"
+    assert got["layer_misses"] == list(st.per_layer_misses)
+    assert got["h2d_bytes"] == got["loads"] * p.model.expert_bytes
+    if policy == "ahead_of_time":
+        assert got["prefetch_issued"] > 0
+
+
+def test_small_cache_gives_the_same_outputs_as_all_resident():
+    """Copies into a 4-slot cache deliver the same expert weights as an
+    all-resident cache: logits and routing are bitwise equal."""
+    w = synth.make_weights(synth.CONFIGS["small_moe"])
+    a = MoePair("small_moe", slots=4, weights=w)
+    _, sa, pa, oa = a.run(8, check=False)
+    b = MoePair("small_moe", slots=16, weights=w)
+    _, sb, pb, ob = b.run(8, check=False)
+    assert a.model.moe_stats()["misses"] > 0 and b.model.moe_stats()["misses"] == 0
+    for i in range(8):
+        np.testing.assert_array_equal(sa[i], sb[i])
+        np.testing.assert_array_equal(pa[i], pb[i])
+        np.testing.assert_array_equal(oa[i], ob[i])
+
+
+def test_external_prefetch_makes_experts_resident():
+    p = MoePair("small_moe", slots=4, policy="on_demand")
+    p.model.moe_reset()
+    p.model.prefetch_experts(3, [9, 10, 11])
+    torch.cuda.synchronize()
+    st = p.model.moe_stats()
+    assert st["prefetch_issued"] == 3 and st["loads"] == 3
+    p.model.prefetch_experts(3, [9, 10, 11], priority=True)   # already resident: refreshed, no copy
+    assert p.model.moe_stats()["loads"] == 3
