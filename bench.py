@@ -1,17 +1,30 @@
 #!/usr/bin/env python3
-"""Throughput of the M2R2 dual-stream decode step on one MI355X.
+"""Throughput of the M2R2 decode path on one MI355X.
 
-Workload (default): a Phi-3-mini-shaped dense decoder (32 layers, d_model 3072,
-32 heads x 96, SwiGLU 8192, vocab 32064), bfloat16 weights and KV cache,
-accelerator adapters of rank 16 on all seven projections, batch 1.  Weights
-are seeded N(0, 0.02) (norm gains 1.0); a 1024-token random prompt is
-prefilled through the chunked slow forward.  One step = one dual-stream decode
-step: embedding, 32 layers carrying the slow and the fast row (shared paged
-KV cache, exit signal at every layer, OBSERVE-mode gates at every interior
-boundary, tau 0.9), final norm, LM head and argmax.  The step is captured in a
-HIP graph and replayed; inputs are resident in HBM before timing starts.
+Default workload (``--mode dense``): a Phi-3-mini-shaped dense decoder (32
+layers, d_model 3072, 32 heads x 96, SwiGLU 8192, vocab 32064), bfloat16
+weights and KV cache, accelerator adapters of rank 16 on all seven
+projections, batch 1.  Weights are seeded N(0, 0.02) (norm gains 1.0); a
+1024-token random prompt is prefilled through the chunked slow forward.  One
+step = one dual-stream decode step: embedding, 32 layers carrying the slow
+and the fast row (shared paged KV cache, exit signal at every layer,
+OBSERVE-mode gates at every interior boundary, tau 0.9), final norm, LM head
+and argmax.  The step is captured in a HIP graph and replayed; inputs are
+resident in HBM before timing starts.  Prints one JSON line.
 
-Prints one JSON line (see the repository's design notes for every field).
+Other measurements (one JSON line each, same fields where they apply):
+  --mode batch  the same model, 8 sequences with 4096-token paged contexts
+                (block 16, shuffled block table, seeded synthetic cache content)
+  --mode spec   self-speculative decoding: drafts of 4 tokens from the fast
+                stream exiting at layer 8, verified as 5-token chunks on the
+                slow stream; 512 tokens from a 128-token prompt, against plain
+                greedy decoding on the same kernels (and the token streams are
+                checked to be equal)
+  --mode moe    OLMoE-shaped mixture of experts (16 layers, d 2048, 64 experts
+                of width 1024, top 8, vocab 50304) with every expert in pinned
+                host memory and a 16-slot HBM cache per layer: on-demand LRU
+                (slow stream alone), M2R2 ahead-of-time prefetch from the fast
+                stream's predictions, and an all-resident cache
 """
 from __future__ import annotations
 
@@ -24,30 +37,67 @@ import time
 import numpy as np
 
 HBM_PEAK_GBS = 8000.0
+METRIC = "decode tokens/s at batch 1 + achieved HBM GB/s of dual-stream layer step"
 
 
-def step_bytes(cfg, ctx: float, dual: bool = True) -> float:
-    """Algorithmic HBM bytes of one decode step at context length ctx."""
-    d, q, F, V, r, L = cfg.d_model, cfg.qdim, cfg.ffn, cfg.vocab, cfg.rank, cfg.n_layers
+# ----------------------------------------------------------------------------
+# algorithmic bytes
+# ----------------------------------------------------------------------------
+
+def layer_weight_bytes(cfg, dual: bool = True) -> float:
+    d, q, F, r = cfg.d_model, cfg.qdim, cfg.ffn, cfg.rank
     ew = 2 if cfg.wdtype == "bf16" else 4
-    ek = 2 if cfg.kvdtype == "bf16" else 4
     mats = (3 * q * d + d * q + 2 * F * d + d * F) * ew
     adapters = r * ((d + q) * 3 + (q + d) + (d + F) * 2 + (F + d)) * ew if dual else 0
-    norms = 2 * d * 4
-    kv = (ctx * 2 * q + 2 * q) * ek
-    per_layer = mats + adapters + norms + kv
-    return L * per_layer + V * d * ew + d * 4 + d * ew
+    return mats + adapters + 2 * d * 4
 
 
-def gateup_bytes(cfg, dual: bool = True) -> float:
+def step_bytes(cfg, ctx: float, dual: bool = True, batch: int = 1) -> float:
+    """Algorithmic HBM bytes of one decode step: every weight once, the KV
+    cache of every sequence once (context ctx each), the new KV entries."""
+    d, q, V, L = cfg.d_model, cfg.qdim, cfg.vocab, cfg.n_layers
+    ew = 2 if cfg.wdtype == "bf16" else 4
+    ek = 2 if cfg.kvdtype == "bf16" else 4
+    kv = batch * (ctx * 2 * q + 2 * q) * ek
+    return L * (layer_weight_bytes(cfg, dual) + kv) + V * d * ew + d * 4 + batch * d * ew
+
+
+def gateup_bytes(cfg, rows: int, fast_rows: int) -> float:
     """Algorithmic bytes of one gate/up launch: both weight matrices, the
     adapter factors it reads (B_g, B_u, and the columns of A_d for the down
-    adapter's partial sums), the input rows and the activation it writes."""
+    adapter's partial sums) when fast rows are present, the input rows and the
+    activations it writes."""
     d, F, r = cfg.d_model, cfg.ffn, cfg.rank
     ew = 2 if cfg.wdtype == "bf16" else 4
-    rows = 2 if dual else 1
-    return 2 * F * d * ew + (3 * F * r * ew if dual else 0) + rows * (d * 4 + F * 4) + d * 4
+    return 2 * F * d * ew + (3 * F * r * ew if fast_rows else 0) + rows * (d * 4 + F * 4) + d * 4
 
+
+def attn_bytes(cfg, batch: int, ctx: float) -> float:
+    """Algorithmic bytes of one attention launch: the cached keys and values
+    of every sequence plus the new entries."""
+    ek = 2 if cfg.kvdtype == "bf16" else 4
+    return batch * (ctx + 1) * 2 * cfg.qdim * ek
+
+
+def expert_gateup_bytes(cfg) -> float:
+    ew = 2 if cfg.wdtype == "bf16" else 4
+    return cfg.top_k * 2 * cfg.expert_ffn * cfg.d_model * ew + cfg.d_model * 4 * 2 + cfg.top_k * cfg.expert_ffn * 4
+
+
+def moe_token_bytes(cfg, ctx: float) -> float:
+    """HBM bytes of one MoE decode token with every chosen expert resident:
+    attention weights, KV, the router, the k experts, the LM head."""
+    d, q, L, r = cfg.d_model, cfg.qdim, cfg.n_layers, cfg.rank
+    ew = 2 if cfg.wdtype == "bf16" else 4
+    ek = 2 if cfg.kvdtype == "bf16" else 4
+    attn = (3 * q * d + d * q) * ew + (ctx * 2 * q + 2 * q) * ek
+    experts = cfg.top_k * 3 * cfg.expert_ffn * d * ew + cfg.n_experts * d * ew
+    return L * (attn + experts + 2 * d * 4) + cfg.vocab * d * ew
+
+
+# ----------------------------------------------------------------------------
+# CPU baseline: the oracle timed on the host cores
+# ----------------------------------------------------------------------------
 
 def cpu_baseline(cfg, weights, ctx: int, budget_s: float):
     """Time the CPU oracle (float32) on the same decode step at the same
@@ -76,22 +126,66 @@ def cpu_baseline(cfg, weights, ctx: int, budget_s: float):
                        f"(synthetic cache content), {el:.1f} s")
 
 
-def main() -> int:
-    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=256)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", default="phi3")
-    ap.add_argument("--ctx", type=int, default=1024)
-    ap.add_argument("--single", action="store_true", help="slow row only (plain decoding on the same kernels)")
-    ap.add_argument("--kernel-reps", type=int, default=20, help="graph replays of the instrumented step")
-    ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of CPU oracle timing (0: skip)")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU: --gpus {args.gpus} is not supported by this build "
-              f"(the multi-GPU sharding is a design note, not an implementation)", file=sys.stderr)
-        return 2
+# ----------------------------------------------------------------------------
+# shared helpers
+# ----------------------------------------------------------------------------
 
+def _progress(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def _line(**kw):
+    base = {"metric": METRIC, "n_gpus": 1, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "data": "synthetic"}
+    base.update(kw)
+    print(json.dumps(base), flush=True)
+
+
+def _prefill(model, prompt, pos, desc, dev):
+    """Chunked slow forward of the prompt (chunks of 16); returns the first token."""
+    import torch
+    targets = torch.zeros(16, dtype=torch.int32, device=dev)
+    chunk = torch.tensor(np.asarray(prompt, np.int32), dtype=torch.int32, device=dev)
+    n_all = len(prompt)
+    for c0 in range(0, n_all, 16):
+        n = min(16, n_all - c0)
+        model.verify(chunk[c0:c0 + n], n, pos, desc, targets)
+    torch.cuda.synchronize()
+    i = (n_all - 1) % 16
+    return targets[i:i + 1].clone()
+
+
+def _time_graph(g, stream, steps):
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        e0.record(stream)
+        for _ in range(steps):
+            g.replay()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1)
+
+
+def _kernel_avg_ms(model, kernel, stream, fn, reps):
+    """Average duration of one kernel class over `reps` direct calls of fn,
+    from HIP events recorded on the launch stream around each launch."""
+    import torch
+    model.timing_enable(kernel)
+    with torch.cuda.stream(stream):
+        for _ in range(reps):
+            fn()
+    k_ms, k_n = model.timing_read()
+    model.timing_enable(None)
+    return k_ms / max(k_n, 1), k_n
+
+
+# ----------------------------------------------------------------------------
+# modes
+# ----------------------------------------------------------------------------
+
+def run_dense(args) -> int:
     import torch
     import synth
     from paper_2502_02040_amd import Model, PagedKV
@@ -99,26 +193,17 @@ def main() -> int:
     cfg = synth.CONFIGS[args.config]
     dual = not args.single
     dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
     t_setup = time.perf_counter()
     weights = synth.make_weights(cfg)
     n_inst = 2 * args.kernel_reps
     max_ctx = args.ctx + args.warmup + args.steps + n_inst + 32
     model = Model(cfg, weights, max_batch=1, max_chunk=16, max_ctx=max_ctx)
+    _progress(f"dense: model ready after {time.perf_counter() - t_setup:.1f} s")
     bps = (max_ctx + 15) // 16
     kv = PagedKV(cfg, 1, max_ctx, block_size=16, block_table=synth.block_table(1, bps, seed=cfg.seed))
     desc = kv.desc()
-
-    # prefill the prompt through the chunked slow forward
-    prompt = synth.prompt_ids(cfg, args.ctx)
     pos = torch.zeros(1, dtype=torch.int32, device=dev)
-    targets = torch.zeros(16, dtype=torch.int32, device=dev)
-    chunk = torch.tensor(prompt, dtype=torch.int32, device=dev)
-    for c0 in range(0, args.ctx, 16):
-        n = min(16, args.ctx - c0)
-        model.verify(chunk[c0:c0 + n], n, pos, desc, targets)
-    torch.cuda.synchronize()
-    tok = targets[(args.ctx - 1) % 16:(args.ctx - 1) % 16 + 1].clone()
+    tok = _prefill(model, synth.prompt_ids(cfg, args.ctx), pos, desc, dev)
 
     N = cfg.n_layers
     gates = list(range(1, N)) if dual else []
@@ -141,72 +226,424 @@ def main() -> int:
     setup_s = time.perf_counter() - t_setup
 
     ctx0 = int(pos.item())
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    with torch.cuda.stream(stream):
-        e0.record(stream)
-        for _ in range(args.steps):
-            g.replay()
-        e1.record(stream)
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1)
+    ms = _time_graph(g, stream, args.steps)
     ms_step = ms / args.steps
     ctx_mean = ctx0 + (args.steps - 1) / 2.0
 
-    # dominant kernel (gate/up projection): HIP events recorded on the launch
-    # stream around each of its launches in further steps of the same decode
-    # (launched directly: HIP does not time events recorded inside a graph)
-    model.timing_enable("gateup")
-    with torch.cuda.stream(stream):
-        for _ in range(args.kernel_reps):
-            step()
-    k_ms, k_n = model.timing_read()
-    model.timing_enable(None)
+    # dominant kernel (gate/up projection) timed in further direct steps
+    k_avg_ms, k_n = _kernel_avg_ms(model, "gateup", stream, step, args.kernel_reps)
     errs = model.device_errors()
     if errs:
         print(f"device error bits {errs}", file=sys.stderr)
         return 1
-    k_avg_ms = k_ms / max(k_n, 1)
-    kb = gateup_bytes(cfg, dual)
+    kb = gateup_bytes(cfg, 2 if dual else 1, 1 if dual else 0)
     achieved = kb / (k_avg_ms * 1e-3) / 1e9
     sb = step_bytes(cfg, ctx_mean, dual)
     step_gbs = sb / (ms_step * 1e-3) / 1e9
 
-    cpu = None
-    if args.cpu_budget > 0:
-        cpu = cpu_baseline(cfg, weights, args.ctx, args.cpu_budget)
-
-    line = {
-        "metric": "decode tokens/s at batch 1 + achieved HBM GB/s of dual-stream layer step",
-        "value": round(1000.0 / ms_step, 3),
-        "unit": "tokens/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16" if cfg.wdtype == "bf16" else "f32",
-        "data": "synthetic",
-        "config": {"workload": f"{'dual' if dual else 'single'}-stream decode step, {cfg.name}-shaped "
-                               f"{cfg.n_layers}L d{cfg.d_model} {cfg.n_heads}x{cfg.head_dim} ffn{cfg.ffn} "
-                               f"vocab{cfg.vocab} rank{cfg.rank}, {cfg.wdtype} weights/KV, batch 1, "
-                               f"KV context {args.ctx} (+{args.warmup + args.steps} decoded), HIP graph replay",
-                   "batch": 1, "kv_context": args.ctx, "dual_stream": dual},
-        "step_hbm_gbs": round(step_gbs, 1),
-        "step_bytes": int(sb),
-        "step_roofline_frac": round(step_gbs / HBM_PEAK_GBS, 4),
-        "roofline": {"bound": "hbm", "kernel": "gate/up projection (k_gateup)",
-                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                     "avg_kernel_us": round(k_avg_ms * 1e3, 3), "bytes_per_launch": int(kb),
-                     "launches_timed": k_n},
-        "cpu_baseline": cpu,
-        "setup_s": round(setup_s, 1),
-    }
-    print(json.dumps(line), flush=True)
+    cpu = cpu_baseline(cfg, weights, args.ctx, args.cpu_budget) if args.cpu_budget > 0 else None
+    _line(value=round(1000.0 / ms_step, 3), unit="tokens/s", steps=args.steps, warmup=args.warmup,
+          ms_per_step=round(ms_step, 5), dtype="bf16" if cfg.wdtype == "bf16" else "f32",
+          config={"workload": f"{'dual' if dual else 'single'}-stream decode step, {cfg.name}-shaped "
+                              f"{cfg.n_layers}L d{cfg.d_model} {cfg.n_heads}x{cfg.head_dim} ffn{cfg.ffn} "
+                              f"vocab{cfg.vocab} rank{cfg.rank}, {cfg.wdtype} weights/KV, batch 1, "
+                              f"KV context {args.ctx} (+{args.warmup + args.steps} decoded), HIP graph replay",
+                  "batch": 1, "kv_context": args.ctx, "dual_stream": dual},
+          step_hbm_gbs=round(step_gbs, 1), step_bytes=int(sb), step_roofline_frac=round(step_gbs / HBM_PEAK_GBS, 4),
+          roofline={"bound": "hbm", "kernel": "gate/up projection (k_gateup)", "achieved": round(achieved, 1),
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "traffic": None, "avg_kernel_us": round(k_avg_ms * 1e3, 3), "bytes_per_launch": int(kb),
+                    "launches_timed": k_n},
+          cpu_baseline=cpu, setup_s=round(setup_s, 1))
     return 0
+
+
+def run_batch(args) -> int:
+    """8 sequences, 4096-token contexts in a paged cache with seeded content."""
+    import torch
+    import synth
+    from paper_2502_02040_amd import Model, PagedKV
+
+    cfg = synth.CONFIGS[args.config]
+    B, ctx = args.batch, args.ctx
+    dual = not args.single
+    dev = torch.device("cuda:0")
+    t_setup = time.perf_counter()
+    weights = synth.make_weights(cfg)
+    max_ctx = ctx + args.warmup + args.steps + 2 * args.kernel_reps + 16
+    model = Model(cfg, weights, max_batch=B, max_chunk=16, max_ctx=max_ctx)
+    del weights
+    bps = (max_ctx + 15) // 16
+    kv = PagedKV(cfg, B, max_ctx, block_size=16, block_table=synth.block_table(B, bps, seed=3))
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(cfg.seed)
+    _progress("batch: model ready, filling the cache")
+    for t in (kv.k, kv.v):   # synthetic N(0, 1) cache content, every position
+        t.copy_(torch.randn(t.shape, generator=gen, device=dev, dtype=torch.float32).to(t.dtype))
+    kv.seq_lens.fill_(ctx)
+    pos = torch.full((B,), ctx, dtype=torch.int32, device=dev)
+    tok = torch.tensor(synth.prompt_ids(cfg, B, stream="batch"), dtype=torch.int32, device=dev)
+    desc = kv.desc()
+    N = cfg.n_layers
+    gates = list(range(1, N)) if dual else []
+    sig = torch.zeros(B * N, dtype=torch.float32, device=dev)
+    exb = torch.zeros(B, dtype=torch.int32, device=dev)
+    stream = torch.cuda.Stream()
+
+    def step():
+        model.decode_step(tok, pos, desc, dual=dual, gates=gates, tau=0.9, mode="observe", next_token=tok,
+                          exit_boundary=exb if dual else None, signal=sig if dual else None, advance=True)
+
+    with torch.cuda.stream(stream):
+        for _ in range(args.warmup):
+            step()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        step()
+    torch.cuda.synchronize()
+    setup_s = time.perf_counter() - t_setup
+    ctx0 = int(pos[0].item())
+    ms = _time_graph(g, stream, args.steps)
+    ms_step = ms / args.steps
+    ctx_mean = ctx0 + (args.steps - 1) / 2.0
+    k_avg_ms, k_n = _kernel_avg_ms(model, "attn", stream, step, args.kernel_reps)
+    errs = model.device_errors()
+    if errs:
+        print(f"device error bits {errs}", file=sys.stderr)
+        return 1
+    ab = attn_bytes(cfg, B, ctx0 + args.steps + args.kernel_reps / 2)
+    achieved = ab / (k_avg_ms * 1e-3) / 1e9
+    sb = step_bytes(cfg, ctx_mean, dual, batch=B)
+    step_gbs = sb / (ms_step * 1e-3) / 1e9
+    _line(metric="batched decode tokens/s (aggregate) + achieved HBM GB/s of the dual-stream step",
+          value=round(B * 1000.0 / ms_step, 3), unit="tokens/s", steps=args.steps, warmup=args.warmup,
+          ms_per_step=round(ms_step, 5), dtype="bf16" if cfg.wdtype == "bf16" else "f32",
+          config={"workload": f"{'dual' if dual else 'single'}-stream decode step, {cfg.name}-shaped model, batch {B}, "
+                              f"paged KV context {ctx} per sequence (block 16, shuffled table, seeded N(0,1) "
+                              f"content), HIP graph replay", "batch": B, "kv_context": ctx, "dual_stream": dual},
+          step_hbm_gbs=round(step_gbs, 1), step_bytes=int(sb), step_roofline_frac=round(step_gbs / HBM_PEAK_GBS, 4),
+          roofline={"bound": "hbm", "kernel": "split-context attention (k_attn)", "achieved": round(achieved, 1),
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "traffic": None, "avg_kernel_us": round(k_avg_ms * 1e3, 3), "bytes_per_launch": int(ab),
+                    "launches_timed": k_n},
+          cpu_baseline=None, setup_s=round(setup_s, 1))
+    return 0
+
+
+def run_spec(args) -> int:
+    """Draft + verify against plain greedy decoding on the same kernels."""
+    import torch
+    import synth
+    from paper_2502_02040_amd import Model, PagedKV
+
+    base = synth.CONFIGS[args.config]
+    gamma, kL, n_new, plen = args.gamma, args.exit_layer, args.new_tokens, args.prompt
+    dev = torch.device("cuda:0")
+    results = []
+    for lam in args.decay:
+        _progress(f"spec: decay {lam}")
+        cfg = base
+        weights = synth.make_weights(cfg, decay=None if lam == 1.0 else (kL, lam))
+        max_ctx = plen + n_new + 12 * (gamma + 1) + 16
+        model = Model(cfg, weights, max_batch=1, max_chunk=16, max_ctx=max_ctx)
+        del weights
+        prompt = synth.prompt_ids(cfg, plen)
+        stream = torch.cuda.Stream()
+
+        # plain greedy: slow-only decode steps, one graph per step
+        kv = PagedKV(cfg, 1, max_ctx, block_size=16)
+        desc = kv.desc()
+        pos = torch.zeros(1, dtype=torch.int32, device=dev)
+        tok = _prefill(model, prompt, pos, desc, dev)
+        first = int(tok.item())
+        hist = torch.zeros(n_new + 8, dtype=torch.int32, device=dev)
+        hist[0] = first
+        k_i = torch.zeros(1, dtype=torch.int64, device=dev)
+
+        def greedy_step():
+            model.decode_step(tok, pos, desc, dual=False, next_token=tok, advance=True)
+
+        with torch.cuda.stream(stream):
+            greedy_step()   # warm-up (position plen)
+        torch.cuda.synchronize()
+        pos.fill_(plen)
+        kv.seq_lens.fill_(plen)
+        tok.fill_(first)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            greedy_step()
+        torch.cuda.synchronize()
+        pos.fill_(plen)
+        kv.seq_lens.fill_(plen)
+        tok.fill_(first)
+        greedy_tokens = [first]
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        out_buf = torch.zeros(n_new, dtype=torch.int32, device=dev)
+        with torch.cuda.stream(stream):
+            e0.record(stream)
+            for i in range(n_new - 1):
+                g.replay()
+                out_buf[i:i + 1].copy_(tok, non_blocking=True)
+            e1.record(stream)
+        torch.cuda.synchronize()
+        greedy_ms = e0.elapsed_time(e1)
+        greedy_tokens += out_buf[:n_new - 1].cpu().tolist()
+        greedy_tps = (n_new - 1) / (greedy_ms * 1e-3)
+
+        _progress(f"spec: greedy {greedy_tps:.1f} tokens/s")
+        # speculative: a round = gamma draft passes + one verify of gamma+1 rows
+        kv2 = PagedKV(cfg, 1, max_ctx, block_size=16)
+        desc2 = kv2.desc()
+        pos2 = torch.zeros(1, dtype=torch.int32, device=dev)
+        t2 = _prefill(model, prompt, pos2, desc2, dev)
+        assert int(t2.item()) == first
+        chunk = torch.zeros(gamma + 1, dtype=torch.int32, device=dev)
+        targets = torch.zeros(gamma + 1, dtype=torch.int32, device=dev)
+        n_acc = torch.zeros(1, dtype=torch.int32, device=dev)
+        max_rounds = n_new + 1
+        rec_t = torch.zeros((max_rounds, gamma + 1), dtype=torch.int32, device=dev)
+        rec_n = torch.zeros(max_rounds, dtype=torch.int32, device=dev)
+
+        def spec_round():
+            model.draft(chunk, pos2, kL, gamma, desc2, chunk[1:])
+            model.verify(chunk, gamma + 1, pos2, desc2, targets, n_acc, chunk[0:1])
+
+        chunk[0] = first
+        with torch.cuda.stream(stream):
+            spec_round()   # warm-up, then restart from the prompt
+        torch.cuda.synchronize()
+        pos2.fill_(plen)
+        kv2.seq_lens.fill_(plen)
+        chunk.zero_()
+        chunk[0] = first
+        gs = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gs, stream=stream):
+            spec_round()
+        torch.cuda.synchronize()
+        pos2.fill_(plen)
+        kv2.seq_lens.fill_(plen)
+        chunk.zero_()
+        chunk[0] = first
+        # rounds are replayed in groups; the host checks the count between groups
+        produced, rounds = 1, 0
+        e0.record(stream)
+        with torch.cuda.stream(stream):
+            while produced < n_new:
+                grp = max(1, min(32, (n_new - produced + gamma) // (gamma + 1)))
+                for _ in range(grp):
+                    gs.replay()
+                    rec_t[rounds].copy_(targets, non_blocking=True)
+                    rec_n[rounds:rounds + 1].copy_(n_acc, non_blocking=True)
+                    rounds += 1
+                produced = 1 + int((rec_n[:rounds] + 1).sum().item())
+        e1.record(stream)
+        torch.cuda.synchronize()
+        spec_ms = e0.elapsed_time(e1)
+        rt, rn = rec_t[:rounds].cpu().numpy(), rec_n[:rounds].cpu().numpy()
+        spec_tokens = [first]
+        for r in range(rounds):
+            spec_tokens += rt[r, :rn[r] + 1].tolist()
+        spec_tokens = spec_tokens[:n_new]
+        alpha = float(rn.sum()) / (rounds * gamma)
+        spec_tps = (produced - 1) / (spec_ms * 1e-3)   # tokens after the first, as for greedy
+        # model speedup from the measured pass times
+        kv3 = PagedKV(cfg, 1, max_ctx, block_size=16)
+        d3 = kv3.desc()
+        p3 = torch.zeros(1, dtype=torch.int32, device=dev)
+        _prefill(model, prompt, p3, d3, dev)
+        ch3 = torch.zeros(gamma + 1, dtype=torch.int32, device=dev)
+        gd, gv = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gd, stream=stream):
+            model.draft(ch3, p3, kL, gamma, d3, ch3[1:])
+        with torch.cuda.graph(gv, stream=stream):
+            model.verify(ch3, gamma + 1, p3, d3, targets)   # prefill form: keeps the position fixed below
+        torch.cuda.synchronize()
+        t_draft = _time_graph(gd, stream, 20) / 20 / gamma
+        p3.fill_(plen)
+        t_verify = _time_graph(gv, stream, 10) / 10   # each replay advances the context by gamma+1
+        t_step = greedy_ms / (n_new - 1)
+        E = sum(alpha ** i for i in range(gamma + 1))
+        s_model = E * t_step / (gamma * t_draft + t_verify)
+        results.append(dict(decay=lam, alpha=round(alpha, 4), rounds=rounds, tokens=len(spec_tokens),
+                            lossless=spec_tokens == greedy_tokens[:len(spec_tokens)],
+                            greedy_tps=round(greedy_tps, 2), spec_tps=round(spec_tps, 2),
+                            speedup=round(spec_tps / greedy_tps, 4), model_speedup=round(s_model, 4),
+                            ms_draft_token=round(t_draft, 4), ms_verify=round(t_verify, 4),
+                            ms_greedy_step=round(t_step, 4)))
+        del model, kv, kv2, kv3
+        torch.cuda.empty_cache()
+        if not results[-1]["lossless"]:
+            print(f"speculative output differs from greedy at decay {lam}", file=sys.stderr)
+    main_r = results[0]
+    _line(metric="self-speculative decode tokens/s at batch 1 (draft from the fast stream, verify on the slow stream)",
+          value=main_r["spec_tps"], unit="tokens/s", steps=main_r["rounds"], warmup=1,
+          ms_per_step=round(1000.0 / main_r["spec_tps"], 5), dtype="bf16" if base.wdtype == "bf16" else "f32",
+          config={"workload": f"{base.name}-shaped model, prompt {plen}, {n_new} generated tokens, gamma {gamma}, "
+                              f"draft exit layer {kL}; rounds captured as HIP graphs",
+                  "batch": 1, "gamma": gamma, "exit_layer": kL},
+          baseline_greedy_tps=main_r["greedy_tps"], results=results, roofline=None, cpu_baseline=None)
+    return 0 if all(r["lossless"] for r in results) else 1
+
+
+def run_moe(args) -> int:
+    """OLMoE-shaped model with its experts in pinned host memory."""
+    import torch
+    import synth
+    from paper_2502_02040_amd import Model, PagedKV
+    from paper_2502_02040_amd.binding import pack_expert_store
+
+    cfg = synth.CONFIGS["olmoe"]
+    dev = torch.device("cuda:0")
+    t_setup = time.perf_counter()
+    names = [n for n, _, _ in synth.tensor_specs(cfg) if ".E" not in n]
+    spec = {n: (s, k) for n, s, k in synth.tensor_specs(cfg)}
+
+    def expert_source(l, e):
+        return tuple(synth.make_tensor(cfg, f"L{l}.E{e}.{m}", *spec[f"L{l}.E{e}.{m}"]) for m in ("wg", "wu", "wd"))
+
+    store = pack_expert_store(cfg, expert_source, threads=16)
+    gen_s = time.perf_counter() - t_setup
+    _progress(f"moe: {cfg.n_layers * cfg.n_experts} experts packed into pinned host memory in {gen_s:.1f} s")
+    plen, steps, C = args.prompt, args.steps, args.slots
+    max_ctx = plen + steps + args.warmup + 16
+    prompt = synth.prompt_ids(cfg, plen)
+    runs = []
+    for label, variant, slots, policy, dual in (
+            ("on-demand LRU, slow stream alone", {}, C, "on_demand", False),
+            ("M2R2 ahead-of-time prefetch", {}, C, "ahead_of_time", True),
+            ("all experts resident", {}, cfg.n_experts, "on_demand", True),
+            ("M2R2 ahead-of-time, router-coherent variant", {"router_coherent": True}, C, "ahead_of_time", True),
+            ("on-demand LRU, router-coherent variant", {"router_coherent": True}, C, "on_demand", False)):
+        _progress(f"moe: {label}")
+        w = synth.make_weights(cfg, names=names, **variant)
+        model = Model(cfg, w, max_batch=1, max_chunk=16, max_ctx=max_ctx, expert_slots=slots, expert_store=store)
+        del w
+        model.moe_set_policy(policy)
+        kv = PagedKV(cfg, 1, max_ctx, block_size=16)
+        desc = kv.desc()
+        pos = torch.zeros(1, dtype=torch.int32, device=dev)
+        nxt = torch.zeros(1, dtype=torch.int32, device=dev)
+        for t in prompt:   # prefill with slow-only steps (not timed)
+            model.decode_step(torch.tensor([int(t)], dtype=torch.int32, device=dev), pos, desc, dual=False,
+                              next_token=nxt, advance=True)
+        for _ in range(args.warmup):
+            model.decode_step(nxt, pos, desc, dual=dual, next_token=nxt, advance=True)
+        torch.cuda.synchronize()
+        model.moe_reset()
+        stream = torch.cuda.current_stream()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(steps):
+            model.decode_step(nxt, pos, desc, dual=dual, next_token=nxt, advance=True)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        ms = e0.elapsed_time(e1)
+        st = model.moe_stats()
+        k_avg_ms, k_n = _kernel_avg_ms(model, "expert_gateup", stream,
+                                       lambda: model.decode_step(nxt, pos, desc, dual=dual, next_token=nxt,
+                                                                 advance=True), 4)
+        n_use = st["hits"] + st["misses"]
+        runs.append(dict(run=label, slots=slots, policy=policy, dual_stream=dual,
+                         tokens_per_s=round(steps * 1000.0 / ms, 3), ms_per_token=round(ms / steps, 4),
+                         wall_s=round(wall, 3), hit_rate=round(st["hits"] / max(n_use, 1), 4),
+                         misses_per_token=round(st["misses"] / steps, 3),
+                         prefetch_issued=st["prefetch_issued"], prefetch_used=st["prefetch_used"],
+                         prefetch_wasted=st["prefetch_wasted"],
+                         pred_accuracy=round(st["pred_correct"] / st["pred_total"], 4) if st["pred_total"] else None,
+                         h2d_gb=round(st["h2d_bytes"] / 1e9, 3), copy_waits=st["copy_waits"],
+                         host_wait_ms_per_token=round(st["host_wait_ns"] / 1e6 / steps, 4),
+                         layer_misses=st["layer_misses"],
+                         expert_gateup_us=round(k_avg_ms * 1e3, 3)))
+        del model, kv
+        torch.cuda.empty_cache()
+    resident = runs[2]
+    for r in runs:
+        r["stall_ms_per_token_vs_resident"] = round(r["ms_per_token"] - resident["ms_per_token"], 4)
+    kb = expert_gateup_bytes(cfg)
+    achieved = kb / (resident["expert_gateup_us"] * 1e-6) / 1e9
+    m2 = runs[1]
+    _line(metric="MoE decode tokens/s at batch 1 with experts in host memory (HBM expert cache, AoT prefetch)",
+          value=m2["tokens_per_s"], unit="tokens/s", steps=steps, warmup=args.warmup,
+          ms_per_step=m2["ms_per_token"], dtype="bf16",
+          config={"workload": f"olmoe-shaped {cfg.n_layers}L d{cfg.d_model} {cfg.n_heads}x{cfg.head_dim} "
+                              f"E{cfg.n_experts} top{cfg.top_k} Fe{cfg.expert_ffn} vocab{cfg.vocab} rank{cfg.rank}, "
+                              f"experts in pinned host memory, {C} HBM slots per layer, prompt {plen}, "
+                              f"{steps} decode steps", "batch": 1, "slots": C},
+          token_bytes_all_hits=int(moe_token_bytes(cfg, plen + steps / 2)), runs=runs,
+          roofline={"bound": "hbm", "kernel": "expert gate/up (k_moe_gateup)", "achieved": round(achieved, 1),
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "traffic": None, "avg_kernel_us": resident["expert_gateup_us"], "bytes_per_launch": int(kb)},
+          cpu_baseline=None, setup_s=round(gen_s, 1))
+    return 0
+
+
+def run_copy(args) -> int:
+    """A plain device-to-device copy of a known size, for scaling the HBM
+    byte counters of the profiler (FETCH_SIZE / WRITE_SIZE per dispatch)."""
+    import torch
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = args.steps or 8
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    _line(metric="device copy GB/s (read + write) for profiler counter calibration", value=round(2 * n / ms / 1e6, 1),
+          unit="GB/s", steps=reps, warmup=0, ms_per_step=round(ms, 5), dtype="u8",
+          config={"workload": f"copy of {n} bytes"}, bytes_read=n, bytes_written=n, roofline=None, cpu_baseline=None)
+    return 0
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--mode", choices=("dense", "batch", "spec", "moe", "copy"), default="dense")
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="phi3")
+    ap.add_argument("--ctx", type=int, default=None, help="KV context (dense: 1024, batch: 4096)")
+    ap.add_argument("--batch", type=int, default=8, help="sequences (batch mode)")
+    ap.add_argument("--single", action="store_true", help="slow row only (plain decoding on the same kernels)")
+    ap.add_argument("--kernel-reps", type=int, default=20, help="direct steps timed for the dominant kernel")
+    ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of CPU oracle timing (0: skip)")
+    ap.add_argument("--gamma", type=int, default=4)
+    ap.add_argument("--exit-layer", type=int, default=8)
+    ap.add_argument("--new-tokens", type=int, default=512)
+    ap.add_argument("--prompt", type=int, default=128)
+    ap.add_argument("--decay", type=float, nargs="*", default=[1.0, 0.1],
+                    help="spec mode: scale of wo/wd in layers >= exit layer (1.0 = plain weights)")
+    ap.add_argument("--slots", type=int, default=16, help="moe mode: HBM expert slots per layer")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: --gpus {args.gpus} is not supported by this build "
+              f"(the multi-GPU sharding is a design note, not an implementation)", file=sys.stderr)
+        return 2
+    import torch
+    torch.cuda.set_device(0)
+    if args.mode == "dense":
+        args.steps = args.steps or 256
+        args.ctx = args.ctx or 1024
+        return run_dense(args)
+    if args.mode == "batch":
+        args.steps = args.steps or 64
+        args.ctx = args.ctx or 4096
+        return run_batch(args)
+    if args.mode == "spec":
+        return run_spec(args)
+    if args.mode == "copy":
+        return run_copy(args)
+    args.steps = args.steps or 256
+    args.warmup = min(args.warmup, 4)
+    return run_moe(args)
 
 
 if __name__ == "__main__":

@@ -45,13 +45,15 @@ constexpr int kPerMaxBase = kScoreCap;
 int per_max(int rows) { return (kPerMaxBase / std::max(rows, 1)) & ~15; }
 
 // Context splits of the attention for `nseq` sequences of `rows` rows each:
-// about 256 workgroups in total (each streams its share of the cache with many
-// loads in flight), at least as many as the LDS score buffer requires.
+// at least about 256 workgroups in total, at most 128 tokens per split (the
+// attention kernel puts 128 tokens of keys and values in flight before it
+// forms q), at least as many as the LDS score buffer requires, at most 63
+// (the merge holds 64 partials).
 int choose_splits(int nseq, int rows, int H, int max_ctx) {
   const int target = std::max(1, (256 + nseq * H - 1) / (nseq * H));
-  const int useful = std::max(1, (max_ctx + 127) / 128);
+  const int prefetched = std::max(1, (max_ctx + 127) / 128);
   const int need = std::max(1, (max_ctx + per_max(rows) - 1) / per_max(rows));
-  return std::max(need, std::min(target, useful));
+  return std::min(63, std::max(need, std::max(target, prefetched)));
 }
 
 struct Layout {
@@ -74,6 +76,14 @@ size_t expert_bytes_of(const m2r2_config& c) {
   const int wb = c.wdtype == M2R2_BF16;
   return 2 * packed_bytes(c.expert_ffn, c.d_model, wb) + packed_bytes(c.d_model, c.expert_ffn, wb);
 }
+
+// Workgroups the GPU holds at once for each tile GEMV kernel (filled at
+// context creation from the occupancy of the kernel with its LDS):
+// index [wb][row class 0: 2 rows, 1: 16 rows][kernel 0 qkv, 1 o, 2 gate/up,
+// 3 down, 4 head].
+struct Resident {
+  int n[2][2][5];
+};
 
 Layout make_layout(const m2r2_config& c, int max_batch, int max_chunk, int max_ctx) {
   Layout L{};
@@ -174,6 +184,8 @@ m2r2_status check_config(const m2r2_config* c, int max_batch, int max_chunk, int
   if (c->n_heads < 1 || (c->n_heads * c->head_dim) % kstep)
     return fail(M2R2_E_SHAPE, "n_heads*head_dim %d not a multiple of %d", c->n_heads * c->head_dim, kstep);
   if (c->rank < 1 || c->rank > kMaxRank) return fail(M2R2_E_SHAPE, "rank %d not in [1,%d]", c->rank, kMaxRank);
+  if (std::max({c->d_model, c->n_heads * c->head_dim, c->ffn}) > 16384)
+    return fail(M2R2_E_UNSUPPORTED, "reduction length above 16384 (activation rows are held in LDS)");
   if (c->vocab < 1) return fail(M2R2_E_SHAPE, "vocab %d", c->vocab);
   if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f)) return fail(M2R2_E_INVALID, "rms_eps/rope_theta");
   if (max_batch < 1 || max_batch > 8) return fail(M2R2_E_SHAPE, "max_batch %d not in [1,8]", max_batch);
@@ -218,6 +230,7 @@ struct m2r2_ctx {
   int max_batch, max_chunk, max_ctx;
   WS ws;
   // kernel timing (measurement only)
+  Resident resident;
   int timed_class = -1;
   std::vector<hipEvent_t> ev;   // pairs
   int ev_used = 0;
@@ -270,6 +283,27 @@ m2r2_status timed(m2r2_ctx* c, int cls, hipStream_t st, F&& fn) {
     if (m2r2_status s_ = timed(c, cls, st, [&]() { launch; })) return s_;   \
   } while (0)
 
+// Grid sizes and dynamic LDS of the tile GEMV launches of one pass.
+struct Grids {
+  int qkv, o, gu, head;
+  size_t l_d, l_q, l_f;   // LDS for reduction lengths d, H*hd, ffn
+};
+
+template <int WB, int MT>
+Grids grids(const m2r2_ctx* c) {
+  const Dims& D = c->D;
+  const int* cap = c->resident.n[WB][MT <= 2 ? 0 : 1];
+  Grids g;
+  g.qkv = std::min(3 * (D.qdim / 16) + (3 * D.r + 15) / 16, cap[0]);
+  g.o = std::min(D.d / 16, std::min(cap[1], cap[3]));
+  g.gu = std::min(std::max(D.F / 16, 1), cap[2]);
+  g.head = std::min(c->lay.TV, cap[4]);
+  g.l_d = tile_lds_bytes(WB, MT, D.d);
+  g.l_q = tile_lds_bytes(WB, MT, D.qdim);
+  g.l_f = tile_lds_bytes(WB, MT, std::max(D.F, 1));
+  return g;
+}
+
 template <int WB, int KB, int HD, int MT>
 m2r2_status run_layers_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPtrs& kv, int n_layers_run,
                          hipStream_t st) {
@@ -281,18 +315,17 @@ m2r2_status run_layers_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const 
   if (S > c->lay.S_max) return fail(M2R2_E_SHAPE, "attention splits exceed the workspace");
   if (S + 1 > 64) return fail(M2R2_E_SHAPE, "context too long for the attention merge (max_ctx %d)", c->max_ctx);
   const size_t smem = attn_smem_bytes();
-  const size_t gl = gemv_lds_bytes(WB, MT);
+  const Grids G = grids<WB, MT>(c);
   for (int l = 0; l < n_layers_run; ++l) {
     const LayerPtrs& L = c->layers[l];
-    TIMED(0, (k_qkv<WB, MT><<<3 * (D.qdim / 16) + (3 * D.r + 15) / 16, kGemvThreads, gl, st>>>(D, L, rm, c->ws, io, l)));
+    TIMED(0, (k_qkv<WB, MT><<<G.qkv, kGemvThreads, G.l_d, st>>>(D, L, rm, c->ws, io, l)));
     TIMED(1, (k_attn<KB, HD><<<dim3(S + 1, D.H, rm.nseq), kAttnThreads, smem, st>>>(D, L, rm, c->ws, io, kv, l, S)));
-    TIMED(7, (k_attn_merge<<<dim3(D.H, rm.nseq), kAttnThreads, 0, st>>>(D, rm, c->ws, S)));
-    TIMED(2, (k_oproj<WB, MT><<<c->lay.TD, kGemvThreads, gl, st>>>(D, L, rm, c->ws, io, l)));
-    TIMED(3, (k_gateup<WB, MT><<<c->lay.TF, kGemvThreads, gl, st>>>(D, L, rm, c->ws, io, l)));
-    TIMED(4, (k_down<WB, MT><<<c->lay.TD, kGemvThreads, gl, st>>>(D, L, rm, c->ws, io, l)));
+    TIMED(2, (k_oproj<WB, MT><<<G.o, kGemvThreads, G.l_q, st>>>(D, L, rm, c->ws, io, l)));
+    TIMED(3, (k_gateup<WB, MT><<<G.gu, kGemvThreads, G.l_d, st>>>(D, L, rm, c->ws, io, l)));
+    TIMED(4, (k_down<WB, MT><<<G.o, kGemvThreads, G.l_f, st>>>(D, L, rm, c->ws, io, l)));
   }
-  TIMED(5, (k_head<WB, MT><<<c->lay.TV, kGemvThreads, gl, st>>>(D, c->lm_head, c->final_norm, rm, c->ws, io, kv,
-                                                            c->lay.TV, n_layers_run)));
+  TIMED(5, (k_head<WB, MT><<<G.head, kGemvThreads, G.l_d, st>>>(D, c->lm_head, c->final_norm, rm, c->ws, io, kv,
+                                                              c->lay.TV, n_layers_run)));
   HIP_TRY(hipGetLastError());
   return M2R2_OK;
 }
@@ -349,16 +382,26 @@ hipError_t pack_all(m2r2_ctx* c, const m2r2_weights* w, void* workspace) {
   return e;
 }
 
-// Allow the GEMV kernels the dynamic LDS of 16-row staging (> 64 KB).
+// Allow the tile GEMV kernels the dynamic LDS they take (> 64 KB: resident
+// rows of long reductions, 16-row chunk staging).
+// and record how many workgroups of each the GPU holds at once.
 template <int WB, int MT>
-hipError_t set_lds_limits() {
-  const int bytes = gemv_lds_bytes(WB, MT);
-  hipError_t e = hipSuccess;
+hipError_t set_lds_limits(const m2r2_config& c, Resident& res) {
+  const int q = c.n_heads * c.head_dim;
+  const int K = std::max({c.d_model, q, c.ffn});
+  const int bytes = tile_lds_bytes(WB, MT, K);
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   const void* fns[] = {(const void*)k_qkv<WB, MT>, (const void*)k_oproj<WB, MT>, (const void*)k_gateup<WB, MT>,
                        (const void*)k_down<WB, MT>, (const void*)k_head<WB, MT>};
-  for (const void* f : fns) {
-    hipError_t r = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-    if (r != hipSuccess) e = r;
+  const int kk[] = {c.d_model, q, c.d_model, std::max(c.ffn, 1), c.d_model};
+  for (int i = 0; i < 5 && e == hipSuccess; ++i) {
+    e = hipFuncSetAttribute(fns[i], hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    int per_cu = 0;
+    if (e == hipSuccess)
+      e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fns[i], kGemvThreads, tile_lds_bytes(WB, MT, kk[i]));
+    res.n[WB][MT <= 2 ? 0 : 1][i] = std::max(1, per_cu) * std::max(1, cus);
   }
   return e;
 }
@@ -430,15 +473,15 @@ m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVP
   const size_t gl = gemv_lds_bytes(WB, MT);
   const bool ahead = dual && M.policy == M2R2_MOE_AHEAD_OF_TIME;
   const bool want_pred = dual && (ahead || (out && out->pred_experts_d));
+  const Grids G = grids<WB, MT>(c);
   const int tiles = (M.E + 15) / 16;
   float* logits = (float*)M.mp.logits;
   std::vector<int> pslots, pexperts;
   for (int l = 0; l < D.n_layers; ++l) {
     const LayerPtrs& L = c->layers[l];
-    TIMED(0, (k_qkv<WB, MT><<<3 * (D.qdim / 16) + (3 * D.r + 15) / 16, kGemvThreads, gl, st>>>(D, L, rm, c->ws, io, l)));
+    TIMED(0, (k_qkv<WB, MT><<<G.qkv, kGemvThreads, G.l_d, st>>>(D, L, rm, c->ws, io, l)));
     TIMED(1, (k_attn<KB, HD><<<dim3(S + 1, D.H, 1), kAttnThreads, smem, st>>>(D, L, rm, c->ws, io, kv, l, S)));
-    TIMED(7, (k_attn_merge<<<dim3(D.H, 1), kAttnThreads, 0, st>>>(D, rm, c->ws, S)));
-    TIMED(2, (k_oproj<WB, MT><<<c->lay.TD, kGemvThreads, gl, st>>>(D, L, rm, c->ws, io, l)));
+    TIMED(2, (k_oproj<WB, MT><<<G.o, kGemvThreads, G.l_q, st>>>(D, L, rm, c->ws, io, l)));
     if (dual) TIMED(10, (k_fast_mlp<<<(D.d + 255) / 256, 256, 0, st>>>(D, rm, L, l, c->ws)));
     // routing of the slow row, predictions for layers 2l+2 and 2l+3 from the fast row
     RouterTask t[3] = {};
@@ -501,8 +544,8 @@ m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVP
       }
     }
   }
-  TIMED(5, (k_head<WB, MT><<<c->lay.TV, kGemvThreads, gl, st>>>(D, c->lm_head, c->final_norm, rm, c->ws, io, kv,
-                                                            c->lay.TV, D.n_layers)));
+  TIMED(5, (k_head<WB, MT><<<G.head, kGemvThreads, G.l_d, st>>>(D, c->lm_head, c->final_norm, rm, c->ws, io, kv,
+                                                              c->lay.TV, D.n_layers)));
   HIP_TRY(hipGetLastError());
   M.pol.end_token();
   return M2R2_OK;
@@ -704,10 +747,10 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
     e = hipMemcpy(b + lay.rope, t.data(), t.size() * sizeof(float), hipMemcpyHostToDevice);
   }
   if (e == hipSuccess) e = pack_all(c, w, workspace);
-  if (e == hipSuccess) e = set_lds_limits<0, 2>();
-  if (e == hipSuccess) e = set_lds_limits<1, 2>();
-  if (e == hipSuccess) e = set_lds_limits<0, 16>();
-  if (e == hipSuccess) e = set_lds_limits<1, 16>();
+  if (e == hipSuccess) e = set_lds_limits<0, 2>(*cfg, c->resident);
+  if (e == hipSuccess) e = set_lds_limits<1, 2>(*cfg, c->resident);
+  if (e == hipSuccess) e = set_lds_limits<0, 16>(*cfg, c->resident);
+  if (e == hipSuccess) e = set_lds_limits<1, 16>(*cfg, c->resident);
   if (e == hipSuccess && moe) {
     MoeState& M = c->moe;
     M.on = true;

@@ -355,6 +355,255 @@ __device__ __forceinline__ void gemv_reduce(const f32x4_t (&acc)[NT], int M, flo
   __syncthreads();
 }
 
+
+// ============================================================================
+// Persistent tile GEMV.
+//
+// A launch has at most as many workgroups as the GPU holds at once; each
+// workgroup walks the tiles blockIdx.x, blockIdx.x + gridDim.x, ... (a tile is
+// 16 weight rows).  Its 8 waves split every tile's K-steps into the same
+// contiguous ranges and stream them in chunks of 8 one-kilobyte blocks, one
+// continuous sequence over all of the workgroup's tiles: the next chunk --
+// possibly the first of the next tile -- is in flight while the current one
+// is multiplied, so the LDS reduction and epilogue of one tile overlap the
+// next tile's loads.  Per-wave partial sums are added through LDS (gemv_reduce) in
+// a fixed order and the epilogue runs workgroup-wide.
+//
+// Activations: for the 2-row class the input rows (times the norm gain) are
+// staged once in LDS in MFMA fragment order, each wave its own K range -- bf16 weights:
+// hi and lo bf16 planes [step][row][32] (two MFMAs, 16 significant bits of the
+// activation); f32 weights: [step][row][16] -- so the stream loop only loads
+// weights and reads fragments from LDS.  The 16-row class stages each chunk's
+// activations in the wave's own LDS region as it goes.
+// ============================================================================
+__device__ __forceinline__ u32x4_t ld_glob(const char* p) {
+  return __builtin_nontemporal_load((const __attribute__((address_space(1))) u32x4_t*)p);
+}
+
+// Dynamic LDS of a tile GEMV launch with reduction length K.
+__host__ __device__ constexpr int tile_lds_bytes(int wb, int MT, int K) {
+  return MT <= 2 ? MT * K * 4 : kGemvWaves * MT * kChunk * (wb ? 32 : 16) * 4;
+}
+
+template <int WB, int MT>
+struct TileGemv {
+  static constexpr int KSTEP = WB ? 32 : 16;
+  static constexpr int P = KSTEP / 4;
+  static constexpr bool XRES = MT <= 2;
+  u32x4_t w[kChunk], w2[kChunk];
+  int nsteps, s0, s1, nchunks;
+  char* xl;                   // LDS: resident rows (XRES) or per-wave chunk staging
+  const float* xr[MT];        // activation rows (16-row class)
+  const float* gain;
+
+  __device__ __forceinline__ void init(int K, char* lds) {
+    const int wave = threadIdx.x >> 6;
+    nsteps = K / KSTEP;
+    const int per = (nsteps + kGemvWaves - 1) / kGemvWaves;
+    s0 = min(nsteps, wave * per);
+    s1 = min(nsteps, s0 + per);
+    nchunks = (s1 - s0 + kChunk - 1) / kChunk;
+    xl = XRES ? lds : lds + wave * (MT * kChunk * KSTEP * 4);
+  }
+
+  // blocks sb.. of the tile at `base` (this lane's 16 bytes); blocks past the
+  // wave's range repeat its last block (a cache hit, never used)
+  __device__ __forceinline__ void load(const char* base, int sb, u32x4_t (&dst)[kChunk]) const {
+#pragma unroll
+    for (int j = 0; j < kChunk; ++j) dst[j] = ld_glob(base + (size_t)min(sb + j, s1 - 1) * 1024);
+  }
+
+  // first chunk of the first tile
+  __device__ __forceinline__ void prime(const char* tile) {
+    if (s0 < s1) load(tile + (threadIdx.x & 63) * 16, s0, w);
+  }
+
+  // Activation rows (rows >= M repeat row 0), multiplied by `gn` when given.
+  // Resident class: every wave stages the steps of its own K range now (the
+  // LDS layout is indexed by step, the ranges are disjoint, and a wave reads
+  // only its own steps, so no workgroup barrier is needed).
+  __device__ __forceinline__ void set_rows(const float* const* xrow, const float* gn, int M, int K) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m) xr[m] = xrow[m < M ? m : 0];
+    gain = gn;
+    if constexpr (XRES) {
+      const int lane = threadIdx.x & 63;
+      const int per_step = MT * P;   // float4 pieces of one step (all rows)
+      for (int i = lane; i < (s1 - s0) * per_step; i += 64) {
+        const int st = s0 + i / per_step, rem = i % per_step;
+        const int m = rem / P, e = (rem % P) * 4;
+        const int k = st * KSTEP + e;
+        float4 v = ldg4(xrow[m < M ? m : 0] + k);   // (a runtime index into xr[] would put this object in scratch)
+        if (gn) {
+          const float4 g = ldg4(gn + k);
+          v.x *= g.x; v.y *= g.y; v.z *= g.z; v.w *= g.w;
+        }
+        if constexpr (WB) {
+          uint16_t* hi = (uint16_t*)xl;
+          uint16_t* lo = hi + nsteps * MT * 32;
+          const float xs[4] = {v.x, v.y, v.z, v.w};
+          uint32_t h[4], l[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            h[q] = f32_to_bf16_bits(xs[q]);
+            l[q] = f32_to_bf16_bits(xs[q] - __uint_as_float(h[q] << 16));
+          }
+          const int o = (st * MT + m) * 32 + e;
+          *(uint2*)(hi + o) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+          *(uint2*)(lo + o) = make_uint2(l[0] | (l[1] << 16), l[2] | (l[3] << 16));
+        } else {
+          *(float4*)((float*)xl + (st * MT + m) * 16 + e) = v;
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+  }
+
+  // One chunk of steps [sb, sb+8) ∩ [.., s1): the next chunk's weights (nbase,
+  // nsb) are put in flight, then the MFMAs consume wcur.
+  __device__ __forceinline__ void chunk(int sb, const char* nbase, int nsb, const u32x4_t (&wcur)[kChunk],
+                                        u32x4_t (&wnext)[kChunk], f32x4_t& acc) const {
+    const int lane = threadIdx.x & 63;
+    const int mr = lane & 15, grp = lane >> 4;
+    const int mread = mr < MT ? mr : MT - 1;
+    const int nst = min(kChunk, s1 - sb);
+    if constexpr (XRES) {
+      load(nbase, nsb, wnext);
+#pragma unroll
+      for (int jj = 0; jj < kChunk; ++jj) {
+        const int st = min(sb + jj, nsteps - 1);
+        const bool on = jj < nst;
+        if constexpr (WB) {
+          const uint16_t* hi = (const uint16_t*)xl;
+          const uint16_t* lo = hi + nsteps * MT * 32;
+          const int o = (st * MT + mread) * 32 + 8 * grp;
+          u32x4_t h = *(const u32x4_t*)(hi + o), l = *(const u32x4_t*)(lo + o);
+          if (!on) { h = u32x4_t{0u, 0u, 0u, 0u}; l = h; }
+          const bf16x8_t bw = __builtin_bit_cast(bf16x8_t, wcur[jj]);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, h), bw, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, l), bw, acc, 0, 0, 0);
+        } else {
+          float4 a = *(const float4*)((const float*)xl + (st * MT + mread) * 16 + 4 * grp);
+          if (!on) a = make_float4(0.f, 0.f, 0.f, 0.f);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, __uint_as_float(wcur[jj][0]), acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, __uint_as_float(wcur[jj][1]), acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, __uint_as_float(wcur[jj][2]), acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, __uint_as_float(wcur[jj][3]), acc, 0, 0, 0);
+        }
+      }
+    } else {
+      // stage this chunk's activations (loaded before the weight prefetch, so
+      // waiting for them never waits for the prefetch)
+      const int q = WB ? lane : (lane & 31);
+      const bool live = q < nst * P;
+      const int kq = sb * KSTEP + 4 * (live ? q : 0);
+      float4 xv[MT];
+      float4 gv = make_float4(1.f, 1.f, 1.f, 1.f);
+      if (gain) gv = ldg4(gain + kq);
+#pragma unroll
+      for (int m = 0; m < MT; ++m) xv[m] = ldg4(xr[m] + kq);
+      __builtin_amdgcn_sched_barrier(0);
+      load(nbase, nsb, wnext);
+      __builtin_amdgcn_sched_barrier(0);
+      char* my = xl;
+      const int j = q / P, e = (q % P) * 4;
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+        float4 v = xv[m];
+        v.x = live ? v.x * gv.x : 0.f;
+        v.y = live ? v.y * gv.y : 0.f;
+        v.z = live ? v.z * gv.z : 0.f;
+        v.w = live ? v.w * gv.w : 0.f;
+        if constexpr (WB) {
+          uint16_t* hi = (uint16_t*)my;
+          uint16_t* lo = hi + kChunk * MT * 32;
+          const float xs[4] = {v.x, v.y, v.z, v.w};
+          uint32_t h[4], l[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            h[i] = f32_to_bf16_bits(xs[i]);
+            l[i] = f32_to_bf16_bits(xs[i] - __uint_as_float(h[i] << 16));
+          }
+          const int o = (j * MT + m) * 32 + e;
+          *(uint2*)(hi + o) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+          *(uint2*)(lo + o) = make_uint2(l[0] | (l[1] << 16), l[2] | (l[3] << 16));
+        } else {
+          *(float4*)((float*)my + (j * MT + m) * 16 + e) = v;
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+      for (int jj = 0; jj < kChunk; ++jj) {
+        if constexpr (WB) {
+          const uint16_t* hi = (const uint16_t*)my;
+          const uint16_t* lo = hi + kChunk * MT * 32;
+          const int o = (jj * MT + mread) * 32 + 8 * grp;
+          const bf16x8_t a_hi = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(hi + o));
+          const bf16x8_t a_lo = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(lo + o));
+          const bf16x8_t bw = __builtin_bit_cast(bf16x8_t, wcur[jj]);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_hi, bw, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_lo, bw, acc, 0, 0, 0);
+        } else {
+          const float4 a = *(const float4*)((const float*)my + (jj * MT + mread) * 16 + 4 * grp);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, __uint_as_float(wcur[jj][0]), acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, __uint_as_float(wcur[jj][1]), acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, __uint_as_float(wcur[jj][2]), acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, __uint_as_float(wcur[jj][3]), acc, 0, 0, 0);
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+  }
+
+  // Stream the workgroup's tiles: local tile i (i < n_local) starts at
+  // ptr(i).  When every wave has finished tile i, epi(i, acc) runs
+  // workgroup-wide (it reduces the per-wave accumulators); the next tile's
+  // first chunk is already in flight by then.
+  template <class Ptr, class Epi>
+  __device__ __forceinline__ void run(int n_local, const Ptr& ptr, Epi& epi) {
+    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    if (s0 >= s1) {   // a wave without steps still takes part in every epilogue
+      for (int i = 0; i < n_local; ++i) epi(i, acc);
+      return;
+    }
+    const int lo16 = (threadIdx.x & 63) * 16;
+    const char* cur = ptr(0) + lo16;
+    int i = 0, k = 0;
+    for (;;) {
+      {
+        int ni = i, nk = k + 1;
+        if (nk == nchunks) { nk = 0; ++ni; }
+        const bool more = ni < n_local;
+        const char* nb = more && nk == 0 ? ptr(ni) + lo16 : cur;
+        chunk(s0 + k * kChunk, nb, more ? s0 + nk * kChunk : s1, w, w2, acc);
+        if (nk == 0) {
+          epi(i, acc);
+          acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        }
+        if (!more) break;
+        i = ni; k = nk; cur = nb;
+      }
+      {
+        int ni = i, nk = k + 1;
+        if (nk == nchunks) { nk = 0; ++ni; }
+        const bool more = ni < n_local;
+        const char* nb = more && nk == 0 ? ptr(ni) + lo16 : cur;
+        chunk(s0 + k * kChunk, nb, more ? s0 + nk * kChunk : s1, w2, w, acc);
+        if (nk == 0) {
+          epi(i, acc);
+          acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        }
+        if (!more) break;
+        i = ni; k = nk; cur = nb;
+      }
+    }
+  }
+};
+
 __device__ __forceinline__ float ld_w(const void* p, size_t i, int wb) {
   return wb ? bf16_to_f32(((const uint16_t*)p)[i]) : ((const float*)p)[i];
 }
@@ -535,24 +784,22 @@ __global__ __launch_bounds__(kGemvThreads) void k_qkv(Dims D, LayerPtrs L, RowMa
   __shared__ float inv_rms[kMaxRows];
   __shared__ const float* xrow_s[kMaxRows];
   extern __shared__ __attribute__((aligned(16))) char dyn[];
-  const int nq = D.qdim;
+  const int nq = D.qdim, tq = nq / 16;
   const int nqkv = 3 * nq + 3 * D.r;
-  const int n0 = blockIdx.x * 16;
-  // this lane's weight row
-  const int lane = threadIdx.x & 63;
-  const void* wrow[1];
-  {
-    const int tq = nq / 16, b = blockIdx.x;
-    const size_t tb = (size_t)16 * D.d * (WB ? 2 : 4);   // bytes of one packed tile
-    if (b < 3 * tq) {
-      const void* base = b < tq ? L.pq : (b < 2 * tq ? L.pk : L.pv);
-      wrow[0] = (const char*)base + (size_t)(b % tq) * tb;
-    } else {
-      wrow[0] = (const char*)L.pa + (size_t)(b - 3 * tq) * tb;
+  const int ntiles = 3 * tq + (3 * D.r + 15) / 16;
+  const size_t tb = (size_t)16 * D.d * (WB ? 2 : 4);   // bytes of one packed tile
+  // tile t: Wq, Wk, Wv, then the stacked adapter-down rows [A_q; A_k; A_v]
+  auto tile_ptr = [&](int t) -> const char* {
+    if (t < 3 * tq) {
+      const int which = t / tq;
+      return (const char*)(which == 0 ? L.pq : (which == 1 ? L.pk : L.pv)) + (size_t)(t - which * tq) * tb;
     }
-  }
-  GemvWave<WB, 1, MT, true> gw;
-  gw.begin(wrow, D.d);
+    return (const char*)L.pa + (size_t)(t - 3 * tq) * tb;
+  };
+  if ((int)blockIdx.x >= ntiles) return;
+  TileGemv<WB, MT> tg;
+  tg.init(D.d, dyn);
+  tg.prime(tile_ptr(blockIdx.x));
   // row statistics: sum of the bins filled by the previous kernel
   if (threadIdx.x < rm.M * 4) {
     float a = 0.f;
@@ -564,33 +811,33 @@ __global__ __launch_bounds__(kGemvThreads) void k_qkv(Dims D, LayerPtrs L, RowMa
   if (threadIdx.x == 0) {
     gate_logic(D, rm, ws, io, layer, ssum, reinit_s, exited_s, exitb_s, sig_s);
     for (int m = 0; m < rm.M; ++m) {
-      const int s = rm.seq[m];
+      const int sq = rm.seq[m];
       int src = m;
-      if (rm.fast[m] && reinit_s[s]) src = rm.slow_of[m];
+      if (rm.fast[m] && reinit_s[sq]) src = rm.slow_of[m];
       xrow_s[m] = ws.X + (size_t)src * D.d;
       inv_rms[m] = rsqrtf(ssum[src * 4] / D.d + D.eps);
     }
   }
   __syncthreads();
   if (blockIdx.x == 0 && threadIdx.x < rm.nseq) {
-    const int s = threadIdx.x;
-    ws.reinit[layer * kMaxSeq + s] = reinit_s[s];
-    ws.exited[s] = exited_s[s];
-    ws.exitb[s] = exitb_s[s];
-    if (layer > 0) ws.sig[s * D.n_layers + layer - 1] = sig_s[s];
+    const int sq = threadIdx.x;
+    ws.reinit[layer * kMaxSeq + sq] = reinit_s[sq];
+    ws.exited[sq] = exited_s[sq];
+    ws.exitb[sq] = exitb_s[sq];
+    if (layer > 0) ws.sig[sq * D.n_layers + layer - 1] = sig_s[sq];
   }
-  // every sequence stopped: only the K and V rows are still needed
-  bool all_exited = true;
-  for (int s = 0; s < rm.nseq; ++s) all_exited &= exited_s[s] != 0;
-  if (all_exited && (n0 < nq || n0 >= 3 * nq)) return;
-
-  f32x4_t acc[1];
-  gw.run(xrow_s, L.attn_norm, rm.M, dyn, acc);
-  gemv_reduce<1>(acc, rm.M, red, y);
-  for (int e = threadIdx.x; e < rm.M * 16; e += kGemvThreads) {
-    const int m = e >> 4, nn = n0 + (e & 15);
-    if (nn < nqkv) ws.QKV[(size_t)m * nqkv + nn] = y[e] * inv_rms[m];
-  }
+  tg.set_rows(xrow_s, L.attn_norm, rm.M, D.d);
+  auto ptr = [&](int i) { return tile_ptr(blockIdx.x + i * gridDim.x); };
+  auto epi = [&](int i, const f32x4_t& a) {
+    const int t = blockIdx.x + i * gridDim.x;
+    f32x4_t acc[1] = {a};
+    gemv_reduce<1>(acc, rm.M, red, y);
+    for (int e = threadIdx.x; e < rm.M * 16; e += kGemvThreads) {
+      const int m = e >> 4, nn = t * 16 + (e & 15);
+      if (nn < nqkv) ws.QKV[(size_t)m * nqkv + nn] = y[e] * inv_rms[m];
+    }
+  };
+  tg.run((ntiles - blockIdx.x + gridDim.x - 1) / gridDim.x, ptr, epi);
 }
 
 // ============================================================================
@@ -689,10 +936,64 @@ __device__ __forceinline__ float* att_part(const WS& ws, const Dims& D, int s, i
   return ws.att + ((((size_t)s * D.H + h) * (n_split + 1) + sp) * kMaxRows + i) * stride;
 }
 
+// Merge the partials of one (sequence, head): the output o of every row and,
+// for fast rows, the o-adapter down-projection of that head.  The partials
+// were written by other workgroups: device-coherent loads.
+__device__ void attn_merge(const Dims& D, const RowMap& rm, const WS& ws, int s, int h, int n_split) {
+  __shared__ float stat[kMaxRows * 64 * 2];   // m, l of every split (n_split + 1 <= 64)
+  __shared__ float wgt[kMaxRows * 64];
+  __shared__ float linv[kMaxRows];
+  const int R = rm.cnt[s], first = rm.first[s];
+  const int S1 = n_split + 1;
+  for (int e = threadIdx.x; e < R * S1; e += blockDim.x) {
+    const int i = e / S1, sp = e % S1;
+    const float* pp = att_part(ws, D, s, h, sp, n_split, i);
+    stat[(i * 64 + sp) * 2] = ld_agent(pp);
+    stat[(i * 64 + sp) * 2 + 1] = ld_agent(pp + 1);
+  }
+  __syncthreads();
+  if (threadIdx.x < R) {
+    const int i = threadIdx.x;
+    float M = -INFINITY;
+    for (int sp = 0; sp < S1; ++sp)
+      if (stat[(i * 64 + sp) * 2 + 1] > 0.f) M = fmaxf(M, stat[(i * 64 + sp) * 2]);
+    float Lsum = 0.f;
+    for (int sp = 0; sp < S1; ++sp) {
+      const float l = stat[(i * 64 + sp) * 2 + 1];
+      const float w = l > 0.f ? __expf(stat[(i * 64 + sp) * 2] - M) : 0.f;
+      wgt[i * 64 + sp] = w;
+      Lsum += w * l;
+    }
+    linv[i] = 1.f / Lsum;
+  }
+  __syncthreads();
+  const int W = D.hd + D.r;
+  for (int e = threadIdx.x; e < R * W; e += blockDim.x) {
+    const int i = e / W, c = e % W;
+    float v = 0.f;
+    for (int sp0 = 0; sp0 < S1; sp0 += 8) {
+      float part[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) part[u] = ld_agent(att_part(ws, D, s, h, min(sp0 + u, S1 - 1), n_split, i) + 2 + c);
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (sp0 + u < S1) v += wgt[i * 64 + sp0 + u] * part[u];
+    }
+    v *= linv[i];
+    const int mi = first + i;
+    if (c < D.hd) ws.O[(size_t)mi * D.qdim + h * D.hd + c] = v;
+    else ws.uo[((size_t)mi * D.H + h) * D.r + (c - D.hd)] = rm.fast[mi] ? v : 0.f;
+  }
+}
+
 // Kernel: attention over the shared cache, one context split per workgroup,
 // plus one workgroup per (sequence, head) for the rows' own keys and the cache
-// writes.  grid = (splits + 1, H, nseq), block = 256.  The partials are merged
-// by k_attn_merge.
+// writes; the last workgroup of a (sequence, head) to finish merges the
+// partials.  A split's first 128 cached keys and values (usually all of them)
+// are put in flight before q is formed.  grid = (splits + 1, H, nseq),
+// block = 256.
+constexpr int kAttnPrefetch = 2;   // tokens per thread loaded ahead (x 64 slots = 128 tokens)
+
 template <int KB, int HD>
 __global__ __launch_bounds__(kAttnThreads) void k_attn(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, KVPtrs kv,
                                                        int layer, int n_split) {
@@ -708,10 +1009,12 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn(Dims D, LayerPtrs L, RowM
   float* redp = sc + kScoreCap;            // [4 waves][2 rows][hd]
   __shared__ float rowm[kMaxRows], rowl[kMaxRows];
   __shared__ float uacc_s[kMaxRows * kMaxRank];
+  __shared__ int last_flag;
 
   const int ctx = io.positions[s] + rm.pos_offset;
   const bool frozen = ws.exited[s] != 0;
   const bool own = split == n_split;
+  bool store = !frozen;   // this workgroup produces a partial
 
   if (own) {
     // ---- the rows' own keys and the cache writes -------------------------------
@@ -731,151 +1034,174 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn(Dims D, LayerPtrs L, RowM
         ((float*)kv.v)[ix] = vx[e];
       }
     }
-    if (frozen) return;   // exited sequence: only its cache entries are produced
-    head_vectors(D, L, rm, ws, io, first, R, 0, h, q);
-    // a slow row sees the chunk's slow rows up to itself (as stored in the
-    // cache); a fast row sees only its own exact key/value
-    float* ownsc = sc;   // [R][R]
-    for (int e = threadIdx.x; e < R * R; e += kAttnThreads) {
-      const int i = e / R, jj = e % R;
-      const int mi = first + i, mj = first + jj;
-      bool vis;
-      if (rm.fast[mi]) vis = (jj == i);
-      else vis = !rm.fast[mj] && rm.idx[mj] <= rm.idx[mi];
-      float p = -INFINITY;
-      if (vis) {
-        p = 0.f;
-        const bool rnd = !rm.fast[mi];
-        for (int d = 0; d < hd; ++d) {
-          const float kk = rnd ? kv_round(kx[jj * hd + d], KB) : kx[jj * hd + d];
-          p += q[i * hd + d] * kk;
+    if (!frozen) {
+      head_vectors(D, L, rm, ws, io, first, R, 0, h, q);
+      // a slow row sees the chunk's slow rows up to itself (as stored in the
+      // cache); a fast row sees only its own exact key/value
+      float* ownsc = sc;   // [R][R]
+      for (int e = threadIdx.x; e < R * R; e += kAttnThreads) {
+        const int i = e / R, jj = e % R;
+        const int mi = first + i, mj = first + jj;
+        bool vis;
+        if (rm.fast[mi]) vis = (jj == i);
+        else vis = !rm.fast[mj] && rm.idx[mj] <= rm.idx[mi];
+        float p = -INFINITY;
+        if (vis) {
+          p = 0.f;
+          const bool rnd = !rm.fast[mi];
+          for (int d = 0; d < hd; ++d) {
+            const float kk = rnd ? kv_round(kx[jj * hd + d], KB) : kx[jj * hd + d];
+            p += q[i * hd + d] * kk;
+          }
+          p *= scale;
         }
-        p *= scale;
+        ownsc[e] = p;
       }
-      ownsc[e] = p;
-    }
-    __syncthreads();
-    if (threadIdx.x < R) {
-      const int i = threadIdx.x;
-      float mx = -INFINITY;
-      for (int jj = 0; jj < R; ++jj) mx = fmaxf(mx, ownsc[i * R + jj]);
-      float l = 0.f;
-      for (int jj = 0; jj < R; ++jj) {
-        const float v = ownsc[i * R + jj] == -INFINITY ? 0.f : __expf(ownsc[i * R + jj] - mx);
-        ownsc[i * R + jj] = v;
-        l += v;
+      __syncthreads();
+      if (threadIdx.x < R) {
+        const int i = threadIdx.x;
+        float mx = -INFINITY;
+        for (int jj = 0; jj < R; ++jj) mx = fmaxf(mx, ownsc[i * R + jj]);
+        float l = 0.f;
+        for (int jj = 0; jj < R; ++jj) {
+          const float v = ownsc[i * R + jj] == -INFINITY ? 0.f : __expf(ownsc[i * R + jj] - mx);
+          ownsc[i * R + jj] = v;
+          l += v;
+        }
+        rowm[i] = mx;
+        rowl[i] = l;
       }
-      rowm[i] = mx;
-      rowl[i] = l;
-    }
-    __syncthreads();
-    for (int e = threadIdx.x; e < R * hd; e += kAttnThreads) {
-      const int i = e / hd, d = e % hd;
-      const bool rnd = !rm.fast[first + i];
-      float a = 0.f;
-      for (int jj = 0; jj < R; ++jj) {
-        const float w = ownsc[i * R + jj];
-        if (w != 0.f) a += w * (rnd ? kv_round(vx[jj * hd + d], KB) : vx[jj * hd + d]);
+      __syncthreads();
+      for (int e = threadIdx.x; e < R * hd; e += kAttnThreads) {
+        const int i = e / hd, d = e % hd;
+        const bool rnd = !rm.fast[first + i];
+        float a = 0.f;
+        for (int jj = 0; jj < R; ++jj) {
+          const float w = ownsc[i * R + jj];
+          if (w != 0.f) a += w * (rnd ? kv_round(vx[jj * hd + d], KB) : vx[jj * hd + d]);
+        }
+        q[e] = a;   // acc of the own-key partial
       }
-      q[e] = a;   // acc of the own-key partial
+      __syncthreads();
     }
-    __syncthreads();
-  } else {
+  } else if (!frozen) {
     // ---- this split's share of the cached context [0, ctx) -------------------
-    if (frozen) return;
-    head_vectors(D, L, rm, ws, io, first, R, 0, h, q);
     const int per = ((ctx + n_split - 1) / n_split + 15) & ~15;
-    if (per * R > kScoreCap) {             // the host sizes splits so that this cannot happen
-      if (threadIdx.x == 0) atomicOr(ws.err, 4);
-      return;
-    }
     const int t0 = min(ctx, split * per), t1 = min(ctx, t0 + per);
     const int nt = t1 - t0;
     const int sub = threadIdx.x & 3, slot = threadIdx.x >> 2;
     const int d0 = sub * DPL;
-#pragma unroll 4
-    for (int j = slot; j < nt; j += kAttnThreads / 4) {
+    // keys and values of the first tokens, in flight while q is formed
+    float kpf[kAttnPrefetch][DPL], vpf[kAttnPrefetch][DPL];
+#pragma unroll
+    for (int it = 0; it < kAttnPrefetch; ++it) {
+      const int j = slot + it * (kAttnThreads / 4);
       bool ok;
-      const size_t base = kv_index(kv, D, layer, s, t0 + j, h, d0, ok);
-      float kk[DPL];
-      kv_row_load<KB, HD>(kv.k, base, ok, kk);
-      for (int i = 0; i < R; ++i) {
-        float p = 0.f;
-#pragma unroll
-        for (int c = 0; c < DPL; ++c) p += q[i * hd + d0 + c] * kk[c];
-        p += __shfl_xor(p, 1);
-        p += __shfl_xor(p, 2);
-        if (sub == 0) sc[i * per + j] = p * scale;
-      }
+      const size_t base = kv_index(kv, D, layer, s, t0 + min(j, max(nt - 1, 0)), h, d0, ok);
+      kv_row_load<KB, HD>(kv.k, base, ok && j < nt, kpf[it]);
+      kv_row_load<KB, HD>(kv.v, base, ok && j < nt, vpf[it]);
     }
-    __syncthreads();
-    {
-      const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-      for (int i = w; i < R; i += 4) {
-        float mx = -INFINITY;
-        for (int j = lane; j < nt; j += 64) mx = fmaxf(mx, sc[i * per + j]);
-        mx = wave_max(mx);
-        float l = 0.f;
-        for (int j = lane; j < nt; j += 64) {
-          const float e = __expf(sc[i * per + j] - mx);
-          sc[i * per + j] = e;
-          l += e;
+    head_vectors(D, L, rm, ws, io, first, R, 0, h, q);
+    if (per * R > kScoreCap) {             // the host sizes splits so that this cannot happen
+      if (threadIdx.x == 0) atomicOr(ws.err, 4);
+      store = false;
+    } else {
+      {
+        int it = 0;
+        for (int j = slot; j < nt; j += kAttnThreads / 4, ++it) {
+          float kk[DPL];
+          if (it < kAttnPrefetch) {
+#pragma unroll
+            for (int c = 0; c < DPL; ++c) kk[c] = it == 0 ? kpf[0][c] : kpf[kAttnPrefetch - 1][c];
+          } else {
+            bool ok;
+            const size_t base = kv_index(kv, D, layer, s, t0 + j, h, d0, ok);
+            kv_row_load<KB, HD>(kv.k, base, ok, kk);
+          }
+          for (int i = 0; i < R; ++i) {
+            float p = 0.f;
+#pragma unroll
+            for (int c = 0; c < DPL; ++c) p += q[i * hd + d0 + c] * kk[c];
+            p += __shfl_xor(p, 1);
+            p += __shfl_xor(p, 2);
+            if (sub == 0) sc[i * per + j] = p * scale;
+          }
         }
-        l = wave_sum(l);
-        if (lane == 0) { rowm[i] = nt > 0 ? mx : -INFINITY; rowl[i] = nt > 0 ? l : 0.f; }
       }
-    }
-    __syncthreads();
-    const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    for (int i0 = 0; i0 < R; i0 += 2) {
-      const bool two = i0 + 1 < R;
-      float acc0[DPL], acc1[DPL];
-#pragma unroll
-      for (int c = 0; c < DPL; ++c) { acc0[c] = 0.f; acc1[c] = 0.f; }
-#pragma unroll 4
-      for (int j = slot; j < nt; j += kAttnThreads / 4) {
-        bool ok;
-        const size_t base = kv_index(kv, D, layer, s, t0 + j, h, d0, ok);
-        float vv[DPL];
-        kv_row_load<KB, HD>(kv.v, base, ok, vv);
-        const float p0 = sc[i0 * per + j];
-        const float p1 = two ? sc[(i0 + 1) * per + j] : 0.f;
-#pragma unroll
-        for (int c = 0; c < DPL; ++c) { acc0[c] += p0 * vv[c]; acc1[c] += p1 * vv[c]; }
+      __syncthreads();
+      {
+        const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+        for (int i = w; i < R; i += 4) {
+          float mx = -INFINITY;
+          for (int j = lane; j < nt; j += 64) mx = fmaxf(mx, sc[i * per + j]);
+          mx = wave_max(mx);
+          float l = 0.f;
+          for (int j = lane; j < nt; j += 64) {
+            const float e = __expf(sc[i * per + j] - mx);
+            sc[i * per + j] = e;
+            l += e;
+          }
+          l = wave_sum(l);
+          if (lane == 0) { rowm[i] = nt > 0 ? mx : -INFINITY; rowl[i] = nt > 0 ? l : 0.f; }
+        }
       }
+      __syncthreads();
+      const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+      for (int i0 = 0; i0 < R; i0 += 2) {
+        const bool two = i0 + 1 < R;
+        float acc0[DPL], acc1[DPL];
 #pragma unroll
-      for (int c = 0; c < DPL; ++c) {
-        float a = acc0[c], b = acc1[c];
-        a += __shfl_xor(a, 4); b += __shfl_xor(b, 4);
-        a += __shfl_xor(a, 8); b += __shfl_xor(b, 8);
-        a += __shfl_xor(a, 16); b += __shfl_xor(b, 16);
-        a += __shfl_xor(a, 32); b += __shfl_xor(b, 32);
-        acc0[c] = a; acc1[c] = b;
-      }
-      if (lane < 4) {
+        for (int c = 0; c < DPL; ++c) { acc0[c] = 0.f; acc1[c] = 0.f; }
+        int it = 0;
+        for (int j = slot; j < nt; j += kAttnThreads / 4, ++it) {
+          float vv[DPL];
+          if (it < kAttnPrefetch) {
+#pragma unroll
+            for (int c = 0; c < DPL; ++c) vv[c] = it == 0 ? vpf[0][c] : vpf[kAttnPrefetch - 1][c];
+          } else {
+            bool ok;
+            const size_t base = kv_index(kv, D, layer, s, t0 + j, h, d0, ok);
+            kv_row_load<KB, HD>(kv.v, base, ok, vv);
+          }
+          const float p0 = sc[i0 * per + j];
+          const float p1 = two ? sc[(i0 + 1) * per + j] : 0.f;
+#pragma unroll
+          for (int c = 0; c < DPL; ++c) { acc0[c] += p0 * vv[c]; acc1[c] += p1 * vv[c]; }
+        }
 #pragma unroll
         for (int c = 0; c < DPL; ++c) {
-          redp[(wv * 2 + 0) * hd + d0 + c] = acc0[c];
-          redp[(wv * 2 + 1) * hd + d0 + c] = acc1[c];
+          float a = acc0[c], b = acc1[c];
+          a += __shfl_xor(a, 4); b += __shfl_xor(b, 4);
+          a += __shfl_xor(a, 8); b += __shfl_xor(b, 8);
+          a += __shfl_xor(a, 16); b += __shfl_xor(b, 16);
+          a += __shfl_xor(a, 32); b += __shfl_xor(b, 32);
+          acc0[c] = a; acc1[c] = b;
         }
-      }
-      __syncthreads();
-      for (int e = threadIdx.x; e < 2 * hd; e += kAttnThreads) {
-        const int a = e / hd, d = e % hd;
-        if (i0 + a < R) {
-          float v = 0.f;
-          for (int w = 0; w < 4; ++w) v += redp[(w * 2 + a) * hd + d];
-          q[(i0 + a) * hd + d] = v;   // q is no longer needed: reuse it for acc
+        if (lane < 4) {
+#pragma unroll
+          for (int c = 0; c < DPL; ++c) {
+            redp[(wv * 2 + 0) * hd + d0 + c] = acc0[c];
+            redp[(wv * 2 + 1) * hd + d0 + c] = acc1[c];
+          }
         }
+        __syncthreads();
+        for (int e = threadIdx.x; e < 2 * hd; e += kAttnThreads) {
+          const int a = e / hd, d = e % hd;
+          if (i0 + a < R) {
+            float v = 0.f;
+            for (int w = 0; w < 4; ++w) v += redp[(w * 2 + a) * hd + d];
+            q[(i0 + a) * hd + d] = v;   // q is no longer needed: reuse it for acc
+          }
+        }
+        __syncthreads();
       }
-      __syncthreads();
     }
   }
-  // ---- store the partial: m, l, acc, and A_o[:, head cols] . acc (fast rows) ----
-  {
+  if (store) {
+    // ---- store the partial: m, l, acc, and A_o[:, head cols] . acc (fast rows) ----
     // A_o[j][h*hd + d] . acc_i[d]: 8 dims per thread, then a sum over hd/8 threads
     constexpr int PCS = HD / 8;
-    float* up = redp;   // [R*r][PCS] partials (R*r*PCS <= 16*32*16 would overflow: rows done in groups)
+    float* up = redp;
     for (int i0 = 0; i0 < R; ++i0) {
       if (!rm.fast[first + i0] || !L.A[3]) {
         for (int j = threadIdx.x; j < D.r; j += kAttnThreads) uacc_s[i0 * D.r + j] = 0.f;
@@ -897,76 +1223,28 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn(Dims D, LayerPtrs L, RowM
       }
       __syncthreads();
     }
-  }
-  __syncthreads();
-  for (int i = 0; i < R; ++i) {
-    float* pp = att_part(ws, D, s, h, split, n_split, i);
-    for (int e = threadIdx.x; e < 2 + hd + D.r; e += kAttnThreads) {
-      float v;
-      if (e == 0) v = rowm[i];
-      else if (e == 1) v = rowl[i];
-      else if (e < 2 + hd) v = q[i * hd + e - 2];
-      else v = uacc_s[i * D.r + e - 2 - hd];
-      pp[e] = v;
+    __syncthreads();
+    for (int i = 0; i < R; ++i) {
+      float* pp = att_part(ws, D, s, h, split, n_split, i);
+      for (int e = threadIdx.x; e < 2 + hd + D.r; e += kAttnThreads) {
+        float v;
+        if (e == 0) v = rowm[i];
+        else if (e == 1) v = rowl[i];
+        else if (e < 2 + hd) v = q[i * hd + e - 2];
+        else v = uacc_s[i * D.r + e - 2 - hd];
+        st_agent(pp + e, v);
+      }
     }
   }
-}
-
-// Kernel: merge the attention partials of one (sequence, head): the output o
-// of every row and, for fast rows, the o-adapter down-projection of that head.
-// grid = (H, nseq), block = 256.
-__global__ __launch_bounds__(kAttnThreads) void k_attn_merge(Dims D, RowMap rm, WS ws, int n_split) {
-  __shared__ float stat[kMaxRows * 64 * 2];   // m, l of every split (n_split + 1 <= 64)
-  __shared__ float wgt[kMaxRows * 64];
-  __shared__ float linv[kMaxRows];
-  const int h = blockIdx.x, s = blockIdx.y;
-  if (ws.exited[s]) return;
-  const int R = rm.cnt[s], first = rm.first[s];
-  const int S1 = n_split + 1;
-  for (int e = threadIdx.x; e < R * S1; e += kAttnThreads) {
-    const int i = e / S1, sp = e % S1;
-    const float* pp = att_part(ws, D, s, h, sp, n_split, i);
-    stat[(i * 64 + sp) * 2] = pp[0];
-    stat[(i * 64 + sp) * 2 + 1] = pp[1];
-  }
-  __syncthreads();
-  if (threadIdx.x < R) {
-    const int i = threadIdx.x;
-    float M = -INFINITY;
-    for (int sp = 0; sp < S1; ++sp)
-      if (stat[(i * 64 + sp) * 2 + 1] > 0.f) M = fmaxf(M, stat[(i * 64 + sp) * 2]);
-    float Lsum = 0.f;
-    for (int sp = 0; sp < S1; ++sp) {
-      const float l = stat[(i * 64 + sp) * 2 + 1];
-      const float w = l > 0.f ? __expf(stat[(i * 64 + sp) * 2] - M) : 0.f;
-      wgt[i * 64 + sp] = w;
-      Lsum += w * l;
-    }
-    linv[i] = 1.f / Lsum;
-  }
-  __syncthreads();
-  const int W = D.hd + D.r;
-  for (int e = threadIdx.x; e < R * W; e += kAttnThreads) {
-    const int i = e / W, c = e % W;
-    float v = 0.f;
-    for (int sp0 = 0; sp0 < S1; sp0 += 8) {
-      float part[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) part[u] = att_part(ws, D, s, h, min(sp0 + u, S1 - 1), n_split, i)[2 + c];
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if (sp0 + u < S1) v += wgt[i * 64 + sp0 + u] * part[u];
-    }
-    v *= linv[i];
-    const int mi = first + i;
-    if (c < D.hd) ws.O[(size_t)mi * D.qdim + h * D.hd + c] = v;
-    else ws.uo[((size_t)mi * D.H + h) * D.r + (c - D.hd)] = rm.fast[mi] ? v : 0.f;
-  }
+  // every workgroup of the (sequence, head) counts in; the last one merges
+  if (!arrive_last(&ws.att_cnt[s * D.H + h], n_split + 1, &last_flag)) return;
+  if (frozen) return;
+  attn_merge(D, rm, ws, s, h, n_split);
 }
 
 // ============================================================================
-// Kernel: output projection + residual add (+ adapter on the fast row).
-// grid = d/16 tiles, block = 512.
+// Kernel: output projection + residual add (+ adapter on the fast row);
+// partial sums for the gate/up prologue.  Persistent tile GEMV, grid <= d/16.
 // ============================================================================
 template <int WB, int MT>
 __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int layer) {
@@ -976,85 +1254,89 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
   __shared__ float newx[256];
   __shared__ const float* xrow_s[kMaxRows];
   extern __shared__ __attribute__((aligned(16))) char dyn[];
-  const int n0 = blockIdx.x * 16;
-  const int lane = threadIdx.x & 63;
-  const size_t esz = WB ? 2 : 4;
+  const int ntiles = D.d / 16;
+  if ((int)blockIdx.x >= ntiles) return;
   if (io.mode == EX_EXIT) {
     bool all_exited = true;
-    for (int s = 0; s < rm.nseq; ++s) all_exited &= ws.exited[s] != 0;
+    for (int sq = 0; sq < rm.nseq; ++sq) all_exited &= ws.exited[sq] != 0;
     if (all_exited) return;
   }
-  const void* wrow[1] = {(const char*)L.po + (size_t)blockIdx.x * 16 * D.qdim * esz};
-  GemvWave<WB, 1, MT, false> gw;
-  gw.begin(wrow, D.qdim);
+  const size_t tb = (size_t)16 * D.qdim * (WB ? 2 : 4);
+  auto tile_ptr = [&](int t) -> const char* { return (const char*)L.po + (size_t)t * tb; };
+  TileGemv<WB, MT> tg;
+  tg.init(D.qdim, dyn);
+  tg.prime(tile_ptr(blockIdx.x));
   if (threadIdx.x < rm.M) xrow_s[threadIdx.x] = ws.O + (size_t)threadIdx.x * D.qdim;
+  // adapter-down of o, summed over heads (uo is [16][H][r])
+  for (int e = threadIdx.x; e < rm.M * D.r; e += kGemvThreads) uo_s[e] = 0.f;
   __syncthreads();
-  f32x4_t acc[1];
-  gw.run(xrow_s, nullptr, rm.M, dyn, acc);
-  // adapter-down of o, summed over heads (uo is [16][H][r]: column sums over H
-  // with stride r per head, one column per (row, j))
-  if (L.A[3]) {
-    for (int e = threadIdx.x; e < rm.M * D.r; e += kGemvThreads) uo_s[e] = 0.f;
-    __syncthreads();
+  if (L.A[3])
     for (int m = 0; m < rm.M; ++m)
       if (rm.fast[m]) column_sums(ws.uo + (size_t)m * D.H * D.r, D.H, D.r, D.r, uo_s + m * D.r, red);
-  }
-  gemv_reduce<1>(acc, rm.M, red, y);
-  // epilogue: thread e -> (m, n) ; read everything first, write after a barrier
-  const int e = threadIdx.x;
-  const int m = e >> 4, nn = n0 + (e & 15);
-  float xnew = 0.f, pin = 0.f;
-  bool upd = false;
-  if (e < rm.M * 16) {
-    const int s = rm.seq[m];
-    const bool ex = ws.exited[s] != 0;
-    const float xo = ws.X[(size_t)m * D.d + nn];
-    xnew = xo;
-    if (!ex) {
-      upd = true;
-      if (rm.fast[m]) {
-        const bool ri = ws.reinit[layer * kMaxSeq + s] != 0;
-        pin = ri ? ws.X[(size_t)rm.slow_of[m] * D.d + nn] : xo;
-        float ad = 0.f;
-        if (L.B[3] && L.A[3])
-          ad = dot_row(L.B[3], nn, D.r, uo_s + m * D.r, D.wbf16);
-        xnew = pin + y[e] + ad;
-      } else {
-        xnew = xo + y[e];
-      }
-    }
-    newx[e] = xnew;
-  }
   __syncthreads();
-  if (e < rm.M * 16) {
+  tg.set_rows(xrow_s, nullptr, rm.M, D.qdim);
+  const int PO = 1 + 2 * D.r;
+  auto ptr = [&](int i) { return tile_ptr(blockIdx.x + i * gridDim.x); };
+  auto epi = [&](int i, const f32x4_t& a) {
+    const int t = blockIdx.x + i * gridDim.x;
+    f32x4_t acc[1] = {a};
+    gemv_reduce<1>(acc, rm.M, red, y);
+    const int n0 = t * 16;
+    // epilogue: read everything first (a fast row restarting at a gate reads
+    // its slow row's old value), write after a barrier
+    const int e = threadIdx.x;
+    const int m = e >> 4, nn = n0 + (e & 15);
+    float xnew = 0.f, pin = 0.f;
+    bool upd = false;
+    if (e < rm.M * 16) {
+      const int sq = rm.seq[m];
+      const float xo = ws.X[(size_t)m * D.d + nn];
+      xnew = xo;
+      if (!ws.exited[sq]) {
+        upd = true;
+        if (rm.fast[m]) {
+          const bool ri = ws.reinit[layer * kMaxSeq + sq] != 0;
+          pin = ri ? ws.X[(size_t)rm.slow_of[m] * D.d + nn] : xo;
+          float ad = 0.f;
+          if (L.B[3] && L.A[3]) ad = dot_row(L.B[3], nn, D.r, uo_s + m * D.r, D.wbf16);
+          xnew = pin + y[e] + ad;
+        } else {
+          xnew = xo + y[e];
+        }
+      }
+      newx[e] = xnew;
+    }
+    __syncthreads();
     if (upd) {
       ws.X[(size_t)m * D.d + nn] = xnew;
       if (rm.fast[m]) ws.PIN[(size_t)m * D.d + nn] = pin;
     }
-  }
-  // partial sums for the gate/up prologue: sum x^2 and the adapter-down of
-  // gate and up (fast rows): sum_n A[j][n] g_mlp[n] x[n]
-  const int PO = 1 + 2 * D.r;
-  const int bin = blockIdx.x % kBins;
-  for (int q = threadIdx.x; q < rm.M * PO; q += kGemvThreads) {
-    const int mm = q / PO, c = q % PO;
-    float v = 0.f;
-    if (c == 0) {
-      for (int i = 0; i < 16; ++i) v += newx[mm * 16 + i] * newx[mm * 16 + i];
-    } else if (rm.fast[mm]) {
-      const int which = (c - 1) / D.r, j = (c - 1) % D.r;   // 0: gate (A[4]), 1: up (A[5])
-      const void* A = L.A[4 + which];
-      if (A)
-        for (int i = 0; i < 16; ++i)
-          v += ld_w(A, (size_t)j * D.d + n0 + i, D.wbf16) * L.mlp_norm[n0 + i] * newx[mm * 16 + i];
+    // partial sums for the gate/up prologue: sum x^2 and the adapter-down of
+    // gate and up (fast rows): sum_n A[j][n] g_mlp[n] x[n]
+    const int bin = t % kBins;
+    for (int q = threadIdx.x; q < rm.M * PO; q += kGemvThreads) {
+      const int mm = q / PO, c = q % PO;
+      float v = 0.f;
+      if (c == 0) {
+        for (int i = 0; i < 16; ++i) v += newx[mm * 16 + i] * newx[mm * 16 + i];
+      } else if (rm.fast[mm]) {
+        const int which = (c - 1) / D.r, j = (c - 1) % D.r;   // 0: gate (A[4]), 1: up (A[5])
+        const void* A = L.A[4 + which];
+        if (A)
+          for (int i = 0; i < 16; ++i)
+            v += ld_w(A, (size_t)j * D.d + n0 + i, D.wbf16) * L.mlp_norm[n0 + i] * newx[mm * 16 + i];
+      }
+      if (c == 0 || rm.fast[mm]) add_agent(bin_o_at(ws, D, layer, bin, mm) + c, v);
     }
-    if (c == 0 || rm.fast[mm]) add_agent(bin_o_at(ws, D, layer, bin, mm) + c, v);
-  }
+    __syncthreads();
+  };
+  tg.run((ntiles - blockIdx.x + gridDim.x - 1) / gridDim.x, ptr, epi);
 }
 
 // ============================================================================
-// Kernel: gate/up projections (paired tiles), adapter-up, SwiGLU.
-// grid = F/16 tiles, block = 512.
+// Kernel: gate/up projections (the gate and up tiles of the same 16 rows, one
+// after the other), adapter-up, SwiGLU; partial sums of the down adapter's
+// down-projection.  Persistent tile GEMV, grid <= ffn/16.
 // ============================================================================
 template <int WB, int MT>
 __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int layer) {
@@ -1065,22 +1347,18 @@ __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, Ro
   __shared__ float act[256];
   __shared__ const float* xrow_s[kMaxRows];
   extern __shared__ __attribute__((aligned(16))) char dyn[];
-  const int n0 = blockIdx.x * 16;
-  const int lane = threadIdx.x & 63;
-  const size_t esz = WB ? 2 : 4;
+  const int ntiles = D.F / 16;
+  if ((int)blockIdx.x >= ntiles) return;
   if (io.mode == EX_EXIT) {
     bool all_exited = true;
-    for (int s = 0; s < rm.nseq; ++s) all_exited &= ws.exited[s] != 0;
+    for (int sq = 0; sq < rm.nseq; ++sq) all_exited &= ws.exited[sq] != 0;
     if (all_exited) return;
   }
-  const void* wrow[2] = {(const char*)L.pg + (size_t)blockIdx.x * 16 * D.d * esz,
-                         (const char*)L.pu + (size_t)blockIdx.x * 16 * D.d * esz};
-  GemvWave<WB, 2, MT, true> gw;
-  gw.begin(wrow, D.d);
+  const size_t tb = (size_t)16 * D.d * (WB ? 2 : 4);
+  TileGemv<WB, MT> tg;
+  tg.init(D.d, dyn);
+  tg.prime((const char*)L.pg + (size_t)blockIdx.x * tb);
   if (threadIdx.x < rm.M) xrow_s[threadIdx.x] = ws.X + (size_t)threadIdx.x * D.d;
-  __syncthreads();
-  f32x4_t acc[2];
-  gw.run(xrow_s, L.mlp_norm, rm.M, dyn, acc);
   const int PO = 1 + 2 * D.r;
   for (int q = threadIdx.x; q < rm.M * PO; q += kGemvThreads) {
     float a = 0.f;
@@ -1090,35 +1368,77 @@ __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, Ro
   }
   __syncthreads();
   if (threadIdx.x < rm.M) inv_rms[threadIdx.x] = rsqrtf(stat[threadIdx.x * PO] / D.d + D.eps);
-  gemv_reduce<2>(acc, rm.M, red, y);
-  const int e = threadIdx.x;
-  if (e < rm.M * 16) {
-    const int m = e >> 4, nn = n0 + (e & 15);
-    const float ir = inv_rms[m];
-    float g = y[e] * ir, u = y[256 + e] * ir;
-    if (rm.fast[m]) {
-      if (L.B[4] && L.A[4]) g += dot_row(L.B[4], nn, D.r, stat + m * PO + 1, D.wbf16) * ir;
-      if (L.B[5] && L.A[5]) u += dot_row(L.B[5], nn, D.r, stat + m * PO + 1 + D.r, D.wbf16) * ir;
-    }
-    const float a = silu(g) * u;
-    ws.ACT[(size_t)m * D.F + nn] = a;
-    act[e] = a;
-  }
+  tg.set_rows(xrow_s, L.mlp_norm, rm.M, D.d);
   __syncthreads();
-  // partials of the down adapter-down: sum_n A_d[j][n] a[n]
-  const int bin = blockIdx.x % kBins;
-  for (int q = threadIdx.x; q < rm.M * D.r; q += kGemvThreads) {
-    const int mm = q / D.r, j = q % D.r;
-    float v = 0.f;
-    if (rm.fast[mm] && L.A[6])
+  // local tiles 2i and 2i+1: the gate and up tiles of rows 16*t, t = blockIdx.x + i*gridDim.x
+  auto ptr = [&](int i) {
+    return (const char*)((i & 1) ? L.pu : L.pg) + (size_t)(blockIdx.x + (i >> 1) * gridDim.x) * tb;
+  };
+  f32x4_t acc_g = {0.f, 0.f, 0.f, 0.f};
+  auto epi = [&](int i, const f32x4_t& a) {
+    if (!(i & 1)) {
+      acc_g = a;
+      return;
+    }
+    const int t = blockIdx.x + (i >> 1) * gridDim.x;
+    f32x4_t acc[2] = {acc_g, a};
+    gemv_reduce<2>(acc, rm.M, red, y);
+    const int n0 = t * 16;
+    const int e = threadIdx.x;
+    if (e < rm.M * 16) {
+      const int m = e >> 4, nn = n0 + (e & 15);
+      const float ir = inv_rms[m];
+      float g = y[e] * ir, u = y[256 + e] * ir;
+      if (rm.fast[m]) {
+        if (L.B[4] && L.A[4]) g += dot_row(L.B[4], nn, D.r, stat + m * PO + 1, D.wbf16) * ir;
+        if (L.B[5] && L.A[5]) u += dot_row(L.B[5], nn, D.r, stat + m * PO + 1 + D.r, D.wbf16) * ir;
+      }
+      const float a = silu(g) * u;
+      ws.ACT[(size_t)m * D.F + nn] = a;
+      act[e] = a;
+    }
+    __syncthreads();
+    // partials of the down adapter-down: sum_n A_d[j][n] a[n]
+    const int bin = t % kBins;
+    for (int q = threadIdx.x; q < rm.M * D.r; q += kGemvThreads) {
+      const int mm = q / D.r, j = q % D.r;
+      if (!rm.fast[mm] || !L.A[6]) continue;
+      float v = 0.f;
       for (int i = 0; i < 16; ++i) v += ld_w(L.A[6], (size_t)j * D.F + n0 + i, D.wbf16) * act[mm * 16 + i];
-    if (rm.fast[mm] && L.A[6]) add_agent(bin_gu_at(ws, D, layer, bin, mm) + j, v);
+      add_agent(bin_gu_at(ws, D, layer, bin, mm) + j, v);
+    }
+    __syncthreads();
+  };
+  tg.run(2 * ((ntiles - blockIdx.x + gridDim.x - 1) / gridDim.x), ptr, epi);
+}
+
+// Partial sums entering layer `next` (sum x^2, sum pin*x, sum pin^2 of every
+// row) when no kernel updates the rows: every sequence has exited.  One
+// workgroup.
+__device__ void rows_unchanged_stats(const Dims& D, const RowMap& rm, const WS& ws, int next) {
+  __shared__ float red[kGemvWaves];
+  for (int m = 0; m < rm.M; ++m) {
+    float a = 0.f, b = 0.f, c = 0.f;
+    for (int i = threadIdx.x; i < D.d; i += blockDim.x) {
+      const float x = ws.X[(size_t)m * D.d + i];
+      const float p = rm.fast[m] ? ws.PIN[(size_t)m * D.d + i] : 0.f;
+      a += x * x; b += p * x; c += p * p;
+    }
+    a = block_sum(a, red);
+    b = block_sum(b, red);
+    c = block_sum(c, red);
+    if (threadIdx.x == 0) {
+      add_agent(bin_d_at(ws, next, 0, m) + 0, a);
+      add_agent(bin_d_at(ws, next, 0, m) + 1, b);
+      add_agent(bin_d_at(ws, next, 0, m) + 2, c);
+    }
+    __syncthreads();
   }
 }
 
 // ============================================================================
-// Kernel: down projection + residual add (+ adapter), partial sums for the
-// next layer's norm and the exit signal.  grid = d/16 tiles, block = 512.
+// Kernel: down projection + residual add (+ adapter); partial sums for the
+// next layer's norm and the exit signal.  Persistent tile GEMV, grid <= d/16.
 // ============================================================================
 template <int WB, int MT>
 __global__ __launch_bounds__(kGemvThreads) void k_down(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int layer) {
@@ -1128,61 +1448,68 @@ __global__ __launch_bounds__(kGemvThreads) void k_down(Dims D, LayerPtrs L, RowM
   __shared__ float newx[256], pin_s[256];
   __shared__ const float* xrow_s[kMaxRows];
   extern __shared__ __attribute__((aligned(16))) char dyn[];
-  const int n0 = blockIdx.x * 16;
-  const int lane = threadIdx.x & 63;
-  const size_t esz = WB ? 2 : 4;
-  bool all_exited = false;
+  const int ntiles = D.d / 16;
+  if ((int)blockIdx.x >= ntiles) return;
   if (io.mode == EX_EXIT) {
-    all_exited = true;
-    for (int s = 0; s < rm.nseq; ++s) all_exited &= ws.exited[s] != 0;
+    bool all_exited = true;
+    for (int sq = 0; sq < rm.nseq; ++sq) all_exited &= ws.exited[sq] != 0;
+    if (all_exited) {
+      if (blockIdx.x == 0) rows_unchanged_stats(D, rm, ws, layer + 1);
+      return;
+    }
   }
-  const int e = threadIdx.x;
-  if (!all_exited) {
-    const void* wrow[1] = {(const char*)L.pd + (size_t)blockIdx.x * 16 * D.F * esz};
-    GemvWave<WB, 1, MT, false> gw;
-    gw.begin(wrow, D.F);
-    if (threadIdx.x < rm.M) xrow_s[threadIdx.x] = ws.ACT + (size_t)threadIdx.x * D.F;
-    for (int q = threadIdx.x; q < rm.M * D.r; q += kGemvThreads) {
-      float a = 0.f;
+  const size_t tb = (size_t)16 * D.F * (WB ? 2 : 4);
+  auto tile_ptr = [&](int t) -> const char* { return (const char*)L.pd + (size_t)t * tb; };
+  TileGemv<WB, MT> tg;
+  tg.init(D.F, dyn);
+  tg.prime(tile_ptr(blockIdx.x));
+  if (threadIdx.x < rm.M) xrow_s[threadIdx.x] = ws.ACT + (size_t)threadIdx.x * D.F;
+  for (int q = threadIdx.x; q < rm.M * D.r; q += kGemvThreads) {
+    float a = 0.f;
 #pragma unroll
-      for (int b = 0; b < kBins; ++b) a += bin_gu_at(ws, D, layer, b, q / D.r)[q % D.r];
-      ud[q] = a;
-    }
-    __syncthreads();
-    f32x4_t acc[1];
-    gw.run(xrow_s, nullptr, rm.M, dyn, acc);
-    gemv_reduce<1>(acc, rm.M, red, y);
-  }
-  if (e < rm.M * 16) {
-    const int m = e >> 4, nn = n0 + (e & 15);
-    const int s = rm.seq[m];
-    const bool ex = ws.exited[s] != 0;
-    float x = ws.X[(size_t)m * D.d + nn];
-    if (!ex) {
-      x += y[e];
-      if (rm.fast[m] && L.B[6] && L.A[6]) x += dot_row(L.B[6], nn, D.r, ud + m * D.r, D.wbf16);
-      ws.X[(size_t)m * D.d + nn] = x;
-    }
-    newx[e] = x;
-    pin_s[e] = rm.fast[m] ? ws.PIN[(size_t)m * D.d + nn] : 0.f;
+    for (int b = 0; b < kBins; ++b) a += bin_gu_at(ws, D, layer, b, q / D.r)[q % D.r];
+    ud[q] = a;
   }
   __syncthreads();
-  const int bin = blockIdx.x % kBins;
-  for (int q = threadIdx.x; q < rm.M * 4; q += kGemvThreads) {
-    const int mm = q >> 2, c = q & 3;
-    float v = 0.f;
-    for (int i = 0; i < 16; ++i) {
-      const float x = newx[mm * 16 + i], p = pin_s[mm * 16 + i];
-      v += c == 0 ? x * x : (c == 1 ? p * x : (c == 2 ? p * p : 0.f));
+  tg.set_rows(xrow_s, nullptr, rm.M, D.F);
+  auto ptr = [&](int i) { return tile_ptr(blockIdx.x + i * gridDim.x); };
+  auto epi = [&](int i, const f32x4_t& a) {
+    const int t = blockIdx.x + i * gridDim.x;
+    f32x4_t acc[1] = {a};
+    gemv_reduce<1>(acc, rm.M, red, y);
+    const int n0 = t * 16;
+    const int e = threadIdx.x;
+    if (e < rm.M * 16) {
+      const int m = e >> 4, nn = n0 + (e & 15);
+      float x = ws.X[(size_t)m * D.d + nn];
+      if (!ws.exited[rm.seq[m]]) {
+        x += y[e];
+        if (rm.fast[m] && L.B[6] && L.A[6]) x += dot_row(L.B[6], nn, D.r, ud + m * D.r, D.wbf16);
+        ws.X[(size_t)m * D.d + nn] = x;
+      }
+      newx[e] = x;
+      pin_s[e] = rm.fast[m] ? ws.PIN[(size_t)m * D.d + nn] : 0.f;
     }
-    if (c < 3) add_agent(bin_d_at(ws, layer + 1, bin, mm) + c, v);
-  }
+    __syncthreads();
+    const int bin = t % kBins;
+    for (int q = threadIdx.x; q < rm.M * 3; q += kGemvThreads) {
+      const int mm = q / 3, c = q % 3;
+      float v = 0.f;
+      for (int i = 0; i < 16; ++i) {
+        const float x = newx[mm * 16 + i], p = pin_s[mm * 16 + i];
+        v += c == 0 ? x * x : (c == 1 ? p * x : p * p);
+      }
+      add_agent(bin_d_at(ws, layer + 1, bin, mm) + c, v);
+    }
+    __syncthreads();
+  };
+  tg.run((ntiles - blockIdx.x + gridDim.x - 1) / gridDim.x, ptr, epi);
 }
 
 // ============================================================================
-// Kernel: final norm + LM head + argmax; the last workgroup finishes the step
-// (tokens, exit bookkeeping, acceptance of a verified chunk).
-// grid = V/16 tiles, block = 512.
+// Kernel: final norm + LM head + argmax; the last workgroup to finish takes
+// the global arg-max and finishes the step (tokens, exit bookkeeping,
+// acceptance of a verified chunk).  Persistent tile GEMV, grid <= V/16.
 // ============================================================================
 template <int WB, int MT>
 __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_head, const float* final_norm, RowMap rm,
@@ -1196,12 +1523,13 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
   __shared__ int last_flag;
   __shared__ const float* xrow_s[kMaxRows];
   extern __shared__ __attribute__((aligned(16))) char dyn[];
-  const int n0 = blockIdx.x * 16;
+  if ((int)blockIdx.x >= n_tiles) return;
   const int lane = threadIdx.x & 63;
-  const size_t esz = WB ? 2 : 4;
-  const void* wrow[1] = {(const char*)lm_head + (size_t)blockIdx.x * 16 * D.d * esz};
-  GemvWave<WB, 1, MT, true> gw;
-  gw.begin(wrow, D.d);
+  const size_t tb = (size_t)16 * D.d * (WB ? 2 : 4);
+  auto tile_ptr = [&](int t) -> const char* { return (const char*)lm_head + (size_t)t * tb; };
+  TileGemv<WB, MT> tg;
+  tg.init(D.d, dyn);
+  tg.prime(tile_ptr(blockIdx.x));
   for (int q = threadIdx.x; q < rm.M * 4; q += kGemvThreads) {
     float a = 0.f;
 #pragma unroll
@@ -1214,10 +1542,10 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
     if (rm.head_all) {
       for (int m = 0; m < rm.M; ++m) hrow[nh++] = m;
     } else {
-      for (int s = 0; s < rm.nseq; ++s) {
-        const int f = rm.first[s], c = rm.cnt[s];
+      for (int sq = 0; sq < rm.nseq; ++sq) {
+        const int f = rm.first[sq], c = rm.cnt[sq];
         int pick = f;                       // slow row
-        if (rm.fast[f + c - 1] && (ws.exited[s] || rm.slow_of[f + c - 1] < 0)) pick = f + c - 1;
+        if (rm.fast[f + c - 1] && (ws.exited[sq] || rm.slow_of[f + c - 1] < 0)) pick = f + c - 1;
         hrow[nh++] = pick;
       }
     }
@@ -1230,30 +1558,34 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
   }
   __syncthreads();
   const int nh = nh_s;
-  f32x4_t acc[1];
-  gw.run(xrow_s, final_norm, nh, dyn, acc);
-  gemv_reduce<1>(acc, nh, red, y);
-  // logits and per-tile argmax (lowest index on ties)
-  const int e = threadIdx.x;
-  if (e < nh * 16) {
-    const int k = e >> 4, nn = n0 + (e & 15);
-    float z = y[e] * inv_rms[k];
-    if (nn >= D.V) z = -INFINITY;
-    else if (io.logits_out) io.logits_out[(size_t)k * D.V + nn] = z;
-    int idx = nn;
-    // reduce over the 16 consecutive lanes holding this row's tile
+  tg.set_rows(xrow_s, final_norm, nh, D.d);
+  auto ptr = [&](int i) { return tile_ptr(blockIdx.x + i * gridDim.x); };
+  auto epi = [&](int i, const f32x4_t& a) {
+    const int t = blockIdx.x + i * gridDim.x;
+    f32x4_t acc[1] = {a};
+    gemv_reduce<1>(acc, nh, red, y);
+    // logits and the tile's arg-max per head row (lowest index on ties)
+    const int e = threadIdx.x;
+    if (e < nh * 16) {
+      const int k = e >> 4, nn = t * 16 + (e & 15);
+      float z = y[e] * inv_rms[k];
+      if (nn >= D.V) z = -INFINITY;
+      else if (io.logits_out) io.logits_out[(size_t)k * D.V + nn] = z;
+      int idx = nn;
 #pragma unroll
-    for (int o = 8; o > 0; o >>= 1) {
-      const float z2 = __shfl_xor(z, o);
-      const int i2 = __shfl_xor(idx, o);
-      if (z2 > z || (z2 == z && i2 < idx)) { z = z2; idx = i2; }
+      for (int o = 8; o > 0; o >>= 1) {
+        const float z2 = __shfl_xor(z, o);
+        const int i2 = __shfl_xor(idx, o);
+        if (z2 > z || (z2 == z && i2 < idx)) { z = z2; idx = i2; }
+      }
+      if ((e & 15) == 0) {
+        st_agent(&ws.lm_val[(size_t)t * kMaxRows + k], z);
+        st_agent(&ws.lm_idx[(size_t)t * kMaxRows + k], idx);
+      }
     }
-    if ((e & 15) == 0) {
-      st_agent(&ws.lm_val[(size_t)blockIdx.x * kMaxRows + k], z);
-      st_agent(&ws.lm_idx[(size_t)blockIdx.x * kMaxRows + k], idx);
-    }
-  }
-  if (!arrive_last(ws.lm_cnt, n_tiles, &last_flag)) return;
+  };
+  tg.run((n_tiles - blockIdx.x + gridDim.x - 1) / gridDim.x, ptr, epi);
+  if (!arrive_last(ws.lm_cnt, gridDim.x, &last_flag)) return;
 
   // ---- last workgroup: global argmax per head row, then bookkeeping ----------
   __shared__ int best_s[kMaxRows];
@@ -1294,34 +1626,34 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
     return;
   }
   // decode step / draft step
-  for (int s = threadIdx.x; s < rm.nseq; s += kGemvThreads) {
-    const int f = rm.first[s] + rm.cnt[s] - 1;
-    io.next_token[s + io.draft_slot] = best_s[s];
-    const int t = io.positions[s] + rm.pos_offset;
-    if (rm.slow_of[f] >= 0 || !rm.fast[f]) kv.seq_lens[s] = t + 1;
+  for (int sq = threadIdx.x; sq < rm.nseq; sq += kGemvThreads) {
+    const int f = rm.first[sq] + rm.cnt[sq] - 1;
+    io.next_token[sq + io.draft_slot] = best_s[sq];
+    const int t = io.positions[sq] + rm.pos_offset;
+    if (rm.slow_of[f] >= 0 || !rm.fast[f]) kv.seq_lens[sq] = t + 1;
     if (rm.fast[f] && rm.slow_of[f] >= 0) {
       // signal of the last layer
       const float dot = ssum[f * 4 + 1], pin2 = ssum[f * 4 + 2], pp = ssum[f * 4 + 0];
-      ws.sig[s * D.n_layers + D.n_layers - 1] = ws.exited[s] ? 0.f : dot * rsqrtf(fmaxf(pin2 * pp, 1e-30f));
+      ws.sig[sq * D.n_layers + D.n_layers - 1] = ws.exited[sq] ? 0.f : dot * rsqrtf(fmaxf(pin2 * pp, 1e-30f));
     }
-    if (io.exit_b_out) io.exit_b_out[s] = ws.exitb[s];
-    if (io.advance) io.positions[s] = io.positions[s] + 1;
+    if (io.exit_b_out) io.exit_b_out[sq] = ws.exitb[sq];
+    if (io.advance) io.positions[sq] = io.positions[sq] + 1;
   }
   __syncthreads();
   if (io.signal_out) {
     for (int q = threadIdx.x; q < rm.nseq * D.n_layers; q += kGemvThreads) {
-      const int s = q / D.n_layers, l = q % D.n_layers;
-      const int f = rm.first[s] + rm.cnt[s] - 1;
+      const int sq = q / D.n_layers, l = q % D.n_layers;
+      const int f = rm.first[sq] + rm.cnt[sq] - 1;
       float v = ws.sig[q];
       // layers after an exit were not run
-      if (!rm.fast[f] || rm.slow_of[f] < 0 || (ws.exited[s] && l >= ws.exitb[s])) v = 0.f;
+      if (!rm.fast[f] || rm.slow_of[f] < 0 || (ws.exited[sq] && l >= ws.exitb[sq])) v = 0.f;
       io.signal_out[q] = v;
     }
   }
   if (io.h_out || io.p_out) {
     for (int q = threadIdx.x; q < rm.nseq * D.d; q += kGemvThreads) {
-      const int s = q / D.d, i = q % D.d;
-      const int f = rm.first[s], c = rm.cnt[s];
+      const int sq = q / D.d, i = q % D.d;
+      const int f = rm.first[sq], c = rm.cnt[sq];
       if (io.h_out) io.h_out[q] = ws.X[(size_t)f * D.d + i];
       if (io.p_out) io.p_out[q] = ws.X[(size_t)(f + c - 1) * D.d + i];
     }
