@@ -218,22 +218,22 @@ def prompt_ids(cfg: ModelConfig, n: int, *, seed: Optional[int] = None, stream: 
     return g.integers(0, cfg.vocab, size=n, dtype=np.int64).astype(np.int32)
 
 
-def synthetic_kv(cfg: ModelConfig, length: int, *, seq: int = 0, layers: Optional[Iterable[int]] = None
-                 ) -> Dict[int, Tuple[np.ndarray, np.ndarray]]:
+def synthetic_kv(cfg: ModelConfig, length: int, *, seq: int = 0, layers: Optional[Iterable[int]] = None,
+                 threads: int = 1) -> Dict[int, Tuple[np.ndarray, np.ndarray]]:
     """Seeded stand-in KV cache content: per layer ``(K, V)`` each
     ``[length][n_heads][head_dim]`` drawn N(0, 1) and stored in the cache dtype."""
-    layers = range(cfg.n_layers) if layers is None else layers
-    out = {}
-    for l in layers:
-        kv = []
-        for which in ("K", "V"):
-            a = np.empty((length, cfg.n_heads, cfg.head_dim), np.float32)
-            _stream(cfg.seed, f"kv.{seq}.{l}.{which}").standard_normal(out=a, dtype=np.float32)
-            if cfg.kvdtype == "bf16":
-                a = bf16_round(a)
-            kv.append(a)
-        out[l] = (kv[0], kv[1])
-    return out
+    layers = list(range(cfg.n_layers) if layers is None else layers)
+
+    def one(lw):
+        l, which = lw
+        a = np.empty((length, cfg.n_heads, cfg.head_dim), np.float32)
+        _stream(cfg.seed, f"kv.{seq}.{l}.{which}").standard_normal(out=a, dtype=np.float32)
+        return bf16_round(a) if cfg.kvdtype == "bf16" else a
+
+    jobs = [(l, w) for l in layers for w in ("K", "V")]
+    with ThreadPoolExecutor(max(1, threads)) as ex:
+        arrs = list(ex.map(one, jobs))
+    return {l: (arrs[2 * i], arrs[2 * i + 1]) for i, l in enumerate(layers)}
 
 
 def block_table(n_seqs: int, blocks_per_seq: int, *, seed: int = 0, shuffle: bool = True) -> np.ndarray:

@@ -1,0 +1,206 @@
+"""GPU parity at the benchmarked sizes of the dense model (Phi-3-mini shape:
+32 layers, d 3072, 32 heads x 96, SwiGLU 8192, vocab 32064, rank 16, bf16),
+through the C ABI and in the launch configuration bench.py times, against the
+float64 oracle on sampled outputs:
+
+  * the dual-stream step at batch 1 (OBSERVE gates at every boundary);
+  * a draft of 4 tokens from the fast stream exiting at layer 8 and the
+    verification of the 5-token chunk;
+  * one dual-stream step of 8 sequences with 4096-token paged contexts (seeded
+    synthetic cache content), checked on two of the sequences.
+
+The oracle's weights are the same seeded arrays the GPU consumes."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import KVCache, Oracle
+from oracle.decoder import argmax_first, round_to_cache
+from paper_2502_02040_amd import Model, PagedKV
+from tests.gpu_harness import Tally, shuffled_table
+
+pytestmark = pytest.mark.gpu
+
+CFG = synth.CONFIGS["phi3"]
+TOL = 2e-2
+PROMPT = 16
+CTX_B = 4096
+
+
+@pytest.fixture(scope="module")
+def world():
+    w = synth.make_weights(CFG)
+    model = Model(CFG, w, max_batch=8, max_chunk=16, max_ctx=CTX_B + 16)
+    orc = Oracle(CFG, w)
+    del w
+    yield model, orc
+    del model, orc
+    torch.cuda.empty_cache()
+
+
+def _prefill(model, orc, kv, cache, prompt, t):
+    dev = torch.device("cuda")
+    pos = torch.zeros(1, dtype=torch.int32, device=dev)
+    targets = torch.zeros(16, dtype=torch.int32, device=dev)
+    chunk = torch.tensor(prompt, dtype=torch.int32, device=dev)
+    model.verify(chunk, len(prompt), pos, kv.desc(), targets)
+    torch.cuda.synchronize()
+    ref = orc.slow_chunk(list(prompt), 0, cache)
+    got = targets[:len(prompt)].cpu().numpy()
+    for i in range(len(prompt)):
+        t.token(int(got[i]), ref[i], TOL, f"prefill row {i}")
+    return int(got[-1]), pos
+
+
+def _check_cache(kv, cache, seq, start, end, t, layers, what):
+    for l in layers:
+        K, V = kv.read(seq, l, start, end)
+        t.rel(K, cache.K[l][start:end], TOL, f"{what} K layer {l}")
+        t.rel(V, cache.V[l][start:end], TOL, f"{what} V layer {l}")
+
+
+def test_phi3_dual_step(world):
+    model, orc = world
+    t = Tally()
+    kv = PagedKV(CFG, 1, 64, block_size=16, block_table=shuffled_table(1, 64, 16, 7))
+    cache = KVCache(CFG, 64)
+    prompt = list(synth.prompt_ids(CFG, PROMPT))
+    tok, pos_d = _prefill(model, orc, kv, cache, prompt, t)
+    _check_cache(kv, cache, 0, 0, PROMPT, t, (0, 15, 31), "prefill")
+    dev = torch.device("cuda")
+    N = CFG.n_layers
+    gates = list(range(1, N))
+    tok_d = torch.tensor([tok], dtype=torch.int32, device=dev)
+    nxt = torch.zeros(1, dtype=torch.int32, device=dev)
+    exb = torch.zeros(1, dtype=torch.int32, device=dev)
+    sig = torch.zeros(N, dtype=torch.float32, device=dev)
+    logits = torch.zeros(CFG.vocab, dtype=torch.float32, device=dev)
+    h_out = torch.zeros(CFG.d_model, dtype=torch.float32, device=dev)
+    p_out = torch.zeros(CFG.d_model, dtype=torch.float32, device=dev)
+    for step in range(3):
+        pos = PROMPT + step
+        model.decode_step(tok_d, pos_d, kv.desc(), gates=gates, tau=0.9, mode="observe", next_token=nxt,
+                          exit_boundary=exb, signal=sig, logits=logits, h_out=h_out, p_out=p_out, advance=True)
+        torch.cuda.synchronize()
+        r = orc.decode_step(int(tok_d.item()), pos, cache, gates=gates, tau=0.9, mode="observe")
+        t.rel(logits.cpu().numpy(), r.logits, TOL, f"step {step} logits")
+        t.rel(h_out.cpu().numpy(), r.h, TOL, f"step {step} h")
+        t.rel(p_out.cpu().numpy(), r.p, TOL, f"step {step} p")
+        assert np.max(np.abs(sig.cpu().numpy() - r.signal)) <= TOL, f"step {step} signal"
+        if all(abs(r.signal[b - 1] - 0.9) > TOL for b in gates):
+            assert int(exb.item()) == r.exit_boundary
+        t.token(int(nxt.item()), r.logits, TOL, f"step {step} token")
+        _check_cache(kv, cache, 0, pos, pos + 1, t, (0, 7, 31), f"step {step}")
+        tok_d.copy_(nxt)
+    assert t.compared >= 5
+
+
+def _oracle_draft_logits(orc, token, pos, cache, exit_layer, gamma):
+    """The oracle's draft (Sec. 2.3.2) with the logits of every draft position."""
+    cfg = orc.cfg
+    scK = [np.zeros((gamma, cfg.n_heads, cfg.head_dim)) for _ in range(exit_layer)]
+    scV = [np.zeros((gamma, cfg.n_heads, cfg.head_dim)) for _ in range(exit_layer)]
+    out, zs, tok = [], [], token
+    for j in range(gamma):
+        p = orc.w["embed"][tok].copy()
+        for l in range(exit_layer):
+            ctxK = np.concatenate([cache.K[l][:pos], scK[l][:j]], axis=0)
+            ctxV = np.concatenate([cache.V[l][:pos], scV[l][:j]], axis=0)
+            p, (k, v) = orc._fast_layer(l, p, pos + j, ctxK, ctxV)
+            scK[l][j] = round_to_cache(k, cfg.kvdtype)
+            scV[l][j] = round_to_cache(v, cfg.kvdtype)
+        z = orc.head_logits(p)
+        tok = argmax_first(z)
+        out.append(tok)
+        zs.append(z)
+    return out, zs
+
+
+def test_phi3_draft_and_verify(world):
+    """gamma = 4 drafts from the fast stream exiting at layer 8, then the
+    5-row verification chunk through all 32 layers."""
+    model, orc = world
+    gamma, kL = 4, 8
+    t = Tally()
+    kv = PagedKV(CFG, 1, 64, block_size=16, block_table=shuffled_table(1, 64, 16, 9))
+    cache = KVCache(CFG, 64)
+    prompt = list(synth.prompt_ids(CFG, PROMPT, stream="spec"))
+    tok, pos_d = _prefill(model, orc, kv, cache, prompt, t)
+    dev = torch.device("cuda")
+    buf = torch.zeros(gamma + 1, dtype=torch.int32, device=dev)
+    buf[0] = tok
+    targets = torch.zeros(gamma + 1, dtype=torch.int32, device=dev)
+    n_acc = torch.zeros(1, dtype=torch.int32, device=dev)
+    model.draft(buf[0:1], pos_d, kL, gamma, kv.desc(), buf[1:])
+    torch.cuda.synchronize()
+    drafts = buf[1:].cpu().numpy().tolist()
+    ref_d, ref_z = _oracle_draft_logits(orc, tok, PROMPT, cache, kL, gamma)
+    for j in range(gamma):
+        t.token(drafts[j], ref_z[j], TOL, f"draft {j}")
+        if drafts[j] != ref_d[j]:
+            break   # the next drafts start from different tokens
+    model.verify(buf, gamma + 1, pos_d, kv.desc(), targets, n_accepted=n_acc, bonus=buf[0:1])
+    torch.cuda.synchronize()
+    tg = targets.cpu().numpy().tolist()
+    ref = orc.slow_chunk([tok] + drafts, PROMPT, cache)
+    for i in range(gamma + 1):
+        t.token(tg[i], ref[i], TOL, f"target {i}")
+    j = 0
+    while j < gamma and drafts[j] == tg[j]:
+        j += 1
+    assert int(n_acc.item()) == j and int(buf[0].item()) == tg[j]
+    assert int(pos_d.item()) == PROMPT + j + 1 == int(kv.seq_lens[0].item())
+    _check_cache(kv, cache, 0, PROMPT, PROMPT + j + 1, t, (0, 8, 31), "verify")
+    assert t.compared >= 3
+
+
+def test_batch8_long_context_step(world):
+    """8 sequences, 4096-token contexts each (seeded N(0,1) cache content,
+    shuffled block table), one dual-stream step; sequences 0 and 5 are
+    recomputed by the oracle."""
+    model, orc = world
+    B, sampled = 8, (0, 5)
+    t = Tally()
+    max_ctx = CTX_B + 16
+    bps = (max_ctx + 15) // 16
+    kv = PagedKV(CFG, B, max_ctx, block_size=16, block_table=synth.block_table(B, bps, seed=3))
+    caches = {}
+    for s in range(B):
+        content = synth.synthetic_kv(CFG, CTX_B, seq=s, threads=16)
+        for l, (K, V) in content.items():
+            kv.load(s, l, K, V)
+        if s in sampled:
+            c = KVCache(CFG, max_ctx)
+            for l, (K, V) in content.items():
+                c.load(l, K, V)
+            caches[s] = c
+        del content
+    kv.seq_lens.fill_(CTX_B)
+    dev = torch.device("cuda")
+    toks = synth.prompt_ids(CFG, B, stream="batch")
+    tok_d = torch.tensor(toks, dtype=torch.int32, device=dev)
+    pos_d = torch.full((B,), CTX_B, dtype=torch.int32, device=dev)
+    N = CFG.n_layers
+    gates = list(range(1, N))
+    nxt = torch.zeros(B, dtype=torch.int32, device=dev)
+    sig = torch.zeros(B * N, dtype=torch.float32, device=dev)
+    logits = torch.zeros(B * CFG.vocab, dtype=torch.float32, device=dev)
+    h_out = torch.zeros(B * CFG.d_model, dtype=torch.float32, device=dev)
+    p_out = torch.zeros(B * CFG.d_model, dtype=torch.float32, device=dev)
+    model.decode_step(tok_d, pos_d, kv.desc(), gates=gates, tau=0.9, mode="observe", next_token=nxt, signal=sig,
+                      logits=logits, h_out=h_out, p_out=p_out, advance=True)
+    torch.cuda.synchronize()
+    assert pos_d.cpu().numpy().tolist() == [CTX_B + 1] * B
+    L = logits.cpu().numpy().reshape(B, -1)
+    Hh = h_out.cpu().numpy().reshape(B, -1)
+    Pp = p_out.cpu().numpy().reshape(B, -1)
+    S = sig.cpu().numpy().reshape(B, N)
+    for s in sampled:
+        r = orc.decode_step(int(toks[s]), CTX_B, caches[s], gates=gates, tau=0.9, mode="observe")
+        t.rel(L[s], r.logits, TOL, f"seq {s} logits")
+        t.rel(Hh[s], r.h, TOL, f"seq {s} h")
+        t.rel(Pp[s], r.p, TOL, f"seq {s} p")
+        assert np.max(np.abs(S[s] - r.signal)) <= TOL, f"seq {s} signal"
+        t.token(int(nxt[s].item()), r.logits, TOL, f"seq {s} token")
+        _check_cache(kv, caches[s], s, CTX_B, CTX_B + 1, t, (0, 16, 31), f"seq {s}")

@@ -1,0 +1,81 @@
+"""GPU parity of the mixture-of-experts step at the benchmarked size
+(OLMoE shape: 16 layers, d 2048, 16 heads x 128, 64 experts of width 1024,
+top 8, vocab 50304, rank 16, bf16) with every expert in pinned host memory and
+a 16-slot HBM cache per layer (ahead-of-time policy), against the float64
+oracle: slow routing, predictions, logits, hidden states and the cache, for
+two decode steps after an 8-token prefill."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import KVCache, Oracle
+from paper_2502_02040_amd import Model, PagedKV
+from tests.gpu_harness import Tally, shuffled_table
+from tests.test_gpu_moe import topk_decidable
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+
+
+def test_olmoe_dual_step():
+    cfg = synth.CONFIGS["olmoe"]
+    N, K = cfg.n_layers, cfg.top_k
+    w = synth.make_weights(cfg)
+    model = Model(cfg, w, max_batch=1, max_chunk=16, max_ctx=32, expert_slots=16)
+    model.moe_set_policy("ahead_of_time")
+    orc = Oracle(cfg, w)
+    del w
+    t = Tally()
+    dev = torch.device("cuda")
+    kv = PagedKV(cfg, 1, 32, block_size=16, block_table=shuffled_table(1, 32, 16, 2))
+    cache = KVCache(cfg, 32)
+    prompt = list(synth.prompt_ids(cfg, 8))
+    ref = orc.slow_chunk(prompt, 0, cache)
+    pos = torch.zeros(1, dtype=torch.int32, device=dev)
+    nxt = torch.zeros(1, dtype=torch.int32, device=dev)
+    for i, tok in enumerate(prompt):
+        model.decode_step(torch.tensor([tok], dtype=torch.int32, device=dev), pos, kv.desc(), dual=False,
+                          next_token=nxt, advance=True)
+        torch.cuda.synchronize()
+        t.token(int(nxt.item()), ref[i], TOL, f"prefill row {i}")
+    model.moe_reset()
+    slow = torch.zeros(N * K, dtype=torch.int32, device=dev)
+    pred = torch.zeros(N * K, dtype=torch.int32, device=dev)
+    logits = torch.zeros(cfg.vocab, dtype=torch.float32, device=dev)
+    h_out = torch.zeros(cfg.d_model, dtype=torch.float32, device=dev)
+    p_out = torch.zeros(cfg.d_model, dtype=torch.float32, device=dev)
+    tok_d = nxt.clone()
+    for step in range(2):
+        p0 = len(prompt) + step
+        model.decode_step(tok_d, pos, kv.desc(), mode="off", next_token=nxt, logits=logits, h_out=h_out,
+                          p_out=p_out, advance=True, slow_experts=slow, pred_experts=pred)
+        torch.cuda.synchronize()
+        r = orc.decode_step(int(tok_d.item()), p0, cache, mode="off")
+        gs = slow.cpu().numpy().reshape(N, K)
+        gp = pred.cpu().numpy().reshape(N, K)
+        for l in range(N):
+            same = set(gs[l]) == set(r.slow_experts[l])
+            if topk_decidable(r.router_logits[l], K, TOL):
+                t.compared += 1
+                assert same, f"step {step} layer {l}: slow experts"
+            else:
+                t.skipped += 1
+                if not same:
+                    return
+            if r.pred_experts[l][0] >= 0 and topk_decidable(r.pred_logits[l], K, TOL):
+                t.compared += 1
+                assert set(gp[l]) == set(r.pred_experts[l]), f"step {step} layer {l}: predicted experts"
+        t.rel(logits.cpu().numpy(), r.logits, TOL, f"step {step} logits")
+        t.rel(h_out.cpu().numpy(), r.h, TOL, f"step {step} h")
+        t.rel(p_out.cpu().numpy(), r.p, TOL, f"step {step} p")
+        t.token(int(nxt.item()), r.logits, TOL, f"step {step} token")
+        for l in (0, 8, 15):
+            Kg, Vg = kv.read(0, l, p0, p0 + 1)
+            t.rel(Kg, cache.K[l][p0:p0 + 1], TOL, f"step {step} K layer {l}")
+            t.rel(Vg, cache.V[l][p0:p0 + 1], TOL, f"step {step} V layer {l}")
+        tok_d.copy_(nxt)
+    st = model.moe_stats()
+    assert st["hits"] + st["misses"] == 2 * N * K
+    assert t.compared >= 8
