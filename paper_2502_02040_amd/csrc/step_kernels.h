@@ -413,9 +413,18 @@ struct TileGemv {
     for (int j = 0; j < kChunk; ++j) dst[j] = ld_glob(base + (size_t)min(sb + j, s1 - 1) * 1024);
   }
 
-  // first chunk of the first tile
-  __device__ __forceinline__ void prime(const char* tile) {
-    if (s0 < s1) load(tile + (threadIdx.x & 63) * 16, s0, w);
+  // The first two chunks of the workgroup's chunk sequence (tile i starts at
+  // ptr(i)), put in flight before the kernel's prologue.
+  template <class Ptr>
+  __device__ __forceinline__ void prime(int n_local, const Ptr& ptr) {
+    if (s0 >= s1 || n_local <= 0) return;
+    const int lo16 = (threadIdx.x & 63) * 16;
+    // second chunk: in the first tile, else the next tile, else repeats of the last block
+    const bool next_tile = nchunks == 1 && n_local > 1;
+    const char* b2 = next_tile ? ptr(1) : ptr(0);
+    const int sb2 = nchunks > 1 ? s0 + kChunk : (next_tile ? s0 : s1);
+    load(ptr(0) + lo16, s0, w);
+    load(b2 + lo16, sb2, w2);
   }
 
   // Activation rows (rows >= M repeat row 0), multiplied by `gn` when given.
@@ -461,16 +470,104 @@ struct TileGemv {
     }
   }
 
-  // One chunk of steps [sb, sb+8) ∩ [.., s1): the next chunk's weights (nbase,
-  // nsb) are put in flight, then the MFMAs consume wcur.
-  __device__ __forceinline__ void chunk(int sb, const char* nbase, int nsb, const u32x4_t (&wcur)[kChunk],
-                                        u32x4_t (&wnext)[kChunk], f32x4_t& acc) const {
+  // ---- resident rows in two halves (2-row class) ---------------------------
+  // Loads are waited for in issue order, so anything a kernel needs before
+  // its weights arrive must be issued before prime().  load_pieces issues this
+  // wave's activation pieces of the candidate rows (and the gain) into
+  // registers; store_pieces stages them into LDS after prime(), row m taken
+  // from candidate sel[m].  Pieces past PM per lane (very long reductions) are
+  // loaded and staged by store_pieces itself.
+  template <int PM>
+  struct Pieces {
+    float4 v[PM][MT];
+    float4 g[PM];
+  };
+
+  template <int PM>
+  __device__ __forceinline__ void load_pieces(const float* const (&rows)[MT], const float* gn, Pieces<PM>& xp) const {
+    const int lane = threadIdx.x & 63;
+    const int npc = (s1 - s0) * P;
+#pragma unroll
+    for (int p = 0; p < PM; ++p) {
+      const int q = lane + 64 * p;
+      const int k = (s0 < s1 ? s0 * KSTEP : 0) + 4 * (q < npc ? q : 0);
+#pragma unroll
+      for (int m = 0; m < MT; ++m) xp.v[p][m] = ldg4(rows[m] + k);
+      xp.g[p] = ldg4((gn ? gn : rows[0]) + k);   // unconditional (ignored without a gain)
+    }
+  }
+
+  __device__ __forceinline__ void put_piece(int k, int m, float4 v) const {
+    const int st = k / KSTEP, e = k - st * KSTEP;
+    if constexpr (WB) {
+      uint16_t* hi = (uint16_t*)xl;
+      uint16_t* lo = hi + nsteps * MT * 32;
+      const float xs[4] = {v.x, v.y, v.z, v.w};
+      uint32_t h[4], l[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        h[q] = f32_to_bf16_bits(xs[q]);
+        l[q] = f32_to_bf16_bits(xs[q] - __uint_as_float(h[q] << 16));
+      }
+      const int o = (st * MT + m) * 32 + e;
+      *(uint2*)(hi + o) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+      *(uint2*)(lo + o) = make_uint2(l[0] | (l[1] << 16), l[2] | (l[3] << 16));
+    } else {
+      *(float4*)((float*)xl + (st * MT + m) * 16 + e) = v;
+    }
+  }
+
+  template <int PM>
+  __device__ __forceinline__ void store_pieces(const Pieces<PM>& xp, const float* const (&rows)[MT], const float* gn,
+                                               const int (&sel)[MT]) {
+    const int lane = threadIdx.x & 63;
+    const int npc = (s1 - s0) * P;
+#pragma unroll
+    for (int p = 0; p < PM; ++p) {
+      const int q = lane + 64 * p;
+      if (q < npc) {
+        const int k = s0 * KSTEP + 4 * q;
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+          float4 v = xp.v[p][0];
+#pragma unroll
+          for (int c = 1; c < MT; ++c)
+            if (sel[m] == c) v = xp.v[p][c];
+          if (gn) {
+            const float4 g = xp.g[p];
+            v.x *= g.x; v.y *= g.y; v.z *= g.z; v.w *= g.w;
+          }
+          put_piece(k, m, v);
+        }
+      }
+    }
+    for (int q = lane + 64 * PM; q < npc; q += 64) {
+      const int k = s0 * KSTEP + 4 * q;
+      const float4 g = gn ? ldg4(gn + k) : make_float4(1.f, 1.f, 1.f, 1.f);
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+        float4 v = ldg4(rows[0] + k);
+#pragma unroll
+        for (int c = 1; c < MT; ++c)
+          if (sel[m] == c) v = ldg4(rows[c] + k);
+        v.x *= g.x; v.y *= g.y; v.z *= g.z; v.w *= g.w;
+        put_piece(k, m, v);
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+
+  // One chunk of steps [sb, sb+8) ∩ [.., s1): the MFMAs consume buf, then buf
+  // is refilled with the chunk two ahead (nbase, nsb), so two chunks are in
+  // flight while the wave multiplies.
+  __device__ __forceinline__ void chunk(int sb, const char* nbase, int nsb, u32x4_t (&buf)[kChunk], f32x4_t& acc) const {
     const int lane = threadIdx.x & 63;
     const int mr = lane & 15, grp = lane >> 4;
     const int mread = mr < MT ? mr : MT - 1;
     const int nst = min(kChunk, s1 - sb);
     if constexpr (XRES) {
-      load(nbase, nsb, wnext);
 #pragma unroll
       for (int jj = 0; jj < kChunk; ++jj) {
         const int st = min(sb + jj, nsteps - 1);
@@ -481,21 +578,20 @@ struct TileGemv {
           const int o = (st * MT + mread) * 32 + 8 * grp;
           u32x4_t h = *(const u32x4_t*)(hi + o), l = *(const u32x4_t*)(lo + o);
           if (!on) { h = u32x4_t{0u, 0u, 0u, 0u}; l = h; }
-          const bf16x8_t bw = __builtin_bit_cast(bf16x8_t, wcur[jj]);
+          const bf16x8_t bw = __builtin_bit_cast(bf16x8_t, buf[jj]);
           acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, h), bw, acc, 0, 0, 0);
           acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, l), bw, acc, 0, 0, 0);
         } else {
           float4 a = *(const float4*)((const float*)xl + (st * MT + mread) * 16 + 4 * grp);
           if (!on) a = make_float4(0.f, 0.f, 0.f, 0.f);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, __uint_as_float(wcur[jj][0]), acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, __uint_as_float(wcur[jj][1]), acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, __uint_as_float(wcur[jj][2]), acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, __uint_as_float(wcur[jj][3]), acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, __uint_as_float(buf[jj][0]), acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, __uint_as_float(buf[jj][1]), acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, __uint_as_float(buf[jj][2]), acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, __uint_as_float(buf[jj][3]), acc, 0, 0, 0);
         }
       }
     } else {
-      // stage this chunk's activations (loaded before the weight prefetch, so
-      // waiting for them never waits for the prefetch)
+      // stage this chunk's activations
       const int q = WB ? lane : (lane & 31);
       const bool live = q < nst * P;
       const int kq = sb * KSTEP + 4 * (live ? q : 0);
@@ -504,9 +600,6 @@ struct TileGemv {
       if (gain) gv = ldg4(gain + kq);
 #pragma unroll
       for (int m = 0; m < MT; ++m) xv[m] = ldg4(xr[m] + kq);
-      __builtin_amdgcn_sched_barrier(0);
-      load(nbase, nsb, wnext);
-      __builtin_amdgcn_sched_barrier(0);
       char* my = xl;
       const int j = q / P, e = (q % P) * 4;
 #pragma unroll
@@ -544,25 +637,26 @@ struct TileGemv {
           const int o = (jj * MT + mread) * 32 + 8 * grp;
           const bf16x8_t a_hi = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(hi + o));
           const bf16x8_t a_lo = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(lo + o));
-          const bf16x8_t bw = __builtin_bit_cast(bf16x8_t, wcur[jj]);
+          const bf16x8_t bw = __builtin_bit_cast(bf16x8_t, buf[jj]);
           acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_hi, bw, acc, 0, 0, 0);
           acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_lo, bw, acc, 0, 0, 0);
         } else {
           const float4 a = *(const float4*)((const float*)my + (jj * MT + mread) * 16 + 4 * grp);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, __uint_as_float(wcur[jj][0]), acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, __uint_as_float(wcur[jj][1]), acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, __uint_as_float(wcur[jj][2]), acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, __uint_as_float(wcur[jj][3]), acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, __uint_as_float(buf[jj][0]), acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, __uint_as_float(buf[jj][1]), acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, __uint_as_float(buf[jj][2]), acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, __uint_as_float(buf[jj][3]), acc, 0, 0, 0);
         }
       }
       __builtin_amdgcn_wave_barrier();
     }
+    load(nbase, nsb, buf);
   }
 
   // Stream the workgroup's tiles: local tile i (i < n_local) starts at
   // ptr(i).  When every wave has finished tile i, epi(i, acc) runs
-  // workgroup-wide (it reduces the per-wave accumulators); the next tile's
-  // first chunk is already in flight by then.
+  // workgroup-wide (it reduces the per-wave accumulators); later chunks are
+  // in flight by then.  Chunk c of the sequence is in w (c even) or w2 (c odd).
   template <class Ptr, class Epi>
   __device__ __forceinline__ void run(int n_local, const Ptr& ptr, Epi& epi) {
     f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
@@ -571,34 +665,37 @@ struct TileGemv {
       return;
     }
     const int lo16 = (threadIdx.x & 63) * 16;
-    const char* cur = ptr(0) + lo16;
-    int i = 0, k = 0;
+    int i = 0, k = 0;     // current chunk
+    int i2 = 0, k2 = 0;   // the chunk two ahead
+    for (int a = 0; a < 2; ++a)
+      if (++k2 == nchunks) { k2 = 0; ++i2; }
+    const char* cur_tile = ptr(0);
     for (;;) {
       {
-        int ni = i, nk = k + 1;
-        if (nk == nchunks) { nk = 0; ++ni; }
-        const bool more = ni < n_local;
-        const char* nb = more && nk == 0 ? ptr(ni) + lo16 : cur;
-        chunk(s0 + k * kChunk, nb, more ? s0 + nk * kChunk : s1, w, w2, acc);
-        if (nk == 0) {
+        const bool more2 = i2 < n_local;
+        const char* nb = more2 ? ptr(i2) + lo16 : cur_tile + lo16;
+        chunk(s0 + k * kChunk, nb, more2 ? s0 + k2 * kChunk : s1, w, acc);
+        if (k == nchunks - 1) {
           epi(i, acc);
           acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
         }
-        if (!more) break;
-        i = ni; k = nk; cur = nb;
+        if (++k == nchunks) { k = 0; ++i; }
+        if (++k2 == nchunks) { k2 = 0; ++i2; }
+        if (i >= n_local) break;
+        if (k == 0) cur_tile = ptr(i);
       }
       {
-        int ni = i, nk = k + 1;
-        if (nk == nchunks) { nk = 0; ++ni; }
-        const bool more = ni < n_local;
-        const char* nb = more && nk == 0 ? ptr(ni) + lo16 : cur;
-        chunk(s0 + k * kChunk, nb, more ? s0 + nk * kChunk : s1, w2, w, acc);
-        if (nk == 0) {
+        const bool more2 = i2 < n_local;
+        const char* nb = more2 ? ptr(i2) + lo16 : cur_tile + lo16;
+        chunk(s0 + k * kChunk, nb, more2 ? s0 + k2 * kChunk : s1, w2, acc);
+        if (k == nchunks - 1) {
           epi(i, acc);
           acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
         }
-        if (!more) break;
-        i = ni; k = nk; cur = nb;
+        if (++k == nchunks) { k = 0; ++i; }
+        if (++k2 == nchunks) { k2 = 0; ++i2; }
+        if (i >= n_local) break;
+        if (k == 0) cur_tile = ptr(i);
       }
     }
   }
@@ -632,6 +729,65 @@ __device__ __forceinline__ float dot_row(const void* W, size_t row, int r, const
   }
 #pragma unroll 8
   for (int j = 0; j < r; ++j) v += ld_w(W, b + j, wb) * u[j];
+  return v;
+}
+
+// The same with the weight dtype fixed at compile time (no branch between
+// two loads, which would make the wave wait for every load in flight).
+template <int WB>
+__device__ __forceinline__ float ld_wt(const void* p, size_t i) {
+  if constexpr (WB) return bf16_to_f32(((const uint16_t*)p)[i]);
+  else return ((const float*)p)[i];
+}
+template <int WB>
+__device__ __forceinline__ float dot_row_t(const void* W, size_t row, int r, const float* u) {
+  float v = 0.f;
+  const size_t b = row * r;
+  if constexpr (WB) {
+    if ((r & 7) == 0) {
+      const u32x4_t* p = (const u32x4_t*)((const uint16_t*)W + b);
+      for (int j = 0; j < r; j += 8) {
+        const u32x4_t w = p[j / 8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v += bf16lo(w[i]) * u[j + 2 * i] + bf16hi(w[i]) * u[j + 2 * i + 1];
+      }
+      return v;
+    }
+  } else {
+    if ((r & 3) == 0) {
+      const float4* p = (const float4*)((const float*)W + b);
+      for (int j = 0; j < r; j += 4) {
+        const float4 w = p[j / 4];
+        v += w.x * u[j] + w.y * u[j + 1] + w.z * u[j + 2] + w.w * u[j + 3];
+      }
+      return v;
+    }
+  }
+  for (int j = 0; j < r; ++j) v += ld_wt<WB>(W, b + j) * u[j];
+  return v;
+}
+
+// Raw bits of a weight element (bf16 zero-extended or f32), to be turned
+// into a float later (raw_f): loads issued before the weights are primed
+// must not be consumed before the prime.
+template <int WB>
+__device__ __forceinline__ uint32_t ld_raw(const void* p, size_t i) {
+  if constexpr (WB) return ((const uint16_t*)p)[i];
+  else return ((const uint32_t*)p)[i];
+}
+template <int WB>
+__device__ __forceinline__ float raw_f(uint32_t r) {
+  return WB ? __uint_as_float(r << 16) : __uint_as_float(r);
+}
+
+// Element m of a per-row field of the row map, for a per-thread m: built
+// from selects over constant indices (the row map is a kernel argument, so
+// these are scalar loads; a runtime index would become a vector load and a
+// wait for every load in flight).
+__device__ __forceinline__ int rsel(const int8_t (&a)[kMaxRows], int m) {
+  int v = a[0];
+#pragma unroll
+  for (int c = 1; c < kMaxRows; ++c) v = (m == c) ? (int)a[c] : v;
   return v;
 }
 
@@ -749,10 +905,11 @@ __global__ __launch_bounds__(256) void k_embed(Dims D, const void* embed, RowMap
 // workgroup (same inputs, same summation order).  Fills, per sequence,
 // reinit (p <- h for this layer) and the updated exited flag / boundary;
 // sig[s] receives the signal of layer-1.
-__device__ void gate_logic(const Dims& D, const RowMap& rm, const WS& ws, const StepIO& io, int layer,
-                           const float* ssum /* [16][4] */, int* reinit_s, int* exited_s, int* exitb_s, float* sig_s) {
+__device__ void gate_logic(const Dims& D, const RowMap& rm, const int* ex_in, const int* eb_in, const StepIO& io,
+                           int layer, const float* ssum /* [16][4] */, int* reinit_s, int* exited_s, int* exitb_s,
+                           float* sig_s) {
   for (int s = 0; s < rm.nseq; ++s) {
-    int ex = ws.exited[s], eb = ws.exitb[s], ri = 0;
+    int ex = ex_in[s], eb = eb_in[s], ri = 0;
     float sg = 0.f;
     const int f = rm.first[s] + rm.cnt[s] - 1;
     if (layer > 0 && rm.fast[f]) {
@@ -776,12 +933,15 @@ __device__ void gate_logic(const Dims& D, const RowMap& rm, const WS& ws, const 
 // ============================================================================
 template <int WB, int MT>
 __global__ __launch_bounds__(kGemvThreads) void k_qkv(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int layer) {
+  using TG = TileGemv<WB, MT>;
   __shared__ float red[kGemvWaves * 256];
   __shared__ float y[256];
   __shared__ float ssum[kMaxRows * 4];
+  __shared__ int ex_in[kMaxSeq], eb_in[kMaxSeq];
   __shared__ int reinit_s[kMaxSeq], exited_s[kMaxSeq], exitb_s[kMaxSeq];
   __shared__ float sig_s[kMaxSeq];
   __shared__ float inv_rms[kMaxRows];
+  __shared__ int src_s[kMaxRows];
   __shared__ const float* xrow_s[kMaxRows];
   extern __shared__ __attribute__((aligned(16))) char dyn[];
   const int nq = D.qdim, tq = nq / 16;
@@ -797,23 +957,46 @@ __global__ __launch_bounds__(kGemvThreads) void k_qkv(Dims D, LayerPtrs L, RowMa
     return (const char*)L.pa + (size_t)(t - 3 * tq) * tb;
   };
   if ((int)blockIdx.x >= ntiles) return;
-  TileGemv<WB, MT> tg;
+  auto ptr = [&](int i) { return tile_ptr(blockIdx.x + i * gridDim.x); };
+  const int n_local = (ntiles - blockIdx.x + gridDim.x - 1) / gridDim.x;
+  TG tg;
   tg.init(D.d, dyn);
-  tg.prime(tile_ptr(blockIdx.x));
-  // row statistics: sum of the bins filled by the previous kernel
+  // ---- everything needed before the weights: issued first ----
+  // (unconditional loads at clamped indices; consumed after the prime)
+  float bv[kBins];
+  {
+    const int q = min((int)threadIdx.x, rm.M * 4 - 1);
+#pragma unroll
+    for (int b = 0; b < kBins; ++b) bv[b] = bin_d_at(ws, layer, b, q >> 2)[q & 3];
+  }
+  const int sq0 = min((int)threadIdx.x, rm.nseq - 1);
+  const int exv = ws.exited[sq0], ebv = ws.exitb[sq0];
+  const float* rows[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) rows[m] = ws.X + (size_t)min(m, rm.M - 1) * D.d;
+  typename TG::template Pieces<2> xp;
+  if constexpr (TG::XRES) tg.load_pieces(rows, L.attn_norm, xp);
+  __builtin_amdgcn_sched_barrier(0);
+  tg.prime(n_local, ptr);
+  __builtin_amdgcn_sched_barrier(0);
   if (threadIdx.x < rm.M * 4) {
     float a = 0.f;
 #pragma unroll
-    for (int b = 0; b < kBins; ++b) a += bin_d_at(ws, layer, b, threadIdx.x >> 2)[threadIdx.x & 3];
+    for (int b = 0; b < kBins; ++b) a += bv[b];
     ssum[threadIdx.x] = a;
+  }
+  if (threadIdx.x < rm.nseq) {
+    ex_in[threadIdx.x] = exv;
+    eb_in[threadIdx.x] = ebv;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    gate_logic(D, rm, ws, io, layer, ssum, reinit_s, exited_s, exitb_s, sig_s);
+    gate_logic(D, rm, ex_in, eb_in, io, layer, ssum, reinit_s, exited_s, exitb_s, sig_s);
     for (int m = 0; m < rm.M; ++m) {
-      const int sq = rm.seq[m];
+      const int sq = rsel(rm.seq, m);
       int src = m;
-      if (rm.fast[m] && reinit_s[sq]) src = rm.slow_of[m];
+      if (rsel(rm.fast, m) && reinit_s[sq]) src = rsel(rm.slow_of, m);
+      src_s[m] = src;
       xrow_s[m] = ws.X + (size_t)src * D.d;
       inv_rms[m] = rsqrtf(ssum[src * 4] / D.d + D.eps);
     }
@@ -826,8 +1009,14 @@ __global__ __launch_bounds__(kGemvThreads) void k_qkv(Dims D, LayerPtrs L, RowMa
     ws.exitb[sq] = exitb_s[sq];
     if (layer > 0) ws.sig[sq * D.n_layers + layer - 1] = sig_s[sq];
   }
-  tg.set_rows(xrow_s, L.attn_norm, rm.M, D.d);
-  auto ptr = [&](int i) { return tile_ptr(blockIdx.x + i * gridDim.x); };
+  if constexpr (TG::XRES) {
+    int sel[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) sel[m] = m < rm.M ? src_s[m] : 0;
+    tg.store_pieces(xp, rows, L.attn_norm, sel);
+  } else {
+    tg.set_rows(xrow_s, L.attn_norm, rm.M, D.d);
+  }
   auto epi = [&](int i, const f32x4_t& a) {
     const int t = blockIdx.x + i * gridDim.x;
     f32x4_t acc[1] = {a};
@@ -837,7 +1026,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_qkv(Dims D, LayerPtrs L, RowMa
       if (nn < nqkv) ws.QKV[(size_t)m * nqkv + nn] = y[e] * inv_rms[m];
     }
   };
-  tg.run((ntiles - blockIdx.x + gridDim.x - 1) / gridDim.x, ptr, epi);
+  tg.run(n_local, ptr, epi);
 }
 
 // ============================================================================
@@ -1245,13 +1434,23 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn(Dims D, LayerPtrs L, RowM
 // ============================================================================
 // Kernel: output projection + residual add (+ adapter on the fast row);
 // partial sums for the gate/up prologue.  Persistent tile GEMV, grid <= d/16.
+// The 2-row class issues its epilogue operands for the workgroup's first tile
+// (old residual values, the B_o rows, the A_g/A_u columns and gains) before
+// the weights, so the epilogue waits for nothing but the reduction.
 // ============================================================================
 template <int WB, int MT>
 __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int layer) {
+  using TG = TileGemv<WB, MT>;
+  constexpr bool PRE = TG::XRES;
   __shared__ float red[kGemvWaves * 256];
   __shared__ float y[256];
   __shared__ float uo_s[kMaxRows * kMaxRank];
   __shared__ float newx[256];
+  __shared__ float xo_s[kMaxRows * 16];      // first tile: X of every row (PRE)
+  __shared__ float bo_s[16 * kMaxRank];      // first tile: B_o rows (PRE)
+  __shared__ float agu_s[2 * kMaxRank * 16]; // first tile: A_g, A_u columns times g_mlp (PRE)
+  __shared__ float ud_s[2 * kGemvThreads];   // per-head o-adapter values of the fast row (PRE)
+  __shared__ int flag_s[2 * kMaxSeq];        // exited, reinit (PRE)
   __shared__ const float* xrow_s[kMaxRows];
   extern __shared__ __attribute__((aligned(16))) char dyn[];
   const int ntiles = D.d / 16;
@@ -1263,22 +1462,91 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
   }
   const size_t tb = (size_t)16 * D.qdim * (WB ? 2 : 4);
   auto tile_ptr = [&](int t) -> const char* { return (const char*)L.po + (size_t)t * tb; };
-  TileGemv<WB, MT> tg;
-  tg.init(D.qdim, dyn);
-  tg.prime(tile_ptr(blockIdx.x));
-  if (threadIdx.x < rm.M) xrow_s[threadIdx.x] = ws.O + (size_t)threadIdx.x * D.qdim;
-  // adapter-down of o, summed over heads (uo is [16][H][r])
-  for (int e = threadIdx.x; e < rm.M * D.r; e += kGemvThreads) uo_s[e] = 0.f;
-  __syncthreads();
-  if (L.A[3])
-    for (int m = 0; m < rm.M; ++m)
-      if (rm.fast[m]) column_sums(ws.uo + (size_t)m * D.H * D.r, D.H, D.r, D.r, uo_s + m * D.r, red);
-  __syncthreads();
-  tg.set_rows(xrow_s, nullptr, rm.M, D.qdim);
-  const int PO = 1 + 2 * D.r;
   auto ptr = [&](int i) { return tile_ptr(blockIdx.x + i * gridDim.x); };
+  const int n_local = (ntiles - blockIdx.x + gridDim.x - 1) / gridDim.x;
+  const int PO = 1 + 2 * D.r;
+  const int n00 = blockIdx.x * 16;
+  int fast_m = -1;   // the fast row (2-row class: at most one); constant indices keep rm in scalar registers
+#pragma unroll
+  for (int m = 0; m < kMaxRows; ++m)
+    if (m < rm.M && rm.fast[m]) fast_m = m;
+  TG tg;
+  tg.init(D.qdim, dyn);
+  const float* rows[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) rows[m] = ws.O + (size_t)min(m, rm.M - 1) * D.qdim;
+  typename TG::template Pieces<2> xp;
+  float pre[3] = {0.f, 0.f, 0.f};
+  uint32_t praw = 0, araw = 0;
+  float gmlp = 0.f;
+  int fl = 0;
+  const int tid = threadIdx.x;
+  const int HR = D.H * D.r;
+  const bool pre_uo = PRE && HR <= 2 * kGemvThreads;     // per-head values fit two per thread
+  const bool pre_agu = PRE && 2 * D.r * 16 <= kGemvThreads;
+  if constexpr (PRE) {
+    // ---- everything needed before the weights: issued first, unconditional
+    // loads at clamped indices (a load under a branch, or a value consumed
+    // right away, would make the wave wait before the prime) ----
+    tg.load_pieces(rows, nullptr, xp);
+    const int fm = fast_m >= 0 ? fast_m : 0;
+    pre[0] = ws.uo[(size_t)fm * HR + min(tid, HR - 1)];
+    pre[1] = ws.uo[(size_t)fm * HR + min(tid + kGemvThreads, HR - 1)];
+    const int mx = min(tid >> 4, rm.M - 1);
+    pre[2] = ws.X[(size_t)mx * D.d + n00 + (tid & 15)];
+    const int bq = min(tid, 16 * D.r - 1);
+    praw = ld_raw<WB>(L.B[3] ? L.B[3] : L.po, (size_t)(n00 + bq / D.r) * D.r + bq % D.r);
+    const int aq = min(tid, 2 * D.r * 16 - 1);
+    const int which = aq / (D.r * 16), j = (aq / 16) % D.r, i = aq % 16;
+    const void* A = which ? L.A[5] : L.A[4];
+    araw = ld_raw<WB>(A ? A : L.po, (size_t)j * D.d + n00 + i);
+    gmlp = L.mlp_norm[n00 + i];
+    const int fq = min(tid, 2 * rm.nseq - 1);
+    fl = fq < rm.nseq ? ws.exited[fq] : ws.reinit[layer * kMaxSeq + fq - rm.nseq];
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  tg.prime(n_local, ptr);
+  __builtin_amdgcn_sched_barrier(0);
+  if (threadIdx.x < rm.M) xrow_s[threadIdx.x] = ws.O + (size_t)threadIdx.x * D.qdim;
+  for (int e = threadIdx.x; e < rm.M * D.r; e += kGemvThreads) uo_s[e] = 0.f;
+  if constexpr (PRE) {
+    ud_s[tid] = pre[0];
+    ud_s[tid + kGemvThreads] = pre[1];
+    if (tid < rm.M * 16) xo_s[tid] = pre[2];
+    if (tid < 16 * D.r) bo_s[tid] = L.B[3] ? raw_f<WB>(praw) : 0.f;
+    if (pre_agu && tid < 2 * D.r * 16) {
+      const void* A = (tid / (D.r * 16)) ? L.A[5] : L.A[4];
+      agu_s[tid] = A ? raw_f<WB>(araw) * gmlp : 0.f;
+    }
+    if (tid < 2 * rm.nseq) flag_s[tid] = fl;
+  }
+  __syncthreads();
+  if constexpr (PRE) {
+    // adapter-down of o summed over heads: uo is [H][r] per row
+    if (pre_uo) {
+      if (fast_m >= 0 && L.A[3] && tid < D.r) {
+        float a = 0.f;
+        for (int h = 0; h < D.H; ++h) a += ud_s[h * D.r + tid];
+        uo_s[fast_m * D.r + tid] = a;
+      }
+    } else if (L.A[3]) {
+      for (int m = 0; m < rm.M; ++m)
+        if (rsel(rm.fast, m)) column_sums(ws.uo + (size_t)m * D.H * D.r, D.H, D.r, D.r, uo_s + m * D.r, red);
+    }
+    int sel[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) sel[m] = m < rm.M ? m : 0;
+    tg.store_pieces(xp, rows, nullptr, sel);
+  } else {
+    if (L.A[3])
+      for (int m = 0; m < rm.M; ++m)
+        if (rsel(rm.fast, m)) column_sums(ws.uo + (size_t)m * D.H * D.r, D.H, D.r, D.r, uo_s + m * D.r, red);
+    tg.set_rows(xrow_s, nullptr, rm.M, D.qdim);
+  }
+  __syncthreads();
   auto epi = [&](int i, const f32x4_t& a) {
     const int t = blockIdx.x + i * gridDim.x;
+    const bool first = PRE && i == 0;   // operands already in LDS
     f32x4_t acc[1] = {a};
     gemv_reduce<1>(acc, rm.M, red, y);
     const int n0 = t * 16;
@@ -1289,16 +1557,24 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
     float xnew = 0.f, pin = 0.f;
     bool upd = false;
     if (e < rm.M * 16) {
-      const int sq = rm.seq[m];
-      const float xo = ws.X[(size_t)m * D.d + nn];
+      const int sq = rsel(rm.seq, m);
+      const float xo = first ? xo_s[e] : ws.X[(size_t)m * D.d + nn];
       xnew = xo;
-      if (!ws.exited[sq]) {
+      const bool ex = first ? flag_s[sq] != 0 : ws.exited[sq] != 0;
+      if (!ex) {
         upd = true;
-        if (rm.fast[m]) {
-          const bool ri = ws.reinit[layer * kMaxSeq + sq] != 0;
-          pin = ri ? ws.X[(size_t)rm.slow_of[m] * D.d + nn] : xo;
+        if (rsel(rm.fast, m)) {
+          const bool ri = first ? flag_s[rm.nseq + sq] != 0 : ws.reinit[layer * kMaxSeq + sq] != 0;
+          const int so = rsel(rm.slow_of, m);
+          pin = ri ? (first ? xo_s[so * 16 + (e & 15)] : ws.X[(size_t)so * D.d + nn]) : xo;
           float ad = 0.f;
-          if (L.B[3] && L.A[3]) ad = dot_row(L.B[3], nn, D.r, uo_s + m * D.r, D.wbf16);
+          if (L.B[3] && L.A[3]) {
+            if (first) {
+              for (int j = 0; j < D.r; ++j) ad += bo_s[(e & 15) * D.r + j] * uo_s[m * D.r + j];
+            } else {
+              ad = dot_row_t<WB>(L.B[3], nn, D.r, uo_s + m * D.r);
+            }
+          }
           xnew = pin + y[e] + ad;
         } else {
           xnew = xo + y[e];
@@ -1309,7 +1585,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
     __syncthreads();
     if (upd) {
       ws.X[(size_t)m * D.d + nn] = xnew;
-      if (rm.fast[m]) ws.PIN[(size_t)m * D.d + nn] = pin;
+      if (rsel(rm.fast, m)) ws.PIN[(size_t)m * D.d + nn] = pin;
     }
     // partial sums for the gate/up prologue: sum x^2 and the adapter-down of
     // gate and up (fast rows): sum_n A[j][n] g_mlp[n] x[n]
@@ -1318,33 +1594,44 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
       const int mm = q / PO, c = q % PO;
       float v = 0.f;
       if (c == 0) {
-        for (int i = 0; i < 16; ++i) v += newx[mm * 16 + i] * newx[mm * 16 + i];
-      } else if (rm.fast[mm]) {
+        for (int ii = 0; ii < 16; ++ii) v += newx[mm * 16 + ii] * newx[mm * 16 + ii];
+      } else if (rsel(rm.fast, mm)) {
         const int which = (c - 1) / D.r, j = (c - 1) % D.r;   // 0: gate (A[4]), 1: up (A[5])
-        const void* A = L.A[4 + which];
-        if (A)
-          for (int i = 0; i < 16; ++i)
-            v += ld_w(A, (size_t)j * D.d + n0 + i, D.wbf16) * L.mlp_norm[n0 + i] * newx[mm * 16 + i];
+        const void* A = which ? L.A[5] : L.A[4];
+        if (A) {
+          if (first && pre_agu) {
+            for (int ii = 0; ii < 16; ++ii) v += agu_s[(which * D.r + j) * 16 + ii] * newx[mm * 16 + ii];
+          } else {
+            for (int ii = 0; ii < 16; ++ii)
+              v += ld_wt<WB>(A, (size_t)j * D.d + n0 + ii) * L.mlp_norm[n0 + ii] * newx[mm * 16 + ii];
+          }
+        }
       }
-      if (c == 0 || rm.fast[mm]) add_agent(bin_o_at(ws, D, layer, bin, mm) + c, v);
+      if (c == 0 || rsel(rm.fast, mm)) add_agent(bin_o_at(ws, D, layer, bin, mm) + c, v);
     }
     __syncthreads();
   };
-  tg.run((ntiles - blockIdx.x + gridDim.x - 1) / gridDim.x, ptr, epi);
+  tg.run(n_local, ptr, epi);
 }
 
 // ============================================================================
 // Kernel: gate/up projections (the gate and up tiles of the same 16 rows, one
 // after the other), adapter-up, SwiGLU; partial sums of the down adapter's
-// down-projection.  Persistent tile GEMV, grid <= ffn/16.
+// down-projection.  Persistent tile GEMV, grid <= ffn/16.  The 2-row class
+// issues the row statistics, its activation pieces and the first pair's
+// B_g, B_u rows and A_d columns before the weights.
 // ============================================================================
 template <int WB, int MT>
 __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int layer) {
+  using TG = TileGemv<WB, MT>;
+  constexpr bool PRE = TG::XRES;
   __shared__ float red[kGemvWaves * 512];
   __shared__ float y[512];
   __shared__ float stat[kMaxRows * (1 + 2 * kMaxRank)];
   __shared__ float inv_rms[kMaxRows];
   __shared__ float act[256];
+  __shared__ float bgu_s[2 * 16 * kMaxRank];   // first pair: B_g, B_u rows (PRE)
+  __shared__ float ad_s[kMaxRank * 16];        // first pair: A_d columns (PRE)
   __shared__ const float* xrow_s[kMaxRows];
   extern __shared__ __attribute__((aligned(16))) char dyn[];
   const int ntiles = D.F / 16;
@@ -1355,25 +1642,66 @@ __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, Ro
     if (all_exited) return;
   }
   const size_t tb = (size_t)16 * D.d * (WB ? 2 : 4);
-  TileGemv<WB, MT> tg;
-  tg.init(D.d, dyn);
-  tg.prime((const char*)L.pg + (size_t)blockIdx.x * tb);
-  if (threadIdx.x < rm.M) xrow_s[threadIdx.x] = ws.X + (size_t)threadIdx.x * D.d;
-  const int PO = 1 + 2 * D.r;
-  for (int q = threadIdx.x; q < rm.M * PO; q += kGemvThreads) {
-    float a = 0.f;
-#pragma unroll
-    for (int b = 0; b < kBins; ++b) a += bin_o_at(ws, D, layer, b, q / PO)[q % PO];
-    stat[q] = a;
-  }
-  __syncthreads();
-  if (threadIdx.x < rm.M) inv_rms[threadIdx.x] = rsqrtf(stat[threadIdx.x * PO] / D.d + D.eps);
-  tg.set_rows(xrow_s, L.mlp_norm, rm.M, D.d);
-  __syncthreads();
   // local tiles 2i and 2i+1: the gate and up tiles of rows 16*t, t = blockIdx.x + i*gridDim.x
   auto ptr = [&](int i) {
     return (const char*)((i & 1) ? L.pu : L.pg) + (size_t)(blockIdx.x + (i >> 1) * gridDim.x) * tb;
   };
+  const int n_local = 2 * ((ntiles - blockIdx.x + gridDim.x - 1) / gridDim.x);
+  const int PO = 1 + 2 * D.r;
+  const int n00 = blockIdx.x * 16;
+  const int tid = threadIdx.x;
+  const bool pre_b = PRE && 2 * 16 * D.r <= kGemvThreads;
+  TG tg;
+  tg.init(D.d, dyn);
+  // ---- everything needed before the weights: issued first ----
+  // (unconditional loads at clamped indices; consumed after the prime)
+  float sv[kBins];
+  {
+    const int q = min(tid, rm.M * PO - 1);
+#pragma unroll
+    for (int b = 0; b < kBins; ++b) sv[b] = bin_o_at(ws, D, layer, b, q / PO)[q % PO];
+  }
+  const float* rows[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) rows[m] = ws.X + (size_t)min(m, rm.M - 1) * D.d;
+  typename TG::template Pieces<2> xp;
+  uint32_t pb = 0, pa = 0;
+  if constexpr (PRE) {
+    tg.load_pieces(rows, L.mlp_norm, xp);
+    const int bq = min(tid, 2 * 16 * D.r - 1);
+    const int which = bq / (16 * D.r), rr = (bq / D.r) % 16, j = bq % D.r;
+    const void* B = which ? L.B[5] : L.B[4];
+    pb = ld_raw<WB>(B ? B : L.pg, (size_t)(n00 + rr) * D.r + j);
+    const int aq = min(tid, D.r * 16 - 1);
+    pa = ld_raw<WB>(L.A[6] ? L.A[6] : L.pg, (size_t)(aq / 16) * D.F + n00 + (aq % 16));
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  tg.prime(n_local, ptr);
+  __builtin_amdgcn_sched_barrier(0);
+  if (tid < rm.M) xrow_s[tid] = ws.X + (size_t)tid * D.d;
+  if (tid < rm.M * PO) {
+    float a = 0.f;
+#pragma unroll
+    for (int b = 0; b < kBins; ++b) a += sv[b];
+    stat[tid] = a;
+  }
+  if (pre_b && tid < 2 * 16 * D.r) {
+    const int which = tid / (16 * D.r);
+    const bool has = which ? (L.B[5] && L.A[5]) : (L.B[4] && L.A[4]);
+    bgu_s[tid] = has ? raw_f<WB>(pb) : 0.f;
+  }
+  if (PRE && tid < D.r * 16) ad_s[tid] = L.A[6] ? raw_f<WB>(pa) : 0.f;
+  __syncthreads();
+  if (tid < rm.M) inv_rms[tid] = rsqrtf(stat[tid * PO] / D.d + D.eps);
+  if constexpr (PRE) {
+    int sel[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) sel[m] = m < rm.M ? m : 0;
+    tg.store_pieces(xp, rows, L.mlp_norm, sel);
+  } else {
+    tg.set_rows(xrow_s, L.mlp_norm, rm.M, D.d);
+  }
+  __syncthreads();
   f32x4_t acc_g = {0.f, 0.f, 0.f, 0.f};
   auto epi = [&](int i, const f32x4_t& a) {
     if (!(i & 1)) {
@@ -1381,6 +1709,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, Ro
       return;
     }
     const int t = blockIdx.x + (i >> 1) * gridDim.x;
+    const bool first = PRE && i == 1;
     f32x4_t acc[2] = {acc_g, a};
     gemv_reduce<2>(acc, rm.M, red, y);
     const int n0 = t * 16;
@@ -1389,27 +1718,41 @@ __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, Ro
       const int m = e >> 4, nn = n0 + (e & 15);
       const float ir = inv_rms[m];
       float g = y[e] * ir, u = y[256 + e] * ir;
-      if (rm.fast[m]) {
-        if (L.B[4] && L.A[4]) g += dot_row(L.B[4], nn, D.r, stat + m * PO + 1, D.wbf16) * ir;
-        if (L.B[5] && L.A[5]) u += dot_row(L.B[5], nn, D.r, stat + m * PO + 1 + D.r, D.wbf16) * ir;
+      if (rsel(rm.fast, m)) {
+        if (first && pre_b) {
+          float dg = 0.f, du = 0.f;
+          for (int j = 0; j < D.r; ++j) {
+            dg += bgu_s[(e & 15) * D.r + j] * stat[m * PO + 1 + j];
+            du += bgu_s[(16 + (e & 15)) * D.r + j] * stat[m * PO + 1 + D.r + j];
+          }
+          g += dg * ir;
+          u += du * ir;
+        } else {
+          if (L.B[4] && L.A[4]) g += dot_row_t<WB>(L.B[4], nn, D.r, stat + m * PO + 1) * ir;
+          if (L.B[5] && L.A[5]) u += dot_row_t<WB>(L.B[5], nn, D.r, stat + m * PO + 1 + D.r) * ir;
+        }
       }
-      const float a = silu(g) * u;
-      ws.ACT[(size_t)m * D.F + nn] = a;
-      act[e] = a;
+      const float av = silu(g) * u;
+      ws.ACT[(size_t)m * D.F + nn] = av;
+      act[e] = av;
     }
     __syncthreads();
     // partials of the down adapter-down: sum_n A_d[j][n] a[n]
     const int bin = t % kBins;
     for (int q = threadIdx.x; q < rm.M * D.r; q += kGemvThreads) {
       const int mm = q / D.r, j = q % D.r;
-      if (!rm.fast[mm] || !L.A[6]) continue;
+      if (!rsel(rm.fast, mm) || !L.A[6]) continue;
       float v = 0.f;
-      for (int i = 0; i < 16; ++i) v += ld_w(L.A[6], (size_t)j * D.F + n0 + i, D.wbf16) * act[mm * 16 + i];
+      if (first) {
+        for (int ii = 0; ii < 16; ++ii) v += ad_s[j * 16 + ii] * act[mm * 16 + ii];
+      } else {
+        for (int ii = 0; ii < 16; ++ii) v += ld_wt<WB>(L.A[6], (size_t)j * D.F + n0 + ii) * act[mm * 16 + ii];
+      }
       add_agent(bin_gu_at(ws, D, layer, bin, mm) + j, v);
     }
     __syncthreads();
   };
-  tg.run(2 * ((ntiles - blockIdx.x + gridDim.x - 1) / gridDim.x), ptr, epi);
+  tg.run(n_local, ptr, epi);
 }
 
 // Partial sums entering layer `next` (sum x^2, sum pin*x, sum pin^2 of every
@@ -1421,7 +1764,7 @@ __device__ void rows_unchanged_stats(const Dims& D, const RowMap& rm, const WS& 
     float a = 0.f, b = 0.f, c = 0.f;
     for (int i = threadIdx.x; i < D.d; i += blockDim.x) {
       const float x = ws.X[(size_t)m * D.d + i];
-      const float p = rm.fast[m] ? ws.PIN[(size_t)m * D.d + i] : 0.f;
+      const float p = rsel(rm.fast, m) ? ws.PIN[(size_t)m * D.d + i] : 0.f;
       a += x * x; b += p * x; c += p * p;
     }
     a = block_sum(a, red);
@@ -1439,13 +1782,21 @@ __device__ void rows_unchanged_stats(const Dims& D, const RowMap& rm, const WS& 
 // ============================================================================
 // Kernel: down projection + residual add (+ adapter); partial sums for the
 // next layer's norm and the exit signal.  Persistent tile GEMV, grid <= d/16.
+// The 2-row class issues the adapter sums, its activation pieces and the
+// first tile's residual values, fast-row inputs and B_d rows before the
+// weights.
 // ============================================================================
 template <int WB, int MT>
 __global__ __launch_bounds__(kGemvThreads) void k_down(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int layer) {
+  using TG = TileGemv<WB, MT>;
+  constexpr bool PRE = TG::XRES;
   __shared__ float red[kGemvWaves * 256];
   __shared__ float y[256];
   __shared__ float ud[kMaxRows * kMaxRank];
   __shared__ float newx[256], pin_s[256];
+  __shared__ float xo_s[kMaxRows * 16], pino_s[kMaxRows * 16];   // first tile (PRE)
+  __shared__ float bd_s[16 * kMaxRank];                          // first tile: B_d rows (PRE)
+  __shared__ int ex_s[kMaxSeq];                                  // exited (PRE)
   __shared__ const float* xrow_s[kMaxRows];
   extern __shared__ __attribute__((aligned(16))) char dyn[];
   const int ntiles = D.d / 16;
@@ -1460,50 +1811,104 @@ __global__ __launch_bounds__(kGemvThreads) void k_down(Dims D, LayerPtrs L, RowM
   }
   const size_t tb = (size_t)16 * D.F * (WB ? 2 : 4);
   auto tile_ptr = [&](int t) -> const char* { return (const char*)L.pd + (size_t)t * tb; };
-  TileGemv<WB, MT> tg;
+  auto ptr = [&](int i) { return tile_ptr(blockIdx.x + i * gridDim.x); };
+  const int n_local = (ntiles - blockIdx.x + gridDim.x - 1) / gridDim.x;
+  const int n00 = blockIdx.x * 16;
+  const int tid = threadIdx.x;
+  TG tg;
   tg.init(D.F, dyn);
-  tg.prime(tile_ptr(blockIdx.x));
-  if (threadIdx.x < rm.M) xrow_s[threadIdx.x] = ws.ACT + (size_t)threadIdx.x * D.F;
-  for (int q = threadIdx.x; q < rm.M * D.r; q += kGemvThreads) {
+  // ---- everything needed before the weights: issued first ----
+  // (unconditional loads at clamped indices; consumed after the prime)
+  float uv[kBins];
+  {
+    const int q = min(tid, rm.M * D.r - 1);
+#pragma unroll
+    for (int b = 0; b < kBins; ++b) uv[b] = bin_gu_at(ws, D, layer, b, q / D.r)[q % D.r];
+  }
+  const float* rows[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) rows[m] = ws.ACT + (size_t)min(m, rm.M - 1) * D.F;
+  typename TG::template Pieces<4> xp;
+  float px = 0.f, pp = 0.f;
+  uint32_t pb = 0;
+  int pe = 0;
+  if constexpr (PRE) {
+    tg.load_pieces(rows, nullptr, xp);
+    const int m = min(tid >> 4, rm.M - 1);
+    px = ws.X[(size_t)m * D.d + n00 + (tid & 15)];
+    pp = ws.PIN[(size_t)m * D.d + n00 + (tid & 15)];
+    const int bq = min(tid, 16 * D.r - 1);
+    pb = ld_raw<WB>(L.B[6] ? L.B[6] : L.pd, (size_t)(n00 + bq / D.r) * D.r + bq % D.r);
+    pe = ws.exited[min(tid, rm.nseq - 1)];
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  tg.prime(n_local, ptr);
+  __builtin_amdgcn_sched_barrier(0);
+  if (tid < rm.M) xrow_s[tid] = ws.ACT + (size_t)tid * D.F;
+  if (tid < rm.M * D.r) {
     float a = 0.f;
 #pragma unroll
-    for (int b = 0; b < kBins; ++b) a += bin_gu_at(ws, D, layer, b, q / D.r)[q % D.r];
-    ud[q] = a;
+    for (int b = 0; b < kBins; ++b) a += uv[b];
+    ud[tid] = a;
+  }
+  if constexpr (PRE) {
+    if (tid < rm.M * 16) {
+      xo_s[tid] = px;
+      pino_s[tid] = rsel(rm.fast, tid >> 4) ? pp : 0.f;
+    }
+    if (tid < 16 * D.r) bd_s[tid] = (L.B[6] && L.A[6]) ? raw_f<WB>(pb) : 0.f;
+    if (tid < rm.nseq) ex_s[tid] = pe;
   }
   __syncthreads();
-  tg.set_rows(xrow_s, nullptr, rm.M, D.F);
-  auto ptr = [&](int i) { return tile_ptr(blockIdx.x + i * gridDim.x); };
+  if constexpr (PRE) {
+    int sel[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) sel[m] = m < rm.M ? m : 0;
+    tg.store_pieces(xp, rows, nullptr, sel);
+  } else {
+    tg.set_rows(xrow_s, nullptr, rm.M, D.F);
+  }
   auto epi = [&](int i, const f32x4_t& a) {
     const int t = blockIdx.x + i * gridDim.x;
+    const bool first = PRE && i == 0;
     f32x4_t acc[1] = {a};
     gemv_reduce<1>(acc, rm.M, red, y);
     const int n0 = t * 16;
     const int e = threadIdx.x;
     if (e < rm.M * 16) {
       const int m = e >> 4, nn = n0 + (e & 15);
-      float x = ws.X[(size_t)m * D.d + nn];
-      if (!ws.exited[rm.seq[m]]) {
+      float x = first ? xo_s[e] : ws.X[(size_t)m * D.d + nn];
+      const bool ex = first ? ex_s[rsel(rm.seq, m)] != 0 : ws.exited[rsel(rm.seq, m)] != 0;
+      if (!ex) {
         x += y[e];
-        if (rm.fast[m] && L.B[6] && L.A[6]) x += dot_row(L.B[6], nn, D.r, ud + m * D.r, D.wbf16);
+        if (rsel(rm.fast, m) && L.B[6] && L.A[6]) {
+          if (first) {
+            float ad = 0.f;
+            for (int j = 0; j < D.r; ++j) ad += bd_s[(e & 15) * D.r + j] * ud[m * D.r + j];
+            x += ad;
+          } else {
+            x += dot_row_t<WB>(L.B[6], nn, D.r, ud + m * D.r);
+          }
+        }
         ws.X[(size_t)m * D.d + nn] = x;
       }
       newx[e] = x;
-      pin_s[e] = rm.fast[m] ? ws.PIN[(size_t)m * D.d + nn] : 0.f;
+      pin_s[e] = rsel(rm.fast, m) ? (first ? pino_s[e] : ws.PIN[(size_t)m * D.d + nn]) : 0.f;
     }
     __syncthreads();
     const int bin = t % kBins;
     for (int q = threadIdx.x; q < rm.M * 3; q += kGemvThreads) {
       const int mm = q / 3, c = q % 3;
       float v = 0.f;
-      for (int i = 0; i < 16; ++i) {
-        const float x = newx[mm * 16 + i], p = pin_s[mm * 16 + i];
+      for (int ii = 0; ii < 16; ++ii) {
+        const float x = newx[mm * 16 + ii], p = pin_s[mm * 16 + ii];
         v += c == 0 ? x * x : (c == 1 ? p * x : p * p);
       }
       add_agent(bin_d_at(ws, layer + 1, bin, mm) + c, v);
     }
     __syncthreads();
   };
-  tg.run((ntiles - blockIdx.x + gridDim.x - 1) / gridDim.x, ptr, epi);
+  tg.run(n_local, ptr, epi);
 }
 
 // ============================================================================
@@ -1524,18 +1929,40 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
   __shared__ const float* xrow_s[kMaxRows];
   extern __shared__ __attribute__((aligned(16))) char dyn[];
   if ((int)blockIdx.x >= n_tiles) return;
+  using TG = TileGemv<WB, MT>;
   const int lane = threadIdx.x & 63;
   const size_t tb = (size_t)16 * D.d * (WB ? 2 : 4);
   auto tile_ptr = [&](int t) -> const char* { return (const char*)lm_head + (size_t)t * tb; };
-  TileGemv<WB, MT> tg;
+  auto ptr = [&](int i) { return tile_ptr(blockIdx.x + i * gridDim.x); };
+  const int n_local = (n_tiles - blockIdx.x + gridDim.x - 1) / gridDim.x;
+  __shared__ int ex_in[kMaxSeq];
+  TG tg;
   tg.init(D.d, dyn);
-  tg.prime(tile_ptr(blockIdx.x));
-  for (int q = threadIdx.x; q < rm.M * 4; q += kGemvThreads) {
+  // ---- everything needed before the weights: issued first ----
+  // (unconditional loads at clamped indices; consumed after the prime)
+  float bv[kBins];
+  {
+    const int q = min((int)threadIdx.x, rm.M * 4 - 1);
+#pragma unroll
+    for (int b = 0; b < kBins; ++b) bv[b] = bin_d_at(ws, n_layers_run, b, q >> 2)[q & 3];
+  }
+  const int exv = ws.exited[min((int)threadIdx.x, rm.nseq - 1)];
+  const float* rows[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) rows[m] = ws.X + (size_t)min(m, rm.M - 1) * D.d;
+  typename TG::template Pieces<2> xp;
+  if constexpr (TG::XRES) tg.load_pieces(rows, final_norm, xp);
+  __builtin_amdgcn_sched_barrier(0);
+  tg.prime(n_local, ptr);
+  __builtin_amdgcn_sched_barrier(0);
+  if (threadIdx.x < rm.M * 4) {
     float a = 0.f;
 #pragma unroll
-    for (int b = 0; b < kBins; ++b) a += bin_d_at(ws, n_layers_run, b, q >> 2)[q & 3];
-    ssum[q] = a;
+    for (int b = 0; b < kBins; ++b) a += bv[b];
+    ssum[threadIdx.x] = a;
   }
+  if (threadIdx.x < rm.nseq) ex_in[threadIdx.x] = exv;
+  __syncthreads();
   if (threadIdx.x == 0) {
     // rows fed to the head
     int nh = 0;
@@ -1545,7 +1972,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
       for (int sq = 0; sq < rm.nseq; ++sq) {
         const int f = rm.first[sq], c = rm.cnt[sq];
         int pick = f;                       // slow row
-        if (rm.fast[f + c - 1] && (ws.exited[sq] || rm.slow_of[f + c - 1] < 0)) pick = f + c - 1;
+        if (rm.fast[f + c - 1] && (ex_in[sq] || rm.slow_of[f + c - 1] < 0)) pick = f + c - 1;
         hrow[nh++] = pick;
       }
     }
@@ -1558,8 +1985,14 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
   }
   __syncthreads();
   const int nh = nh_s;
-  tg.set_rows(xrow_s, final_norm, nh, D.d);
-  auto ptr = [&](int i) { return tile_ptr(blockIdx.x + i * gridDim.x); };
+  if constexpr (TG::XRES) {
+    int sel[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) sel[m] = m < nh ? hrow[m] : 0;
+    tg.store_pieces(xp, rows, final_norm, sel);
+  } else {
+    tg.set_rows(xrow_s, final_norm, nh, D.d);
+  }
   auto epi = [&](int i, const f32x4_t& a) {
     const int t = blockIdx.x + i * gridDim.x;
     f32x4_t acc[1] = {a};
@@ -1584,7 +2017,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
       }
     }
   };
-  tg.run((n_tiles - blockIdx.x + gridDim.x - 1) / gridDim.x, ptr, epi);
+  tg.run(n_local, ptr, epi);
   if (!arrive_last(ws.lm_cnt, gridDim.x, &last_flag)) return;
 
   // ---- last workgroup: global argmax per head row, then bookkeeping ----------
@@ -1630,8 +2063,8 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
     const int f = rm.first[sq] + rm.cnt[sq] - 1;
     io.next_token[sq + io.draft_slot] = best_s[sq];
     const int t = io.positions[sq] + rm.pos_offset;
-    if (rm.slow_of[f] >= 0 || !rm.fast[f]) kv.seq_lens[sq] = t + 1;
-    if (rm.fast[f] && rm.slow_of[f] >= 0) {
+    if (rsel(rm.slow_of, f) >= 0 || !rsel(rm.fast, f)) kv.seq_lens[sq] = t + 1;
+    if (rsel(rm.fast, f) && rsel(rm.slow_of, f) >= 0) {
       // signal of the last layer
       const float dot = ssum[f * 4 + 1], pin2 = ssum[f * 4 + 2], pp = ssum[f * 4 + 0];
       ws.sig[sq * D.n_layers + D.n_layers - 1] = ws.exited[sq] ? 0.f : dot * rsqrtf(fmaxf(pin2 * pp, 1e-30f));
@@ -1646,7 +2079,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
       const int f = rm.first[sq] + rm.cnt[sq] - 1;
       float v = ws.sig[q];
       // layers after an exit were not run
-      if (!rm.fast[f] || rm.slow_of[f] < 0 || (ws.exited[sq] && l >= ws.exitb[sq])) v = 0.f;
+      if (!rsel(rm.fast, f) || rsel(rm.slow_of, f) < 0 || (ws.exited[sq] && l >= ws.exitb[sq])) v = 0.f;
       io.signal_out[q] = v;
     }
   }
