@@ -250,7 +250,7 @@ def run_dense(args) -> int:
                               f"KV context {args.ctx} (+{args.warmup + args.steps} decoded), HIP graph replay",
                   "batch": 1, "kv_context": args.ctx, "dual_stream": dual},
           step_hbm_gbs=round(step_gbs, 1), step_bytes=int(sb), step_roofline_frac=round(step_gbs / HBM_PEAK_GBS, 4),
-          roofline={"bound": "hbm", "kernel": "gate/up projection (k_gateup)", "achieved": round(achieved, 1),
+          roofline={"bound": "hbm", "kernel": "gate/up projection, one output row per wave (kr_gateup)", "achieved": round(achieved, 1),
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                     "traffic": None, "avg_kernel_us": round(k_avg_ms * 1e3, 3), "bytes_per_launch": int(kb),
                     "launches_timed": k_n},

@@ -23,12 +23,13 @@
  *    pointers, *_h host pointers.  The library never allocates device memory:
  *    the workspace passed to m2r2_create holds a tile-packed copy of every
  *    projection matrix (so that each wave's 16-byte loads form 1 KB contiguous
- *    blocks that are exactly MFMA operands) and all scratch.  The row-major
- *    projection matrices (wq, wk, wv, wo, wg, wu, wd, the LM head) and the
- *    q/k/v adapter-down factors A[0..2] are read only during m2r2_create and
- *    may be freed afterwards; the embedding, norm gains and the remaining
- *    adapter factors are borrowed for the lifetime of the context.
- *    Activations, KV pages and outputs are borrowed for the duration of a call.
+ *    blocks that are exactly MFMA operands; read by calls with more than two
+ *    rows) and all scratch.  Calls with one or two rows (a decode step of one
+ *    sequence, a draft, a two-row chunk) stream the caller's row-major
+ *    matrices directly, one output row per wave.  Every weight pointer
+ *    (matrices, LM head, embedding, norm gains, adapter factors) is therefore
+ *    borrowed for the lifetime of the context.  Activations, KV pages and
+ *    outputs are borrowed for the duration of a call.
  *  - Layout: matrices are row-major [d_out][d_in] (the reduction dimension is
  *    contiguous).  Adapter factors are A [rank][d_in] and B [d_out][rank]; the
  *    adapter adds (x A^T) B^T to the projection of x.  Matrices and adapters

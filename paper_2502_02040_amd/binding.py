@@ -279,13 +279,12 @@ class Model:
             self._keep.append(t)
             return t.data_ptr()
 
-        # projection matrices (and the q/k/v adapter-down factors) are read by
-        # m2r2_create only: it packs them into the workspace
-        self._transient = []
-
+        # projection matrices: m2r2_create packs them into the workspace (for
+        # chunks of more than two rows); one- and two-row calls stream these
+        # row-major copies, so they live as long as the context
         def up_t(name):
             t = torch.from_numpy(np.ascontiguousarray(weights[name], dtype=np.float32)).to(device=device, dtype=wdt)
-            self._transient.append(t)
+            self._keep.append(t)
             return t.data_ptr()
 
         self._layers = (LayerWeights * cfg.n_layers)()
@@ -325,7 +324,6 @@ class Model:
         _check(lib().m2r2_create(ctypes.byref(make_config(cfg, self.expert_slots)), ctypes.byref(self._w), max_batch,
                                  max_chunk, max_ctx, ws_ptr, self.ws_bytes, ctypes.byref(self._ctx)), "m2r2_create")
         torch.cuda.synchronize()
-        self._transient = []   # packed copies live in the workspace
 
     def __del__(self):
         try:

@@ -66,6 +66,31 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Lane exchanges inside a row of 16 lanes through DPP (a VALU operand
+// modifier; __shfl_xor compiles to ds_bpermute, an LDS round trip).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppQuadXor1 = 0xB1, kDppQuadXor2 = 0x4E, kDppRowHalfMirror = 0x141, kDppRowMirror = 0x140,
+              kDppRowRor4 = 0x124, kDppRowRor8 = 0x128;
+// sum over the 4 lanes of a quad (every lane of the quad gets it)
+__device__ __forceinline__ float quad_sum(float v) {
+  v += dpp_f<kDppQuadXor1>(v);
+  return v + dpp_f<kDppQuadXor2>(v);
+}
+// sum over the 16 lanes of a row (every lane of the row gets it)
+__device__ __forceinline__ float row_sum16(float v) {
+  v = quad_sum(v);
+  v += dpp_f<kDppRowHalfMirror>(v);
+  return v + dpp_f<kDppRowMirror>(v);
+}
+// sum over the lanes l, l+4, l+8, l+12 of a row
+__device__ __forceinline__ float row_sum_stride4(float v) {
+  v += dpp_f<kDppRowRor8>(v);
+  return v + dpp_f<kDppRowRor4>(v);
+}
+
 // Block-wide sum of one value per thread; `red` holds blockDim/64 floats.
 __device__ __forceinline__ float block_sum(float v, float* red) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;

@@ -17,6 +17,9 @@
 #include "m2r2.h"
 #include "moe_kernels.h"
 #include "step_kernels.h"
+#include "sk_kernels.h"
+#include "sk_attn.h"
+#include "rw_kernels.h"
 
 using namespace m2r2;
 
@@ -61,12 +64,14 @@ struct Layout {
   std::vector<size_t> lay_off;           // per layer: pq pk pv pa po pg pu pd (8 offsets)
   size_t lm;                             // packed LM head
   size_t X, PIN, QKV, O, ACT, bin_d, bin_o, bin_gu, uo, att, att_cnt, lm_val, lm_idx, lm_cnt, exited, exitb,
-      reinit, err, sig, rope, total;
+      reinit, err, sig, rope, sk_part, sk_cnt, total;
   // mixture of experts: router logits, choices, probabilities, activations,
   // and the expert cache ([n_layers][slots] slots of expert_stride bytes)
   size_t moe_logits, moe_sel, moe_prob, moe_act, moe_slots;
   size_t expert_bytes, expert_stride;
   int TD, TF, TV, S_max;
+  size_t sk_slots;                       // partial-sum slots of the stream-K GEMVs
+  int lm_slots;                          // arg-max partial slots (per LM-head tile or workgroup)
 };
 
 bool is_moe(const m2r2_config& c) { return c.n_experts > 0; }
@@ -84,6 +89,51 @@ size_t expert_bytes_of(const m2r2_config& c) {
 struct Resident {
   int n[2][2][5];
 };
+
+// ---- stream-K GEMV plans ----------------------------------------------------
+constexpr int kSkMaxWaves = 8 * 320;   // partial slots are sized for up to 320 compute units
+constexpr int kSkMinLds = 82 * 1024;   // dynamic LDS of every stream-K launch: one workgroup per compute unit
+constexpr int kLmMinSlots = 1024;      // arg-max slots: at least one per workgroup of a one-per-compute-unit launch
+
+SkPlan sk_plan(int ntiles, int nblk, int W, bool pair) {
+  SkPlan p{};
+  p.ntiles = ntiles;
+  p.nblk = nblk;
+  p.W = W;
+  const long long T = (long long)ntiles * nblk;
+  // equal ranges over all waves, but long enough that a tile has at most
+  // kSkMaxSeg segments (small matrices leave waves idle)
+  long long L = std::max({1LL, (T + W - 1) / W, (long long)(nblk + kSkMaxSeg - 2) / (kSkMaxSeg - 1)});
+  if (pair && (L & 1)) ++L;
+  p.L = (int)L;
+  int smax = 1;
+  for (int t = 0; t < ntiles; ++t)
+    smax = std::max(smax, std::min(sk_last_wave(p, t), W - 1) - sk_first_wave(p, t) + 1);
+  p.smax = smax;
+  return p;
+}
+
+// Plans of the five matrix kinds: 0 qkv (+ adapter-down rows), 1 o, 2 gate/up pairs, 3 down, 4 LM head.
+void sk_plans(const m2r2_config& c, int W, SkPlan (&out)[5]) {
+  const int kstep = c.wdtype == M2R2_BF16 ? 32 : 16;
+  const int d = c.d_model, q = c.n_heads * c.head_dim, r = c.rank, F = std::max(c.ffn, kstep);
+  out[0] = sk_plan(3 * ((q + 15) / 16) + (3 * r + 15) / 16, d / kstep, W, false);
+  out[1] = sk_plan((d + 15) / 16, q / kstep, W, false);
+  out[2] = sk_plan((F + 15) / 16, 2 * (d / kstep), W, true);
+  out[3] = sk_plan((d + 15) / 16, F / kstep, W, false);
+  out[4] = sk_plan((c.vocab + 15) / 16, d / kstep, W, false);
+}
+
+size_t sk_slot_bound(const m2r2_config& c) {
+  if (c.n_experts > 0) return 0;
+  size_t n = 0;
+  for (int W : {kSkMaxWaves, 8 * 256, 8 * 128, 8 * 64}) {
+    SkPlan p[5];
+    sk_plans(c, W, p);
+    for (const SkPlan& x : p) n = std::max(n, (size_t)x.ntiles * x.smax);
+  }
+  return n;
+}
 
 Layout make_layout(const m2r2_config& c, int max_batch, int max_chunk, int max_ctx) {
   Layout L{};
@@ -119,8 +169,8 @@ Layout make_layout(const m2r2_config& c, int max_batch, int max_chunk, int max_c
       L.lay_off.push_back(0);
       L.lay_off.push_back(0);
     } else {
-      L.lay_off.push_back(take(packed_bytes(c.ffn, d, wb)));
-      L.lay_off.push_back(take(packed_bytes(c.ffn, d, wb)));
+      L.lay_off.push_back(take(2 * packed_bytes(c.ffn, d, wb)));   // gate and up, interleaved tile pairs
+      L.lay_off.push_back(0);
       L.lay_off.push_back(take(packed_bytes(d, c.ffn, wb)));
     }
   }
@@ -130,15 +180,17 @@ Layout make_layout(const m2r2_config& c, int max_batch, int max_chunk, int max_c
   L.QKV = take(sizeof(float) * kMaxRows * nqkv);
   L.O = take(sizeof(float) * kMaxRows * qdim);
   L.ACT = take(sizeof(float) * kMaxRows * std::max(c.ffn, 1));
-  L.bin_d = take(sizeof(float) * (c.n_layers + 1) * kBins * kMaxRows * 4);
-  L.bin_o = take(sizeof(float) * c.n_layers * kBins * kMaxRows * (1 + 2 * r));
-  L.bin_gu = take(sizeof(float) * c.n_layers * kBins * kMaxRows * std::max(r, 1));
+  L.bin_d = take(sizeof(float) * (c.n_layers + 1) * kBinSlots * kMaxRows * 4);
+  L.bin_o = take(sizeof(float) * c.n_layers * kBinSlots * kMaxRows * (1 + 2 * r));
+  L.bin_gu = take(sizeof(float) * c.n_layers * kBinSlots * kMaxRows * std::max(r, 1));
   L.uo = take(sizeof(float) * kMaxRows * c.n_heads * std::max(r, 1));
   L.att = take(sizeof(float) * (size_t)std::max(max_batch, 1) * c.n_heads * (smax + 1) * kMaxRows *
                (c.head_dim + 2 + r));
   L.att_cnt = take(sizeof(uint32_t) * kMaxSeq * c.n_heads);
-  L.lm_val = take(sizeof(float) * L.TV * kMaxRows);
-  L.lm_idx = take(sizeof(int) * L.TV * kMaxRows);
+  // per-tile (or, for the row-per-wave head, per-workgroup) arg-max partials
+  L.lm_slots = std::max(L.TV, kLmMinSlots);
+  L.lm_val = take(sizeof(float) * L.lm_slots * kMaxRows);
+  L.lm_idx = take(sizeof(int) * L.lm_slots * kMaxRows);
   L.lm_cnt = take(sizeof(uint32_t));
   L.exited = take(sizeof(int) * kMaxSeq);
   L.exitb = take(sizeof(int) * kMaxSeq);
@@ -146,6 +198,9 @@ Layout make_layout(const m2r2_config& c, int max_batch, int max_chunk, int max_c
   L.err = take(sizeof(int));
   L.sig = take(sizeof(float) * kMaxSeq * c.n_layers);
   L.rope = take(sizeof(float) * 2 * (size_t)max_ctx * (c.head_dim / 2));
+  L.sk_slots = sk_slot_bound(c);
+  L.sk_part = take(sizeof(float) * 64 * std::max<size_t>(L.sk_slots, 1));
+  L.sk_cnt = take(sizeof(uint32_t) * (65 + std::max({L.TD, L.TF, L.TV, 3 * ((qdim + 15) / 16) + (3 * r + 15) / 16})));
   if (moe) {
     L.moe_logits = take(sizeof(float) * 3 * c.n_experts);
     L.moe_sel = take(sizeof(int) * 3 * kMaxTopK);
@@ -227,10 +282,19 @@ struct m2r2_ctx {
   const void* embed;
   const float* final_norm;
   const void* lm_head;   // packed
+  const void* lm_head_rm;   // the caller's row-major LM head
   int max_batch, max_chunk, max_ctx;
   WS ws;
   // kernel timing (measurement only)
   Resident resident;
+  // stream-K GEMVs of the one- and two-row class
+  bool sk_on = false;
+  int sk_grid = 0;
+  int sk_attn_S = 0;   // splits of the stream-K path's attention (0: the general attention kernel)
+  bool rw_on = false;  // row-per-wave GEMVs for the one- and two-row class
+  int rw_nch[3] = {0, 0, 0};   // 1 KB pieces per row for reductions over d, qdim, ffn
+  SkPlan sk[5];
+  SkWS skws{};
   int timed_class = -1;
   std::vector<hipEvent_t> ev;   // pairs
   int ev_used = 0;
@@ -304,9 +368,96 @@ Grids grids(const m2r2_ctx* c) {
   return g;
 }
 
+size_t sk_lds(int K) { return (size_t)std::max(sk_act_bytes(K), kSkMinLds); }
+
+// ---- row-per-wave GEMVs: kernels instantiated for these piece counts per row
+#define M2R2_RW_NCH(X) X(1) X(2) X(4) X(6) X(8) X(16)
+bool rw_nch_ok(int n) {
+#define M2R2_RW_CASE(N) if (n == N) return true;
+  M2R2_RW_NCH(M2R2_RW_CASE)
+#undef M2R2_RW_CASE
+  return false;
+}
+#define M2R2_RW_LAUNCHER(NAME, ...)                                                                     \
+  template <int WB, class... A>                                                                       \
+  void NAME##_launch(int nch, int grid, size_t lds, hipStream_t st, A... args) {                      \
+    switch (nch) {                                                                                    \
+      case 1: NAME<WB, 1, 1><<<grid, kRwThreads, lds, st>>>(args...); break;                          \
+      case 2: NAME<WB, 2, 1><<<grid, kRwThreads, lds, st>>>(args...); break;                          \
+      case 4: NAME<WB, 4, 1><<<grid, kRwThreads, lds, st>>>(args...); break;                          \
+      case 6: NAME<WB, 6, 1><<<grid, kRwThreads, lds, st>>>(args...); break;                          \
+      case 8: NAME<WB, 8, 1><<<grid, kRwThreads, lds, st>>>(args...); break;                          \
+      case 16: NAME<WB, 8, 2><<<grid, kRwThreads, lds, st>>>(args...); break;                         \
+    }                                                                                                 \
+  }
+M2R2_RW_LAUNCHER(kr_qkv)
+M2R2_RW_LAUNCHER(kr_oproj)
+M2R2_RW_LAUNCHER(kr_gateup)
+M2R2_RW_LAUNCHER(kr_down)
+M2R2_RW_LAUNCHER(kr_head)
+
+// One or two rows: row-per-wave GEMVs and the short-chain attention.
+template <int WB, int KB, int HD>
+m2r2_status run_layers_rw(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPtrs& kv, int n_layers_run,
+                          hipStream_t st) {
+  const Dims& D = c->D;
+  const int G = c->sk_grid;
+  const size_t lds = (size_t)kSkMinLds;
+  const int nd = c->rw_nch[0], nq = c->rw_nch[1], nf = c->rw_nch[2];
+  for (int l = 0; l < n_layers_run; ++l) {
+    const LayerPtrs& L = c->layers[l];
+    TIMED(0, (kr_qkv_launch<WB>(nd, G, lds, st, D, L, rm, c->ws, io, l)));
+    TIMED(1, (ks_attn<WB, KB, HD><<<dim3(c->sk_attn_S, D.H, rm.nseq), kSkAttnThreads, sk_attn_lds_bytes(HD, D.r, WB),
+                                    st>>>(D, L, rm, c->ws, io, kv, l, c->sk_attn_S)));
+    TIMED(2, (kr_oproj_launch<WB>(nq, G, lds, st, D, L, rm, c->ws, io, l)));
+    TIMED(3, (kr_gateup_launch<WB>(nd, G, lds, st, D, L, rm, c->ws, io, l)));
+    TIMED(4, (kr_down_launch<WB>(nf, G, lds, st, D, L, rm, c->ws, io, l)));
+  }
+  TIMED(5, (kr_head_launch<WB>(nd, G, lds, st, D, c->lm_head_rm, c->final_norm, rm, c->ws, io, kv, c->skws,
+                                n_layers_run)));
+  HIP_TRY(hipGetLastError());
+  return M2R2_OK;
+}
+
+// One or two rows: stream-K GEMVs, one workgroup per compute unit.
+template <int WB, int KB, int HD>
+m2r2_status run_layers_sk(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPtrs& kv, int n_layers_run,
+                          hipStream_t st) {
+  const Dims& D = c->D;
+  int rows_per_seq = 1;
+  for (int s = 0; s < rm.nseq; ++s) rows_per_seq = std::max(rows_per_seq, (int)rm.cnt[s]);
+  const int S = choose_splits(rm.nseq, rows_per_seq, D.H, c->max_ctx);
+  if (S > c->lay.S_max) return fail(M2R2_E_SHAPE, "attention splits exceed the workspace");
+  if (S + 1 > 64) return fail(M2R2_E_SHAPE, "context too long for the attention merge (max_ctx %d)", c->max_ctx);
+  const size_t smem = attn_smem_bytes();
+  const int G = c->sk_grid;
+  const size_t ld = sk_lds(D.d), lq = sk_lds(D.qdim), lf = sk_lds(D.F);
+  const SkWS& sk = c->skws;
+  for (int l = 0; l < n_layers_run; ++l) {
+    const LayerPtrs& L = c->layers[l];
+    TIMED(0, (ks_qkv<WB><<<G, kSkThreads, ld, st>>>(D, L, rm, c->ws, io, c->sk[0], sk, l)));
+    if (c->sk_attn_S)
+      TIMED(1, (ks_attn<WB, KB, HD><<<dim3(c->sk_attn_S, D.H, rm.nseq), kSkAttnThreads,
+                                       sk_attn_lds_bytes(HD, D.r, WB), st>>>(D, L, rm, c->ws, io, kv, l, c->sk_attn_S)));
+    else
+      TIMED(1, (k_attn<KB, HD><<<dim3(S + 1, D.H, rm.nseq), kAttnThreads, smem, st>>>(D, L, rm, c->ws, io, kv, l, S)));
+    TIMED(2, (ks_oproj<WB><<<G, kSkThreads, lq, st>>>(D, L, rm, c->ws, io, c->sk[1], sk, l)));
+    TIMED(3, (ks_gateup<WB><<<G, kSkThreads, ld, st>>>(D, L, rm, c->ws, io, c->sk[2], sk, l)));
+    TIMED(4, (ks_down<WB><<<G, kSkThreads, lf, st>>>(D, L, rm, c->ws, io, c->sk[3], sk, l)));
+  }
+  TIMED(5, (ks_head<WB><<<G, kSkThreads, ld, st>>>(D, c->lm_head, c->final_norm, rm, c->ws, io, kv, c->sk[4], sk,
+                                                   n_layers_run)));
+  HIP_TRY(hipGetLastError());
+  return M2R2_OK;
+}
+
 template <int WB, int KB, int HD, int MT>
 m2r2_status run_layers_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPtrs& kv, int n_layers_run,
                          hipStream_t st) {
+  if constexpr (MT == 2) {
+    if (c->rw_on) return run_layers_rw<WB, KB, HD>(c, rm, io, kv, n_layers_run, st);
+    if (c->sk_on) return run_layers_sk<WB, KB, HD>(c, rm, io, kv, n_layers_run, st);
+  }
   const Dims& D = c->D;
   const int nqkv = 3 * D.qdim + 3 * D.r;
   int rows_per_seq = 1;
@@ -374,8 +525,13 @@ hipError_t pack_all(m2r2_ctx* c, const m2r2_weights* w, void* workspace) {
       if (e == hipSuccess) e = pack_one(wb, one(L.router, cf.n_experts), cf.n_experts, d, b + o[5]);
       continue;
     }
-    if (e == hipSuccess) e = pack_one(wb, one(L.wg, F), F, d, b + o[5]);
-    if (e == hipSuccess) e = pack_one(wb, one(L.wu, F), F, d, b + o[6]);
+    if (e == hipSuccess) {
+      const size_t chunks = (size_t)((F + 15) / 16) * 2 * (d / (wb ? 32 : 16)) * 64;
+      const int grid = (int)std::min<size_t>(8192, (chunks + 255) / 256);
+      if (wb) k_pack_pair<1><<<grid, 256>>>(L.wg, L.wu, F, d, b + o[5]);
+      else k_pack_pair<0><<<grid, 256>>>(L.wg, L.wu, F, d, b + o[5]);
+      e = hipGetLastError();
+    }
     if (e == hipSuccess) e = pack_one(wb, one(L.wd, d), d, F, b + o[7]);
   }
   if (e == hipSuccess) e = pack_one(wb, one(w->lm_head, cf.vocab), cf.vocab, d, b + c->lay.lm);
@@ -406,9 +562,95 @@ hipError_t set_lds_limits(const m2r2_config& c, Resident& res) {
   return e;
 }
 
+template <int WB>
+hipError_t sk_set_lds(int bytes) {
+  const void* fns[] = {(const void*)ks_qkv<WB>, (const void*)ks_oproj<WB>, (const void*)ks_gateup<WB>,
+                       (const void*)ks_down<WB>, (const void*)ks_head<WB>};
+  hipError_t e = hipSuccess;
+  for (const void* f : fns)
+    if (e == hipSuccess) e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  return e;
+}
+
+bool getenv_zero(const char* name) {
+  const char* v = getenv(name);
+  return v && v[0] == '0';
+}
+
+template <int WB>
+hipError_t rw_set_lds(int bytes) {
+  hipError_t e = hipSuccess;
+#define M2R2_RW_ATTR(N, S)                                                                                    \
+  for (const void* f : {(const void*)kr_qkv<WB, N, S>, (const void*)kr_oproj<WB, N, S>,                        \
+                        (const void*)kr_gateup<WB, N, S>, (const void*)kr_down<WB, N, S>,                       \
+                        (const void*)kr_head<WB, N, S>})                                                      \
+    if (e == hipSuccess) e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  M2R2_RW_ATTR(1, 1) M2R2_RW_ATTR(2, 1) M2R2_RW_ATTR(4, 1) M2R2_RW_ATTR(6, 1) M2R2_RW_ATTR(8, 1) M2R2_RW_ATTR(8, 2)
+#undef M2R2_RW_ATTR
+  return e;
+}
+
+// Decide whether the one- and two-row class runs the stream-K GEMVs: dense
+// models whose every matrix has at least 8 blocks per tile, whose projection
+// matrices q|k|v|adapter-down are consecutive, and whose partial slots fit.
+// M2R2_STREAMK=0 in the environment selects the per-tile GEMVs instead.
+hipError_t sk_setup(m2r2_ctx* c) {
+  c->sk_on = false;
+  const m2r2_config& cf = c->cfg;
+  if (is_moe(cf)) return hipSuccess;
+  const char* env = getenv("M2R2_STREAMK");
+  if (env && env[0] == '0') return hipSuccess;
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess || cus < 1) return e;
+  const int W = kSkWaves * cus;
+  sk_plans(cf, W, c->sk);
+  bool ok = true;
+  for (const SkPlan& p : c->sk)
+    ok = ok && p.nblk >= 8 && p.smax <= kSkMaxSeg && (p.L + p.nblk - 1) / p.nblk + 1 <= 64 &&
+         (size_t)p.ntiles * p.smax <= c->lay.sk_slots;
+  const Dims& D = c->D;
+  const int K = std::max({D.d, D.qdim, D.F});
+  ok = ok && K <= kSkMaxK && sk_lds(K) <= 160 * 1024;
+  const size_t tb = (size_t)16 * D.d * (D.wbf16 ? 2 : 4), tq = (size_t)(D.qdim / 16) * tb;
+  for (const LayerPtrs& L : c->layers)
+    ok = ok && (const char*)L.pk == (const char*)L.pq + tq && (const char*)L.pv == (const char*)L.pk + tq &&
+         (const char*)L.pa == (const char*)L.pv + tq;
+  ok = ok && cus <= c->lay.lm_slots;   // one arg-max slot per workgroup of the row-per-wave head
+  if (!ok) return hipSuccess;
+  e = D.wbf16 ? sk_set_lds<1>((int)sk_lds(K)) : sk_set_lds<0>((int)sk_lds(K));
+  if (e == hipSuccess) {
+    c->sk_on = true;
+    c->sk_grid = cus;
+    // attention of the stream-K path: fixed 128-token splits over the cache
+    // capacity (at most 64, within the workspace's partial slots), the head's
+    // B rows in at most three 16-byte pieces per thread, A_o in two
+    const int S = (c->max_ctx + kSkAttnP - 1) / kSkAttnP;
+    const int wsz = D.wbf16 ? 2 : 4;
+    const bool ok_a = S <= 64 && S <= c->lay.S_max && D.hd * D.r * wsz <= 2 * kSkAttnThreads * 16 &&
+                      (D.hd * D.r * wsz) % 16 == 0 && D.r * D.hd / 8 <= 2 * kSkAttnThreads;
+    c->sk_attn_S = ok_a ? S : 0;
+    // row-per-wave GEMVs: rows of whole 1 KB pieces, a piece count with a
+    // kernel, adapter up-factor rows of whole 16-byte pieces, and the
+    // short-chain attention
+    const int epp = 64 * (D.wbf16 ? 8 : 4);   // elements per 1 KB piece
+    const int Ks[3] = {D.d, D.qdim, D.F};
+    bool ok_r = c->sk_attn_S > 0 && (D.r * wsz) % 16 == 0 && D.r * wsz <= kRwMaxBRowBytes &&
+                !getenv_zero("M2R2_ROWWAVE");
+    for (int i = 0; i < 3; ++i) {
+      c->rw_nch[i] = Ks[i] / epp;
+      ok_r = ok_r && Ks[i] % epp == 0 && rw_nch_ok(c->rw_nch[i]) && Ks[i] <= kSkMaxK;
+    }
+    if (ok_r) e = D.wbf16 ? rw_set_lds<1>(kSkMinLds) : rw_set_lds<0>(kSkMinLds);
+    c->rw_on = ok_r && e == hipSuccess;
+  }
+  return e;
+}
+
 // Embedding, n_layers_run layers, head.
 m2r2_status run_pass(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPtrs& kv, int nl, hipStream_t st) {
-  TIMED(6, (k_embed<<<rm.M, 256, 0, st>>>(c->D, c->embed, rm, c->ws, io, 1)));
+  TIMED(6, (k_embed<<<rm.M + kEmbedZeroBlocks, 256, 0, st>>>(c->D, c->embed, rm, c->ws, io, 1)));
   HIP_TRY(hipGetLastError());
   const int wb = c->D.wbf16, kb = c->D.kvbf16;
   if (wb && kb) return run_hd<1, 1>(c, rm, io, kv, nl, st);
@@ -567,7 +809,7 @@ m2r2_status run_moe_pass(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const 
   const int N = c->D.n_layers, K = c->moe.K;
   if (out->slow_experts_d) HIP_TRY(hipMemsetAsync(out->slow_experts_d, 0xff, sizeof(int32_t) * N * K, st));
   if (out->pred_experts_d) HIP_TRY(hipMemsetAsync(out->pred_experts_d, 0xff, sizeof(int32_t) * N * K, st));
-  TIMED(6, (k_embed<<<rm.M, 256, 0, st>>>(c->D, c->embed, rm, c->ws, io, 1)));
+  TIMED(6, (k_embed<<<rm.M + kEmbedZeroBlocks, 256, 0, st>>>(c->D, c->embed, rm, c->ws, io, 1)));
   HIP_TRY(hipGetLastError());
   const int wb = c->D.wbf16, kb = c->D.kvbf16;
   if (wb && kb) return run_moe_hd<1, 1>(c, rm, io, kv, out, dual, st);
@@ -696,6 +938,7 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
   c->embed = w->embed;
   c->final_norm = w->final_norm;
   c->lm_head = (char*)workspace + lay.lm;
+  c->lm_head_rm = w->lm_head;
   Dims& D = c->D;
   D.n_layers = cfg->n_layers; D.d = cfg->d_model; D.H = cfg->n_heads; D.hd = cfg->head_dim;
   D.qdim = cfg->n_heads * cfg->head_dim; D.F = cfg->ffn; D.V = cfg->vocab; D.r = cfg->rank;
@@ -710,6 +953,7 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
     const size_t* o = &lay.lay_off[8 * l];
     L.pq = wsb + o[0]; L.pk = wsb + o[1]; L.pv = wsb + o[2]; L.pa = wsb + o[3];
     L.po = wsb + o[4];
+    L.wq = s.wq; L.wk = s.wk; L.wv = s.wv; L.wo = s.wo; L.wg = s.wg; L.wu = s.wu; L.wd = s.wd;
     for (int a = 0; a < 7; ++a) { L.A[a] = s.A[a]; L.B[a] = s.B[a]; }
     if (moe) {
       // the fast MLP adapter rides in the gate slot: the o projection sums its
@@ -718,7 +962,7 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
       L.A[4] = s.A_m; L.B[4] = s.B_m;
       c->moe.router.push_back(wsb + o[5]);
     } else {
-      L.pg = wsb + o[5]; L.pu = wsb + o[6]; L.pd = wsb + o[7];
+      L.pg = wsb + o[5]; L.pu = nullptr; L.pd = wsb + o[7];
     }
   }
   char* b = (char*)workspace;
@@ -732,6 +976,9 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
   ws.sig = (float*)(b + lay.sig);
   ws.rope = (const float2*)(b + lay.rope);
   ws.rope_len = max_ctx;
+  c->skws.part = (float*)(b + lay.sk_part);
+  c->skws.hier = (uint32_t*)(b + lay.sk_cnt);
+  c->skws.cnt = c->skws.hier + 65;
 
   hipError_t e = hipMemset(workspace, 0, lay.total);
   if (e == hipSuccess) {
@@ -751,6 +998,7 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
   if (e == hipSuccess) e = set_lds_limits<1, 2>(*cfg, c->resident);
   if (e == hipSuccess) e = set_lds_limits<0, 16>(*cfg, c->resident);
   if (e == hipSuccess) e = set_lds_limits<1, 16>(*cfg, c->resident);
+  if (e == hipSuccess) e = sk_setup(c);
   if (e == hipSuccess && moe) {
     MoeState& M = c->moe;
     M.on = true;

@@ -35,12 +35,14 @@ struct Dims {
 };
 
 // Projection matrices are read from a tile-packed copy (pack_index below):
-// pq/pk/pv/pa (q, k, v and the stacked adapter-down rows [A_q; A_k; A_v]),
-// po, pg, pu, pd.  Adapter factors and norms stay row-major.
+// pq/pk/pv/pa (q, k, v and the stacked adapter-down rows [A_q; A_k; A_v],
+// consecutive in memory), po, pg (gate and up as interleaved tile pairs; pu
+// is unused), pd.  Adapter factors and norms stay row-major.
 struct LayerPtrs {
   const float* attn_norm;
   const float* mlp_norm;
   const void *pq, *pk, *pv, *pa, *po, *pg, *pu, *pd;
+  const void *wq, *wk, *wv, *wo, *wg, *wu, *wd;   // the caller's row-major matrices
   const void* A[7];
   const void* B[7];
 };
@@ -107,14 +109,19 @@ struct WS {
   int rope_len;
 };
 
+// Bins per layer and row: kBinSlots are stored (and zeroed every pass); the
+// per-tile kernels use the first kBins, the stream-K kernels (whose tile
+// epilogues all run at the end of the launch) spread their atomics over all
+// kBinSlots.
 constexpr int kBins = 8;
+constexpr int kBinSlots = 64;
 
-__device__ __forceinline__ float* bin_d_at(const WS& ws, int l, int b, int m) { return ws.bin_d + (((size_t)l * kBins + b) * kMaxRows + m) * 4; }
+__device__ __forceinline__ float* bin_d_at(const WS& ws, int l, int b, int m) { return ws.bin_d + (((size_t)l * kBinSlots + b) * kMaxRows + m) * 4; }
 __device__ __forceinline__ float* bin_o_at(const WS& ws, const Dims& D, int l, int b, int m) {
-  return ws.bin_o + (((size_t)l * kBins + b) * kMaxRows + m) * (1 + 2 * D.r);
+  return ws.bin_o + (((size_t)l * kBinSlots + b) * kMaxRows + m) * (1 + 2 * D.r);
 }
 __device__ __forceinline__ float* bin_gu_at(const WS& ws, const Dims& D, int l, int b, int m) {
-  return ws.bin_gu + (((size_t)l * kBins + b) * kMaxRows + m) * D.r;
+  return ws.bin_gu + (((size_t)l * kBinSlots + b) * kMaxRows + m) * D.r;
 }
 __device__ __forceinline__ void add_agent(float* p, float v) {
   __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -385,7 +392,7 @@ __host__ __device__ constexpr int tile_lds_bytes(int wb, int MT, int K) {
   return MT <= 2 ? MT * K * 4 : kGemvWaves * MT * kChunk * (wb ? 32 : 16) * 4;
 }
 
-template <int WB, int MT>
+template <int WB, int MT, int BS = 1024>
 struct TileGemv {
   static constexpr int KSTEP = WB ? 32 : 16;
   static constexpr int P = KSTEP / 4;
@@ -410,7 +417,7 @@ struct TileGemv {
   // wave's range repeat its last block (a cache hit, never used)
   __device__ __forceinline__ void load(const char* base, int sb, u32x4_t (&dst)[kChunk]) const {
 #pragma unroll
-    for (int j = 0; j < kChunk; ++j) dst[j] = ld_glob(base + (size_t)min(sb + j, s1 - 1) * 1024);
+    for (int j = 0; j < kChunk; ++j) dst[j] = ld_glob(base + (size_t)min(sb + j, s1 - 1) * BS);
   }
 
   // The first two chunks of the workgroup's chunk sequence (tile i starts at
@@ -857,12 +864,55 @@ __global__ __launch_bounds__(256) void k_pack(PackSrc src, int total_rows, int K
   }
 }
 
+// Pack the gate and up matrices ([rows][K] each) as interleaved tile pairs:
+// pair t holds gate rows 16t.. and up rows 16t..; K-step s of the gate is
+// block 2s of the pair, of the up projection block 2s+1.
+template <int WB>
+__global__ __launch_bounds__(256) void k_pack_pair(const void* wg, const void* wu, int rows, int K, void* dst) {
+  constexpr int KSTEP = WB ? 32 : 16, EPL = WB ? 8 : 4, ESZ = WB ? 2 : 4;
+  const int S = K / KSTEP;
+  const size_t n = (size_t)((rows + 15) / 16) * 2 * S * 64;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+    const int l = (int)(i & 63);
+    const size_t ts = i >> 6;
+    const int j = (int)(ts % (2 * S));
+    const size_t t = ts / (2 * S);
+    const int r = (int)(t * 16) + (l & 15);
+    const int col = (j >> 1) * KSTEP + EPL * (l >> 4);
+    const void* src = (j & 1) ? wu : wg;
+    u32x4_t v = {0u, 0u, 0u, 0u};
+    if (r < rows) v = *(const u32x4_t*)((const char*)src + ((size_t)r * K + col) * ESZ);
+    *(u32x4_t*)((char*)dst + i * 16) = v;
+  }
+}
+
 // ============================================================================
-// Kernel: embedding gather + per-step control initialisation.
-// grid = M rows, block = 256.
+// Kernel: embedding gather + per-step control initialisation + zeroed bins.
+// grid = M rows + kEmbedZeroBlocks, block = 256.  Block m < M gathers row m
+// and writes its layer-0 bins (every slot); the other blocks zero the bins
+// of every later layer (all rows, all slots).
 // ============================================================================
+constexpr int kEmbedZeroBlocks = 64;
+
 __global__ __launch_bounds__(256) void k_embed(Dims D, const void* embed, RowMap rm, WS ws, StepIO io, int init_ctl) {
   __shared__ float red[4];
+  if ((int)blockIdx.x >= rm.M) {
+    // zero bin_d of layers 1..n_layers, bin_o and bin_gu (float4 stores)
+    const size_t nd = (size_t)D.n_layers * kBinSlots * kMaxRows * 4 / 4;
+    const size_t no = (size_t)D.n_layers * kBinSlots * kMaxRows * (1 + 2 * D.r) / 4;
+    const size_t ng = (size_t)D.n_layers * kBinSlots * kMaxRows * D.r / 4;
+    float4* pd = (float4*)(ws.bin_d + (size_t)kBinSlots * kMaxRows * 4);
+    float4* po = (float4*)ws.bin_o;
+    float4* pg = (float4*)ws.bin_gu;
+    const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+    const size_t stride = (size_t)(gridDim.x - rm.M) * 256;
+    for (size_t i = (size_t)(blockIdx.x - rm.M) * 256 + threadIdx.x; i < nd + no + ng; i += stride) {
+      if (i < nd) pd[i] = z;
+      else if (i < nd + no) po[i - nd] = z;
+      else pg[i - nd - no] = z;
+    }
+    return;
+  }
   const int m = blockIdx.x;
   const int tok = io.tokens[rm.tok[m]];
   const bool ok = tok >= 0 && tok < D.V;
@@ -874,24 +924,11 @@ __global__ __launch_bounds__(256) void k_embed(Dims D, const void* embed, RowMap
     ws.PIN[m * D.d + i] = v;
     ss += v * v;
   }
-  // zero this row's bins of every layer
-  const int PO = 1 + 2 * D.r;
-  for (int i = threadIdx.x; i < (D.n_layers + 1) * kBins * 4; i += 256) {
-    const int l = i / (kBins * 4), b = (i / 4) % kBins;
-    bin_d_at(ws, l, b, m)[i % 4] = 0.f;
-  }
-  for (int i = threadIdx.x; i < D.n_layers * kBins * PO; i += 256) {
-    const int l = i / (kBins * PO), b = (i / PO) % kBins;
-    bin_o_at(ws, D, l, b, m)[i % PO] = 0.f;
-  }
-  for (int i = threadIdx.x; i < D.n_layers * kBins * D.r; i += 256) {
-    const int l = i / (kBins * D.r), b = (i / D.r) % kBins;
-    bin_gu_at(ws, D, l, b, m)[i % D.r] = 0.f;
-  }
-  ss = block_sum(ss, red);   // contains a barrier: the zeroing above is done
-  if (threadIdx.x == 0) {
-    float* pd = bin_d_at(ws, 0, 0, m);
-    pd[0] = ss; pd[1] = ss; pd[2] = ss; pd[3] = 0.f;
+  ss = block_sum(ss, red);
+  // layer-0 bins of this row: slot 0 holds the sums, the other slots zero
+  for (int i = threadIdx.x; i < kBinSlots * 4; i += 256) {
+    const int b = i / 4, c = i % 4;
+    bin_d_at(ws, 0, b, m)[c] = (b == 0 && c < 3) ? ss : 0.f;
   }
   if (init_ctl && m == 0) {
     for (int s = threadIdx.x; s < kMaxSeq; s += 256) {
@@ -1623,7 +1660,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
 // ============================================================================
 template <int WB, int MT>
 __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int layer) {
-  using TG = TileGemv<WB, MT>;
+  using TG = TileGemv<WB, MT, 2048>;   // gate and up blocks alternate in the pair layout
   constexpr bool PRE = TG::XRES;
   __shared__ float red[kGemvWaves * 512];
   __shared__ float y[512];
@@ -1642,9 +1679,10 @@ __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, Ro
     if (all_exited) return;
   }
   const size_t tb = (size_t)16 * D.d * (WB ? 2 : 4);
-  // local tiles 2i and 2i+1: the gate and up tiles of rows 16*t, t = blockIdx.x + i*gridDim.x
+  // local tiles 2i and 2i+1: the gate and up tiles of rows 16*t, t = blockIdx.x + i*gridDim.x, in the
+  // interleaved pair layout (pair t at 2*t*tb; gate step s at block 2s, up step s at block 2s+1)
   auto ptr = [&](int i) {
-    return (const char*)((i & 1) ? L.pu : L.pg) + (size_t)(blockIdx.x + (i >> 1) * gridDim.x) * tb;
+    return (const char*)L.pg + (size_t)(blockIdx.x + (i >> 1) * gridDim.x) * 2 * tb + (i & 1) * 1024;
   };
   const int n_local = 2 * ((ntiles - blockIdx.x + gridDim.x - 1) / gridDim.x);
   const int PO = 1 + 2 * D.r;
