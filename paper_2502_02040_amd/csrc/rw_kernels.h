@@ -133,9 +133,10 @@ struct RwStream {
 
   // Stream units [u0, u1): epi.fetch(unit, ops) issues the unit's epilogue
   // operands (in flight with its weights), epi.run(unit, y, ops) runs the
-  // epilogue.  bA holds sub-unit 0 of unit u0 already (prime).  Loads past
-  // the range repeat its last unit (never used): every path issues the same
-  // loads.
+  // epilogue.  bA holds sub-unit 0 of unit u0 already (prime).  Inside the
+  // loop every iteration issues the same loads (the compiler's wait counts
+  // stay exact); the last unit is finished after the loop, so nothing past
+  // the range is read.
   template <class PF, class Epi>
   __device__ __forceinline__ void run(const PF& row_ptr, int u0, int u1, const float* act, int K, Epi& epi) {
     if (u0 >= u1) return;
@@ -143,47 +144,84 @@ struct RwStream {
     float y[U][2];
     if constexpr (NS == 1) {
       epi.fetch(u0, oA);
-      for (int u = u0;; u += 2) {
-        load(row_ptr, min(u + 1, u1 - 1), 0, bB);
-        epi.fetch(min(u + 1, u1 - 1), oB);
+      int u = u0;
+      // pairs of units with a successor each: A -> B -> A
+      for (; u + 2 < u1; u += 2) {
+        load(row_ptr, u + 1, 0, bB);
+        epi.fetch(u + 1, oB);
         zero(y);
         dot(bA, act, K, 0, y);
         finish(y);
         epi.run(u, y, oA);
-        if (u + 1 >= u1) break;
-        load(row_ptr, min(u + 2, u1 - 1), 0, bA);
-        epi.fetch(min(u + 2, u1 - 1), oA);
+        load(row_ptr, u + 2, 0, bA);
+        epi.fetch(u + 2, oA);
         zero(y);
         dot(bB, act, K, 0, y);
         finish(y);
         epi.run(u + 1, y, oB);
-        if (u + 2 >= u1) break;
+      }
+      if (u + 1 < u1) {   // two units left: u in bA, u + 1 to load
+        load(row_ptr, u + 1, 0, bB);
+        epi.fetch(u + 1, oB);
+        zero(y);
+        dot(bA, act, K, 0, y);
+        finish(y);
+        epi.run(u, y, oA);
+        zero(y);
+        dot(bB, act, K, 0, y);
+        finish(y);
+        epi.run(u + 1, y, oB);
+      } else {            // one unit left, in bA
+        zero(y);
+        dot(bA, act, K, 0, y);
+        finish(y);
+        epi.run(u, y, oA);
       }
     } else {
       static_assert(NS == 2, "one or two sub-units per unit");
       load(row_ptr, u0, 1, bB);
       epi.fetch(u0, oA);
-      for (int u = u0;; u += 2) {
-        int un = min(u + 1, u1 - 1);
+      int u = u0;
+      // unit u in bA (sub-unit 0) and bB (sub-unit 1), its operands in oA;
+      // two units per iteration so the operand buffers alternate in place
+      for (; u + 2 < u1; u += 2) {
         zero(y);
         dot(bA, act, K, 0, y);
-        load(row_ptr, un, 0, bA);
-        epi.fetch(un, oB);
+        load(row_ptr, u + 1, 0, bA);
+        epi.fetch(u + 1, oB);
         dot(bB, act, K, 1, y);
-        load(row_ptr, un, 1, bB);
+        load(row_ptr, u + 1, 1, bB);
         finish(y);
         epi.run(u, y, oA);
-        if (u + 1 >= u1) break;
-        un = min(u + 2, u1 - 1);
         zero(y);
         dot(bA, act, K, 0, y);
-        load(row_ptr, un, 0, bA);
-        epi.fetch(un, oA);
+        load(row_ptr, u + 2, 0, bA);
+        epi.fetch(u + 2, oA);
         dot(bB, act, K, 1, y);
-        load(row_ptr, un, 1, bB);
+        load(row_ptr, u + 2, 1, bB);
         finish(y);
         epi.run(u + 1, y, oB);
-        if (u + 2 >= u1) break;
+      }
+      if (u + 1 < u1) {
+        zero(y);
+        dot(bA, act, K, 0, y);
+        load(row_ptr, u + 1, 0, bA);
+        epi.fetch(u + 1, oB);
+        dot(bB, act, K, 1, y);
+        load(row_ptr, u + 1, 1, bB);
+        finish(y);
+        epi.run(u, y, oA);
+        zero(y);
+        dot(bA, act, K, 0, y);
+        dot(bB, act, K, 1, y);
+        finish(y);
+        epi.run(u + 1, y, oB);
+      } else {
+        zero(y);
+        dot(bA, act, K, 0, y);
+        dot(bB, act, K, 1, y);
+        finish(y);
+        epi.run(u, y, oA);
       }
     }
   }
