@@ -642,6 +642,9 @@ hipError_t sk_setup(m2r2_ctx* c) {
       c->rw_nch[i] = Ks[i] / epp;
       ok_r = ok_r && Ks[i] % epp == 0 && rw_nch_ok(c->rw_nch[i]) && Ks[i] <= kSkMaxK;
     }
+    // the waves split their units with 32-bit products unit * wave count
+    const long long nmax = std::max<long long>({3LL * D.qdim + 3LL * D.r, D.d, D.F, D.V});
+    ok_r = ok_r && nmax * cus * kRwWaves < (1LL << 32);
     if (ok_r) e = D.wbf16 ? rw_set_lds<1>(kSkMinLds) : rw_set_lds<0>(kSkMinLds);
     c->rw_on = ok_r && e == hipSuccess;
   }

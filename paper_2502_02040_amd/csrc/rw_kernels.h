@@ -31,26 +31,50 @@ struct RwPM {
   static constexpr int value = (K / 4 + kRwThreads - 1) / kRwThreads;
 };
 
-// Units [u0, u1) of wave gw of W for n units.
+// Units [u0, u1) of wave gw of W for n units (n * W < 2^32, checked by the
+// host; gw is wave-uniform, so this is scalar arithmetic).
 __device__ __forceinline__ void rw_range(int n, int W, int gw, int& u0, int& u1) {
-  u0 = (int)(((long long)gw * n) / W);
-  u1 = (int)(((long long)(gw + 1) * n) / W);
+  u0 = (int)((unsigned)gw * (unsigned)n / (unsigned)W);
+  u1 = (int)((unsigned)(gw + 1) * (unsigned)n / (unsigned)W);
 }
 
-// Activation rows into LDS as fp32 [2][K]: row m = candidate m times the gain.
-// Ends with a workgroup barrier.
+// Activation rows (and the norm gain when G) read into registers before the
+// weights are primed, then stored into LDS as fp32 [2][K]: row m = candidate
+// m times the gain.
 template <int PM>
-__device__ __forceinline__ void rw_store_pieces(const SkPiecesT<PM>& xp, const float* gain, int K, float* act) {
+struct RwPieces {
+  float4 v[PM][2];
+  float4 g[PM];
+};
+// float4 index of piece p of this thread (pieces past the row repeat the last)
+__device__ __forceinline__ int rw_piece_q(int p, int nq) { return min((int)threadIdx.x + kRwThreads * p, nq - 1); }
+template <bool G, int PM>
+__device__ __forceinline__ void rw_load_pieces(const float* r0, const float* r1, const float* gain, int K,
+                                               RwPieces<PM>& xp) {
   const int nq = K / 4;
 #pragma unroll
   for (int p = 0; p < PM; ++p) {
-    const int q = (int)threadIdx.x + kSkThreads * p;
-    if (q < nq) {
-      const float4 g = gain ? xp.g[p] : make_float4(1.f, 1.f, 1.f, 1.f);
+    const int q = rw_piece_q(p, nq);
+    xp.v[p][0] = ldg4(r0 + 4 * q);
+    xp.v[p][1] = ldg4(r1 + 4 * q);
+    if constexpr (G) xp.g[p] = ldg4(gain + 4 * q);
+  }
+}
+// Ends with a workgroup barrier.
+template <bool G, int PM>
+__device__ __forceinline__ void rw_store_pieces(const RwPieces<PM>& xp, int K, float* act) {
+  const int nq = K / 4;
+#pragma unroll
+  for (int p = 0; p < PM; ++p) {
+    if ((int)threadIdx.x + kRwThreads * p < nq) {
+      const int q = rw_piece_q(p, nq);
 #pragma unroll
       for (int m = 0; m < 2; ++m) {
         float4 v = xp.v[p][m];
-        v.x *= g.x; v.y *= g.y; v.z *= g.z; v.w *= g.w;
+        if constexpr (G) {
+          const float4 g = xp.g[p];
+          v.x *= g.x; v.y *= g.y; v.z *= g.z; v.w *= g.w;
+        }
         *(float4*)(act + (size_t)m * K + 4 * q) = v;
       }
     }
@@ -72,21 +96,38 @@ struct RwStream {
   static constexpr int EPL = WB ? 8 : 4;   // weight elements per lane and piece
   u32x4_t bA[U][NCH], bB[U][NCH];
 
+  // The loads of one sub-unit are issued as a group (nothing is scheduled
+  // into or across it): the compiler's in-order wait counts then agree
+  // between the loop entry and its back edge, so a wait for one piece never
+  // waits for the loads issued after it.
   template <class PF>
   __device__ __forceinline__ void load(const PF& row_ptr, int unit, int sub, u32x4_t (&dst)[U][NCH]) const {
     const int lane = threadIdx.x & 63;
+    const char* p[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) p[u] = (const char*)row_ptr(unit, u) + (size_t)sub * NCH * 1024 + lane * 16;
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const char* p = (const char*)row_ptr(unit, u) + (size_t)sub * NCH * 1024 + lane * 16;
 #pragma unroll
-      for (int c = 0; c < NCH; ++c) dst[u][c] = ld_glob(p + (size_t)c * 1024);
+      for (int c = 0; c < NCH; ++c) dst[u][c] = ld_glob(p[u] + (size_t)c * 1024);
     }
+    __builtin_amdgcn_sched_barrier(0);
   }
 
   // a[u][m] += lane partial dot products of sub-unit `sub` with activation rows m.
   __device__ __forceinline__ void dot(const u32x4_t (&w)[U][NCH], const float* act, int K, int sub,
                                       float (&a)[U][2]) const {
     const int lane = threadIdx.x & 63;
+    if constexpr (NS > 1) {
+      // A row of several sub-units: re-read the activations from LDS for
+      // every sub-unit.  (The optimizer would otherwise keep the values read
+      // for one unit live for the next, which needs more registers than a
+      // wave has.)  The opaque zero offset keeps the reads distinct.
+      int zoff = 0;
+      asm volatile("" : "+s"(zoff));
+      act += zoff;
+    }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       float a0 = a[u][0], a1 = a[u][1];
@@ -100,15 +141,24 @@ struct RwStream {
           const float w4 = bf16lo(w[u][c][2]), w5 = bf16hi(w[u][c][2]), w6 = bf16lo(w[u][c][3]), w7 = bf16hi(w[u][c][3]);
           a0 += w0 * x0a.x + w1 * x0a.y + w2 * x0a.z + w3 * x0a.w + w4 * x0b.x + w5 * x0b.y + w6 * x0b.z + w7 * x0b.w;
           a1 += w0 * x1a.x + w1 * x1a.y + w2 * x1a.z + w3 * x1a.w + w4 * x1b.x + w5 * x1b.y + w6 * x1b.z + w7 * x1b.w;
-          // keep the activation reads of later pieces from being hoisted
-          // (register pressure with many pieces in flight)
-          if (c % 2 == 1) __builtin_amdgcn_sched_barrier(0);
+          // finish every two pieces in place: the sums are pinned by an
+          // empty asm (the optimizer would otherwise sink the arithmetic to
+          // the end and read every piece's activations first) and the
+          // activation reads of later pieces are not hoisted above it
+          if (c % 2 == 1) {
+            asm volatile("" : "+v"(a0), "+v"(a1));
+            __builtin_amdgcn_sched_barrier(0);
+          }
         } else {
           const float4 x0 = *(const float4*)(act + k), x1 = *(const float4*)(act + K + k);
           const float w0 = __uint_as_float(w[u][c][0]), w1 = __uint_as_float(w[u][c][1]);
           const float w2 = __uint_as_float(w[u][c][2]), w3 = __uint_as_float(w[u][c][3]);
           a0 += w0 * x0.x + w1 * x0.y + w2 * x0.z + w3 * x0.w;
           a1 += w0 * x1.x + w1 * x1.y + w2 * x1.z + w3 * x1.w;
+          if (c % 4 == 3) {   // as above, every four (smaller) pieces
+            asm volatile("" : "+v"(a0), "+v"(a1));
+            __builtin_amdgcn_sched_barrier(0);
+          }
         }
       }
       a[u][0] = a0;
@@ -128,60 +178,78 @@ struct RwStream {
     }
   }
 
-  template <class PF>
-  __device__ __forceinline__ void prime(const PF& row_ptr, int unit) { load(row_ptr, unit, 0, bA); }
-
-  // Stream units [u0, u1): epi.fetch(unit, ops) issues the unit's epilogue
-  // operands (in flight with its weights), epi.run(unit, y, ops) runs the
-  // epilogue.  bA holds sub-unit 0 of unit u0 already (prime).  Inside the
-  // loop every iteration issues the same loads (the compiler's wait counts
-  // stay exact); the last unit is finished after the loop, so nothing past
-  // the range is read.
+  // Issue the first weights of the range [u0, u1) and their epilogue
+  // operands, ahead of the activation staging: sub-unit 0 of units u0 and
+  // u0 + 1 (NS == 1) or both sub-units of unit u0 (NS == 2).  Every load is
+  // unconditional (the compiler's wait counts stay exact): a range of one
+  // unit reads its unit twice, an empty range (u0 < n always) reads unit u0.
   template <class PF, class Epi>
-  __device__ __forceinline__ void run(const PF& row_ptr, int u0, int u1, const float* act, int K, Epi& epi) {
-    if (u0 >= u1) return;
-    typename Epi::Ops oA, oB;
-    float y[U][2];
+  __device__ __forceinline__ void begin(const PF& row_ptr, int u0, int u1, const Epi& epi,
+                                        typename Epi::Ops& oA, typename Epi::Ops& oB) {
+    const int ub = min(u0 + 1, max(u1 - 1, u0));
+    load(row_ptr, u0, 0, bA);
+    epi.fetch(u0, oA);
     if constexpr (NS == 1) {
-      epi.fetch(u0, oA);
-      int u = u0;
-      // pairs of units with a successor each: A -> B -> A
-      for (; u + 2 < u1; u += 2) {
-        load(row_ptr, u + 1, 0, bB);
-        epi.fetch(u + 1, oB);
-        zero(y);
-        dot(bA, act, K, 0, y);
-        finish(y);
-        epi.run(u, y, oA);
-        load(row_ptr, u + 2, 0, bA);
-        epi.fetch(u + 2, oA);
-        zero(y);
-        dot(bB, act, K, 0, y);
-        finish(y);
-        epi.run(u + 1, y, oB);
-      }
-      if (u + 1 < u1) {   // two units left: u in bA, u + 1 to load
-        load(row_ptr, u + 1, 0, bB);
-        epi.fetch(u + 1, oB);
-        zero(y);
-        dot(bA, act, K, 0, y);
-        finish(y);
-        epi.run(u, y, oA);
-        zero(y);
-        dot(bB, act, K, 0, y);
-        finish(y);
-        epi.run(u + 1, y, oB);
-      } else {            // one unit left, in bA
-        zero(y);
-        dot(bA, act, K, 0, y);
-        finish(y);
-        epi.run(u, y, oA);
-      }
+      load(row_ptr, ub, 0, bB);
+      epi.fetch(ub, oB);
     } else {
       static_assert(NS == 2, "one or two sub-units per unit");
       load(row_ptr, u0, 1, bB);
-      epi.fetch(u0, oA);
-      int u = u0;
+    }
+  }
+
+  // Stream units [u0, u1) after begin(): epi.fetch(unit, ops) issues a unit's
+  // epilogue operands (in flight with its weights), epi.run(unit, y, ops)
+  // runs the epilogue.  Inside the loops every iteration issues the same
+  // loads; the last units are finished after the loop, so nothing past the
+  // range is read.
+  template <class PF, class Epi>
+  __device__ __forceinline__ void run(const PF& row_ptr, int u0, int u1, const float* act, int K, Epi& epi,
+                                      typename Epi::Ops& oA, typename Epi::Ops& oB) {
+    if (u0 >= u1) return;
+    float y[U][2];
+    int u = u0;
+    if constexpr (NS == 1) {
+      // bA holds unit u, bB unit u + 1; each unit's successor-but-one is
+      // loaded into its buffer as soon as its dot products are done
+      for (; u + 3 < u1; u += 2) {
+        zero(y);
+        dot(bA, act, K, 0, y);
+        load(row_ptr, u + 2, 0, bA);
+        finish(y);
+        epi.run(u, y, oA);
+        epi.fetch(u + 2, oA);
+        zero(y);
+        dot(bB, act, K, 0, y);
+        load(row_ptr, u + 3, 0, bB);
+        finish(y);
+        epi.run(u + 1, y, oB);
+        epi.fetch(u + 3, oB);
+      }
+      // the last one to three units: the loads here are conditional (what
+      // they bring is needed next anyway), and no two branches start with
+      // the same code (which the compiler would hoist above the branch,
+      // converting every weight of the unit at once)
+      const int left = u1 - u;
+      zero(y);
+      dot(bA, act, K, 0, y);
+      if (left == 3) load(row_ptr, u + 2, 0, bA);
+      finish(y);
+      epi.run(u, y, oA);
+      if (left == 3) epi.fetch(u + 2, oA);
+      if (left >= 2) {
+        zero(y);
+        dot(bB, act, K, 0, y);
+        finish(y);
+        epi.run(u + 1, y, oB);
+      }
+      if (left == 3) {
+        zero(y);
+        dot(bA, act, K, 0, y);
+        finish(y);
+        epi.run(u + 2, y, oA);
+      }
+    } else {
       // unit u in bA (sub-unit 0) and bB (sub-unit 1), its operands in oA;
       // two units per iteration so the operand buffers alternate in place
       for (; u + 2 < u1; u += 2) {
@@ -202,26 +270,24 @@ struct RwStream {
         finish(y);
         epi.run(u + 1, y, oB);
       }
-      if (u + 1 < u1) {
-        zero(y);
-        dot(bA, act, K, 0, y);
+      // the last one or two units (conditional loads, no common branch prefix)
+      const bool two = u + 1 < u1;
+      zero(y);
+      dot(bA, act, K, 0, y);
+      if (two) {
         load(row_ptr, u + 1, 0, bA);
         epi.fetch(u + 1, oB);
-        dot(bB, act, K, 1, y);
-        load(row_ptr, u + 1, 1, bB);
-        finish(y);
-        epi.run(u, y, oA);
+      }
+      dot(bB, act, K, 1, y);
+      if (two) load(row_ptr, u + 1, 1, bB);
+      finish(y);
+      epi.run(u, y, oA);
+      if (two) {
         zero(y);
         dot(bA, act, K, 0, y);
         dot(bB, act, K, 1, y);
         finish(y);
         epi.run(u + 1, y, oB);
-      } else {
-        zero(y);
-        dot(bA, act, K, 0, y);
-        dot(bB, act, K, 1, y);
-        finish(y);
-        epi.run(u, y, oA);
       }
     }
   }
@@ -287,7 +353,7 @@ __global__ __launch_bounds__(kRwThreads) void kr_qkv(Dims D, LayerPtrs L, RowMap
   __shared__ int src_s[2];
   __shared__ SkRmLds rmu;
   const RowMap& rml = rmu.rm;
-  const int tid = threadIdx.x, gw = blockIdx.x * kRwWaves + (tid >> 6);
+  const int tid = threadIdx.x, gw = blockIdx.x * kRwWaves + __builtin_amdgcn_readfirstlane(tid >> 6);
   const int esz = WB ? 2 : 4, qd = D.qdim, r = D.r;
   const int nu = 3 * qd + 3 * r;
   const void* Ap[3] = {L.A[0], L.A[1], L.A[2]};
@@ -303,38 +369,12 @@ __global__ __launch_bounds__(kRwThreads) void kr_qkv(Dims D, LayerPtrs L, RowMap
   int u0, u1;
   rw_range(nu, gridDim.x * kRwWaves, gw, u0, u1);
   RwStream<WB, NCH, 1, NS> st;
-  const int rmw = sk_rm_word(rm);
   float bv[1];
-  sk_bins_load(rm.M * 4, [&](int q, int b) { return bin_d_at(ws, layer, b, q >> 2) + (q & 3); }, bv);
+  sk_bins_load(rm.M * 4, bin_d_at(ws, layer, 0, 0), kMaxRows * 4, bv);
   const int sq0 = min(tid, rm.nseq - 1);
   const int exv = ws.exited[sq0], ebv = ws.exitb[sq0];
-  SkPiecesT<RwPM<WB, NCH, NS>::value> xp;
-  sk_load_pieces(ws.X, ws.X + (size_t)(rm.M > 1 ? 1 : 0) * D.d, L.attn_norm, D.d, xp);
-  __builtin_amdgcn_sched_barrier(0);
-  st.prime(row_ptr, min(u0, nu - 1));
-  __builtin_amdgcn_sched_barrier(0);
-  if (tid < rm.nseq) { ex_in[tid] = exv; eb_in[tid] = ebv; }
-  sk_rm_put(rmu, rmw);
-  sk_bins_sum(rm.M * 4, bv, actf, ssum);
-  if (tid == 0) {
-    sk_gate_logic(D, rml, ex_in, eb_in, io, layer, ssum, reinit_s, exited_s, exitb_s, sig_s);
-#pragma unroll
-    for (int m = 0; m < 2; ++m) {
-      const int mm = min(m, rm.M - 1);
-      int src = mm;
-      if (rml.fast[mm] && reinit_s[rml.seq[mm]]) src = rml.slow_of[mm];
-      src_s[m] = src;
-      inv_rms[m] = rsqrtf(ssum[src * 4] / D.d + D.eps);
-    }
-  }
-  __syncthreads();
-  if (blockIdx.x == 0 && tid < rm.nseq) {
-    ws.reinit[layer * kMaxSeq + tid] = reinit_s[tid];
-    ws.exited[tid] = exited_s[tid];
-    ws.exitb[tid] = exitb_s[tid];
-    if (layer > 0) ws.sig[tid * D.n_layers + layer - 1] = sig_s[tid];
-  }
-  rw_store_pieces(xp, L.attn_norm, D.d, actf);
+  RwPieces<RwPM<WB, NCH, NS>::value> xp;
+  rw_load_pieces<true>(ws.X, ws.X + (size_t)(rm.M > 1 ? 1 : 0) * D.d, L.attn_norm, D.d, xp);
   const int nqkv = nu;
   struct Epi {
     struct Ops {};
@@ -358,7 +398,33 @@ __global__ __launch_bounds__(kRwThreads) void kr_qkv(Dims D, LayerPtrs L, RowMap
       }
     }
   } epi{&rml, src_s, inv_rms, ws.QKV, nqkv, qd, r, Ap};
-  st.run(row_ptr, u0, u1, actf, D.d, epi);
+  typename Epi::Ops oA, oB;
+  __builtin_amdgcn_sched_barrier(0);
+  st.begin(row_ptr, u0, u1, epi, oA, oB);
+  __builtin_amdgcn_sched_barrier(0);
+  if (tid < rm.nseq) { ex_in[tid] = exv; eb_in[tid] = ebv; }
+  sk_rm_copy(rmu, rm);
+  sk_bins_sum(rm.M * 4, bv, actf, ssum);
+  if (tid == 0) {
+    sk_gate_logic(D, rml, ex_in, eb_in, io, layer, ssum, reinit_s, exited_s, exitb_s, sig_s);
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {
+      const int mm = min(m, rm.M - 1);
+      int src = mm;
+      if (rml.fast[mm] && reinit_s[rml.seq[mm]]) src = rml.slow_of[mm];
+      src_s[m] = src;
+      inv_rms[m] = rsqrtf(ssum[src * 4] / D.d + D.eps);
+    }
+  }
+  __syncthreads();
+  if (blockIdx.x == 0 && tid < rm.nseq) {
+    ws.reinit[layer * kMaxSeq + tid] = reinit_s[tid];
+    ws.exited[tid] = exited_s[tid];
+    ws.exitb[tid] = exitb_s[tid];
+    if (layer > 0) ws.sig[tid * D.n_layers + layer - 1] = sig_s[tid];
+  }
+  rw_store_pieces<true>(xp, D.d, actf);
+  st.run(row_ptr, u0, u1, actf, D.d, epi, oA, oB);
 }
 
 // ============================================================================
@@ -375,41 +441,20 @@ __global__ __launch_bounds__(kRwThreads) void kr_oproj(Dims D, LayerPtrs L, RowM
   __shared__ int flag_s[2 * kMaxSeq];   // exited, reinit per sequence
   __shared__ SkRmLds rmu;
   const RowMap& rml = rmu.rm;
-  const int tid = threadIdx.x, lane = tid & 63, gw = blockIdx.x * kRwWaves + (tid >> 6);
+  const int tid = threadIdx.x, lane = tid & 63, gw = blockIdx.x * kRwWaves + __builtin_amdgcn_readfirstlane(tid >> 6);
   if (io.mode == EX_EXIT && sk_all_exited(rm, ws)) return;
   const int esz = WB ? 2 : 4, r = D.r, HR = D.H * D.r;
   auto row_ptr = [&](int u, int) -> const void* { return (const char*)L.wo + (size_t)u * D.qdim * esz; };
   int u0, u1;
   rw_range(D.d, gridDim.x * kRwWaves, gw, u0, u1);
   RwStream<WB, NCH, 1, NS> st;
-  const int rmw = sk_rm_word(rm);
-  SkPiecesT<RwPM<WB, NCH, NS>::value> xp;
-  sk_load_pieces(ws.O, ws.O + (size_t)(rm.M > 1 ? 1 : 0) * D.qdim, nullptr, D.qdim, xp);
+  RwPieces<RwPM<WB, NCH, NS>::value> xp;
+  rw_load_pieces<false>(ws.O, ws.O + (size_t)(rm.M > 1 ? 1 : 0) * D.qdim, nullptr, D.qdim, xp);
   const float uv0 = ws.uo[min(tid, 2 * HR - 1)];
   const float uv1 = ws.uo[min(tid + kRwThreads, 2 * HR - 1)];
   const int fe = ws.exited[min(tid, kMaxSeq - 1)];
   const int fr = ws.reinit[layer * kMaxSeq + min(tid, kMaxSeq - 1)];
-  __builtin_amdgcn_sched_barrier(0);
-  st.prime(row_ptr, min(u0, D.d - 1));
-  __builtin_amdgcn_sched_barrier(0);
   const bool has_o = L.A[3] && L.B[3];
-  sk_rm_put(rmu, rmw);
-  if (tid < kMaxSeq) { flag_s[tid] = fe; flag_s[kMaxSeq + tid] = fr; }
-  ud_s[tid] = uv0;
-  ud_s[tid + kRwThreads] = uv1;
-  __syncthreads();
-  if (tid < 2 * r) {
-    const int m = tid / r, j = tid % r;
-    float a = 0.f;
-    if (has_o && m < rm.M && rml.fast[m] && 2 * HR <= 2 * kRwThreads) {
-#pragma unroll 8
-      for (int h = 0; h < D.H; ++h) a += ud_s[(m * D.H + h) * r + j];
-    } else if (has_o && m < rm.M && rml.fast[m]) {
-      for (int h = 0; h < D.H; ++h) a += ws.uo[(m * D.H + h) * r + j];
-    }
-    uo_s[tid] = a;
-  }
-  rw_store_pieces(xp, nullptr, D.qdim, actf);
   // per-wave sums: lane m (< 2): sum x^2 of row m; lane c (< 2r): the
   // adapter-down partial c of row 0 (acc0) and row 1 (acc1) when fast
   struct Epi {
@@ -470,7 +515,28 @@ __global__ __launch_bounds__(kRwThreads) void kr_oproj(Dims D, LayerPtrs L, RowM
       if (rm->M > 1 && rm->fast[1]) acc1 += ga * xnew[1];
     }
   } epi{&D, &L, &rml, flag_s, uo_s, ws, layer, has_o, 0.f, 0.f, 0.f};
-  st.run(row_ptr, u0, u1, actf, D.qdim, epi);
+  typename Epi::Ops oA, oB;
+  __builtin_amdgcn_sched_barrier(0);
+  st.begin(row_ptr, u0, u1, epi, oA, oB);
+  __builtin_amdgcn_sched_barrier(0);
+  sk_rm_copy(rmu, rm);
+  if (tid < kMaxSeq) { flag_s[tid] = fe; flag_s[kMaxSeq + tid] = fr; }
+  ud_s[tid] = uv0;
+  ud_s[tid + kRwThreads] = uv1;
+  __syncthreads();
+  if (tid < 2 * r) {
+    const int m = tid / r, j = tid % r;
+    float a = 0.f;
+    if (has_o && m < rm.M && rml.fast[m] && 2 * HR <= 2 * kRwThreads) {
+#pragma unroll 8
+      for (int h = 0; h < D.H; ++h) a += ud_s[(m * D.H + h) * r + j];
+    } else if (has_o && m < rm.M && rml.fast[m]) {
+      for (int h = 0; h < D.H; ++h) a += ws.uo[(m * D.H + h) * r + j];
+    }
+    uo_s[tid] = a;
+  }
+  rw_store_pieces<false>(xp, D.qdim, actf);
+  st.run(row_ptr, u0, u1, actf, D.qdim, epi, oA, oB);
   const int bin = blockIdx.x % kBinSlots;
   rw_wg_sum(epi.accx, 2, wsum, tot);
   if (tid < rm.M) add_agent(bin_o_at(ws, D, layer, bin, tid), tot[tid]);
@@ -495,7 +561,7 @@ __global__ __launch_bounds__(kRwThreads) void kr_gateup(Dims D, LayerPtrs L, Row
   __shared__ float tot[64];
   __shared__ SkRmLds rmu;
   const RowMap& rml = rmu.rm;
-  const int tid = threadIdx.x, gw = blockIdx.x * kRwWaves + (tid >> 6);
+  const int tid = threadIdx.x, gw = blockIdx.x * kRwWaves + __builtin_amdgcn_readfirstlane(tid >> 6);
   if (io.mode == EX_EXIT && sk_all_exited(rm, ws)) return;
   const int esz = WB ? 2 : 4, r = D.r, PO = 1 + 2 * r;
   auto row_ptr = [&](int hu, int) -> const void* {
@@ -505,18 +571,10 @@ __global__ __launch_bounds__(kRwThreads) void kr_gateup(Dims D, LayerPtrs L, Row
   rw_range(D.F, gridDim.x * kRwWaves, gw, j0, j1);
   const int u0 = 2 * j0, u1 = 2 * j1;
   RwStream<WB, NCH, 1, NS> st;
-  const int rmw = sk_rm_word(rm);
   float sv[(2 * (1 + 2 * kMaxRank) * kBinSlots + kSkThreads - 1) / kSkThreads];
-  sk_bins_load(rm.M * PO, [&](int q, int b) { return bin_o_at(ws, D, layer, b, q / PO) + q % PO; }, sv);
-  SkPiecesT<RwPM<WB, NCH, NS>::value> xp;
-  sk_load_pieces(ws.X, ws.X + (size_t)(rm.M > 1 ? 1 : 0) * D.d, L.mlp_norm, D.d, xp);
-  __builtin_amdgcn_sched_barrier(0);
-  st.prime(row_ptr, min(u0, 2 * D.F - 1));
-  __builtin_amdgcn_sched_barrier(0);
-  sk_rm_put(rmu, rmw);
-  sk_bins_sum(rm.M * PO, sv, actf, stat);
-  if (tid < 2) inv_rms[tid] = rsqrtf(stat[min(tid, rm.M - 1) * PO] / D.d + D.eps);
-  rw_store_pieces(xp, L.mlp_norm, D.d, actf);
+  sk_bins_load(rm.M * PO, bin_o_at(ws, D, layer, 0, 0), kMaxRows * PO, sv);
+  RwPieces<RwPM<WB, NCH, NS>::value> xp;
+  rw_load_pieces<true>(ws.X, ws.X + (size_t)(rm.M > 1 ? 1 : 0) * D.d, L.mlp_norm, D.d, xp);
   struct Epi {
     struct Ops {
       float a;   // A_d[lane % r][j]
@@ -562,7 +620,15 @@ __global__ __launch_bounds__(kRwThreads) void kr_gateup(Dims D, LayerPtrs L, Row
       if (rm->M > 1 && rm->fast[1]) acc1 += o.a * av[1];
     }
   } epi{&D, &L, &rml, stat, inv_rms, ws, L.A[4] && L.B[4], L.A[5] && L.B[5], 0.f, 0.f, 0.f, 0.f};
-  st.run(row_ptr, u0, u1, actf, D.d, epi);
+  typename Epi::Ops oA, oB;
+  __builtin_amdgcn_sched_barrier(0);
+  st.begin(row_ptr, u0, u1, epi, oA, oB);
+  __builtin_amdgcn_sched_barrier(0);
+  sk_rm_copy(rmu, rm);
+  sk_bins_sum(rm.M * PO, sv, actf, stat);
+  if (tid < 2) inv_rms[tid] = rsqrtf(stat[min(tid, rm.M - 1) * PO] / D.d + D.eps);
+  rw_store_pieces<true>(xp, D.d, actf);
+  st.run(row_ptr, u0, u1, actf, D.d, epi, oA, oB);
   for (int m = 0; m < 2; ++m) {
     rw_wg_sum(m ? epi.acc1 : epi.acc0, r, wsum, tot);
     if (tid < r && L.A[6] && m < rm.M && rml.fast[m])
@@ -583,7 +649,7 @@ __global__ __launch_bounds__(kRwThreads) void kr_down(Dims D, LayerPtrs L, RowMa
   __shared__ int ex_s[kMaxSeq];
   __shared__ SkRmLds rmu;
   const RowMap& rml = rmu.rm;
-  const int tid = threadIdx.x, gw = blockIdx.x * kRwWaves + (tid >> 6);
+  const int tid = threadIdx.x, gw = blockIdx.x * kRwWaves + __builtin_amdgcn_readfirstlane(tid >> 6);
   if (io.mode == EX_EXIT && sk_all_exited(rm, ws)) {
     if (blockIdx.x == 0) rows_unchanged_stats(D, rm, ws, layer + 1);
     return;
@@ -593,19 +659,11 @@ __global__ __launch_bounds__(kRwThreads) void kr_down(Dims D, LayerPtrs L, RowMa
   int u0, u1;
   rw_range(D.d, gridDim.x * kRwWaves, gw, u0, u1);
   RwStream<WB, NCH, 1, NS> st;
-  const int rmw = sk_rm_word(rm);
   float uv[(2 * kMaxRank * kBinSlots + kSkThreads - 1) / kSkThreads];
-  sk_bins_load(rm.M * r, [&](int q, int b) { return bin_gu_at(ws, D, layer, b, q / r) + q % r; }, uv);
-  SkPiecesT<RwPM<WB, NCH, NS>::value> xp;
-  sk_load_pieces(ws.ACT, ws.ACT + (size_t)(rm.M > 1 ? 1 : 0) * D.F, nullptr, D.F, xp);
+  sk_bins_load(rm.M * r, bin_gu_at(ws, D, layer, 0, 0), kMaxRows * r, uv);
+  RwPieces<RwPM<WB, NCH, NS>::value> xp;
+  rw_load_pieces<false>(ws.ACT, ws.ACT + (size_t)(rm.M > 1 ? 1 : 0) * D.F, nullptr, D.F, xp);
   const int exv = ws.exited[min(tid, kMaxSeq - 1)];
-  __builtin_amdgcn_sched_barrier(0);
-  st.prime(row_ptr, min(u0, D.d - 1));
-  __builtin_amdgcn_sched_barrier(0);
-  sk_rm_put(rmu, rmw);
-  if (tid < kMaxSeq) ex_s[tid] = exv;
-  sk_bins_sum(rm.M * r, uv, actf, ud);
-  rw_store_pieces(xp, nullptr, D.F, actf);
   struct Epi {
     struct Ops {
       float x0, x1, p0, p1;
@@ -650,7 +708,15 @@ __global__ __launch_bounds__(kRwThreads) void kr_down(Dims D, LayerPtrs L, RowMa
       }
     }
   } epi{&D, &L, &rml, ud, ex_s, ws, L.A[6] && L.B[6], 0.f};
-  st.run(row_ptr, u0, u1, actf, D.F, epi);
+  typename Epi::Ops oA, oB;
+  __builtin_amdgcn_sched_barrier(0);
+  st.begin(row_ptr, u0, u1, epi, oA, oB);
+  __builtin_amdgcn_sched_barrier(0);
+  sk_rm_copy(rmu, rm);
+  if (tid < kMaxSeq) ex_s[tid] = exv;
+  sk_bins_sum(rm.M * r, uv, actf, ud);
+  rw_store_pieces<false>(xp, D.F, actf);
+  st.run(row_ptr, u0, u1, actf, D.F, epi, oA, oB);
   rw_wg_sum(epi.acc, 6, wsum, tot);
   if (tid < 2 * 3 && tid / 3 < rm.M) add_agent(bin_d_at(ws, layer + 1, blockIdx.x % kBinSlots, tid / 3) + tid % 3, tot[tid]);
 }
@@ -672,24 +738,45 @@ __global__ __launch_bounds__(kRwThreads) void kr_head(Dims D, const void* lm_hea
   __shared__ int bi_s[kRwWaves][2];
   __shared__ SkRmLds rmu;
   const RowMap& rml = rmu.rm;
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, gw = blockIdx.x * kRwWaves + wv;
+  const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6), gw = blockIdx.x * kRwWaves + wv;
   const int esz = WB ? 2 : 4;
   auto row_ptr = [&](int u, int) -> const void* { return (const char*)lm_head + (size_t)u * D.d * esz; };
   int u0, u1;
   rw_range(D.V, gridDim.x * kRwWaves, gw, u0, u1);
   RwStream<WB, NCH, 1, NS> st;
-  const int rmw = sk_rm_word(rm);
   float bv[1];
-  sk_bins_load(rm.M * 4, [&](int q, int b) { return bin_d_at(ws, n_layers_run, b, q >> 2) + (q & 3); }, bv);
+  sk_bins_load(rm.M * 4, bin_d_at(ws, n_layers_run, 0, 0), kMaxRows * 4, bv);
   const int exv = ws.exited[min(tid, rm.nseq - 1)];
   const float* X1 = ws.X + (size_t)(rm.M > 1 ? 1 : 0) * D.d;
-  SkPiecesT<RwPM<WB, NCH, NS>::value> xp;
-  sk_load_pieces(ws.X, X1, final_norm, D.d, xp);
+  RwPieces<RwPM<WB, NCH, NS>::value> xp;
+  rw_load_pieces<true>(ws.X, X1, final_norm, D.d, xp);
+  struct Epi {
+    struct Ops {};
+    const Dims* D;
+    const int* hrow;
+    const float* ir;
+    float* logits;
+    int nh;
+    float bz[2];
+    int bi[2];
+    __device__ void fetch(int, Ops&) const {}
+    __device__ void run(int v, const float (&y)[1][2], const Ops&) {
+      const int lane = threadIdx.x & 63;
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        if (k >= nh) continue;
+        const float z = y[0][hrow[k]] * ir[k];
+        if (logits && lane == k) logits[(size_t)k * D->V + v] = z;
+        if (z > bz[k]) { bz[k] = z; bi[k] = v; }   // rows in increasing order: the lowest index wins ties
+      }
+    }
+  } epi{&D, hrow, inv_rms, io.logits_out, 0, {-INFINITY, -INFINITY}, {0x7fffffff, 0x7fffffff}};
+  typename Epi::Ops oA, oB;
   __builtin_amdgcn_sched_barrier(0);
-  st.prime(row_ptr, min(u0, D.V - 1));
+  st.begin(row_ptr, u0, u1, epi, oA, oB);
   __builtin_amdgcn_sched_barrier(0);
   if (tid < rm.nseq) ex_in[tid] = exv;
-  sk_rm_put(rmu, rmw);
+  sk_rm_copy(rmu, rm);
   sk_bins_sum(rm.M * 4, bv, actf, ssum);
   if (tid == 0) {
     int nh = 0;
@@ -712,29 +799,9 @@ __global__ __launch_bounds__(kRwThreads) void kr_head(Dims D, const void* lm_hea
   __syncthreads();
   const int nh = nh_s;
   // head row k reads activation row hrow[k] (the staged rows are X[0] and X[1])
-  rw_store_pieces(xp, final_norm, D.d, actf);
-  struct Epi {
-    struct Ops {};
-    const Dims* D;
-    const int* hrow;
-    const float* ir;
-    float* logits;
-    int nh;
-    float bz[2];
-    int bi[2];
-    __device__ void fetch(int, Ops&) const {}
-    __device__ void run(int v, const float (&y)[1][2], const Ops&) {
-      const int lane = threadIdx.x & 63;
-#pragma unroll
-      for (int k = 0; k < 2; ++k) {
-        if (k >= nh) continue;
-        const float z = y[0][hrow[k]] * ir[k];
-        if (logits && lane == k) logits[(size_t)k * D->V + v] = z;
-        if (z > bz[k]) { bz[k] = z; bi[k] = v; }   // rows in increasing order: the lowest index wins ties
-      }
-    }
-  } epi{&D, hrow, inv_rms, io.logits_out, nh, {-INFINITY, -INFINITY}, {0x7fffffff, 0x7fffffff}};
-  st.run(row_ptr, u0, u1, actf, D.d, epi);
+  rw_store_pieces<true>(xp, D.d, actf);
+  epi.nh = nh;
+  st.run(row_ptr, u0, u1, actf, D.d, epi, oA, oB);
   if (lane == 0) {
     bz_s[wv][0] = epi.bz[0]; bz_s[wv][1] = epi.bz[1];
     bi_s[wv][0] = epi.bi[0]; bi_s[wv][1] = epi.bi[1];

@@ -55,7 +55,6 @@ __global__ __launch_bounds__(kSkAttnThreads) void ks_attn(Dims D, LayerPtrs L, R
   const float scale = rsqrtf((float)HD);
 
   // ---- round one: everything that does not depend on the position ----------
-  const int rmw = sk_rm_word(rm);
   const int posv = io.positions[sq];
   const int exv = ws.exited[sq];
   int blk[TPT];
@@ -107,7 +106,7 @@ __global__ __launch_bounds__(kSkAttnThreads) void ks_attn(Dims D, LayerPtrs L, R
   }
 
   // ---- round-one values into LDS (the wait for them drains nothing else) ------
-  sk_rm_put(rmu, rmw);
+  sk_rm_copy(rmu, rm);
 #pragma unroll
   for (int w = 0; w < 3; ++w)
 #pragma unroll

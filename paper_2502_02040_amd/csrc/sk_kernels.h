@@ -157,17 +157,24 @@ __device__ __forceinline__ void sk_store_pieces(const SkPieces& xp, const float*
 
 // ---------------------------------------------------------------------------
 // Row statistics: sums over the kBinSlots bins of nv values (value q of bin b
-// at ptr(q, b)).  Every thread loads NPT bin entries before the weights are
-// primed; sk_bins_sum adds them in bin order (results do not depend on
-// timing) through the LDS scratch (nv * kBinSlots floats) into out[nv].
+// at base[b * stride + q]).  Every thread loads NPT bin entries before the
+// weights are primed, consecutive threads reading consecutive values of one
+// bin; sk_bins_sum adds them in bin order (results do not depend on timing)
+// through the LDS scratch (nv * kBinSlots floats) into out[nv].
 // ---------------------------------------------------------------------------
-template <int NPT, class Ptr>
-__device__ __forceinline__ void sk_bins_load(int nv, const Ptr& ptr, float (&v)[NPT]) {
-  const int n = nv * kBinSlots;
+template <int NPT>
+__device__ __forceinline__ void sk_bins_load(int nv, const float* base, int stride, float (&v)[NPT]) {
+  // element i = threadIdx.x + kSkThreads * k as (bin b, value q), stepped
+  // without a division per element
+  int b = (int)threadIdx.x / nv, q = (int)threadIdx.x - b * nv;
+  const int db = kSkThreads / nv, dq = kSkThreads - db * nv;
 #pragma unroll
   for (int k = 0; k < NPT; ++k) {
-    const int i = min((int)threadIdx.x + kSkThreads * k, n - 1);
-    v[k] = *ptr(i / kBinSlots, i % kBinSlots);
+    const bool in = b < kBinSlots;   // past the end: read the last entry
+    v[k] = base[(size_t)(in ? b : kBinSlots - 1) * stride + (in ? q : nv - 1)];
+    b += db;
+    q += dq;
+    if (q >= nv) { q -= nv; ++b; }
   }
 }
 template <int NPT>
@@ -182,7 +189,7 @@ __device__ __forceinline__ void sk_bins_sum(int nv, const float (&v)[NPT], float
   if ((int)threadIdx.x < nv) {
     float a = 0.f;
 #pragma unroll
-    for (int b = 0; b < kBinSlots; ++b) a += scratch[threadIdx.x * kBinSlots + b];
+    for (int b = 0; b < kBinSlots; ++b) a += scratch[b * nv + threadIdx.x];
     out[threadIdx.x] = a;
   }
   __syncthreads();
@@ -421,14 +428,31 @@ __device__ __forceinline__ float sum16(float v) { return row_sum16(v); }
 // copy in LDS.
 static_assert(sizeof(RowMap) % 4 == 0, "row map copied as words");
 constexpr int kRmWords = (int)(sizeof(RowMap) / 4);
-__device__ __forceinline__ int sk_rm_word(const RowMap& rm) {
-  return ((const int*)&rm)[min((int)threadIdx.x, kRmWords - 1)];
-}
 union SkRmLds {
   RowMap rm;
-  int w[kRmWords + 1];   // word kRmWords: written by every thread past the map (no branch around the store)
+  int w[kRmWords];
 };
-__device__ __forceinline__ void sk_rm_put(SkRmLds& dst, int w) { dst.w[min((int)threadIdx.x, kRmWords)] = w; }
+// Copy of the map into LDS by the first wave (readable after the next
+// workgroup barrier).  The words are read with constant indices, i.e. scalar
+// loads through the constant cache (a lane-indexed read of a kernel argument
+// would be a vector load from the argument segment, which misses every cache
+// at kernel start); lane i stores word i.
+__device__ __forceinline__ void sk_rm_copy(SkRmLds& dst, const RowMap& rm) {
+  static_assert(kRmWords <= 64, "one word per lane of the first wave");
+  if (threadIdx.x >= 64) return;
+  const int* w = (const int*)&rm;
+  const int t = (int)threadIdx.x;
+  int wv[kRmWords];
+#pragma unroll
+  for (int i = 0; i < kRmWords; ++i) {
+    wv[i] = w[i];
+    asm volatile("" : "+s"(wv[i]));   // opaque: the select below stays a select of values
+  }
+  int v = wv[kRmWords - 1];
+#pragma unroll
+  for (int i = 0; i < kRmWords - 1; ++i) v = t == i ? wv[i] : v;
+  if (t < kRmWords) dst.w[t] = v;
+}
 
 // The gate decision of gate_logic for at most two sequences.
 __device__ __forceinline__ void sk_gate_logic(const Dims& D, const RowMap& rm, const int* ex_in, const int* eb_in,
@@ -479,10 +503,9 @@ __global__ __launch_bounds__(kSkThreads) void ks_qkv(Dims D, LayerPtrs L, RowMap
   const int tid = threadIdx.x, gw = blockIdx.x * kSkWaves + (tid >> 6);
   SkStream<WB, false> st;
   st.init(P, L.pq, gw, D.d);
-  const int rmw = sk_rm_word(rm);
   // loads needed before the weights: issued first
   float bv[1];
-  sk_bins_load(rm.M * 4, [&](int q, int b) { return bin_d_at(ws, layer, b, q >> 2) + (q & 3); }, bv);
+  sk_bins_load(rm.M * 4, bin_d_at(ws, layer, 0, 0), kMaxRows * 4, bv);
   const int sq0 = min(tid, rm.nseq - 1);
   const int exv = ws.exited[sq0], ebv = ws.exitb[sq0];
   const float* r0 = ws.X;
@@ -493,7 +516,7 @@ __global__ __launch_bounds__(kSkThreads) void ks_qkv(Dims D, LayerPtrs L, RowMap
   st.prime();
   __builtin_amdgcn_sched_barrier(0);
   if (tid < rm.nseq) { ex_in[tid] = exv; eb_in[tid] = ebv; }
-  sk_rm_put(rmu, rmw);
+  sk_rm_copy(rmu, rm);
   sk_bins_sum(rm.M * 4, bv, (float*)act, ssum);
   if (tid == 0) {
     sk_gate_logic(D, rml, ex_in, eb_in, io, layer, ssum, reinit_s, exited_s, exitb_s, sig_s);
@@ -541,7 +564,6 @@ __global__ __launch_bounds__(kSkThreads) void ks_oproj(Dims D, LayerPtrs L, RowM
   if (io.mode == EX_EXIT && sk_all_exited(rm, ws)) return;
   SkStream<WB, false> st;
   st.init(P, L.po, gw, D.qdim);
-  const int rmw = sk_rm_word(rm);
   const int HR = D.H * D.r;
   const float* r0 = ws.O;
   const float* r1 = ws.O + (size_t)(rm.M > 1 ? 1 : 0) * D.qdim;
@@ -554,7 +576,7 @@ __global__ __launch_bounds__(kSkThreads) void ks_oproj(Dims D, LayerPtrs L, RowM
   st.prime();
   __builtin_amdgcn_sched_barrier(0);
   const bool has_o = L.A[3] && L.B[3];
-  sk_rm_put(rmu, rmw);
+  sk_rm_copy(rmu, rm);
   __syncthreads();
   if (2 * HR <= 2 * kSkThreads) {
     ud_s[tid] = u0;
@@ -654,7 +676,7 @@ __global__ __launch_bounds__(kSkThreads) void ks_gateup(Dims D, LayerPtrs L, Row
   st.init(P, L.pg, gw, D.d);
   const int PO = 1 + 2 * D.r;
   float sv[(2 * (1 + 2 * kMaxRank) * kBinSlots + kSkThreads - 1) / kSkThreads];
-  sk_bins_load(rm.M * PO, [&](int q, int b) { return bin_o_at(ws, D, layer, b, q / PO) + q % PO; }, sv);
+  sk_bins_load(rm.M * PO, bin_o_at(ws, D, layer, 0, 0), kMaxRows * PO, sv);
   const float* r0 = ws.X;
   const float* r1 = ws.X + (size_t)(rm.M > 1 ? 1 : 0) * D.d;
   SkPieces xp;
@@ -719,7 +741,7 @@ __global__ __launch_bounds__(kSkThreads) void ks_down(Dims D, LayerPtrs L, RowMa
   SkStream<WB, false> st;
   st.init(P, L.pd, gw, D.F);
   float uv[(2 * kMaxRank * kBinSlots + kSkThreads - 1) / kSkThreads];
-  sk_bins_load(rm.M * D.r, [&](int q, int b) { return bin_gu_at(ws, D, layer, b, q / D.r) + q % D.r; }, uv);
+  sk_bins_load(rm.M * D.r, bin_gu_at(ws, D, layer, 0, 0), kMaxRows * D.r, uv);
   const float* r0 = ws.ACT;
   const float* r1 = ws.ACT + (size_t)(rm.M > 1 ? 1 : 0) * D.F;
   SkPieces xp;
@@ -778,9 +800,8 @@ __global__ __launch_bounds__(kSkThreads) void ks_head(Dims D, const void* lm_hea
   const int tid = threadIdx.x, gw = blockIdx.x * kSkWaves + (tid >> 6);
   SkStream<WB, false> st;
   st.init(P, lm_head, gw, D.d);
-  const int rmw = sk_rm_word(rm);
   float bv[1];
-  sk_bins_load(rm.M * 4, [&](int q, int b) { return bin_d_at(ws, n_layers_run, b, q >> 2) + (q & 3); }, bv);
+  sk_bins_load(rm.M * 4, bin_d_at(ws, n_layers_run, 0, 0), kMaxRows * 4, bv);
   const int exv = ws.exited[min(tid, rm.nseq - 1)];
   const float* r0 = ws.X;
   const float* r1 = ws.X + (size_t)(rm.M > 1 ? 1 : 0) * D.d;
@@ -790,7 +811,7 @@ __global__ __launch_bounds__(kSkThreads) void ks_head(Dims D, const void* lm_hea
   st.prime();
   __builtin_amdgcn_sched_barrier(0);
   if (tid < rm.nseq) ex_in[tid] = exv;
-  sk_rm_put(rmu, rmw);
+  sk_rm_copy(rmu, rm);
   sk_bins_sum(rm.M * 4, bv, (float*)act, ssum);
   if (tid == 0) {
     // rows fed to the head
