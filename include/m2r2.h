@@ -317,6 +317,19 @@ M2R2_API m2r2_status m2r2_expert_cache_replay(int32_t n_layers, int32_t n_expert
 M2R2_API m2r2_status m2r2_timing_enable(m2r2_ctx* ctx, int32_t kernel_class);
 M2R2_API m2r2_status m2r2_timing_read(m2r2_ctx* ctx, double* ms_sum, int32_t* launches);
 
+/* Average duration of one gate/up launch (kernel class 3) of the
+ * one-sequence decode step (two rows when `dual`, one otherwise): the kernel
+ * of every layer is launched back to back on `stream` between one pair of HIP
+ * events (which keeps the events' own latency out of the per-launch figure;
+ * each layer streams its own weights, as in a step), and *avg_ms receives the
+ * elapsed time divided by the layer count.  Waits for `stream`.  Side
+ * effects: the workspace's SwiGLU activations and the gate/up row statistics
+ * (zeroed at the start of every pass) are overwritten; the residual stream,
+ * the cache and the positions are not touched.  Returns M2R2_E_UNSUPPORTED
+ * when the one- and two-row decode class does not use the row-per-wave
+ * kernels (for example a mixture-of-experts model). */
+M2R2_API m2r2_status m2r2_time_gateup_layers(m2r2_ctx* ctx, int32_t dual, hipStream_t stream, double* avg_ms);
+
 /* Sticky device error bits set by kernels since the context was created
  * (1: token id out of range, 2: cache position outside the block table,
  * 4: context longer than the workspace was sized for); waits for `stream`. */

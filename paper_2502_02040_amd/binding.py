@@ -22,8 +22,8 @@ MODES = {"off": EXIT_OFF, "observe": EXIT_OBSERVE, "exit": EXIT_EXIT}
 PROJ = ("q", "k", "v", "o", "g", "u", "d")
 
 EXPORTS = ("m2r2_workspace_size", "m2r2_create", "m2r2_destroy", "m2r2_decode_step", "m2r2_draft", "m2r2_verify",
-           "m2r2_timing_enable", "m2r2_timing_read", "m2r2_device_errors", "m2r2_last_error",
-           "m2r2_expert_bytes", "m2r2_pack_expert", "m2r2_moe_set_policy", "m2r2_prefetch_experts",
+           "m2r2_timing_enable", "m2r2_timing_read", "m2r2_time_gateup_layers", "m2r2_device_errors",
+           "m2r2_last_error", "m2r2_expert_bytes", "m2r2_pack_expert", "m2r2_moe_set_policy", "m2r2_prefetch_experts",
            "m2r2_moe_reset", "m2r2_moe_stats", "m2r2_expert_cache_replay")
 KERNEL_CLASSES = {"qkv": 0, "attn": 1, "oproj": 2, "gateup": 3, "down": 4, "head": 5, "embed": 6, "attn_merge": 7,
                   "expert_gateup": 8, "expert_down": 9, "router": 10}
@@ -100,6 +100,7 @@ def lib() -> ctypes.CDLL:
                                   c_void_p]
         L.m2r2_timing_enable.argtypes = [c_void_p, c_int32]
         L.m2r2_timing_read.argtypes = [c_void_p, POINTER(ctypes.c_double), POINTER(c_int32)]
+        L.m2r2_time_gateup_layers.argtypes = [c_void_p, c_int32, c_void_p, POINTER(ctypes.c_double)]
         L.m2r2_device_errors.argtypes = [c_void_p, c_void_p, POINTER(c_int32)]
         L.m2r2_last_error.restype = ctypes.c_char_p
         L.m2r2_expert_bytes.argtypes = [POINTER(Config), POINTER(c_size_t)]
@@ -111,7 +112,8 @@ def lib() -> ctypes.CDLL:
         L.m2r2_expert_cache_replay.argtypes = [c_int32, c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,
                                                c_int32, POINTER(MoeCounters)]
         for f in ("m2r2_workspace_size", "m2r2_create", "m2r2_decode_step", "m2r2_draft", "m2r2_verify",
-                  "m2r2_timing_enable", "m2r2_timing_read", "m2r2_device_errors", "m2r2_expert_bytes",
+                  "m2r2_timing_enable", "m2r2_timing_read", "m2r2_time_gateup_layers", "m2r2_device_errors",
+                  "m2r2_expert_bytes",
                   "m2r2_pack_expert", "m2r2_moe_set_policy", "m2r2_prefetch_experts", "m2r2_moe_reset",
                   "m2r2_moe_stats", "m2r2_expert_cache_replay"):
             getattr(L, f).restype = c_int32
@@ -364,6 +366,14 @@ class Model:
         ms, n = ctypes.c_double(0.0), c_int32(0)
         _check(lib().m2r2_timing_read(self._ctx, ctypes.byref(ms), ctypes.byref(n)), "m2r2_timing_read")
         return ms.value, n.value
+
+    def time_gateup_layers(self, dual: bool = True, *, stream=None) -> float:
+        """Average milliseconds of one gate/up launch, the kernel of every
+        layer launched back to back between one pair of events (waits)."""
+        ms = ctypes.c_double(0.0)
+        _check(lib().m2r2_time_gateup_layers(self._ctx, int(bool(dual)), _stream(stream), ctypes.byref(ms)),
+               "m2r2_time_gateup_layers")
+        return ms.value
 
     # -- mixture of experts --------------------------------------------------------
     def moe_set_policy(self, policy: str) -> None:

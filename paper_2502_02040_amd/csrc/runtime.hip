@@ -1078,6 +1078,38 @@ M2R2_API m2r2_status m2r2_timing_read(m2r2_ctx* c, double* ms_sum, int32_t* laun
   return M2R2_OK;
 }
 
+M2R2_API m2r2_status m2r2_time_gateup_layers(m2r2_ctx* c, int32_t dual, hipStream_t st, double* avg_ms) {
+  if (!c || !avg_ms) return fail(M2R2_E_INVALID, "NULL argument");
+  if (!c->rw_on || c->moe.on) return fail(M2R2_E_UNSUPPORTED, "the decode class does not use the row-per-wave kernels");
+  const Dims& D = c->D;
+  RowMap rm = empty_rowmap();
+  rm.nseq = 1;
+  rm.M = dual ? 2 : 1;
+  rm.first[0] = 0;
+  rm.cnt[0] = rm.M;
+  rm.seq[0] = 0; rm.fast[0] = 0; rm.wr[0] = 1;
+  if (dual) { rm.seq[1] = 0; rm.fast[1] = 1; rm.wr[1] = 0; rm.slow_of[1] = 0; }
+  const StepIO io = empty_io();
+  hipEvent_t a, b;
+  HIP_TRY(hipEventCreate(&a));
+  HIP_TRY(hipEventCreate(&b));
+  hipError_t e = hipEventRecord(a, st);
+  for (int l = 0; l < D.n_layers && e == hipSuccess; ++l) {
+    if (D.wbf16) kr_gateup_launch<1>(c->rw_nch[0], c->sk_grid, (size_t)kSkMinLds, st, D, c->layers[l], rm, c->ws, io, l);
+    else kr_gateup_launch<0>(c->rw_nch[0], c->sk_grid, (size_t)kSkMinLds, st, D, c->layers[l], rm, c->ws, io, l);
+    e = hipGetLastError();
+  }
+  if (e == hipSuccess) e = hipEventRecord(b, st);
+  if (e == hipSuccess) e = hipEventSynchronize(b);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, a, b);
+  (void)hipEventDestroy(a);
+  (void)hipEventDestroy(b);
+  HIP_TRY(e);
+  *avg_ms = (double)ms / D.n_layers;
+  return M2R2_OK;
+}
+
 M2R2_API m2r2_status m2r2_device_errors(m2r2_ctx* c, hipStream_t stream, int32_t* bits) {
   if (!c || !bits) return fail(M2R2_E_INVALID, "NULL argument");
   HIP_TRY(hipMemcpyAsync(bits, c->ws.err, sizeof(int32_t), hipMemcpyDeviceToHost, stream));

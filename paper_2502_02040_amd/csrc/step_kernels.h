@@ -890,26 +890,26 @@ __global__ __launch_bounds__(256) void k_pack_pair(const void* wg, const void* w
 // Kernel: embedding gather + per-step control initialisation + zeroed bins.
 // grid = M rows + kEmbedZeroBlocks, block = 256.  Block m < M gathers row m
 // and writes its layer-0 bins (every slot); the other blocks zero the bins
-// of every later layer (all rows, all slots).
+// of every later layer (all slots, the M rows in use).
 // ============================================================================
 constexpr int kEmbedZeroBlocks = 64;
 
 __global__ __launch_bounds__(256) void k_embed(Dims D, const void* embed, RowMap rm, WS ws, StepIO io, int init_ctl) {
   __shared__ float red[4];
   if ((int)blockIdx.x >= rm.M) {
-    // zero bin_d of layers 1..n_layers, bin_o and bin_gu (float4 stores)
-    const size_t nd = (size_t)D.n_layers * kBinSlots * kMaxRows * 4 / 4;
-    const size_t no = (size_t)D.n_layers * kBinSlots * kMaxRows * (1 + 2 * D.r) / 4;
-    const size_t ng = (size_t)D.n_layers * kBinSlots * kMaxRows * D.r / 4;
-    float4* pd = (float4*)(ws.bin_d + (size_t)kBinSlots * kMaxRows * 4);
-    float4* po = (float4*)ws.bin_o;
-    float4* pg = (float4*)ws.bin_gu;
-    const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
-    const size_t stride = (size_t)(gridDim.x - rm.M) * 256;
-    for (size_t i = (size_t)(blockIdx.x - rm.M) * 256 + threadIdx.x; i < nd + no + ng; i += stride) {
-      if (i < nd) pd[i] = z;
-      else if (i < nd + no) po[i - nd] = z;
-      else pg[i - nd - no] = z;
+    // zero bin_d of layers 1..n_layers, bin_o and bin_gu: every (layer, slot)
+    // block holds kMaxRows rows of nv values, of which rows < M are used
+    const int nvs[3] = {4, 1 + 2 * D.r, D.r};
+    float* bases[3] = {ws.bin_d + (size_t)kBinSlots * kMaxRows * 4, ws.bin_o, ws.bin_gu};
+    const int nblk = D.n_layers * kBinSlots;
+    const int stride = (gridDim.x - rm.M) * 256;
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+      const int used = rm.M * nvs[a], n = nblk * used;
+      for (int i = (blockIdx.x - rm.M) * 256 + threadIdx.x; i < n; i += stride) {
+        const int blk = i / used;
+        bases[a][(size_t)blk * kMaxRows * nvs[a] + (i - blk * used)] = 0.f;
+      }
     }
     return;
   }
