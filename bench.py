@@ -369,7 +369,7 @@ def run_batch(args) -> int:
                               f"paged KV context {ctx} per sequence (block 16, shuffled table, seeded N(0,1) "
                               f"content), HIP graph replay", "batch": B, "kv_context": ctx, "dual_stream": dual},
           step_hbm_gbs=round(step_gbs, 1), step_bytes=int(sb), step_roofline_frac=round(step_gbs / HBM_PEAK_GBS, 4),
-          roofline={"bound": "hbm", "kernel": "split-context attention (k_attn)", "achieved": round(achieved, 1),
+          roofline={"bound": "hbm", "kernel": "split-context attention, 128-token splits (ks_attn)", "achieved": round(achieved, 1),
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                     "traffic": None, "avg_kernel_us": round(k_avg_ms * 1e3, 3), "bytes_per_launch": int(ab),
                     "launches_timed": k_n},

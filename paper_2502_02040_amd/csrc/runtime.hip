@@ -462,15 +462,23 @@ m2r2_status run_layers_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const 
   const int nqkv = 3 * D.qdim + 3 * D.r;
   int rows_per_seq = 1;
   for (int s = 0; s < rm.nseq; ++s) rows_per_seq = std::max(rows_per_seq, (int)rm.cnt[s]);
+  // one or two rows per sequence (batched decoding): the short-chain
+  // attention with fixed splits; longer chunks: the general kernel
+  const bool short_attn = c->sk_attn_S > 0 && rows_per_seq <= 2;
   const int S = choose_splits(rm.nseq, rows_per_seq, D.H, c->max_ctx);
-  if (S > c->lay.S_max) return fail(M2R2_E_SHAPE, "attention splits exceed the workspace");
-  if (S + 1 > 64) return fail(M2R2_E_SHAPE, "context too long for the attention merge (max_ctx %d)", c->max_ctx);
+  if (!short_attn && S > c->lay.S_max) return fail(M2R2_E_SHAPE, "attention splits exceed the workspace");
+  if (!short_attn && S + 1 > 64)
+    return fail(M2R2_E_SHAPE, "context too long for the attention merge (max_ctx %d)", c->max_ctx);
   const size_t smem = attn_smem_bytes();
   const Grids G = grids<WB, MT>(c);
   for (int l = 0; l < n_layers_run; ++l) {
     const LayerPtrs& L = c->layers[l];
     TIMED(0, (k_qkv<WB, MT><<<G.qkv, kGemvThreads, G.l_d, st>>>(D, L, rm, c->ws, io, l)));
-    TIMED(1, (k_attn<KB, HD><<<dim3(S + 1, D.H, rm.nseq), kAttnThreads, smem, st>>>(D, L, rm, c->ws, io, kv, l, S)));
+    if (short_attn)
+      TIMED(1, (ks_attn<WB, KB, HD><<<dim3(c->sk_attn_S, D.H, rm.nseq), kSkAttnThreads,
+                                       sk_attn_lds_bytes(HD, D.r, WB), st>>>(D, L, rm, c->ws, io, kv, l, c->sk_attn_S)));
+    else
+      TIMED(1, (k_attn<KB, HD><<<dim3(S + 1, D.H, rm.nseq), kAttnThreads, smem, st>>>(D, L, rm, c->ws, io, kv, l, S)));
     TIMED(2, (k_oproj<WB, MT><<<G.o, kGemvThreads, G.l_q, st>>>(D, L, rm, c->ws, io, l)));
     TIMED(3, (k_gateup<WB, MT><<<G.gu, kGemvThreads, G.l_d, st>>>(D, L, rm, c->ws, io, l)));
     TIMED(4, (k_down<WB, MT><<<G.o, kGemvThreads, G.l_f, st>>>(D, L, rm, c->ws, io, l)));

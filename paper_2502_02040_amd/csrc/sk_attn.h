@@ -66,11 +66,13 @@ __global__ __launch_bounds__(kSkAttnThreads) void ks_attn(Dims D, LayerPtrs L, R
   // projection outputs of row m = e / HD, dim d = e % HD (rows of this
   // sequence: the map is read below; row indices are clamped to the batch)
   const int e_m = min(tid / HD, 1), e_d = tid % HD;
-  const int prow0 = min(sq, rm.M - 1);   // first row of the sequence for nseq <= 2 with one or two rows each
+  // first row of sequence sq (scalar: constant-index reads of the map, a
+  // uniform select; the sequence's rows are [first, first + cnt))
+  int prow0 = rm.first[0];
+#pragma unroll
+  for (int i = 1; i < kMaxSeq; ++i) prow0 = sq == i ? (int)rm.first[i] : prow0;
   float pv[3];
   {
-    // rows of sequence sq: [first, first + cnt); with M <= 2 the first row is
-    // 0 for sequence 0 and 1 for sequence 1 of a two-sequence batch
     const int row = min(prow0 + e_m, rm.M - 1);
 #pragma unroll
     for (int w = 0; w < 3; ++w) pv[w] = ws.QKV[(size_t)row * nqkv + w * qd + h * HD + e_d];

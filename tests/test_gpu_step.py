@@ -166,3 +166,55 @@ def test_draft_and_verify(name, gamma, exit_layer):
         pair.check_cache(0, pos, pos + j + 1, t, f"round {rnd}")
         pos += j + 1
     assert t.compared > 0
+
+
+@pytest.mark.parametrize("name", CASES)
+def test_batched_dual_step(name):
+    """Three sequences with different context lengths decoded together
+    (two rows each: the batched short-chain attention and the 16-row GEMVs):
+    every sequence's logits, h, p, signal, token and cache entry match the
+    oracle step by step."""
+    cfg = synth.CONFIGS[name]
+    w = synth.make_weights(cfg)
+    B, n_steps = 3, 4
+    lens = [5, 19, 37]
+    pair = Pair(cfg, w, max_ctx=64, table_seed=5, max_batch=B, n_seqs=B)
+    t = Tally()
+    toks = [pair.prefill(list(synth.prompt_ids(cfg, n, stream=f"b{s}")), seq=s, tally=t) for s, n in enumerate(lens)]
+    dev = pair.dev
+    N = cfg.n_layers
+    gates = list(range(1, N))
+    tok_d = torch.tensor(toks, dtype=torch.int32, device=dev)
+    pos_d = torch.tensor(lens, dtype=torch.int32, device=dev)
+    nxt = torch.zeros(B, dtype=torch.int32, device=dev)
+    sig = torch.zeros(B * N, dtype=torch.float32, device=dev)
+    logits = torch.zeros(B * cfg.vocab, dtype=torch.float32, device=dev)
+    h_out = torch.zeros(B * cfg.d_model, dtype=torch.float32, device=dev)
+    p_out = torch.zeros(B * cfg.d_model, dtype=torch.float32, device=dev)
+    live = [True] * B
+    for step in range(n_steps):
+        pair.model.decode_step(tok_d, pos_d, pair.kv.desc(), gates=gates, tau=0.9, mode="observe", next_token=nxt,
+                               signal=sig, logits=logits, h_out=h_out, p_out=p_out, advance=True)
+        torch.cuda.synchronize()
+        L = logits.cpu().numpy().reshape(B, -1)
+        Hh, Pp = h_out.cpu().numpy().reshape(B, -1), p_out.cpu().numpy().reshape(B, -1)
+        S = sig.cpu().numpy().reshape(B, N)
+        got = nxt.cpu().numpy().tolist()
+        for s in range(B):
+            if not live[s]:
+                continue
+            pos = lens[s] + step
+            r = pair.orc.decode_step(int(tok_d[s].item()), pos, pair.caches[s], gates=gates, tau=0.9, mode="observe")
+            if any(abs(r.signal[b - 1] - 0.9) <= pair.tol for b in gates):
+                live[s] = False   # the two sides may take different gate decisions from here
+                t.skipped += 1
+                continue
+            t.rel(L[s], r.logits, pair.tol, f"step {step} seq {s} logits")
+            t.rel(Hh[s], r.h, pair.tol, f"step {step} seq {s} h")
+            t.rel(Pp[s], r.p, pair.tol, f"step {step} seq {s} p")
+            assert np.max(np.abs(S[s] - r.signal)) <= pair.tol, f"step {step} seq {s} signal"
+            t.token(got[s], r.logits, pair.tol, f"step {step} seq {s} token")
+            pair.check_cache(s, pos, pos + 1, t, f"step {step} seq {s}")
+        assert pos_d.cpu().numpy().tolist() == [n + step + 1 for n in lens]
+        tok_d.copy_(nxt)
+    assert t.compared >= 3 * B
