@@ -82,6 +82,27 @@ __device__ __forceinline__ void rw_store_pieces(const RwPieces<PM>& xp, int K, f
   __syncthreads();
 }
 
+// One weight element as raw bits (bf16 in the low half, or fp32), loaded
+// without converting: the epilogue operand groups must not wait for their
+// loads; the epilogue converts with rw_wt().
+template <int WB>
+struct RwRaw {
+  using type = uint16_t;
+};
+template <>
+struct RwRaw<0> {
+  using type = uint32_t;
+};
+template <int WB>
+__device__ __forceinline__ typename RwRaw<WB>::type rw_wt_raw(const void* p, size_t i) {
+  return ((const typename RwRaw<WB>::type*)p)[i];
+}
+template <int WB>
+__device__ __forceinline__ float rw_wt(typename RwRaw<WB>::type bits) {
+  if constexpr (WB) return __uint_as_float((uint32_t)bits << 16);
+  else return __uint_as_float(bits);
+}
+
 // Sum over the 64 lanes of a wave (every lane gets it).
 __device__ __forceinline__ float wave_allsum(float v) {
   v = row_sum16(v);
@@ -90,11 +111,15 @@ __device__ __forceinline__ float wave_allsum(float v) {
 }
 
 // The weight stream of one wave: U rows per unit, each row NS * NCH pieces of
-// 1 KB, read NCH pieces (a sub-unit) at a time; two sub-units are in flight.
-template <int WB, int NCH, int U, int NS>
+// 1 KB, read NCH pieces (a sub-unit) at a time.  Rows of one sub-unit keep P
+// units in flight (a ring of P register buffers); rows of two sub-units keep
+// both halves of one unit and the next unit's first half in flight.
+template <int WB, int NCH, int U, int NS, int PD = 2>
 struct RwStream {
   static constexpr int EPL = WB ? 8 : 4;   // weight elements per lane and piece
-  u32x4_t bA[U][NCH], bB[U][NCH];
+  static constexpr int P = PD;             // register buffers (operand sets)
+  static_assert(NS == 1 || P == 2, "rows of two sub-units use two buffers");
+  u32x4_t bb[P][U][NCH];
 
   // The loads of one sub-unit are issued as a group (nothing is scheduled
   // into or across it): the compiler's in-order wait counts then agree
@@ -113,6 +138,18 @@ struct RwStream {
       for (int c = 0; c < NCH; ++c) dst[u][c] = ld_glob(p[u] + (size_t)c * 1024);
     }
     __builtin_amdgcn_sched_barrier(0);
+  }
+
+  // A unit's epilogue operand loads, issued as a group after the weights
+  // before it (compiler memory barriers keep the optimizer from hoisting
+  // them, whose addresses are known early, above the weight loads).
+  template <class Epi, class F>
+  __device__ __forceinline__ static void fetch_grouped(const Epi&, const F& f) {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    f();
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("" ::: "memory");
   }
 
   // a[u][m] += lane partial dot products of sub-unit `sub` with activation rows m.
@@ -179,22 +216,26 @@ struct RwStream {
   }
 
   // Issue the first weights of the range [u0, u1) and their epilogue
-  // operands, ahead of the activation staging: sub-unit 0 of units u0 and
-  // u0 + 1 (NS == 1) or both sub-units of unit u0 (NS == 2).  Every load is
-  // unconditional (the compiler's wait counts stay exact): a range of one
-  // unit reads its unit twice, an empty range (u0 < n always) reads unit u0.
+  // operands, ahead of the activation staging: sub-unit 0 of unit u0 (the
+  // other buffers are filled when the stream starts: more loads before the
+  // staging delay the staging's own, and its barriers wait for every wave).  Every load is unconditional (the
+  // compiler's wait counts stay exact): units past the range read the
+  // range's last unit again, an empty range (u0 < n always) reads unit u0.
+  static constexpr int kBegin = 1;
   template <class PF, class Epi>
   __device__ __forceinline__ void begin(const PF& row_ptr, int u0, int u1, const Epi& epi,
-                                        typename Epi::Ops& oA, typename Epi::Ops& oB) {
-    const int ub = min(u0 + 1, max(u1 - 1, u0));
-    load(row_ptr, u0, 0, bA);
-    epi.fetch(u0, oA);
+                                        typename Epi::Ops (&ops)[P]) {
+    const int last = max(u1 - 1, u0);
     if constexpr (NS == 1) {
-      load(row_ptr, ub, 0, bB);
-      epi.fetch(ub, oB);
+#pragma unroll
+      for (int i = 0; i < kBegin; ++i) {
+        load(row_ptr, min(u0 + i, last), 0, bb[i]);
+        fetch_grouped(epi, [&] { epi.fetch(min(u0 + i, last), ops[i]); });
+      }
     } else {
       static_assert(NS == 2, "one or two sub-units per unit");
-      load(row_ptr, u0, 1, bB);
+      load(row_ptr, u0, 0, bb[0]);
+      fetch_grouped(epi, [&] { epi.fetch(u0, ops[0]); });
     }
   }
 
@@ -205,89 +246,88 @@ struct RwStream {
   // range is read.
   template <class PF, class Epi>
   __device__ __forceinline__ void run(const PF& row_ptr, int u0, int u1, const float* act, int K, Epi& epi,
-                                      typename Epi::Ops& oA, typename Epi::Ops& oB) {
+                                      typename Epi::Ops (&ops)[P]) {
     if (u0 >= u1) return;
     float y[U][2];
     int u = u0;
     if constexpr (NS == 1) {
-      // bA holds unit u, bB unit u + 1; each unit's successor-but-one is
-      // loaded into its buffer as soon as its dot products are done
-      for (; u + 3 < u1; u += 2) {
-        zero(y);
-        dot(bA, act, K, 0, y);
-        load(row_ptr, u + 2, 0, bA);
-        finish(y);
-        epi.run(u, y, oA);
-        epi.fetch(u + 2, oA);
-        zero(y);
-        dot(bB, act, K, 0, y);
-        load(row_ptr, u + 3, 0, bB);
-        finish(y);
-        epi.run(u + 1, y, oB);
-        epi.fetch(u + 3, oB);
+      {
+        const int last = u1 - 1;
+#pragma unroll
+        for (int i = kBegin; i < P; ++i) {
+          load(row_ptr, min(u0 + i, last), 0, bb[i]);
+          fetch_grouped(epi, [&] { epi.fetch(min(u0 + i, last), ops[i]); });
+        }
       }
-      // the last one to three units: the loads here are conditional (what
-      // they bring is needed next anyway), and no two branches start with
-      // the same code (which the compiler would hoist above the branch,
+      // buffer i holds unit u + i; a unit's buffer is refilled with the unit
+      // P further on as soon as its dot products are done
+      for (; u + 2 * P - 1 < u1; u += P) {
+#pragma unroll
+        for (int i = 0; i < P; ++i) {
+          zero(y);
+          dot(bb[i], act, K, 0, y);
+          load(row_ptr, u + i + P, 0, bb[i]);
+          finish(y);
+          epi.run(u + i, y, ops[i]);
+          fetch_grouped(epi, [&] { epi.fetch(u + i + P, ops[i]); });
+        }
+      }
+      // the last 1 .. 2P-1 units: refills are conditional here (what they
+      // bring is needed next anyway); the blocks have no else branches (the
+      // compiler would hoist a common prefix of two branches above them,
       // converting every weight of the unit at once)
       const int left = u1 - u;
-      zero(y);
-      dot(bA, act, K, 0, y);
-      if (left == 3) load(row_ptr, u + 2, 0, bA);
-      finish(y);
-      epi.run(u, y, oA);
-      if (left == 3) epi.fetch(u + 2, oA);
-      if (left >= 2) {
-        zero(y);
-        dot(bB, act, K, 0, y);
-        finish(y);
-        epi.run(u + 1, y, oB);
-      }
-      if (left == 3) {
-        zero(y);
-        dot(bA, act, K, 0, y);
-        finish(y);
-        epi.run(u + 2, y, oA);
+#pragma unroll
+      for (int i = 0; i < 2 * P - 1; ++i) {
+        if (i < left) {
+          zero(y);
+          dot(bb[i % P], act, K, 0, y);
+          if (i + P < left) load(row_ptr, u + i + P, 0, bb[i % P]);
+          finish(y);
+          epi.run(u + i, y, ops[i % P]);
+          if (i + P < left) epi.fetch(u + i + P, ops[i % P]);
+        }
       }
     } else {
-      // unit u in bA (sub-unit 0) and bB (sub-unit 1), its operands in oA;
+      load(row_ptr, u0, 1, bb[1]);   // the second half of the first unit
+      // unit u in bb[0] (sub-unit 0) and bb[1] (sub-unit 1), its operands in ops[0];
       // two units per iteration so the operand buffers alternate in place
       for (; u + 2 < u1; u += 2) {
         zero(y);
-        dot(bA, act, K, 0, y);
-        load(row_ptr, u + 1, 0, bA);
-        epi.fetch(u + 1, oB);
-        dot(bB, act, K, 1, y);
-        load(row_ptr, u + 1, 1, bB);
+        dot(bb[0], act, K, 0, y);
+        load(row_ptr, u + 1, 0, bb[0]);
+        fetch_grouped(epi, [&] { epi.fetch(u + 1, ops[1]); });
+        dot(bb[1], act, K, 1, y);
+        load(row_ptr, u + 1, 1, bb[1]);
         finish(y);
-        epi.run(u, y, oA);
+        epi.run(u, y, ops[0]);
         zero(y);
-        dot(bA, act, K, 0, y);
-        load(row_ptr, u + 2, 0, bA);
-        epi.fetch(u + 2, oA);
-        dot(bB, act, K, 1, y);
-        load(row_ptr, u + 2, 1, bB);
+        dot(bb[0], act, K, 0, y);
+        load(row_ptr, u + 2, 0, bb[0]);
+        fetch_grouped(epi, [&] { epi.fetch(u + 2, ops[0]); });
+        dot(bb[1], act, K, 1, y);
+        load(row_ptr, u + 2, 1, bb[1]);
         finish(y);
-        epi.run(u + 1, y, oB);
+        epi.run(u + 1, y, ops[1]);
       }
       // the last one or two units (conditional loads, no common branch prefix)
       const bool two = u + 1 < u1;
       zero(y);
-      dot(bA, act, K, 0, y);
+      dot(bb[0], act, K, 0, y);
       if (two) {
-        load(row_ptr, u + 1, 0, bA);
-        epi.fetch(u + 1, oB);
+        load(row_ptr, u + 1, 0, bb[0]);
+        fetch_grouped(epi, [&] { epi.fetch(u + 1, ops[1]); });
       }
-      dot(bB, act, K, 1, y);
-      if (two) load(row_ptr, u + 1, 1, bB);
+      dot(bb[1], act, K, 1, y);
+      if (two) load(row_ptr, u + 1, 1, bb[1]);
       finish(y);
-      epi.run(u, y, oA);
+      epi.run(u, y, ops[0]);
       if (two) {
         zero(y);
-        dot(bA, act, K, 0, y);
-        dot(bB, act, K, 1, y);
+        dot(bb[0], act, K, 0, y);
+        dot(bb[1], act, K, 1, y);
         finish(y);
-        epi.run(u + 1, y, oB);
+        epi.run(u + 1, y, ops[1]);
       }
     }
   }
@@ -398,9 +438,9 @@ __global__ __launch_bounds__(kRwThreads) void kr_qkv(Dims D, LayerPtrs L, RowMap
       }
     }
   } epi{&rml, src_s, inv_rms, ws.QKV, nqkv, qd, r, Ap};
-  typename Epi::Ops oA, oB;
+  typename Epi::Ops ops[decltype(st)::P];
   __builtin_amdgcn_sched_barrier(0);
-  st.begin(row_ptr, u0, u1, epi, oA, oB);
+  st.begin(row_ptr, u0, u1, epi, ops);
   __builtin_amdgcn_sched_barrier(0);
   if (tid < rm.nseq) { ex_in[tid] = exv; eb_in[tid] = ebv; }
   sk_rm_copy(rmu, rm);
@@ -424,7 +464,7 @@ __global__ __launch_bounds__(kRwThreads) void kr_qkv(Dims D, LayerPtrs L, RowMap
     if (layer > 0) ws.sig[tid * D.n_layers + layer - 1] = sig_s[tid];
   }
   rw_store_pieces<true>(xp, D.d, actf);
-  st.run(row_ptr, u0, u1, actf, D.d, epi, oA, oB);
+  st.run(row_ptr, u0, u1, actf, D.d, epi, ops);
 }
 
 // ============================================================================
@@ -460,7 +500,7 @@ __global__ __launch_bounds__(kRwThreads) void kr_oproj(Dims D, LayerPtrs L, RowM
   struct Epi {
     struct Ops {
       float x0, x1, g;
-      float a;   // A_g[c][n] (c < r) or A_u[c - r][n] of this lane's c
+      typename RwRaw<WB>::type a;   // A_g[c][n] (c < r) or A_u[c - r][n] of this lane's c (raw bits)
       RwBRow<WB> b;
     };
     const Dims* D;
@@ -480,7 +520,7 @@ __global__ __launch_bounds__(kRwThreads) void kr_oproj(Dims D, LayerPtrs L, RowM
       o.g = L->mlp_norm[n];
       const int c = lane % (2 * r);
       const void* A = c < r ? L->A[4] : L->A[5];
-      o.a = ld_wt<WB>(A ? A : (const void*)L->mlp_norm, A ? (size_t)(c % r) * D->d + n : 0);
+      o.a = rw_wt_raw<WB>(A ? A : (const void*)L->mlp_norm, A ? (size_t)(c % r) * D->d + n : 0);
       o.b.load(has_o ? L->B[3] : (const void*)L->mlp_norm, has_o ? n : 0, r);
     }
     __device__ void run(int n, const float (&y)[1][2], const Ops& o) {
@@ -510,14 +550,14 @@ __global__ __launch_bounds__(kRwThreads) void kr_oproj(Dims D, LayerPtrs L, RowM
         xnew[m] = xn;
       }
       accx += lane == 0 ? xnew[0] * xnew[0] : (lane == 1 ? xnew[1] * xnew[1] : 0.f);
-      const float ga = o.a * o.g;
+      const float ga = rw_wt<WB>(o.a) * o.g;
       if (rm->fast[0]) acc0 += ga * xnew[0];
       if (rm->M > 1 && rm->fast[1]) acc1 += ga * xnew[1];
     }
   } epi{&D, &L, &rml, flag_s, uo_s, ws, layer, has_o, 0.f, 0.f, 0.f};
-  typename Epi::Ops oA, oB;
+  typename Epi::Ops ops[decltype(st)::P];
   __builtin_amdgcn_sched_barrier(0);
-  st.begin(row_ptr, u0, u1, epi, oA, oB);
+  st.begin(row_ptr, u0, u1, epi, ops);
   __builtin_amdgcn_sched_barrier(0);
   sk_rm_copy(rmu, rm);
   if (tid < kMaxSeq) { flag_s[tid] = fe; flag_s[kMaxSeq + tid] = fr; }
@@ -536,7 +576,7 @@ __global__ __launch_bounds__(kRwThreads) void kr_oproj(Dims D, LayerPtrs L, RowM
     uo_s[tid] = a;
   }
   rw_store_pieces<false>(xp, D.qdim, actf);
-  st.run(row_ptr, u0, u1, actf, D.qdim, epi, oA, oB);
+  st.run(row_ptr, u0, u1, actf, D.qdim, epi, ops);
   const int bin = blockIdx.x % kBinSlots;
   rw_wg_sum(epi.accx, 2, wsum, tot);
   if (tid < rm.M) add_agent(bin_o_at(ws, D, layer, bin, tid), tot[tid]);
@@ -577,7 +617,7 @@ __global__ __launch_bounds__(kRwThreads) void kr_gateup(Dims D, LayerPtrs L, Row
   rw_load_pieces<true>(ws.X, ws.X + (size_t)(rm.M > 1 ? 1 : 0) * D.d, L.mlp_norm, D.d, xp);
   struct Epi {
     struct Ops {
-      float a;   // A_d[lane % r][j]
+      typename RwRaw<WB>::type a;   // A_d[lane % r][j] (raw bits)
       RwBRow<WB> bg, bu;
     };
     const Dims* D;
@@ -592,7 +632,7 @@ __global__ __launch_bounds__(kRwThreads) void kr_gateup(Dims D, LayerPtrs L, Row
     __device__ void fetch(int h, Ops& o) const {
       const int lane = threadIdx.x & 63, r = D->r, j = h >> 1;
       const void* fb = (const void*)L->mlp_norm;   // stand-in for missing factors (loads stay unconditional)
-      o.a = ld_wt<WB>(L->A[6] ? L->A[6] : fb, L->A[6] ? (size_t)(lane % r) * D->F + j : 0);
+      o.a = rw_wt_raw<WB>(L->A[6] ? L->A[6] : fb, L->A[6] ? (size_t)(lane % r) * D->F + j : 0);
       o.bg.load(hg ? L->B[4] : fb, hg ? j : 0, r);
       o.bu.load(hu ? L->B[5] : fb, hu ? j : 0, r);
     }
@@ -616,19 +656,20 @@ __global__ __launch_bounds__(kRwThreads) void kr_gateup(Dims D, LayerPtrs L, Row
         av[m] = silu(g) * u;
         if (lane == m) ws.ACT[(size_t)m * D->F + j] = av[m];
       }
-      if (rm->fast[0]) acc0 += o.a * av[0];
-      if (rm->M > 1 && rm->fast[1]) acc1 += o.a * av[1];
+      const float aw = rw_wt<WB>(o.a);
+      if (rm->fast[0]) acc0 += aw * av[0];
+      if (rm->M > 1 && rm->fast[1]) acc1 += aw * av[1];
     }
   } epi{&D, &L, &rml, stat, inv_rms, ws, L.A[4] && L.B[4], L.A[5] && L.B[5], 0.f, 0.f, 0.f, 0.f};
-  typename Epi::Ops oA, oB;
+  typename Epi::Ops ops[decltype(st)::P];
   __builtin_amdgcn_sched_barrier(0);
-  st.begin(row_ptr, u0, u1, epi, oA, oB);
+  st.begin(row_ptr, u0, u1, epi, ops);
   __builtin_amdgcn_sched_barrier(0);
   sk_rm_copy(rmu, rm);
   sk_bins_sum(rm.M * PO, sv, actf, stat);
   if (tid < 2) inv_rms[tid] = rsqrtf(stat[min(tid, rm.M - 1) * PO] / D.d + D.eps);
   rw_store_pieces<true>(xp, D.d, actf);
-  st.run(row_ptr, u0, u1, actf, D.d, epi, oA, oB);
+  st.run(row_ptr, u0, u1, actf, D.d, epi, ops);
   for (int m = 0; m < 2; ++m) {
     rw_wg_sum(m ? epi.acc1 : epi.acc0, r, wsum, tot);
     if (tid < r && L.A[6] && m < rm.M && rml.fast[m])
@@ -708,15 +749,15 @@ __global__ __launch_bounds__(kRwThreads) void kr_down(Dims D, LayerPtrs L, RowMa
       }
     }
   } epi{&D, &L, &rml, ud, ex_s, ws, L.A[6] && L.B[6], 0.f};
-  typename Epi::Ops oA, oB;
+  typename Epi::Ops ops[decltype(st)::P];
   __builtin_amdgcn_sched_barrier(0);
-  st.begin(row_ptr, u0, u1, epi, oA, oB);
+  st.begin(row_ptr, u0, u1, epi, ops);
   __builtin_amdgcn_sched_barrier(0);
   sk_rm_copy(rmu, rm);
   if (tid < kMaxSeq) ex_s[tid] = exv;
   sk_bins_sum(rm.M * r, uv, actf, ud);
   rw_store_pieces<false>(xp, D.F, actf);
-  st.run(row_ptr, u0, u1, actf, D.F, epi, oA, oB);
+  st.run(row_ptr, u0, u1, actf, D.F, epi, ops);
   rw_wg_sum(epi.acc, 6, wsum, tot);
   if (tid < 2 * 3 && tid / 3 < rm.M) add_agent(bin_d_at(ws, layer + 1, blockIdx.x % kBinSlots, tid / 3) + tid % 3, tot[tid]);
 }
@@ -771,9 +812,9 @@ __global__ __launch_bounds__(kRwThreads) void kr_head(Dims D, const void* lm_hea
       }
     }
   } epi{&D, hrow, inv_rms, io.logits_out, 0, {-INFINITY, -INFINITY}, {0x7fffffff, 0x7fffffff}};
-  typename Epi::Ops oA, oB;
+  typename Epi::Ops ops[decltype(st)::P];
   __builtin_amdgcn_sched_barrier(0);
-  st.begin(row_ptr, u0, u1, epi, oA, oB);
+  st.begin(row_ptr, u0, u1, epi, ops);
   __builtin_amdgcn_sched_barrier(0);
   if (tid < rm.nseq) ex_in[tid] = exv;
   sk_rm_copy(rmu, rm);
@@ -801,7 +842,7 @@ __global__ __launch_bounds__(kRwThreads) void kr_head(Dims D, const void* lm_hea
   // head row k reads activation row hrow[k] (the staged rows are X[0] and X[1])
   rw_store_pieces<true>(xp, D.d, actf);
   epi.nh = nh;
-  st.run(row_ptr, u0, u1, actf, D.d, epi, oA, oB);
+  st.run(row_ptr, u0, u1, actf, D.d, epi, ops);
   if (lane == 0) {
     bz_s[wv][0] = epi.bz[0]; bz_s[wv][1] = epi.bz[1];
     bi_s[wv][0] = epi.bi[0]; bi_s[wv][1] = epi.bi[1];
