@@ -293,6 +293,7 @@ struct m2r2_ctx {
   int sk_attn_S = 0;   // splits of the stream-K path's attention (0: the general attention kernel)
   bool rw_on = false;  // row-per-wave GEMVs for the one- and two-row class
   int rw_nch[3] = {0, 0, 0};   // 1 KB pieces per row for reductions over d, qdim, ffn
+  int rw_nw[2] = {8, 8};       // waves per workgroup of the o and down projections
   SkPlan sk[5];
   SkWS skws{};
   int timed_class = -1;
@@ -391,10 +392,29 @@ bool rw_nch_ok(int n) {
     }                                                                                                 \
   }
 M2R2_RW_LAUNCHER(kr_qkv)
-M2R2_RW_LAUNCHER(kr_oproj)
 M2R2_RW_LAUNCHER(kr_gateup)
-M2R2_RW_LAUNCHER(kr_down)
 M2R2_RW_LAUNCHER(kr_head)
+// o projection and down projection: 8 or 12 waves per workgroup (12 when the
+// rows then split evenly over the waves, as d = 3072 over 256 x 12 does)
+#define M2R2_RW_LAUNCHER_NW(NAME)                                                                      \
+  template <int WB, int NW, class... A>                                                               \
+  void NAME##_launch_w(int nch, int grid, size_t lds, hipStream_t st, A... args) {                    \
+    switch (nch) {                                                                                    \
+      case 1: NAME<WB, 1, 1, NW><<<grid, 64 * NW, lds, st>>>(args...); break;                         \
+      case 2: NAME<WB, 2, 1, NW><<<grid, 64 * NW, lds, st>>>(args...); break;                         \
+      case 4: NAME<WB, 4, 1, NW><<<grid, 64 * NW, lds, st>>>(args...); break;                         \
+      case 6: NAME<WB, 6, 1, NW><<<grid, 64 * NW, lds, st>>>(args...); break;                         \
+      case 8: NAME<WB, 8, 1, NW><<<grid, 64 * NW, lds, st>>>(args...); break;                         \
+      case 16: NAME<WB, 8, 2, NW><<<grid, 64 * NW, lds, st>>>(args...); break;                        \
+    }                                                                                                 \
+  }                                                                                                   \
+  template <int WB, class... A>                                                                       \
+  void NAME##_launch(int nch, int nw, int grid, size_t lds, hipStream_t st, A... args) {              \
+    if (nw == 12) NAME##_launch_w<WB, 12>(nch, grid, lds, st, args...);                               \
+    else NAME##_launch_w<WB, 8>(nch, grid, lds, st, args...);                                         \
+  }
+M2R2_RW_LAUNCHER_NW(kr_oproj)
+M2R2_RW_LAUNCHER_NW(kr_down)
 
 // One or two rows: row-per-wave GEMVs and the short-chain attention.
 template <int WB, int KB, int HD>
@@ -409,9 +429,9 @@ m2r2_status run_layers_rw(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const
     TIMED(0, (kr_qkv_launch<WB>(nd, G, lds, st, D, L, rm, c->ws, io, l)));
     TIMED(1, (ks_attn<WB, KB, HD><<<dim3(c->sk_attn_S, D.H, rm.nseq), kSkAttnThreads, sk_attn_lds_bytes(HD, D.r, WB),
                                     st>>>(D, L, rm, c->ws, io, kv, l, c->sk_attn_S)));
-    TIMED(2, (kr_oproj_launch<WB>(nq, G, lds, st, D, L, rm, c->ws, io, l)));
+    TIMED(2, (kr_oproj_launch<WB>(nq, c->rw_nw[0], G, lds, st, D, L, rm, c->ws, io, l)));
     TIMED(3, (kr_gateup_launch<WB>(nd, G, lds, st, D, L, rm, c->ws, io, l)));
-    TIMED(4, (kr_down_launch<WB>(nf, G, lds, st, D, L, rm, c->ws, io, l)));
+    TIMED(4, (kr_down_launch<WB>(nf, c->rw_nw[1], G, lds, st, D, L, rm, c->ws, io, l)));
   }
   TIMED(5, (kr_head_launch<WB>(nd, G, lds, st, D, c->lm_head_rm, c->final_norm, rm, c->ws, io, kv, c->skws,
                                 n_layers_run)));
@@ -595,6 +615,12 @@ hipError_t rw_set_lds(int bytes) {
     if (e == hipSuccess) e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
   M2R2_RW_ATTR(1, 1) M2R2_RW_ATTR(2, 1) M2R2_RW_ATTR(4, 1) M2R2_RW_ATTR(6, 1) M2R2_RW_ATTR(8, 1) M2R2_RW_ATTR(8, 2)
 #undef M2R2_RW_ATTR
+#define M2R2_RW_ATTR12(N, S)                                                                                  \
+  for (const void* f : {(const void*)kr_oproj<WB, N, S, 12>, (const void*)kr_down<WB, N, S, 12>})              \
+    if (e == hipSuccess) e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  M2R2_RW_ATTR12(1, 1) M2R2_RW_ATTR12(2, 1) M2R2_RW_ATTR12(4, 1) M2R2_RW_ATTR12(6, 1) M2R2_RW_ATTR12(8, 1)
+  M2R2_RW_ATTR12(8, 2)
+#undef M2R2_RW_ATTR12
   return e;
 }
 
@@ -652,7 +678,18 @@ hipError_t sk_setup(m2r2_ctx* c) {
     }
     // the waves split their units with 32-bit products unit * wave count
     const long long nmax = std::max<long long>({3LL * D.qdim + 3LL * D.r, D.d, D.F, D.V});
-    ok_r = ok_r && nmax * cus * kRwWaves < (1LL << 32);
+    ok_r = ok_r && nmax * cus * 12 < (1LL << 32);
+    // o and down projections (D.d output rows each): 12 waves per workgroup
+    // when that puts the same number of rows on every wave and the rows are
+    // long (at least 8 KB; for short rows the extra waves' staging costs
+    // more than the uneven split: measured)
+    auto eff = [&](int nw) {
+      const double avg = (double)D.d / ((double)cus * nw);
+      return avg / std::ceil(avg);
+    };
+    const bool even12 = eff(12) > eff(8) + 1e-9;
+    c->rw_nw[0] = even12 && (size_t)D.qdim * wsz >= 8192 ? 12 : 8;
+    c->rw_nw[1] = even12 && (size_t)D.F * wsz >= 8192 ? 12 : 8;
     if (ok_r) e = D.wbf16 ? rw_set_lds<1>(kSkMinLds) : rw_set_lds<0>(kSkMinLds);
     c->rw_on = ok_r && e == hipSuccess;
   }

@@ -25,10 +25,10 @@ constexpr int kRwThreads = 64 * kRwWaves;
 
 // Activation pieces (4 floats) per thread for a reduction of NS * NCH pieces
 // of 1 KB per row.
-template <int WB, int NCH, int NS>
+template <int WB, int NCH, int NS, int T = kRwThreads>
 struct RwPM {
   static constexpr int K = NS * NCH * 64 * (WB ? 8 : 4);
-  static constexpr int value = (K / 4 + kRwThreads - 1) / kRwThreads;
+  static constexpr int value = (K / 4 + T - 1) / T;
 };
 
 // Units [u0, u1) of wave gw of W for n units (n * W < 2^32, checked by the
@@ -47,27 +47,28 @@ struct RwPieces {
   float4 g[PM];
 };
 // float4 index of piece p of this thread (pieces past the row repeat the last)
-__device__ __forceinline__ int rw_piece_q(int p, int nq) { return min((int)threadIdx.x + kRwThreads * p, nq - 1); }
-template <bool G, int PM>
+template <int T>
+__device__ __forceinline__ int rw_piece_q(int p, int nq) { return min((int)threadIdx.x + T * p, nq - 1); }
+template <bool G, int PM, int T = kRwThreads>
 __device__ __forceinline__ void rw_load_pieces(const float* r0, const float* r1, const float* gain, int K,
                                                RwPieces<PM>& xp) {
   const int nq = K / 4;
 #pragma unroll
   for (int p = 0; p < PM; ++p) {
-    const int q = rw_piece_q(p, nq);
+    const int q = rw_piece_q<T>(p, nq);
     xp.v[p][0] = ldg4(r0 + 4 * q);
     xp.v[p][1] = ldg4(r1 + 4 * q);
     if constexpr (G) xp.g[p] = ldg4(gain + 4 * q);
   }
 }
 // Ends with a workgroup barrier.
-template <bool G, int PM>
+template <bool G, int PM, int T = kRwThreads>
 __device__ __forceinline__ void rw_store_pieces(const RwPieces<PM>& xp, int K, float* act) {
   const int nq = K / 4;
 #pragma unroll
   for (int p = 0; p < PM; ++p) {
-    if ((int)threadIdx.x + kRwThreads * p < nq) {
-      const int q = rw_piece_q(p, nq);
+    if ((int)threadIdx.x + T * p < nq) {
+      const int q = rw_piece_q<T>(p, nq);
 #pragma unroll
       for (int m = 0; m < 2; ++m) {
         float4 v = xp.v[p][m];
@@ -333,8 +334,9 @@ struct RwStream {
   }
 };
 
-// Workgroup sum of per-wave values v[0..n) (n <= 64, lane i of each wave
-// holds value i) into out[0..n) (LDS); scratch holds kRwWaves * 64 floats.
+// Workgroup sum of per-wave values v[0..n) (n <= 64, lane i of each of the
+// NW waves holds value i) into out[0..n) (LDS); scratch holds NW * 64 floats.
+template <int NW = kRwWaves>
 __device__ __forceinline__ void rw_wg_sum(float v, int n, float* scratch, float* out) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   scratch[wv * 64 + lane] = v;
@@ -342,7 +344,7 @@ __device__ __forceinline__ void rw_wg_sum(float v, int n, float* scratch, float*
   if ((int)threadIdx.x < n) {
     float a = 0.f;
 #pragma unroll
-    for (int w = 0; w < kRwWaves; ++w) a += scratch[w * 64 + threadIdx.x];
+    for (int w = 0; w < NW; ++w) a += scratch[w * 64 + threadIdx.x];
     out[threadIdx.x] = a;
   }
   __syncthreads();
@@ -471,27 +473,27 @@ __global__ __launch_bounds__(kRwThreads) void kr_qkv(Dims D, LayerPtrs L, RowMap
 // Output projection + residual (+ adapter on fast rows); partial sums for the
 // gate/up prologue (sum x^2, adapter-down of gate and up).
 // ============================================================================
-template <int WB, int NCH, int NS>
-__global__ __launch_bounds__(kRwThreads) void kr_oproj(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int layer) {
+template <int WB, int NCH, int NS, int NW = kRwWaves>
+__global__ __launch_bounds__(64 * NW) void kr_oproj(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int layer) {
   extern __shared__ __attribute__((aligned(16))) float actf[];
-  __shared__ float ud_s[2 * kRwThreads];
+  __shared__ float ud_s[2 * (64 * NW)];
   __shared__ float uo_s[2 * kMaxRank];
-  __shared__ float wsum[kRwWaves * 64];
+  __shared__ float wsum[NW * 64];
   __shared__ float tot[64];
   __shared__ int flag_s[2 * kMaxSeq];   // exited, reinit per sequence
   __shared__ SkRmLds rmu;
   const RowMap& rml = rmu.rm;
-  const int tid = threadIdx.x, lane = tid & 63, gw = blockIdx.x * kRwWaves + __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int tid = threadIdx.x, lane = tid & 63, gw = blockIdx.x * NW + __builtin_amdgcn_readfirstlane(tid >> 6);
   if (io.mode == EX_EXIT && sk_all_exited(rm, ws)) return;
   const int esz = WB ? 2 : 4, r = D.r, HR = D.H * D.r;
   auto row_ptr = [&](int u, int) -> const void* { return (const char*)L.wo + (size_t)u * D.qdim * esz; };
   int u0, u1;
-  rw_range(D.d, gridDim.x * kRwWaves, gw, u0, u1);
+  rw_range(D.d, gridDim.x * NW, gw, u0, u1);
   RwStream<WB, NCH, 1, NS> st;
-  RwPieces<RwPM<WB, NCH, NS>::value> xp;
-  rw_load_pieces<false>(ws.O, ws.O + (size_t)(rm.M > 1 ? 1 : 0) * D.qdim, nullptr, D.qdim, xp);
+  RwPieces<RwPM<WB, NCH, NS, 64 * NW>::value> xp;
+  rw_load_pieces<false, RwPM<WB, NCH, NS, 64 * NW>::value, 64 * NW>(ws.O, ws.O + (size_t)(rm.M > 1 ? 1 : 0) * D.qdim, nullptr, D.qdim, xp);
   const float uv0 = ws.uo[min(tid, 2 * HR - 1)];
-  const float uv1 = ws.uo[min(tid + kRwThreads, 2 * HR - 1)];
+  const float uv1 = ws.uo[min(tid + (64 * NW), 2 * HR - 1)];
   const int fe = ws.exited[min(tid, kMaxSeq - 1)];
   const int fr = ws.reinit[layer * kMaxSeq + min(tid, kMaxSeq - 1)];
   const bool has_o = L.A[3] && L.B[3];
@@ -562,12 +564,12 @@ __global__ __launch_bounds__(kRwThreads) void kr_oproj(Dims D, LayerPtrs L, RowM
   sk_rm_copy(rmu, rm);
   if (tid < kMaxSeq) { flag_s[tid] = fe; flag_s[kMaxSeq + tid] = fr; }
   ud_s[tid] = uv0;
-  ud_s[tid + kRwThreads] = uv1;
+  ud_s[tid + (64 * NW)] = uv1;
   __syncthreads();
   if (tid < 2 * r) {
     const int m = tid / r, j = tid % r;
     float a = 0.f;
-    if (has_o && m < rm.M && rml.fast[m] && 2 * HR <= 2 * kRwThreads) {
+    if (has_o && m < rm.M && rml.fast[m] && 2 * HR <= 2 * (64 * NW)) {
 #pragma unroll 8
       for (int h = 0; h < D.H; ++h) a += ud_s[(m * D.H + h) * r + j];
     } else if (has_o && m < rm.M && rml.fast[m]) {
@@ -575,13 +577,13 @@ __global__ __launch_bounds__(kRwThreads) void kr_oproj(Dims D, LayerPtrs L, RowM
     }
     uo_s[tid] = a;
   }
-  rw_store_pieces<false>(xp, D.qdim, actf);
+  rw_store_pieces<false, RwPM<WB, NCH, NS, 64 * NW>::value, 64 * NW>(xp, D.qdim, actf);
   st.run(row_ptr, u0, u1, actf, D.qdim, epi, ops);
   const int bin = blockIdx.x % kBinSlots;
-  rw_wg_sum(epi.accx, 2, wsum, tot);
+  rw_wg_sum<NW>(epi.accx, 2, wsum, tot);
   if (tid < rm.M) add_agent(bin_o_at(ws, D, layer, bin, tid), tot[tid]);
   for (int m = 0; m < 2; ++m) {
-    rw_wg_sum(m ? epi.acc1 : epi.acc0, 2 * r, wsum, tot);
+    rw_wg_sum<NW>(m ? epi.acc1 : epi.acc0, 2 * r, wsum, tot);
     if (tid < 2 * r && m < rm.M && rml.fast[m] && (tid < r ? L.A[4] : L.A[5]))
       add_agent(bin_o_at(ws, D, layer, bin, m) + 1 + tid, tot[tid]);
   }
@@ -681,16 +683,16 @@ __global__ __launch_bounds__(kRwThreads) void kr_gateup(Dims D, LayerPtrs L, Row
 // Down projection + residual (+ adapter); partial sums for the next layer's
 // norm and the exit signal.
 // ============================================================================
-template <int WB, int NCH, int NS>
-__global__ __launch_bounds__(kRwThreads) void kr_down(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int layer) {
+template <int WB, int NCH, int NS, int NW = kRwWaves>
+__global__ __launch_bounds__(64 * NW) void kr_down(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int layer) {
   extern __shared__ __attribute__((aligned(16))) float actf[];
   __shared__ float ud[2 * kMaxRank];
-  __shared__ float wsum[kRwWaves * 64];
+  __shared__ float wsum[NW * 64];
   __shared__ float tot[64];
   __shared__ int ex_s[kMaxSeq];
   __shared__ SkRmLds rmu;
   const RowMap& rml = rmu.rm;
-  const int tid = threadIdx.x, gw = blockIdx.x * kRwWaves + __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int tid = threadIdx.x, gw = blockIdx.x * NW + __builtin_amdgcn_readfirstlane(tid >> 6);
   if (io.mode == EX_EXIT && sk_all_exited(rm, ws)) {
     if (blockIdx.x == 0) rows_unchanged_stats(D, rm, ws, layer + 1);
     return;
@@ -698,12 +700,12 @@ __global__ __launch_bounds__(kRwThreads) void kr_down(Dims D, LayerPtrs L, RowMa
   const int esz = WB ? 2 : 4, r = D.r;
   auto row_ptr = [&](int u, int) -> const void* { return (const char*)L.wd + (size_t)u * D.F * esz; };
   int u0, u1;
-  rw_range(D.d, gridDim.x * kRwWaves, gw, u0, u1);
+  rw_range(D.d, gridDim.x * NW, gw, u0, u1);
   RwStream<WB, NCH, 1, NS> st;
-  float uv[(2 * kMaxRank * kBinSlots + kSkThreads - 1) / kSkThreads];
-  sk_bins_load(rm.M * r, bin_gu_at(ws, D, layer, 0, 0), kMaxRows * r, uv);
-  RwPieces<RwPM<WB, NCH, NS>::value> xp;
-  rw_load_pieces<false>(ws.ACT, ws.ACT + (size_t)(rm.M > 1 ? 1 : 0) * D.F, nullptr, D.F, xp);
+  float uv[(2 * kMaxRank * kBinSlots + 64 * NW - 1) / (64 * NW)];
+  sk_bins_load<64 * NW>(rm.M * r, bin_gu_at(ws, D, layer, 0, 0), kMaxRows * r, uv);
+  RwPieces<RwPM<WB, NCH, NS, 64 * NW>::value> xp;
+  rw_load_pieces<false, RwPM<WB, NCH, NS, 64 * NW>::value, 64 * NW>(ws.ACT, ws.ACT + (size_t)(rm.M > 1 ? 1 : 0) * D.F, nullptr, D.F, xp);
   const int exv = ws.exited[min(tid, kMaxSeq - 1)];
   struct Epi {
     struct Ops {
@@ -755,10 +757,10 @@ __global__ __launch_bounds__(kRwThreads) void kr_down(Dims D, LayerPtrs L, RowMa
   __builtin_amdgcn_sched_barrier(0);
   sk_rm_copy(rmu, rm);
   if (tid < kMaxSeq) ex_s[tid] = exv;
-  sk_bins_sum(rm.M * r, uv, actf, ud);
-  rw_store_pieces<false>(xp, D.F, actf);
+  sk_bins_sum<64 * NW>(rm.M * r, uv, actf, ud);
+  rw_store_pieces<false, RwPM<WB, NCH, NS, 64 * NW>::value, 64 * NW>(xp, D.F, actf);
   st.run(row_ptr, u0, u1, actf, D.F, epi, ops);
-  rw_wg_sum(epi.acc, 6, wsum, tot);
+  rw_wg_sum<NW>(epi.acc, 6, wsum, tot);
   if (tid < 2 * 3 && tid / 3 < rm.M) add_agent(bin_d_at(ws, layer + 1, blockIdx.x % kBinSlots, tid / 3) + tid % 3, tot[tid]);
 }
 

@@ -162,12 +162,12 @@ __device__ __forceinline__ void sk_store_pieces(const SkPieces& xp, const float*
 // bin; sk_bins_sum adds them in bin order (results do not depend on timing)
 // through the LDS scratch (nv * kBinSlots floats) into out[nv].
 // ---------------------------------------------------------------------------
-template <int NPT>
+template <int T = kSkThreads, int NPT>
 __device__ __forceinline__ void sk_bins_load(int nv, const float* base, int stride, float (&v)[NPT]) {
-  // element i = threadIdx.x + kSkThreads * k as (bin b, value q), stepped
+  // element i = threadIdx.x + T * k (T threads) as (bin b, value q), stepped
   // without a division per element
   int b = (int)threadIdx.x / nv, q = (int)threadIdx.x - b * nv;
-  const int db = kSkThreads / nv, dq = kSkThreads - db * nv;
+  const int db = T / nv, dq = T - db * nv;
 #pragma unroll
   for (int k = 0; k < NPT; ++k) {
     const bool in = b < kBinSlots;   // past the end: read the last entry
@@ -177,12 +177,12 @@ __device__ __forceinline__ void sk_bins_load(int nv, const float* base, int stri
     if (q >= nv) { q -= nv; ++b; }
   }
 }
-template <int NPT>
+template <int T = kSkThreads, int NPT>
 __device__ __forceinline__ void sk_bins_sum(int nv, const float (&v)[NPT], float* scratch, float* out) {
   const int n = nv * kBinSlots;
 #pragma unroll
   for (int k = 0; k < NPT; ++k) {
-    const int i = (int)threadIdx.x + kSkThreads * k;
+    const int i = (int)threadIdx.x + T * k;
     if (i < n) scratch[i] = v[k];
   }
   __syncthreads();
