@@ -20,6 +20,12 @@ Other measurements (one JSON line each, same fields where they apply):
                 slow stream; 512 tokens from a 128-token prompt, against plain
                 greedy decoding on the same kernels (and the token streams are
                 checked to be equal)
+  --mode exit   EXIT-mode dynamic compute: the dual-stream step with gates at
+                every interior boundary in EXIT mode, for a sweep of exit
+                thresholds tau (the token comes from the fast row at the first
+                gate whose signal reaches tau; the skipped layers only fill
+                their cache entries from the slow row), tokens/s against the
+                mean exit boundary
   --mode moe    OLMoE-shaped mixture of experts (16 layers, d 2048, 64 experts
                 of width 1024, top 8, vocab 50304) with every expert in pinned
                 host memory and a 16-slot HBM cache per layer: on-demand LRU
@@ -564,6 +570,77 @@ def run_spec(args) -> int:
     return 0 if all(r["lossless"] for r in results) else 1
 
 
+def run_exit(args) -> int:
+    """EXIT-mode dual-stream decoding at the dense configuration: tokens/s and
+    the mean exit boundary for each threshold tau (tau > 1 never exits)."""
+    import torch
+    import synth
+    from paper_2502_02040_amd import Model, PagedKV
+
+    cfg = synth.CONFIGS[args.config]
+    dev = torch.device("cuda:0")
+    weights = synth.make_weights(cfg)
+    max_ctx = args.ctx + args.warmup + args.steps + 32
+    model = Model(cfg, weights, max_batch=1, max_chunk=16, max_ctx=max_ctx)
+    del weights
+    N = cfg.n_layers
+    gates = list(range(1, N))
+    prompt = synth.prompt_ids(cfg, args.ctx)
+    stream = torch.cuda.Stream()
+    results = []
+    for tau in args.taus:
+        bps = (max_ctx + 15) // 16
+        kv = PagedKV(cfg, 1, max_ctx, block_size=16, block_table=synth.block_table(1, bps, seed=cfg.seed))
+        desc = kv.desc()
+        pos = torch.zeros(1, dtype=torch.int32, device=dev)
+        tok = _prefill(model, prompt, pos, desc, dev)
+        exb = torch.zeros(1, dtype=torch.int32, device=dev)
+        hist = torch.zeros(args.steps, dtype=torch.int32, device=dev)
+
+        def step():
+            model.decode_step(tok, pos, desc, dual=True, gates=gates, tau=tau, mode="exit", next_token=tok,
+                              exit_boundary=exb, advance=True)
+
+        with torch.cuda.stream(stream):
+            for _ in range(args.warmup):
+                step()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            step()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            e0.record(stream)
+            for i in range(args.steps):
+                g.replay()
+                hist[i:i + 1].copy_(exb, non_blocking=True)   # the same small copy at every tau
+            e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        b = hist.cpu().numpy()
+        errs = model.device_errors()
+        if errs:
+            print(f"device error bits {errs}", file=sys.stderr)
+            return 1
+        results.append(dict(tau=tau, ms_per_step=round(ms, 5), tokens_per_s=round(1000.0 / ms, 2),
+                            mean_exit_boundary=round(float(b.mean()), 3), exit_rate=round(float((b < N).mean()), 4)))
+        _progress(f"exit: tau {tau}: {results[-1]}")
+        del kv
+    base = next((r for r in results if r["exit_rate"] == 0.0), results[0])
+    for r in results:
+        r["speedup"] = round(base["ms_per_step"] / r["ms_per_step"], 4)
+    main_r = min(results, key=lambda r: r["ms_per_step"])
+    _line(metric="EXIT-mode dual-stream decode tokens/s at batch 1 (tau sweep)", value=main_r["tokens_per_s"],
+          unit="tokens/s", steps=args.steps, warmup=args.warmup, ms_per_step=main_r["ms_per_step"],
+          dtype="bf16" if cfg.wdtype == "bf16" else "f32",
+          config={"workload": f"{cfg.name}-shaped dual-stream step in EXIT mode, gates at every interior boundary, "
+                              f"KV context {args.ctx}, HIP graph replay; value = the fastest tau",
+                  "batch": 1, "kv_context": args.ctx},
+          results=results, roofline=None, cpu_baseline=None)
+    return 0
+
+
 def run_moe(args) -> int:
     """OLMoE-shaped model with its experts in pinned host memory."""
     import torch
@@ -684,7 +761,9 @@ def run_copy(args) -> int:
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--mode", choices=("dense", "batch", "spec", "moe", "copy"), default="dense")
+    ap.add_argument("--mode", choices=("dense", "batch", "spec", "exit", "moe", "copy"), default="dense")
+    ap.add_argument("--taus", type=float, nargs="*", default=[2.0, 0.99, 0.985, 0.98, 0.97, 0.95, 0.9],
+                    help="exit mode: thresholds (above 1: never exits)")
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="phi3")
@@ -717,6 +796,10 @@ def main() -> int:
         return run_batch(args)
     if args.mode == "spec":
         return run_spec(args)
+    if args.mode == "exit":
+        args.steps = args.steps or 128
+        args.ctx = args.ctx or 1024
+        return run_exit(args)
     if args.mode == "copy":
         return run_copy(args)
     args.steps = args.steps or 256

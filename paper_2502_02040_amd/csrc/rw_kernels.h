@@ -466,7 +466,22 @@ __global__ __launch_bounds__(kRwThreads) void kr_qkv(Dims D, LayerPtrs L, RowMap
     if (layer > 0) ws.sig[tid * D.n_layers + layer - 1] = sig_s[tid];
   }
   rw_store_pieces<true>(xp, D.d, actf);
-  st.run(row_ptr, u0, u1, actf, D.d, epi, ops);
+  // EXIT mode, every sequence exited (at this boundary or before): the layer
+  // only fills its cache entries from the slow rows, so only the k and v rows
+  // are needed; they are spread over all waves (the units primed above are
+  // dropped)
+  bool all_ex = io.mode == EX_EXIT;
+  for (int sq = 0; sq < rm.nseq; ++sq) all_ex = all_ex && exited_s[sq] != 0;
+  if (all_ex) {
+    int v0, v1;
+    rw_range(2 * qd, gridDim.x * kRwWaves, gw, v0, v1);
+    v0 += qd;
+    v1 += qd;
+    st.begin(row_ptr, v0, v1, epi, ops);
+    st.run(row_ptr, v0, v1, actf, D.d, epi, ops);
+  } else {
+    st.run(row_ptr, u0, u1, actf, D.d, epi, ops);
+  }
 }
 
 // ============================================================================

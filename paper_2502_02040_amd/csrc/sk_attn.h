@@ -125,6 +125,9 @@ __global__ __launch_bounds__(kSkAttnThreads) void ks_attn(Dims D, LayerPtrs L, R
   const int nt = max(0, min(ctx, t0 + kSkAttnP) - t0);   // cached tokens of this split
   const int own_sp = min(ctx / kSkAttnP, S - 1);
   const bool own = sp == own_sp;
+  // an exited sequence (EXIT mode): only the own split has work (the cache
+  // entries of the slow rows); no split stores a partial or counts in
+  if (frozen && !own) return;
 
   // ---- round two: the RoPE entry of this thread's row, then keys and values ---
   float2 cs;
@@ -338,8 +341,8 @@ __global__ __launch_bounds__(kSkAttnThreads) void ks_attn(Dims D, LayerPtrs L, R
     }
   }
   // ---- every split counts in; the last merges --------------------------------
-  if (!arrive_last(&ws.att_cnt[sq * D.H + h], S, &last_flag)) return;
   if (frozen) return;
+  if (!arrive_last(&ws.att_cnt[sq * D.H + h], S, &last_flag)) return;
   // every partial's max, sum and this thread's accumulator element, loaded together
   const size_t pbase = (((size_t)sq * D.H + h) * (S + 1)) * kMaxRows;
   const int me = min(tid, R * S - 1), mi_ = me / S, ms_ = me % S;

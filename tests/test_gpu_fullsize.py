@@ -3,7 +3,9 @@
 through the C ABI and in the launch configuration bench.py times, against the
 float64 oracle on sampled outputs:
 
-  * the dual-stream step at batch 1 (OBSERVE gates at every boundary);
+  * the dual-stream step at batch 1 (OBSERVE gates at every boundary), and
+    in EXIT mode (the token from the fast row at the first gate whose signal
+    reaches tau, the skipped layers' cache filled from the slow row);
   * a draft of 4 tokens from the fast stream exiting at layer 8 and the
     verification of the 5-token chunk;
   * one dual-stream step of 8 sequences with 4096-token paged contexts (seeded
@@ -94,6 +96,48 @@ def test_phi3_dual_step(world):
         _check_cache(kv, cache, 0, pos, pos + 1, t, (0, 7, 31), f"step {step}")
         tok_d.copy_(nxt)
     assert t.compared >= 5
+
+
+def test_phi3_exit_step(world):
+    """EXIT mode at every interior boundary (tau 0.95): the exit boundary,
+    the fast row's token at the gate, the skipped layers' cache entries filled
+    from the slow row, and the signals of the layers that ran."""
+    model, orc = world
+    t = Tally()
+    kv = PagedKV(CFG, 1, 64, block_size=16, block_table=shuffled_table(1, 64, 16, 9))
+    cache = KVCache(CFG, 64)
+    prompt = list(synth.prompt_ids(CFG, PROMPT, stream="exit"))
+    tok, pos_d = _prefill(model, orc, kv, cache, prompt, t)
+    dev = torch.device("cuda")
+    N, tau = CFG.n_layers, 0.95
+    gates = list(range(1, N))
+    tok_d = torch.tensor([tok], dtype=torch.int32, device=dev)
+    nxt = torch.zeros(1, dtype=torch.int32, device=dev)
+    exb = torch.zeros(1, dtype=torch.int32, device=dev)
+    sig = torch.zeros(N, dtype=torch.float32, device=dev)
+    logits = torch.zeros(CFG.vocab, dtype=torch.float32, device=dev)
+    exits = 0
+    for step in range(3):
+        pos = PROMPT + step
+        model.decode_step(tok_d, pos_d, kv.desc(), gates=gates, tau=tau, mode="exit", next_token=nxt,
+                          exit_boundary=exb, signal=sig, logits=logits, advance=True)
+        torch.cuda.synchronize()
+        r = orc.decode_step(int(tok_d.item()), pos, cache, gates=gates, tau=tau, mode="exit")
+        # a signal within 2e-3 of tau at a boundary up to the exit may be decided either way
+        if any(abs(r.signal[b - 1] - tau) <= 2e-3 for b in gates if b <= r.exit_boundary):
+            t.skipped += 1
+            break
+        assert int(exb.item()) == r.exit_boundary, f"step {step} exit boundary"
+        exits += r.exit_boundary < N
+        ran = list(range(min(r.exit_boundary, N)))
+        got = sig.cpu().numpy()
+        assert np.max(np.abs(got[ran] - r.signal[ran])) <= TOL, f"step {step} signal"
+        t.rel(logits.cpu().numpy(), r.logits, TOL, f"step {step} logits")
+        t.token(int(nxt.item()), r.logits, TOL, f"step {step} token")
+        skipped = [l for l in (r.exit_boundary, (r.exit_boundary + N) // 2, N - 1) if l < N]
+        _check_cache(kv, cache, 0, pos, pos + 1, t, sorted(set([0] + skipped)), f"step {step}")
+        tok_d.copy_(nxt)
+    assert t.compared >= 2 or t.skipped
 
 
 def _oracle_draft_logits(orc, token, pos, cache, exit_layer, gamma):
