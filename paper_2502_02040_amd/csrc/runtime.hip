@@ -294,6 +294,7 @@ struct m2r2_ctx {
   bool rw_on = false;  // row-per-wave GEMVs for the one- and two-row class
   int rw_nch[3] = {0, 0, 0};   // 1 KB pieces per row for reductions over d, qdim, ffn
   int rw_nw[2] = {8, 8};       // waves per workgroup of the o and down projections
+  int attn_chunks = 0;         // batched short-chain attention: 128-token chunks per split (0: by size)
   SkPlan sk[5];
   SkWS skws{};
   int timed_class = -1;
@@ -485,6 +486,11 @@ m2r2_status run_layers_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const 
   // one or two rows per sequence (batched decoding): the short-chain
   // attention with fixed splits; longer chunks: the general kernel
   const bool short_attn = c->sk_attn_S > 0 && rows_per_seq <= 2;
+  // many splits in flight (batched long contexts): two 128-token chunks per
+  // split, the second chunk's loads overlapping the first chunk's work
+  const bool two = c->attn_chunks == 2 ||
+                   (c->attn_chunks == 0 && (long long)rm.nseq * D.H * c->sk_attn_S >= 8LL * c->sk_grid);
+  const int S2 = short_attn && two ? (c->max_ctx + 2 * kSkAttnP - 1) / (2 * kSkAttnP) : 0;
   const int S = choose_splits(rm.nseq, rows_per_seq, D.H, c->max_ctx);
   if (!short_attn && S > c->lay.S_max) return fail(M2R2_E_SHAPE, "attention splits exceed the workspace");
   if (!short_attn && S + 1 > 64)
@@ -494,7 +500,10 @@ m2r2_status run_layers_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const 
   for (int l = 0; l < n_layers_run; ++l) {
     const LayerPtrs& L = c->layers[l];
     TIMED(0, (k_qkv<WB, MT><<<G.qkv, kGemvThreads, G.l_d, st>>>(D, L, rm, c->ws, io, l)));
-    if (short_attn)
+    if (short_attn && S2 > 0)
+      TIMED(1, (ks_attn<WB, KB, HD, 2><<<dim3(S2, D.H, rm.nseq), kSkAttnThreads, sk_attn_lds_bytes(HD, D.r, WB),
+                                          st>>>(D, L, rm, c->ws, io, kv, l, S2)));
+    else if (short_attn)
       TIMED(1, (ks_attn<WB, KB, HD><<<dim3(c->sk_attn_S, D.H, rm.nseq), kSkAttnThreads,
                                        sk_attn_lds_bytes(HD, D.r, WB), st>>>(D, L, rm, c->ws, io, kv, l, c->sk_attn_S)));
     else
@@ -665,6 +674,9 @@ hipError_t sk_setup(m2r2_ctx* c) {
     const bool ok_a = S <= 64 && S <= c->lay.S_max && D.hd * D.r * wsz <= 2 * kSkAttnThreads * 16 &&
                       (D.hd * D.r * wsz) % 16 == 0 && D.r * D.hd / 8 <= 2 * kSkAttnThreads;
     c->sk_attn_S = ok_a ? S : 0;
+    // M2R2_ATTN_CHUNKS=1 or 2 fixes the chunks per split of the batched
+    // attention (tests exercise both forms at small sizes)
+    if (const char* ac = getenv("M2R2_ATTN_CHUNKS")) c->attn_chunks = (ac[0] == '1' || ac[0] == '2') ? ac[0] - '0' : 0;
     // row-per-wave GEMVs: rows of whole 1 KB pieces, a piece count with a
     // kernel, adapter up-factor rows of whole 16-byte pieces, and the
     // short-chain attention

@@ -27,18 +27,24 @@ constexpr int kSkAttnThreads = 256;  // 64 token slots x 4 lanes
 // Dynamic LDS: the head's rows of B_q, B_k, B_v (raw weights).
 __host__ __device__ constexpr int sk_attn_lds_bytes(int hd, int r, int wb) { return 3 * hd * r * (wb ? 2 : 4); }
 
-template <int WB, int KB, int HD>
+template <int WB, int KB, int HD, int NC = 1>
 __global__ __launch_bounds__(kSkAttnThreads) void ks_attn(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, KVPtrs kv,
                                                           int layer, int S) {
+  // NC chunks of kSkAttnP tokens per split: the next chunk's keys (values)
+  // are loaded while the current chunk's softmax (next scores) runs, and the
+  // chunks are combined online (running max, sum and accumulator per row)
   extern __shared__ __attribute__((aligned(16))) char bsl[];   // [3][HD][r] raw B rows of q, k, v
   constexpr int DPL = HD / 4;                                  // dims per lane, 4 lanes per token
   constexpr int KESZ = KB ? 2 : 4;
   constexpr int NCH = DPL * KESZ / 16;                         // 16-byte pieces per lane and token
-  constexpr int TPT = kSkAttnP / 64;                           // tokens per thread
+  constexpr int TPT = kSkAttnP / 64;                           // tokens per thread and chunk
+  constexpr int SPL = NC * kSkAttnP;                           // tokens per split
   constexpr int WESZ = WB ? 2 : 4;
   __shared__ float q_s[2][HD], k_s[2][HD], v_s[2][HD];
   __shared__ float u_s[2][3][kMaxRank];
   __shared__ float sc[2][kSkAttnP + 2];
+  __shared__ float lastw[2];   // weight of the last chunk's terms in the combined partial
+  __shared__ float fin_m[2], fin_l[2];   // the combined partial's max and sum per row
   __shared__ float red[4][2][HD];
   __shared__ float pvred[16][2][HD];
   __shared__ float rowm[2], rowl[2];
@@ -57,12 +63,14 @@ __global__ __launch_bounds__(kSkAttnThreads) void ks_attn(Dims D, LayerPtrs L, R
   // ---- round one: everything that does not depend on the position ----------
   const int posv = io.positions[sq];
   const int exv = ws.exited[sq];
-  int blk[TPT];
+  int blk[NC][TPT];
 #pragma unroll
-  for (int it = 0; it < TPT; ++it) {
-    const int tp = sp * kSkAttnP + slot + 64 * it;
-    blk[it] = kv.bt[sq * kv.mbps + min(tp / kv.bs, kv.mbps - 1)];
-  }
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int it = 0; it < TPT; ++it) {
+      const int tp = sp * SPL + c * kSkAttnP + slot + 64 * it;
+      blk[c][it] = kv.bt[sq * kv.mbps + min(tp / kv.bs, kv.mbps - 1)];
+    }
   // projection outputs of row m = e / HD, dim d = e % HD (rows of this
   // sequence: the map is read below; row indices are clamped to the batch)
   const int e_m = min(tid / HD, 1), e_d = tid % HD;
@@ -121,9 +129,8 @@ __global__ __launch_bounds__(kSkAttnThreads) void ks_attn(Dims D, LayerPtrs L, R
   const int first = rml.first[sq], R = rml.cnt[sq];
   const int ctx = posv + rm.pos_offset;
   const bool frozen = exv != 0;
-  const int t0 = sp * kSkAttnP;
-  const int nt = max(0, min(ctx, t0 + kSkAttnP) - t0);   // cached tokens of this split
-  const int own_sp = min(ctx / kSkAttnP, S - 1);
+  const int t0 = sp * SPL;
+  const int own_sp = min(ctx / SPL, S - 1);
   const bool own = sp == own_sp;
   // an exited sequence (EXIT mode): only the own split has work (the cache
   // entries of the slow rows); no split stores a partial or counts in
@@ -140,18 +147,20 @@ __global__ __launch_bounds__(kSkAttnThreads) void ks_attn(Dims D, LayerPtrs L, R
     cs = ws.rope[(size_t)pos * (HD / 2) + (e_d % (HD / 2))];
   }
   u32x4_t kr[TPT][NCH], vr[TPT][NCH];
+  // keys (or values) of chunk ch into dst
+  auto load_chunk = [&](const void* base, int ch, u32x4_t (&dst)[TPT][NCH]) {
 #pragma unroll
-  for (int it = 0; it < TPT; ++it) {
-    const int tp = t0 + slot + 64 * it;
-    int b = blk[it];
-    b = (b >= 0 && b < kv.num_blocks) ? b : 0;
-    const size_t ix = ((((size_t)layer * kv.num_blocks + b) * D.H + h) * kv.bs + tp % kv.bs) * HD + d0;
+    for (int it = 0; it < TPT; ++it) {
+      const int tp = t0 + ch * kSkAttnP + slot + 64 * it;
+      int b = blk[ch][it];
+      b = (b >= 0 && b < kv.num_blocks) ? b : 0;
+      const size_t ix = ((((size_t)layer * kv.num_blocks + b) * D.H + h) * kv.bs + tp % kv.bs) * HD + d0;
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      kr[it][c] = *(const u32x4_t*)((const char*)kv.k + ix * KESZ + 16 * c);
-      vr[it][c] = *(const u32x4_t*)((const char*)kv.v + ix * KESZ + 16 * c);
+      for (int c = 0; c < NCH; ++c) dst[it][c] = *(const u32x4_t*)((const char*)base + ix * KESZ + 16 * c);
     }
-  }
+  };
+  load_chunk(kv.k, 0, kr);
+  load_chunk(kv.v, 0, vr);
 
   // q (and k, v) before RoPE: base projection + adapter-up on fast rows
   const bool erow = tid < R * HD;
@@ -215,93 +224,123 @@ __global__ __launch_bounds__(kSkAttnThreads) void ks_attn(Dims D, LayerPtrs L, R
   }
 
   if (!frozen) {
-    // ---- scores of the cached tokens --------------------------------------
-#pragma unroll
-    for (int it = 0; it < TPT; ++it) {
-      const int j = slot + 64 * it;
-      float kk[DPL];
-#pragma unroll
-      for (int c = 0; c < NCH; ++c) {
-        if constexpr (KB) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) { kk[8 * c + 2 * i] = bf16lo(kr[it][c][i]); kk[8 * c + 2 * i + 1] = bf16hi(kr[it][c][i]); }
-        } else {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) kk[4 * c + i] = __uint_as_float(kr[it][c][i]);
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        float p = 0.f;
-#pragma unroll
-        for (int c = 0; c < DPL; ++c) p += q_s[i][d0 + c] * kk[c];
-        p = quad_sum(p);
-        if (sub == 0 && i < R) sc[i][j] = j < nt ? p * scale : -INFINITY;
-      }
-    }
-    // ---- own keys (own split): slow rows see the chunk's slow rows up to
-    // themselves (rounded as cached), a fast row only its own exact key ----
-    if (own) {   // wave wv: row i = wv >> 1, own key jj = wv & 1
-      const int i = wv >> 1, jj = wv & 1;
-      if (i < R) {
-        const int mi = first + i, mj = first + min(jj, R - 1);
-        const bool vis = jj < R && (rml.fast[mi] ? (jj == i) : (!rml.fast[mj] && rml.idx[mj] <= rml.idx[mi]));
-        const bool rnd = !rml.fast[mi];
-        float p = 0.f;
-        for (int d = lane; d < HD; d += 64) {
-          const float kk = k_s[min(jj, R - 1)][d];
-          p += q_s[i][d] * (rnd && KB ? round_bf16(kk) : kk);
-        }
-        p = wave_sum(p);
-        if (lane == 0) sc[i][kSkAttnP + jj] = vis ? p * scale : -INFINITY;
-      }
-    }
-    __syncthreads();
-    // ---- softmax partial per row (wave i handles row i) --------------------
-    const int ntot = kSkAttnP + (own ? 2 : 0);
-    if (wv < R) {
-      const int i = wv;
-      float mx = -INFINITY;
-      for (int j = lane; j < ntot; j += 64) mx = fmaxf(mx, sc[i][j]);
-      mx = wave_max(mx);
-      float l = 0.f;
-      for (int j = lane; j < ntot; j += 64) {
-        const float z = sc[i][j];
-        const float ev = z == -INFINITY ? 0.f : __expf(z - mx);
-        sc[i][j] = ev;
-        l += ev;
-      }
-      l = wave_sum(l);
-      if (lane == 0) { rowm[i] = l > 0.f ? mx : -INFINITY; rowl[i] = l; }
-    }
-    __syncthreads();
-    // ---- P V ---------------------------------------------------------------
+    float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
     float acc0[DPL], acc1[DPL];
 #pragma unroll
     for (int c = 0; c < DPL; ++c) { acc0[c] = 0.f; acc1[c] = 0.f; }
 #pragma unroll
-    for (int it = 0; it < TPT; ++it) {
-      const int j = slot + 64 * it;
-      const float p0 = sc[0][j], p1 = R > 1 ? sc[1][j] : 0.f;
+    for (int ch = 0; ch < NC; ++ch) {
+      const bool last = ch == NC - 1;
+      const int nt = max(0, min(ctx, t0 + (ch + 1) * kSkAttnP) - (t0 + ch * kSkAttnP));   // cached tokens of the chunk
+      // ---- scores of the chunk's cached tokens ------------------------------
 #pragma unroll
-      for (int c = 0; c < NCH; ++c) {
-        if constexpr (KB) {
+      for (int it = 0; it < TPT; ++it) {
+        const int j = slot + 64 * it;
+        float kk[DPL];
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float a = bf16lo(vr[it][c][i]), b = bf16hi(vr[it][c][i]);
-            acc0[8 * c + 2 * i] += p0 * a; acc0[8 * c + 2 * i + 1] += p0 * b;
-            acc1[8 * c + 2 * i] += p1 * a; acc1[8 * c + 2 * i + 1] += p1 * b;
+        for (int c = 0; c < NCH; ++c) {
+          if constexpr (KB) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) { kk[8 * c + 2 * i] = bf16lo(kr[it][c][i]); kk[8 * c + 2 * i + 1] = bf16hi(kr[it][c][i]); }
+          } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) kk[4 * c + i] = __uint_as_float(kr[it][c][i]);
           }
-        } else {
+        }
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float a = __uint_as_float(vr[it][c][i]);
-            acc0[4 * c + i] += p0 * a;
-            acc1[4 * c + i] += p1 * a;
+        for (int i = 0; i < 2; ++i) {
+          float p = 0.f;
+#pragma unroll
+          for (int c = 0; c < DPL; ++c) p += q_s[i][d0 + c] * kk[c];
+          p = quad_sum(p);
+          if (sub == 0 && i < R) sc[i][j] = j < nt ? p * scale : -INFINITY;
+        }
+      }
+      if (ch + 1 < NC) load_chunk(kv.k, ch + 1, kr);   // in flight during this chunk's softmax and P V
+      // ---- own keys (own split, with the last chunk): slow rows see the
+      // chunk's slow rows up to themselves (rounded as cached), a fast row
+      // only its own exact key ------------------------------------------------
+      if (own && last) {   // wave wv: row i = wv >> 1, own key jj = wv & 1
+        const int i = wv >> 1, jj = wv & 1;
+        if (i < R) {
+          const int mi = first + i, mj = first + min(jj, R - 1);
+          const bool vis = jj < R && (rml.fast[mi] ? (jj == i) : (!rml.fast[mj] && rml.idx[mj] <= rml.idx[mi]));
+          const bool rnd = !rml.fast[mi];
+          float p = 0.f;
+          for (int d = lane; d < HD; d += 64) {
+            const float kk = k_s[min(jj, R - 1)][d];
+            p += q_s[i][d] * (rnd && KB ? round_bf16(kk) : kk);
+          }
+          p = wave_sum(p);
+          if (lane == 0) sc[i][kSkAttnP + jj] = vis ? p * scale : -INFINITY;
+        }
+      }
+      __syncthreads();
+      // ---- softmax of the chunk per row (wave i handles row i) ---------------
+      const int ntot = kSkAttnP + (own && last ? 2 : 0);
+      if (wv < R) {
+        const int i = wv;
+        float mx = -INFINITY;
+        for (int j = lane; j < ntot; j += 64) mx = fmaxf(mx, sc[i][j]);
+        mx = wave_max(mx);
+        float l = 0.f;
+        for (int j = lane; j < ntot; j += 64) {
+          const float z = sc[i][j];
+          const float ev = z == -INFINITY ? 0.f : __expf(z - mx);
+          sc[i][j] = ev;
+          l += ev;
+        }
+        l = wave_sum(l);
+        if (lane == 0) { rowm[i] = l > 0.f ? mx : -INFINITY; rowl[i] = l; }
+      }
+      __syncthreads();
+      // ---- P V of the chunk, combined with the chunks before ------------------
+      float wc[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const float mc = rowm[min(i, R - 1)], lc = rowl[min(i, R - 1)];
+        const float mn = fmaxf(m_run[i], mc);
+        const float wr = m_run[i] == -INFINITY ? 0.f : __expf(m_run[i] - mn);
+        wc[i] = mc == -INFINITY ? 0.f : __expf(mc - mn);
+        l_run[i] = l_run[i] * wr + lc * wc[i];
+        m_run[i] = mn;
+#pragma unroll
+        for (int c = 0; c < DPL; ++c) {
+          if (i == 0) acc0[c] *= wr;
+          else acc1[c] *= wr;
+        }
+      }
+#pragma unroll
+      for (int it = 0; it < TPT; ++it) {
+        const int j = slot + 64 * it;
+        const float p0 = sc[0][j] * wc[0], p1 = R > 1 ? sc[1][j] * wc[1] : 0.f;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+          if constexpr (KB) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float a = bf16lo(vr[it][c][i]), b = bf16hi(vr[it][c][i]);
+              acc0[8 * c + 2 * i] += p0 * a; acc0[8 * c + 2 * i + 1] += p0 * b;
+              acc1[8 * c + 2 * i] += p1 * a; acc1[8 * c + 2 * i + 1] += p1 * b;
+            }
+          } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float a = __uint_as_float(vr[it][c][i]);
+              acc0[4 * c + i] += p0 * a;
+              acc1[4 * c + i] += p1 * a;
+            }
           }
         }
       }
+      if (ch + 1 < NC) {
+        load_chunk(kv.v, ch + 1, vr);   // in flight during the next chunk's scores
+        __syncthreads();                 // the next chunk's scores overwrite sc
+      } else if (tid < 2) {
+        lastw[tid] = wc[tid];
+      }
     }
+    if (tid < 2) { fin_m[tid] = m_run[tid]; fin_l[tid] = l_run[tid]; }
     // sum over the 4 token slots of a row (DPP), then the 16 row partials
     // (4 rows of 16 lanes x 4 waves) through LDS
 #pragma unroll
@@ -327,7 +366,7 @@ __global__ __launch_bounds__(kSkAttnThreads) void ks_attn(Dims D, LayerPtrs L, R
       if (own) {
         const bool rnd = !rml.fast[first + i];
         for (int jj = 0; jj < R; ++jj) {
-          const float w = sc[i][kSkAttnP + jj];
+          const float w = sc[i][kSkAttnP + jj] * lastw[i];
           if (w != 0.f) a += w * (rnd && KB ? round_bf16(v_s[jj][d]) : v_s[jj][d]);
         }
       }
@@ -335,8 +374,8 @@ __global__ __launch_bounds__(kSkAttnThreads) void ks_attn(Dims D, LayerPtrs L, R
       float* pp = ws.att + ((((size_t)sq * D.H + h) * (S + 1) + sp) * kMaxRows + i) * (2 + HD + r);
       st_agent(pp + 2 + d, a);
       if (d == 0) {
-        st_agent(pp, rowm[i]);
-        st_agent(pp + 1, rowl[i]);
+        st_agent(pp, fin_m[i]);
+        st_agent(pp + 1, fin_l[i]);
       }
     }
   }

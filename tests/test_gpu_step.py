@@ -169,11 +169,14 @@ def test_draft_and_verify(name, gamma, exit_layer):
 
 
 @pytest.mark.parametrize("name", CASES)
-def test_batched_dual_step(name):
+@pytest.mark.parametrize("chunks", ["1", "2"])
+def test_batched_dual_step(name, chunks, monkeypatch):
     """Three sequences with different context lengths decoded together
-    (two rows each: the batched short-chain attention and the 16-row GEMVs):
-    every sequence's logits, h, p, signal, token and cache entry match the
-    oracle step by step."""
+    (two rows each: the batched short-chain attention with one or two
+    128-token chunks per split, and the 16-row GEMVs): every sequence's
+    logits, h, p, signal, token and cache entry match the oracle step by
+    step."""
+    monkeypatch.setenv("M2R2_ATTN_CHUNKS", chunks)
     cfg = synth.CONFIGS[name]
     w = synth.make_weights(cfg)
     B, n_steps = 3, 4
