@@ -488,9 +488,9 @@ m2r2_status run_layers_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const 
   const bool short_attn = c->sk_attn_S > 0 && rows_per_seq <= 2;
   // many splits in flight (batched long contexts): two 128-token chunks per
   // split, the second chunk's loads overlapping the first chunk's work
-  const bool two = c->attn_chunks == 2 ||
-                   (c->attn_chunks == 0 && (long long)rm.nseq * D.H * c->sk_attn_S >= 8LL * c->sk_grid);
-  const int S2 = short_attn && two ? (c->max_ctx + 2 * kSkAttnP - 1) / (2 * kSkAttnP) : 0;
+  const int NCA = c->attn_chunks != 0 ? c->attn_chunks
+                  : ((long long)rm.nseq * D.H * c->sk_attn_S >= 8LL * c->sk_grid ? 2 : 1);
+  const int S2 = short_attn && NCA > 1 ? (c->max_ctx + NCA * kSkAttnP - 1) / (NCA * kSkAttnP) : 0;
   const int S = choose_splits(rm.nseq, rows_per_seq, D.H, c->max_ctx);
   if (!short_attn && S > c->lay.S_max) return fail(M2R2_E_SHAPE, "attention splits exceed the workspace");
   if (!short_attn && S + 1 > 64)
@@ -500,7 +500,10 @@ m2r2_status run_layers_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const 
   for (int l = 0; l < n_layers_run; ++l) {
     const LayerPtrs& L = c->layers[l];
     TIMED(0, (k_qkv<WB, MT><<<G.qkv, kGemvThreads, G.l_d, st>>>(D, L, rm, c->ws, io, l)));
-    if (short_attn && S2 > 0)
+    if (short_attn && S2 > 0 && NCA == 4)
+      TIMED(1, (ks_attn<WB, KB, HD, 4><<<dim3(S2, D.H, rm.nseq), kSkAttnThreads, sk_attn_lds_bytes(HD, D.r, WB),
+                                          st>>>(D, L, rm, c->ws, io, kv, l, S2)));
+    else if (short_attn && S2 > 0)
       TIMED(1, (ks_attn<WB, KB, HD, 2><<<dim3(S2, D.H, rm.nseq), kSkAttnThreads, sk_attn_lds_bytes(HD, D.r, WB),
                                           st>>>(D, L, rm, c->ws, io, kv, l, S2)));
     else if (short_attn)
@@ -674,9 +677,10 @@ hipError_t sk_setup(m2r2_ctx* c) {
     const bool ok_a = S <= 64 && S <= c->lay.S_max && D.hd * D.r * wsz <= 2 * kSkAttnThreads * 16 &&
                       (D.hd * D.r * wsz) % 16 == 0 && D.r * D.hd / 8 <= 2 * kSkAttnThreads;
     c->sk_attn_S = ok_a ? S : 0;
-    // M2R2_ATTN_CHUNKS=1 or 2 fixes the chunks per split of the batched
+    // M2R2_ATTN_CHUNKS=1, 2 or 4 fixes the chunks per split of the batched
     // attention (tests exercise both forms at small sizes)
-    if (const char* ac = getenv("M2R2_ATTN_CHUNKS")) c->attn_chunks = (ac[0] == '1' || ac[0] == '2') ? ac[0] - '0' : 0;
+    if (const char* ac = getenv("M2R2_ATTN_CHUNKS"))
+      c->attn_chunks = (ac[0] == '1' || ac[0] == '2' || ac[0] == '4') ? ac[0] - '0' : 0;
     // row-per-wave GEMVs: rows of whole 1 KB pieces, a piece count with a
     // kernel, adapter up-factor rows of whole 16-byte pieces, and the
     // short-chain attention
