@@ -425,11 +425,18 @@ m2r2_status run_layers_rw(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const
   const int G = c->sk_grid;
   const size_t lds = (size_t)kSkMinLds;
   const int nd = c->rw_nch[0], nq = c->rw_nch[1], nf = c->rw_nch[2];
+  // attention: one 128-token chunk per split (two only when M2R2_ATTN_CHUNKS
+  // asks for it: measured no faster at one sequence)
+  const int S2 = c->attn_chunks == 2 ? (c->max_ctx + 2 * kSkAttnP - 1) / (2 * kSkAttnP) : 0;
   for (int l = 0; l < n_layers_run; ++l) {
     const LayerPtrs& L = c->layers[l];
     TIMED(0, (kr_qkv_launch<WB>(nd, G, lds, st, D, L, rm, c->ws, io, l)));
-    TIMED(1, (ks_attn<WB, KB, HD><<<dim3(c->sk_attn_S, D.H, rm.nseq), kSkAttnThreads, sk_attn_lds_bytes(HD, D.r, WB),
-                                    st>>>(D, L, rm, c->ws, io, kv, l, c->sk_attn_S)));
+    if (S2 > 0)
+      TIMED(1, (ks_attn<WB, KB, HD, 2><<<dim3(S2, D.H, rm.nseq), kSkAttnThreads, sk_attn_lds_bytes(HD, D.r, WB),
+                                          st>>>(D, L, rm, c->ws, io, kv, l, S2)));
+    else
+      TIMED(1, (ks_attn<WB, KB, HD><<<dim3(c->sk_attn_S, D.H, rm.nseq), kSkAttnThreads,
+                                       sk_attn_lds_bytes(HD, D.r, WB), st>>>(D, L, rm, c->ws, io, kv, l, c->sk_attn_S)));
     TIMED(2, (kr_oproj_launch<WB>(nq, c->rw_nw[0], G, lds, st, D, L, rm, c->ws, io, l)));
     TIMED(3, (kr_gateup_launch<WB>(nd, G, lds, st, D, L, rm, c->ws, io, l)));
     TIMED(4, (kr_down_launch<WB>(nf, c->rw_nw[1], G, lds, st, D, L, rm, c->ws, io, l)));
