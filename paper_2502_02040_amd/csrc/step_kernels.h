@@ -110,11 +110,13 @@ struct WS {
 };
 
 // Bins per layer and row: kBinSlots are stored (and zeroed every pass); the
-// per-tile kernels use the first kBins, the stream-K kernels (whose tile
-// epilogues all run at the end of the launch) spread their atomics over all
-// kBinSlots.
+// per-tile kernels use the first kBins, the stream-K and row-per-wave kernels
+// spread their atomics over all kBinSlots (a workgroup adds into slot
+// blockIdx % kBinSlots).  Every consumer workgroup reads all slots, so the
+// count trades atomic contention against the bytes each consumer stages:
+// 16 (64 made the gate/up staging 1.2 us longer, 8 was no faster).
 constexpr int kBins = 8;
-constexpr int kBinSlots = 64;
+constexpr int kBinSlots = 16;
 
 __device__ __forceinline__ float* bin_d_at(const WS& ws, int l, int b, int m) { return ws.bin_d + (((size_t)l * kBinSlots + b) * kMaxRows + m) * 4; }
 __device__ __forceinline__ float* bin_o_at(const WS& ws, const Dims& D, int l, int b, int m) {
