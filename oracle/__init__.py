@@ -25,7 +25,7 @@ hit rates of real routers) are parity unpinned and are not claimed.
 """
 from .decoder import (Oracle, KVCache, StepResult, rms_norm, rope, attend, silu, topk_desc,
                       round_to_cache)
-from .cache_sim import simulate_expert_cache, CacheStats
+from .cache_sim import simulate_expert_cache, simulate_fixed_experts, CacheStats
 
 __all__ = ["Oracle", "KVCache", "StepResult", "rms_norm", "rope", "attend", "silu", "topk_desc",
-           "round_to_cache", "simulate_expert_cache", "CacheStats"]
+           "round_to_cache", "simulate_expert_cache", "simulate_fixed_experts", "CacheStats"]

@@ -22,6 +22,19 @@ demand).  The paper leaves the bookkeeping open; the reading used here:
      resident one is refreshed, a missing one is inserted into the slot with
      the smallest stamp among experts not predicted for L in this token;
   5. "hit" is logical: resident (or in flight) when the layer's MLP starts.
+
+The baselines the paper compares against (Sec. 3.3) reuse these rules:
+  * least-recently-used alone: no predictions;
+  * random preload and speculation from the previous layer's residual state:
+    the predictions for layer i+1 (random experts, or the top-k of layer
+    i+1's router applied to the slow row that enters layer i's MLP) are
+    applied after layer i (``schedule="next"``), instead of the fast row's
+    predictions for 2i+2 and 2i+3 (``schedule="aot"``);
+  * experts fixed in HBM without replacement (``simulate_fixed_experts``):
+    the paper does not say which experts are fixed or where a missing one
+    goes; the reading here keeps the first C-K experts of every layer
+    resident for good and copies every other needed expert, at every use,
+    into one of K staging slots, so that the HBM budget is the same C slots.
 """
 from __future__ import annotations
 
@@ -75,17 +88,20 @@ class _Layer:
 
 
 def simulate_expert_cache(slow: np.ndarray, pred: Optional[np.ndarray], n_experts: int, slots: int,
-                          *, prefetch: bool = True) -> CacheStats:
+                          *, prefetch: bool = True, schedule: str = "aot") -> CacheStats:
     """Run the policy over a trace.
 
     ``slow[t, l]``: experts used by layer l at token t (router order).
     ``pred[t, l]``: experts predicted for layer l at token t (row of -1 when
-    layer l has no prediction), or None.  Predictions for layer L=2i+2, 2i+3
-    are applied right after layer i of the same token.
+    layer l has no prediction), or None.  With ``schedule="aot"`` the
+    predictions for layers L=2i+2, 2i+3 are applied right after layer i of
+    the same token; with ``schedule="next"`` those for layer L=i+1.
     """
     T, N, K = slow.shape
     if slots < K or slots > n_experts:
         raise ValueError("need top_k <= slots <= n_experts")
+    if schedule not in ("aot", "next"):
+        raise ValueError(f"schedule {schedule!r}")
     clock = [0]
     layers = [_Layer(slots, clock) for _ in range(N)]
     st = CacheStats(per_layer_misses=[0] * N)
@@ -111,7 +127,7 @@ def simulate_expert_cache(slow: np.ndarray, pred: Optional[np.ndarray], n_expert
                     st.per_layer_misses[i] += 1
                     L.insert(e, protect, st, fallback=set(need))
             if use_pred:
-                for Lp in (2 * i + 2, 2 * i + 3):
+                for Lp in ((2 * i + 2, 2 * i + 3) if schedule == "aot" else (i + 1,)):
                     if Lp >= N:
                         continue
                     P = [int(e) for e in pred[t, Lp] if e >= 0]
@@ -124,4 +140,27 @@ def simulate_expert_cache(slow: np.ndarray, pred: Optional[np.ndarray], n_expert
                             tgt.insert(e, set(P), st)
                             tgt.prefetched[e] = True
                             st.prefetch_issued += 1
+    return st
+
+
+def simulate_fixed_experts(slow: np.ndarray, n_experts: int, slots: int) -> CacheStats:
+    """Experts fixed in HBM without replacement (Sec. 3.3, first strategy).
+
+    Experts 0..C-K-1 of every layer stay resident; every other needed expert
+    is a miss and is copied into a staging slot each time a layer needs it.
+    """
+    T, N, K = slow.shape
+    if slots < K or slots > n_experts:
+        raise ValueError("need top_k <= slots <= n_experts")
+    fixed = slots - K
+    st = CacheStats(per_layer_misses=[0] * N)
+    for t in range(T):
+        for i in range(N):
+            for e in slow[t, i]:
+                if int(e) < fixed:
+                    st.hits += 1
+                else:
+                    st.misses += 1
+                    st.per_layer_misses[i] += 1
+                    st.loads += 1
     return st

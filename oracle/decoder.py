@@ -143,6 +143,8 @@ class StepResult:
     slow_probs: Optional[np.ndarray] = None     # [N, E] router probabilities (MoE)
     pred_experts: Optional[np.ndarray] = None   # [N, K], -1 where no prediction (MoE)
     pred_logits: Optional[np.ndarray] = None    # [N, E] fast-router logits (MoE)
+    prev_pred_experts: Optional[np.ndarray] = None   # [N, K] layer l's top-k from the slow row entering layer l-1's MLP
+    prev_pred_logits: Optional[np.ndarray] = None    # [N, E] the logits behind prev_pred_experts
     router_logits: Optional[np.ndarray] = None  # [N, E] slow-router logits (MoE)
 
 
@@ -239,7 +241,7 @@ class Oracle:
         if self.cfg.is_moe:
             y, S, pz, z = self._moe_mlp(l, h1)
             if moe_out is not None:
-                moe_out.append((S, pz, z))
+                moe_out.append((S, pz, z, h1))
             return h1 + y
         return h1 + self._dense_mlp(l, h1, fast=False)
 
@@ -319,6 +321,17 @@ class Oracle:
             r.router_logits = np.array([m[2] for m in moe_rec]).reshape(n, cfg.n_experts)
             r.pred_experts = pred
             r.pred_logits = pred_logits
+            # speculation from the previous layer's residual state (the comparison
+            # strategy of Sec. 3.3): layer l+1's router on the slow row that enters
+            # layer l's MLP
+            N = cfg.n_layers
+            r.prev_pred_experts = np.full((N, cfg.top_k), -1, np.int64)
+            r.prev_pred_logits = np.full((N, cfg.n_experts), np.nan)
+            for l in range(n):
+                if l + 1 < N:
+                    z = self.router_logits(l + 1, moe_rec[l][3])
+                    r.prev_pred_logits[l + 1] = z
+                    r.prev_pred_experts[l + 1] = topk_desc(z, cfg.top_k)
         return r
 
     # -- slow-only chunk forward (prefill and verification) ------------------------------

@@ -243,3 +243,12 @@ def block_table(n_seqs: int, blocks_per_seq: int, *, seed: int = 0, shuffle: boo
     if shuffle:
         _stream(seed, "block_table").shuffle(ids)
     return ids.reshape(n_seqs, blocks_per_seq)
+
+
+def preload_table(cfg: ModelConfig, n_tokens: int, *, seed: Optional[int] = None) -> np.ndarray:
+    """``[n_tokens][n_layers][top_k]`` expert ids for the random-preload cache
+    strategy: in every row ``top_k`` distinct experts drawn uniformly from
+    ``[0, n_experts)`` (row 0 of each token, layer 0, is never used)."""
+    g = _stream(cfg.seed if seed is None else seed, "preload")
+    keys = g.random((n_tokens, cfg.n_layers, cfg.n_experts))
+    return np.argsort(keys, axis=-1, kind="stable")[..., :cfg.top_k].astype(np.int32)

@@ -1,6 +1,8 @@
 """Pins of the MoE parts of the oracle: the slow MoE stream against a library
-MoE decoder, and the expert-cache simulation against a textbook LRU and
-against the special cases the policy fixes."""
+MoE decoder, the speculation from the previous layer's residual state against
+the library decoder's own hidden states, and the expert-cache simulations
+against a textbook LRU, hand-worked traces and the special cases the policies
+fix."""
 from collections import OrderedDict
 
 import numpy as np
@@ -8,7 +10,7 @@ import pytest
 import torch
 
 import synth
-from oracle import Oracle, KVCache, simulate_expert_cache
+from oracle import Oracle, KVCache, simulate_expert_cache, simulate_fixed_experts
 
 MOE = synth.ModelConfig("moe_pin", n_layers=3, d_model=64, n_heads=2, head_dim=32, ffn=0, vocab=50, rank=4,
                         wdtype="f32", kvdtype="f64", n_experts=8, top_k=2, expert_ffn=32, seed=21)
@@ -56,6 +58,55 @@ def test_moe_slow_stream_matches_library_moe_decoder():
     got = Oracle(cfg, w).slow_chunk(ids, 0, KVCache(cfg, 16))
     # the library evaluates rotary angles and router softmax in float32
     np.testing.assert_allclose(got, ref, rtol=1e-5, atol=2e-6)
+
+
+def test_previous_layer_prediction_matches_library_hidden_states():
+    """The previous-layer strategy of Sec. 3.3: layer l+1's router applied to
+    the residual entering layer l's MLP.  The residual is captured from the
+    library decoder (input of its post-attention norm) and fed to the
+    library's own norm and router of layer l+1."""
+    cfg = MOE
+    N, K = cfg.n_layers, cfg.top_k
+    w = synth.make_weights(cfg, threads=4)
+    ids = list(synth.prompt_ids(cfg, 10))
+    m = _qwen2moe(cfg, w)
+    seen = {}
+    hooks = [m.model.layers[l].post_attention_layernorm.register_forward_hook(
+        lambda mod, inp, out, l=l: seen.__setitem__(l, inp[0][0, -1].detach().clone())) for l in range(N)]
+    ref = {}
+    with torch.no_grad():
+        m(torch.tensor([ids]))
+        for hk in hooks:
+            hk.remove()
+        for l in range(N - 1):
+            nxt = m.model.layers[l + 1]
+            z = nxt.mlp.gate(nxt.post_attention_layernorm(seen[l][None]))[0]
+            ref[l + 1] = z[0].numpy()
+    orc = Oracle(cfg, w)
+    cache = KVCache(cfg, 16)
+    orc.slow_chunk(ids[:-1], 0, cache)
+    r = orc.decode_step(ids[-1], len(ids) - 1, cache)
+    assert np.all(r.prev_pred_experts[0] == -1)
+    for l in range(1, N):
+        np.testing.assert_allclose(r.prev_pred_logits[l], ref[l], rtol=1e-6, atol=1e-9)
+        assert set(r.prev_pred_experts[l]) == set(np.argsort(-ref[l])[:K].tolist())
+
+
+def test_previous_layer_prediction_with_a_repeated_router_is_the_layers_own_choice():
+    """If layer l+1 has layer l's router and norm gain, the prediction for
+    l+1 equals the experts layer l itself chose (the same vector is routed)."""
+    cfg = MOE
+    w = dict(synth.make_weights(cfg, threads=4))
+    for l in range(1, cfg.n_layers):
+        w[f"L{l}.router"] = w["L0.router"]
+        w[f"L{l}.mlp_norm"] = w["L0.mlp_norm"]
+    orc = Oracle(cfg, w)
+    cache = KVCache(cfg, 16)
+    ids = list(synth.prompt_ids(cfg, 6))
+    orc.slow_chunk(ids[:-1], 0, cache)
+    r = orc.decode_step(ids[-1], len(ids) - 1, cache)
+    for l in range(cfg.n_layers - 1):
+        assert list(r.prev_pred_experts[l + 1]) == list(r.slow_experts[l])
 
 
 def test_moe_dual_step_slow_logits_equal_chunk_forward():
@@ -160,3 +211,59 @@ def test_cache_sim_worked_example():
     # t4 need 3: miss, evict 2 -> {1, 3}; t5 need 1: hit
     st = simulate_expert_cache(trace, None, 4, 2)
     assert (st.hits, st.misses) == (2, 4)
+
+
+def test_next_layer_schedule_worked_example():
+    """Hand-worked trace for predictions applied to layer i+1 after layer i:
+    E=4, K=1, C=2, two layers, both caches start as {0 (oldest), 1}."""
+    slow = np.array([[[2], [3]], [[2], [0]], [[1], [3]]])
+    pred = np.array([[[-1], [3]], [[-1], [1]], [[-1], [3]]])
+    # t0: L0 needs 2: miss, evict 0 -> {1, 2}; predict L1 {3}: load, evict 0 -> {1, 3*}
+    #     L1 needs 3: hit (prefetch used)
+    # t1: L0 needs 2: hit; predict L1 {1}: resident, refreshed -> {3, 1}
+    #     L1 needs 0: miss; victims exclude predicted 1 -> evict 3 -> {1, 0}
+    # t2: L0 needs 1: hit; predict L1 {3}: load, evict 1 (older than 0) -> {0, 3*}
+    #     L1 needs 3: hit (prefetch used)
+    st = simulate_expert_cache(slow, pred, 4, 2, schedule="next")
+    assert (st.hits, st.misses) == (4, 2)
+    assert st.per_layer_misses == [1, 1]
+    assert (st.prefetch_issued, st.prefetch_used, st.prefetch_wasted) == (2, 2, 0)
+    assert (st.pred_correct, st.pred_total) == (2, 3)
+    assert st.loads == 4
+
+
+def test_next_layer_schedule_special_cases():
+    rng = np.random.default_rng(9)
+    E, K, N, T = 16, 4, 6, 25
+    trace = np.stack([[rng.choice(E, K, replace=False) for _ in range(N)] for _ in range(T)])
+    # a perfect predictor for layer i+1: every layer but the first hits, even with C = K
+    pred = trace.copy()
+    pred[:, 0] = -1
+    st = simulate_expert_cache(trace, pred, E, K, schedule="next")
+    assert st.per_layer_misses[1:] == [0] * (N - 1)
+    assert st.prefetch_used == st.prefetch_issued
+    # without predictions both schedules are plain LRU
+    a = simulate_expert_cache(trace, None, E, 6, schedule="next")
+    b = simulate_expert_cache(trace, None, E, 6, schedule="aot")
+    assert a == b
+    with pytest.raises(ValueError):
+        simulate_expert_cache(trace, pred, E, K, schedule="later")
+
+
+def test_fixed_experts_closed_form():
+    """Fixed experts: a use is a hit exactly when the expert is one of the
+    first C-K, and every other use is a copy."""
+    rng = np.random.default_rng(11)
+    E, K, N, T, C = 12, 3, 4, 30, 7
+    trace = np.stack([[rng.choice(E, K, replace=False) for _ in range(N)] for _ in range(T)])
+    st = simulate_fixed_experts(trace, E, C)
+    low = trace < C - K
+    assert st.hits == int(low.sum()) and st.misses == int((~low).sum()) == st.loads
+    assert st.per_layer_misses == [int((~low[:, l]).sum()) for l in range(N)]
+    assert st.prefetch_issued == st.pred_total == 0
+    # C = K leaves nothing fixed; C = E keeps E-K experts, so only the top ids miss
+    assert simulate_fixed_experts(trace, E, K).misses == trace.size
+    st = simulate_fixed_experts(np.array([[[0, 9], [11, 10]]]), 12, 12)
+    assert (st.hits, st.misses) == (2, 2)
+    with pytest.raises(ValueError):
+        simulate_fixed_experts(trace, E, K - 1)
