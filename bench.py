@@ -28,9 +28,12 @@ Other measurements (one JSON line each, same fields where they apply):
                 mean exit boundary
   --mode moe    OLMoE-shaped mixture of experts (16 layers, d 2048, 64 experts
                 of width 1024, top 8, vocab 50304) with every expert in pinned
-                host memory and a 16-slot HBM cache per layer: on-demand LRU
-                (slow stream alone), M2R2 ahead-of-time prefetch from the fast
-                stream's predictions, and an all-resident cache
+                host memory and a 16-slot HBM cache per layer, fed a
+                teacher-forced Zipf token stream: the five placement
+                strategies of the paper's comparison (fixed experts, LRU, LRU
+                with random preload, previous-layer speculation on the slow
+                stream alone; M2R2 ahead-of-time prefetch from the fast
+                stream) and an all-resident cache, with per-layer miss rates
 """
 from __future__ import annotations
 
@@ -663,17 +666,27 @@ def run_moe(args) -> int:
     plen, steps, C = args.prompt, args.steps, args.slots
     max_ctx = plen + steps + args.warmup + 16
     prompt = synth.prompt_ids(cfg, plen)
+    # decode inputs: a teacher-forced token stream with natural-text (Zipf)
+    # frequencies, so that routing varies from token to token as it does on
+    # text (greedy tokens of random weights fall into short cycles)
+    stream_ids = torch.tensor(synth.zipf_ids(cfg, args.warmup + steps), dtype=torch.int32, device=dev)
+    table = synth.preload_table(cfg, args.warmup + steps)
+    E = cfg.n_experts
     runs = []
-    for label, variant, slots, policy, dual in (
-            ("on-demand LRU, slow stream alone", {}, C, "on_demand", False),
-            ("M2R2 ahead-of-time prefetch", {}, C, "ahead_of_time", True),
-            ("all experts resident", {}, cfg.n_experts, "on_demand", True),
-            ("M2R2 ahead-of-time, router-coherent variant", {"router_coherent": True}, C, "ahead_of_time", True),
-            ("on-demand LRU, router-coherent variant", {"router_coherent": True}, C, "on_demand", False)):
+    # the four strategies the paper compares with (Sec. 3.3) run the slow
+    # stream alone; M2R2 runs both rows
+    for label, slots, policy, dual in (
+            ("fixed experts, no replacement", C, "fixed", False),
+            ("on-demand LRU", C, "on_demand", False),
+            ("LRU + random preload", C, "random_preload", False),
+            ("previous-layer residual speculation", C, "previous_layer", False),
+            ("M2R2 ahead-of-time prefetch", C, "ahead_of_time", True),
+            ("all experts resident", E, "on_demand", True)):
         _progress(f"moe: {label}")
-        w = synth.make_weights(cfg, names=names, **variant)
+        w = synth.make_weights(cfg, names=names)
         model = Model(cfg, w, max_batch=1, max_chunk=16, max_ctx=max_ctx, expert_slots=slots, expert_store=store)
         del w
+        model.moe_set_preload_table(table)
         model.moe_set_policy(policy)
         kv = PagedKV(cfg, 1, max_ctx, block_size=16)
         desc = kv.desc()
@@ -682,24 +695,25 @@ def run_moe(args) -> int:
         for t in prompt:   # prefill with slow-only steps (not timed)
             model.decode_step(torch.tensor([int(t)], dtype=torch.int32, device=dev), pos, desc, dual=False,
                               next_token=nxt, advance=True)
-        for _ in range(args.warmup):
-            model.decode_step(nxt, pos, desc, dual=dual, next_token=nxt, advance=True)
+        for i in range(args.warmup):
+            model.decode_step(stream_ids[i:i + 1], pos, desc, dual=dual, next_token=nxt, advance=True)
         torch.cuda.synchronize()
-        model.moe_reset()
+        model.moe_reset()   # the preload table restarts at its row 0: the same draws as the replay
         stream = torch.cuda.current_stream()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         t0 = time.perf_counter()
         e0.record(stream)
-        for _ in range(steps):
-            model.decode_step(nxt, pos, desc, dual=dual, next_token=nxt, advance=True)
+        for i in range(steps):
+            j = args.warmup + i
+            model.decode_step(stream_ids[j:j + 1], pos, desc, dual=dual, next_token=nxt, advance=True)
         e1.record(stream)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
         ms = e0.elapsed_time(e1)
         st = model.moe_stats()
         k_avg_ms, k_n = _kernel_avg_ms(model, "expert_gateup", stream,
-                                       lambda: model.decode_step(nxt, pos, desc, dual=dual, next_token=nxt,
-                                                                 advance=True), 4)
+                                       lambda: model.decode_step(stream_ids[0:1], pos, desc, dual=dual,
+                                                                 next_token=nxt, advance=True), 4)
         n_use = st["hits"] + st["misses"]
         runs.append(dict(run=label, slots=slots, policy=policy, dual_stream=dual,
                          tokens_per_s=round(steps * 1000.0 / ms, 3), ms_per_token=round(ms / steps, 4),
@@ -710,23 +724,23 @@ def run_moe(args) -> int:
                          pred_accuracy=round(st["pred_correct"] / st["pred_total"], 4) if st["pred_total"] else None,
                          h2d_gb=round(st["h2d_bytes"] / 1e9, 3), copy_waits=st["copy_waits"],
                          host_wait_ms_per_token=round(st["host_wait_ns"] / 1e6 / steps, 4),
-                         layer_misses=st["layer_misses"],
+                         layer_miss_rate=[round(m / (steps * cfg.top_k), 4) for m in st["layer_misses"]],
                          expert_gateup_us=round(k_avg_ms * 1e3, 3)))
         del model, kv
         torch.cuda.empty_cache()
-    resident = runs[2]
+    resident = runs[-1]
     for r in runs:
         r["stall_ms_per_token_vs_resident"] = round(r["ms_per_token"] - resident["ms_per_token"], 4)
     kb = expert_gateup_bytes(cfg)
     achieved = kb / (resident["expert_gateup_us"] * 1e-6) / 1e9
-    m2 = runs[1]
+    m2 = next(r for r in runs if r["policy"] == "ahead_of_time")
     _line(metric="MoE decode tokens/s at batch 1 with experts in host memory (HBM expert cache, AoT prefetch)",
           value=m2["tokens_per_s"], unit="tokens/s", steps=steps, warmup=args.warmup,
           ms_per_step=m2["ms_per_token"], dtype="bf16",
           config={"workload": f"olmoe-shaped {cfg.n_layers}L d{cfg.d_model} {cfg.n_heads}x{cfg.head_dim} "
                               f"E{cfg.n_experts} top{cfg.top_k} Fe{cfg.expert_ffn} vocab{cfg.vocab} rank{cfg.rank}, "
                               f"experts in pinned host memory, {C} HBM slots per layer, prompt {plen}, "
-                              f"{steps} decode steps", "batch": 1, "slots": C},
+                              f"{steps} teacher-forced Zipf-token decode steps", "batch": 1, "slots": C},
           token_bytes_all_hits=int(moe_token_bytes(cfg, plen + steps / 2)), runs=runs,
           roofline={"bound": "hbm", "kernel": "expert gate/up (k_moe_gateup)", "achieved": round(achieved, 1),
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),

@@ -162,8 +162,10 @@ typedef struct {
   int32_t advance;          /* nonzero: positions_d[b] += 1 at the end of the step */
   /* mixture of experts, optional: [batch][n_layers][top_k] experts chosen by
    * the slow row's router (descending probability, lowest id on ties; -1 for
-   * layers not run after an exit), and experts predicted for layer l from the
-   * fast row after layer (l-2)/2 (Sec. 2.3.3; -1 where no prediction) */
+   * layers not run after an exit), and experts predicted for layer l: from
+   * the fast row after layer (l-2)/2 (Sec. 2.3.3), or, under the
+   * M2R2_MOE_PREVIOUS_LAYER policy, by layer l's router from the slow row
+   * entering layer l-1's MLP (-1 where no prediction) */
   int32_t* slow_experts_d;
   int32_t* pred_experts_d;
 } m2r2_step_out;
@@ -211,9 +213,12 @@ M2R2_API void m2r2_destroy(m2r2_ctx* ctx);
  * library's on-demand copy stream), makes `stream` wait for any copy still in
  * flight, and runs the experts from their cache slots.  Under the
  * M2R2_MOE_AHEAD_OF_TIME policy the predicted experts are then copied on the
- * library's prefetch stream.  Cache replacement is least-recently-used, with
- * the experts needed now and those predicted for the layer protected from
- * eviction.  The call returns once the last layer's experts are enqueued. */
+ * library's prefetch stream; the comparison policies preload their own
+ * picks for the next layer on that stream instead (m2r2_moe_policy).  Cache
+ * replacement is least-recently-used, with the experts needed now and those
+ * predicted for the layer protected from eviction (M2R2_MOE_FIXED: no
+ * replacement).  The call returns once the last layer's experts are
+ * enqueued. */
 M2R2_API m2r2_status m2r2_decode_step(m2r2_ctx* ctx, int32_t batch, int32_t dual, const int32_t* tokens_d,
                                       int32_t* positions_d, const m2r2_kv* kv, const m2r2_exit* ex,
                                       const m2r2_step_out* out, hipStream_t stream);
@@ -247,16 +252,26 @@ M2R2_API m2r2_status m2r2_verify(m2r2_ctx* ctx, const int32_t* chunk_d, int32_t 
 
 /* ---- mixture of experts (Sec. 2.3.3) ----------------------------------- */
 
+/* Expert placement strategies: M2R2's own and the four it is compared with
+ * (Sec. 3.3).  Every policy works in the same `slots` slots per layer. */
 typedef enum {
   M2R2_MOE_ON_DEMAND = 0,      /* least-recently-used cache, misses loaded when routed */
-  M2R2_MOE_AHEAD_OF_TIME = 1   /* as above, plus copies of the fast stream's predictions */
+  M2R2_MOE_AHEAD_OF_TIME = 1,  /* as above, plus copies of the fast stream's predictions for
+                                  layers 2i+2 and 2i+3, issued after layer i (dual steps) */
+  M2R2_MOE_FIXED = 2,          /* experts 0..slots-top_k-1 resident for good; every other chosen
+                                  expert is copied, at every use, into one of top_k staging slots */
+  M2R2_MOE_RANDOM_PRELOAD = 3, /* least-recently-used, plus a preload of top_k random experts
+                                  (a caller's table) for layer i+1 after layer i */
+  M2R2_MOE_PREVIOUS_LAYER = 4  /* least-recently-used, plus a preload of the top_k experts that
+                                  layer i+1's router picks from the slow row entering layer i's
+                                  MLP, issued after layer i */
 } m2r2_moe_policy;
 
 typedef struct {
   int64_t hits, misses;             /* chosen experts resident (or in flight) / not, when routed */
   int64_t prefetch_issued, prefetch_used, prefetch_wasted;   /* wasted: evicted before any use */
   int64_t loads;                    /* host-to-device expert copies */
-  int64_t pred_correct, pred_total; /* |P ∩ S| and |P| over predicted layers (ahead-of-time policy) */
+  int64_t pred_correct, pred_total; /* |P ∩ S| and |P| over predicted layers (preloading policies) */
   int64_t h2d_bytes;                /* bytes copied host to device */
   int64_t copy_waits;               /* times the compute stream was made to wait for a copy */
   int64_t host_wait_ns;             /* host time spent waiting for routing results */
@@ -274,15 +289,27 @@ M2R2_API m2r2_status m2r2_expert_bytes(const m2r2_config* cfg, size_t* bytes_out
 M2R2_API m2r2_status m2r2_pack_expert(const m2r2_config* cfg, const void* wg_h, const void* wu_h, const void* wd_h,
                                       void* dst_h);
 
-/* Select the cache policy for later decode steps (default: ahead of time). */
+/* Select the cache policy (m2r2_moe_policy) for later decode steps (default:
+ * ahead of time) and restore the warm start as m2r2_moe_reset does
+ * (synchronous).  M2R2_E_INVALID for an unknown policy. */
 M2R2_API m2r2_status m2r2_moe_set_policy(m2r2_ctx* ctx, int32_t policy);
+
+/* Random draws of the M2R2_MOE_RANDOM_PRELOAD policy: ids_h is
+ * [n_tokens][n_layers][top_k] expert ids in [0, n_experts) (-1: no preload),
+ * copied into the context.  The decode step that is the t-th since the last
+ * reset (counting from 0) preloads row (t mod n_tokens, i+1) for layer i+1
+ * after layer i.  Host-only; M2R2_E_SHAPE for ids out of range or
+ * n_tokens < 1.  A decode step under that policy without a table fails with
+ * M2R2_E_STATE. */
+M2R2_API m2r2_status m2r2_moe_set_preload_table(m2r2_ctx* ctx, const int32_t* ids_h, int32_t n_tokens);
 
 /* Make experts ids_h[0..n) of `layer` resident or in flight (Sec. 2.3.3,
  * Appendix B): a resident expert is marked as just used; a missing one
  * replaces the least recently used expert not in ids_h and is copied from the
  * host store on copy_stream (priority != 0: on the library's on-demand copy
  * stream; NULL copy_stream: the library's prefetch stream).  Later decode
- * steps wait for the copy before they use the slot.  Counts as prefetches. */
+ * steps wait for the copy before they use the slot.  Counts as prefetches.
+ * M2R2_E_STATE under the M2R2_MOE_FIXED policy (its slots never change). */
 M2R2_API m2r2_status m2r2_prefetch_experts(m2r2_ctx* ctx, int32_t layer, const int32_t* ids_h, int32_t n,
                                            int32_t priority, hipStream_t copy_stream);
 
@@ -293,15 +320,17 @@ M2R2_API m2r2_status m2r2_moe_reset(m2r2_ctx* ctx);
 /* Counters since the last reset. */
 M2R2_API m2r2_status m2r2_moe_stats(m2r2_ctx* ctx, m2r2_moe_counters* out);
 
-/* Host-only replay of the cache policy on a routing trace, with no copies:
+/* Host-only replay of a cache policy on a routing trace, with no copies:
  * slow_h[t][l][top_k] experts chosen at token t, layer l; pred_h (may be
- * NULL) the same shape, predictions (-1 where none).  With prefetch != 0 the
- * predictions for layers 2i+2, 2i+3 are applied after layer i as the
- * ahead-of-time policy does.  Fills the counters of `out` (h2d_bytes,
- * copy_waits and host_wait_ns are 0). */
+ * NULL) the same shape, predictions (-1 where none).  `policy` is an
+ * m2r2_moe_policy: ON_DEMAND ignores pred_h; AHEAD_OF_TIME applies the
+ * predictions for layers 2i+2, 2i+3 after layer i; RANDOM_PRELOAD and
+ * PREVIOUS_LAYER apply those for layer i+1 after layer i; FIXED ignores
+ * pred_h.  Fills the counters of `out` (h2d_bytes, copy_waits and
+ * host_wait_ns are 0). */
 M2R2_API m2r2_status m2r2_expert_cache_replay(int32_t n_layers, int32_t n_experts, int32_t top_k, int32_t slots,
                                               int32_t n_tokens, const int32_t* slow_h, const int32_t* pred_h,
-                                              int32_t prefetch, m2r2_moe_counters* out);
+                                              int32_t policy, m2r2_moe_counters* out);
 
 /* Kernel timing for measurement.  Kernel classes of one decode pass:
  * 0 qkv, 1 attention, 2 output projection, 3 gate/up, 4 down, 5 LM head,

@@ -24,11 +24,12 @@ PROJ = ("q", "k", "v", "o", "g", "u", "d")
 EXPORTS = ("m2r2_workspace_size", "m2r2_create", "m2r2_destroy", "m2r2_decode_step", "m2r2_draft", "m2r2_verify",
            "m2r2_timing_enable", "m2r2_timing_read", "m2r2_time_gateup_layers", "m2r2_device_errors",
            "m2r2_last_error", "m2r2_expert_bytes", "m2r2_pack_expert", "m2r2_moe_set_policy", "m2r2_prefetch_experts",
-           "m2r2_moe_reset", "m2r2_moe_stats", "m2r2_expert_cache_replay")
+           "m2r2_moe_reset", "m2r2_moe_stats", "m2r2_expert_cache_replay", "m2r2_moe_set_preload_table")
 KERNEL_CLASSES = {"qkv": 0, "attn": 1, "oproj": 2, "gateup": 3, "down": 4, "head": 5, "embed": 6, "attn_merge": 7,
                   "expert_gateup": 8, "expert_down": 9, "router": 10}
-MOE_ON_DEMAND, MOE_AHEAD_OF_TIME = 0, 1
-POLICIES = {"on_demand": MOE_ON_DEMAND, "ahead_of_time": MOE_AHEAD_OF_TIME}
+MOE_ON_DEMAND, MOE_AHEAD_OF_TIME, MOE_FIXED, MOE_RANDOM_PRELOAD, MOE_PREVIOUS_LAYER = 0, 1, 2, 3, 4
+POLICIES = {"on_demand": MOE_ON_DEMAND, "ahead_of_time": MOE_AHEAD_OF_TIME, "fixed": MOE_FIXED,
+            "random_preload": MOE_RANDOM_PRELOAD, "previous_layer": MOE_PREVIOUS_LAYER}
 
 
 class Config(ctypes.Structure):
@@ -108,6 +109,7 @@ def lib() -> ctypes.CDLL:
         L.m2r2_moe_set_policy.argtypes = [c_void_p, c_int32]
         L.m2r2_prefetch_experts.argtypes = [c_void_p, c_int32, POINTER(c_int32), c_int32, c_int32, c_void_p]
         L.m2r2_moe_reset.argtypes = [c_void_p]
+        L.m2r2_moe_set_preload_table.argtypes = [c_void_p, c_void_p, c_int32]
         L.m2r2_moe_stats.argtypes = [c_void_p, POINTER(MoeCounters)]
         L.m2r2_expert_cache_replay.argtypes = [c_int32, c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,
                                                c_int32, POINTER(MoeCounters)]
@@ -115,7 +117,7 @@ def lib() -> ctypes.CDLL:
                   "m2r2_timing_enable", "m2r2_timing_read", "m2r2_time_gateup_layers", "m2r2_device_errors",
                   "m2r2_expert_bytes",
                   "m2r2_pack_expert", "m2r2_moe_set_policy", "m2r2_prefetch_experts", "m2r2_moe_reset",
-                  "m2r2_moe_stats", "m2r2_expert_cache_replay"):
+                  "m2r2_moe_stats", "m2r2_expert_cache_replay", "m2r2_moe_set_preload_table"):
             getattr(L, f).restype = c_int32
         _lib = L
     return _lib
@@ -195,14 +197,16 @@ def pack_expert_store(cfg, expert_source, *, threads: int = 8):
 
 
 def cache_replay(n_layers: int, n_experts: int, top_k: int, slots: int, slow: np.ndarray,
-                 pred: Optional[np.ndarray] = None, prefetch: bool = True) -> dict:
+                 pred: Optional[np.ndarray] = None, prefetch=True) -> dict:
     """Host-only replay of the library's expert-cache policy on a trace
-    ``slow[t][l][k]`` (and predictions of the same shape, -1 where none)."""
+    ``slow[t][l][k]`` (and predictions of the same shape, -1 where none).
+    ``prefetch``: a policy name, or a bool (ahead of time / on demand)."""
+    policy = POLICIES[prefetch] if isinstance(prefetch, str) else (MOE_AHEAD_OF_TIME if prefetch else MOE_ON_DEMAND)
     slow = np.ascontiguousarray(slow, dtype=np.int32)
     pr = None if pred is None else np.ascontiguousarray(pred, dtype=np.int32)
     out = MoeCounters()
     _check(lib().m2r2_expert_cache_replay(n_layers, n_experts, top_k, slots, slow.shape[0], slow.ctypes.data,
-                                          None if pr is None else pr.ctypes.data, 1 if prefetch else 0,
+                                          None if pr is None else pr.ctypes.data, policy,
                                           ctypes.byref(out)), "m2r2_expert_cache_replay")
     return out.as_dict(n_layers)
 
@@ -387,6 +391,13 @@ class Model:
 
     def moe_reset(self) -> None:
         _check(lib().m2r2_moe_reset(self._ctx), "m2r2_moe_reset")
+
+    def moe_set_preload_table(self, ids: np.ndarray) -> None:
+        """Random-preload draws ``[n_tokens][n_layers][top_k]``."""
+        a = np.ascontiguousarray(ids, dtype=np.int32)
+        if a.ndim != 3 or a.shape[1:] != (self.cfg.n_layers, self.cfg.top_k):
+            raise ValueError(f"preload table of shape {a.shape}")
+        _check(lib().m2r2_moe_set_preload_table(self._ctx, a.ctypes.data, a.shape[0]), "m2r2_moe_set_preload_table")
 
     def moe_stats(self) -> dict:
         out = MoeCounters()

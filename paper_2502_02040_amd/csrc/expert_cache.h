@@ -120,6 +120,29 @@ class ExpertCachePolicy {
     }
   }
 
+  // Experts fixed in HBM without replacement (the first strategy the paper
+  // compares with, Sec. 3.3): experts 0..C-k-1 stay in slots 0..C-k-1 (where
+  // the warm start put them); every other needed expert is a miss and goes,
+  // at every use, into staging slot C-k+j, j its rank among the layer's
+  // misses.  No stamps move.
+  void use_fixed(int l, const int* need, int k, int* slot_out, bool* load_out) {
+    const int fixed = C_ - k;
+    int j = 0;
+    for (int i = 0; i < k; ++i) {
+      if (need[i] < fixed) {
+        ++cnt_.hits;
+        slot_out[i] = need[i];
+        load_out[i] = false;
+      } else {
+        ++cnt_.misses;
+        ++cnt_.layer_misses[l];
+        ++cnt_.loads;
+        slot_out[i] = fixed + j++;
+        load_out[i] = true;
+      }
+    }
+  }
+
   // Experts pred[0..n) (entries < 0 ignored) are predicted for layer l.
   // For each expert that must be copied, its slot is appended to slots_out
   // and the expert to experts_out.

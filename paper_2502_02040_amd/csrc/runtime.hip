@@ -265,6 +265,9 @@ struct MoeState {
   int* host_words = nullptr;       // mapped host block written by k_topk
   int seq = 0;
   int policy = M2R2_MOE_AHEAD_OF_TIME;
+  std::vector<int> preload;        // [preload_tokens][n_layers][K] random-preload draws
+  int preload_tokens = 0;
+  int64_t token = 0;               // decode steps since the last warm start
   ExpertCachePolicy pol;
   std::vector<hipEvent_t> slot_ev;   // [n_layers*C] last copy into the slot
   std::vector<char> slot_pending;    // a copy was recorded and not yet seen complete
@@ -785,7 +788,15 @@ m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVP
   const size_t smem = attn_smem_bytes();
   const size_t gl = gemv_lds_bytes(WB, MT);
   const bool ahead = dual && M.policy == M2R2_MOE_AHEAD_OF_TIME;
-  const bool want_pred = dual && (ahead || (out && out->pred_experts_d));
+  const bool prev = M.policy == M2R2_MOE_PREVIOUS_LAYER;
+  const bool fixed = M.policy == M2R2_MOE_FIXED;
+  const int* random_row = nullptr;   // this token's random-preload draws
+  if (M.policy == M2R2_MOE_RANDOM_PRELOAD) {
+    if (M.preload_tokens < 1) return fail(M2R2_E_STATE, "random preload without a table");
+    random_row = M.preload.data() + (size_t)(M.token % M.preload_tokens) * D.n_layers * M.K;
+  }
+  // fast-row predictions: for the ahead-of-time copies, or reported on request
+  const bool want_pred = dual && !prev && (ahead || (out && out->pred_experts_d));
   const Grids G = grids<WB, MT>(c);
   const int tiles = (M.E + 15) / 16;
   float* logits = (float*)M.mp.logits;
@@ -803,10 +814,15 @@ m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVP
     if (want_pred)
       for (int lp = 2 * l + 2; lp <= 2 * l + 3 && lp < D.n_layers; ++lp, ++n_pred)
         t[1 + n_pred] = RouterTask{M.router[lp], c->layers[lp].mlp_norm, 1, 1, l + 1, logits + (1 + n_pred) * M.E};
+    // previous-layer speculation (Sec. 3.3): layer l+1's router on the same
+    // slow-row vector that layer l routes
+    if (prev && l + 1 < D.n_layers)
+      t[1 + n_pred++] = RouterTask{M.router[l + 1], c->layers[l + 1].mlp_norm, 0, 0, l, logits + M.E};
     TIMED(10, (k_router<WB><<<tiles * (1 + n_pred), kGemvThreads, gl, st>>>(D, M.E, t[0], t[1], t[2], 1 + n_pred,
                                                                           c->ws)));
     int* slow_out = out->slow_experts_d ? out->slow_experts_d + l * M.K : nullptr;
-    int* pred_out = (out->pred_experts_d && n_pred) ? out->pred_experts_d + (2 * l + 2) * M.K : nullptr;
+    int* pred_out = (out->pred_experts_d && n_pred) ? out->pred_experts_d + (prev ? l + 1 : 2 * l + 2) * M.K
+                                                    : nullptr;
     const int seq = ++M.seq;
     TIMED(10, (k_topk<<<1, 256, 0, st>>>(M.E, M.K, logits, 1, n_pred, M.mp, c->ws, slow_out, pred_out, seq)));
     HIP_TRY(hipGetLastError());
@@ -822,7 +838,10 @@ m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVP
       need[k] = M.host_words[k];
       if (need[k] < 0 || need[k] >= M.E) return fail(M2R2_E_HIP, "layer %d: router returned expert %d", l, need[k]);
     }
-    M.pol.use(l, need, M.K, slot, load);
+    if (fixed)
+      M.pol.use_fixed(l, need, M.K, slot, load);
+    else
+      M.pol.use(l, need, M.K, slot, load);
     for (int k = 0; k < M.K; ++k)
       if (load[k]) HIP_TRY(moe_copy(c, l, slot[k], need[k], M.copy_demand));
     ExpertSlots es{};
@@ -847,20 +866,25 @@ m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVP
     HIP_TRY(hipGetLastError());
     HIP_TRY(hipEventRecord(M.layer_done[l], st));
     M.layer_done_rec[l] = 1;
-    if (ahead) {
-      for (int j = 0; j < n_pred; ++j) {
-        pslots.clear();
-        pexperts.clear();
-        M.pol.predict(2 * l + 2 + j, M.host_words + (1 + j) * kMaxTopK, M.K, &pslots, &pexperts);
-        for (size_t q = 0; q < pslots.size(); ++q)
-          HIP_TRY(moe_copy(c, 2 * l + 2 + j, pslots[q], pexperts[q], M.copy_ahead));
-      }
-    }
+    auto preload = [&](int lp, const int* ids) -> hipError_t {
+      pslots.clear();
+      pexperts.clear();
+      M.pol.predict(lp, ids, M.K, &pslots, &pexperts);
+      hipError_t r = hipSuccess;
+      for (size_t q = 0; q < pslots.size() && r == hipSuccess; ++q)
+        r = moe_copy(c, lp, pslots[q], pexperts[q], M.copy_ahead);
+      return r;
+    };
+    if (ahead)
+      for (int j = 0; j < n_pred; ++j) HIP_TRY(preload(2 * l + 2 + j, M.host_words + (1 + j) * kMaxTopK));
+    if (prev && n_pred) HIP_TRY(preload(l + 1, M.host_words + kMaxTopK));
+    if (random_row && l + 1 < D.n_layers) HIP_TRY(preload(l + 1, random_row + (l + 1) * M.K));
   }
   TIMED(5, (k_head<WB, MT><<<G.head, kGemvThreads, G.l_d, st>>>(D, c->lm_head, c->final_norm, rm, c->ws, io, kv,
                                                               c->lay.TV, D.n_layers)));
   HIP_TRY(hipGetLastError());
   M.pol.end_token();
+  ++M.token;
   return M2R2_OK;
 }
 
@@ -915,6 +939,7 @@ hipError_t moe_warm(m2r2_ctx* c) {
   std::fill(M.slot_pending.begin(), M.slot_pending.end(), 0);
   std::fill(M.layer_done_rec.begin(), M.layer_done_rec.end(), 0);
   M.h2d_bytes = M.copy_waits = M.host_wait_ns = 0;
+  M.token = 0;
   return e;
 }
 
@@ -1327,8 +1352,22 @@ M2R2_API m2r2_status m2r2_pack_expert(const m2r2_config* cfg, const void* wg_h, 
 M2R2_API m2r2_status m2r2_moe_set_policy(m2r2_ctx* c, int32_t policy) {
   if (!c) return fail(M2R2_E_INVALID, "ctx is NULL");
   if (!c->moe.on) return fail(M2R2_E_STATE, "not a mixture-of-experts context");
-  if (policy != M2R2_MOE_ON_DEMAND && policy != M2R2_MOE_AHEAD_OF_TIME) return fail(M2R2_E_INVALID, "policy %d", policy);
+  if (policy < M2R2_MOE_ON_DEMAND || policy > M2R2_MOE_PREVIOUS_LAYER) return fail(M2R2_E_INVALID, "policy %d", policy);
   c->moe.policy = policy;
+  HIP_TRY(moe_warm(c));
+  return M2R2_OK;
+}
+
+M2R2_API m2r2_status m2r2_moe_set_preload_table(m2r2_ctx* c, const int32_t* ids_h, int32_t n_tokens) {
+  if (!c || !ids_h) return fail(M2R2_E_INVALID, "NULL argument");
+  MoeState& M = c->moe;
+  if (!M.on) return fail(M2R2_E_STATE, "not a mixture-of-experts context");
+  if (n_tokens < 1) return fail(M2R2_E_SHAPE, "n_tokens %d", n_tokens);
+  const size_t n = (size_t)n_tokens * c->D.n_layers * M.K;
+  for (size_t i = 0; i < n; ++i)
+    if (ids_h[i] < -1 || ids_h[i] >= M.E) return fail(M2R2_E_SHAPE, "preload expert id %d", ids_h[i]);
+  M.preload.assign(ids_h, ids_h + n);
+  M.preload_tokens = n_tokens;
   return M2R2_OK;
 }
 
@@ -1337,6 +1376,7 @@ M2R2_API m2r2_status m2r2_prefetch_experts(m2r2_ctx* c, int32_t layer, const int
   if (!c) return fail(M2R2_E_INVALID, "ctx is NULL");
   MoeState& M = c->moe;
   if (!M.on) return fail(M2R2_E_STATE, "not a mixture-of-experts context");
+  if (M.policy == M2R2_MOE_FIXED) return fail(M2R2_E_STATE, "the fixed-experts policy takes no prefetches");
   if (layer < 0 || layer >= c->D.n_layers) return fail(M2R2_E_SHAPE, "layer %d", layer);
   if (n < 0 || n > M.C || (n > 0 && !ids_h)) return fail(M2R2_E_SHAPE, "n %d not in [0, slots]", n);
   for (int i = 0; i < n; ++i) {
@@ -1370,8 +1410,9 @@ M2R2_API m2r2_status m2r2_moe_stats(m2r2_ctx* c, m2r2_moe_counters* out) {
 
 M2R2_API m2r2_status m2r2_expert_cache_replay(int32_t n_layers, int32_t n_experts, int32_t top_k, int32_t slots,
                                               int32_t n_tokens, const int32_t* slow_h, const int32_t* pred_h,
-                                              int32_t prefetch, m2r2_moe_counters* out) {
+                                              int32_t policy, m2r2_moe_counters* out) {
   if (!slow_h || !out) return fail(M2R2_E_INVALID, "NULL argument");
+  if (policy < M2R2_MOE_ON_DEMAND || policy > M2R2_MOE_PREVIOUS_LAYER) return fail(M2R2_E_INVALID, "policy %d", policy);
   if (n_layers < 1 || n_layers > 127 || n_experts < 1 || top_k < 1 || top_k > kMaxTopK || n_tokens < 0)
     return fail(M2R2_E_SHAPE, "sizes");
   if (slots < top_k || slots > n_experts) return fail(M2R2_E_SHAPE, "need top_k <= slots <= n_experts");
@@ -1387,10 +1428,17 @@ M2R2_API m2r2_status m2r2_expert_cache_replay(int32_t n_layers, int32_t n_expert
   std::vector<int> s1, e1;
   for (int t = 0; t < n_tokens; ++t) {
     for (int l = 0; l < n_layers; ++l) {
-      pol.use(l, slow_h + t * per_tok + l * top_k, top_k, slot, load);
-      if (prefetch && pred_h)
-        for (int lp = 2 * l + 2; lp <= 2 * l + 3 && lp < n_layers; ++lp)
-          pol.predict(lp, pred_h + t * per_tok + lp * top_k, top_k, &s1, &e1);
+      const int32_t* need = slow_h + t * per_tok + l * top_k;
+      if (policy == M2R2_MOE_FIXED) {
+        pol.use_fixed(l, need, top_k, slot, load);
+        continue;
+      }
+      pol.use(l, need, top_k, slot, load);
+      if (!pred_h || policy == M2R2_MOE_ON_DEMAND) continue;
+      const int lp0 = policy == M2R2_MOE_AHEAD_OF_TIME ? 2 * l + 2 : l + 1;
+      const int lp1 = policy == M2R2_MOE_AHEAD_OF_TIME ? 2 * l + 3 : l + 1;
+      for (int lp = lp0; lp <= lp1 && lp < n_layers; ++lp)
+        pol.predict(lp, pred_h + t * per_tok + lp * top_k, top_k, &s1, &e1);
     }
     pol.end_token();
   }

@@ -161,7 +161,7 @@ def _stream(seed: int, name: str) -> np.random.Generator:
 
 def make_tensor(cfg: ModelConfig, name: str, shape: Tuple[int, ...], kind: str, *,
                 adapter_scale: float = 1.0, decay: Optional[Tuple[int, float]] = None,
-                router_coherent: bool = False) -> np.ndarray:
+                router_coherent: bool = False, embed_scale: float = 1.0) -> np.ndarray:
     """One weight tensor as float32 (already rounded to bf16 for bf16 configs).
 
     Variants used by the structured experiments:
@@ -169,7 +169,11 @@ def make_tensor(cfg: ModelConfig, name: str, shape: Tuple[int, ...], kind: str, 
         stream identical to the slow one);
       * ``decay=(layer, lam)`` scales ``wo`` and ``wd`` of layers >= layer by
         ``lam`` (a shrinking late-layer update);
-      * ``router_coherent`` draws router ``l`` as ``shared + 0.5 * noise_l``.
+      * ``router_coherent`` draws router ``l`` as ``shared + 0.5 * noise_l``;
+      * ``embed_scale`` multiplies the token embedding (a larger one keeps the
+        token's identity visible in the residual stream through the layers,
+        as in trained models, instead of a residual dominated by the context
+        average that the attention layers add).
     """
     if kind == "ones":
         a = np.ones(shape, np.float32)
@@ -181,6 +185,8 @@ def make_tensor(cfg: ModelConfig, name: str, shape: Tuple[int, ...], kind: str, 
             _stream(cfg.seed, "router.shared").standard_normal(out=shared, dtype=np.float32)
             a = shared + np.float32(0.5) * a
         a *= np.float32(0.02)
+        if name == "embed":
+            a *= np.float32(embed_scale)
         base = name.split(".")[-1]
         if base.startswith("A_") or base.startswith("B_"):
             a *= np.float32(adapter_scale)
@@ -252,3 +258,15 @@ def preload_table(cfg: ModelConfig, n_tokens: int, *, seed: Optional[int] = None
     g = _stream(cfg.seed if seed is None else seed, "preload")
     keys = g.random((n_tokens, cfg.n_layers, cfg.n_experts))
     return np.argsort(keys, axis=-1, kind="stable")[..., :cfg.top_k].astype(np.int32)
+
+
+def zipf_ids(cfg: ModelConfig, n: int, *, s: float = 1.0, seed: Optional[int] = None,
+             stream: str = "zipf") -> np.ndarray:
+    """``n`` token ids whose frequencies follow Zipf's law, the rank-frequency
+    shape of natural text: the id of rank r (a seeded permutation of the
+    vocabulary) is drawn with probability proportional to r**-s."""
+    g = _stream(cfg.seed if seed is None else seed, stream)
+    p = np.arange(1, cfg.vocab + 1, dtype=np.float64) ** -s
+    p /= p.sum()
+    perm = g.permutation(cfg.vocab)
+    return perm[g.choice(cfg.vocab, size=n, p=p)].astype(np.int32)

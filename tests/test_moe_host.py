@@ -1,11 +1,11 @@
 """Host-side parts of the mixture-of-experts path, no GPU needed: the C
-library's expert-cache policy (replayed on routing traces) against the
-oracle's cache simulation, and the packed expert layout."""
+library's expert-cache policies (replayed on routing traces) against the
+oracle's cache simulations, and the packed expert layout."""
 import numpy as np
 import pytest
 
 import synth
-from oracle import simulate_expert_cache
+from oracle import simulate_expert_cache, simulate_fixed_experts
 from paper_2502_02040_amd import binding as B
 
 FIELDS = ("hits", "misses", "prefetch_issued", "prefetch_used", "prefetch_wasted", "loads", "pred_correct",
@@ -51,6 +51,41 @@ def test_policy_replay_matches_cache_simulation(seed, C, prefetch):
     E, K, N, T = 12, 3, 7, 40
     slow, pred = _trace(rng, T, N, E, K, correlated=0.5)
     assert _lib(slow, pred, E, C, prefetch) == _oracle(slow, pred, E, C, prefetch)
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+@pytest.mark.parametrize("C", [3, 6, 12])
+@pytest.mark.parametrize("policy", ["random_preload", "previous_layer"])
+def test_next_layer_policies_replay_matches_cache_simulation(seed, C, policy):
+    """Both comparison strategies that preload for layer i+1 after layer i."""
+    rng = np.random.default_rng(seed + 10)
+    E, K, N, T = 12, 3, 7, 40
+    slow, pred = _trace(rng, T, N, E, K, correlated=0.6)
+    pred[:, 1] = slow[:, 1]          # layer 1 gets a prediction too under this schedule
+    st = simulate_expert_cache(slow, pred, E, C, schedule="next")
+    want = {f: getattr(st, f) for f in FIELDS}
+    want["layer_misses"] = list(st.per_layer_misses)
+    assert _lib(slow, pred, E, C, policy) == want
+    assert want["prefetch_issued"] > 0 or C == E
+
+
+@pytest.mark.parametrize("C", [3, 5, 12])
+def test_fixed_policy_replay_matches_simulation(C):
+    rng = np.random.default_rng(C)
+    E, K, N, T = 12, 3, 5, 30
+    slow, pred = _trace(rng, T, N, E, K)
+    st = simulate_fixed_experts(slow, E, C)
+    got = _lib(slow, pred, E, C, "fixed")
+    want = {f: getattr(st, f) for f in FIELDS}
+    want["layer_misses"] = list(st.per_layer_misses)
+    assert got == want
+
+
+def test_replay_rejects_unknown_policy():
+    slow = np.zeros((1, 2, 2), np.int32)
+    slow[..., 1] = 1
+    out = B.MoeCounters()
+    assert B.lib().m2r2_expert_cache_replay(2, 4, 2, 2, 1, slow.ctypes.data, None, 5, B.ctypes.byref(out)) != 0
 
 
 def test_policy_replay_without_predictions_matches():
