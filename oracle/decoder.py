@@ -104,6 +104,33 @@ def round_to_cache(x: np.ndarray, kvdtype: str) -> np.ndarray:
     raise ValueError(kvdtype)
 
 
+ARLA_DIM = 64   # latent width of the exit router (the value the paper uses)
+
+
+def arla_score(wq: np.ndarray, wk: np.ndarray, wv: np.ndarray, w_out: np.ndarray, b_out: float,
+               states: Sequence[np.ndarray], eps: float) -> float:
+    """Exit probability of the accelerated-residual latent-attention router
+    (Sec. 2.3.1, ARLA; Fig. 4a) at a gate.
+
+    ``states`` are the fast residuals after each layer of the interval that
+    ends at the gate, oldest first.  Each is RMS-normalised without a gain,
+    then projected to the latent space (``wk``, ``wv``: [64, d]); the query is
+    the projection (``wq``) of the last state; single-query softmax attention
+    with scale 1/sqrt(64) pools the values, and a linear readout with a
+    sigmoid gives the probability.  (The paper does not fix the query, the
+    normalisation or the readout; these are the readings used throughout.)
+    """
+    U = [x / np.sqrt(np.mean(x * x) + eps) for x in states]
+    q = wq @ U[-1]
+    K = np.stack([wk @ u for u in U])
+    V = np.stack([wv @ u for u in U])
+    z = K @ q / np.sqrt(ARLA_DIM)
+    a = np.exp(z - z.max())
+    a = a / a.sum()
+    o = a @ V
+    return float(1.0 / (1.0 + np.exp(-(w_out @ o + b_out))))
+
+
 def cosine(a: np.ndarray, b: np.ndarray) -> float:
     return float(np.dot(a, b) / (np.linalg.norm(a) * np.linalg.norm(b)))
 
@@ -145,6 +172,7 @@ class StepResult:
     pred_logits: Optional[np.ndarray] = None    # [N, E] fast-router logits (MoE)
     prev_pred_experts: Optional[np.ndarray] = None   # [N, K] layer l's top-k from the slow row entering layer l-1's MLP
     prev_pred_logits: Optional[np.ndarray] = None    # [N, E] the logits behind prev_pred_experts
+    fast_states: Optional[np.ndarray] = None    # [N, d] p after each layer (before a gate's restart), nan if not run
     router_logits: Optional[np.ndarray] = None  # [N, E] slow-router logits (MoE)
 
 
@@ -266,13 +294,19 @@ class Oracle:
 
     # -- the dual-stream decode step -------------------------------------------------
     def decode_step(self, token: int, pos: int, cache: KVCache, *, gates: Sequence[int] = (),
-                    tau: float = 2.0, mode: str = "observe") -> StepResult:
+                    tau: float = 2.0, mode: str = "observe", arla: Optional[Dict[str, np.ndarray]] = None
+                    ) -> StepResult:
         """One decode step carrying the slow row ``h`` and the fast row ``p``.
 
         ``gates`` are boundaries b in [1, N-1]; at a gate the signal of layer
         b-1 is compared with ``tau``: the first gate with signal >= tau is
         recorded as the exit boundary; in ``exit`` mode the step stops there,
         otherwise (and whenever the test fails) ``p`` restarts from ``h``.
+
+        With ``arla`` (arrays ``wq``, ``wk``, ``wv`` [N, 64, d], ``w_out``
+        [N, 64], ``b_out`` [N]; block b belongs to boundary b) the signal at a
+        gate b is ``arla_score`` over the fast states after the layers
+        [previous gate (or 0), b-1] instead of the cosine of layer b-1.
         """
         cfg = self.cfg
         assert mode in MODES
@@ -285,12 +319,20 @@ class Oracle:
         moe_rec: List = []
         pred = np.full((N, max(cfg.top_k, 1)), -1, np.int64)
         pred_logits = np.full((N, max(cfg.n_experts, 1)), np.nan)
+        self._fast_states = np.full((N, cfg.d_model), np.nan)
+        interval: List[np.ndarray] = []   # fast states since the last gate
         for l in range(N):
             p_in = p
             # fast row first: it sees the cache before the slow row writes position pos
             p, _ = self._fast_layer(l, p, pos, cache.K[l][:pos], cache.V[l][:pos])
             h = self._slow_layer(l, h, pos, cache, moe_rec)
+            self._fast_states[l] = p
+            interval.append(p)
             signal[l] = cosine(p_in, p)
+            if arla is not None and mode != "off" and (l + 1) in gates:
+                b = l + 1
+                signal[l] = arla_score(arla["wq"][b], arla["wk"][b], arla["wv"][b], arla["w_out"][b],
+                                       float(arla["b_out"][b]), interval, cfg.rms_eps)
             if cfg.is_moe:
                 for lp in (2 * l + 2, 2 * l + 3):
                     if lp < N:
@@ -298,6 +340,8 @@ class Oracle:
                         pred_logits[lp] = z
                         pred[lp] = topk_desc(z, cfg.top_k)
             b = l + 1
+            if b in gates:
+                interval = []
             if mode != "off" and b in gates:
                 fired = signal[l] >= tau
                 if fired and exit_b == N:
@@ -313,7 +357,8 @@ class Oracle:
 
     def _result(self, logits, exit_b, signal, h, p, moe_rec, pred, pred_logits) -> StepResult:
         cfg = self.cfg
-        r = StepResult(token=argmax_first(logits), logits=logits, exit_boundary=exit_b, signal=signal, h=h, p=p)
+        r = StepResult(token=argmax_first(logits), logits=logits, exit_boundary=exit_b, signal=signal, h=h, p=p,
+                       fast_states=self._fast_states)
         if cfg.is_moe:
             n = len(moe_rec)
             r.slow_experts = np.array([m[0] for m in moe_rec]).reshape(n, cfg.top_k)

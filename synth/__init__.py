@@ -270,3 +270,20 @@ def zipf_ids(cfg: ModelConfig, n: int, *, s: float = 1.0, seed: Optional[int] = 
     p /= p.sum()
     perm = g.permutation(cfg.vocab)
     return perm[g.choice(cfg.vocab, size=n, p=p)].astype(np.int32)
+
+
+def arla_weights(cfg: ModelConfig, *, dim: int = 64, seed: Optional[int] = None) -> Dict[str, np.ndarray]:
+    """Weights of the latent-attention exit router, one block per boundary b
+    (block 0 unused): ``wq``, ``wk``, ``wv`` [n_layers, dim, d] N(0, 0.02) in
+    the weight dtype (as float32), ``w_out`` [n_layers, dim] N(0, 1/dim) and
+    ``b_out`` [n_layers] zero, float32."""
+    s = cfg.seed if seed is None else seed
+    out: Dict[str, np.ndarray] = {}
+    for nm in ("wq", "wk", "wv"):
+        a = _stream(s, f"arla.{nm}").standard_normal((cfg.n_layers, dim, cfg.d_model), dtype=np.float32)
+        a *= np.float32(0.02)
+        out[nm] = bf16_round(a) if cfg.wdtype == "bf16" else a
+    out["w_out"] = (_stream(s, "arla.w_out").standard_normal((cfg.n_layers, dim), dtype=np.float32)
+                    * np.float32(1.0 / np.sqrt(dim))).astype(np.float32)
+    out["b_out"] = np.zeros(cfg.n_layers, np.float32)
+    return out
