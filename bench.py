@@ -25,7 +25,9 @@ Other measurements (one JSON line each, same fields where they apply):
                 thresholds tau (the token comes from the fast row at the first
                 gate whose signal reaches tau; the skipped layers only fill
                 their cache entries from the slow row), tokens/s against the
-                mean exit boundary
+                mean exit boundary; --gate-every K puts the gates every K
+                layers, --arla decides them with the latent-attention exit
+                router (seeded synthetic weights)
   --mode moe    OLMoE-shaped mixture of experts (16 layers, d 2048, 64 experts
                 of width 1024, top 8, vocab 50304) with every expert in pinned
                 host memory and a 16-slot HBM cache per layer, fed a
@@ -587,7 +589,9 @@ def run_exit(args) -> int:
     model = Model(cfg, weights, max_batch=1, max_chunk=16, max_ctx=max_ctx)
     del weights
     N = cfg.n_layers
-    gates = list(range(1, N))
+    gates = list(range(args.gate_every, N, args.gate_every))
+    if args.arla:
+        model.set_arla(synth.arla_weights(cfg))
     prompt = synth.prompt_ids(cfg, args.ctx)
     stream = torch.cuda.Stream()
     results = []
@@ -634,12 +638,14 @@ def run_exit(args) -> int:
     for r in results:
         r["speedup"] = round(base["ms_per_step"] / r["ms_per_step"], 4)
     main_r = min(results, key=lambda r: r["ms_per_step"])
+    signal = ("latent-attention exit router (seeded synthetic weights, 64-wide)" if args.arla
+              else "cosine signal")
     _line(metric="EXIT-mode dual-stream decode tokens/s at batch 1 (tau sweep)", value=main_r["tokens_per_s"],
           unit="tokens/s", steps=args.steps, warmup=args.warmup, ms_per_step=main_r["ms_per_step"],
           dtype="bf16" if cfg.wdtype == "bf16" else "f32",
-          config={"workload": f"{cfg.name}-shaped dual-stream step in EXIT mode, gates at every interior boundary, "
-                              f"KV context {args.ctx}, HIP graph replay; value = the fastest tau",
-                  "batch": 1, "kv_context": args.ctx},
+          config={"workload": f"{cfg.name}-shaped dual-stream step in EXIT mode, gates every {args.gate_every} "
+                              f"layer(s), {signal}, KV context {args.ctx}, HIP graph replay; value = the fastest tau",
+                  "batch": 1, "kv_context": args.ctx, "gates": gates},
           results=results, roofline=None, cpu_baseline=None)
     return 0
 
@@ -793,6 +799,9 @@ def main() -> int:
     ap.add_argument("--decay", type=float, nargs="*", default=[1.0, 0.1],
                     help="spec mode: scale of wo/wd in layers >= exit layer (1.0 = plain weights)")
     ap.add_argument("--slots", type=int, default=16, help="moe mode: HBM expert slots per layer")
+    ap.add_argument("--gate-every", type=int, default=1, help="exit mode: a gate every this many layers")
+    ap.add_argument("--arla", action="store_true",
+                    help="exit mode: decide the gates with the latent-attention exit router")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: --gpus {args.gpus} is not supported "

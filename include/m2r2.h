@@ -155,7 +155,9 @@ typedef struct {
 typedef struct {
   int32_t* next_token_d;    /* [batch] required: greedy token (lowest id on ties) */
   int32_t* exit_boundary_d; /* [batch] optional: first gate whose signal >= tau, n_layers if none */
-  float* signal_d;          /* [batch][n_layers] optional: cos(p entering, p leaving) per layer */
+  float* signal_d;          /* [batch][n_layers] optional: cos(p entering, p leaving) per layer; with
+                               the exit router set (m2r2_set_arla), its score at the layer before
+                               each gate */
   float* logits_d;          /* [batch][vocab] optional: logits of the emitted row */
   float* h_out_d;           /* [batch][d] optional: slow row fed to the head (gate state on exit) */
   float* p_out_d;           /* [batch][d] optional: fast row at the end of the step */
@@ -222,6 +224,31 @@ M2R2_API void m2r2_destroy(m2r2_ctx* ctx);
 M2R2_API m2r2_status m2r2_decode_step(m2r2_ctx* ctx, int32_t batch, int32_t dual, const int32_t* tokens_d,
                                       int32_t* positions_d, const m2r2_kv* kv, const m2r2_exit* ex,
                                       const m2r2_step_out* out, hipStream_t stream);
+
+/* Accelerated-residual latent-attention exit router (Sec. 2.3.1, ARLA; Fig.
+ * 4a), replacing the cosine signal at the gates of later dual decode steps
+ * with the exit settings on.  Weights are borrowed device pointers, read
+ * during the steps; block b of each array belongs to boundary b (1 <= b <
+ * n_layers; block 0 is not read):
+ *   wq, wk, wv: [n_layers][64][d_model] in the weight dtype, row-major;
+ *   w_out: [n_layers][64] float; b_out: [n_layers] float.
+ * At a gate b the fast states after the layers since the previous gate (or
+ * layer 0) through b-1 are scaled to unit RMS (no gain, the model's epsilon),
+ * projected to latent keys and values with boundary b's wk, wv; the state
+ * after layer b-1 also gives the query (wq).  Single-query softmax attention
+ * with scale 1/8 pools the values; the score is sigmoid(w_out . pooled +
+ * b_out), and the gate fires iff score >= tau.  A NULL `w` switches the
+ * router off.  Dense models, batch 1 (a decode step with batch > 1 and gates
+ * on fails with M2R2_E_UNSUPPORTED while the router is set).  Host-only. */
+typedef struct {
+  const void* wq;
+  const void* wk;
+  const void* wv;
+  const float* w_out;
+  const float* b_out;
+} m2r2_arla;
+
+M2R2_API m2r2_status m2r2_set_arla(m2r2_ctx* ctx, const m2r2_arla* w);
 
 /* Self-speculative draft (Sec. 2.3.2): gamma greedy tokens from the fast row
  * alone, run through layers 0..exit_layer-1 (a fast stream at rate

@@ -24,7 +24,8 @@ PROJ = ("q", "k", "v", "o", "g", "u", "d")
 EXPORTS = ("m2r2_workspace_size", "m2r2_create", "m2r2_destroy", "m2r2_decode_step", "m2r2_draft", "m2r2_verify",
            "m2r2_timing_enable", "m2r2_timing_read", "m2r2_time_gateup_layers", "m2r2_device_errors",
            "m2r2_last_error", "m2r2_expert_bytes", "m2r2_pack_expert", "m2r2_moe_set_policy", "m2r2_prefetch_experts",
-           "m2r2_moe_reset", "m2r2_moe_stats", "m2r2_expert_cache_replay", "m2r2_moe_set_preload_table")
+           "m2r2_moe_reset", "m2r2_moe_stats", "m2r2_expert_cache_replay", "m2r2_moe_set_preload_table",
+           "m2r2_set_arla")
 KERNEL_CLASSES = {"qkv": 0, "attn": 1, "oproj": 2, "gateup": 3, "down": 4, "head": 5, "embed": 6, "attn_merge": 7,
                   "expert_gateup": 8, "expert_down": 9, "router": 10}
 MOE_ON_DEMAND, MOE_AHEAD_OF_TIME, MOE_FIXED, MOE_RANDOM_PRELOAD, MOE_PREVIOUS_LAYER = 0, 1, 2, 3, 4
@@ -70,6 +71,10 @@ COUNTER_FIELDS = ("hits", "misses", "prefetch_issued", "prefetch_used", "prefetc
                   "pred_total", "h2d_bytes", "copy_waits", "host_wait_ns")
 
 
+class Arla(ctypes.Structure):
+    _fields_ = [("wq", c_void_p), ("wk", c_void_p), ("wv", c_void_p), ("w_out", c_void_p), ("b_out", c_void_p)]
+
+
 class MoeCounters(ctypes.Structure):
     _fields_ = [(f, _I64) for f in COUNTER_FIELDS] + [("layer_misses", _I64 * 128)]
 
@@ -110,6 +115,7 @@ def lib() -> ctypes.CDLL:
         L.m2r2_prefetch_experts.argtypes = [c_void_p, c_int32, POINTER(c_int32), c_int32, c_int32, c_void_p]
         L.m2r2_moe_reset.argtypes = [c_void_p]
         L.m2r2_moe_set_preload_table.argtypes = [c_void_p, c_void_p, c_int32]
+        L.m2r2_set_arla.argtypes = [c_void_p, c_void_p]
         L.m2r2_moe_stats.argtypes = [c_void_p, POINTER(MoeCounters)]
         L.m2r2_expert_cache_replay.argtypes = [c_int32, c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,
                                                c_int32, POINTER(MoeCounters)]
@@ -117,7 +123,7 @@ def lib() -> ctypes.CDLL:
                   "m2r2_timing_enable", "m2r2_timing_read", "m2r2_time_gateup_layers", "m2r2_device_errors",
                   "m2r2_expert_bytes",
                   "m2r2_pack_expert", "m2r2_moe_set_policy", "m2r2_prefetch_experts", "m2r2_moe_reset",
-                  "m2r2_moe_stats", "m2r2_expert_cache_replay", "m2r2_moe_set_preload_table"):
+                  "m2r2_moe_stats", "m2r2_expert_cache_replay", "m2r2_moe_set_preload_table", "m2r2_set_arla"):
             getattr(L, f).restype = c_int32
         _lib = L
     return _lib
@@ -398,6 +404,22 @@ class Model:
         if a.ndim != 3 or a.shape[1:] != (self.cfg.n_layers, self.cfg.top_k):
             raise ValueError(f"preload table of shape {a.shape}")
         _check(lib().m2r2_moe_set_preload_table(self._ctx, a.ctypes.data, a.shape[0]), "m2r2_moe_set_preload_table")
+
+    def set_arla(self, weights: Optional[dict]) -> None:
+        """Latent-attention exit router (``synth.arla_weights`` layout), or
+        None to return to the cosine signal.  The weights are copied to the
+        device and kept as long as the model."""
+        import torch
+        if weights is None:
+            _check(lib().m2r2_set_arla(self._ctx, None), "m2r2_set_arla")
+            return
+        wdt = torch.bfloat16 if self.cfg.wdtype == "bf16" else torch.float32
+        ts = {k: torch.from_numpy(np.ascontiguousarray(weights[k], dtype=np.float32)).to(
+            device=self.device, dtype=wdt if k in ("wq", "wk", "wv") else torch.float32) for k in
+            ("wq", "wk", "wv", "w_out", "b_out")}
+        self._arla = ts
+        a = Arla(*(ts[k].data_ptr() for k in ("wq", "wk", "wv", "w_out", "b_out")))
+        _check(lib().m2r2_set_arla(self._ctx, ctypes.byref(a)), "m2r2_set_arla")
 
     def moe_stats(self) -> dict:
         out = MoeCounters()

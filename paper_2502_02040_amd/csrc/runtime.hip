@@ -20,6 +20,7 @@
 #include "sk_kernels.h"
 #include "sk_attn.h"
 #include "rw_kernels.h"
+#include "arla.h"
 
 using namespace m2r2;
 
@@ -64,7 +65,7 @@ struct Layout {
   std::vector<size_t> lay_off;           // per layer: pq pk pv pa po pg pu pd (8 offsets)
   size_t lm;                             // packed LM head
   size_t X, PIN, QKV, O, ACT, bin_d, bin_o, bin_gu, uo, att, att_cnt, lm_val, lm_idx, lm_cnt, exited, exitb,
-      reinit, err, sig, rope, sk_part, sk_cnt, total;
+      reinit, err, sig, arla_kv, arla_q, arla_sig, arla_cnt, rope, sk_part, sk_cnt, total;
   // mixture of experts: router logits, choices, probabilities, activations,
   // and the expert cache ([n_layers][slots] slots of expert_stride bytes)
   size_t moe_logits, moe_sel, moe_prob, moe_act, moe_slots;
@@ -197,6 +198,10 @@ Layout make_layout(const m2r2_config& c, int max_batch, int max_chunk, int max_c
   L.reinit = take(sizeof(int) * c.n_layers * kMaxSeq);
   L.err = take(sizeof(int));
   L.sig = take(sizeof(float) * kMaxSeq * c.n_layers);
+  L.arla_kv = take(sizeof(float) * c.n_layers * 2 * kArlaDim);
+  L.arla_q = take(sizeof(float) * kArlaDim);
+  L.arla_sig = take(sizeof(float) * kMaxSeq);
+  L.arla_cnt = take(sizeof(uint32_t));
   L.rope = take(sizeof(float) * 2 * (size_t)max_ctx * (c.head_dim / 2));
   L.sk_slots = sk_slot_bound(c);
   L.sk_part = take(sizeof(float) * 64 * std::max<size_t>(L.sk_slots, 1));
@@ -304,6 +309,15 @@ struct m2r2_ctx {
   std::vector<hipEvent_t> ev;   // pairs
   int ev_used = 0;
   MoeState moe;
+  // latent-attention exit router weights (borrowed device pointers; on = set)
+  struct {
+    bool on = false;
+    const char* wq = nullptr;
+    const char* wk = nullptr;
+    const char* wv = nullptr;
+    const float* w_out = nullptr;
+    const float* b_out = nullptr;
+  } arla;
 };
 
 namespace {
@@ -420,6 +434,31 @@ M2R2_RW_LAUNCHER(kr_head)
 M2R2_RW_LAUNCHER_NW(kr_oproj)
 M2R2_RW_LAUNCHER_NW(kr_down)
 
+// Exit router after layer l (a one-sequence dual step with the router on):
+// latent key and value of the fast state for the next gate, and at the layer
+// before that gate the query and the score.
+bool host_is_gate(const StepIO& io, int b) {
+  if (b <= 0 || b >= 128) return false;
+  return b < 64 ? ((io.gate_mask_lo >> b) & 1ull) : ((io.gate_mask_hi >> (b - 64)) & 1ull);
+}
+
+template <int WB>
+hipError_t arla_after(m2r2_ctx* c, const StepIO& io, int l, hipStream_t st) {
+  if (!io.arla_sig) return hipSuccess;
+  const int N = c->D.n_layers;
+  int b = l + 1;
+  while (b < N && !host_is_gate(io, b)) ++b;
+  if (b >= N) return hipSuccess;   // no gate after this layer
+  int first = l;
+  while (first > 0 && !host_is_gate(io, first)) --first;
+  const size_t blk = (size_t)kArlaDim * c->D.d * (WB ? 2 : 4);
+  ArlaArgs a{c->arla.wq + b * blk, c->arla.wk + b * blk, c->arla.wv + b * blk, c->arla.w_out + (size_t)b * kArlaDim,
+             c->arla.b_out + b, 1, l, first, b == l + 1};
+  const int rows = (a.gate_now ? 3 : 2) * kArlaDim;
+  k_arla<WB><<<(rows + kArlaWaves - 1) / kArlaWaves, kArlaThreads, 0, st>>>(c->D, c->ws, a);
+  return hipGetLastError();
+}
+
 // One or two rows: row-per-wave GEMVs and the short-chain attention.
 template <int WB, int KB, int HD>
 m2r2_status run_layers_rw(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPtrs& kv, int n_layers_run,
@@ -443,6 +482,7 @@ m2r2_status run_layers_rw(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const
     TIMED(2, (kr_oproj_launch<WB>(nq, c->rw_nw[0], G, lds, st, D, L, rm, c->ws, io, l)));
     TIMED(3, (kr_gateup_launch<WB>(nd, G, lds, st, D, L, rm, c->ws, io, l)));
     TIMED(4, (kr_down_launch<WB>(nf, c->rw_nw[1], G, lds, st, D, L, rm, c->ws, io, l)));
+    HIP_TRY(arla_after<WB>(c, io, l, st));
   }
   TIMED(5, (kr_head_launch<WB>(nd, G, lds, st, D, c->lm_head_rm, c->final_norm, rm, c->ws, io, kv, c->skws,
                                 n_layers_run)));
@@ -475,6 +515,7 @@ m2r2_status run_layers_sk(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const
     TIMED(2, (ks_oproj<WB><<<G, kSkThreads, lq, st>>>(D, L, rm, c->ws, io, c->sk[1], sk, l)));
     TIMED(3, (ks_gateup<WB><<<G, kSkThreads, ld, st>>>(D, L, rm, c->ws, io, c->sk[2], sk, l)));
     TIMED(4, (ks_down<WB><<<G, kSkThreads, lf, st>>>(D, L, rm, c->ws, io, c->sk[3], sk, l)));
+    HIP_TRY(arla_after<WB>(c, io, l, st));
   }
   TIMED(5, (ks_head<WB><<<G, kSkThreads, ld, st>>>(D, c->lm_head, c->final_norm, rm, c->ws, io, kv, c->sk[4], sk,
                                                    n_layers_run)));
@@ -524,6 +565,7 @@ m2r2_status run_layers_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const 
     TIMED(2, (k_oproj<WB, MT><<<G.o, kGemvThreads, G.l_q, st>>>(D, L, rm, c->ws, io, l)));
     TIMED(3, (k_gateup<WB, MT><<<G.gu, kGemvThreads, G.l_d, st>>>(D, L, rm, c->ws, io, l)));
     TIMED(4, (k_down<WB, MT><<<G.o, kGemvThreads, G.l_f, st>>>(D, L, rm, c->ws, io, l)));
+    HIP_TRY(arla_after<WB>(c, io, l, st));
   }
   TIMED(5, (k_head<WB, MT><<<G.head, kGemvThreads, G.l_d, st>>>(D, c->lm_head, c->final_norm, rm, c->ws, io, kv,
                                                               c->lay.TV, n_layers_run)));
@@ -1070,6 +1112,8 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
   ws.lm_idx = (int*)(b + lay.lm_idx); ws.lm_cnt = (uint32_t*)(b + lay.lm_cnt); ws.exited = (int*)(b + lay.exited);
   ws.exitb = (int*)(b + lay.exitb); ws.reinit = (int*)(b + lay.reinit); ws.err = (int*)(b + lay.err);
   ws.sig = (float*)(b + lay.sig);
+  ws.arla_kv = (float*)(b + lay.arla_kv); ws.arla_q = (float*)(b + lay.arla_q);
+  ws.arla_sig = (float*)(b + lay.arla_sig); ws.arla_cnt = (uint32_t*)(b + lay.arla_cnt);
   ws.rope = (const float2*)(b + lay.rope);
   ws.rope_len = max_ctx;
   c->skws.part = (float*)(b + lay.sk_part);
@@ -1258,7 +1302,28 @@ M2R2_API m2r2_status m2r2_decode_step(m2r2_ctx* c, int32_t batch, int32_t dual, 
     if (batch != 1) return fail(M2R2_E_UNSUPPORTED, "mixture-of-experts decoding takes batch 1");
     return run_moe_pass(c, rm, io, kv_ptrs(kv), out, dual != 0, stream);
   }
+  if (c->arla.on && io.mode != EX_OFF && (io.gate_mask_lo | io.gate_mask_hi)) {
+    if (batch != 1) return fail(M2R2_E_UNSUPPORTED, "the latent-attention exit router takes batch 1");
+    io.arla_sig = c->ws.arla_sig;
+  }
   return run_pass(c, rm, io, kv_ptrs(kv), c->D.n_layers, stream);
+}
+
+M2R2_API m2r2_status m2r2_set_arla(m2r2_ctx* c, const m2r2_arla* w) {
+  if (!c) return fail(M2R2_E_INVALID, "ctx is NULL");
+  if (c->moe.on) return fail(M2R2_E_UNSUPPORTED, "the latent-attention exit router is for dense models");
+  if (!w) {
+    c->arla.on = false;
+    return M2R2_OK;
+  }
+  if (!w->wq || !w->wk || !w->wv || !w->w_out || !w->b_out) return fail(M2R2_E_INVALID, "NULL router weight");
+  c->arla.wq = (const char*)w->wq;
+  c->arla.wk = (const char*)w->wk;
+  c->arla.wv = (const char*)w->wv;
+  c->arla.w_out = w->w_out;
+  c->arla.b_out = w->b_out;
+  c->arla.on = true;
+  return M2R2_OK;
 }
 
 M2R2_API m2r2_status m2r2_draft(m2r2_ctx* c, const int32_t* last_token_d, const int32_t* positions_d,

@@ -467,6 +467,7 @@ __device__ __forceinline__ void sk_gate_logic(const Dims& D, const RowMap& rm, c
     if (layer > 0 && rm.fast[f]) {
       const float dot = ssum[f * 4 + 1], pin2 = ssum[f * 4 + 2], pp = ssum[f * 4 + 0];
       sg = dot * rsqrtf(fmaxf(pin2 * pp, 1e-30f));
+      if (io.arla_sig && is_gate(io, layer)) sg = io.arla_sig[s];
       if (!ex && io.mode != EX_OFF && is_gate(io, layer) && rm.slow_of[f] >= 0) {
         const bool fired = sg >= io.tau;
         if (fired && eb == D.n_layers) eb = layer;

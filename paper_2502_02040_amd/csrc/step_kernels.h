@@ -105,6 +105,10 @@ struct WS {
   int* reinit;     // [n_layers][16]
   int* err;        // sticky device error bits
   float* sig;      // [16][n_layers] scratch signal (copied to the caller's buffer if any)
+  float* arla_kv;  // [n_layers][2][64] latent keys and values of the fast states (exit router)
+  float* arla_q;   // [64] latent query at a gate
+  float* arla_sig; // [16] router score of the last gate
+  uint32_t* arla_cnt;   // arrival counter of the router kernel
   const float2* rope;  // [rope_len][hd/2] (cos, sin), built in double precision on the host
   int rope_len;
 };
@@ -149,6 +153,9 @@ struct StepIO {
   int mode;
   float tau;
   unsigned long long gate_mask_lo, gate_mask_hi;   // bit b: boundary b is a gate (b < 128)
+  // latent-attention exit router: score of the gate just passed, written by
+  // the router kernel after the layer before the gate (null: cosine signal)
+  const float* arla_sig;
 };
 
 __device__ __forceinline__ bool is_gate(const StepIO& io, int b) {
@@ -954,6 +961,7 @@ __device__ void gate_logic(const Dims& D, const RowMap& rm, const int* ex_in, co
     if (layer > 0 && rm.fast[f]) {
       const float dot = ssum[f * 4 + 1], pin2 = ssum[f * 4 + 2], pp = ssum[f * 4 + 0];
       sg = dot * rsqrtf(fmaxf(pin2 * pp, 1e-30f));
+      if (io.arla_sig && is_gate(io, layer)) sg = io.arla_sig[s];
       if (!ex && io.mode != EX_OFF && is_gate(io, layer) && rm.slow_of[f] >= 0) {
         const bool fired = sg >= io.tau;
         if (fired && eb == D.n_layers) eb = layer;

@@ -140,6 +140,51 @@ def test_phi3_exit_step(world):
     assert t.compared >= 2 or t.skipped
 
 
+def test_phi3_arla_exit_step(world):
+    """EXIT mode decided by the latent-attention exit router (Sec. 2.3.1) at
+    gates 8, 16 and 24 (intervals of eight fast states), bias 1.5 on the
+    last gate's readout so that some steps exit: boundary, token, signals of
+    the layers that ran and the skipped layers' cache entries."""
+    model, orc = world
+    N, tau, gates = CFG.n_layers, 0.7, [8, 16, 24]
+    a = synth.arla_weights(CFG)
+    a["b_out"][24] = 1.5
+    model.set_arla(a)
+    try:
+        t = Tally()
+        kv = PagedKV(CFG, 1, 64, block_size=16, block_table=shuffled_table(1, 64, 16, 4))
+        cache = KVCache(CFG, 64)
+        prompt = list(synth.prompt_ids(CFG, PROMPT, stream="arla"))
+        tok, pos_d = _prefill(model, orc, kv, cache, prompt, t)
+        dev = torch.device("cuda")
+        tok_d = torch.tensor([tok], dtype=torch.int32, device=dev)
+        nxt = torch.zeros(1, dtype=torch.int32, device=dev)
+        exb = torch.zeros(1, dtype=torch.int32, device=dev)
+        sig = torch.zeros(N, dtype=torch.float32, device=dev)
+        logits = torch.zeros(CFG.vocab, dtype=torch.float32, device=dev)
+        for step in range(3):
+            pos = PROMPT + step
+            model.decode_step(tok_d, pos_d, kv.desc(), gates=gates, tau=tau, mode="exit", next_token=nxt,
+                              exit_boundary=exb, signal=sig, logits=logits, advance=True)
+            torch.cuda.synchronize()
+            r = orc.decode_step(int(tok_d.item()), pos, cache, gates=gates, tau=tau, mode="exit", arla=a)
+            if any(abs(r.signal[b - 1] - tau) <= 2e-3 for b in gates if b <= r.exit_boundary):
+                t.skipped += 1
+                break
+            assert int(exb.item()) == r.exit_boundary, f"step {step} exit boundary"
+            ran = list(range(min(r.exit_boundary, N)))
+            got = sig.cpu().numpy()
+            assert np.max(np.abs(got[ran] - r.signal[ran])) <= TOL, f"step {step} signal"
+            t.rel(logits.cpu().numpy(), r.logits, TOL, f"step {step} logits")
+            t.token(int(nxt.item()), r.logits, TOL, f"step {step} token")
+            skipped = [l for l in (r.exit_boundary, N - 1) if l < N]
+            _check_cache(kv, cache, 0, pos, pos + 1, t, sorted(set([0] + skipped)), f"step {step}")
+            tok_d.copy_(nxt)
+        assert t.compared >= 2 or t.skipped
+    finally:
+        model.set_arla(None)
+
+
 def _oracle_draft_logits(orc, token, pos, cache, exit_layer, gamma):
     """The oracle's draft (Sec. 2.3.2) with the logits of every draft position."""
     cfg = orc.cfg

@@ -18,10 +18,12 @@ pytestmark = pytest.mark.gpu
 CASES = ["tiny", "small_bf16"]
 
 
-def _decode_run(name, *, mode, tau, gates, n_steps, adapter_scale=1.0, block_size=16, prompt_len=16):
+def _decode_run(name, *, mode, tau, gates, n_steps, adapter_scale=1.0, block_size=16, prompt_len=16, arla=None):
     cfg = synth.CONFIGS[name]
     w = synth.make_weights(cfg, adapter_scale=adapter_scale)
     pair = Pair(cfg, w, max_ctx=prompt_len + n_steps + 8, block_size=block_size, table_seed=3)
+    if arla is not None:
+        pair.model.set_arla(arla)
     t = Tally()
     prompt = list(synth.prompt_ids(cfg, prompt_len))
     tok = pair.prefill(prompt, tally=t)
@@ -42,7 +44,8 @@ def _decode_run(name, *, mode, tau, gates, n_steps, adapter_scale=1.0, block_siz
         pair.model.decode_step(tok_d, pos_d, pair.kv.desc(), gates=gates, tau=tau, mode=mode, next_token=nxt,
                                exit_boundary=exb, signal=sig, logits=logits, h_out=h_out, p_out=p_out, advance=True)
         torch.cuda.synchronize()
-        r = pair.orc.decode_step(int(tok_d.item()), pos, pair.caches[0], gates=gates, tau=tau, mode=mode)
+        r = pair.orc.decode_step(int(tok_d.item()), pos, pair.caches[0], gates=gates, tau=tau, mode=mode,
+                                 arla=arla)
         assert int(pos_d.item()) == pos + 1 and int(pair.kv.seq_lens[0].item()) == pos + 1
         got_sig = sig.cpu().numpy()
         ambiguous = any(abs(r.signal[b - 1] - tau) <= pair.tol for b in gates if b - 1 < N)
@@ -81,6 +84,59 @@ def test_dual_step_exit(name, tau):
     t, exits = _decode_run(name, mode="exit", tau=tau, gates=[1], n_steps=8)
     if tau < 0:
         assert exits == 8
+
+
+def _arla(name, bias=0.0):
+    cfg = synth.CONFIGS[name]
+    a = synth.arla_weights(cfg)
+    a["b_out"][:] = bias
+    return a
+
+
+@pytest.mark.parametrize("name", CASES)
+def test_arla_signal_observe(name):
+    """Latent-attention exit router (Sec. 2.3.1): in OBSERVE mode with gates
+    at the last boundary only (small_bf16: an interval of two layers), the
+    router score at the gate and every other signal match the oracle."""
+    cfg = synth.CONFIGS[name]
+    t, _ = _decode_run(name, mode="observe", tau=0.5, gates=[cfg.n_layers - 1], n_steps=6, arla=_arla(name))
+    assert t.compared >= 3
+
+
+@pytest.mark.parametrize("name", CASES)
+@pytest.mark.parametrize("bias", [-40.0, 40.0, 0.0])
+def test_arla_exit(name, bias):
+    """EXIT mode decided by the router at every interior boundary: a large
+    bias forces (or forbids) the exit at the first gate; bias 0 leaves it to
+    the latent attention."""
+    cfg = synth.CONFIGS[name]
+    gates = list(range(1, cfg.n_layers))
+    t, exits = _decode_run(name, mode="exit", tau=0.5, gates=gates, n_steps=5, arla=_arla(name, bias))
+    if bias > 0:
+        assert exits == 5
+    if bias < 0:
+        assert exits == 0
+
+
+def test_arla_switched_off_restores_cosine_signal():
+    cfg = synth.CONFIGS["tiny"]
+    w = synth.make_weights(cfg)
+    pair = Pair(cfg, w, max_ctx=32, table_seed=3)
+    pair.model.set_arla(_arla("tiny", 40.0))
+    pair.model.set_arla(None)
+    t = Tally()
+    tok = pair.prefill(list(synth.prompt_ids(cfg, 8)), tally=t)
+    dev = pair.dev
+    nxt = torch.zeros(1, dtype=torch.int32, device=dev)
+    exb = torch.zeros(1, dtype=torch.int32, device=dev)
+    sig = torch.zeros(cfg.n_layers, dtype=torch.float32, device=dev)
+    pos_d = torch.tensor([8], dtype=torch.int32, device=dev)
+    pair.model.decode_step(torch.tensor([tok], dtype=torch.int32, device=dev), pos_d, pair.kv.desc(), gates=[1],
+                           tau=2.0, mode="exit", next_token=nxt, exit_boundary=exb, signal=sig, advance=True)
+    torch.cuda.synchronize()
+    r = pair.orc.decode_step(tok, 8, pair.caches[0], gates=[1], tau=2.0, mode="exit")
+    assert int(exb.item()) == cfg.n_layers == r.exit_boundary
+    assert abs(float(sig[0]) - r.signal[0]) <= pair.tol
 
 
 def test_zero_adapters_fast_row_tracks_slow_row():
