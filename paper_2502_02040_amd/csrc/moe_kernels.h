@@ -75,37 +75,61 @@ constexpr int kHostWords = 64;
 // host memory, then `seq` with release semantics at system scope.
 __global__ __launch_bounds__(256) void k_topk(int E, int K, const float* logits, int route, int n_pred, MoePtrs mp,
                                               WS ws, int* slow_out, int* pred_out, int seq) {
-  __shared__ float z[3][kMaxExperts];
   __shared__ int chosen[3][kMaxTopK];
   __shared__ float pr[kMaxTopK];
   const bool exited = ws.exited[0] != 0;
   if (exited) { route = 0; n_pred = 0; }
-  for (int e = threadIdx.x; e < 3 * E; e += 256) z[e / E][e % E] = logits[e];
-  __syncthreads();
-  if (threadIdx.x < 3) {
-    const int t = threadIdx.x;
+  // wave t takes task t; lane l holds experts l, l+64, l+128, l+192
+  constexpr int J = kMaxExperts / 64;
+  const int lane = threadIdx.x & 63, t = threadIdx.x >> 6;
+  if (t < 3) {
     const bool active = t == 0 ? route != 0 : (t - 1) < n_pred;
     if (active) {
-      float mx = -INFINITY;
-      for (int e = 0; e < E; ++e) mx = fmaxf(mx, z[t][e]);
-      float sum = 0.f;
-      if (t == 0)
-        for (int e = 0; e < E; ++e) sum += __expf(z[t][e] - mx);
-      // selection by repeated arg-max (ties to the lower id); E and K are small
-      unsigned long long taken[kMaxExperts / 64] = {};
-      for (int k = 0; k < K; ++k) {
-        int bi = -1;
-        float bz = -INFINITY;
-        for (int e = 0; e < E; ++e) {
-          if ((taken[e >> 6] >> (e & 63)) & 1ull) continue;
-          if (bi < 0 || z[t][e] > bz) { bz = z[t][e]; bi = e; }
-        }
-        taken[bi >> 6] |= 1ull << (bi & 63);
-        chosen[t][k] = bi;
-        if (t == 0) pr[k] = __expf(bz - mx) / sum;
+      float v[J];
+#pragma unroll
+      for (int j = 0; j < J; ++j) v[j] = lane + 64 * j < E ? logits[t * E + lane + 64 * j] : -INFINITY;
+      float lm = v[0];
+#pragma unroll
+      for (int j = 1; j < J; ++j) lm = fmaxf(lm, v[j]);
+      const float mx = wave_max(lm);
+      float sum = 1.f;
+      if (t == 0) {
+        float se = 0.f;
+#pragma unroll
+        for (int j = 0; j < J; ++j)
+          if (lane + 64 * j < E) se += __expf(v[j] - mx);
+        sum = wave_sum(se);
       }
-    } else {
-      for (int k = 0; k < K; ++k) chosen[t][k] = -1;
+      // K rounds of a wave-wide arg-max (larger logit, then lower id)
+      unsigned taken = 0;
+      for (int k = 0; k < K; ++k) {
+        float bv = -INFINITY;
+        int bi = 0x7fffffff;
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+          const int e = lane + 64 * j;
+          if (e < E && !((taken >> j) & 1u) && (v[j] > bv || (v[j] == bv && e < bi))) {
+            bv = v[j];
+            bi = e;
+          }
+        }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) {
+          const float ov = __shfl_xor(bv, off);
+          const int oi = __shfl_xor(bi, off);
+          if (ov > bv || (ov == bv && oi < bi)) {
+            bv = ov;
+            bi = oi;
+          }
+        }
+        if ((bi & 63) == lane) taken |= 1u << (bi >> 6);
+        if (lane == 0) {
+          chosen[t][k] = bi;
+          if (t == 0) pr[k] = __expf(bv - mx) / sum;
+        }
+      }
+    } else if (lane < K) {
+      chosen[t][lane] = -1;
     }
   }
   __syncthreads();
