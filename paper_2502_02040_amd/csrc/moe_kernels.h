@@ -51,7 +51,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_router(Dims D, int E, RouterTa
   if (threadIdx.x == 0) {
     xrow_s[0] = ws.X + (size_t)T.row * D.d;
     float a = 0.f;
-    for (int b = 0; b < kBins; ++b)
+    for (int b = 0; b < kBinSlots; ++b)
       a += T.stat_kind == 0 ? bin_o_at(ws, D, T.stat_layer, b, T.row)[0] : bin_d_at(ws, T.stat_layer, b, T.row)[0];
     inv_rms = rsqrtf(a / D.d + D.eps);
   }
@@ -166,7 +166,7 @@ __global__ __launch_bounds__(256) void k_fast_mlp(Dims D, RowMap rm, LayerPtrs L
     const bool ex = ws.exited[rm.seq[m]] != 0;
     if (threadIdx.x < D.r) {
       float a = 0.f, ss = 0.f;
-      for (int b = 0; b < kBins; ++b) {
+      for (int b = 0; b < kBinSlots; ++b) {
         a += bin_o_at(ws, D, layer, b, m)[1 + threadIdx.x];
         ss += bin_o_at(ws, D, layer, b, m)[0];
       }
@@ -235,7 +235,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_moe_gateup(Dims D, int Fe, int
   if (threadIdx.x == 0) {
     xrow_s[0] = ws.X + (size_t)slow_row * D.d;
     float a = 0.f;
-    for (int b = 0; b < kBins; ++b) a += bin_o_at(ws, D, layer, b, slow_row)[0];
+    for (int b = 0; b < kBinSlots; ++b) a += bin_o_at(ws, D, layer, b, slow_row)[0];
     inv_rms = rsqrtf(a / D.d + D.eps);
   }
   __syncthreads();

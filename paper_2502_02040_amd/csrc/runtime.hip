@@ -695,7 +695,11 @@ hipError_t rw_set_lds(int bytes) {
 hipError_t sk_setup(m2r2_ctx* c) {
   c->sk_on = false;
   const m2r2_config& cf = c->cfg;
-  if (is_moe(cf)) return hipSuccess;
+  // a mixture-of-experts model uses the row-per-wave q/k/v and o projections,
+  // the short-chain attention and the row-per-wave head (its MLP has kernels
+  // of its own); the stream-K GEMVs, whose partial slots its layout does not
+  // hold, stay off
+  const bool moe = is_moe(cf);
   const char* env = getenv("M2R2_STREAMK");
   if (env && env[0] == '0') return hipSuccess;
   int dev = 0, cus = 0;
@@ -705,11 +709,12 @@ hipError_t sk_setup(m2r2_ctx* c) {
   const int W = kSkWaves * cus;
   sk_plans(cf, W, c->sk);
   bool ok = true;
-  for (const SkPlan& p : c->sk)
-    ok = ok && p.nblk >= 8 && p.smax <= kSkMaxSeg && (p.L + p.nblk - 1) / p.nblk + 1 <= 64 &&
-         (size_t)p.ntiles * p.smax <= c->lay.sk_slots;
+  if (!moe)
+    for (const SkPlan& p : c->sk)
+      ok = ok && p.nblk >= 8 && p.smax <= kSkMaxSeg && (p.L + p.nblk - 1) / p.nblk + 1 <= 64 &&
+           (size_t)p.ntiles * p.smax <= c->lay.sk_slots;
   const Dims& D = c->D;
-  const int K = std::max({D.d, D.qdim, D.F});
+  const int K = moe ? std::max(D.d, D.qdim) : std::max({D.d, D.qdim, D.F});
   ok = ok && K <= kSkMaxK && sk_lds(K) <= 160 * 1024;
   const size_t tb = (size_t)16 * D.d * (D.wbf16 ? 2 : 4), tq = (size_t)(D.qdim / 16) * tb;
   for (const LayerPtrs& L : c->layers)
@@ -719,7 +724,7 @@ hipError_t sk_setup(m2r2_ctx* c) {
   if (!ok) return hipSuccess;
   e = D.wbf16 ? sk_set_lds<1>((int)sk_lds(K)) : sk_set_lds<0>((int)sk_lds(K));
   if (e == hipSuccess) {
-    c->sk_on = true;
+    c->sk_on = !moe;
     c->sk_grid = cus;
     // attention of the stream-K path: fixed 128-token splits over the cache
     // capacity (at most 64, within the workspace's partial slots), the head's
@@ -740,7 +745,7 @@ hipError_t sk_setup(m2r2_ctx* c) {
     const int Ks[3] = {D.d, D.qdim, D.F};
     bool ok_r = c->sk_attn_S > 0 && (D.r * wsz) % 16 == 0 && D.r * wsz <= kRwMaxBRowBytes &&
                 !getenv_zero("M2R2_ROWWAVE");
-    for (int i = 0; i < 3; ++i) {
+    for (int i = 0; i < (moe ? 2 : 3); ++i) {
       c->rw_nch[i] = Ks[i] / epp;
       ok_r = ok_r && Ks[i] % epp == 0 && rw_nch_ok(c->rw_nch[i]) && Ks[i] <= kSkMaxK;
     }
@@ -845,9 +850,17 @@ m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVP
   std::vector<int> pslots, pexperts;
   for (int l = 0; l < D.n_layers; ++l) {
     const LayerPtrs& L = c->layers[l];
-    TIMED(0, (k_qkv<WB, MT><<<G.qkv, kGemvThreads, G.l_d, st>>>(D, L, rm, c->ws, io, l)));
-    TIMED(1, (k_attn<KB, HD><<<dim3(S + 1, D.H, 1), kAttnThreads, smem, st>>>(D, L, rm, c->ws, io, kv, l, S)));
-    TIMED(2, (k_oproj<WB, MT><<<G.o, kGemvThreads, G.l_q, st>>>(D, L, rm, c->ws, io, l)));
+    if (c->rw_on) {
+      TIMED(0, (kr_qkv_launch<WB>(c->rw_nch[0], c->sk_grid, (size_t)kSkMinLds, st, D, L, rm, c->ws, io, l)));
+      TIMED(1, (ks_attn<WB, KB, HD><<<dim3(c->sk_attn_S, D.H, rm.nseq), kSkAttnThreads,
+                                       sk_attn_lds_bytes(HD, D.r, WB), st>>>(D, L, rm, c->ws, io, kv, l, c->sk_attn_S)));
+      TIMED(2, (kr_oproj_launch<WB>(c->rw_nch[1], c->rw_nw[0], c->sk_grid, (size_t)kSkMinLds, st, D, L, rm, c->ws,
+                                    io, l)));
+    } else {
+      TIMED(0, (k_qkv<WB, MT><<<G.qkv, kGemvThreads, G.l_d, st>>>(D, L, rm, c->ws, io, l)));
+      TIMED(1, (k_attn<KB, HD><<<dim3(S + 1, D.H, 1), kAttnThreads, smem, st>>>(D, L, rm, c->ws, io, kv, l, S)));
+      TIMED(2, (k_oproj<WB, MT><<<G.o, kGemvThreads, G.l_q, st>>>(D, L, rm, c->ws, io, l)));
+    }
     if (dual) TIMED(10, (k_fast_mlp<<<(D.d + 255) / 256, 256, 0, st>>>(D, rm, L, l, c->ws)));
     // routing of the slow row, predictions for layers 2l+2 and 2l+3 from the fast row
     RouterTask t[3] = {};
@@ -922,8 +935,12 @@ m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVP
     if (prev && n_pred) HIP_TRY(preload(l + 1, M.host_words + kMaxTopK));
     if (random_row && l + 1 < D.n_layers) HIP_TRY(preload(l + 1, random_row + (l + 1) * M.K));
   }
-  TIMED(5, (k_head<WB, MT><<<G.head, kGemvThreads, G.l_d, st>>>(D, c->lm_head, c->final_norm, rm, c->ws, io, kv,
-                                                              c->lay.TV, D.n_layers)));
+  if (c->rw_on)
+    TIMED(5, (kr_head_launch<WB>(c->rw_nch[0], c->sk_grid, (size_t)kSkMinLds, st, D, c->lm_head_rm, c->final_norm, rm,
+                                  c->ws, io, kv, c->skws, D.n_layers)));
+  else
+    TIMED(5, (k_head<WB, MT><<<G.head, kGemvThreads, G.l_d, st>>>(D, c->lm_head, c->final_norm, rm, c->ws, io, kv,
+                                                                c->lay.TV, D.n_layers)));
   HIP_TRY(hipGetLastError());
   M.pol.end_token();
   ++M.token;

@@ -7,8 +7,11 @@ counters, under each of the five placement strategies, against the oracle's
 cache simulations replayed on the GPU's own routing trace.
 
 Sizes: a bfloat16 model with 6 layers, d 256, 2 heads x 128, 16 experts of
-width 96, top-4 (caches of 5 and 16 slots), and a float32 model with 5
-layers, d 128, 2 heads x 64, 8 experts of width 64, top-2."""
+width 96, top-4 (caches of 5 and 16 slots), a float32 model with 5 layers,
+d 128, 2 heads x 64, 8 experts of width 64, top-2 (both on the tile GEMVs),
+and a bfloat16 model with 4 layers, d 512, 4 heads x 128, rank 8 (rows of
+whole 1 KB pieces: the row-per-wave q/k/v, o and head kernels and the
+short-chain attention)."""
 import numpy as np
 import pytest
 import torch
@@ -140,7 +143,8 @@ class MoePair:
         return t, slow_tr, pred_tr, outs
 
 
-@pytest.mark.parametrize("name,slots", [("small_moe", 5), ("small_moe", 16), ("small_moe_f32", 3)])
+@pytest.mark.parametrize("name,slots", [("small_moe", 5), ("small_moe", 16), ("small_moe_f32", 3),
+                                        ("small_moe_rw", 6)])
 def test_moe_dual_step_observe(name, slots):
     cfg = synth.CONFIGS[name]
     p = MoePair(name, slots=slots)
@@ -148,8 +152,9 @@ def test_moe_dual_step_observe(name, slots):
     assert t.compared >= 12
 
 
-def test_moe_exit_mode_fills_skipped_layers():
-    p = MoePair("small_moe_f32", slots=4)
+@pytest.mark.parametrize("name", ["small_moe_f32", "small_moe_rw"])
+def test_moe_exit_mode_fills_skipped_layers(name):
+    p = MoePair(name, slots=4)
     t, slow_tr, _, _ = p.run(6, mode="exit", gates=[2], tau=-1.0)
     assert t.compared >= 4
     assert all(np.all(s[2:] == -1) for s in slow_tr)
