@@ -388,7 +388,8 @@ M2R2_API m2r2_status m2r2_time_gateup_layers(m2r2_ctx* ctx, int32_t dual, hipStr
 
 /* Sticky device error bits set by kernels since the context was created
  * (1: token id out of range, 2: cache position outside the block table,
- * 4: context longer than the workspace was sized for); waits for `stream`. */
+ * 4: context longer than the workspace was sized for, 8: a position beyond
+ * the RoPE table, i.e. at or past max_ctx); waits for `stream`. */
 M2R2_API m2r2_status m2r2_device_errors(m2r2_ctx* ctx, hipStream_t stream, int32_t* bits);
 
 /* Description of the last error on this thread ("" if none). */

@@ -59,3 +59,6 @@ def test_null_arguments_are_rejected():
     cfg = binding.make_config(synth.CONFIGS["tiny"])
     out = ctypes.c_void_p()
     assert lib.m2r2_create(ctypes.byref(cfg), None, 1, 16, 128, None, 0, ctypes.byref(out)) == -1
+    assert lib.m2r2_set_arla(None, None) == -1
+    assert lib.m2r2_moe_set_policy(None, 0) == -1
+    assert lib.m2r2_moe_set_preload_table(None, None, 1) == -1

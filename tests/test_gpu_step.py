@@ -18,10 +18,11 @@ pytestmark = pytest.mark.gpu
 CASES = ["tiny", "small_bf16"]
 
 
-def _decode_run(name, *, mode, tau, gates, n_steps, adapter_scale=1.0, block_size=16, prompt_len=16, arla=None):
+def _decode_run(name, *, mode, tau, gates, n_steps, adapter_scale=1.0, block_size=16, prompt_len=16, arla=None,
+                max_ctx=None):
     cfg = synth.CONFIGS[name]
     w = synth.make_weights(cfg, adapter_scale=adapter_scale)
-    pair = Pair(cfg, w, max_ctx=prompt_len + n_steps + 8, block_size=block_size, table_seed=3)
+    pair = Pair(cfg, w, max_ctx=max_ctx or prompt_len + n_steps + 8, block_size=block_size, table_seed=3)
     if arla is not None:
         pair.model.set_arla(arla)
     t = Tally()
@@ -137,6 +138,14 @@ def test_arla_switched_off_restores_cosine_signal():
     r = pair.orc.decode_step(tok, 8, pair.caches[0], gates=[1], tau=2.0, mode="exit")
     assert int(exb.item()) == cfg.n_layers == r.exit_boundary
     assert abs(float(sig[0]) - r.signal[0]) <= pair.tol
+
+
+@pytest.mark.parametrize("name", CASES)
+def test_decode_to_cache_capacity(name):
+    """The last steps fill the cache exactly: positions 250..255 of a 256-slot
+    cache (two 128-token attention splits, the last block's last slot)."""
+    t, _ = _decode_run(name, mode="observe", tau=0.9, gates=[1], n_steps=6, prompt_len=250, max_ctx=256)
+    assert t.compared >= 3
 
 
 def test_zero_adapters_fast_row_tracks_slow_row():
