@@ -143,12 +143,17 @@ __global__ __launch_bounds__(256) void k_topk(int E, int K, const float* logits,
       if (t > 0 && pred_out) pred_out[(t - 1) * K + k] = chosen[t][k];
     }
   }
-  if (threadIdx.x == 0 && mp.sel_host) {
-    for (int i = 0; i < 3 * K; ++i)
+  if (mp.sel_host) {
+    // one word per thread, then the sequence number with release semantics
+    const int i = threadIdx.x;
+    if (i < 3 * K)
       __hip_atomic_store(&mp.sel_host[(i / K) * kMaxTopK + i % K], chosen[i / K][i % K], __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_SYSTEM);
-    __hip_atomic_store(&mp.sel_host[kHostExited], exited ? 1 : 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-    __hip_atomic_store(&mp.sel_host[kHostSeq], seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+    else if (i == 3 * K)
+      __hip_atomic_store(&mp.sel_host[kHostExited], exited ? 1 : 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    __threadfence_system();
+    __syncthreads();
+    if (i == 0) __hip_atomic_store(&mp.sel_host[kHostSeq], seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
   }
 }
 
@@ -214,11 +219,53 @@ struct ExpertSlots {
   const void* w[kMaxTopK];   // start of the expert: gate [F_e][d], up [F_e][d], down [d][F_e], each packed
 };
 
+// Device-side slot resolution: slot_tab[layer][expert] is the HBM cache slot
+// whose copy of the expert is complete, or -1.  The host keeps it in stream
+// order: an evicted expert is cleared before any later launch can read it, a
+// newly copied one is published only once its copy has completed.
+struct SlotTable {
+  const int* tab;      // [n_layers][E]
+  const char* slots;   // [n_layers][C][stride]
+  size_t stride;
+  int E, C;
+};
+
+// Slot lookup from the table: lane k of every wave gets the slot of chosen
+// expert k (two dependent loads).  False, for every workgroup alike, when the
+// sequence has exited or a chosen expert is not published; the host then
+// launches the kernels again with its own addresses.
+__device__ __forceinline__ bool spec_slot(const SlotTable& t, const MoePtrs& mp, const WS& ws, int layer, int K,
+                                          int& slot) {
+  const int lane = threadIdx.x & 63;
+  const int ex = ws.exited[0];
+  const int e = lane < K ? mp.sel[lane] : 0;
+  slot = lane < K ? ((e >= 0 && e < t.E) ? t.tab[(size_t)layer * t.E + e] : -1) : 0;
+  return !ex && !__any(lane < K && (slot < 0 || slot >= t.C));
+}
+__device__ __forceinline__ const char* slot_addr(const SlotTable& t, int layer, int slot) {
+  return t.slots + ((size_t)layer * t.C + slot) * t.stride;
+}
+
+// Kernel: table entries idx[i] = val[i], i < n (one launch per batch of host
+// decisions, in stream order).
+struct TabUpdates {
+  int n;
+  int idx[30];
+  int val[30];
+};
+__global__ __launch_bounds__(64) void k_tab_set(int* tab, TabUpdates u) {
+  if ((int)threadIdx.x < u.n) tab[u.idx[threadIdx.x]] = u.val[threadIdx.x];
+}
+
 // Kernel: gate/up of the chosen experts for the slow row, SwiGLU, times the
 // router probability.  grid = K * F_e/16, block = 512.
-template <int WB>
+template <int WB, bool SPEC = false>
 __global__ __launch_bounds__(kGemvThreads) void k_moe_gateup(Dims D, int Fe, int K, ExpertSlots es, int slow_row,
-                                                             const float* mlp_norm, int layer, MoePtrs mp, WS ws) {
+                                                             const float* mlp_norm, int layer, MoePtrs mp, WS ws,
+                                                             SlotTable stab) {
+  int sslot = 0;
+  if constexpr (SPEC)
+    if (!spec_slot(stab, mp, ws, layer, K, sslot)) return;
   __shared__ float red[kGemvWaves * 512];
   __shared__ float y[512];
   __shared__ const float* xrow_s[kMaxRows];
@@ -227,7 +274,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_moe_gateup(Dims D, int Fe, int
   const int tiles = Fe / 16;
   const int k = blockIdx.x / tiles, t = blockIdx.x % tiles;
   const size_t esz = WB ? 2 : 4;
-  const char* base = (const char*)es.w[k];
+  const char* base = SPEC ? slot_addr(stab, layer, __shfl(sslot, k)) : (const char*)es.w[k];
   const size_t mat = (size_t)Fe * D.d * esz;
   const void* wrow[2] = {base + (size_t)t * 16 * D.d * esz, base + mat + (size_t)t * 16 * D.d * esz};
   GemvWave<WB, 2, 2, true> gw;
@@ -252,9 +299,12 @@ __global__ __launch_bounds__(kGemvThreads) void k_moe_gateup(Dims D, int Fe, int
 // (the K experts' matrices form one reduction of length K*F_e over the
 // probability-weighted activations), then the slow row's partial sums for the
 // next layer's norm.  grid = d/16, block = 512.
-template <int WB>
+template <int WB, bool SPEC = false>
 __global__ __launch_bounds__(kGemvThreads) void k_moe_down(Dims D, int Fe, int K, ExpertSlots es, int slow_row,
-                                                           int layer, MoePtrs mp, WS ws) {
+                                                           int layer, MoePtrs mp, WS ws, SlotTable stab) {
+  int sslot = 0;
+  if constexpr (SPEC)
+    if (!spec_slot(stab, mp, ws, layer, K, sslot)) return;
   __shared__ float red[kGemvWaves * 256];
   __shared__ float y[256];
   __shared__ float newx[16];
@@ -264,8 +314,9 @@ __global__ __launch_bounds__(kGemvThreads) void k_moe_down(Dims D, int Fe, int K
   const int n0 = blockIdx.x * 16;
   const size_t esz = WB ? 2 : 4;
   const size_t mat = (size_t)Fe * D.d * esz;
-  if (threadIdx.x < K)
-    segs[threadIdx.x] = (const char*)es.w[threadIdx.x] + 2 * mat + (size_t)blockIdx.x * 16 * Fe * esz;
+  if (threadIdx.x < K)   // lanes of the first wave: lane k holds expert k's slot
+    segs[threadIdx.x] = (SPEC ? slot_addr(stab, layer, sslot) : (const char*)es.w[threadIdx.x]) + 2 * mat +
+                        (size_t)blockIdx.x * 16 * Fe * esz;
   if (threadIdx.x == 0) xrow_s[0] = mp.act;
   __syncthreads();
   GemvWave<WB, 1, 2, false> gw;

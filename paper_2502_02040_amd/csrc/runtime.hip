@@ -68,7 +68,7 @@ struct Layout {
       reinit, err, sig, arla_kv, arla_q, arla_sig, arla_cnt, rope, sk_part, sk_cnt, total;
   // mixture of experts: router logits, choices, probabilities, activations,
   // and the expert cache ([n_layers][slots] slots of expert_stride bytes)
-  size_t moe_logits, moe_sel, moe_prob, moe_act, moe_slots;
+  size_t moe_logits, moe_sel, moe_prob, moe_act, moe_slots, moe_tab;
   size_t expert_bytes, expert_stride;
   int TD, TF, TV, S_max;
   size_t sk_slots;                       // partial-sum slots of the stream-K GEMVs
@@ -214,6 +214,7 @@ Layout make_layout(const m2r2_config& c, int max_batch, int max_chunk, int max_c
     L.expert_bytes = expert_bytes_of(c);
     L.expert_stride = (L.expert_bytes + 255) & ~(size_t)255;
     L.moe_slots = take(L.expert_stride * c.n_layers * c.expert_slots);
+    L.moe_tab = take(sizeof(int) * c.n_layers * c.n_experts);
   }
   L.total = off;
   return L;
@@ -280,6 +281,15 @@ struct MoeState {
   std::vector<char> layer_done_rec;
   hipStream_t copy_demand = nullptr, copy_ahead = nullptr;
   int64_t h2d_bytes = 0, copy_waits = 0, host_wait_ns = 0;
+  // device-side slot resolution: the expert kernels are launched right after
+  // the routing kernels and read the slots from tab_d; the host launches them
+  // again with its own slots only when a chosen expert is not published there
+  bool spec = true;
+  int* tab_d = nullptr;             // [n_layers][E] slot of a completed copy, or -1
+  std::vector<int> tab;             // tab_d once every enqueued update has run
+  std::vector<int> tab_idx, tab_val;   // updates still to enqueue
+  struct Pending { int l, slot, e; };
+  std::vector<Pending> pend;        // copies published once they are complete
 };
 
 struct m2r2_ctx {
@@ -822,6 +832,59 @@ m2r2_status wait_routing(m2r2_ctx* c, int seq, hipStream_t st) {
   return M2R2_OK;
 }
 
+// ---- the device slot table ----
+void tab_put(MoeState& M, int l, int e, int slot) {
+  if (!M.spec) return;
+  const int i = l * M.E + e;
+  if (M.tab[i] == slot) return;
+  M.tab[i] = slot;
+  M.tab_idx.push_back(i);
+  M.tab_val.push_back(slot);
+}
+
+// The expert held in `slot` of layer l (if published) is about to be replaced.
+void tab_evict_slot(MoeState& M, int l, int slot) {
+  for (int e = 0; e < M.E; ++e)
+    if (M.tab[l * M.E + e] == slot) tab_put(M, l, e, -1);
+}
+
+// Publish the copies that have completed (and still hold their expert).
+void tab_publish_done(MoeState& M) {
+  size_t keep = 0;
+  for (size_t j = 0; j < M.pend.size(); ++j) {
+    const MoeState::Pending p = M.pend[j];
+    const int i = p.l * M.C + p.slot;
+    if (M.pol.layer(p.l).expert_in[p.slot] != p.e) continue;   // replaced since: drop
+    if (M.slot_pending[i]) {
+      if (hipEventQuery(M.slot_ev[i]) != hipSuccess) {
+        M.pend[keep++] = p;
+        continue;
+      }
+      M.slot_pending[i] = 0;
+    }
+    tab_put(M, p.l, p.e, p.slot);
+  }
+  M.pend.resize(keep);
+}
+
+hipError_t tab_flush(m2r2_ctx* c, hipStream_t st) {
+  MoeState& M = c->moe;
+  for (size_t j0 = 0; j0 < M.tab_idx.size(); j0 += 30) {
+    TabUpdates u{};
+    u.n = (int)std::min<size_t>(30, M.tab_idx.size() - j0);
+    for (int j = 0; j < u.n; ++j) {
+      u.idx[j] = M.tab_idx[j0 + j];
+      u.val[j] = M.tab_val[j0 + j];
+    }
+    k_tab_set<<<1, 64, 0, st>>>(M.tab_d, u);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  M.tab_idx.clear();
+  M.tab_val.clear();
+  return hipSuccess;
+}
+
 // Dual-stream (or slow-only) pass of a mixture-of-experts model, batch 1:
 // rows 0 (slow) and 1 (fast).
 template <int WB, int KB, int HD>
@@ -881,6 +944,20 @@ m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVP
     const int seq = ++M.seq;
     TIMED(10, (k_topk<<<1, 256, 0, st>>>(M.E, M.K, logits, 1, n_pred, M.mp, c->ws, slow_out, pred_out, seq)));
     HIP_TRY(hipGetLastError());
+    const SlotTable stab{M.tab_d, M.slots_d, M.stride, M.E, M.C};
+    if (M.spec) {
+      // the experts from the slots the table publishes, without waiting for
+      // the host (they return at once if a chosen expert is not published)
+      tab_publish_done(M);
+      HIP_TRY(tab_flush(c, st));
+      TIMED(8, (k_moe_gateup<WB, true><<<M.K * (M.Fe / 16), kGemvThreads, gl, st>>>(D, M.Fe, M.K, ExpertSlots{}, 0,
+                                                                                   L.mlp_norm, l, M.mp, c->ws, stab)));
+      TIMED(9, (k_moe_down<WB, true><<<c->lay.TD, kGemvThreads, gl, st>>>(D, M.Fe, M.K, ExpertSlots{}, 0, l, M.mp,
+                                                                         c->ws, stab)));
+      HIP_TRY(hipGetLastError());
+      HIP_TRY(hipEventRecord(M.layer_done[l], st));
+      M.layer_done_rec[l] = 1;
+    }
     if (m2r2_status s = wait_routing(c, seq, st)) return s;
     if (M.host_words[kHostExited]) {   // exited: no MLP for the remaining layers
       TIMED(10, (k_row_stats<<<1, 256, 0, st>>>(D, 0, l + 1, c->ws)));
@@ -897,8 +974,15 @@ m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVP
       M.pol.use_fixed(l, need, M.K, slot, load);
     else
       M.pol.use(l, need, M.K, slot, load);
+    // did the launches above find every chosen expert in its slot?
+    bool done = M.spec;
+    for (int k = 0; k < M.K && done; ++k) done = M.tab[l * M.E + need[k]] == slot[k];
+    if (!done) {
     for (int k = 0; k < M.K; ++k)
-      if (load[k]) HIP_TRY(moe_copy(c, l, slot[k], need[k], M.copy_demand));
+      if (load[k]) {
+        tab_evict_slot(M, l, slot[k]);
+        HIP_TRY(moe_copy(c, l, slot[k], need[k], M.copy_demand));
+      }
     ExpertSlots es{};
     for (int k = 0; k < M.K; ++k) {
       const int i = l * M.C + slot[k];
@@ -916,18 +1000,26 @@ m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVP
       es.w[k] = M.slots_d + (size_t)i * M.stride;
     }
     TIMED(8, (k_moe_gateup<WB><<<M.K * (M.Fe / 16), kGemvThreads, gl, st>>>(D, M.Fe, M.K, es, 0, L.mlp_norm, l, M.mp,
-                                                                           c->ws)));
-    TIMED(9, (k_moe_down<WB><<<c->lay.TD, kGemvThreads, gl, st>>>(D, M.Fe, M.K, es, 0, l, M.mp, c->ws)));
+                                                                           c->ws, stab)));
+    TIMED(9, (k_moe_down<WB><<<c->lay.TD, kGemvThreads, gl, st>>>(D, M.Fe, M.K, es, 0, l, M.mp, c->ws, stab)));
     HIP_TRY(hipGetLastError());
     HIP_TRY(hipEventRecord(M.layer_done[l], st));
     M.layer_done_rec[l] = 1;
+    // the copies above are complete for every later launch on `st`
+    if (!fixed)
+      for (int k = 0; k < M.K; ++k)
+        if (load[k]) tab_put(M, l, need[k], slot[k]);
+    }
     auto preload = [&](int lp, const int* ids) -> hipError_t {
       pslots.clear();
       pexperts.clear();
       M.pol.predict(lp, ids, M.K, &pslots, &pexperts);
       hipError_t r = hipSuccess;
-      for (size_t q = 0; q < pslots.size() && r == hipSuccess; ++q)
+      for (size_t q = 0; q < pslots.size() && r == hipSuccess; ++q) {
+        tab_evict_slot(M, lp, pslots[q]);
         r = moe_copy(c, lp, pslots[q], pexperts[q], M.copy_ahead);
+        if (M.spec) M.pend.push_back({lp, pslots[q], pexperts[q]});
+      }
       return r;
     };
     if (ahead)
@@ -976,7 +1068,8 @@ template <int WB>
 hipError_t set_moe_lds_limits() {
   const int bytes = gemv_lds_bytes(WB, 2);
   hipError_t e = hipSuccess;
-  const void* fns[] = {(const void*)k_router<WB>, (const void*)k_moe_gateup<WB>, (const void*)k_moe_down<WB>};
+  const void* fns[] = {(const void*)k_router<WB>, (const void*)k_moe_gateup<WB>, (const void*)k_moe_down<WB>,
+                       (const void*)k_moe_gateup<WB, true>, (const void*)k_moe_down<WB, true>};
   for (const void* f : fns) {
     hipError_t r = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
     if (r != hipSuccess) e = r;
@@ -999,6 +1092,16 @@ hipError_t moe_warm(m2r2_ctx* c) {
   std::fill(M.layer_done_rec.begin(), M.layer_done_rec.end(), 0);
   M.h2d_bytes = M.copy_waits = M.host_wait_ns = 0;
   M.token = 0;
+  // the slot table: the warm experts, except that the fixed-experts policy
+  // publishes only the ones it keeps (the last top_k slots are its staging)
+  const int n_pub = M.policy == M2R2_MOE_FIXED ? M.C - M.K : M.C;
+  M.tab.assign((size_t)c->D.n_layers * M.E, -1);
+  for (int l = 0; l < c->D.n_layers; ++l)
+    for (int s = 0; s < n_pub; ++s) M.tab[(size_t)l * M.E + s] = s;
+  M.tab_idx.clear();
+  M.tab_val.clear();
+  M.pend.clear();
+  if (e == hipSuccess) e = hipMemcpy(M.tab_d, M.tab.data(), sizeof(int) * M.tab.size(), hipMemcpyHostToDevice);
   return e;
 }
 
@@ -1164,6 +1267,7 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
     M.stride = lay.expert_stride;
     M.store_h = (const char*)w->experts_h;
     M.slots_d = b + lay.moe_slots;
+    M.tab_d = (int*)(b + lay.moe_tab);
     M.mp.logits = (const float*)(b + lay.moe_logits);
     M.mp.sel = (int*)(b + lay.moe_sel);
     M.mp.prob = (float*)(b + lay.moe_prob);
@@ -1189,6 +1293,7 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
     M.slot_pending.assign(n_ev, 0);
     M.layer_done_rec.assign(cfg->n_layers, 0);
     M.pol.init(cfg->n_layers, M.E, M.C);
+    M.spec = !getenv_zero("M2R2_MOE_DEVICE_SLOTS");
     if (e == hipSuccess) e = set_moe_lds_limits<0>();
     if (e == hipSuccess) e = set_moe_lds_limits<1>();
     if (e == hipSuccess) e = moe_warm(c);
@@ -1469,7 +1574,11 @@ M2R2_API m2r2_status m2r2_prefetch_experts(m2r2_ctx* c, int32_t layer, const int
   hipStream_t cs = copy_stream ? copy_stream : (priority ? M.copy_demand : M.copy_ahead);
   std::vector<int> slots, experts;
   M.pol.predict(layer, ids_h, n, &slots, &experts);
-  for (size_t q = 0; q < slots.size(); ++q) HIP_TRY(moe_copy(c, layer, slots[q], experts[q], cs));
+  for (size_t q = 0; q < slots.size(); ++q) {
+    tab_evict_slot(M, layer, slots[q]);
+    HIP_TRY(moe_copy(c, layer, slots[q], experts[q], cs));
+    if (M.spec) M.pend.push_back({layer, slots[q], experts[q]});
+  }
   return M2R2_OK;
 }
 

@@ -225,3 +225,28 @@ def test_external_prefetch_makes_experts_resident():
     assert st["prefetch_issued"] == 3 and st["loads"] == 3
     p.model.prefetch_experts(3, [9, 10, 11], priority=True)   # already resident: refreshed, no copy
     assert p.model.moe_stats()["loads"] == 3
+
+
+@pytest.mark.parametrize("name", ["small_moe", "small_moe_rw"])
+@pytest.mark.parametrize("policy", ["on_demand", "ahead_of_time", "fixed", "previous_layer"])
+def test_device_slot_table_matches_host_slots(name, policy, monkeypatch):
+    """Expert kernels that read their slots from the device table (launched
+    before the host has seen the routing) give the same routing, predictions
+    and cache counters, and the same logits, as kernels launched by the host
+    with its own slots after every routing decision.  (The logits are equal
+    to float rounding: the row-per-wave kernels add their row statistics
+    with atomics, whose order varies from run to run.)"""
+    w = synth.make_weights(synth.CONFIGS[name])
+    monkeypatch.setenv("M2R2_MOE_DEVICE_SLOTS", "0")
+    a = MoePair(name, slots=5, weights=w, policy=policy)
+    _, sa, pa, oa = a.run(10, check=False)
+    monkeypatch.delenv("M2R2_MOE_DEVICE_SLOTS")
+    b = MoePair(name, slots=5, weights=w, policy=policy)
+    _, sb, pb, ob = b.run(10, check=False)
+    for i in range(10):
+        np.testing.assert_array_equal(sa[i], sb[i])
+        np.testing.assert_array_equal(pa[i], pb[i])
+        np.testing.assert_allclose(oa[i], ob[i], rtol=1e-4, atol=1e-4 * np.max(np.abs(oa[i])))
+    ga, gb = a.model.moe_stats(), b.model.moe_stats()
+    for f in FIELDS + ("h2d_bytes", "layer_misses"):
+        assert ga[f] == gb[f], f
