@@ -72,7 +72,7 @@ typedef enum {
   M2R2_E_NOMEM = -4,        /* workspace smaller than m2r2_workspace_size() */
   M2R2_E_HIP = -5,          /* a HIP runtime call failed */
   M2R2_E_STATE = -6,        /* call not valid in the context's current state */
-  M2R2_E_UNSUPPORTED = -7   /* valid request this build does not implement */
+  M2R2_E_UNSUPPORTED = -7   /* valid request the library does not implement */
 } m2r2_status;
 
 typedef enum { M2R2_F32 = 0, M2R2_BF16 = 1 } m2r2_dtype;
