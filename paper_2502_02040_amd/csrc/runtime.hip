@@ -88,8 +88,11 @@ size_t expert_bytes_of(const m2r2_config& c) {
 // index [wb][row class 0: 2 rows, 1: 16 rows][kernel 0 qkv, 1 o, 2 gate/up,
 // 3 down, 4 head].
 struct Resident {
-  int n[2][2][5];
+  int n[2][3][5];
 };
+
+// Row classes of the tile GEMVs: up to 2, 8 or 16 activation rows staged.
+constexpr int row_class(int mt) { return mt <= 2 ? 0 : (mt <= 8 ? 2 : 1); }
 
 // ---- stream-K GEMV plans ----------------------------------------------------
 constexpr int kSkMaxWaves = 8 * 320;   // partial slots are sized for up to 320 compute units
@@ -385,7 +388,7 @@ struct Grids {
 template <int WB, int MT>
 Grids grids(const m2r2_ctx* c) {
   const Dims& D = c->D;
-  const int* cap = c->resident.n[WB][MT <= 2 ? 0 : 1];
+  const int* cap = c->resident.n[WB][row_class(MT)];
   Grids g;
   g.qkv = std::min(3 * (D.qdim / 16) + (3 * D.r + 15) / 16, cap[0]);
   g.o = std::min(D.d / 16, std::min(cap[1], cap[3]));
@@ -586,6 +589,9 @@ m2r2_status run_layers_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const 
 template <int WB, int KB, int HD>
 m2r2_status run_mt(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPtrs& kv, int nl, hipStream_t st) {
   if (rm.M <= 2) return run_layers_t<WB, KB, HD, 2>(c, rm, io, kv, nl, st);
+  // up to 8 rows (a verification chunk of up to 7 drafts, a prefill tail):
+  // half the activation rows to stage per tile
+  if (rm.M <= 8) return run_layers_t<WB, KB, HD, 8>(c, rm, io, kv, nl, st);
   return run_layers_t<WB, KB, HD, 16>(c, rm, io, kv, nl, st);
 }
 
@@ -659,7 +665,7 @@ hipError_t set_lds_limits(const m2r2_config& c, Resident& res) {
     int per_cu = 0;
     if (e == hipSuccess)
       e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fns[i], kGemvThreads, tile_lds_bytes(WB, MT, kk[i]));
-    res.n[WB][MT <= 2 ? 0 : 1][i] = std::max(1, per_cu) * std::max(1, cus);
+    res.n[WB][row_class(MT)][i] = std::max(1, per_cu) * std::max(1, cus);
   }
   return e;
 }
@@ -1256,6 +1262,8 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
   if (e == hipSuccess) e = pack_all(c, w, workspace);
   if (e == hipSuccess) e = set_lds_limits<0, 2>(*cfg, c->resident);
   if (e == hipSuccess) e = set_lds_limits<1, 2>(*cfg, c->resident);
+  if (e == hipSuccess) e = set_lds_limits<0, 8>(*cfg, c->resident);
+  if (e == hipSuccess) e = set_lds_limits<1, 8>(*cfg, c->resident);
   if (e == hipSuccess) e = set_lds_limits<0, 16>(*cfg, c->resident);
   if (e == hipSuccess) e = set_lds_limits<1, 16>(*cfg, c->resident);
   if (e == hipSuccess) e = sk_setup(c);
