@@ -234,18 +234,18 @@ def test_draft_and_verify(name, gamma, exit_layer):
 
 
 @pytest.mark.parametrize("name", CASES)
-@pytest.mark.parametrize("chunks", ["1", "2"])
-def test_batched_dual_step(name, chunks, monkeypatch):
-    """Three sequences with different context lengths decoded together
-    (two rows each: the batched short-chain attention with one or two
-    128-token chunks per split, and the 16-row GEMVs): every sequence's
-    logits, h, p, signal, token and cache entry match the oracle step by
-    step."""
+@pytest.mark.parametrize("chunks,B", [("1", 3), ("2", 3), ("1", 8)])
+def test_batched_dual_step(name, chunks, B, monkeypatch):
+    """Three (eight) sequences with different context lengths decoded
+    together (two rows each: the batched short-chain attention with one or
+    two 128-token chunks per split, and the 8-row (16-row) tile GEMVs): every
+    sequence's logits, h, p, signal, token and cache entry match the oracle
+    step by step."""
     monkeypatch.setenv("M2R2_ATTN_CHUNKS", chunks)
     cfg = synth.CONFIGS[name]
     w = synth.make_weights(cfg)
-    B, n_steps = 3, 4
-    lens = [5, 19, 37]
+    n_steps = 4
+    lens = [5, 19, 37, 2, 11, 30, 8, 23][:B]
     pair = Pair(cfg, w, max_ctx=64, table_seed=5, max_batch=B, n_seqs=B)
     t = Tally()
     toks = [pair.prefill(list(synth.prompt_ids(cfg, n, stream=f"b{s}")), seq=s, tally=t) for s, n in enumerate(lens)]
