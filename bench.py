@@ -183,6 +183,15 @@ def cpu_baseline(cfg, weights, ctx: int, budget_s: float):
 # shared helpers
 # ----------------------------------------------------------------------------
 
+def dense_capacity(ctx: int, warmup: int, steps: int, kernel_reps: int) -> int:
+    """Cache capacity (max_ctx) of the dense and exit runs: room for the
+    decoded tokens, rounded up to a multiple of 512 past the prompt, so that
+    runs of different lengths share one launch configuration (the parity test
+    of the benched configuration builds its model with this capacity)."""
+    need = ctx + warmup + steps + 2 * kernel_reps + 32
+    return max(ctx + 512, (need + 511) // 512 * 512)
+
+
 def _progress(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -248,8 +257,7 @@ def run_dense(args) -> int:
     dev = torch.device("cuda:0")
     t_setup = time.perf_counter()
     weights = synth.make_weights(cfg)
-    n_inst = 2 * args.kernel_reps
-    max_ctx = args.ctx + args.warmup + args.steps + n_inst + 32
+    max_ctx = dense_capacity(args.ctx, args.warmup, args.steps, args.kernel_reps)
     model = Model(cfg, weights, max_batch=1, max_chunk=16, max_ctx=max_ctx)
     _progress(f"dense: model ready after {time.perf_counter() - t_setup:.1f} s")
     bps = (max_ctx + 15) // 16

@@ -359,38 +359,21 @@ M2R2_API m2r2_status m2r2_expert_cache_replay(int32_t n_layers, int32_t n_expert
                                               int32_t n_tokens, const int32_t* slow_h, const int32_t* pred_h,
                                               int32_t policy, m2r2_moe_counters* out);
 
-/* Kernel timing for measurement.  Kernel classes of one decode pass:
- * 0 qkv, 1 attention, 2 output projection, 3 gate/up, 4 down, 5 LM head,
- * 6 embedding, 7 attention merge, 8 expert gate/up, 9 expert down, 10
- * router and top-k.  m2r2_timing_enable(ctx, k) starts a new record: every
- * launch of class k made by later calls is bracketed by a pair of HIP events
- * recorded on the call's stream (up to 1024 launches; record with direct
- * launches: events recorded inside a captured graph cannot be timed).
- * m2r2_timing_read waits for the recorded events and returns the summed
- * kernel milliseconds and the launch count of the record.  k = -1 stops
- * recording.  Events are host-side objects created by the library (no device
- * memory). */
-M2R2_API m2r2_status m2r2_timing_enable(m2r2_ctx* ctx, int32_t kernel_class);
-M2R2_API m2r2_status m2r2_timing_read(m2r2_ctx* ctx, double* ms_sum, int32_t* launches);
-
-/* Average duration of one gate/up launch (kernel class 3) of the
- * one-sequence decode step (two rows when `dual`, one otherwise): the kernel
- * of every layer is launched back to back on `stream` between one pair of HIP
- * events (which keeps the events' own latency out of the per-launch figure;
- * each layer streams its own weights, as in a step), and *avg_ms receives the
- * elapsed time divided by the layer count.  Waits for `stream`.  Side
- * effects: the workspace's SwiGLU activations and the gate/up row statistics
- * (zeroed at the start of every pass) are overwritten; the residual stream,
- * the cache and the positions are not touched.  Returns M2R2_E_UNSUPPORTED
- * when the one- and two-row decode class does not use the row-per-wave
- * kernels (for example a mixture-of-experts model). */
-M2R2_API m2r2_status m2r2_time_gateup_layers(m2r2_ctx* ctx, int32_t dual, hipStream_t stream, double* avg_ms);
-
 /* Sticky device error bits set by kernels since the context was created
  * (1: token id out of range, 2: cache position outside the block table,
  * 4: context longer than the workspace was sized for, 8: a position beyond
  * the RoPE table, i.e. at or past max_ctx); waits for `stream`. */
 M2R2_API m2r2_status m2r2_device_errors(m2r2_ctx* ctx, hipStream_t stream, int32_t* bits);
+
+/* Report the asynchronous errors of the work enqueued so far: waits for
+ * `stream`, then returns M2R2_E_HIP if the stream or an earlier launch
+ * failed (the HIP error in m2r2_last_error()), M2R2_E_STATE if a kernel set
+ * one of the sticky device error bits above (the bits in m2r2_last_error()),
+ * else M2R2_OK.  Entry points check their arguments before they enqueue
+ * anything and report launch failures at once; a fault or a device-side
+ * range violation inside a kernel can only be seen here (or by the next
+ * call's launch).  The error bits stay set once seen. */
+M2R2_API m2r2_status m2r2_sync_check(m2r2_ctx* ctx, hipStream_t stream);
 
 /* Description of the last error on this thread ("" if none). */
 M2R2_API const char* m2r2_last_error(void);

@@ -21,11 +21,14 @@ EXIT_OFF, EXIT_OBSERVE, EXIT_EXIT = 0, 1, 2
 MODES = {"off": EXIT_OFF, "observe": EXIT_OBSERVE, "exit": EXIT_EXIT}
 PROJ = ("q", "k", "v", "o", "g", "u", "d")
 
+# include/m2r2.h: the decode path's boundary
 EXPORTS = ("m2r2_workspace_size", "m2r2_create", "m2r2_destroy", "m2r2_decode_step", "m2r2_draft", "m2r2_verify",
-           "m2r2_timing_enable", "m2r2_timing_read", "m2r2_time_gateup_layers", "m2r2_device_errors",
+           "m2r2_device_errors", "m2r2_sync_check",
            "m2r2_last_error", "m2r2_expert_bytes", "m2r2_pack_expert", "m2r2_moe_set_policy", "m2r2_prefetch_experts",
            "m2r2_moe_reset", "m2r2_moe_stats", "m2r2_expert_cache_replay", "m2r2_moe_set_preload_table",
            "m2r2_set_arla")
+# include/m2r2_measure.h: measurement hooks
+MEASURE_EXPORTS = ("m2r2_timing_enable", "m2r2_timing_read", "m2r2_time_gateup_layers")
 KERNEL_CLASSES = {"qkv": 0, "attn": 1, "oproj": 2, "gateup": 3, "down": 4, "head": 5, "embed": 6, "attn_merge": 7,
                   "expert_gateup": 8, "expert_down": 9, "router": 10}
 MOE_ON_DEMAND, MOE_AHEAD_OF_TIME, MOE_FIXED, MOE_RANDOM_PRELOAD, MOE_PREVIOUS_LAYER = 0, 1, 2, 3, 4
@@ -108,6 +111,7 @@ def lib() -> ctypes.CDLL:
         L.m2r2_timing_read.argtypes = [c_void_p, POINTER(ctypes.c_double), POINTER(c_int32)]
         L.m2r2_time_gateup_layers.argtypes = [c_void_p, c_int32, c_void_p, POINTER(ctypes.c_double)]
         L.m2r2_device_errors.argtypes = [c_void_p, c_void_p, POINTER(c_int32)]
+        L.m2r2_sync_check.argtypes = [c_void_p, c_void_p]
         L.m2r2_last_error.restype = ctypes.c_char_p
         L.m2r2_expert_bytes.argtypes = [POINTER(Config), POINTER(c_size_t)]
         L.m2r2_pack_expert.argtypes = [POINTER(Config), c_void_p, c_void_p, c_void_p, c_void_p]
@@ -121,7 +125,7 @@ def lib() -> ctypes.CDLL:
                                                c_int32, POINTER(MoeCounters)]
         for f in ("m2r2_workspace_size", "m2r2_create", "m2r2_decode_step", "m2r2_draft", "m2r2_verify",
                   "m2r2_timing_enable", "m2r2_timing_read", "m2r2_time_gateup_layers", "m2r2_device_errors",
-                  "m2r2_expert_bytes",
+                  "m2r2_sync_check", "m2r2_expert_bytes",
                   "m2r2_pack_expert", "m2r2_moe_set_policy", "m2r2_prefetch_experts", "m2r2_moe_reset",
                   "m2r2_moe_stats", "m2r2_expert_cache_replay", "m2r2_moe_set_preload_table", "m2r2_set_arla"):
             getattr(L, f).restype = c_int32
@@ -425,6 +429,10 @@ class Model:
         out = MoeCounters()
         _check(lib().m2r2_moe_stats(self._ctx, ctypes.byref(out)), "m2r2_moe_stats")
         return out.as_dict(self.cfg.n_layers)
+
+    def sync_check(self, stream=None) -> None:
+        """Raise M2R2Error if the enqueued work failed or set a device error bit."""
+        _check(lib().m2r2_sync_check(self._ctx, _stream(stream)), "m2r2_sync_check")
 
     def device_errors(self, stream=None) -> int:
         bits = c_int32(0)

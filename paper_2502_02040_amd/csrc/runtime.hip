@@ -15,6 +15,7 @@
 
 #include "expert_cache.h"
 #include "m2r2.h"
+#include "m2r2_measure.h"
 #include "moe_kernels.h"
 #include "step_kernels.h"
 #include "sk_kernels.h"
@@ -1381,6 +1382,18 @@ M2R2_API m2r2_status m2r2_device_errors(m2r2_ctx* c, hipStream_t stream, int32_t
   if (!c || !bits) return fail(M2R2_E_INVALID, "NULL argument");
   HIP_TRY(hipMemcpyAsync(bits, c->ws.err, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
   HIP_TRY(hipStreamSynchronize(stream));
+  return M2R2_OK;
+}
+
+M2R2_API m2r2_status m2r2_sync_check(m2r2_ctx* c, hipStream_t stream) {
+  if (!c) return fail(M2R2_E_INVALID, "ctx is NULL");
+  hipError_t e = hipStreamSynchronize(stream);
+  if (e == hipSuccess) e = hipGetLastError();
+  if (e != hipSuccess) return fail(M2R2_E_HIP, "asynchronous error: %s", hipGetErrorString(e));
+  int32_t bits = 0;
+  HIP_TRY(hipMemcpyAsync(&bits, c->ws.err, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
+  HIP_TRY(hipStreamSynchronize(stream));
+  if (bits) return fail(M2R2_E_STATE, "device error bits %#x", (unsigned)bits);
   return M2R2_OK;
 }
 

@@ -13,13 +13,30 @@ from paper_2502_02040_amd import binding
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-def _declared():
-    src = open(os.path.join(ROOT, "include", "m2r2.h")).read()
-    return set(re.findall(r"M2R2_API\s+[\w\s\*]+?\b(m2r2_\w+)\s*\(", src))
+def _declared(header=None):
+    """Entry points declared in include/<header> (every header if None)."""
+    names = set()
+    for h in ([header] if header else sorted(os.listdir(os.path.join(ROOT, "include")))):
+        if h.endswith(".h"):
+            src = open(os.path.join(ROOT, "include", h)).read()
+            names |= set(re.findall(r"M2R2_API\s+[\w\s\*]+?\b(m2r2_\w+)\s*\(", src))
+    return names
+
+
+# the calls the decode path's boundary is built around: create/destroy and
+# the workspace size, one decode step, the draft, the verification, the
+# expert prefetch, and the error reporting
+CORE = {"m2r2_workspace_size", "m2r2_create", "m2r2_destroy", "m2r2_decode_step", "m2r2_draft", "m2r2_verify",
+        "m2r2_prefetch_experts", "m2r2_last_error", "m2r2_sync_check"}
+# declared extensions of the boundary (each with its reason in the header)
+EXTENSIONS = {"m2r2_device_errors", "m2r2_expert_bytes", "m2r2_pack_expert", "m2r2_moe_set_policy",
+              "m2r2_moe_reset", "m2r2_moe_stats", "m2r2_expert_cache_replay", "m2r2_moe_set_preload_table",
+              "m2r2_set_arla"}
 
 
 def test_header_declarations_match_binding():
-    assert _declared() == set(binding.EXPORTS)
+    assert _declared("m2r2.h") == set(binding.EXPORTS) == CORE | EXTENSIONS
+    assert _declared("m2r2_measure.h") == set(binding.MEASURE_EXPORTS)
 
 
 def test_library_exports_every_declared_symbol():
@@ -62,3 +79,4 @@ def test_null_arguments_are_rejected():
     assert lib.m2r2_set_arla(None, None) == -1
     assert lib.m2r2_moe_set_policy(None, 0) == -1
     assert lib.m2r2_moe_set_preload_table(None, None, 1) == -1
+    assert lib.m2r2_sync_check(None, None) == -1

@@ -3,8 +3,10 @@
 through the C ABI and in the launch configuration bench.py times, against the
 float64 oracle on sampled outputs:
 
-  * the dual-stream step at batch 1 (OBSERVE gates at every boundary), and
-    in EXIT mode (the token from the fast row at the first gate whose signal
+  * the dual-stream step at batch 1 (OBSERVE gates at every boundary) after
+    a 16-token prompt, and at context 1024 (seeded synthetic cache content)
+    in the cache capacity the benchmark uses, so the attention runs with the
+    same splits as in the timed step; and in EXIT mode (the token from the fast row at the first gate whose signal
     reaches tau, the skipped layers' cache filled from the slow row);
   * a draft of 4 tokens from the fast stream exiting at layer 8 and the
     verification of the 5-token chunk;
@@ -20,7 +22,7 @@ import synth
 from oracle import KVCache, Oracle
 from oracle.decoder import argmax_first, round_to_cache
 from paper_2502_02040_amd import Model, PagedKV
-from tests.gpu_harness import Tally, shuffled_table
+from tests.gpu_harness import Tally, oracle_draft_logits, pick_tau, shuffled_table, track
 
 pytestmark = pytest.mark.gpu
 
@@ -33,10 +35,9 @@ CTX_B = 4096
 @pytest.fixture(scope="module")
 def world():
     w = synth.make_weights(CFG)
-    model = Model(CFG, w, max_batch=8, max_chunk=16, max_ctx=CTX_B + 16)
+    model = track(Model(CFG, w, max_batch=8, max_chunk=16, max_ctx=CTX_B + 16))
     orc = Oracle(CFG, w)
-    del w
-    yield model, orc
+    yield model, orc, w
     del model, orc
     torch.cuda.empty_cache()
 
@@ -63,7 +64,7 @@ def _check_cache(kv, cache, seq, start, end, t, layers, what):
 
 
 def test_phi3_dual_step(world):
-    model, orc = world
+    model, orc, _ = world
     t = Tally()
     kv = PagedKV(CFG, 1, 64, block_size=16, block_table=shuffled_table(1, 64, 16, 7))
     cache = KVCache(CFG, 64)
@@ -86,23 +87,92 @@ def test_phi3_dual_step(world):
                           exit_boundary=exb, signal=sig, logits=logits, h_out=h_out, p_out=p_out, advance=True)
         torch.cuda.synchronize()
         r = orc.decode_step(int(tok_d.item()), pos, cache, gates=gates, tau=0.9, mode="observe")
-        t.rel(logits.cpu().numpy(), r.logits, TOL, f"step {step} logits")
-        t.rel(h_out.cpu().numpy(), r.h, TOL, f"step {step} h")
-        t.rel(p_out.cpu().numpy(), r.p, TOL, f"step {step} p")
-        assert np.max(np.abs(sig.cpu().numpy() - r.signal)) <= TOL, f"step {step} signal"
-        if all(abs(r.signal[b - 1] - 0.9) > TOL for b in gates):
-            assert int(exb.item()) == r.exit_boundary
-        t.token(int(nxt.item()), r.logits, TOL, f"step {step} token")
+        _compare_observe_step(t, r, logits, h_out, p_out, sig, exb, nxt, gates, 0.9, step)
         _check_cache(kv, cache, 0, pos, pos + 1, t, (0, 7, 31), f"step {step}")
+        t.steps += 1
         tok_d.copy_(nxt)
-    assert t.compared >= 5
+    assert t.steps == 3 and t.compared >= 5
+
+
+def _compare_observe_step(t, r, logits, h_out, p_out, sig, exb, nxt, gates, tau, step):
+    """Outputs of an OBSERVE step (which do not depend on the gate
+    decisions); the exit boundary where every gate signal decides it."""
+    t.rel(logits.cpu().numpy(), r.logits, TOL, f"step {step} logits")
+    t.rel(h_out.cpu().numpy(), r.h, TOL, f"step {step} h")
+    t.rel(p_out.cpu().numpy(), r.p, TOL, f"step {step} p")
+    t.close(sig.cpu().numpy(), r.signal, TOL, f"step {step} signal")
+    if all(abs(r.signal[b - 1] - tau) > TOL for b in gates):
+        t.equal(int(exb.item()), r.exit_boundary, f"step {step} exit boundary")
+    else:
+        t.skipped += 1
+    t.token(int(nxt.item()), r.logits, TOL, f"step {step} token")
+
+
+def test_phi3_dual_step_bench_context(world):
+    """The benchmarked configuration: batch 1, context 1024 (seeded N(0,1)
+    cache content, shuffled block table), the cache capacity bench.py uses
+    (the attention then runs with the splits of the timed step, the context
+    spread over all of them), three OBSERVE dual-stream steps."""
+    from bench import dense_capacity
+    _, orc, w = world
+    ctx = 1024
+    cap = dense_capacity(ctx, 5, 20, 20)
+    assert cap == dense_capacity(ctx, 10, 256, 20)   # the default run shares it
+    model = track(Model(CFG, w, max_batch=1, max_chunk=16, max_ctx=cap))
+    try:
+        t = Tally()
+        kv = PagedKV(CFG, 1, cap, block_size=16, block_table=shuffled_table(1, cap, 16, 11))
+        cache = KVCache(CFG, cap)
+        content = synth.synthetic_kv(CFG, ctx, seq=0, threads=16)
+        for l, (K, V) in content.items():
+            kv.load(0, l, K, V)
+            cache.load(l, K, V)
+        del content
+        kv.seq_lens.fill_(ctx)
+        dev = torch.device("cuda")
+        N = CFG.n_layers
+        gates = list(range(1, N))
+        tok_d = torch.tensor(synth.prompt_ids(CFG, 1, stream="benchctx"), dtype=torch.int32, device=dev)
+        pos_d = torch.full((1,), ctx, dtype=torch.int32, device=dev)
+        nxt = torch.zeros(1, dtype=torch.int32, device=dev)
+        exb = torch.zeros(1, dtype=torch.int32, device=dev)
+        sig = torch.zeros(N, dtype=torch.float32, device=dev)
+        logits = torch.zeros(CFG.vocab, dtype=torch.float32, device=dev)
+        h_out = torch.zeros(CFG.d_model, dtype=torch.float32, device=dev)
+        p_out = torch.zeros(CFG.d_model, dtype=torch.float32, device=dev)
+        for step in range(3):
+            pos = ctx + step
+            model.decode_step(tok_d, pos_d, kv.desc(), gates=gates, tau=0.9, mode="observe", next_token=nxt,
+                              exit_boundary=exb, signal=sig, logits=logits, h_out=h_out, p_out=p_out, advance=True)
+            torch.cuda.synchronize()
+            r = orc.decode_step(int(tok_d.item()), pos, cache, gates=gates, tau=0.9, mode="observe")
+            assert int(pos_d.item()) == pos + 1 and int(kv.seq_lens[0].item()) == pos + 1
+            _compare_observe_step(t, r, logits, h_out, p_out, sig, exb, nxt, gates, 0.9, step)
+            _check_cache(kv, cache, 0, pos, pos + 1, t, (0, 13, 31), f"step {step}")
+            t.steps += 1
+            tok_d.copy_(nxt)
+        # per step: logits, h, p, signals and 6 cache slabs element by element;
+        # the token and the exit boundary compared or counted as near ties
+        assert t.steps == 3 and t.arrays >= 30 and t.compared + t.skipped == 6
+        assert model.device_errors() == 0
+    finally:
+        del model
+        torch.cuda.empty_cache()
+
+
+# EXIT-mode thresholds, in order of preference, and the window around a gate
+# signal inside which a threshold is not used: the measured signal errors
+# are below 1e-3, so a decision further than 2e-3 from tau is taken alike
+EXIT_TAUS = (0.95, 0.945, 0.955, 0.94, 0.96, 0.935, 0.965, 0.93, 0.97)
+EXIT_EPS = 2e-3
 
 
 def test_phi3_exit_step(world):
-    """EXIT mode at every interior boundary (tau 0.95): the exit boundary,
+    """EXIT mode at every interior boundary (tau 0.95, or the nearest
+    threshold that every gate signal of the step decides): the exit boundary,
     the fast row's token at the gate, the skipped layers' cache entries filled
     from the slow row, and the signals of the layers that ran."""
-    model, orc = world
+    model, orc, _ = world
     t = Tally()
     kv = PagedKV(CFG, 1, 64, block_size=16, block_table=shuffled_table(1, 64, 16, 9))
     cache = KVCache(CFG, 64)
@@ -119,25 +189,23 @@ def test_phi3_exit_step(world):
     exits = 0
     for step in range(3):
         pos = PROMPT + step
-        model.decode_step(tok_d, pos_d, kv.desc(), gates=gates, tau=tau, mode="exit", next_token=nxt,
+        tau_s = pick_tau(orc, int(tok_d.item()), pos, cache, gates, EXIT_TAUS, EXIT_EPS)
+        assert tau_s is not None, f"step {step}: every threshold lies near a gate signal"
+        model.decode_step(tok_d, pos_d, kv.desc(), gates=gates, tau=tau_s, mode="exit", next_token=nxt,
                           exit_boundary=exb, signal=sig, logits=logits, advance=True)
         torch.cuda.synchronize()
-        r = orc.decode_step(int(tok_d.item()), pos, cache, gates=gates, tau=tau, mode="exit")
-        # a signal within 2e-3 of tau at a boundary up to the exit may be decided either way
-        if any(abs(r.signal[b - 1] - tau) <= 2e-3 for b in gates if b <= r.exit_boundary):
-            t.skipped += 1
-            break
-        assert int(exb.item()) == r.exit_boundary, f"step {step} exit boundary"
+        r = orc.decode_step(int(tok_d.item()), pos, cache, gates=gates, tau=tau_s, mode="exit")
+        t.equal(int(exb.item()), r.exit_boundary, f"step {step} exit boundary")
         exits += r.exit_boundary < N
         ran = list(range(min(r.exit_boundary, N)))
-        got = sig.cpu().numpy()
-        assert np.max(np.abs(got[ran] - r.signal[ran])) <= TOL, f"step {step} signal"
+        t.close(sig.cpu().numpy()[ran], r.signal[ran], TOL, f"step {step} signal")
         t.rel(logits.cpu().numpy(), r.logits, TOL, f"step {step} logits")
         t.token(int(nxt.item()), r.logits, TOL, f"step {step} token")
         skipped = [l for l in (r.exit_boundary, (r.exit_boundary + N) // 2, N - 1) if l < N]
         _check_cache(kv, cache, 0, pos, pos + 1, t, sorted(set([0] + skipped)), f"step {step}")
+        t.steps += 1
         tok_d.copy_(nxt)
-    assert t.compared >= 2 or t.skipped
+    assert t.steps == 3 and exits >= 1
 
 
 def test_phi3_arla_exit_step(world):
@@ -145,7 +213,7 @@ def test_phi3_arla_exit_step(world):
     gates 8, 16 and 24 (intervals of eight fast states), bias 1.5 on the
     last gate's readout so that some steps exit: boundary, token, signals of
     the layers that ran and the skipped layers' cache entries."""
-    model, orc = world
+    model, orc, _ = world
     N, tau, gates = CFG.n_layers, 0.7, [8, 16, 24]
     a = synth.arla_weights(CFG)
     a["b_out"][24] = 1.5
@@ -164,52 +232,31 @@ def test_phi3_arla_exit_step(world):
         logits = torch.zeros(CFG.vocab, dtype=torch.float32, device=dev)
         for step in range(3):
             pos = PROMPT + step
-            model.decode_step(tok_d, pos_d, kv.desc(), gates=gates, tau=tau, mode="exit", next_token=nxt,
+            tau_s = pick_tau(orc, int(tok_d.item()), pos, cache, gates, (tau, 0.69, 0.71, 0.68, 0.72, 0.66, 0.74),
+                             EXIT_EPS, arla=a)
+            assert tau_s is not None, f"step {step}: every threshold lies near a gate score"
+            model.decode_step(tok_d, pos_d, kv.desc(), gates=gates, tau=tau_s, mode="exit", next_token=nxt,
                               exit_boundary=exb, signal=sig, logits=logits, advance=True)
             torch.cuda.synchronize()
-            r = orc.decode_step(int(tok_d.item()), pos, cache, gates=gates, tau=tau, mode="exit", arla=a)
-            if any(abs(r.signal[b - 1] - tau) <= 2e-3 for b in gates if b <= r.exit_boundary):
-                t.skipped += 1
-                break
-            assert int(exb.item()) == r.exit_boundary, f"step {step} exit boundary"
+            r = orc.decode_step(int(tok_d.item()), pos, cache, gates=gates, tau=tau_s, mode="exit", arla=a)
+            t.equal(int(exb.item()), r.exit_boundary, f"step {step} exit boundary")
             ran = list(range(min(r.exit_boundary, N)))
-            got = sig.cpu().numpy()
-            assert np.max(np.abs(got[ran] - r.signal[ran])) <= TOL, f"step {step} signal"
+            t.close(sig.cpu().numpy()[ran], r.signal[ran], TOL, f"step {step} signal")
             t.rel(logits.cpu().numpy(), r.logits, TOL, f"step {step} logits")
             t.token(int(nxt.item()), r.logits, TOL, f"step {step} token")
             skipped = [l for l in (r.exit_boundary, N - 1) if l < N]
             _check_cache(kv, cache, 0, pos, pos + 1, t, sorted(set([0] + skipped)), f"step {step}")
+            t.steps += 1
             tok_d.copy_(nxt)
-        assert t.compared >= 2 or t.skipped
+        assert t.steps == 3
     finally:
         model.set_arla(None)
-
-
-def _oracle_draft_logits(orc, token, pos, cache, exit_layer, gamma):
-    """The oracle's draft (Sec. 2.3.2) with the logits of every draft position."""
-    cfg = orc.cfg
-    scK = [np.zeros((gamma, cfg.n_heads, cfg.head_dim)) for _ in range(exit_layer)]
-    scV = [np.zeros((gamma, cfg.n_heads, cfg.head_dim)) for _ in range(exit_layer)]
-    out, zs, tok = [], [], token
-    for j in range(gamma):
-        p = orc.w["embed"][tok].copy()
-        for l in range(exit_layer):
-            ctxK = np.concatenate([cache.K[l][:pos], scK[l][:j]], axis=0)
-            ctxV = np.concatenate([cache.V[l][:pos], scV[l][:j]], axis=0)
-            p, (k, v) = orc._fast_layer(l, p, pos + j, ctxK, ctxV)
-            scK[l][j] = round_to_cache(k, cfg.kvdtype)
-            scV[l][j] = round_to_cache(v, cfg.kvdtype)
-        z = orc.head_logits(p)
-        tok = argmax_first(z)
-        out.append(tok)
-        zs.append(z)
-    return out, zs
 
 
 def test_phi3_draft_and_verify(world):
     """gamma = 4 drafts from the fast stream exiting at layer 8, then the
     5-row verification chunk through all 32 layers."""
-    model, orc = world
+    model, orc, _ = world
     gamma, kL = 4, 8
     t = Tally()
     kv = PagedKV(CFG, 1, 64, block_size=16, block_table=shuffled_table(1, 64, 16, 9))
@@ -224,11 +271,9 @@ def test_phi3_draft_and_verify(world):
     model.draft(buf[0:1], pos_d, kL, gamma, kv.desc(), buf[1:])
     torch.cuda.synchronize()
     drafts = buf[1:].cpu().numpy().tolist()
-    ref_d, ref_z = _oracle_draft_logits(orc, tok, PROMPT, cache, kL, gamma)
+    _, ref_z = oracle_draft_logits(orc, tok, PROMPT, cache, kL, gamma, drafts_fed=drafts)
     for j in range(gamma):
         t.token(drafts[j], ref_z[j], TOL, f"draft {j}")
-        if drafts[j] != ref_d[j]:
-            break   # the next drafts start from different tokens
     model.verify(buf, gamma + 1, pos_d, kv.desc(), targets, n_accepted=n_acc, bonus=buf[0:1])
     torch.cuda.synchronize()
     tg = targets.cpu().numpy().tolist()
@@ -238,17 +283,18 @@ def test_phi3_draft_and_verify(world):
     j = 0
     while j < gamma and drafts[j] == tg[j]:
         j += 1
-    assert int(n_acc.item()) == j and int(buf[0].item()) == tg[j]
+    t.equal(int(n_acc.item()), j, "accepted")
+    t.equal(int(buf[0].item()), tg[j], "bonus")
     assert int(pos_d.item()) == PROMPT + j + 1 == int(kv.seq_lens[0].item())
     _check_cache(kv, cache, 0, PROMPT, PROMPT + j + 1, t, (0, 8, 31), "verify")
-    assert t.compared >= 3
+    assert t.compared >= 2 + gamma + 1
 
 
 def test_batch8_long_context_step(world):
     """8 sequences, 4096-token contexts each (seeded N(0,1) cache content,
     shuffled block table), one dual-stream step; sequences 0 and 5 are
     recomputed by the oracle."""
-    model, orc = world
+    model, orc, _ = world
     B, sampled = 8, (0, 5)
     t = Tally()
     max_ctx = CTX_B + 16
@@ -290,6 +336,8 @@ def test_batch8_long_context_step(world):
         t.rel(L[s], r.logits, TOL, f"seq {s} logits")
         t.rel(Hh[s], r.h, TOL, f"seq {s} h")
         t.rel(Pp[s], r.p, TOL, f"seq {s} p")
-        assert np.max(np.abs(S[s] - r.signal)) <= TOL, f"seq {s} signal"
+        t.close(S[s], r.signal, TOL, f"seq {s} signal")
         t.token(int(nxt[s].item()), r.logits, TOL, f"seq {s} token")
         _check_cache(kv, caches[s], s, CTX_B, CTX_B + 1, t, (0, 16, 31), f"seq {s}")
+        t.steps += 1
+    assert t.steps == len(sampled)

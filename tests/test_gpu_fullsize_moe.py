@@ -11,8 +11,7 @@ import torch
 import synth
 from oracle import KVCache, Oracle
 from paper_2502_02040_amd import Model, PagedKV
-from tests.gpu_harness import Tally, shuffled_table
-from tests.test_gpu_moe import topk_decidable
+from tests.gpu_harness import Tally, shuffled_table, track
 
 pytestmark = pytest.mark.gpu
 
@@ -23,7 +22,7 @@ def test_olmoe_dual_step():
     cfg = synth.CONFIGS["olmoe"]
     N, K = cfg.n_layers, cfg.top_k
     w = synth.make_weights(cfg)
-    model = Model(cfg, w, max_batch=1, max_chunk=16, max_ctx=32, expert_slots=16)
+    model = track(Model(cfg, w, max_batch=1, max_chunk=16, max_ctx=32, expert_slots=16))
     model.moe_set_policy("ahead_of_time")
     orc = Oracle(cfg, w)
     del w
@@ -55,18 +54,19 @@ def test_olmoe_dual_step():
         r = orc.decode_step(int(tok_d.item()), p0, cache, mode="off")
         gs = slow.cpu().numpy().reshape(N, K)
         gp = pred.cpu().numpy().reshape(N, K)
+        diverged = False
         for l in range(N):
-            same = set(gs[l]) == set(r.slow_experts[l])
-            if topk_decidable(r.router_logits[l], K, TOL):
-                t.compared += 1
-                assert same, f"step {step} layer {l}: slow experts"
+            decided = t.experts(gs[l], r.slow_experts[l], r.router_logits[l], K, TOL, f"step {step} layer {l} slow")
+            if not decided and set(gs[l]) != set(r.slow_experts[l]):
+                diverged = True   # a near tie went the other way: later layers differ
+                break
+            if r.pred_experts[l][0] >= 0:
+                t.experts(gp[l], r.pred_experts[l], r.pred_logits[l], K, TOL, f"step {step} layer {l} predicted")
             else:
-                t.skipped += 1
-                if not same:
-                    return
-            if r.pred_experts[l][0] >= 0 and topk_decidable(r.pred_logits[l], K, TOL):
-                t.compared += 1
-                assert set(gp[l]) == set(r.pred_experts[l]), f"step {step} layer {l}: predicted experts"
+                assert np.all(gp[l] == -1), f"step {step} layer {l}: unexpected prediction"
+        if diverged:
+            t.skipped += 1
+            break
         t.rel(logits.cpu().numpy(), r.logits, TOL, f"step {step} logits")
         t.rel(h_out.cpu().numpy(), r.h, TOL, f"step {step} h")
         t.rel(p_out.cpu().numpy(), r.p, TOL, f"step {step} p")
@@ -75,7 +75,9 @@ def test_olmoe_dual_step():
             Kg, Vg = kv.read(0, l, p0, p0 + 1)
             t.rel(Kg, cache.K[l][p0:p0 + 1], TOL, f"step {step} K layer {l}")
             t.rel(Vg, cache.V[l][p0:p0 + 1], TOL, f"step {step} V layer {l}")
+        t.steps += 1
         tok_d.copy_(nxt)
     st = model.moe_stats()
     assert st["hits"] + st["misses"] == 2 * N * K
-    assert t.compared >= 8
+    # at least the first step in full, with most expert positions decided
+    assert t.steps >= 1 and t.compared >= 16 * t.steps
