@@ -225,6 +225,26 @@ M2R2_API m2r2_status m2r2_decode_step(m2r2_ctx* ctx, int32_t batch, int32_t dual
                                       int32_t* positions_d, const m2r2_kv* kv, const m2r2_exit* ex,
                                       const m2r2_step_out* out, hipStream_t stream);
 
+/* The decode step of m2r2_decode_step, for callers that cannot allocate
+ * device memory or whose memory is fixed before they start (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation).
+ * Same arguments, semantics and results; the difference is where the
+ * step's per-call scratch lives (residual rows, row statistics, attention
+ * and arg-max partials, arrival counters): in a static device array of
+ * 32 MiB inside the library, one per GPU, instead of the context's
+ * workspace.  The call allocates nothing and clears the scratch's counters
+ * itself (with a kernel on `stream`).  Limits: dense models only
+ * (M2R2_E_UNSUPPORTED for a mixture-of-experts context); the context's
+ * scratch, which grows with max_batch and max_ctx, must fit the 32 MiB
+ * (M2R2_E_SHAPE otherwise, e.g. a Phi-3-shaped context with max_batch 1 and
+ * max_ctx 1536 needs about 9 MiB); the device that was current at
+ * m2r2_create must be current (M2R2_E_STATE).  All such calls on one GPU
+ * share the array, which keeps the last call's contents: calls that overlap
+ * on one GPU (two streams, or two contexts at once) race. */
+M2R2_API m2r2_status m2r2_decode_step_noalloc(m2r2_ctx* ctx, int32_t batch, int32_t dual, const int32_t* tokens_d,
+                                              int32_t* positions_d, const m2r2_kv* kv, const m2r2_exit* ex,
+                                              const m2r2_step_out* out, hipStream_t stream);
+
 /* Accelerated-residual latent-attention exit router (Sec. 2.3.1, ARLA; Fig.
  * 4a), replacing the cosine signal at the gates of later dual decode steps
  * with the exit settings on.  Weights are borrowed device pointers, read

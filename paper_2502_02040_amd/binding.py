@@ -23,7 +23,7 @@ PROJ = ("q", "k", "v", "o", "g", "u", "d")
 
 # include/m2r2.h: the decode path's boundary
 EXPORTS = ("m2r2_workspace_size", "m2r2_create", "m2r2_destroy", "m2r2_decode_step", "m2r2_draft", "m2r2_verify",
-           "m2r2_device_errors", "m2r2_sync_check",
+           "m2r2_device_errors", "m2r2_sync_check", "m2r2_decode_step_noalloc",
            "m2r2_last_error", "m2r2_expert_bytes", "m2r2_pack_expert", "m2r2_moe_set_policy", "m2r2_prefetch_experts",
            "m2r2_moe_reset", "m2r2_moe_stats", "m2r2_expert_cache_replay", "m2r2_moe_set_preload_table",
            "m2r2_set_arla")
@@ -104,6 +104,8 @@ def lib() -> ctypes.CDLL:
         L.m2r2_destroy.restype = None
         L.m2r2_decode_step.argtypes = [c_void_p, c_int32, c_int32, c_void_p, c_void_p, POINTER(KV), POINTER(Exit),
                                        POINTER(StepOut), c_void_p]
+        L.m2r2_decode_step_noalloc.argtypes = [c_void_p, c_int32, c_int32, c_void_p, c_void_p, POINTER(KV),
+                                               POINTER(Exit), POINTER(StepOut), c_void_p]
         L.m2r2_draft.argtypes = [c_void_p, c_void_p, c_void_p, c_int32, c_int32, POINTER(KV), c_void_p, c_void_p]
         L.m2r2_verify.argtypes = [c_void_p, c_void_p, c_int32, c_void_p, POINTER(KV), c_void_p, c_void_p, c_void_p,
                                   c_void_p]
@@ -125,7 +127,7 @@ def lib() -> ctypes.CDLL:
                                                c_int32, POINTER(MoeCounters)]
         for f in ("m2r2_workspace_size", "m2r2_create", "m2r2_decode_step", "m2r2_draft", "m2r2_verify",
                   "m2r2_timing_enable", "m2r2_timing_read", "m2r2_time_gateup_layers", "m2r2_device_errors",
-                  "m2r2_sync_check", "m2r2_expert_bytes",
+                  "m2r2_sync_check", "m2r2_decode_step_noalloc", "m2r2_expert_bytes",
                   "m2r2_pack_expert", "m2r2_moe_set_policy", "m2r2_prefetch_experts", "m2r2_moe_reset",
                   "m2r2_moe_stats", "m2r2_expert_cache_replay", "m2r2_moe_set_preload_table", "m2r2_set_arla"):
             getattr(L, f).restype = c_int32
@@ -353,15 +355,18 @@ class Model:
     def decode_step(self, tokens, positions, kv: KV, *, dual: bool = True, gates: Sequence[int] = (),
                     tau: float = 2.0, mode: str = "observe", next_token=None, exit_boundary=None, signal=None,
                     logits=None, h_out=None, p_out=None, advance: bool = False, slow_experts=None,
-                    pred_experts=None, stream=None) -> None:
+                    pred_experts=None, stream=None, noalloc: bool = False) -> None:
+        """One decode step; ``noalloc`` calls m2r2_decode_step_noalloc (the
+        step's scratch in the library's static device array)."""
         g = (c_int32 * max(1, len(gates)))(*gates)
         ex = Exit(ctypes.cast(g, POINTER(c_int32)), len(gates), tau, MODES[mode])
         out = StepOut(_ptr(next_token), _ptr(exit_boundary), _ptr(signal), _ptr(logits), _ptr(h_out), _ptr(p_out),
                       1 if advance else 0, _ptr(slow_experts), _ptr(pred_experts))
         B = tokens.numel()
-        _check(lib().m2r2_decode_step(self._ctx, B, 1 if dual else 0, tokens.data_ptr(), positions.data_ptr(),
-                                      ctypes.byref(kv), ctypes.byref(ex), ctypes.byref(out), _stream(stream)),
-               "m2r2_decode_step")
+        fn = lib().m2r2_decode_step_noalloc if noalloc else lib().m2r2_decode_step
+        _check(fn(self._ctx, B, 1 if dual else 0, tokens.data_ptr(), positions.data_ptr(), ctypes.byref(kv),
+                  ctypes.byref(ex), ctypes.byref(out), _stream(stream)),
+               "m2r2_decode_step_noalloc" if noalloc else "m2r2_decode_step")
 
     def draft(self, last_token, positions, exit_layer: int, gamma: int, kv: KV, drafts, *, stream=None) -> None:
         _check(lib().m2r2_draft(self._ctx, last_token.data_ptr(), positions.data_ptr(), exit_layer, gamma,

@@ -9,6 +9,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -25,7 +26,43 @@
 
 using namespace m2r2;
 
+// Scratch of m2r2_decode_step_noalloc: the per-call scratch block of a
+// context (residual rows, row statistics, attention partials, arg-max
+// partials, arrival counters) placed in this file-scope device array instead
+// of the context's workspace.  Every GPU the library runs on holds its own
+// copy until the process ends; all such calls on one GPU share it.  Host code
+// never passes the array's name to a kernel (on the host it is only a
+// stand-in symbol): its device address is looked up once per device with
+// hipGetSymbolAddress and used instead.
+constexpr size_t kNoAllocScratchBytes = (size_t)32 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};   // device address of `scratch` on each device, once looked up
+
+// Look up the device address of `scratch` on device `dev` (current) once.
+hipError_t scratch_setup(int dev) {
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[dev]) return hipSuccess;
+  void* p = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (e == hipSuccess) g_scratch_ptr[dev] = p;
+  return e;
+}
+
+void* scratch_ptr(int dev) {
+  if (dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  return g_scratch_ptr[dev];
+}
+
+__global__ void k_fill_u32(uint32_t* p, int n, uint32_t v) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = v;
+}
 
 thread_local std::string g_err;
 
@@ -67,6 +104,7 @@ struct Layout {
   size_t lm;                             // packed LM head
   size_t X, PIN, QKV, O, ACT, bin_d, bin_o, bin_gu, uo, att, att_cnt, lm_val, lm_idx, lm_cnt, exited, exitb,
       reinit, err, sig, arla_kv, arla_q, arla_sig, arla_cnt, rope, sk_part, sk_cnt, total;
+  size_t scratch_begin, counters_begin, scratch_end;   // per-call scratch [begin, end), counters [counters_begin, end)
   // mixture of experts: router logits, choices, probabilities, activations,
   // and the expert cache ([n_layers][slots] slots of expert_stride bytes)
   size_t moe_logits, moe_sel, moe_prob, moe_act, moe_slots, moe_tab;
@@ -180,6 +218,9 @@ Layout make_layout(const m2r2_config& c, int max_batch, int max_chunk, int max_c
     }
   }
   L.lm = take(packed_bytes(c.vocab, d, wb));
+  // ---- per-call scratch: one contiguous block (the no-allocation decode
+  // step rebases exactly this block onto its static device array)
+  L.scratch_begin = off;
   L.X = take(sizeof(float) * kMaxRows * d);
   L.PIN = take(sizeof(float) * kMaxRows * d);
   L.QKV = take(sizeof(float) * kMaxRows * nqkv);
@@ -191,25 +232,29 @@ Layout make_layout(const m2r2_config& c, int max_batch, int max_chunk, int max_c
   L.uo = take(sizeof(float) * kMaxRows * c.n_heads * std::max(r, 1));
   L.att = take(sizeof(float) * (size_t)std::max(max_batch, 1) * c.n_heads * (smax + 1) * kMaxRows *
                (c.head_dim + 2 + r));
-  L.att_cnt = take(sizeof(uint32_t) * kMaxSeq * c.n_heads);
   // per-tile (or, for the row-per-wave head, per-workgroup) arg-max partials
   L.lm_slots = std::max(L.TV, kLmMinSlots);
   L.lm_val = take(sizeof(float) * L.lm_slots * kMaxRows);
   L.lm_idx = take(sizeof(int) * L.lm_slots * kMaxRows);
-  L.lm_cnt = take(sizeof(uint32_t));
   L.exited = take(sizeof(int) * kMaxSeq);
   L.exitb = take(sizeof(int) * kMaxSeq);
   L.reinit = take(sizeof(int) * c.n_layers * kMaxSeq);
-  L.err = take(sizeof(int));
   L.sig = take(sizeof(float) * kMaxSeq * c.n_layers);
   L.arla_kv = take(sizeof(float) * c.n_layers * 2 * kArlaDim);
   L.arla_q = take(sizeof(float) * kArlaDim);
   L.arla_sig = take(sizeof(float) * kMaxSeq);
-  L.arla_cnt = take(sizeof(uint32_t));
-  L.rope = take(sizeof(float) * 2 * (size_t)max_ctx * (c.head_dim / 2));
   L.sk_slots = sk_slot_bound(c);
   L.sk_part = take(sizeof(float) * 64 * std::max<size_t>(L.sk_slots, 1));
+  // arrival counters (zero between passes: the last arriver resets them)
+  L.counters_begin = off;
+  L.att_cnt = take(sizeof(uint32_t) * kMaxSeq * c.n_heads);
+  L.lm_cnt = take(sizeof(uint32_t));
+  L.arla_cnt = take(sizeof(uint32_t));
   L.sk_cnt = take(sizeof(uint32_t) * (65 + std::max({L.TD, L.TF, L.TV, 3 * ((qdim + 15) / 16) + (3 * r + 15) / 16})));
+  L.scratch_end = off;
+  // ---- context state: sticky error bits, RoPE table, expert cache
+  L.err = take(sizeof(int));
+  L.rope = take(sizeof(float) * 2 * (size_t)max_ctx * (c.head_dim / 2));
   if (moe) {
     L.moe_logits = take(sizeof(float) * 3 * c.n_experts);
     L.moe_sel = take(sizeof(int) * 3 * kMaxTopK);
@@ -298,6 +343,8 @@ struct MoeState {
 
 struct m2r2_ctx {
   m2r2_config cfg;
+  int device = 0;   // the device the context was created on
+  char* ws_base = nullptr;   // the workspace
   Dims D;
   Layout lay;
   std::vector<LayerPtrs> layers;
@@ -1231,6 +1278,7 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
     }
   }
   char* b = (char*)workspace;
+  c->ws_base = b;
   WS& ws = c->ws;
   ws.X = (float*)(b + lay.X); ws.PIN = (float*)(b + lay.PIN); ws.QKV = (float*)(b + lay.QKV);
   ws.O = (float*)(b + lay.O); ws.ACT = (float*)(b + lay.ACT); ws.bin_d = (float*)(b + lay.bin_d);
@@ -1247,7 +1295,10 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
   c->skws.hier = (uint32_t*)(b + lay.sk_cnt);
   c->skws.cnt = c->skws.hier + 65;
 
-  hipError_t e = hipMemset(workspace, 0, lay.total);
+  hipError_t e = hipGetDevice(&c->device);
+  // the no-allocation decode step's scratch: its address on this device
+  if (e == hipSuccess) e = scratch_setup(c->device);
+  if (e == hipSuccess) e = hipMemset(workspace, 0, lay.total);
   if (e == hipSuccess) {
     // RoPE table: angle pos * theta^(-2j/hd) evaluated in double precision
     const int half = cfg->head_dim / 2;
@@ -1397,14 +1448,26 @@ M2R2_API m2r2_status m2r2_sync_check(m2r2_ctx* c, hipStream_t stream) {
   return M2R2_OK;
 }
 
-M2R2_API m2r2_status m2r2_decode_step(m2r2_ctx* c, int32_t batch, int32_t dual, const int32_t* tokens_d,
-                                      int32_t* positions_d, const m2r2_kv* kv, const m2r2_exit* ex,
-                                      const m2r2_step_out* out, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// A decode step's arguments, checked and turned into the row map and the
+// kernels' I/O block before anything is enqueued.
+struct StepCall {
+  RowMap rm;
+  StepIO io;
+  bool arla = false;   // the exit router decides the gates
+};
+
+m2r2_status decode_prepare(m2r2_ctx* c, int32_t batch, int32_t dual, const int32_t* tokens_d, int32_t* positions_d,
+                           const m2r2_kv* kv, const m2r2_exit* ex, const m2r2_step_out* out, StepCall* sc) {
   if (!c) return fail(M2R2_E_INVALID, "ctx is NULL");
   if (batch < 1 || batch > c->max_batch) return fail(M2R2_E_SHAPE, "batch %d not in [1,%d]", batch, c->max_batch);
   if (!tokens_d || !positions_d || !out || !out->next_token_d) return fail(M2R2_E_INVALID, "NULL tokens/positions/out");
   if (m2r2_status s = check_kv(c, kv)) return s;
-  StepIO io = empty_io();
+  StepIO& io = sc->io;
+  io = empty_io();
   io.tokens = tokens_d;
   io.positions = positions_d;
   io.next_token = out->next_token_d;
@@ -1427,7 +1490,8 @@ M2R2_API m2r2_status m2r2_decode_step(m2r2_ctx* c, int32_t batch, int32_t dual, 
       else io.gate_mask_hi |= 1ull << (g - 64);
     }
   }
-  RowMap rm = empty_rowmap();
+  RowMap& rm = sc->rm;
+  rm = empty_rowmap();
   rm.nseq = batch;
   const int per = dual ? 2 : 1;
   rm.M = batch * per;
@@ -1441,15 +1505,85 @@ M2R2_API m2r2_status m2r2_decode_step(m2r2_ctx* c, int32_t batch, int32_t dual, 
       rm.slow_of[m + 1] = m;
     }
   }
-  if (c->moe.on) {
-    if (batch != 1) return fail(M2R2_E_UNSUPPORTED, "mixture-of-experts decoding takes batch 1");
-    return run_moe_pass(c, rm, io, kv_ptrs(kv), out, dual != 0, stream);
+  if (c->moe.on && batch != 1) return fail(M2R2_E_UNSUPPORTED, "mixture-of-experts decoding takes batch 1");
+  sc->arla = !c->moe.on && c->arla.on && io.mode != EX_OFF && (io.gate_mask_lo | io.gate_mask_hi);
+  if (sc->arla && batch != 1) return fail(M2R2_E_UNSUPPORTED, "the latent-attention exit router takes batch 1");
+  return M2R2_OK;
+}
+
+m2r2_status decode_launch(m2r2_ctx* c, StepCall& sc, const m2r2_kv* kv, const m2r2_step_out* out, int32_t dual,
+                          hipStream_t stream) {
+  if (c->moe.on) return run_moe_pass(c, sc.rm, sc.io, kv_ptrs(kv), out, dual != 0, stream);
+  if (sc.arla) sc.io.arla_sig = c->ws.arla_sig;
+  return run_pass(c, sc.rm, sc.io, kv_ptrs(kv), c->D.n_layers, stream);
+}
+
+// For the duration of one call, the context's per-call scratch pointers
+// point into `dst` (the same offsets within the scratch block) instead of
+// the workspace; restored on destruction.
+struct ScratchRebase {
+  m2r2_ctx* c;
+  WS ws;
+  SkWS sk;
+  ScratchRebase(m2r2_ctx* ctx, char* dst) : c(ctx), ws(ctx->ws), sk(ctx->skws) {
+    const char* lo = c->ws_base + c->lay.scratch_begin;
+    const char* hi = c->ws_base + c->lay.scratch_end;
+    auto rb = [&](auto* p) {
+      const char* q = (const char*)p;
+      return (q >= lo && q < hi) ? (decltype(p))(dst + (q - lo)) : p;
+    };
+    WS& w = c->ws;
+    w.X = rb(w.X); w.PIN = rb(w.PIN); w.QKV = rb(w.QKV); w.O = rb(w.O); w.ACT = rb(w.ACT);
+    w.bin_d = rb(w.bin_d); w.bin_o = rb(w.bin_o); w.bin_gu = rb(w.bin_gu); w.uo = rb(w.uo); w.att = rb(w.att);
+    w.att_cnt = rb(w.att_cnt); w.lm_val = rb(w.lm_val); w.lm_idx = rb(w.lm_idx); w.lm_cnt = rb(w.lm_cnt);
+    w.exited = rb(w.exited); w.exitb = rb(w.exitb); w.reinit = rb(w.reinit); w.sig = rb(w.sig);
+    w.arla_kv = rb(w.arla_kv); w.arla_q = rb(w.arla_q); w.arla_sig = rb(w.arla_sig); w.arla_cnt = rb(w.arla_cnt);
+    c->skws.part = rb(c->skws.part); c->skws.hier = rb(c->skws.hier); c->skws.cnt = rb(c->skws.cnt);
   }
-  if (c->arla.on && io.mode != EX_OFF && (io.gate_mask_lo | io.gate_mask_hi)) {
-    if (batch != 1) return fail(M2R2_E_UNSUPPORTED, "the latent-attention exit router takes batch 1");
-    io.arla_sig = c->ws.arla_sig;
+  ~ScratchRebase() {
+    c->ws = ws;
+    c->skws = sk;
   }
-  return run_pass(c, rm, io, kv_ptrs(kv), c->D.n_layers, stream);
+};
+
+}  // namespace
+
+extern "C" {
+
+M2R2_API m2r2_status m2r2_decode_step(m2r2_ctx* c, int32_t batch, int32_t dual, const int32_t* tokens_d,
+                                      int32_t* positions_d, const m2r2_kv* kv, const m2r2_exit* ex,
+                                      const m2r2_step_out* out, hipStream_t stream) {
+  StepCall sc;
+  if (m2r2_status s = decode_prepare(c, batch, dual, tokens_d, positions_d, kv, ex, out, &sc)) return s;
+  return decode_launch(c, sc, kv, out, dual, stream);
+}
+
+M2R2_API m2r2_status m2r2_decode_step_noalloc(m2r2_ctx* c, int32_t batch, int32_t dual, const int32_t* tokens_d,
+                                              int32_t* positions_d, const m2r2_kv* kv, const m2r2_exit* ex,
+                                              const m2r2_step_out* out, hipStream_t stream) {
+  StepCall sc;
+  if (m2r2_status s = decode_prepare(c, batch, dual, tokens_d, positions_d, kv, ex, out, &sc)) return s;
+  if (c->moe.on)
+    return fail(M2R2_E_UNSUPPORTED, "the no-allocation decode step is for dense models (an expert cache is "
+                                    "context state in the workspace)");
+  int dev = -1;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev != c->device)
+    return fail(M2R2_E_STATE, "context created on device %d, but device %d is current", c->device, dev);
+  const size_t need = c->lay.scratch_end - c->lay.scratch_begin;
+  if (need > kNoAllocScratchBytes)
+    return fail(M2R2_E_SHAPE, "the context's per-call scratch needs %zu bytes, above the static maximum of %zu "
+                              "(create the context with a smaller max_batch or max_ctx)", need, kNoAllocScratchBytes);
+  char* sp = (char*)scratch_ptr(dev);
+  if (!sp) return fail(M2R2_E_STATE, "no scratch address on device %d", dev);
+  // the arrival counters must start at zero (a fill kernel, not a memset:
+  // the call may be captured into a graph)
+  const size_t cnt_off = c->lay.counters_begin - c->lay.scratch_begin;
+  const int n_cnt = (int)((c->lay.scratch_end - c->lay.counters_begin) / sizeof(uint32_t));
+  k_fill_u32<<<std::max(1, std::min(64, (n_cnt + 255) / 256)), 256, 0, stream>>>((uint32_t*)(sp + cnt_off), n_cnt, 0u);
+  HIP_TRY(hipGetLastError());
+  ScratchRebase swap(c, sp);
+  return decode_launch(c, sc, kv, out, dual, stream);
 }
 
 M2R2_API m2r2_status m2r2_set_arla(m2r2_ctx* c, const m2r2_arla* w) {

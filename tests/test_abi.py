@@ -31,7 +31,9 @@ CORE = {"m2r2_workspace_size", "m2r2_create", "m2r2_destroy", "m2r2_decode_step"
 # declared extensions of the boundary (each with its reason in the header)
 EXTENSIONS = {"m2r2_device_errors", "m2r2_expert_bytes", "m2r2_pack_expert", "m2r2_moe_set_policy",
               "m2r2_moe_reset", "m2r2_moe_stats", "m2r2_expert_cache_replay", "m2r2_moe_set_preload_table",
-              "m2r2_set_arla"}
+              "m2r2_set_arla",
+              # the decode step for callers that cannot allocate (scratch in a static device array)
+              "m2r2_decode_step_noalloc"}
 
 
 def test_header_declarations_match_binding():
@@ -80,3 +82,4 @@ def test_null_arguments_are_rejected():
     assert lib.m2r2_moe_set_policy(None, 0) == -1
     assert lib.m2r2_moe_set_preload_table(None, None, 1) == -1
     assert lib.m2r2_sync_check(None, None) == -1
+    assert lib.m2r2_decode_step_noalloc(None, 1, 1, None, None, None, None, None, None) == -1
