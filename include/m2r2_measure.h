@@ -16,7 +16,8 @@ extern "C" {
 /* Kernel timing for measurement.  Kernel classes of one decode pass:
  * 0 qkv, 1 attention, 2 output projection, 3 gate/up, 4 down, 5 LM head,
  * 6 embedding, 7 attention merge, 8 expert gate/up, 9 expert down, 10
- * router and top-k.  m2r2_timing_enable(ctx, k) starts a new record: every
+ * router and top-k, 11 the one-launch decode step of one sequence (every
+ * layer and the head in one kernel).  m2r2_timing_enable(ctx, k) starts a new record: every
  * launch of class k made by later calls is bracketed by a pair of HIP events
  * recorded on the call's stream (up to 1024 launches; record with direct
  * launches: events recorded inside a captured graph cannot be timed).

@@ -30,7 +30,7 @@ EXPORTS = ("m2r2_workspace_size", "m2r2_create", "m2r2_destroy", "m2r2_decode_st
 # include/m2r2_measure.h: measurement hooks
 MEASURE_EXPORTS = ("m2r2_timing_enable", "m2r2_timing_read", "m2r2_time_gateup_layers")
 KERNEL_CLASSES = {"qkv": 0, "attn": 1, "oproj": 2, "gateup": 3, "down": 4, "head": 5, "embed": 6, "attn_merge": 7,
-                  "expert_gateup": 8, "expert_down": 9, "router": 10}
+                  "expert_gateup": 8, "expert_down": 9, "router": 10, "step": 11}
 MOE_ON_DEMAND, MOE_AHEAD_OF_TIME, MOE_FIXED, MOE_RANDOM_PRELOAD, MOE_PREVIOUS_LAYER = 0, 1, 2, 3, 4
 POLICIES = {"on_demand": MOE_ON_DEMAND, "ahead_of_time": MOE_AHEAD_OF_TIME, "fixed": MOE_FIXED,
             "random_preload": MOE_RANDOM_PRELOAD, "previous_layer": MOE_PREVIOUS_LAYER}

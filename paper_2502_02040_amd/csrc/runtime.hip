@@ -23,6 +23,7 @@
 #include "sk_attn.h"
 #include "rw_kernels.h"
 #include "arla.h"
+#include "persist.h"
 
 using namespace m2r2;
 
@@ -105,6 +106,8 @@ struct Layout {
   size_t X, PIN, QKV, O, ACT, bin_d, bin_o, bin_gu, uo, att, att_cnt, lm_val, lm_idx, lm_cnt, exited, exitb,
       reinit, err, sig, arla_kv, arla_q, arla_sig, arla_cnt, rope, sk_part, sk_cnt, total;
   size_t scratch_begin, counters_begin, scratch_end;   // per-call scratch [begin, end), counters [counters_begin, end)
+  size_t pk_sd, pk_so, pk_sgu, pk_bar, pk_rel, layers_d;   // one-launch step: statistics slots, barrier, layer table
+  int pk_so_w, pk_sgu_w;
   // mixture of experts: router logits, choices, probabilities, activations,
   // and the expert cache ([n_layers][slots] slots of expert_stride bytes)
   size_t moe_logits, moe_sel, moe_prob, moe_act, moe_slots, moe_tab;
@@ -245,15 +248,24 @@ Layout make_layout(const m2r2_config& c, int max_batch, int max_chunk, int max_c
   L.arla_sig = take(sizeof(float) * kMaxSeq);
   L.sk_slots = sk_slot_bound(c);
   L.sk_part = take(sizeof(float) * 64 * std::max<size_t>(L.sk_slots, 1));
+  // the one-launch step's per-workgroup statistics slots
+  L.pk_so_w = (2 + 2 * r + 3) & ~3;
+  L.pk_sgu_w = (r + 3) & ~3;
+  L.pk_sd = take(sizeof(float) * kPkMaxWG * kPkSdW);
+  L.pk_so = take(sizeof(float) * kPkMaxWG * L.pk_so_w);
+  L.pk_sgu = take(sizeof(float) * kPkMaxWG * L.pk_sgu_w);
   // arrival counters (zero between passes: the last arriver resets them)
   L.counters_begin = off;
   L.att_cnt = take(sizeof(uint32_t) * kMaxSeq * c.n_heads);
   L.lm_cnt = take(sizeof(uint32_t));
   L.arla_cnt = take(sizeof(uint32_t));
   L.sk_cnt = take(sizeof(uint32_t) * (65 + std::max({L.TD, L.TF, L.TV, 3 * ((qdim + 15) / 16) + (3 * r + 15) / 16})));
+  L.pk_bar = take(sizeof(uint32_t));
+  L.pk_rel = take(sizeof(uint32_t) * kPkRelStride * kPkMaxWG);
   L.scratch_end = off;
   // ---- context state: sticky error bits, RoPE table, expert cache
   L.err = take(sizeof(int));
+  L.layers_d = take(sizeof(LayerPtrs) * c.n_layers);
   L.rope = take(sizeof(float) * 2 * (size_t)max_ctx * (c.head_dim / 2));
   if (moe) {
     L.moe_logits = take(sizeof(float) * 3 * c.n_experts);
@@ -364,6 +376,16 @@ struct m2r2_ctx {
   int rw_nch[3] = {0, 0, 0};   // 1 KB pieces per row for reductions over d, qdim, ffn
   int rw_nw[2] = {8, 8};       // waves per workgroup of the o and down projections
   int attn_chunks = 0;         // batched short-chain attention: 128-token chunks per split (0: by size)
+  // one-launch decode step (one sequence, one or two rows): instantiation,
+  // grid (one workgroup per compute unit), attention splits per head, LDS
+  struct {
+    int kind = -1;   // index into M2R2_PK_SHAPES, -1: not available
+    int grid = 0, S = 0;
+    size_t lds = 0;
+    float *sd = nullptr, *so = nullptr, *sgu = nullptr;
+    uint32_t *bar = nullptr, *rel = nullptr;
+    const LayerPtrs* layers_d = nullptr;
+  } pk;
   SkPlan sk[5];
   SkWS skws{};
   int timed_class = -1;
@@ -833,8 +855,104 @@ hipError_t sk_setup(m2r2_ctx* c) {
   return e;
 }
 
-// Embedding, n_layers_run layers, head.
+// ---- the one-launch decode step (persist.h) -----------------------------------
+// Instantiations: (index, weight bf16, cache bf16, head_dim, 1 KB pieces per
+// row of length d, H*hd, ffn).  Phi-3-mini shape; the tiny float32 and the
+// small bfloat16 test decoders.
+#define M2R2_PK_SHAPES(X) X(0, 1, 1, 96, 6, 6, 16) X(1, 0, 0, 64, 1, 1, 4) X(2, 1, 1, 128, 1, 1, 2)
+
+template <int WB, int KB, int HD, int ND, int NQ, int NF>
+hipError_t pk_attr(size_t lds, int* per_cu) {
+  const void* f = (const void*)kp_step<WB, KB, HD, ND, NQ, NF>;
+  hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(per_cu, f, kPkThreads, lds);
+  return e;
+}
+
+// Use the one-launch step for this context when its shape has an
+// instantiation: dense, rows of whole 1 KB pieces (the row-per-wave
+// streams), rank a multiple of 4 with the o-projection slot (2 + 2r floats)
+// within 64, every head at least one attention split, one workgroup per
+// compute unit resident.
+hipError_t pk_setup(m2r2_ctx* c) {
+  c->pk.kind = -1;
+  const Dims& D = c->D;
+  if (is_moe(c->cfg) || !c->rw_on) return hipSuccess;
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  if (D.r % 4 || 2 + 2 * D.r > 64 || cus < 1 || cus > kPkMaxWG || D.H > cus) return hipSuccess;
+  const int S = std::min(kPkMaxSplits, std::max(1, cus / D.H));
+  if (S > c->lay.S_max) return hipSuccess;
+  const int nd = c->rw_nch[0], nq = c->rw_nch[1], nf = c->rw_nch[2];
+  const size_t lds = pk_lds_bytes(D.hd, D.wbf16, std::max({D.d, D.qdim, D.F}));
+  if (lds > 150 * 1024) return hipSuccess;
+  int kind = -1, per_cu = 0;
+#define M2R2_PK_MATCH(K, WB, KB, HD, ND, NQ, NF)                                                       \
+  if (kind < 0 && D.wbf16 == WB && D.kvbf16 == KB && D.hd == HD && nd == ND && nq == NQ && nf == NF) { \
+    kind = K;                                                                                         \
+    e = pk_attr<WB, KB, HD, ND, NQ, NF>(lds, &per_cu);                                                \
+  }
+  M2R2_PK_SHAPES(M2R2_PK_MATCH)
+#undef M2R2_PK_MATCH
+  if (e != hipSuccess || kind < 0 || per_cu < 1) return e;
+  char* b = c->ws_base;
+  e = hipMemcpy(b + c->lay.layers_d, c->layers.data(), sizeof(LayerPtrs) * D.n_layers, hipMemcpyHostToDevice);
+  if (e != hipSuccess) return e;
+  c->pk.kind = kind;
+  c->pk.grid = cus;
+  c->pk.S = S;
+  c->pk.lds = lds;
+  c->pk.layers_d = (const LayerPtrs*)(b + c->lay.layers_d);
+  c->pk.sd = (float*)(b + c->lay.pk_sd);
+  c->pk.so = (float*)(b + c->lay.pk_so);
+  c->pk.sgu = (float*)(b + c->lay.pk_sgu);
+  c->pk.bar = (uint32_t*)(b + c->lay.pk_bar);
+  c->pk.rel = (uint32_t*)(b + c->lay.pk_rel);
+  return hipSuccess;
+}
+
+bool pk_eligible(const m2r2_ctx* c, const RowMap& rm, const StepIO& io) {
+  return c->pk.kind >= 0 && rm.nseq == 1 && rm.M >= 1 && rm.M <= 2 && !rm.head_all && !io.arla_sig &&
+         rm.first[0] == 0 && rm.cnt[0] == rm.M;
+}
+
+m2r2_status run_pk(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPtrs& kv, int nl, hipStream_t st) {
+  PkArgs a;
+  a.D = c->D;
+  a.layers = c->pk.layers_d;
+  a.embed = c->embed;
+  a.lm_head = c->lm_head_rm;
+  a.final_norm = c->final_norm;
+  a.rm = rm;
+  a.ws = c->ws;
+  a.io = io;
+  a.kv = kv;
+  a.sd = c->pk.sd;
+  a.so = c->pk.so;
+  a.sgu = c->pk.sgu;
+  a.bar = PkBar{c->pk.bar, c->pk.rel};
+  a.n_layers_run = nl;
+  a.S = c->pk.S;
+  a.so_w = c->lay.pk_so_w;
+  a.sgu_w = c->lay.pk_sgu_w;
+  const int grid = c->pk.grid;
+  const size_t lds = c->pk.lds;
+#define M2R2_PK_LAUNCH(K, WB, KB, HD, ND, NQ, NF) \
+  case K: TIMED(11, (kp_step<WB, KB, HD, ND, NQ, NF><<<grid, kPkThreads, lds, st>>>(a))); break;
+  switch (c->pk.kind) {
+    M2R2_PK_SHAPES(M2R2_PK_LAUNCH)
+    default: return fail(M2R2_E_STATE, "no one-launch step for this context");
+  }
+#undef M2R2_PK_LAUNCH
+  HIP_TRY(hipGetLastError());
+  return M2R2_OK;
+}
+
+// Embedding, n_layers_run layers, head (one launch where the shape allows).
 m2r2_status run_pass(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPtrs& kv, int nl, hipStream_t st) {
+  if (pk_eligible(c, rm, io)) return run_pk(c, rm, io, kv, nl, st);
   TIMED(6, (k_embed<<<rm.M + kEmbedZeroBlocks, 256, 0, st>>>(c->D, c->embed, rm, c->ws, io, 1)));
   HIP_TRY(hipGetLastError());
   const int wb = c->D.wbf16, kb = c->D.kvbf16;
@@ -1319,6 +1437,7 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
   if (e == hipSuccess) e = set_lds_limits<0, 16>(*cfg, c->resident);
   if (e == hipSuccess) e = set_lds_limits<1, 16>(*cfg, c->resident);
   if (e == hipSuccess) e = sk_setup(c);
+  if (e == hipSuccess) e = pk_setup(c);
   if (e == hipSuccess && moe) {
     MoeState& M = c->moe;
     M.on = true;
@@ -1377,7 +1496,7 @@ M2R2_API void m2r2_destroy(m2r2_ctx* ctx) {
 
 M2R2_API m2r2_status m2r2_timing_enable(m2r2_ctx* c, int32_t kernel_class) {
   if (!c) return fail(M2R2_E_INVALID, "ctx is NULL");
-  if (kernel_class < -1 || kernel_class > 10) return fail(M2R2_E_INVALID, "kernel class %d", kernel_class);
+  if (kernel_class < -1 || kernel_class > 11) return fail(M2R2_E_INVALID, "kernel class %d", kernel_class);
   c->timed_class = kernel_class;
   c->ev_used = 0;   // a new record
   return M2R2_OK;
@@ -1525,7 +1644,8 @@ struct ScratchRebase {
   m2r2_ctx* c;
   WS ws;
   SkWS sk;
-  ScratchRebase(m2r2_ctx* ctx, char* dst) : c(ctx), ws(ctx->ws), sk(ctx->skws) {
+  decltype(m2r2_ctx::pk) pk;
+  ScratchRebase(m2r2_ctx* ctx, char* dst) : c(ctx), ws(ctx->ws), sk(ctx->skws), pk(ctx->pk) {
     const char* lo = c->ws_base + c->lay.scratch_begin;
     const char* hi = c->ws_base + c->lay.scratch_end;
     auto rb = [&](auto* p) {
@@ -1539,10 +1659,12 @@ struct ScratchRebase {
     w.exited = rb(w.exited); w.exitb = rb(w.exitb); w.reinit = rb(w.reinit); w.sig = rb(w.sig);
     w.arla_kv = rb(w.arla_kv); w.arla_q = rb(w.arla_q); w.arla_sig = rb(w.arla_sig); w.arla_cnt = rb(w.arla_cnt);
     c->skws.part = rb(c->skws.part); c->skws.hier = rb(c->skws.hier); c->skws.cnt = rb(c->skws.cnt);
+    c->pk.sd = rb(c->pk.sd); c->pk.so = rb(c->pk.so); c->pk.sgu = rb(c->pk.sgu); c->pk.bar = rb(c->pk.bar); c->pk.rel = rb(c->pk.rel);
   }
   ~ScratchRebase() {
     c->ws = ws;
     c->skws = sk;
+    c->pk = pk;
   }
 };
 

@@ -240,19 +240,41 @@ struct RwStream {
     }
   }
 
+  // Issue every register buffer's first weights (and their epilogue
+  // operands) for the range [u0, u1): for a phase whose activations are not
+  // there yet, so that all of them are in flight while it waits; run<true>()
+  // then streams on without issuing them again.  Loads stay unconditional
+  // and in range as in begin().
+  template <class PF, class Epi>
+  __device__ __forceinline__ void begin_all(const PF& row_ptr, int u0, int u1, const Epi& epi,
+                                            typename Epi::Ops (&ops)[P]) {
+    const int last = max(u1 - 1, u0);
+    if constexpr (NS == 1) {
+#pragma unroll
+      for (int i = 0; i < P; ++i) {
+        load(row_ptr, min(u0 + i, last), 0, bb[i]);
+        fetch_grouped(epi, [&] { epi.fetch(min(u0 + i, last), ops[i]); });
+      }
+    } else {
+      load(row_ptr, u0, 0, bb[0]);
+      fetch_grouped(epi, [&] { epi.fetch(u0, ops[0]); });
+      load(row_ptr, u0, 1, bb[1]);
+    }
+  }
+
   // Stream units [u0, u1) after begin(): epi.fetch(unit, ops) issues a unit's
   // epilogue operands (in flight with its weights), epi.run(unit, y, ops)
   // runs the epilogue.  Inside the loops every iteration issues the same
   // loads; the last units are finished after the loop, so nothing past the
   // range is read.
-  template <class PF, class Epi>
+  template <bool PRIMED = false, class PF, class Epi>
   __device__ __forceinline__ void run(const PF& row_ptr, int u0, int u1, const float* act, int K, Epi& epi,
                                       typename Epi::Ops (&ops)[P]) {
     if (u0 >= u1) return;
     float y[U][2];
     int u = u0;
     if constexpr (NS == 1) {
-      {
+      if constexpr (!PRIMED) {
         const int last = u1 - 1;
 #pragma unroll
         for (int i = kBegin; i < P; ++i) {
@@ -290,7 +312,7 @@ struct RwStream {
         }
       }
     } else {
-      load(row_ptr, u0, 1, bb[1]);   // the second half of the first unit
+      if constexpr (!PRIMED) load(row_ptr, u0, 1, bb[1]);   // the second half of the first unit
       // unit u in bb[0] (sub-unit 0) and bb[1] (sub-unit 1), its operands in ops[0];
       // two units per iteration so the operand buffers alternate in place
       for (; u + 2 < u1; u += 2) {

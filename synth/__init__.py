@@ -94,6 +94,10 @@ CONFIGS: Dict[str, ModelConfig] = {
     "small_moe_f32": ModelConfig("small_moe_f32", n_layers=5, d_model=128, n_heads=2, head_dim=64, ffn=0,
                                  vocab=300, rank=4, wdtype="f32", kvdtype="f32", n_experts=8, top_k=2,
                                  expert_ffn=64, seed=19),
+    # a dense bfloat16 decoder whose rows are whole 1 KB pieces (d 512,
+    # ffn 1024): the one-launch decode step at head_dim 128
+    "small_rw": ModelConfig("small_rw", n_layers=3, d_model=512, n_heads=4, head_dim=128, ffn=1024, vocab=1000,
+                            rank=8, wdtype="bf16", kvdtype="bf16", seed=31),
     # rows of whole 1 KB pieces: the one- and two-row q/k/v, o and head kernels
     "small_moe_rw": ModelConfig("small_moe_rw", n_layers=4, d_model=512, n_heads=4, head_dim=128, ffn=0, vocab=1000,
                                 rank=8, wdtype="bf16", kvdtype="bf16", n_experts=16, top_k=4, expert_ffn=96, seed=23),

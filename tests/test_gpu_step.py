@@ -3,9 +3,11 @@ self-speculative draft/verify, through the C ABI, against the CPU oracle.
 
 Inputs are the seeded synthetic weights and prompts of synth; the paged
 cache uses a shuffled block table.  Sizes: the tiny float32 decoder (2
-layers, d 256, 4 heads x 64) and a small bfloat16 decoder (3 layers, d 192,
-2 heads x 96, ffn 320: tiles of 16 rows leave ragged tails in the LM head,
-vocab 1000)."""
+layers, d 256, 4 heads x 64; one sequence runs the one-launch step), a small
+bfloat16 decoder (3 layers, d 192, 2 heads x 96, ffn 320: tiles of 16 rows
+leave ragged tails in the LM head, vocab 1000; rows not whole 1 KB pieces:
+the multi-kernel path) and a small bfloat16 decoder with head_dim 128 (3
+layers, d 512, 4 heads; the one-launch step)."""
 import numpy as np
 import pytest
 import torch
@@ -15,7 +17,7 @@ from tests.gpu_harness import Pair, Tally, oracle_draft_logits, pick_tau
 
 pytestmark = pytest.mark.gpu
 
-CASES = ["tiny", "small_bf16"]
+CASES = ["tiny", "small_bf16", "small_rw"]
 
 
 TAU_ALTERNATIVES = (0.45, 0.55, 0.4, 0.6, 0.35, 0.65, 0.3, 0.7)
