@@ -113,6 +113,7 @@ def moe_token_bytes(cfg, ctx: float) -> float:
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 GATEUP_COUNTERS = "kr_gateup_phi3_dual_ctx1024_hbm_counters.md"
+STEP_COUNTERS = "kp_step_phi3_dual_ctx1024_hbm_counters.md"
 
 
 def sources_digest() -> str:
@@ -291,20 +292,31 @@ def run_dense(args) -> int:
     ms_step = ms / args.steps
     ctx_mean = ctx0 + (args.steps - 1) / 2.0
 
-    # dominant kernel (gate/up projection): every layer's launch back to back
-    # between one pair of HIP events on the step's stream, repeated
+    # dominant kernel: the one-launch decode step (every layer and the head
+    # in one kernel) when the model's shape has it, timed with HIP events on
+    # the launch stream around direct launches; otherwise the gate/up kernel
+    # of the per-kernel path, every layer's launch back to back
     reps = max(1, args.kernel_reps)
-    k_avg_ms = sum(model.time_gateup_layers(dual, stream=stream) for _ in range(reps)) / reps
-    k_n = reps * cfg.n_layers
+    k_avg_ms, k_n = _kernel_avg_ms(model, "step", stream, step, reps)
+    torch.cuda.synchronize()
+    ctx_k = int(pos.item()) - (reps - 1) / 2.0 - 1
+    if k_n > 0:
+        kb = step_bytes(cfg, ctx_k, dual)
+        kname = "one-launch decode step (kp_step): all layers and the LM head"
+        traffic = stored_traffic(STEP_COUNTERS) if (args.config == "phi3" and dual) else None
+    else:
+        k_avg_ms = sum(model.time_gateup_layers(dual, stream=stream) for _ in range(reps)) / reps
+        k_n = reps * cfg.n_layers
+        kb = gateup_bytes(cfg, 2 if dual else 1, 1 if dual else 0)
+        kname = "gate/up projection, one output row per wave (kr_gateup)"
+        traffic = stored_traffic(GATEUP_COUNTERS) if (args.config == "phi3" and dual) else None
     errs = model.device_errors()
     if errs:
         print(f"device error bits {errs}", file=sys.stderr)
         return 1
-    kb = gateup_bytes(cfg, 2 if dual else 1, 1 if dual else 0)
     achieved = kb / (k_avg_ms * 1e-3) / 1e9
     sb = step_bytes(cfg, ctx_mean, dual)
     step_gbs = sb / (ms_step * 1e-3) / 1e9
-    traffic = stored_traffic(GATEUP_COUNTERS) if (args.config == "phi3" and dual) else None
 
     cpu = cpu_baseline(cfg, weights, args.ctx, args.cpu_budget) if args.cpu_budget > 0 else None
     _line(value=round(1000.0 / ms_step, 3), unit="tokens/s", steps=args.steps, warmup=args.warmup,
@@ -315,7 +327,7 @@ def run_dense(args) -> int:
                               f"KV context {args.ctx} (+{args.warmup + args.steps} decoded), HIP graph replay",
                   "batch": 1, "kv_context": args.ctx, "dual_stream": dual},
           step_hbm_gbs=round(step_gbs, 1), step_bytes=int(sb), step_roofline_frac=round(step_gbs / HBM_PEAK_GBS, 4),
-          roofline={"bound": "hbm", "kernel": "gate/up projection, one output row per wave (kr_gateup)", "achieved": round(achieved, 1),
+          roofline={"bound": "hbm", "kernel": kname, "achieved": round(achieved, 1),
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                     "traffic": traffic, "avg_kernel_us": round(k_avg_ms * 1e3, 3), "bytes_per_launch": int(kb),
                     "launches_timed": k_n},

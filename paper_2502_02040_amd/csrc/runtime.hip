@@ -877,7 +877,8 @@ hipError_t pk_attr(size_t lds, int* per_cu) {
 hipError_t pk_setup(m2r2_ctx* c) {
   c->pk.kind = -1;
   const Dims& D = c->D;
-  if (is_moe(c->cfg) || !c->rw_on) return hipSuccess;
+  // M2R2_ONE_LAUNCH=0 keeps one sequence on the multi-kernel path
+  if (is_moe(c->cfg) || !c->rw_on || getenv_zero("M2R2_ONE_LAUNCH")) return hipSuccess;
   int dev = 0, cus = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);

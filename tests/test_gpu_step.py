@@ -81,14 +81,30 @@ def _decode_run(name, *, mode, tau, gates, n_steps, adapter_scale=1.0, block_siz
     return t, exits, pair
 
 
+def _one_launch_steps(pair):
+    """Launches of the one-launch step kernel in one more decode step."""
+    dev = pair.dev
+    pos = pair.kv.seq_lens[:1].clone()
+    tok = torch.zeros(1, dtype=torch.int32, device=dev)
+    pair.model.timing_enable("step")
+    pair.model.decode_step(tok, pos, pair.kv.desc(), gates=[1], tau=0.5, mode="observe", next_token=tok,
+                           advance=False)
+    torch.cuda.synchronize()
+    n = pair.model.timing_read()[1]
+    pair.model.timing_enable(None)
+    return n
+
+
 @pytest.mark.parametrize("name", CASES)
 def test_dual_step_observe(name):
     """OBSERVE mode at every interior boundary: slow token, fast state,
     per-layer signal and the paged cache match the oracle step by step."""
     cfg = synth.CONFIGS[name]
     gates = list(range(1, cfg.n_layers))
-    t, _, _ = _decode_run(name, mode="observe", tau=0.9, gates=gates, n_steps=12)
+    t, _, pair = _decode_run(name, mode="observe", tau=0.9, gates=gates, n_steps=12)
     assert t.steps == 12 and t.compared >= 12
+    # which path one sequence took: the one-launch step where the shape has it
+    assert _one_launch_steps(pair) == (0 if name == "small_bf16" else 1)
 
 
 @pytest.mark.parametrize("name", CASES)
@@ -100,6 +116,19 @@ def test_dual_step_exit(name, tau):
     assert t.steps == 8 and t.compared >= 8
     if tau < 0:
         assert exits == 8
+
+
+@pytest.mark.parametrize("name", ["tiny", "small_rw"])
+@pytest.mark.parametrize("mode,tau,gates", [("observe", 0.9, None), ("exit", 0.5, [1])])
+def test_one_sequence_on_the_multi_kernel_path(name, mode, tau, gates, monkeypatch):
+    """The shapes that have the one-launch step, with it switched off: one
+    sequence runs the multi-kernel path (one launch per phase and layer),
+    which must match the oracle as well."""
+    monkeypatch.setenv("M2R2_ONE_LAUNCH", "0")
+    cfg = synth.CONFIGS[name]
+    t, _, pair = _decode_run(name, mode=mode, tau=tau, gates=gates or list(range(1, cfg.n_layers)), n_steps=6)
+    assert t.steps == 6 and t.compared >= 6
+    assert _one_launch_steps(pair) == 0
 
 
 def _arla(name, bias=0.0):
