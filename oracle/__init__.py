@@ -24,9 +24,9 @@ textbook LRU).  Quantities that depend on trained weights (acceptance rates,
 hit rates of real routers) are parity unpinned and are not claimed.
 """
 from .decoder import (Oracle, KVCache, StepResult, rms_norm, rope, attend, silu, topk_desc,
-                      round_to_cache, arla_score, ARLA_DIM)
+                      round_to_cache, arla_score, ARLA_DIM, select_top, top_gap)
 from .cache_sim import simulate_expert_cache, simulate_fixed_experts, CacheStats
 
 __all__ = ["Oracle", "KVCache", "StepResult", "rms_norm", "rope", "attend", "silu", "topk_desc",
            "round_to_cache", "simulate_expert_cache", "simulate_fixed_experts", "CacheStats", "arla_score",
-           "ARLA_DIM"]
+           "ARLA_DIM", "select_top", "top_gap"]

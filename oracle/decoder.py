@@ -26,6 +26,14 @@ justification in the design notes of the repository):
   * When a token exits at gate b (Eq. 4), its token comes from the final norm
     and LM head applied to ``p`` at the gate, and the skipped layers' cache
     entries at t are projected from the slow ``h`` at the gate.
+  * FLOPs-optimised fast stream (Sec. 2.5), for dense models whose config
+    sets it: the fast row keeps only the first ``fast_heads`` heads (q, k, v
+    and the o input of the others are zero); fast head j attends to the
+    ``fast_topk`` cached positions with the largest scores of the slow row's
+    head j at the same layer (all positions when there are no more than
+    that; ties to the lower position), plus its own key/value; its MLP is the
+    rank-r adapter ``m`` alone, as for MoE layers; a token it emits comes
+    from the final norm and a rank-``head_rank`` head ``head_A``, ``head_B``.
 """
 from __future__ import annotations
 
@@ -80,6 +88,25 @@ def topk_desc(v: np.ndarray, k: int) -> np.ndarray:
     """Indices of the k largest entries, by descending value, ties to the lower index."""
     order = np.lexsort((np.arange(v.shape[-1]), -v))
     return order[:k]
+
+
+def select_top(scores: np.ndarray, k: int) -> np.ndarray:
+    """Positions of the ``k`` largest scores in increasing position order
+    (every position when there are no more than ``k``; ``k <= 0``: all)."""
+    n = scores.shape[0]
+    if k <= 0 or n <= k:
+        return np.arange(n)
+    return np.sort(topk_desc(scores, k))
+
+
+def top_gap(scores: np.ndarray, k: int) -> float:
+    """Distance between the k-th and the (k+1)-th largest score: how far the
+    selection of ``select_top`` is from a tie (inf when it takes everything)."""
+    n = scores.shape[0]
+    if k <= 0 or n <= k:
+        return math.inf
+    srt = np.sort(scores)[::-1]
+    return float(srt[k - 1] - srt[k])
 
 
 def argmax_first(v: np.ndarray) -> int:
@@ -174,6 +201,7 @@ class StepResult:
     prev_pred_logits: Optional[np.ndarray] = None    # [N, E] the logits behind prev_pred_experts
     fast_states: Optional[np.ndarray] = None    # [N, d] p after each layer (before a gate's restart), nan if not run
     router_logits: Optional[np.ndarray] = None  # [N, E] slow-router logits (MoE)
+    topk_gap: Optional[np.ndarray] = None       # [N, H] FLOPs mode: top_gap of each fast head's selection (inf: none)
 
 
 # ----------------------------------------------------------------------------
@@ -253,12 +281,21 @@ class Oracle:
         return y, S, pz, z
 
     def _fast_moe_mlp(self, l: int, x: np.ndarray) -> np.ndarray:
-        """Fast-stream MLP of an MoE layer: the rank-r adapter alone."""
+        """Fast-stream MLP of an MoE layer (or of a dense layer in the FLOPs-
+        optimised form): the rank-r adapter alone."""
         m = rms_norm(x, self._W(l, "mlp_norm"), self.cfg.rms_eps)
         return self._adapter(l, "m", m)
 
     def head_logits(self, x: np.ndarray) -> np.ndarray:
         return rms_norm(x, self.w["final_norm"], self.cfg.rms_eps) @ self.w["lm_head"].T
+
+    def fast_head_logits(self, x: np.ndarray) -> np.ndarray:
+        """Logits of a token the fast row emits: the low-rank head of the
+        FLOPs-optimised form when the config has one, else the LM head."""
+        if not self.cfg.head_rank:
+            return self.head_logits(x)
+        u = rms_norm(x, self.w["final_norm"], self.cfg.rms_eps)
+        return (u @ self.w["head_A"].T) @ self.w["head_B"].T
 
     # -- one layer, one position, slow row --------------------------------------
     def _slow_layer(self, l: int, h: np.ndarray, pos: int, cache: KVCache, moe_out=None) -> np.ndarray:
@@ -286,6 +323,32 @@ class Oracle:
         if self.cfg.is_moe:
             return p1 + self._fast_moe_mlp(l, p1), (k, v)
         return p1 + self._dense_mlp(l, p1, fast=True), (k, v)
+
+    def _fast_layer_flops(self, l: int, p: np.ndarray, h: np.ndarray, pos: int, ctxK: np.ndarray,
+                          ctxV: np.ndarray):
+        """Fast row of layer l in the FLOPs-optimised form (Sec. 2.5).  The
+        slow row's query of the same layer (from ``h``, the slow state
+        entering it) scores the cached context; fast head j < fast_heads
+        attends to the positions ``select_top`` keeps for slow head j plus its
+        own key/value; the other heads contribute nothing.  Returns the new p
+        and the selection gaps of the heads [H]."""
+        cfg = self.cfg
+        nh = cfg.fast_heads or cfg.n_heads
+        qs, _, _ = self._qkv(l, h, pos, fast=False)
+        q, k, v = self._qkv(l, p, pos, fast=True)
+        o = np.zeros_like(q)
+        gaps = np.full(cfg.n_heads, math.inf)
+        for j in range(nh):
+            s = ctxK[:, j] @ qs[j] / math.sqrt(cfg.head_dim)
+            sel = select_top(s, cfg.fast_topk)
+            gaps[j] = top_gap(s, cfg.fast_topk)
+            Kj = np.concatenate([ctxK[sel, j], k[j][None]], axis=0)
+            Vj = np.concatenate([ctxV[sel, j], v[j][None]], axis=0)
+            o[j] = attend(q[j][None], Kj[:, None], Vj[:, None])[0]
+        p1 = p + self._attn_out(l, o, fast=True)
+        if cfg.fast_mlp_adapter:
+            return p1 + self._fast_moe_mlp(l, p1), gaps
+        return p1 + self._dense_mlp(l, p1, fast=True), gaps
 
     def _kv_fill(self, l: int, h: np.ndarray, pos: int, cache: KVCache) -> None:
         """Cache entry of a skipped layer: projected from the slow state at the gate."""
@@ -320,11 +383,16 @@ class Oracle:
         pred = np.full((N, max(cfg.top_k, 1)), -1, np.int64)
         pred_logits = np.full((N, max(cfg.n_experts, 1)), np.nan)
         self._fast_states = np.full((N, cfg.d_model), np.nan)
+        self._topk_gap = np.full((N, cfg.n_heads), np.inf) if cfg.is_flops else None
         interval: List[np.ndarray] = []   # fast states since the last gate
         for l in range(N):
             p_in = p
             # fast row first: it sees the cache before the slow row writes position pos
-            p, _ = self._fast_layer(l, p, pos, cache.K[l][:pos], cache.V[l][:pos])
+            if cfg.is_flops:
+                assert not cfg.is_moe, "the FLOPs-optimised form is defined here for dense models"
+                p, self._topk_gap[l] = self._fast_layer_flops(l, p, h, pos, cache.K[l][:pos], cache.V[l][:pos])
+            else:
+                p, _ = self._fast_layer(l, p, pos, cache.K[l][:pos], cache.V[l][:pos])
             h = self._slow_layer(l, h, pos, cache, moe_rec)
             self._fast_states[l] = p
             interval.append(p)
@@ -349,7 +417,7 @@ class Oracle:
                 if mode == "exit" and fired:
                     for l2 in range(b, N):
                         self._kv_fill(l2, h, pos, cache)
-                    logits = self.head_logits(p)
+                    logits = self.fast_head_logits(p)
                     return self._result(logits, exit_b, signal, h, p, moe_rec, pred, pred_logits)
                 p = h.copy()
         logits = self.head_logits(h)
@@ -358,7 +426,7 @@ class Oracle:
     def _result(self, logits, exit_b, signal, h, p, moe_rec, pred, pred_logits) -> StepResult:
         cfg = self.cfg
         r = StepResult(token=argmax_first(logits), logits=logits, exit_boundary=exit_b, signal=signal, h=h, p=p,
-                       fast_states=self._fast_states)
+                       fast_states=self._fast_states, topk_gap=self._topk_gap)
         if cfg.is_moe:
             n = len(moe_rec)
             r.slow_experts = np.array([m[0] for m in moe_rec]).reshape(n, cfg.top_k)
@@ -411,6 +479,9 @@ class Oracle:
         earlier draft positions are kept, in cache precision, in a scratch area
         that later drafts attend to; the slow cache is not modified."""
         cfg = self.cfg
+        if cfg.is_flops:
+            raise ValueError("a fast-only draft has no slow-row scores: the FLOPs-optimised form is the "
+                             "dual-stream step's")
         scK = [np.zeros((gamma, cfg.n_heads, cfg.head_dim), self.dtype) for _ in range(exit_layer)]
         scV = [np.zeros((gamma, cfg.n_heads, cfg.head_dim), self.dtype) for _ in range(exit_layer)]
         out = []

@@ -59,6 +59,15 @@ class ModelConfig:
     top_k: int = 0
     expert_ffn: int = 0
     seed: int = 0
+    # FLOPs-optimised accelerated stream (dense models; all zero / False:
+    # the memory-bound form): the fast row uses the first ``fast_heads``
+    # heads, each attending to ``fast_topk`` cached positions; its MLP is the
+    # rank-``rank`` adapter ``m`` alone; its tokens come from a rank-
+    # ``head_rank`` head ``head_A [head_rank][d]``, ``head_B [vocab][head_rank]``
+    fast_heads: int = 0
+    fast_topk: int = 0
+    fast_mlp_adapter: bool = False
+    head_rank: int = 0
 
     @property
     def qdim(self) -> int:
@@ -67,6 +76,10 @@ class ModelConfig:
     @property
     def is_moe(self) -> bool:
         return self.n_experts > 0
+
+    @property
+    def is_flops(self) -> bool:
+        return bool(self.fast_heads or self.fast_topk or self.fast_mlp_adapter or self.head_rank)
 
     def replace(self, **kw) -> "ModelConfig":
         return dataclasses.replace(self, **kw)
@@ -102,6 +115,19 @@ CONFIGS: Dict[str, ModelConfig] = {
     "small_moe_rw": ModelConfig("small_moe_rw", n_layers=4, d_model=512, n_heads=4, head_dim=128, ffn=0, vocab=1000,
                                 rank=8, wdtype="bf16", kvdtype="bf16", n_experts=16, top_k=4, expert_ffn=96, seed=23),
 }
+# FLOPs-optimised fast stream on the same shapes: a quarter of the heads
+# (half for the small decoders), top-64 positions (8 at test sizes), the
+# adapter-only MLP and a low-rank head for the fast row's tokens
+CONFIGS["phi3_flops"] = CONFIGS["phi3"].replace(name="phi3_flops", fast_heads=8, fast_topk=64, fast_mlp_adapter=True,
+                                                head_rank=64)
+CONFIGS["tiny_flops"] = CONFIGS["tiny"].replace(name="tiny_flops", fast_heads=2, fast_topk=8, fast_mlp_adapter=True,
+                                                head_rank=16)
+CONFIGS["small_bf16_flops"] = CONFIGS["small_bf16"].replace(name="small_bf16_flops", fast_heads=1, fast_topk=8,
+                                                            fast_mlp_adapter=True, head_rank=16)
+CONFIGS["small_rw_flops"] = CONFIGS["small_rw"].replace(name="small_rw_flops", fast_heads=2, fast_topk=8,
+                                                        fast_mlp_adapter=True, head_rank=32)
+CONFIGS["micro_flops"] = CONFIGS["micro"].replace(name="micro_flops", fast_heads=1, fast_topk=3, fast_mlp_adapter=True,
+                                                  head_rank=3)
 
 
 # ----------------------------------------------------------------------------
@@ -154,11 +180,13 @@ def tensor_specs(cfg: ModelConfig) -> List[Tuple[str, Tuple[int, ...], str]]:
         else:
             specs += [(p + "wg", (cfg.ffn, d), "normal"), (p + "wu", (cfg.ffn, d), "normal"),
                       (p + "wd", (d, cfg.ffn), "normal")]
-            projs = PROJ_DENSE
+            projs = PROJ_MOE if cfg.fast_mlp_adapter else PROJ_DENSE
         for pr in projs:
             din, dout = _adapter_dims(cfg, pr)
             specs += [(p + f"A_{pr}", (r, din), "normal"), (p + f"B_{pr}", (dout, r), "normal")]
     specs += [("final_norm", (d,), "ones"), ("lm_head", (cfg.vocab, d), "normal")]
+    if cfg.head_rank:
+        specs += [("head_A", (cfg.head_rank, d), "normal"), ("head_B", (cfg.vocab, cfg.head_rank), "normal")]
     return specs
 
 

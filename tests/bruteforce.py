@@ -6,7 +6,10 @@ vectorised oracle (a transposed weight, a wrong head slice, a RoPE pair index,
 an adapter on the wrong projection, the wrong keys for the fast query) shows
 up as a mismatch.  It follows the paper's equations directly: Eq. 1 for the
 slow row, Eq. 2 with low-rank adapters for the fast row, the shared KV cache
-of Sec. 2.2, re-initialisation at gates (Fig. 3 caption) and the exit of Eq. 4.
+of Sec. 2.2, re-initialisation at gates (Fig. 3 caption) and the exit of Eq. 4,
+and the FLOPs-optimised fast stream of Sec. 2.5 (pruned heads, a context
+chosen by sorting the slow row's scores, the adapter-only MLP and the
+low-rank head).
 """
 from __future__ import annotations
 
@@ -79,6 +82,25 @@ def mha(q, keys, vals, H, hd):
     return out
 
 
+def one_head(q, keys, vals, hh, hd):
+    """Attention of head hh alone over the given rows: its hd outputs."""
+    sl = range(hh * hd, (hh + 1) * hd)
+    sc = []
+    for k in keys:
+        s = 0.0
+        for d in sl:
+            s += q[d] * k[d]
+        sc.append(s / math.sqrt(hd))
+    mx = max(sc)
+    e = [math.exp(s - mx) for s in sc]
+    tot = sum(e)
+    out = [0.0] * hd
+    for j, v in enumerate(vals):
+        for i, d in enumerate(sl):
+            out[i] += e[j] / tot * v[d]
+    return out
+
+
 def silu(x):
     return x / (1.0 + math.exp(-x))
 
@@ -142,6 +164,33 @@ class BruteDecoder:
     def head(self, x):
         return mv(self.W["lm_head"], rms(x, self.W["final_norm"], self.cfg.rms_eps))
 
+    def fast_head(self, x):
+        if not self.cfg.head_rank:
+            return self.head(x)
+        return mv(self.W["head_B"], mv(self.W["head_A"], rms(x, self.W["final_norm"], self.cfg.rms_eps)))
+
+    def fast_attention_flops(self, l, q_slow, qp, kp, vp, pos):
+        """FLOPs-optimised fast attention (Sec. 2.5): head hh < fast_heads
+        keeps the fast_topk cached positions whose slow-row score (head hh)
+        is largest, by a plain sort on (-score, position); other heads give 0."""
+        c = self.cfg
+        hd = c.head_dim
+        nh = c.fast_heads or c.n_heads
+        out = [0.0] * (c.n_heads * hd)
+        for hh in range(nh):
+            sc = []
+            for t in range(pos):
+                s = 0.0
+                for d in range(hh * hd, (hh + 1) * hd):
+                    s += q_slow[d] * self.K[l][t][d]
+                sc.append(s / math.sqrt(hd))
+            keep = list(range(pos))
+            if 0 < c.fast_topk < pos:
+                keep = sorted(sorted(range(pos), key=lambda t: (-sc[t], t))[:c.fast_topk])
+            o = one_head(qp, [self.K[l][t] for t in keep] + [kp], [self.V[l][t] for t in keep] + [vp], hh, hd)
+            out[hh * hd:(hh + 1) * hd] = o
+        return out
+
     def step(self, token: int, pos: int, gates: Sequence[int] = (), tau: float = 2.0, mode: str = "observe"):
         """Returns dict(logits, h, p, signal, exit_boundary, experts)."""
         c = self.cfg
@@ -166,9 +215,15 @@ class BruteDecoder:
             h = add(h1, y)
             # fast row: slow cache before pos, then its own k/v
             qp, kp, vp = self.qkv(l, p, pos, fast=True)
-            op = mha(qp, self.K[l][:pos] + [kp], self.V[l][:pos] + [vp], c.n_heads, c.head_dim)
+            if c.is_flops:
+                op = self.fast_attention_flops(l, q, qp, kp, vp, pos)
+            else:
+                op = mha(qp, self.K[l][:pos] + [kp], self.V[l][:pos] + [vp], c.n_heads, c.head_dim)
             p1 = add(add(p, mv(self.W[f"L{l}.wo"], op)), self.lora(l, "o", op))
-            yp, _ = self.mlp(l, p1, fast=True)
+            if c.fast_mlp_adapter:
+                yp = self.lora(l, "m", rms(p1, self.W[f"L{l}.mlp_norm"], c.rms_eps))
+            else:
+                yp, _ = self.mlp(l, p1, fast=True)
             p = add(p1, yp)
             dot = sum(p_in[i] * p[i] for i in range(len(p)))
             na = math.sqrt(sum(v * v for v in p_in))
@@ -188,7 +243,7 @@ class BruteDecoder:
                         _, k2, v2 = self.qkv(l2, h, pos, fast=False)
                         self.K[l2].append(store(k2, c.kvdtype))
                         self.V[l2].append(store(v2, c.kvdtype))
-                    return dict(logits=self.head(p), h=h, p=p, signal=signal, exit_boundary=exit_b,
+                    return dict(logits=self.fast_head(p), h=h, p=p, signal=signal, exit_boundary=exit_b,
                                 experts=experts, preds=preds)
                 p = list(h)
         return dict(logits=self.head(h), h=h, p=p, signal=signal, exit_boundary=exit_b, experts=experts,
