@@ -24,7 +24,7 @@
 // are written by every workgroup into its own slot and summed by each
 // consumer in one fixed order: the step is deterministic, run to run.
 //
-// The grid barrier spins on one agent-scope counter with a time limit: if
+// The grid barrier polls its group flags with a time limit: if
 // the workgroups were not all resident (they are, one per compute unit, when
 // nothing else runs), every wave gives up after the limit, sets device error
 // bit 16 and runs to the end, so the launch always drains.
@@ -48,11 +48,13 @@ struct PkPc {
   static constexpr int NS = N > 8 ? N / 8 : 1;
 };
 
-constexpr int kPkRelStride = 32;   // uint32 words between release words (128 bytes)
+constexpr int kPkRelStride = 32;   // uint32 words between barrier words (128 bytes)
+
+constexpr int kPkGroups = 8;       // arrival groups of the grid barrier
 
 struct PkBar {
-  uint32_t* ctr;    // arrivals of this launch
-  uint32_t* rel;    // [G][kPkRelStride] release words (epoch of the last released barrier)
+  uint32_t* ctr;    // [kPkGroups][kPkRelStride] arrivals of each group in this launch
+  uint32_t* flag;   // [kPkGroups][kPkRelStride] epoch of each group's last completed count
 };
 
 struct PkArgs {
@@ -68,7 +70,7 @@ struct PkArgs {
   float* sd;                 // [G][kPkSdW] rows' x^2, pin.x, pin^2 leaving the down projection
   float* so;                 // [G][so_w]   x^2 of rows 0, 1 after the o projection; gate, up adapter-down (fast row)
   float* sgu;                // [G][sgu_w]  down adapter-down of the fast row
-  PkBar bar;                 // grid barrier: counter and release words, zero at launch, reset by the last workgroup
+  PkBar bar;                 // grid barrier: group counters and flags, zero at launch, reset by the last workgroup
   int n_layers_run;
   int S;                     // attention splits per head
   int so_w, sgu_w;
@@ -87,44 +89,45 @@ __device__ __forceinline__ float4 pk_ld4(__amdgpu_buffer_rsrc_t rs, int byte_off
 }
 
 // ---------------------------------------------------------------------------
-// Split grid barrier.  Arrival: one agent-scope atomic add per workgroup on
-// one counter; the workgroup whose add completes the count writes the
-// barrier's epoch into every workgroup's release word (one 128-byte line
-// each), and every workgroup polls only its own line (one counter polled by
-// every workgroup serialises at the memory side: the release reached the
-// last workgroup microseconds after the first).
+// Split grid barrier over arrival groups.  Workgroup b belongs to group
+// b % kPkGroups (under the default dispatch, one group per XCD).  Arrival:
+// one agent-scope atomic add on the group's counter; the workgroup whose add
+// completes its group's count for this epoch stores the epoch into the
+// group's flag.  Waiting: one wave polls the kPkGroups flags (one 128-byte
+// line each) until all have reached the epoch.  Measured on this chip with
+// no work between barriers: 2.0 us per barrier, against 4.2 us for one
+// counter over all workgroups whose last arriver releases every workgroup
+// (same-address atomics serialise at the memory side, and the release is a
+// second round trip).
 // ---------------------------------------------------------------------------
 // Count this workgroup in once every wave's stores are complete; `epoch` is
-// the barrier's number in the launch (1, 2, ...), so the count completes at
-// epoch * G arrivals.
-// `self` (thread 0's word in LDS) records whether this workgroup released
-// the barrier: it then does not poll its own line.
-__device__ __forceinline__ void pk_arrive(const PkBar& b, uint32_t epoch, int* self) {
+// the barrier's number in the launch (1, 2, ...), so a group's count
+// completes at epoch * (its size) arrivals.
+__device__ __forceinline__ void pk_arrive(const PkBar& b, uint32_t epoch) {
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  if (threadIdx.x < 64) {
-    uint32_t last = 0;
-    if (threadIdx.x == 0) {
-      const uint32_t old = __hip_atomic_fetch_add(b.ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      last = old == epoch * gridDim.x - 1;
-      *self = (int)last;
-    }
-    if (__shfl(last, 0)) {
-      for (int w = threadIdx.x; w < (int)gridDim.x; w += 64)
-        __hip_atomic_store(&b.rel[w * kPkRelStride], epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
+  if (threadIdx.x == 0) {
+    const int g = blockIdx.x % kPkGroups;
+    const uint32_t per = (gridDim.x - g + kPkGroups - 1) / kPkGroups;
+    const uint32_t old = __hip_atomic_fetch_add(&b.ctr[g * kPkRelStride], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (old == epoch * per - 1)
+      __hip_atomic_store(&b.flag[g * kPkRelStride], epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
-// Wait for this workgroup's release word to reach `epoch` (or the time limit).
-__device__ __forceinline__ void pk_wait(const PkBar& b, uint32_t epoch, int* err, int* broken, const int* self) {
-  if (threadIdx.x == 0 && !*broken && !*self) {
-    uint32_t* w = &b.rel[blockIdx.x * kPkRelStride];
+// Wait until every group's flag has reached `epoch` (or the time limit).
+__device__ __forceinline__ void pk_wait(const PkBar& b, uint32_t epoch, int* err, int* broken) {
+  if (threadIdx.x < 64 && !*broken) {
+    const int ng = min(kPkGroups, (int)gridDim.x);
     const uint64_t t0 = wall_clock64();
-    while (__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < epoch) {
-      __builtin_amdgcn_s_sleep(1);
-      if (wall_clock64() - t0 > kPkSpinTicks) {
-        atomicOr(err, 16);
-        *broken = 1;
+    while (true) {
+      const bool ok = (int)threadIdx.x >= ng ||
+                      __hip_atomic_load(&b.flag[threadIdx.x * kPkRelStride], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= epoch;
+      if (__all(ok)) break;
+      if (wall_clock64() - t0 > kPkSpinTicks) {   // uniform: the clock is a scalar read
+        if (threadIdx.x == 0) {
+          atomicOr(err, 16);
+          *broken = 1;
+        }
         break;
       }
     }
@@ -402,7 +405,7 @@ struct PkShared {
   float tot[64];
   float inv_rms[2];
   int src[2];
-  int ex, eb, ri, broken, last_flag, rel_self;
+  int ex, eb, ri, broken, last_flag;
   float bz[kPkWaves];
   int bi[kPkWaves];
 };
@@ -511,7 +514,7 @@ __device__ __forceinline__ void pk_phase_qkv(int l, uint32_t& target, PkShared& 
       st.begin_all(row_ptr, u0, u1, epi, ops);
       if (l > 0) {
         target += 1;
-        pk_wait(P.bar, target, P.ws.err, &sh.broken, &sh.rel_self);
+        pk_wait(P.bar, target, P.ws.err, &sh.broken);
       }
       constexpr int PM = RwPM<WB, CD::NCH, CD::NS, kPkThreads>::value;
       RwPieces<PM> xp;
@@ -596,7 +599,7 @@ __device__ __forceinline__ void pk_phase_qkv(int l, uint32_t& target, PkShared& 
       }
       rw_store_pieces<true, PM, kPkThreads>(xp, d, pk_dyn);
       st.template run<true>(row_ptr, u0, u1, pk_dyn, d, epi, ops);
-      pk_arrive(P.bar, target + 1, &sh.rel_self);
+      pk_arrive(P.bar, target + 1);
     }
 
 }
@@ -685,7 +688,7 @@ __device__ __forceinline__ void pk_phase_att(int l, uint32_t& target, PkShared& 
         cs = P.ws.rope[(size_t)pos * (HD / 2) + (e_d % (HD / 2))];
       }
       target += 1;
-      pk_wait(P.bar, target, P.ws.err, &sh.broken, &sh.rel_self);
+      pk_wait(P.bar, target, P.ws.err, &sh.broken);
       if (has) {
         // ---- projections of this head (coherent loads)
         float pv[3];
@@ -992,7 +995,7 @@ __device__ __forceinline__ void pk_phase_att(int l, uint32_t& target, PkShared& 
           }
         }
       }
-      pk_arrive(P.bar, target + 1, &sh.rel_self);
+      pk_arrive(P.bar, target + 1);
     }
 
 }
@@ -1019,7 +1022,7 @@ __device__ __forceinline__ void pk_phase_o(int l, uint32_t& target, PkShared& sh
       typename PkOEpi<WB>::Ops ops[decltype(st)::P];
       st.begin_all(row_ptr, u0, u1, epi, ops);
       target += 1;
-      pk_wait(P.bar, target, P.ws.err, &sh.broken, &sh.rel_self);
+      pk_wait(P.bar, target, P.ws.err, &sh.broken);
       epi.ri = sh.ri;
       constexpr int PM = RwPM<WB, CQ::NCH, CQ::NS, kPkThreads>::value;
       RwPieces<PM> xp;
@@ -1033,7 +1036,7 @@ __device__ __forceinline__ void pk_phase_o(int l, uint32_t& target, PkShared& sh
       pk_wg_store<kPkWaves>(epi.accx, 2, sh.wsum, sh.tot, slot);
       pk_wg_store<kPkWaves>(fm >= 0 ? epi.accf : 0.f, 2 * r, sh.wsum, sh.tot, slot + 2);
       if (tid >= 2 + 2 * r && tid < P.so_w) st_agent(slot + tid, 0.f);   // the slot's padding
-      pk_arrive(P.bar, target + 1, &sh.rel_self);
+      pk_arrive(P.bar, target + 1);
     }
 
 }
@@ -1066,7 +1069,7 @@ __device__ __forceinline__ void pk_phase_gu(int l, uint32_t& target, PkShared& s
       typename PkGuEpi<WB>::Ops ops[decltype(st)::P];
       st.begin_all(row_ptr, u0, u1, epi, ops);
       target += 1;
-      pk_wait(P.bar, target, P.ws.err, &sh.broken, &sh.rel_self);
+      pk_wait(P.bar, target, P.ws.err, &sh.broken);
       constexpr int PM = RwPM<WB, CD::NCH, CD::NS, kPkThreads>::value;
       RwPieces<PM> xp;
       pk_load_rows<PM>(P.ws.X, 0, (M > 1 ? 1 : 0) * d, mlp_norm, d, xp);
@@ -1075,7 +1078,7 @@ __device__ __forceinline__ void pk_phase_gu(int l, uint32_t& target, PkShared& s
       rw_store_pieces<true, PM, kPkThreads>(xp, d, pk_dyn);
       st.template run<true>(row_ptr, u0, u1, pk_dyn, d, epi, ops);
       pk_wg_store<kPkWaves>(fm >= 0 ? epi.accf : 0.f, r, sh.wsum, sh.tot, P.sgu + (size_t)blockIdx.x * P.sgu_w);
-      pk_arrive(P.bar, target + 1, &sh.rel_self);
+      pk_arrive(P.bar, target + 1);
     }
 
 }
@@ -1102,7 +1105,7 @@ __device__ __forceinline__ void pk_phase_dn(int l, uint32_t& target, PkShared& s
       typename PkDnEpi<WB>::Ops ops[decltype(st)::P];
       st.begin_all(row_ptr, u0, u1, epi, ops);
       target += 1;
-      pk_wait(P.bar, target, P.ws.err, &sh.broken, &sh.rel_self);
+      pk_wait(P.bar, target, P.ws.err, &sh.broken);
       constexpr int PM = RwPM<WB, CF::NCH, CF::NS, kPkThreads>::value;
       RwPieces<PM> xp;
       pk_load_rows<PM>(P.ws.ACT, 0, (M > 1 ? 1 : 0) * D.F, nullptr, D.F, xp);
@@ -1110,7 +1113,7 @@ __device__ __forceinline__ void pk_phase_dn(int l, uint32_t& target, PkShared& s
       rw_store_pieces<false, PM, kPkThreads>(xp, D.F, pk_dyn);
       st.template run<true>(row_ptr, u0, u1, pk_dyn, D.F, epi, ops);
       pk_wg_store<kPkWaves>(epi.acc, kPkSdW, sh.wsum, sh.tot, P.sd + (size_t)blockIdx.x * kPkSdW);
-      pk_arrive(P.bar, target + 1, &sh.rel_self);
+      pk_arrive(P.bar, target + 1);
     }
 }
 
@@ -1134,7 +1137,7 @@ __device__ __forceinline__ void pk_phase_head(int l, uint32_t& target, PkShared&
     PkHeadEpi::Ops ops[decltype(st)::P];
     st.begin_all(row_ptr, u0, u1, epi, ops);
     target += 1;
-    pk_wait(P.bar, target, P.ws.err, &sh.broken, &sh.rel_self);
+    pk_wait(P.bar, target, P.ws.err, &sh.broken);
     constexpr int PM = RwPM<WB, CD::NCH, CD::NS, kPkThreads>::value;
     RwPieces<PM> xp;
     pk_load_rows<PM>(P.ws.X, 0, (M > 1 ? 1 : 0) * d, P.final_norm, d, xp);
@@ -1169,9 +1172,10 @@ __device__ __forceinline__ void pk_phase_head(int l, uint32_t& target, PkShared&
     if (!arrive_last(P.ws.lm_cnt, G, &sh.last_flag)) return;
     // ---- the last workgroup: global arg-max and the step's bookkeeping
     // reset the barrier for the next launch (every workgroup has passed its last wait)
-    if (tid == 0) __hip_atomic_store(P.bar.ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    for (int w = tid; w < G; w += kPkThreads)
-      __hip_atomic_store(&P.bar.rel[w * kPkRelStride], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (tid < kPkGroups) {
+      __hip_atomic_store(&P.bar.ctr[tid * kPkRelStride], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&P.bar.flag[tid * kPkRelStride], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     if (wv != 0) return;
     float bz = -INFINITY;
     int bi = 0x7fffffff;

@@ -260,8 +260,8 @@ Layout make_layout(const m2r2_config& c, int max_batch, int max_chunk, int max_c
   L.lm_cnt = take(sizeof(uint32_t));
   L.arla_cnt = take(sizeof(uint32_t));
   L.sk_cnt = take(sizeof(uint32_t) * (65 + std::max({L.TD, L.TF, L.TV, 3 * ((qdim + 15) / 16) + (3 * r + 15) / 16})));
-  L.pk_bar = take(sizeof(uint32_t));
-  L.pk_rel = take(sizeof(uint32_t) * kPkRelStride * kPkMaxWG);
+  L.pk_bar = take(sizeof(uint32_t) * kPkRelStride * kPkGroups);
+  L.pk_rel = take(sizeof(uint32_t) * kPkRelStride * kPkGroups);
   L.scratch_end = off;
   // ---- context state: sticky error bits, RoPE table, expert cache
   L.err = take(sizeof(int));
