@@ -59,7 +59,12 @@ def layer_weight_bytes(cfg, dual: bool = True) -> float:
     d, q, F, r = cfg.d_model, cfg.qdim, cfg.ffn, cfg.rank
     ew = 2 if cfg.wdtype == "bf16" else 4
     mats = (3 * q * d + d * q + 2 * F * d + d * F) * ew
-    adapters = r * ((d + q) * 3 + (q + d) + (d + F) * 2 + (F + d)) * ew if dual else 0
+    if getattr(cfg, "fast_mlp_adapter", False):
+        # FLOPs-optimised fast stream: q, k, v, o adapters and the MLP adapter
+        # (its selected keys/values are cache bytes the slow row reads anyway)
+        adapters = r * ((d + q) * 3 + (q + d) + 2 * d) * ew if dual else 0
+    else:
+        adapters = r * ((d + q) * 3 + (q + d) + (d + F) * 2 + (F + d)) * ew if dual else 0
     return mats + adapters + 2 * d * 4
 
 

@@ -100,6 +100,27 @@ typedef struct {
    * per layer (top_k <= expert_slots <= n_experts; = n_experts keeps every
    * expert resident). */
   int32_t n_experts, top_k, expert_ffn, expert_slots;
+  /* FLOPs-optimised accelerated stream (Sec. 2.5), dense models only; all
+   * zero selects the memory-bound form above.
+   *  fast_heads:        the fast row keeps heads 0 .. fast_heads-1 (0: all);
+   *                     the attention output of the other heads is zero for it.
+   *  fast_topk:         fast head j attends to the fast_topk cached positions
+   *                     with the largest scores of the slow row's head j at the
+   *                     same layer (ties to the lower position; every cached
+   *                     position when there are no more), plus its own
+   *                     key/value (0: every cached position).
+   *  fast_mlp_adapter:  1: the fast row's MLP is the rank-r adapter alone,
+   *                     (m A_m^T) B_m^T with m = rms(x) * mlp_norm, from the
+   *                     layer's A_m/B_m (the gate/up/down adapters are unused).
+   *  head_rank:         a token the fast row emits (an exit in EXIT mode) comes
+   *                     from the final norm and the rank-head_rank head
+   *                     head_a [head_rank][d], head_b [vocab][head_rank] of
+   *                     m2r2_weights (0: the LM head).
+   * Supported for one sequence (batch 1) on shapes whose rows are whole
+   * multiples of 1 KB (the row-per-wave kernels); m2r2_draft and the exit
+   * router are refused with M2R2_E_UNSUPPORTED (a fast-only pass has no
+   * slow-row scores to select positions with). */
+  int32_t fast_heads, fast_topk, fast_mlp_adapter, head_rank;
 } m2r2_config;
 
 /* Per-layer device pointers.  Any adapter pointer may be NULL (adapter
@@ -119,7 +140,8 @@ typedef struct {
   const void* B[7];
   /* mixture-of-experts layers: wg, wu, wd and A/B[4..6] are NULL; the router
    * and the fast row's MLP, which is the rank-r adapter alone (Sec. 2.3.3):
-   * MLP_fast(x) = (m A_m^T) B_m^T with m = rms(x) * mlp_norm */
+   * MLP_fast(x) = (m A_m^T) B_m^T with m = rms(x) * mlp_norm.  A dense model
+   * with fast_mlp_adapter set takes its fast MLP from A_m/B_m too (Sec. 2.5). */
   const void* router;       /* [n_experts][d] */
   const void* A_m;          /* [rank][d], may be NULL with B_m (fast MLP absent) */
   const void* B_m;          /* [d][rank] */
@@ -135,6 +157,10 @@ typedef struct {
    * (l * n_experts + e) * m2r2_expert_bytes(), each filled by
    * m2r2_pack_expert.  Borrowed for the lifetime of the context. */
   const void* experts_h;
+  /* low-rank head of the FLOPs-optimised fast stream (config head_rank > 0):
+   * head_a [head_rank][d], head_b [vocab][head_rank]; NULL otherwise */
+  const void* head_a;
+  const void* head_b;
 } m2r2_weights;
 
 typedef struct {

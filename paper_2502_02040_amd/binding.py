@@ -40,7 +40,8 @@ class Config(ctypes.Structure):
     _fields_ = [("n_layers", c_int32), ("d_model", c_int32), ("n_heads", c_int32), ("head_dim", c_int32),
                 ("ffn", c_int32), ("vocab", c_int32), ("rank", c_int32), ("wdtype", c_int32), ("kvdtype", c_int32),
                 ("rms_eps", c_float), ("rope_theta", c_float), ("n_experts", c_int32), ("top_k", c_int32),
-                ("expert_ffn", c_int32), ("expert_slots", c_int32)]
+                ("expert_ffn", c_int32), ("expert_slots", c_int32), ("fast_heads", c_int32), ("fast_topk", c_int32),
+                ("fast_mlp_adapter", c_int32), ("head_rank", c_int32)]
 
 
 class LayerWeights(ctypes.Structure):
@@ -51,7 +52,8 @@ class LayerWeights(ctypes.Structure):
 
 class Weights(ctypes.Structure):
     _fields_ = [("embed", c_void_p), ("final_norm", c_void_p), ("lm_head", c_void_p),
-                ("layers", POINTER(LayerWeights)), ("experts_h", c_void_p)]
+                ("layers", POINTER(LayerWeights)), ("experts_h", c_void_p), ("head_a", c_void_p),
+                ("head_b", c_void_p)]
 
 
 class KV(ctypes.Structure):
@@ -161,7 +163,9 @@ def make_config(cfg, expert_slots: Optional[int] = None) -> Config:
     slots = cfg.n_experts if expert_slots is None else expert_slots
     return Config(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.ffn, cfg.vocab, cfg.rank,
                   BF16 if cfg.wdtype == "bf16" else F32, BF16 if cfg.kvdtype == "bf16" else F32,
-                  cfg.rms_eps, cfg.rope_theta, cfg.n_experts, cfg.top_k, cfg.expert_ffn, slots)
+                  cfg.rms_eps, cfg.rope_theta, cfg.n_experts, cfg.top_k, cfg.expert_ffn, slots,
+                  getattr(cfg, "fast_heads", 0), getattr(cfg, "fast_topk", 0), int(getattr(cfg, "fast_mlp_adapter", 0)),
+                  getattr(cfg, "head_rank", 0))
 
 
 def workspace_size(cfg, max_batch: int, max_chunk: int, max_ctx: int, expert_slots: Optional[int] = None) -> int:
@@ -314,12 +318,12 @@ class Model:
             L.wq, L.wk, L.wv, L.wo = up_t(p + "wq"), up_t(p + "wk"), up_t(p + "wv"), up_t(p + "wo")
             if cfg.is_moe:
                 L.router = up_t(p + "router")
-                if p + "A_m" in weights:
-                    L.A_m, L.B_m = up(p + "A_m"), up(p + "B_m")
             else:
                 L.wg, L.wu, L.wd = up_t(p + "wg"), up_t(p + "wu"), up_t(p + "wd")
+            if p + "A_m" in weights:   # the adapter-only fast MLP (mixture of experts, FLOPs-optimised form)
+                L.A_m, L.B_m = up(p + "A_m"), up(p + "B_m")
             for i, pr in enumerate(PROJ):
-                if cfg.is_moe and i >= 4:
+                if (cfg.is_moe or getattr(cfg, "fast_mlp_adapter", False)) and i >= 4:
                     break
                 if p + f"A_{pr}" in weights:
                     L.A[i] = up_t(p + f"A_{pr}") if i < 3 else up(p + f"A_{pr}")
@@ -332,8 +336,10 @@ class Model:
                                                       weights[f"L{l}.E{e}.wd"]))
                 expert_store = pack_expert_store(cfg, src)
             self.expert_store = expert_store
+        hr = getattr(cfg, "head_rank", 0)
         self._w = Weights(up("embed"), up("final_norm", torch.float32), up_t("lm_head"), self._layers,
-                          None if self.expert_store is None else self.expert_store.data_ptr())
+                          None if self.expert_store is None else self.expert_store.data_ptr(),
+                          up("head_A") if hr else None, up("head_B") if hr else None)
         self.ws_bytes = workspace_size(cfg, max_batch, max_chunk, max_ctx, self.expert_slots)
         self.workspace = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=device)
         base = self.workspace.data_ptr()

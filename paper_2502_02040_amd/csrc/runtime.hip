@@ -24,6 +24,7 @@
 #include "rw_kernels.h"
 #include "arla.h"
 #include "persist.h"
+#include "flops.h"
 
 using namespace m2r2;
 
@@ -105,6 +106,7 @@ struct Layout {
   size_t lm;                             // packed LM head
   size_t X, PIN, QKV, O, ACT, bin_d, bin_o, bin_gu, uo, att, att_cnt, lm_val, lm_idx, lm_cnt, exited, exitb,
       reinit, err, sig, arla_kv, arla_q, arla_sig, arla_cnt, rope, sk_part, sk_cnt, total;
+  size_t fsc, fqkv, lrz;                 // FLOPs-optimised fast stream: slow scores, fast q/k/v, low-rank head
   size_t scratch_begin, counters_begin, scratch_end;   // per-call scratch [begin, end), counters [counters_begin, end)
   size_t pk_sd, pk_so, pk_sgu, pk_bar, pk_rel, layers_d;   // one-launch step: statistics slots, barrier, layer table
   int pk_so_w, pk_sgu_w;
@@ -118,6 +120,9 @@ struct Layout {
 };
 
 bool is_moe(const m2r2_config& c) { return c.n_experts > 0; }
+bool is_flops(const m2r2_config& c) {
+  return c.fast_heads > 0 || c.fast_topk > 0 || c.fast_mlp_adapter != 0 || c.head_rank > 0;
+}
 
 // Packed gate + up ([F_e][d] each) + down ([d][F_e]).
 size_t expert_bytes_of(const m2r2_config& c) {
@@ -254,6 +259,12 @@ Layout make_layout(const m2r2_config& c, int max_batch, int max_chunk, int max_c
   L.pk_sd = take(sizeof(float) * kPkMaxWG * kPkSdW);
   L.pk_so = take(sizeof(float) * kPkMaxWG * L.pk_so_w);
   L.pk_sgu = take(sizeof(float) * kPkMaxWG * L.pk_sgu_w);
+  // FLOPs-optimised fast stream (one sequence)
+  const int fh = c.fast_heads > 0 ? c.fast_heads : c.n_heads;
+  const bool flops = c.fast_heads > 0 || c.fast_topk > 0 || c.fast_mlp_adapter || c.head_rank > 0;
+  L.fsc = take(flops ? sizeof(float) * (size_t)fh * max_ctx : 0);
+  L.fqkv = take(flops ? sizeof(float) * (size_t)fh * 3 * c.head_dim : 0);
+  L.lrz = take(sizeof(float) * std::max(c.head_rank, 1));
   // arrival counters (zero between passes: the last arriver resets them)
   L.counters_begin = off;
   L.att_cnt = take(sizeof(uint32_t) * kMaxSeq * c.n_heads);
@@ -313,6 +324,17 @@ m2r2_status check_config(const m2r2_config* c, int max_batch, int max_chunk, int
   if (max_batch < 1 || max_batch > 8) return fail(M2R2_E_SHAPE, "max_batch %d not in [1,8]", max_batch);
   if (max_chunk < 1 || max_chunk > kMaxRows) return fail(M2R2_E_SHAPE, "max_chunk %d not in [1,16]", max_chunk);
   if (max_ctx < 1) return fail(M2R2_E_SHAPE, "max_ctx %d", max_ctx);
+  if (c->fast_heads < 0 || c->fast_heads > c->n_heads)
+    return fail(M2R2_E_SHAPE, "fast_heads %d not in [0, n_heads]", c->fast_heads);
+  if (c->fast_topk < 0) return fail(M2R2_E_SHAPE, "fast_topk %d", c->fast_topk);
+  if (c->fast_mlp_adapter != 0 && c->fast_mlp_adapter != 1)
+    return fail(M2R2_E_INVALID, "fast_mlp_adapter %d not 0 or 1", c->fast_mlp_adapter);
+  if (c->head_rank < 0 || c->head_rank > 256) return fail(M2R2_E_SHAPE, "head_rank %d not in [0,256]", c->head_rank);
+  if (is_flops(*c)) {
+    if (is_moe(*c)) return fail(M2R2_E_UNSUPPORTED, "the FLOPs-optimised fast stream is for dense models");
+    if (max_ctx > kFaMaxCtx)
+      return fail(M2R2_E_UNSUPPORTED, "FLOPs-optimised fast stream: max_ctx %d above %d", max_ctx, kFaMaxCtx);
+  }
   return M2R2_OK;
 }
 
@@ -364,6 +386,9 @@ struct m2r2_ctx {
   const float* final_norm;
   const void* lm_head;   // packed
   const void* lm_head_rm;   // the caller's row-major LM head
+  const void* head_a = nullptr;   // low-rank head of the FLOPs-optimised fast stream (or NULL)
+  const void* head_b = nullptr;
+  std::vector<const void*> fmlp_a, fmlp_b;   // its adapter-only fast MLP: A_m, B_m per layer
   int max_batch, max_chunk, max_ctx;
   WS ws;
   // kernel timing (measurement only)
@@ -542,11 +567,63 @@ hipError_t arla_after(m2r2_ctx* c, const StepIO& io, int l, hipStream_t st) {
   return hipGetLastError();
 }
 
+// The dual-stream step of one sequence in the FLOPs-optimised form (Sec. 2.5):
+// the split attention leaves the fast row to k_fattn (kept heads, selected
+// positions); with the adapter-only fast MLP, k_fast_mlp applies it and the
+// gate/up and down kernels see the slow row alone; an exited fast row's
+// token comes from the low-rank head.
+template <int WB, int KB, int HD>
+m2r2_status run_layers_flops(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPtrs& kv, int n_layers_run,
+                             hipStream_t st) {
+  const Dims& D = c->D;
+  const int G = c->sk_grid;
+  const size_t lds = (size_t)kSkMinLds;
+  const int nd = c->rw_nch[0], nq = c->rw_nch[1], nf = c->rw_nch[2];
+  const bool fattn = D.fh > 0 || D.ftk > 0;
+  const int fh = D.fh > 0 ? D.fh : D.H;
+  RowMap rs = rm;   // the slow row alone (row 0)
+  rs.M = 1;
+  rs.cnt[0] = 1;
+  const RowMap& rmlp = D.fmlp ? rs : rm;
+  for (int l = 0; l < n_layers_run; ++l) {
+    const LayerPtrs& L = c->layers[l];
+    // the o projection sums the MLP adapter's down-projection, k_fast_mlp
+    // applies its up factor: both take it in the gate slot ([rank][d], [d][rank])
+    LayerPtrs Lo = L;
+    if (D.fmlp) {
+      Lo.A[4] = c->fmlp_a[l];
+      Lo.B[4] = c->fmlp_b[l];
+    }
+    TIMED(0, (kr_qkv_launch<WB>(nd, G, lds, st, D, L, rm, c->ws, io, l)));
+    TIMED(1, (ks_attn<WB, KB, HD><<<dim3(c->sk_attn_S, D.H, rm.nseq), kSkAttnThreads,
+                                     sk_attn_lds_bytes(HD, D.r, WB), st>>>(D, L, rm, c->ws, io, kv, l, c->sk_attn_S)));
+    if (fattn)
+      TIMED(1, (k_fattn<KB, HD><<<fh, kFaThreads, fattn_lds_bytes(c->max_ctx), st>>>(D, L, rm, c->ws, io, kv, l)));
+    TIMED(2, (kr_oproj_launch<WB>(nq, c->rw_nw[0], G, lds, st, D, Lo, rm, c->ws, io, l)));
+    if (D.fmlp) TIMED(10, (k_fast_mlp<<<(D.d + 255) / 256, 256, 0, st>>>(D, rm, Lo, l, c->ws)));
+    TIMED(3, (kr_gateup_launch<WB>(nd, G, lds, st, D, L, rmlp, c->ws, io, l)));
+    TIMED(4, (kr_down_launch<WB>(nf, c->rw_nw[1], G, lds, st, D, L, rmlp, c->ws, io, l)));
+  }
+  if (D.hr > 0)
+    TIMED(5, (k_lr_z<WB><<<(D.hr + 7) / 8, 512, sizeof(float) * D.d, st>>>(D, c->final_norm, c->head_a, rm, c->ws)));
+  TIMED(5, (kr_head_launch<WB>(nd, G, lds, st, D, c->lm_head_rm, c->final_norm, rm, c->ws, io, kv, c->skws,
+                                n_layers_run, c->head_b)));
+  HIP_TRY(hipGetLastError());
+  return M2R2_OK;
+}
+
+bool has_fast_row(const RowMap& rm) {
+  for (int m = 0; m < rm.M; ++m)
+    if (rm.fast[m]) return true;
+  return false;
+}
+
 // One or two rows: row-per-wave GEMVs and the short-chain attention.
 template <int WB, int KB, int HD>
 m2r2_status run_layers_rw(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPtrs& kv, int n_layers_run,
                           hipStream_t st) {
   const Dims& D = c->D;
+  if (is_flops(c->cfg) && has_fast_row(rm)) return run_layers_flops<WB, KB, HD>(c, rm, io, kv, n_layers_run, st);
   const int G = c->sk_grid;
   const size_t lds = (size_t)kSkMinLds;
   const int nd = c->rw_nch[0], nq = c->rw_nch[1], nf = c->rw_nch[2];
@@ -568,7 +645,7 @@ m2r2_status run_layers_rw(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const
     HIP_TRY(arla_after<WB>(c, io, l, st));
   }
   TIMED(5, (kr_head_launch<WB>(nd, G, lds, st, D, c->lm_head_rm, c->final_norm, rm, c->ws, io, kv, c->skws,
-                                n_layers_run)));
+                                n_layers_run, c->head_b)));
   HIP_TRY(hipGetLastError());
   return M2R2_OK;
 }
@@ -609,6 +686,9 @@ m2r2_status run_layers_sk(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const
 template <int WB, int KB, int HD, int MT>
 m2r2_status run_layers_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPtrs& kv, int n_layers_run,
                          hipStream_t st) {
+  if (is_flops(c->cfg) && has_fast_row(rm) && (rm.nseq != 1 || rm.M != 2 || !c->rw_on || !c->sk_attn_S))
+    return fail(M2R2_E_UNSUPPORTED, "the FLOPs-optimised fast stream runs one sequence's dual-stream step on shapes "
+                                    "whose rows are whole multiples of 1 KB");
   if constexpr (MT == 2) {
     if (c->rw_on) return run_layers_rw<WB, KB, HD>(c, rm, io, kv, n_layers_run, st);
     if (c->sk_on) return run_layers_sk<WB, KB, HD>(c, rm, io, kv, n_layers_run, st);
@@ -744,6 +824,16 @@ template <int WB>
 hipError_t sk_set_lds(int bytes) {
   const void* fns[] = {(const void*)ks_qkv<WB>, (const void*)ks_oproj<WB>, (const void*)ks_gateup<WB>,
                        (const void*)ks_down<WB>, (const void*)ks_head<WB>};
+  hipError_t e = hipSuccess;
+  for (const void* f : fns)
+    if (e == hipSuccess) e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  return e;
+}
+
+// k_fattn holds the scores and positions of the whole cache in LDS
+hipError_t fattn_set_lds(int bytes) {
+  const void* fns[] = {(const void*)k_fattn<0, 64>, (const void*)k_fattn<0, 96>, (const void*)k_fattn<0, 128>,
+                       (const void*)k_fattn<1, 64>, (const void*)k_fattn<1, 96>, (const void*)k_fattn<1, 128>};
   hipError_t e = hipSuccess;
   for (const void* f : fns)
     if (e == hipSuccess) e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
@@ -915,7 +1005,7 @@ hipError_t pk_setup(m2r2_ctx* c) {
 }
 
 bool pk_eligible(const m2r2_ctx* c, const RowMap& rm, const StepIO& io) {
-  return c->pk.kind >= 0 && rm.nseq == 1 && rm.M >= 1 && rm.M <= 2 && !rm.head_all && !io.arla_sig &&
+  return c->pk.kind >= 0 && !is_flops(c->cfg) && rm.nseq == 1 && rm.M >= 1 && rm.M <= 2 && !rm.head_all && !io.arla_sig &&
          rm.first[0] == 0 && rm.cnt[0] == rm.M;
 }
 
@@ -1202,7 +1292,7 @@ m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVP
   }
   if (c->rw_on)
     TIMED(5, (kr_head_launch<WB>(c->rw_nch[0], c->sk_grid, (size_t)kSkMinLds, st, D, c->lm_head_rm, c->final_norm, rm,
-                                  c->ws, io, kv, c->skws, D.n_layers)));
+                                  c->ws, io, kv, c->skws, D.n_layers, (const void*)nullptr)));
   else
     TIMED(5, (k_head<WB, MT><<<G.head, kGemvThreads, G.l_d, st>>>(D, c->lm_head, c->final_norm, rm, c->ws, io, kv,
                                                                 c->lay.TV, D.n_layers)));
@@ -1340,6 +1430,8 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
   if (ws_bytes < lay.total) return fail(M2R2_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, lay.total);
   const bool moe = is_moe(*cfg);
   if (moe && !w->experts_h) return fail(M2R2_E_INVALID, "mixture of experts: experts_h is NULL");
+  if (cfg->head_rank > 0 && (!w->head_a || !w->head_b))
+    return fail(M2R2_E_INVALID, "head_rank %d: head_a/head_b is NULL", cfg->head_rank);
   for (int l = 0; l < cfg->n_layers; ++l) {
     const m2r2_layer_weights& L = w->layers[l];
     if (!L.attn_norm || !L.wq || !L.wk || !L.wv || !L.wo || !L.mlp_norm)
@@ -1374,6 +1466,11 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
   D.n_layers = cfg->n_layers; D.d = cfg->d_model; D.H = cfg->n_heads; D.hd = cfg->head_dim;
   D.qdim = cfg->n_heads * cfg->head_dim; D.F = cfg->ffn; D.V = cfg->vocab; D.r = cfg->rank;
   D.eps = cfg->rms_eps; D.theta = cfg->rope_theta; D.wbf16 = cfg->wdtype == M2R2_BF16; D.kvbf16 = cfg->kvdtype == M2R2_BF16;
+  D.fh = cfg->fast_heads; D.ftk = cfg->fast_topk; D.fmlp = cfg->fast_mlp_adapter; D.hr = cfg->head_rank;
+  if (cfg->head_rank > 0) {
+    c->head_a = w->head_a;
+    c->head_b = w->head_b;
+  }
   c->layers.resize(cfg->n_layers);
   for (int l = 0; l < cfg->n_layers; ++l) {
     const m2r2_layer_weights& s = w->layers[l];
@@ -1394,6 +1491,15 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
       c->moe.router.push_back(wsb + o[5]);
     } else {
       L.pg = wsb + o[5]; L.pu = nullptr; L.pd = wsb + o[7];
+      if (cfg->fast_mlp_adapter) {
+        // FLOPs-optimised form: the fast MLP is the adapter alone; the gate,
+        // up and down slots stay empty (the gate/up kernels read a gate
+        // adapter's up factor as [ffn][rank]); the o projection and the fast
+        // MLP kernel get a copy of the layer with A_m/B_m in the gate slot
+        L.A[4] = L.B[4] = L.A[5] = L.B[5] = L.A[6] = L.B[6] = nullptr;
+        c->fmlp_a.push_back(s.A_m);
+        c->fmlp_b.push_back(s.B_m);
+      }
     }
   }
   char* b = (char*)workspace;
@@ -1410,6 +1516,7 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
   ws.arla_sig = (float*)(b + lay.arla_sig); ws.arla_cnt = (uint32_t*)(b + lay.arla_cnt);
   ws.rope = (const float2*)(b + lay.rope);
   ws.rope_len = max_ctx;
+  ws.fsc = (float*)(b + lay.fsc); ws.fqkv = (float*)(b + lay.fqkv); ws.lrz = (float*)(b + lay.lrz);
   c->skws.part = (float*)(b + lay.sk_part);
   c->skws.hier = (uint32_t*)(b + lay.sk_cnt);
   c->skws.cnt = c->skws.hier + 65;
@@ -1439,6 +1546,7 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
   if (e == hipSuccess) e = set_lds_limits<1, 16>(*cfg, c->resident);
   if (e == hipSuccess) e = sk_setup(c);
   if (e == hipSuccess) e = pk_setup(c);
+  if (e == hipSuccess && is_flops(*cfg)) e = fattn_set_lds((int)fattn_lds_bytes(max_ctx));
   if (e == hipSuccess && moe) {
     MoeState& M = c->moe;
     M.on = true;
@@ -1659,6 +1767,7 @@ struct ScratchRebase {
     w.att_cnt = rb(w.att_cnt); w.lm_val = rb(w.lm_val); w.lm_idx = rb(w.lm_idx); w.lm_cnt = rb(w.lm_cnt);
     w.exited = rb(w.exited); w.exitb = rb(w.exitb); w.reinit = rb(w.reinit); w.sig = rb(w.sig);
     w.arla_kv = rb(w.arla_kv); w.arla_q = rb(w.arla_q); w.arla_sig = rb(w.arla_sig); w.arla_cnt = rb(w.arla_cnt);
+    w.fsc = rb(w.fsc); w.fqkv = rb(w.fqkv); w.lrz = rb(w.lrz);
     c->skws.part = rb(c->skws.part); c->skws.hier = rb(c->skws.hier); c->skws.cnt = rb(c->skws.cnt);
     c->pk.sd = rb(c->pk.sd); c->pk.so = rb(c->pk.so); c->pk.sgu = rb(c->pk.sgu); c->pk.bar = rb(c->pk.bar); c->pk.rel = rb(c->pk.rel);
   }
@@ -1712,6 +1821,7 @@ M2R2_API m2r2_status m2r2_decode_step_noalloc(m2r2_ctx* c, int32_t batch, int32_
 M2R2_API m2r2_status m2r2_set_arla(m2r2_ctx* c, const m2r2_arla* w) {
   if (!c) return fail(M2R2_E_INVALID, "ctx is NULL");
   if (c->moe.on) return fail(M2R2_E_UNSUPPORTED, "the latent-attention exit router is for dense models");
+  if (is_flops(c->cfg)) return fail(M2R2_E_UNSUPPORTED, "the exit router with the FLOPs-optimised fast stream");
   if (!w) {
     c->arla.on = false;
     return M2R2_OK;
@@ -1732,6 +1842,9 @@ M2R2_API m2r2_status m2r2_draft(m2r2_ctx* c, const int32_t* last_token_d, const 
   if (!c) return fail(M2R2_E_INVALID, "ctx is NULL");
   if (!last_token_d || !positions_d || !drafts_d) return fail(M2R2_E_INVALID, "NULL token/position/drafts");
   if (c->moe.on) return fail(M2R2_E_UNSUPPORTED, "drafting is implemented for dense models");
+  if (is_flops(c->cfg))
+    return fail(M2R2_E_UNSUPPORTED, "a fast-only draft has no slow-row scores: the FLOPs-optimised fast stream "
+                                    "is the dual-stream step's");
   if (exit_layer < 1 || exit_layer > c->D.n_layers) return fail(M2R2_E_SHAPE, "exit_layer %d", exit_layer);
   if (gamma < 1 || gamma > 64) return fail(M2R2_E_SHAPE, "gamma %d not in [1,64]", gamma);
   if (m2r2_status s = check_kv(c, kv)) return s;

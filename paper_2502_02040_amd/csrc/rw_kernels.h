@@ -807,7 +807,8 @@ __global__ __launch_bounds__(64 * NW) void kr_down(Dims D, LayerPtrs L, RowMap r
 // ============================================================================
 template <int WB, int NCH, int NS>
 __global__ __launch_bounds__(kRwThreads) void kr_head(Dims D, const void* lm_head, const float* final_norm, RowMap rm,
-                                                      WS ws, StepIO io, KVPtrs kv, SkWS sk, int n_layers_run) {
+                                                      WS ws, StepIO io, KVPtrs kv, SkWS sk, int n_layers_run,
+                                                      const void* head_b) {
   extern __shared__ __attribute__((aligned(16))) float actf[];
   __shared__ float ssum[kMaxRows * 4];
   __shared__ int hrow[2];
@@ -827,6 +828,13 @@ __global__ __launch_bounds__(kRwThreads) void kr_head(Dims D, const void* lm_hea
   float bv[1];
   sk_bins_load(rm.M * 4, bin_d_at(ws, n_layers_run, 0, 0), kMaxRows * 4, bv);
   const int exv = ws.exited[min(tid, rm.nseq - 1)];
+  // FLOPs-optimised form (Sec. 2.5): the fast row that exited emits its token
+  // from the low-rank head, whose first factor k_lr_z has applied (lrz); the
+  // LM head is then not streamed (one sequence: the flag is uniform)
+  const bool lowrank = D.hr > 0 && head_b && rm.nseq == 1 && !rm.head_all && rm.M == 2 && rm.fast[1] &&
+                       rm.slow_of[1] >= 0 && ws.exited[0] != 0;
+  const int lv0 = u0, lv1 = u1;
+  if (lowrank) u1 = u0;
   const float* X1 = ws.X + (size_t)(rm.M > 1 ? 1 : 0) * D.d;
   RwPieces<RwPM<WB, NCH, NS>::value> xp;
   rw_load_pieces<true>(ws.X, X1, final_norm, D.d, xp);
@@ -882,6 +890,31 @@ __global__ __launch_bounds__(kRwThreads) void kr_head(Dims D, const void* lm_hea
   rw_store_pieces<true>(xp, D.d, actf);
   epi.nh = nh;
   st.run(row_ptr, u0, u1, actf, D.d, epi, ops);
+  if (lowrank) {
+    // logits z_v = head_b[v] . lrz for this wave's rows, one row per lane
+    const int hr = D.hr;
+    for (int j = tid; j < hr; j += kRwThreads) actf[j] = ws.lrz[j];
+    __syncthreads();
+    float bz = -INFINITY;
+    int bi = 0x7fffffff;
+    for (int v0 = lv0; v0 < lv1; v0 += 64) {
+      const int v = v0 + lane;
+      if (v < lv1) {
+        float z = 0.f;
+        for (int j = 0; j < hr; ++j) z += rw_wt<WB>(rw_wt_raw<WB>(head_b, (size_t)v * hr + j)) * actf[j];
+        if (io.logits_out) io.logits_out[v] = z;
+        if (z > bz) { bz = z; bi = v; }   // each lane's rows rise: the lowest index wins its ties
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float z2 = __shfl_xor(bz, o);
+      const int i2 = __shfl_xor(bi, o);
+      if (z2 > bz || (z2 == bz && i2 < bi)) { bz = z2; bi = i2; }
+    }
+    epi.bz[0] = bz;
+    epi.bi[0] = bi;
+  }
   if (lane == 0) {
     bz_s[wv][0] = epi.bz[0]; bz_s[wv][1] = epi.bz[1];
     bi_s[wv][0] = epi.bi[0]; bi_s[wv][1] = epi.bi[1];

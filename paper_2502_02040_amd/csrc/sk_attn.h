@@ -128,6 +128,11 @@ __global__ __launch_bounds__(kSkAttnThreads) void ks_attn(Dims D, LayerPtrs L, R
   __syncthreads();
   const int first = rml.first[sq], R = rml.cnt[sq];
   const int ctx = posv + rm.pos_offset;
+  // FLOPs-optimised form (Sec. 2.5, one sequence): the fast row attends in
+  // k_fattn; here its partials carry no weight, the slow row's scores of the
+  // kept heads and the fast row's q, k, v of those heads are stored for it
+  const bool flops = (D.fh > 0 || D.ftk > 0) && R == 2 && rml.fast[first + 1];
+  const bool fkeep = flops && h < (D.fh > 0 ? D.fh : D.H);
   const bool frozen = exv != 0;
   const int t0 = sp * SPL;
   const int own_sp = min(ctx / SPL, S - 1);
@@ -202,6 +207,12 @@ __global__ __launch_bounds__(kSkAttnThreads) void ks_attn(Dims D, LayerPtrs L, R
     k_s[e_m][e_d] = kr1;
   }
   __syncthreads();
+  if (fkeep && own && erow && rml.fast[first + e_m]) {
+    float* f = ws.fqkv + (size_t)h * 3 * HD;
+    f[e_d] = q_s[e_m][e_d];
+    f[HD + e_d] = k_s[e_m][e_d];
+    f[2 * HD + e_d] = v_s[e_m][e_d];
+  }
 
   // ---- own split: cache writes of the slow rows -----------------------------
   if (own && erow && rml.wr[first + e_m]) {
@@ -253,7 +264,12 @@ __global__ __launch_bounds__(kSkAttnThreads) void ks_attn(Dims D, LayerPtrs L, R
 #pragma unroll
           for (int c = 0; c < DPL; ++c) p += q_s[i][d0 + c] * kk[c];
           p = quad_sum(p);
-          if (sub == 0 && i < R) sc[i][j] = j < nt ? p * scale : -INFINITY;
+          if (sub == 0 && i < R) {
+            const bool f = flops && rml.fast[first + i];
+            sc[i][j] = (j < nt && !f) ? p * scale : -INFINITY;
+            if (fkeep && !rml.fast[first + i] && j < nt)
+              ws.fsc[(size_t)h * ws.rope_len + t0 + ch * kSkAttnP + j] = p * scale;
+          }
         }
       }
       if (ch + 1 < NC) load_chunk(kv.k, ch + 1, kr);   // in flight during this chunk's softmax and P V
@@ -264,7 +280,8 @@ __global__ __launch_bounds__(kSkAttnThreads) void ks_attn(Dims D, LayerPtrs L, R
         const int i = wv >> 1, jj = wv & 1;
         if (i < R) {
           const int mi = first + i, mj = first + min(jj, R - 1);
-          const bool vis = jj < R && (rml.fast[mi] ? (jj == i) : (!rml.fast[mj] && rml.idx[mj] <= rml.idx[mi]));
+          const bool vis = jj < R && !(flops && rml.fast[mi]) &&
+                           (rml.fast[mi] ? (jj == i) : (!rml.fast[mj] && rml.idx[mj] <= rml.idx[mi]));
           const bool rnd = !rml.fast[mi];
           float p = 0.f;
           for (int d = lane; d < HD; d += 64) {

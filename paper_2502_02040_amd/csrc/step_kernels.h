@@ -32,6 +32,10 @@ struct Dims {
   int n_layers, d, H, hd, qdim, F, V, r;
   float eps, theta;
   int wbf16, kvbf16;
+  // FLOPs-optimised fast stream (Sec. 2.5; all zero: the memory-bound form):
+  // fast heads kept, positions each attends to, adapter-only fast MLP, rank
+  // of the fast row's head
+  int fh, ftk, fmlp, hr;
 };
 
 // Projection matrices are read from a tile-packed copy (pack_index below):
@@ -111,6 +115,10 @@ struct WS {
   uint32_t* arla_cnt;   // arrival counter of the router kernel
   const float2* rope;  // [rope_len][hd/2] (cos, sin), built in double precision on the host
   int rope_len;
+  // FLOPs-optimised fast stream (one sequence)
+  float* fsc;      // [fast heads][rope_len] scaled slow-row scores of the cached positions
+  float* fqkv;     // [fast heads][3][hd] the fast row's q, k (after RoPE) and v
+  float* lrz;      // [head_rank] low-rank head: the emitted row times head_a
 };
 
 // Bins per layer and row: kBinSlots are stored (and zeroed every pass); the
