@@ -348,6 +348,8 @@ typedef struct {
   int64_t h2d_bytes;                /* bytes copied host to device */
   int64_t copy_waits;               /* times the compute stream was made to wait for a copy */
   int64_t host_wait_ns;             /* host time spent waiting for routing results */
+  int64_t copies_failed;            /* copies that could not be enqueued or completed with an error: the
+                                       slot is invalidated and the expert loaded on demand when used */
   int64_t layer_misses[128];        /* misses per layer */
 } m2r2_moe_counters;
 
@@ -382,6 +384,8 @@ M2R2_API m2r2_status m2r2_moe_set_preload_table(m2r2_ctx* ctx, const int32_t* id
  * host store on copy_stream (priority != 0: on the library's on-demand copy
  * stream; NULL copy_stream: the library's prefetch stream).  Later decode
  * steps wait for the copy before they use the slot.  Counts as prefetches.
+ * A copy that cannot be enqueued invalidates its slot (the expert is loaded
+ * on demand when used; counted in copies_failed) instead of failing the call.
  * M2R2_E_STATE under the M2R2_MOE_FIXED policy (its slots never change). */
 M2R2_API m2r2_status m2r2_prefetch_experts(m2r2_ctx* ctx, int32_t layer, const int32_t* ids_h, int32_t n,
                                            int32_t priority, hipStream_t copy_stream);

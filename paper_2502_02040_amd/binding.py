@@ -73,7 +73,7 @@ class StepOut(ctypes.Structure):
 
 _I64 = ctypes.c_int64
 COUNTER_FIELDS = ("hits", "misses", "prefetch_issued", "prefetch_used", "prefetch_wasted", "loads", "pred_correct",
-                  "pred_total", "h2d_bytes", "copy_waits", "host_wait_ns")
+                  "pred_total", "h2d_bytes", "copy_waits", "host_wait_ns", "copies_failed")
 
 
 class Arla(ctypes.Structure):

@@ -32,6 +32,7 @@ namespace m2r2 {
 struct CacheCounters {
   int64_t hits = 0, misses = 0, prefetch_issued = 0, prefetch_used = 0, prefetch_wasted = 0, loads = 0;
   int64_t pred_correct = 0, pred_total = 0;
+  int64_t copies_failed = 0;   // copies that could not start or completed with an error (slot invalidated)
   std::vector<int64_t> layer_misses;
 };
 
@@ -167,6 +168,34 @@ class ExpertCachePolicy {
       slots_out->push_back(s);
       experts_out->push_back(e);
     }
+  }
+
+  // The copy into slot s of layer l failed (it could not start, or completed
+  // with an error): the slot holds no expert any more and is the first taken
+  // by the next placement; a later use of the expert it was to hold is a
+  // miss, loaded on demand.
+  void invalidate(int l, int s) {
+    Layer& L = layers_[l];
+    const int e = L.expert_in[s];
+    if (e >= 0) L.slot_of[e] = -1;
+    L.expert_in[s] = -1;
+    L.prefetched[s] = 0;
+    ++cnt_.copies_failed;
+  }
+
+  // Place needed expert need[j] of layer l, which is not resident (its
+  // earlier copy failed after the hit was counted), as a load: the victim
+  // rules of use(); returns the slot.
+  int place_needed(int l, const int* need, int k, int j) {
+    Layer& L = layers_[l];
+    auto excluded = [&](int x) {
+      return std::find(need, need + k, x) != need + k ||
+             std::find(L.predicted.begin(), L.predicted.end(), x) != L.predicted.end();
+    };
+    auto needed = [&](int x) { return std::find(need, need + k, x) != need + k; };
+    int s = victim(L, excluded);
+    if (s < 0) s = victim(L, needed);
+    return place(L, s, need[j]);
   }
 
   const CacheCounters& counters() const { return cnt_; }

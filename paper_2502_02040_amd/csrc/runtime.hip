@@ -15,6 +15,7 @@
 #include <vector>
 
 #include "expert_cache.h"
+#include "expert_sched.h"
 #include "m2r2.h"
 #include "m2r2_measure.h"
 #include "moe_kernels.h"
@@ -1150,6 +1151,41 @@ hipError_t tab_flush(m2r2_ctx* c, hipStream_t st) {
 
 // Dual-stream (or slow-only) pass of a mixture-of-experts model, batch 1:
 // rows 0 (slow) and 1 (fast).
+// The expert copies of the scheduler: from the pinned host store on the
+// demand or the ahead-of-time stream, one event per slot.  A copy that cannot
+// be enqueued leaves nothing behind (the error is cleared); a slot whose
+// event reports an error holds no valid expert.
+class HipExpertEngine final : public ExpertCopyEngine {
+ public:
+  explicit HipExpertEngine(m2r2_ctx* c) : c_(c) {}
+  bool start(int l, int s, int e, bool demand) override {
+    MoeState& M = c_->moe;
+    tab_evict_slot(M, l, s);
+    if (moe_copy(c_, l, s, e, demand ? M.copy_demand : M.copy_ahead) != hipSuccess) {
+      (void)hipGetLastError();
+      return false;
+    }
+    if (!demand && M.spec) M.pend.push_back({l, s, e});
+    return true;
+  }
+  State state(int l, int s) override {
+    MoeState& M = c_->moe;
+    const int i = l * M.C + s;
+    if (!M.slot_pending[i]) return kDone;
+    const hipError_t q = hipEventQuery(M.slot_ev[i]);
+    if (q == hipSuccess) {
+      M.slot_pending[i] = 0;
+      return kDone;
+    }
+    if (q == hipErrorNotReady) return kPending;
+    (void)hipGetLastError();
+    return kFailed;   // (stays failed until a new copy into the slot is started)
+  }
+
+ private:
+  m2r2_ctx* c_;
+};
+
 template <int WB, int KB, int HD>
 m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVPtrs& kv, const m2r2_step_out* out,
                       bool dual, hipStream_t st) {
@@ -1173,7 +1209,6 @@ m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVP
   const Grids G = grids<WB, MT>(c);
   const int tiles = (M.E + 15) / 16;
   float* logits = (float*)M.mp.logits;
-  std::vector<int> pslots, pexperts;
   for (int l = 0; l < D.n_layers; ++l) {
     const LayerPtrs& L = c->layers[l];
     if (c->rw_on) {
@@ -1233,19 +1268,22 @@ m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVP
       need[k] = M.host_words[k];
       if (need[k] < 0 || need[k] >= M.E) return fail(M2R2_E_HIP, "layer %d: router returned expert %d", l, need[k]);
     }
+    HipExpertEngine eng(c);
+    ExpertScheduler sched(M.pol, eng);
     if (fixed)
       M.pol.use_fixed(l, need, M.K, slot, load);
-    else
-      M.pol.use(l, need, M.K, slot, load);
+    else if (!sched.acquire(l, need, M.K, slot, load))
+      return fail(M2R2_E_HIP, "layer %d: an on-demand expert copy could not be enqueued", l);
     // did the launches above find every chosen expert in its slot?
     bool done = M.spec;
     for (int k = 0; k < M.K && done; ++k) done = M.tab[l * M.E + need[k]] == slot[k];
     if (!done) {
-    for (int k = 0; k < M.K; ++k)
-      if (load[k]) {
-        tab_evict_slot(M, l, slot[k]);
-        HIP_TRY(moe_copy(c, l, slot[k], need[k], M.copy_demand));
-      }
+    if (fixed)   // (the scheduler started the other policies' on-demand copies)
+      for (int k = 0; k < M.K; ++k)
+        if (load[k]) {
+          tab_evict_slot(M, l, slot[k]);
+          HIP_TRY(moe_copy(c, l, slot[k], need[k], M.copy_demand));
+        }
     ExpertSlots es{};
     for (int k = 0; k < M.K; ++k) {
       const int i = l * M.C + slot[k];
@@ -1273,17 +1311,11 @@ m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVP
       for (int k = 0; k < M.K; ++k)
         if (load[k]) tab_put(M, l, need[k], slot[k]);
     }
+    // prefetches: a copy that cannot be enqueued invalidates its slot (the
+    // expert is then loaded on demand when it is used)
     auto preload = [&](int lp, const int* ids) -> hipError_t {
-      pslots.clear();
-      pexperts.clear();
-      M.pol.predict(lp, ids, M.K, &pslots, &pexperts);
-      hipError_t r = hipSuccess;
-      for (size_t q = 0; q < pslots.size() && r == hipSuccess; ++q) {
-        tab_evict_slot(M, lp, pslots[q]);
-        r = moe_copy(c, lp, pslots[q], pexperts[q], M.copy_ahead);
-        if (M.spec) M.pend.push_back({lp, pslots[q], pexperts[q]});
-      }
-      return r;
+      sched.prefetch(lp, ids, M.K);
+      return hipSuccess;
     };
     if (ahead)
       for (int j = 0; j < n_pred; ++j) HIP_TRY(preload(2 * l + 2 + j, M.host_words + (1 + j) * kMaxTopK));
@@ -1372,7 +1404,7 @@ void fill_stats(const CacheCounters& k, m2r2_moe_counters* o) {
   memset(o, 0, sizeof *o);
   o->hits = k.hits; o->misses = k.misses; o->prefetch_issued = k.prefetch_issued; o->prefetch_used = k.prefetch_used;
   o->prefetch_wasted = k.prefetch_wasted; o->loads = k.loads; o->pred_correct = k.pred_correct;
-  o->pred_total = k.pred_total;
+  o->pred_total = k.pred_total; o->copies_failed = k.copies_failed;
   for (size_t l = 0; l < k.layer_misses.size() && l < 128; ++l) o->layer_misses[l] = k.layer_misses[l];
 }
 
@@ -1967,7 +1999,11 @@ M2R2_API m2r2_status m2r2_prefetch_experts(m2r2_ctx* c, int32_t layer, const int
   M.pol.predict(layer, ids_h, n, &slots, &experts);
   for (size_t q = 0; q < slots.size(); ++q) {
     tab_evict_slot(M, layer, slots[q]);
-    HIP_TRY(moe_copy(c, layer, slots[q], experts[q], cs));
+    if (moe_copy(c, layer, slots[q], experts[q], cs) != hipSuccess) {
+      (void)hipGetLastError();
+      M.pol.invalidate(layer, slots[q]);   // not resident: a later use loads it on demand
+      continue;
+    }
     if (M.spec) M.pend.push_back({layer, slots[q], experts[q]});
   }
   return M2R2_OK;
