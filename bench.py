@@ -196,7 +196,7 @@ def cpu_baseline(cfg, weights, ctx: int, budget_s: float, *, seqs: int = 1):
         tok = r.token
         n += 1
         el = time.perf_counter() - t0
-        if el >= budget_s or n >= 64:
+        if el >= budget_s or n >= 4096:
             break
     what = f"one of the {seqs} sequences' " if seqs > 1 else ""
     return _cpu_line(n / el, "tokens/s", f"{n} dual-stream decode steps of {what}the same model in float32 NumPy at "
@@ -231,7 +231,7 @@ def cpu_moe_baseline(cfg, ctx: int, budget_s: float):
         orc.decode_step(1, ctx, cache)
         n += 1
         el = time.perf_counter() - t0
-        if el >= budget_s or n >= 64:
+        if el >= budget_s or n >= 4096:
             break
     return _cpu_line(n / el, "tokens/s", f"one dual-stream MoE decode step in float32 NumPy at context {ctx} (every "
                                          f"expert available), repeated {n} times in {el:.1f} s after an untimed first "
