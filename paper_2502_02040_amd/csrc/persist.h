@@ -416,7 +416,7 @@ template <int HD, int WB>
 struct PkAttLds {
   float q[2][HD], k[2][HD], v[2][HD];
   float u[2][3][kMaxRank];
-  float sc[2][kPkChunk + 2];
+  float sc[2][2 * kPkChunk + 2];   // a pair of chunks, then the own keys
   float pvred[32][2][HD];
   float mw[2][kPkMaxSplits], ml[2][kPkMaxSplits];
   float rowm[2], rowl[2], lastw[2], fin_m[2], fin_l[2], linv[2];
@@ -774,34 +774,68 @@ __device__ __forceinline__ void pk_phase_att(int l, uint32_t& target, PkShared& 
         float acc0[DPL], acc1[DPL];
 #pragma unroll
         for (int c = 0; c < DPL; ++c) { acc0[c] = 0.f; acc1[c] = 0.f; }
-        auto chunk = [&](int ch, u32x4_t (&kb)[NCH], u32x4_t (&vb)[NCH]) {
-          const bool last = ch == nch - 1;
+        // Chunks are taken in pairs (ch, ch + 1): every thread slot scores one
+        // token of each, one softmax covers both and their P V is summed in
+        // one pass (a split of 129..256 positions costs one pass, not two).
+        // Pairs combine online (running max, sum and accumulator per row).
+        auto scores = [&](int ch, u32x4_t (&kb)[NCH], int off) {
           const int c0 = t0 + ch * kPkChunk;
           const int nt = max(0, min(t1, c0 + kPkChunk) - c0);
-          // scores of the cached tokens (one token per thread slot)
-          {
-            float kk[DPL];
+          float kk[DPL];
 #pragma unroll
-            for (int c = 0; c < NCH; ++c) {
-              if constexpr (KB) {
+          for (int c = 0; c < NCH; ++c) {
+            if constexpr (KB) {
 #pragma unroll
-                for (int i = 0; i < 4; ++i) { kk[8 * c + 2 * i] = bf16lo(kb[c][i]); kk[8 * c + 2 * i + 1] = bf16hi(kb[c][i]); }
-              } else {
+              for (int i = 0; i < 4; ++i) { kk[8 * c + 2 * i] = bf16lo(kb[c][i]); kk[8 * c + 2 * i + 1] = bf16hi(kb[c][i]); }
+            } else {
 #pragma unroll
-                for (int i = 0; i < 4; ++i) kk[4 * c + i] = __uint_as_float(kb[c][i]);
-              }
-            }
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-              float p = 0.f;
-#pragma unroll
-              for (int c = 0; c < DPL; ++c) p += A.q[i][d0 + c] * kk[c];
-              p = quad_sum(p);
-              if (sub == 0 && i < R) A.sc[i][slot] = slot < nt ? p * scale : -INFINITY;
+              for (int i = 0; i < 4; ++i) kk[4 * c + i] = __uint_as_float(kb[c][i]);
             }
           }
-          if (ch + 2 < nch) load_chunk(kv.k, ch + 2, kb);   // in flight during this chunk's softmax and P V
-          // own keys (own split, last chunk): a slow row sees the slow row (its
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+            float p = 0.f;
+#pragma unroll
+            for (int c = 0; c < DPL; ++c) p += A.q[i][d0 + c] * kk[c];
+            p = quad_sum(p);
+            if (sub == 0 && i < R) A.sc[i][off + slot] = slot < nt ? p * scale : -INFINITY;
+          }
+        };
+        auto pv = [&](u32x4_t (&vb)[NCH], float p0, float p1) {
+#pragma unroll
+          for (int c = 0; c < NCH; ++c) {
+            if constexpr (KB) {
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                const float a = bf16lo(vb[c][i]), b = bf16hi(vb[c][i]);
+                acc0[8 * c + 2 * i] += p0 * a; acc0[8 * c + 2 * i + 1] += p0 * b;
+                acc1[8 * c + 2 * i] += p1 * a; acc1[8 * c + 2 * i + 1] += p1 * b;
+              }
+            } else {
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                const float a = __uint_as_float(vb[c][i]);
+                acc0[4 * c + i] += p0 * a;
+                acc1[4 * c + i] += p1 * a;
+              }
+            }
+          }
+        };
+        constexpr int kOwn = 2 * kPkChunk;   // sc index of the own keys
+        for (int ch = 0; ch < nch; ch += 2) {
+          const bool two = ch + 1 < nch;
+          const bool last = ch + 2 >= nch;
+          scores(ch, kr[0], 0);
+          if (two) {
+            scores(ch + 1, kr[1], kPkChunk);
+          } else if (sub == 0) {
+            A.sc[0][kPkChunk + slot] = -INFINITY;
+            A.sc[1][kPkChunk + slot] = -INFINITY;
+          }
+          // the next pair's keys are in flight during this pair's softmax and P V
+          if (ch + 2 < nch) load_chunk(kv.k, ch + 2, kr[0]);
+          if (ch + 3 < nch) load_chunk(kv.k, ch + 3, kr[1]);
+          // own keys (own split, last pair): a slow row sees the slow row (its
           // own key, rounded as cached); a fast row only its own exact key
           if (own && last && wv < 4) {
             const int i = wv >> 1, jj = wv & 1;
@@ -815,18 +849,19 @@ __device__ __forceinline__ void pk_phase_att(int l, uint32_t& target, PkShared& 
                 p += A.q[i][dd] * (rnd && KB ? round_bf16(kk) : kk);
               }
               p = wave_sum(p);
-              if (lane == 0) A.sc[i][kPkChunk + jj] = vis ? p * scale : -INFINITY;
+              if (lane == 0) A.sc[i][kOwn + jj] = vis ? p * scale : -INFINITY;
             }
+          } else if (tid < 4) {
+            A.sc[tid >> 1][kOwn + (tid & 1)] = -INFINITY;
           }
           __syncthreads();
-          const int ntot = kPkChunk + (own && last ? 2 : 0);
           if (wv < R) {
             const int i = wv;
             float mx = -INFINITY;
-            for (int j = lane; j < ntot; j += 64) mx = fmaxf(mx, A.sc[i][j]);
+            for (int j = lane; j < kOwn + 2; j += 64) mx = fmaxf(mx, A.sc[i][j]);
             mx = wave_max(mx);
             float ls = 0.f;
-            for (int j = lane; j < ntot; j += 64) {
+            for (int j = lane; j < kOwn + 2; j += 64) {
               const float z = A.sc[i][j];
               const float ev = z == -INFINITY ? 0.f : __expf(z - mx);
               A.sc[i][j] = ev;
@@ -851,37 +886,15 @@ __device__ __forceinline__ void pk_phase_att(int l, uint32_t& target, PkShared& 
               else acc1[c] *= wr;
             }
           }
-          {
-            const float p0 = A.sc[0][slot] * wc[0], p1 = R > 1 ? A.sc[1][slot] * wc[1] : 0.f;
-#pragma unroll
-            for (int c = 0; c < NCH; ++c) {
-              if constexpr (KB) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                  const float a = bf16lo(vb[c][i]), b = bf16hi(vb[c][i]);
-                  acc0[8 * c + 2 * i] += p0 * a; acc0[8 * c + 2 * i + 1] += p0 * b;
-                  acc1[8 * c + 2 * i] += p1 * a; acc1[8 * c + 2 * i + 1] += p1 * b;
-                }
-              } else {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                  const float a = __uint_as_float(vb[c][i]);
-                  acc0[4 * c + i] += p0 * a;
-                  acc1[4 * c + i] += p1 * a;
-                }
-              }
-            }
-          }
-          if (ch + 2 < nch) load_chunk(kv.v, ch + 2, vb);
+          pv(vr[0], A.sc[0][slot] * wc[0], R > 1 ? A.sc[1][slot] * wc[1] : 0.f);
+          if (two) pv(vr[1], A.sc[0][kPkChunk + slot] * wc[0], R > 1 ? A.sc[1][kPkChunk + slot] * wc[1] : 0.f);
+          if (ch + 2 < nch) load_chunk(kv.v, ch + 2, vr[0]);
+          if (ch + 3 < nch) load_chunk(kv.v, ch + 3, vr[1]);
           if (!last) {
-            __syncthreads();   // the next chunk's scores overwrite sc
+            __syncthreads();   // the next pair's scores overwrite sc
           } else if (tid < 2) {
             A.lastw[tid] = wc[tid];
           }
-        };
-        for (int ch = 0; ch < nch; ch += 2) {
-          chunk(ch, kr[0], vr[0]);
-          if (ch + 1 < nch) chunk(ch + 1, kr[1], vr[1]);
         }
         if (tid < 2) { A.fin_m[tid] = m_run[tid]; A.fin_l[tid] = l_run[tid]; }
         // sum over the 4 token slots of a 16-lane row (DPP), then the 32 row
@@ -908,7 +921,7 @@ __device__ __forceinline__ void pk_phase_att(int l, uint32_t& target, PkShared& 
           if (own) {
             const bool rnd = !rml.fast[i];
             for (int jj = 0; jj < R; ++jj) {
-              const float w = A.sc[i][kPkChunk + jj] * A.lastw[i];
+              const float w = A.sc[i][2 * kPkChunk + jj] * A.lastw[i];
               if (w != 0.f) a += w * (rnd && KB ? round_bf16(A.v[jj][dd]) : A.v[jj][dd]);
             }
           }
