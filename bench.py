@@ -550,7 +550,7 @@ def run_spec(args) -> int:
     for lam in args.decay:
         _progress(f"spec: decay {lam}")
         cfg = base
-        weights = synth.make_weights(cfg, decay=None if lam == 1.0 else (kL, lam))
+        weights = synth.make_weights(cfg, decay=None if lam == 1.0 else (kL, lam), adapter_scale=args.adapter_scale)
         max_ctx = plen + n_new + 12 * (gamma + 1) + 16
         model = Model(cfg, weights, max_batch=1, max_chunk=16, max_ctx=max_ctx)
         del weights
@@ -679,7 +679,8 @@ def run_spec(args) -> int:
         arg, gap, amax = _teacher_forced_greedy(model, cfg, prompt, max_ctx, spec_tokens)
         diffs = [i for i in range(len(spec_tokens)) if int(arg[i]) != spec_tokens[i]]
         ties = [i for i in diffs if gap[i] <= SPEC_TIE_REL * amax[i]]
-        results.append(dict(decay=lam, alpha=round(alpha, 4), rounds=rounds, tokens=len(spec_tokens),
+        results.append(dict(decay=lam, adapter_scale=args.adapter_scale, alpha=round(alpha, 4), rounds=rounds,
+                            tokens=len(spec_tokens),
                             lossless=len(diffs) == len(ties), tokens_checked=len(spec_tokens),
                             differences_from_teacher_forced_greedy=len(diffs), near_tie_exceptions=len(ties),
                             first_difference_free_running=div,
@@ -801,6 +802,7 @@ def run_moe(args) -> int:
         return tuple(synth.make_tensor(cfg, f"L{l}.E{e}.{m}", *spec[f"L{l}.E{e}.{m}"]) for m in ("wg", "wu", "wd"))
 
     store = pack_expert_store(cfg, expert_source, threads=16)
+    variant = {"router_coherent": True} if args.router_coherent else {}
     gen_s = time.perf_counter() - t_setup
     _progress(f"moe: {cfg.n_layers * cfg.n_experts} experts packed into pinned host memory in {gen_s:.1f} s")
     plen, steps, C = args.prompt, args.steps, args.slots
@@ -813,6 +815,38 @@ def run_moe(args) -> int:
     table = synth.preload_table(cfg, args.warmup + steps)
     E = cfg.n_experts
     runs = []
+    want = set(x for x in args.moe_runs.split(",") if x)
+
+    def prefix(model, pos, desc, nxt, dual):
+        for t in prompt:   # prefill with slow-only steps (not timed)
+            model.decode_step(torch.tensor([int(t)], dtype=torch.int32, device=dev), pos, desc, dual=False,
+                              next_token=nxt, advance=True)
+        for i in range(args.warmup):
+            model.decode_step(stream_ids[i:i + 1], pos, desc, dual=dual, next_token=nxt, advance=True)
+
+    # the true routing of the timed steps (untimed pass, every expert
+    # resident): the table of the oracle-predictor run, an upper bound on
+    # prediction (Sec. 3.3 reports accuracy against it implicitly)
+    true_table = None
+    if not want or "oracle" in want:
+        _progress("moe: recording the true routing")
+        w = synth.make_weights(cfg, names=names, **variant)
+        model = Model(cfg, w, max_batch=1, max_chunk=16, max_ctx=max_ctx, expert_slots=E, expert_store=store)
+        del w
+        kv = PagedKV(cfg, 1, max_ctx, block_size=16)
+        desc = kv.desc()
+        pos = torch.zeros(1, dtype=torch.int32, device=dev)
+        nxt = torch.zeros(1, dtype=torch.int32, device=dev)
+        prefix(model, pos, desc, nxt, False)
+        rec = torch.zeros((steps, cfg.n_layers * cfg.top_k), dtype=torch.int32, device=dev)
+        for i in range(steps):
+            j = args.warmup + i
+            model.decode_step(stream_ids[j:j + 1], pos, desc, dual=False, next_token=nxt, advance=True,
+                              slow_experts=rec[i])
+        torch.cuda.synchronize()
+        true_table = rec.cpu().numpy().reshape(steps, cfg.n_layers, cfg.top_k)
+        del model, kv
+        torch.cuda.empty_cache()
     # the four strategies the paper compares with (Sec. 3.3) run the slow
     # stream alone; M2R2 runs both rows
     for label, slots, policy, dual in (
@@ -821,22 +855,21 @@ def run_moe(args) -> int:
             ("LRU + random preload", C, "random_preload", False),
             ("previous-layer residual speculation", C, "previous_layer", False),
             ("M2R2 ahead-of-time prefetch", C, "ahead_of_time", True),
+            ("oracle predictor: the true routing of the next layer preloaded after each layer", C, "oracle", False),
             ("all experts resident", E, "on_demand", True)):
+        if want and policy not in want and not (policy == "on_demand" and slots == E and "resident" in want):
+            continue
         _progress(f"moe: {label}")
-        w = synth.make_weights(cfg, names=names)
+        w = synth.make_weights(cfg, names=names, **variant)
         model = Model(cfg, w, max_batch=1, max_chunk=16, max_ctx=max_ctx, expert_slots=slots, expert_store=store)
         del w
-        model.moe_set_preload_table(table)
-        model.moe_set_policy(policy)
+        model.moe_set_preload_table(true_table if policy == "oracle" else table)
+        model.moe_set_policy("random_preload" if policy == "oracle" else policy)
         kv = PagedKV(cfg, 1, max_ctx, block_size=16)
         desc = kv.desc()
         pos = torch.zeros(1, dtype=torch.int32, device=dev)
         nxt = torch.zeros(1, dtype=torch.int32, device=dev)
-        for t in prompt:   # prefill with slow-only steps (not timed)
-            model.decode_step(torch.tensor([int(t)], dtype=torch.int32, device=dev), pos, desc, dual=False,
-                              next_token=nxt, advance=True)
-        for i in range(args.warmup):
-            model.decode_step(stream_ids[i:i + 1], pos, desc, dual=dual, next_token=nxt, advance=True)
+        prefix(model, pos, desc, nxt, dual)
         torch.cuda.synchronize()
         model.moe_reset()   # the preload table restarts at its row 0: the same draws as the replay
         stream = torch.cuda.current_stream()
@@ -873,7 +906,7 @@ def run_moe(args) -> int:
         r["stall_ms_per_token_vs_resident"] = round(r["ms_per_token"] - resident["ms_per_token"], 4)
     kb = expert_gateup_bytes(cfg)
     achieved = kb / (resident["expert_gateup_us"] * 1e-6) / 1e9
-    m2 = next(r for r in runs if r["policy"] == "ahead_of_time")
+    m2 = next((r for r in runs if r["policy"] == "ahead_of_time"), resident)
     cpu = None
     if args.cpu_budget > 0:
         _progress("moe: CPU oracle baseline")
@@ -884,7 +917,10 @@ def run_moe(args) -> int:
           config={"workload": f"olmoe-shaped {cfg.n_layers}L d{cfg.d_model} {cfg.n_heads}x{cfg.head_dim} "
                               f"E{cfg.n_experts} top{cfg.top_k} Fe{cfg.expert_ffn} vocab{cfg.vocab} rank{cfg.rank}, "
                               f"experts in pinned host memory, {C} HBM slots per layer, prompt {plen}, "
-                              f"{steps} teacher-forced Zipf-token decode steps", "batch": 1, "slots": C},
+                              f"{steps} teacher-forced Zipf-token decode steps"
+                              + (", routers shared + 0.5 x noise per layer (router-coherent variant)"
+                                 if args.router_coherent else ""), "batch": 1, "slots": C,
+                  "router_coherent": bool(args.router_coherent)},
           token_bytes_all_hits=int(moe_token_bytes(cfg, plen + steps / 2)), runs=runs,
           roofline={"bound": "hbm", "kernel": "expert gate/up (k_moe_gateup)", "achieved": round(achieved, 1),
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
@@ -937,6 +973,12 @@ def main() -> int:
     ap.add_argument("--decay", type=float, nargs="*", default=[1.0, 0.1],
                     help="spec mode: scale of wo/wd in layers >= exit layer (1.0 = plain weights)")
     ap.add_argument("--slots", type=int, default=16, help="moe mode: HBM expert slots per layer")
+    ap.add_argument("--router-coherent", action="store_true",
+                    help="moe mode: routers drawn as shared + 0.5 x noise per layer (a labelled structured variant)")
+    ap.add_argument("--moe-runs", default="",
+                    help="moe mode: comma-separated policies to run (default: all), e.g. ahead_of_time,oracle")
+    ap.add_argument("--adapter-scale", type=float, default=1.0,
+                    help="spec mode: scale of the adapter factors (a labelled structured variant; 0: p == h)")
     ap.add_argument("--gate-every", type=int, default=1, help="exit mode: a gate every this many layers")
     ap.add_argument("--arla", action="store_true",
                     help="exit mode: decide the gates with the latent-attention exit router")
