@@ -139,13 +139,17 @@ def arla_score(wq: np.ndarray, wk: np.ndarray, wv: np.ndarray, w_out: np.ndarray
     """Exit probability of the accelerated-residual latent-attention router
     (Sec. 2.3.1, ARLA; Fig. 4a) at a gate.
 
-    ``states`` are the fast residuals after each layer of the interval that
-    ends at the gate, oldest first.  Each is RMS-normalised without a gain,
-    then projected to the latent space (``wk``, ``wv``: [64, d]); the query is
-    the projection (``wq``) of the last state; single-query softmax attention
-    with scale 1/sqrt(64) pools the values, and a linear readout with a
-    sigmoid gives the probability.  (The paper does not fix the query, the
-    normalisation or the readout; these are the readings used throughout.)
+    ``states`` are the fast residuals of the interval that ends at the gate,
+    oldest first: the state the fast stream restarts from at the previous
+    gate, then the state after each layer up to the gate.  Each is
+    RMS-normalised without a gain, then projected to the latent space
+    (``wk``, ``wv``: [64, d]).  Every state has a query too, but the decision
+    is one probability taken at the gate, so attention runs causally over the
+    interval and only the output at its newest state is read: the query is
+    the projection (``wq``) of the last state, its softmax attention (scale
+    1/sqrt(64)) pools the values, and a linear readout with a sigmoid gives
+    the probability.  (The paper does not fix the pooling, the normalisation
+    or the readout; these are the readings used throughout.)
     """
     U = [x / np.sqrt(np.mean(x * x) + eps) for x in states]
     q = wq @ U[-1]
@@ -368,8 +372,10 @@ class Oracle:
 
         With ``arla`` (arrays ``wq``, ``wk``, ``wv`` [N, 64, d], ``w_out``
         [N, 64], ``b_out`` [N]; block b belongs to boundary b) the signal at a
-        gate b is ``arla_score`` over the fast states after the layers
-        [previous gate (or 0), b-1] instead of the cosine of layer b-1.
+        gate b is ``arla_score`` over the interval from the previous gate g
+        (or the start, g = 0) to b instead of the cosine of layer b-1: the
+        state p restarts from at g (h there; the embedding for g = 0), then
+        p after each of the layers g .. b-1.
         """
         cfg = self.cfg
         assert mode in MODES
@@ -384,7 +390,8 @@ class Oracle:
         pred_logits = np.full((N, max(cfg.n_experts, 1)), np.nan)
         self._fast_states = np.full((N, cfg.d_model), np.nan)
         self._topk_gap = np.full((N, cfg.n_heads), np.inf) if cfg.is_flops else None
-        interval: List[np.ndarray] = []   # fast states since the last gate
+        # the gate's interval: the state p (re)starts from, then p after each layer
+        interval: List[np.ndarray] = [h.copy()]
         for l in range(N):
             p_in = p
             # fast row first: it sees the cache before the slow row writes position pos
@@ -409,7 +416,7 @@ class Oracle:
                         pred[lp] = topk_desc(z, cfg.top_k)
             b = l + 1
             if b in gates:
-                interval = []
+                interval = [h.copy()]   # p restarts from h at the gate (when the step goes on)
             if mode != "off" and b in gates:
                 fired = signal[l] >= tau
                 if fired and exit_b == N:

@@ -249,7 +249,7 @@ Layout make_layout(const m2r2_config& c, int max_batch, int max_chunk, int max_c
   L.exitb = take(sizeof(int) * kMaxSeq);
   L.reinit = take(sizeof(int) * c.n_layers * kMaxSeq);
   L.sig = take(sizeof(float) * kMaxSeq * c.n_layers);
-  L.arla_kv = take(sizeof(float) * c.n_layers * 2 * kArlaDim);
+  L.arla_kv = take(sizeof(float) * 2 * c.n_layers * 2 * kArlaDim);   // after each layer, then at each gate
   L.arla_q = take(sizeof(float) * kArlaDim);
   L.arla_sig = take(sizeof(float) * kMaxSeq);
   L.sk_slots = sk_slot_bound(c);
@@ -543,9 +543,12 @@ M2R2_RW_LAUNCHER(kr_head)
 M2R2_RW_LAUNCHER_NW(kr_oproj)
 M2R2_RW_LAUNCHER_NW(kr_down)
 
-// Exit router after layer l (a one-sequence dual step with the router on):
-// latent key and value of the fast state for the next gate, and at the layer
-// before that gate the query and the score.
+// Exit router after layer l (l = -1: before layer 0) of a one-sequence dual
+// step with the router on.  Row 0 is the slow row, row 1 the fast one.  The
+// launch projects the fast state after l into the slots of the next gate b;
+// at the layer before b also the query, and, while the slow row still holds
+// the state the fast row restarts from at b, that state for the gate after
+// b; before layer 0 the embedding for the first gate.  At b it scores.
 bool host_is_gate(const StepIO& io, int b) {
   if (b <= 0 || b >= 128) return false;
   return b < 64 ? ((io.gate_mask_lo >> b) & 1ull) : ((io.gate_mask_hi >> (b - 64)) & 1ull);
@@ -555,16 +558,39 @@ template <int WB>
 hipError_t arla_after(m2r2_ctx* c, const StepIO& io, int l, hipStream_t st) {
   if (!io.arla_sig) return hipSuccess;
   const int N = c->D.n_layers;
-  int b = l + 1;
-  while (b < N && !host_is_gate(io, b)) ++b;
+  auto next_gate = [&](int from) {
+    while (from < N && !host_is_gate(io, from)) ++from;
+    return from;
+  };
+  const int b = next_gate(l + 1);
   if (b >= N) return hipSuccess;   // no gate after this layer
-  int first = l;
+  int first = l < 0 ? 0 : l;
   while (first > 0 && !host_is_gate(io, first)) --first;
   const size_t blk = (size_t)kArlaDim * c->D.d * (WB ? 2 : 4);
-  ArlaArgs a{c->arla.wq + b * blk, c->arla.wk + b * blk, c->arla.wv + b * blk, c->arla.w_out + (size_t)b * kArlaDim,
-             c->arla.b_out + b, 1, l, first, b == l + 1};
-  const int rows = (a.gate_now ? 3 : 2) * kArlaDim;
-  k_arla<WB><<<(rows + kArlaWaves - 1) / kArlaWaves, kArlaThreads, 0, st>>>(c->D, c->ws, a);
+  const int slot = 2 * kArlaDim;
+  ArlaArgs a{};
+  a.w_out = c->arla.w_out + (size_t)b * kArlaDim;
+  a.b_out = c->arla.b_out + b;
+  a.layer = l;
+  a.first = first;
+  a.gate_now = l >= 0 && b == l + 1;
+  auto job = [&](const char* w, int bnd, int row, int dst) { a.job[a.njobs++] = ArlaJob{w + bnd * blk, row, dst}; };
+  if (l < 0) {
+    job(c->arla.wk, b, 0, N * slot);
+    job(c->arla.wv, b, 0, N * slot + kArlaDim);
+  } else {
+    job(c->arla.wk, b, 1, l * slot);
+    job(c->arla.wv, b, 1, l * slot + kArlaDim);
+  }
+  if (a.gate_now) {
+    job(c->arla.wq, b, 1, -1);
+    const int b2 = next_gate(b + 1);
+    if (b2 < N) {
+      job(c->arla.wk, b2, 0, (N + b) * slot);
+      job(c->arla.wv, b2, 0, (N + b) * slot + kArlaDim);
+    }
+  }
+  k_arla<WB><<<a.njobs * (kArlaDim / kArlaWaves), kArlaThreads, 0, st>>>(c->D, c->ws, a);
   return hipGetLastError();
 }
 
@@ -631,6 +657,7 @@ m2r2_status run_layers_rw(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const
   // attention: one 128-token chunk per split (two only when M2R2_ATTN_CHUNKS
   // asks for it: measured no faster at one sequence)
   const int S2 = c->attn_chunks == 2 ? (c->max_ctx + 2 * kSkAttnP - 1) / (2 * kSkAttnP) : 0;
+  HIP_TRY(arla_after<WB>(c, io, -1, st));   // the first interval's restart state
   for (int l = 0; l < n_layers_run; ++l) {
     const LayerPtrs& L = c->layers[l];
     TIMED(0, (kr_qkv_launch<WB>(nd, G, lds, st, D, L, rm, c->ws, io, l)));
@@ -665,6 +692,7 @@ m2r2_status run_layers_sk(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const
   const int G = c->sk_grid;
   const size_t ld = sk_lds(D.d), lq = sk_lds(D.qdim), lf = sk_lds(D.F);
   const SkWS& sk = c->skws;
+  HIP_TRY(arla_after<WB>(c, io, -1, st));   // the first interval's restart state
   for (int l = 0; l < n_layers_run; ++l) {
     const LayerPtrs& L = c->layers[l];
     TIMED(0, (ks_qkv<WB><<<G, kSkThreads, ld, st>>>(D, L, rm, c->ws, io, c->sk[0], sk, l)));
@@ -712,6 +740,7 @@ m2r2_status run_layers_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const 
     return fail(M2R2_E_SHAPE, "context too long for the attention merge (max_ctx %d)", c->max_ctx);
   const size_t smem = attn_smem_bytes();
   const Grids G = grids<WB, MT>(c);
+  HIP_TRY(arla_after<WB>(c, io, -1, st));   // the first interval's restart state
   for (int l = 0; l < n_layers_run; ++l) {
     const LayerPtrs& L = c->layers[l];
     TIMED(0, (k_qkv<WB, MT><<<G.qkv, kGemvThreads, G.l_d, st>>>(D, L, rm, c->ws, io, l)));

@@ -139,12 +139,16 @@ def _arla(name, bias=0.0):
 
 
 @pytest.mark.parametrize("name", CASES)
-def test_arla_signal_observe(name):
-    """Latent-attention exit router (Sec. 2.3.1): in OBSERVE mode with gates
-    at the last boundary only (small_bf16: an interval of two layers), the
-    router score at the gate and every other signal match the oracle."""
+@pytest.mark.parametrize("gate_set", ["last", "all"])
+def test_arla_signal_observe(name, gate_set):
+    """Latent-attention exit router (Sec. 2.3.1): in OBSERVE mode the router
+    score at every gate and every other signal match the oracle.  Gates at
+    the last boundary only: one interval from the embedding over two layers
+    (three-layer shapes); at every boundary: the later intervals start from
+    the slow state the fast row restarts from."""
     cfg = synth.CONFIGS[name]
-    t, _, _ = _decode_run(name, mode="observe", tau=0.5, gates=[cfg.n_layers - 1], n_steps=6, arla=_arla(name))
+    gates = [cfg.n_layers - 1] if gate_set == "last" else list(range(1, cfg.n_layers))
+    t, _, _ = _decode_run(name, mode="observe", tau=0.5, gates=gates, n_steps=6, arla=_arla(name))
     assert t.steps == 6 and t.compared >= 6
 
 

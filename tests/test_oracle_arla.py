@@ -3,6 +3,8 @@
 information), the same computation composed from torch's library routines
 (rms_norm, linear, scaled-dot-product attention, sigmoid), and which fast
 states enter each gate's interval inside the decode step."""
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -71,33 +73,71 @@ def test_score_does_not_depend_on_the_scale_of_the_states():
     assert a == pytest.approx(b, rel=1e-12)
 
 
-def _step(arla, gates, mode="observe", tau=2.0):
-    w = synth.make_weights(CFG, threads=2)
-    orc = Oracle(CFG, w)
-    cache = KVCache(CFG, 16)
-    ids = list(synth.prompt_ids(CFG, 6))
+def _prompt():
+    return [int(t) for t in synth.prompt_ids(CFG, 6)]
+
+
+def _step(arla, gates, mode="observe", tau=2.0, cfg=CFG):
+    w = synth.make_weights(cfg, threads=2)
+    orc = Oracle(cfg, w)
+    cache = KVCache(cfg, 16)
+    ids = _prompt()
     orc.slow_chunk(ids[:-1], 0, cache)
     return orc.decode_step(ids[-1], len(ids) - 1, cache, gates=gates, tau=tau, mode=mode, arla=arla)
 
 
-def test_decode_step_uses_the_states_since_the_previous_gate():
-    """Gates 2 and 5 of 7 layers, keys without information: the signal at
-    gate 2 averages the values of the fast states after layers 0, 1; at gate
-    5 those after layers 2, 3, 4.  Other layers keep the cosine signal."""
-    a = synth.arla_weights(CFG)
-    a = {k: np.asarray(v, np.float64) for k, v in a.items()}
-    a["wk"][:] = 0.0
+def _slow_state_at(b):
+    """The slow residual entering layer b, from a model cut after layer b-1
+    (synth draws every tensor from its own name, so the first b layers are
+    the same tensors)."""
+    cut = dataclasses.replace(CFG, n_layers=b)
+    return _step(None, [], mode="off", cfg=cut).h
+
+
+def _arla_f64():
+    a = {k: np.asarray(v, np.float64) for k, v in synth.arla_weights(CFG).items()}
     a["b_out"][:] = np.arange(CFG.n_layers) * 0.1
+    return a
+
+
+def test_decode_step_interval_bookkeeping():
+    """Gates 2 and 5 of 7 layers, keys without information (uniform
+    attention): the signal at gate 2 averages the values of the embedding
+    (where p starts) and the fast states after layers 0, 1; at gate 5 those
+    of the slow state entering layer 2 (where p restarts) and the fast states
+    after layers 2, 3, 4.  Other layers keep the cosine signal."""
+    a = _arla_f64()
+    a["wk"][:] = 0.0
     plain = _step(None, [2, 5])
     r = _step(a, [2, 5])
     fs = r.fast_states
-    for b, lay in ((2, [0, 1]), (5, [2, 3, 4])):
-        mean_v = np.mean([a["wv"][b] @ _unit(fs[l]) for l in lay], axis=0)
+    emb = synth.make_weights(CFG, names=["embed"])["embed"][_prompt()[-1]].astype(np.float64)
+    for b, states in ((2, [emb, fs[0], fs[1]]), (5, [_slow_state_at(2), fs[2], fs[3], fs[4]])):
+        mean_v = np.mean([a["wv"][b] @ _unit(x) for x in states], axis=0)
         assert r.signal[b - 1] == pytest.approx(_sig(a["w_out"][b] @ mean_v + a["b_out"][b]), rel=1e-10)
     others = [l for l in range(CFG.n_layers) if l not in (1, 4)]
     np.testing.assert_allclose(r.signal[others], plain.signal[others], rtol=1e-12)
     # observe mode restarts p at every gate whatever the signal: same states, same logits
     np.testing.assert_allclose(r.logits, plain.logits, rtol=1e-12)
+
+
+def test_decode_step_interval_matches_arla_score():
+    """With informative keys, the signal at gates 1, 3 and 6 is arla_score
+    over the interval assembled outside the step: the restart state (the
+    embedding, then the slow state entering the previous gate), then the fast
+    states after the interval's layers."""
+    a = _arla_f64()
+    r = _step(a, [1, 3, 6])
+    fs = r.fast_states
+    emb = synth.make_weights(CFG, names=["embed"])["embed"][_prompt()[-1]].astype(np.float64)
+    cases = ((1, [emb, fs[0]]), (3, [_slow_state_at(1), fs[1], fs[2]]),
+             (6, [_slow_state_at(3), fs[3], fs[4], fs[5]]))
+    for b, states in cases:
+        want = arla_score(a["wq"][b], a["wk"][b], a["wv"][b], a["w_out"][b], float(a["b_out"][b]), states, EPS)
+        assert r.signal[b - 1] == pytest.approx(want, rel=1e-12)
+        # the restart state matters: the interval without it scores differently
+        assert abs(arla_score(a["wq"][b], a["wk"][b], a["wv"][b], a["w_out"][b], float(a["b_out"][b]),
+                              states[1:], EPS) - want) > 1e-6
 
 
 def test_decode_step_exit_follows_the_router():
