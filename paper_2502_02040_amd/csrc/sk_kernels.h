@@ -421,39 +421,6 @@ __device__ __forceinline__ void wave_lds_sync() {
 // Sum over the 16 lanes of a row group (lanes 16m .. 16m+15).
 __device__ __forceinline__ float sum16(float v) { return row_sum16(v); }
 
-// The row map is a kernel argument; indexing it at a runtime index is a
-// vector load from the argument segment, and waiting for one after the weight
-// loads are in flight waits for all of them.  Prologues therefore read the
-// argument words into registers before the weights are primed and keep a
-// copy in LDS.
-static_assert(sizeof(RowMap) % 4 == 0, "row map copied as words");
-constexpr int kRmWords = (int)(sizeof(RowMap) / 4);
-union SkRmLds {
-  RowMap rm;
-  int w[kRmWords];
-};
-// Copy of the map into LDS by the first wave (readable after the next
-// workgroup barrier).  The words are read with constant indices, i.e. scalar
-// loads through the constant cache (a lane-indexed read of a kernel argument
-// would be a vector load from the argument segment, which misses every cache
-// at kernel start); lane i stores word i.
-__device__ __forceinline__ void sk_rm_copy(SkRmLds& dst, const RowMap& rm) {
-  static_assert(kRmWords <= 64, "one word per lane of the first wave");
-  if (threadIdx.x >= 64) return;
-  const int* w = (const int*)&rm;
-  const int t = (int)threadIdx.x;
-  int wv[kRmWords];
-#pragma unroll
-  for (int i = 0; i < kRmWords; ++i) {
-    wv[i] = w[i];
-    asm volatile("" : "+s"(wv[i]));   // opaque: the select below stays a select of values
-  }
-  int v = wv[kRmWords - 1];
-#pragma unroll
-  for (int i = 0; i < kRmWords - 1; ++i) v = t == i ? wv[i] : v;
-  if (t < kRmWords) dst.w[t] = v;
-}
-
 // The gate decision of gate_logic for at most two sequences.
 __device__ __forceinline__ void sk_gate_logic(const Dims& D, const RowMap& rm, const int* ex_in, const int* eb_in,
                                               const StepIO& io, int layer, const float* ssum, int* reinit_s,

@@ -414,11 +414,17 @@ struct TileGemv {
   static constexpr int KSTEP = WB ? 32 : 16;
   static constexpr int P = KSTEP / 4;
   static constexpr bool XRES = MT <= 2;
+  // up to 8 rows the next chunk's activations are requested one chunk ahead
+  // (16 rows would not fit the registers: they are requested as the chunk
+  // starts)
+  static constexpr bool XPIPE = !XRES && MT <= 8;
   u32x4_t w[kChunk], w2[kChunk];
   int nsteps, s0, s1, nchunks;
   char* xl;                   // LDS: resident rows (XRES) or per-wave chunk staging
   const float* xr[MT];        // activation rows (16-row class)
   const float* gain;
+  float4 xa[MT];              // activations of the chunk to stage next (not resident)
+  float4 ga;                  // and its gain (row 0 again without a gain: never used)
 
   __device__ __forceinline__ void init(int K, char* lds) {
     const int wave = threadIdx.x >> 6;
@@ -583,10 +589,26 @@ struct TileGemv {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
 
+  // 16-row class: request the activations (and gains) of the chunk at steps
+  // sb.. into xa / ga.  Unconditional loads at clamped addresses.
+  __device__ __forceinline__ void fetch_x(int sb) {
+    const int lane = threadIdx.x & 63;
+    const int q = WB ? lane : (lane & 31);
+    const bool live = q < min(kChunk, s1 - sb) * P;
+    const int kq = sb * KSTEP + 4 * (live ? q : 0);
+    ga = ldg4((gain ? gain : xr[0]) + kq);
+#pragma unroll
+    for (int m = 0; m < MT; ++m) xa[m] = ldg4(xr[m] + kq);
+  }
+
   // One chunk of steps [sb, sb+8) ∩ [.., s1): the MFMAs consume buf, then buf
   // is refilled with the chunk two ahead (nbase, nsb), so two chunks are in
-  // flight while the wave multiplies.
-  __device__ __forceinline__ void chunk(int sb, const char* nbase, int nsb, u32x4_t (&buf)[kChunk], f32x4_t& acc) const {
+  // flight while the wave multiplies.  16-row class: the chunk's activations
+  // were requested one chunk earlier (xa); once they are staged, those of the
+  // next chunk (steps xsb..) are requested before the weights two ahead, so
+  // that waiting for them never waits for weights that are not yet needed.
+  __device__ __forceinline__ void chunk(int sb, const char* nbase, int nsb, u32x4_t (&buf)[kChunk], f32x4_t& acc,
+                                        int xsb) {
     const int lane = threadIdx.x & 63;
     const int mr = lane & 15, grp = lane >> 4;
     const int mread = mr < MT ? mr : MT - 1;
@@ -615,15 +637,12 @@ struct TileGemv {
         }
       }
     } else {
-      // stage this chunk's activations
+      // stage this chunk's activations (up to 8 rows: requested one chunk earlier)
       const int q = WB ? lane : (lane & 31);
       const bool live = q < nst * P;
-      const int kq = sb * KSTEP + 4 * (live ? q : 0);
-      float4 xv[MT];
-      float4 gv = make_float4(1.f, 1.f, 1.f, 1.f);
-      if (gain) gv = ldg4(gain + kq);
-#pragma unroll
-      for (int m = 0; m < MT; ++m) xv[m] = ldg4(xr[m] + kq);
+      if constexpr (!XPIPE) fetch_x(sb);
+      const float4 gv = gain ? ga : make_float4(1.f, 1.f, 1.f, 1.f);
+      const float4* xv = xa;
       char* my = xl;
       const int j = q / P, e = (q % P) * 4;
 #pragma unroll
@@ -653,6 +672,11 @@ struct TileGemv {
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      if constexpr (XPIPE) {
+        __builtin_amdgcn_sched_barrier(0);
+        fetch_x(xsb);
+        __builtin_amdgcn_sched_barrier(0);
+      }
 #pragma unroll
       for (int jj = 0; jj < kChunk; ++jj) {
         if constexpr (WB) {
@@ -694,33 +718,31 @@ struct TileGemv {
     for (int a = 0; a < 2; ++a)
       if (++k2 == nchunks) { k2 = 0; ++i2; }
     const char* cur_tile = ptr(0);
+    if constexpr (XPIPE) fetch_x(s0);
+    // steps of the chunk after chunk k (activations repeat from tile to tile)
+    auto xnext = [&](int kk) { return s0 + (kk + 1 == nchunks ? 0 : kk + 1) * kChunk; };
+    auto step = [&](u32x4_t (&buf)[kChunk]) -> bool {
+      const bool more2 = i2 < n_local;
+      const char* nb = more2 ? ptr(i2) + lo16 : cur_tile + lo16;
+      chunk(s0 + k * kChunk, nb, more2 ? s0 + k2 * kChunk : s1, buf, acc, xnext(k));
+      if (k == nchunks - 1) {
+        epi(i, acc);
+        acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      }
+      if (++k == nchunks) { k = 0; ++i; }
+      if (++k2 == nchunks) { k2 = 0; ++i2; }
+      if (i >= n_local) return true;
+      if (k == 0) cur_tile = ptr(i);
+      return false;
+    };
+    // The first chunk runs before the loop: every path into the loop then
+    // issues its loads in the same order (next chunk's activations, then the
+    // weights two ahead), so the compiler's waits for the activations never
+    // wait for weights that are not yet needed.
+    if (step(w)) return;
     for (;;) {
-      {
-        const bool more2 = i2 < n_local;
-        const char* nb = more2 ? ptr(i2) + lo16 : cur_tile + lo16;
-        chunk(s0 + k * kChunk, nb, more2 ? s0 + k2 * kChunk : s1, w, acc);
-        if (k == nchunks - 1) {
-          epi(i, acc);
-          acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        }
-        if (++k == nchunks) { k = 0; ++i; }
-        if (++k2 == nchunks) { k2 = 0; ++i2; }
-        if (i >= n_local) break;
-        if (k == 0) cur_tile = ptr(i);
-      }
-      {
-        const bool more2 = i2 < n_local;
-        const char* nb = more2 ? ptr(i2) + lo16 : cur_tile + lo16;
-        chunk(s0 + k * kChunk, nb, more2 ? s0 + k2 * kChunk : s1, w2, acc);
-        if (k == nchunks - 1) {
-          epi(i, acc);
-          acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        }
-        if (++k == nchunks) { k = 0; ++i; }
-        if (++k2 == nchunks) { k2 = 0; ++i2; }
-        if (i >= n_local) break;
-        if (k == 0) cur_tile = ptr(i);
-      }
+      if (step(w2)) return;
+      if (step(w)) return;
     }
   }
 };
@@ -802,6 +824,39 @@ __device__ __forceinline__ uint32_t ld_raw(const void* p, size_t i) {
 template <int WB>
 __device__ __forceinline__ float raw_f(uint32_t r) {
   return WB ? __uint_as_float(r << 16) : __uint_as_float(r);
+}
+
+// The row map is a kernel argument; indexing it at a runtime index is a
+// vector load from the argument segment, and waiting for one after the weight
+// loads are in flight waits for all of them.  Prologues therefore read the
+// argument words into registers before the weights are primed and keep a
+// copy in LDS.
+static_assert(sizeof(RowMap) % 4 == 0, "row map copied as words");
+constexpr int kRmWords = (int)(sizeof(RowMap) / 4);
+union SkRmLds {
+  RowMap rm;
+  int w[kRmWords];
+};
+// Copy of the map into LDS by the first wave (readable after the next
+// workgroup barrier).  The words are read with constant indices, i.e. scalar
+// loads through the constant cache (a lane-indexed read of a kernel argument
+// would be a vector load from the argument segment, which misses every cache
+// at kernel start); lane i stores word i.
+__device__ __forceinline__ void sk_rm_copy(SkRmLds& dst, const RowMap& rm) {
+  static_assert(kRmWords <= 64, "one word per lane of the first wave");
+  if (threadIdx.x >= 64) return;
+  const int* w = (const int*)&rm;
+  const int t = (int)threadIdx.x;
+  int wv[kRmWords];
+#pragma unroll
+  for (int i = 0; i < kRmWords; ++i) {
+    wv[i] = w[i];
+    asm volatile("" : "+s"(wv[i]));   // opaque: the select below stays a select of values
+  }
+  int v = wv[kRmWords - 1];
+#pragma unroll
+  for (int i = 0; i < kRmWords - 1; ++i) v = t == i ? wv[i] : v;
+  if (t < kRmWords) dst.w[t] = v;
 }
 
 // Element m of a per-row field of the row map, for a per-thread m: built
@@ -999,6 +1054,8 @@ __global__ __launch_bounds__(kGemvThreads) void k_qkv(Dims D, LayerPtrs L, RowMa
   __shared__ int src_s[kMaxRows];
   __shared__ const float* xrow_s[kMaxRows];
   extern __shared__ __attribute__((aligned(16))) char dyn[];
+  __shared__ SkRmLds rmu;   // the row map, for per-thread indices (read after the first barrier)
+  const RowMap& rml = rmu.rm;
   const int nq = D.qdim, tq = nq / 16;
   const int nqkv = 3 * nq + 3 * D.r;
   const int ntiles = 3 * tq + (3 * D.r + 15) / 16;
@@ -1034,6 +1091,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_qkv(Dims D, LayerPtrs L, RowMa
   __builtin_amdgcn_sched_barrier(0);
   tg.prime(n_local, ptr);
   __builtin_amdgcn_sched_barrier(0);
+  sk_rm_copy(rmu, rm);
   if (threadIdx.x < rm.M * 4) {
     float a = 0.f;
 #pragma unroll
@@ -1048,9 +1106,9 @@ __global__ __launch_bounds__(kGemvThreads) void k_qkv(Dims D, LayerPtrs L, RowMa
   if (threadIdx.x == 0) {
     gate_logic(D, rm, ex_in, eb_in, io, layer, ssum, reinit_s, exited_s, exitb_s, sig_s);
     for (int m = 0; m < rm.M; ++m) {
-      const int sq = rsel(rm.seq, m);
+      const int sq = rml.seq[m];
       int src = m;
-      if (rsel(rm.fast, m) && reinit_s[sq]) src = rsel(rm.slow_of, m);
+      if (rml.fast[m] && reinit_s[sq]) src = rml.slow_of[m];
       src_s[m] = src;
       xrow_s[m] = ws.X + (size_t)src * D.d;
       inv_rms[m] = rsqrtf(ssum[src * 4] / D.d + D.eps);
@@ -1508,6 +1566,8 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
   __shared__ int flag_s[2 * kMaxSeq];        // exited, reinit (PRE)
   __shared__ const float* xrow_s[kMaxRows];
   extern __shared__ __attribute__((aligned(16))) char dyn[];
+  __shared__ SkRmLds rmu;   // the row map, for per-thread indices (read after the first barrier)
+  const RowMap& rml = rmu.rm;
   const int ntiles = D.d / 16;
   if ((int)blockIdx.x >= ntiles) return;
   if (io.mode == EX_EXIT) {
@@ -1562,6 +1622,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
   __builtin_amdgcn_sched_barrier(0);
   tg.prime(n_local, ptr);
   __builtin_amdgcn_sched_barrier(0);
+  sk_rm_copy(rmu, rm);
   if (threadIdx.x < rm.M) xrow_s[threadIdx.x] = ws.O + (size_t)threadIdx.x * D.qdim;
   for (int e = threadIdx.x; e < rm.M * D.r; e += kGemvThreads) uo_s[e] = 0.f;
   if constexpr (PRE) {
@@ -1586,7 +1647,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
       }
     } else if (L.A[3]) {
       for (int m = 0; m < rm.M; ++m)
-        if (rsel(rm.fast, m)) column_sums(ws.uo + (size_t)m * D.H * D.r, D.H, D.r, D.r, uo_s + m * D.r, red);
+        if (rml.fast[m]) column_sums(ws.uo + (size_t)m * D.H * D.r, D.H, D.r, D.r, uo_s + m * D.r, red);
     }
     int sel[MT];
 #pragma unroll
@@ -1595,7 +1656,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
   } else {
     if (L.A[3])
       for (int m = 0; m < rm.M; ++m)
-        if (rsel(rm.fast, m)) column_sums(ws.uo + (size_t)m * D.H * D.r, D.H, D.r, D.r, uo_s + m * D.r, red);
+        if (rml.fast[m]) column_sums(ws.uo + (size_t)m * D.H * D.r, D.H, D.r, D.r, uo_s + m * D.r, red);
     tg.set_rows(xrow_s, nullptr, rm.M, D.qdim);
   }
   __syncthreads();
@@ -1612,15 +1673,15 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
     float xnew = 0.f, pin = 0.f;
     bool upd = false;
     if (e < rm.M * 16) {
-      const int sq = rsel(rm.seq, m);
+      const int sq = rml.seq[m];
       const float xo = first ? xo_s[e] : ws.X[(size_t)m * D.d + nn];
       xnew = xo;
       const bool ex = first ? flag_s[sq] != 0 : ws.exited[sq] != 0;
       if (!ex) {
         upd = true;
-        if (rsel(rm.fast, m)) {
+        if (rml.fast[m]) {
           const bool ri = first ? flag_s[rm.nseq + sq] != 0 : ws.reinit[layer * kMaxSeq + sq] != 0;
-          const int so = rsel(rm.slow_of, m);
+          const int so = rml.slow_of[m];
           pin = ri ? (first ? xo_s[so * 16 + (e & 15)] : ws.X[(size_t)so * D.d + nn]) : xo;
           float ad = 0.f;
           if (L.B[3] && L.A[3]) {
@@ -1640,7 +1701,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
     __syncthreads();
     if (upd) {
       ws.X[(size_t)m * D.d + nn] = xnew;
-      if (rsel(rm.fast, m)) ws.PIN[(size_t)m * D.d + nn] = pin;
+      if (rml.fast[m]) ws.PIN[(size_t)m * D.d + nn] = pin;
     }
     // partial sums for the gate/up prologue: sum x^2 and the adapter-down of
     // gate and up (fast rows): sum_n A[j][n] g_mlp[n] x[n]
@@ -1650,7 +1711,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
       float v = 0.f;
       if (c == 0) {
         for (int ii = 0; ii < 16; ++ii) v += newx[mm * 16 + ii] * newx[mm * 16 + ii];
-      } else if (rsel(rm.fast, mm)) {
+      } else if (rml.fast[mm]) {
         const int which = (c - 1) / D.r, j = (c - 1) % D.r;   // 0: gate (A[4]), 1: up (A[5])
         const void* A = which ? L.A[5] : L.A[4];
         if (A) {
@@ -1662,7 +1723,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
           }
         }
       }
-      if (c == 0 || rsel(rm.fast, mm)) add_agent(bin_o_at(ws, D, layer, bin, mm) + c, v);
+      if (c == 0 || rml.fast[mm]) add_agent(bin_o_at(ws, D, layer, bin, mm) + c, v);
     }
     __syncthreads();
   };
@@ -1689,6 +1750,8 @@ __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, Ro
   __shared__ float ad_s[kMaxRank * 16];        // first pair: A_d columns (PRE)
   __shared__ const float* xrow_s[kMaxRows];
   extern __shared__ __attribute__((aligned(16))) char dyn[];
+  __shared__ SkRmLds rmu;   // the row map, for per-thread indices (read after the first barrier)
+  const RowMap& rml = rmu.rm;
   const int ntiles = D.F / 16;
   if ((int)blockIdx.x >= ntiles) return;
   if (io.mode == EX_EXIT) {
@@ -1734,6 +1797,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, Ro
   __builtin_amdgcn_sched_barrier(0);
   tg.prime(n_local, ptr);
   __builtin_amdgcn_sched_barrier(0);
+  sk_rm_copy(rmu, rm);
   if (tid < rm.M) xrow_s[tid] = ws.X + (size_t)tid * D.d;
   if (tid < rm.M * PO) {
     float a = 0.f;
@@ -1774,7 +1838,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, Ro
       const int m = e >> 4, nn = n0 + (e & 15);
       const float ir = inv_rms[m];
       float g = y[e] * ir, u = y[256 + e] * ir;
-      if (rsel(rm.fast, m)) {
+      if (rml.fast[m]) {
         if (first && pre_b) {
           float dg = 0.f, du = 0.f;
           for (int j = 0; j < D.r; ++j) {
@@ -1797,7 +1861,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, Ro
     const int bin = t % kBins;
     for (int q = threadIdx.x; q < rm.M * D.r; q += kGemvThreads) {
       const int mm = q / D.r, j = q % D.r;
-      if (!rsel(rm.fast, mm) || !L.A[6]) continue;
+      if (!rml.fast[mm] || !L.A[6]) continue;
       float v = 0.f;
       if (first) {
         for (int ii = 0; ii < 16; ++ii) v += ad_s[j * 16 + ii] * act[mm * 16 + ii];
@@ -1855,6 +1919,8 @@ __global__ __launch_bounds__(kGemvThreads) void k_down(Dims D, LayerPtrs L, RowM
   __shared__ int ex_s[kMaxSeq];                                  // exited (PRE)
   __shared__ const float* xrow_s[kMaxRows];
   extern __shared__ __attribute__((aligned(16))) char dyn[];
+  __shared__ SkRmLds rmu;   // the row map, for per-thread indices (read after the first barrier)
+  const RowMap& rml = rmu.rm;
   const int ntiles = D.d / 16;
   if ((int)blockIdx.x >= ntiles) return;
   if (io.mode == EX_EXIT) {
@@ -1900,6 +1966,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_down(Dims D, LayerPtrs L, RowM
   __builtin_amdgcn_sched_barrier(0);
   tg.prime(n_local, ptr);
   __builtin_amdgcn_sched_barrier(0);
+  sk_rm_copy(rmu, rm);
   if (tid < rm.M) xrow_s[tid] = ws.ACT + (size_t)tid * D.F;
   if (tid < rm.M * D.r) {
     float a = 0.f;
@@ -1934,10 +2001,10 @@ __global__ __launch_bounds__(kGemvThreads) void k_down(Dims D, LayerPtrs L, RowM
     if (e < rm.M * 16) {
       const int m = e >> 4, nn = n0 + (e & 15);
       float x = first ? xo_s[e] : ws.X[(size_t)m * D.d + nn];
-      const bool ex = first ? ex_s[rsel(rm.seq, m)] != 0 : ws.exited[rsel(rm.seq, m)] != 0;
+      const bool ex = first ? ex_s[rml.seq[m]] != 0 : ws.exited[rml.seq[m]] != 0;
       if (!ex) {
         x += y[e];
-        if (rsel(rm.fast, m) && L.B[6] && L.A[6]) {
+        if (rml.fast[m] && L.B[6] && L.A[6]) {
           if (first) {
             float ad = 0.f;
             for (int j = 0; j < D.r; ++j) ad += bd_s[(e & 15) * D.r + j] * ud[m * D.r + j];
@@ -1949,7 +2016,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_down(Dims D, LayerPtrs L, RowM
         ws.X[(size_t)m * D.d + nn] = x;
       }
       newx[e] = x;
-      pin_s[e] = rsel(rm.fast, m) ? (first ? pino_s[e] : ws.PIN[(size_t)m * D.d + nn]) : 0.f;
+      pin_s[e] = rml.fast[m] ? (first ? pino_s[e] : ws.PIN[(size_t)m * D.d + nn]) : 0.f;
     }
     __syncthreads();
     const int bin = t % kBins;
@@ -1984,6 +2051,8 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
   __shared__ int last_flag;
   __shared__ const float* xrow_s[kMaxRows];
   extern __shared__ __attribute__((aligned(16))) char dyn[];
+  __shared__ SkRmLds rmu;   // the row map, for per-thread indices (read after the first barrier)
+  const RowMap& rml = rmu.rm;
   if ((int)blockIdx.x >= n_tiles) return;
   using TG = TileGemv<WB, MT>;
   const int lane = threadIdx.x & 63;
@@ -2011,6 +2080,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
   __builtin_amdgcn_sched_barrier(0);
   tg.prime(n_local, ptr);
   __builtin_amdgcn_sched_barrier(0);
+  sk_rm_copy(rmu, rm);
   if (threadIdx.x < rm.M * 4) {
     float a = 0.f;
 #pragma unroll
@@ -2119,8 +2189,8 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
     const int f = rm.first[sq] + rm.cnt[sq] - 1;
     io.next_token[sq + io.draft_slot] = best_s[sq];
     const int t = io.positions[sq] + rm.pos_offset;
-    if (rsel(rm.slow_of, f) >= 0 || !rsel(rm.fast, f)) kv.seq_lens[sq] = t + 1;
-    if (rsel(rm.fast, f) && rsel(rm.slow_of, f) >= 0) {
+    if (rml.slow_of[f] >= 0 || !rml.fast[f]) kv.seq_lens[sq] = t + 1;
+    if (rml.fast[f] && rml.slow_of[f] >= 0) {
       // signal of the last layer
       const float dot = ssum[f * 4 + 1], pin2 = ssum[f * 4 + 2], pp = ssum[f * 4 + 0];
       ws.sig[sq * D.n_layers + D.n_layers - 1] = ws.exited[sq] ? 0.f : dot * rsqrtf(fmaxf(pin2 * pp, 1e-30f));
@@ -2135,7 +2205,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
       const int f = rm.first[sq] + rm.cnt[sq] - 1;
       float v = ws.sig[q];
       // layers after an exit were not run
-      if (!rsel(rm.fast, f) || rsel(rm.slow_of, f) < 0 || (ws.exited[sq] && l >= ws.exitb[sq])) v = 0.f;
+      if (!rml.fast[f] || rml.slow_of[f] < 0 || (ws.exited[sq] && l >= ws.exitb[sq])) v = 0.f;
       io.signal_out[q] = v;
     }
   }
