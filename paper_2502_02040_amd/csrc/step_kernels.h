@@ -406,7 +406,7 @@ __device__ __forceinline__ u32x4_t ld_glob(const char* p) {
 
 // Dynamic LDS of a tile GEMV launch with reduction length K.
 __host__ __device__ constexpr int tile_lds_bytes(int wb, int MT, int K) {
-  return MT <= 2 ? MT * K * 4 : kGemvWaves * MT * kChunk * (wb ? 32 : 16) * 4;
+  return MT <= 2 ? MT * K * 4 : kGemvWaves * MT * (MT <= 8 ? kChunk : kChunk / 2) * (wb ? 32 : 16) * 4;
 }
 
 template <int WB, int MT, int BS = 1024>
@@ -414,16 +414,20 @@ struct TileGemv {
   static constexpr int KSTEP = WB ? 32 : 16;
   static constexpr int P = KSTEP / 4;
   static constexpr bool XRES = MT <= 2;
-  // up to 8 rows the next chunk's activations are requested one chunk ahead
-  // (16 rows would not fit the registers: they are requested as the chunk
-  // starts)
-  static constexpr bool XPIPE = !XRES && MT <= 8;
-  u32x4_t w[kChunk], w2[kChunk];
+  // the next chunk's activations are requested one chunk ahead; 16 rows take
+  // chunks of half as many K-steps so that they fit the registers
+  static constexpr bool XPIPE = !XRES;
+  static constexpr int KC = MT <= 8 ? kChunk : kChunk / 2;   // K-steps per chunk
+  static constexpr int PPR = KC * P;                          // float4 pieces of one row in a chunk
+  static constexpr int RP = 64 / PPR;                         // rows one pass of the lanes covers
+  static constexpr int NX = (MT + RP - 1) / RP;               // activation pieces per lane
+  static_assert(64 % PPR == 0 && MT % RP == 0, "chunk pieces tile the wave");
+  u32x4_t w[KC], w2[KC];
   int nsteps, s0, s1, nchunks;
   char* xl;                   // LDS: resident rows (XRES) or per-wave chunk staging
   const float* xr[MT];        // activation rows (16-row class)
   const float* gain;
-  float4 xa[MT];              // activations of the chunk to stage next (not resident)
+  float4 xa[NX];              // activations of the chunk to stage next (not resident)
   float4 ga;                  // and its gain (row 0 again without a gain: never used)
 
   __device__ __forceinline__ void init(int K, char* lds) {
@@ -432,15 +436,15 @@ struct TileGemv {
     const int per = (nsteps + kGemvWaves - 1) / kGemvWaves;
     s0 = min(nsteps, wave * per);
     s1 = min(nsteps, s0 + per);
-    nchunks = (s1 - s0 + kChunk - 1) / kChunk;
-    xl = XRES ? lds : lds + wave * (MT * kChunk * KSTEP * 4);
+    nchunks = (s1 - s0 + KC - 1) / KC;
+    xl = XRES ? lds : lds + wave * (MT * KC * KSTEP * 4);
   }
 
   // blocks sb.. of the tile at `base` (this lane's 16 bytes); blocks past the
   // wave's range repeat its last block (a cache hit, never used)
-  __device__ __forceinline__ void load(const char* base, int sb, u32x4_t (&dst)[kChunk]) const {
+  __device__ __forceinline__ void load(const char* base, int sb, u32x4_t (&dst)[KC]) const {
 #pragma unroll
-    for (int j = 0; j < kChunk; ++j) dst[j] = ld_glob(base + (size_t)min(sb + j, s1 - 1) * BS);
+    for (int j = 0; j < KC; ++j) dst[j] = ld_glob(base + (size_t)min(sb + j, s1 - 1) * BS);
   }
 
   // The first two chunks of the workgroup's chunk sequence (tile i starts at
@@ -452,7 +456,7 @@ struct TileGemv {
     // second chunk: in the first tile, else the next tile, else repeats of the last block
     const bool next_tile = nchunks == 1 && n_local > 1;
     const char* b2 = next_tile ? ptr(1) : ptr(0);
-    const int sb2 = nchunks > 1 ? s0 + kChunk : (next_tile ? s0 : s1);
+    const int sb2 = nchunks > 1 ? s0 + KC : (next_tile ? s0 : s1);
     load(ptr(0) + lo16, s0, w);
     load(b2 + lo16, sb2, w2);
   }
@@ -593,12 +597,18 @@ struct TileGemv {
   // sb.. into xa / ga.  Unconditional loads at clamped addresses.
   __device__ __forceinline__ void fetch_x(int sb) {
     const int lane = threadIdx.x & 63;
-    const int q = WB ? lane : (lane & 31);
-    const bool live = q < min(kChunk, s1 - sb) * P;
+    const int q = lane % PPR, r0 = lane / PPR;   // piece q of rows r0, r0 + RP, ...
+    const bool live = q < min(KC, s1 - sb) * P;
     const int kq = sb * KSTEP + 4 * (live ? q : 0);
     ga = ldg4((gain ? gain : xr[0]) + kq);
 #pragma unroll
-    for (int m = 0; m < MT; ++m) xa[m] = ldg4(xr[m] + kq);
+    for (int j = 0; j < NX; ++j) {
+      const float* rp = xr[j * RP];   // selects over constant indices (no runtime index into xr[])
+#pragma unroll
+      for (int c = 1; c < RP; ++c)
+        if (r0 == c) rp = xr[j * RP + c];
+      xa[j] = ldg4(rp + kq);
+    }
   }
 
   // One chunk of steps [sb, sb+8) ∩ [.., s1): the MFMAs consume buf, then buf
@@ -607,15 +617,15 @@ struct TileGemv {
   // were requested one chunk earlier (xa); once they are staged, those of the
   // next chunk (steps xsb..) are requested before the weights two ahead, so
   // that waiting for them never waits for weights that are not yet needed.
-  __device__ __forceinline__ void chunk(int sb, const char* nbase, int nsb, u32x4_t (&buf)[kChunk], f32x4_t& acc,
+  __device__ __forceinline__ void chunk(int sb, const char* nbase, int nsb, u32x4_t (&buf)[KC], f32x4_t& acc,
                                         int xsb) {
     const int lane = threadIdx.x & 63;
     const int mr = lane & 15, grp = lane >> 4;
     const int mread = mr < MT ? mr : MT - 1;
-    const int nst = min(kChunk, s1 - sb);
+    const int nst = min(KC, s1 - sb);
     if constexpr (XRES) {
 #pragma unroll
-      for (int jj = 0; jj < kChunk; ++jj) {
+      for (int jj = 0; jj < KC; ++jj) {
         const int st = min(sb + jj, nsteps - 1);
         const bool on = jj < nst;
         if constexpr (WB) {
@@ -637,24 +647,23 @@ struct TileGemv {
         }
       }
     } else {
-      // stage this chunk's activations (up to 8 rows: requested one chunk earlier)
-      const int q = WB ? lane : (lane & 31);
+      // stage this chunk's activations (requested one chunk earlier)
+      const int q = lane % PPR, r0 = lane / PPR;
       const bool live = q < nst * P;
-      if constexpr (!XPIPE) fetch_x(sb);
       const float4 gv = gain ? ga : make_float4(1.f, 1.f, 1.f, 1.f);
-      const float4* xv = xa;
       char* my = xl;
       const int j = q / P, e = (q % P) * 4;
 #pragma unroll
-      for (int m = 0; m < MT; ++m) {
-        float4 v = xv[m];
+      for (int jx = 0; jx < NX; ++jx) {
+        const int m = r0 + RP * jx;
+        float4 v = xa[jx];
         v.x = live ? v.x * gv.x : 0.f;
         v.y = live ? v.y * gv.y : 0.f;
         v.z = live ? v.z * gv.z : 0.f;
         v.w = live ? v.w * gv.w : 0.f;
         if constexpr (WB) {
           uint16_t* hi = (uint16_t*)my;
-          uint16_t* lo = hi + kChunk * MT * 32;
+          uint16_t* lo = hi + KC * MT * 32;
           const float xs[4] = {v.x, v.y, v.z, v.w};
           uint32_t h[4], l[4];
 #pragma unroll
@@ -672,16 +681,14 @@ struct TileGemv {
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      if constexpr (XPIPE) {
-        __builtin_amdgcn_sched_barrier(0);
-        fetch_x(xsb);
-        __builtin_amdgcn_sched_barrier(0);
-      }
+      __builtin_amdgcn_sched_barrier(0);
+      fetch_x(xsb);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int jj = 0; jj < kChunk; ++jj) {
+      for (int jj = 0; jj < KC; ++jj) {
         if constexpr (WB) {
           const uint16_t* hi = (const uint16_t*)my;
-          const uint16_t* lo = hi + kChunk * MT * 32;
+          const uint16_t* lo = hi + KC * MT * 32;
           const int o = (jj * MT + mread) * 32 + 8 * grp;
           const bf16x8_t a_hi = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(hi + o));
           const bf16x8_t a_lo = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(lo + o));
@@ -720,11 +727,11 @@ struct TileGemv {
     const char* cur_tile = ptr(0);
     if constexpr (XPIPE) fetch_x(s0);
     // steps of the chunk after chunk k (activations repeat from tile to tile)
-    auto xnext = [&](int kk) { return s0 + (kk + 1 == nchunks ? 0 : kk + 1) * kChunk; };
-    auto step = [&](u32x4_t (&buf)[kChunk]) -> bool {
+    auto xnext = [&](int kk) { return s0 + (kk + 1 == nchunks ? 0 : kk + 1) * KC; };
+    auto step = [&](u32x4_t (&buf)[KC]) -> bool {
       const bool more2 = i2 < n_local;
       const char* nb = more2 ? ptr(i2) + lo16 : cur_tile + lo16;
-      chunk(s0 + k * kChunk, nb, more2 ? s0 + k2 * kChunk : s1, buf, acc, xnext(k));
+      chunk(s0 + k * KC, nb, more2 ? s0 + k2 * KC : s1, buf, acc, xnext(k));
       if (k == nchunks - 1) {
         epi(i, acc);
         acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
