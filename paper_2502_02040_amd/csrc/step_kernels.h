@@ -429,6 +429,7 @@ struct TileGemv {
   const float* gain;
   float4 xa[NX];              // activations of the chunk to stage next (not resident)
   float4 ga;                  // and its gain (row 0 again without a gain: never used)
+  bool xfetched = false;      // the first chunk's activations were requested before the prime
 
   __device__ __forceinline__ void init(int K, char* lds) {
     const int wave = threadIdx.x >> 6;
@@ -444,14 +445,16 @@ struct TileGemv {
   // wave's range repeat its last block (a cache hit, never used)
   __device__ __forceinline__ void load(const char* base, int sb, u32x4_t (&dst)[KC]) const {
 #pragma unroll
-    for (int j = 0; j < KC; ++j) dst[j] = ld_glob(base + (size_t)min(sb + j, s1 - 1) * BS);
+    for (int j = 0; j < KC; ++j) dst[j] = ld_glob(base + (size_t)max(min(sb + j, s1 - 1), 0) * BS);
   }
 
   // The first two chunks of the workgroup's chunk sequence (tile i starts at
   // ptr(i)), put in flight before the kernel's prologue.
   template <class Ptr>
+  // Unconditional (a wave without steps loads the tile's last block, never
+  // used): the loads issued before it are then waited for by count, never
+  // behind these.  The launching kernels guarantee n_local >= 1.
   __device__ __forceinline__ void prime(int n_local, const Ptr& ptr) {
-    if (s0 >= s1 || n_local <= 0) return;
     const int lo16 = (threadIdx.x & 63) * 16;
     // second chunk: in the first tile, else the next tile, else repeats of the last block
     const bool next_tile = nchunks == 1 && n_local > 1;
@@ -593,6 +596,17 @@ struct TileGemv {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
 
+  // Not resident, rows known at kernel start: the rows (rows >= M repeat a
+  // live row) and the first chunk's activations, requested before the
+  // weights are primed so that waiting for them never waits for the weights.
+  __device__ __forceinline__ void early_rows(const float* const (&rows)[MT], const float* gn) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m) xr[m] = rows[m];
+    gain = gn;
+    fetch_x(s0);
+    xfetched = true;
+  }
+
   // 16-row class: request the activations (and gains) of the chunk at steps
   // sb.. into xa / ga.  Unconditional loads at clamped addresses.
   __device__ __forceinline__ void fetch_x(int sb) {
@@ -603,10 +617,16 @@ struct TileGemv {
     ga = ldg4((gain ? gain : xr[0]) + kq);
 #pragma unroll
     for (int j = 0; j < NX; ++j) {
-      const float* rp = xr[j * RP];   // selects over constant indices (no runtime index into xr[])
+      // a select over opaque values (a select over the array's elements would
+      // become a runtime index into xr[], i.e. scratch memory)
+      const float* rp = xr[j * RP];
+      asm volatile("" : "+v"(rp));
 #pragma unroll
-      for (int c = 1; c < RP; ++c)
-        if (r0 == c) rp = xr[j * RP + c];
+      for (int c = 1; c < RP; ++c) {
+        const float* pc = xr[j * RP + c];
+        asm volatile("" : "+v"(pc));
+        if (r0 == c) rp = pc;
+      }
       xa[j] = ldg4(rp + kq);
     }
   }
@@ -725,7 +745,8 @@ struct TileGemv {
     for (int a = 0; a < 2; ++a)
       if (++k2 == nchunks) { k2 = 0; ++i2; }
     const char* cur_tile = ptr(0);
-    if constexpr (XPIPE) fetch_x(s0);
+    if constexpr (XPIPE)
+      if (!xfetched) fetch_x(s0);
     // steps of the chunk after chunk k (activations repeat from tile to tile)
     auto xnext = [&](int kk) { return s0 + (kk + 1 == nchunks ? 0 : kk + 1) * KC; };
     auto step = [&](u32x4_t (&buf)[KC]) -> bool {
@@ -1017,21 +1038,21 @@ __global__ __launch_bounds__(256) void k_embed(Dims D, const void* embed, RowMap
   }
 }
 
-// Gate decision for the boundary before `layer`, identical in every
-// workgroup (same inputs, same summation order).  Fills, per sequence,
-// reinit (p <- h for this layer) and the updated exited flag / boundary;
-// sig[s] receives the signal of layer-1.
+// Gate decision of sequence s for the boundary before `layer`, identical in
+// every workgroup (same inputs, same summation order): reinit (p <- h for
+// this layer) and the updated exited flag / boundary; sig[s] receives the
+// signal of layer-1.
 __device__ void gate_logic(const Dims& D, const RowMap& rm, const int* ex_in, const int* eb_in, const StepIO& io,
-                           int layer, const float* ssum /* [16][4] */, int* reinit_s, int* exited_s, int* exitb_s,
-                           float* sig_s) {
-  for (int s = 0; s < rm.nseq; ++s) {
+                           int layer, const float* ssum /* [16][4] */, const float* asig, int* reinit_s, int* exited_s,
+                           int* exitb_s, float* sig_s, int s) {
+  {
     int ex = ex_in[s], eb = eb_in[s], ri = 0;
     float sg = 0.f;
     const int f = rm.first[s] + rm.cnt[s] - 1;
     if (layer > 0 && rm.fast[f]) {
       const float dot = ssum[f * 4 + 1], pin2 = ssum[f * 4 + 2], pp = ssum[f * 4 + 0];
       sg = dot * rsqrtf(fmaxf(pin2 * pp, 1e-30f));
-      if (io.arla_sig && is_gate(io, layer)) sg = io.arla_sig[s];
+      if (io.arla_sig && is_gate(io, layer)) sg = asig[s];   // the router scores, read before the weights
       if (!ex && io.mode != EX_OFF && is_gate(io, layer) && rm.slow_of[f] >= 0) {
         const bool fired = sg >= io.tau;
         if (fired && eb == D.n_layers) eb = layer;
@@ -1040,6 +1061,22 @@ __device__ void gate_logic(const Dims& D, const RowMap& rm, const int* ex_in, co
       }
     }
     reinit_s[s] = ri; exited_s[s] = ex; exitb_s[s] = eb; sig_s[s] = sg;
+  }
+}
+
+// uo_s[m][j] = sum over heads h (in order) of uo[m][h][j] for every fast row
+// m: the o-adapter's down-projection, summed over the heads, all rows at
+// once (every thread one (row, j) pair, its loads independent).  Read after
+// the caller's next barrier.
+__device__ __forceinline__ void fast_uo_sums(const Dims& D, const RowMap& rml, int M, const float* uo, float* uo_s) {
+  for (int e = threadIdx.x; e < M * D.r; e += blockDim.x) {
+    const int m = e / D.r, o = e - m * D.r;
+    if (!rml.fast[m]) continue;
+    const float* src = uo + (size_t)m * D.H * D.r + o;
+    float a = 0.f;
+#pragma unroll 8
+    for (int h = 0; h < D.H; ++h) a += ld_agent(src + (size_t)h * D.r);
+    uo_s[e] = a;
   }
 }
 
@@ -1056,7 +1093,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_qkv(Dims D, LayerPtrs L, RowMa
   __shared__ float ssum[kMaxRows * 4];
   __shared__ int ex_in[kMaxSeq], eb_in[kMaxSeq];
   __shared__ int reinit_s[kMaxSeq], exited_s[kMaxSeq], exitb_s[kMaxSeq];
-  __shared__ float sig_s[kMaxSeq];
+  __shared__ float sig_s[kMaxSeq], asig_s[kMaxSeq];
   __shared__ float inv_rms[kMaxRows];
   __shared__ int src_s[kMaxRows];
   __shared__ const float* xrow_s[kMaxRows];
@@ -1068,12 +1105,19 @@ __global__ __launch_bounds__(kGemvThreads) void k_qkv(Dims D, LayerPtrs L, RowMa
   const int ntiles = 3 * tq + (3 * D.r + 15) / 16;
   const size_t tb = (size_t)16 * D.d * (WB ? 2 : 4);   // bytes of one packed tile
   // tile t: Wq, Wk, Wv, then the stacked adapter-down rows [A_q; A_k; A_v]
-  auto tile_ptr = [&](int t) -> const char* {
+  // the four base pointers as values (a select over the kernel-argument
+  // fields would become a vector load from the argument segment)
+  const char* bq = (const char*)L.pq;
+  const char* bk = (const char*)L.pk;
+  const char* bv_ = (const char*)L.pv;
+  const char* ba = (const char*)L.pa;
+  asm volatile("" : "+s"(bq), "+s"(bk), "+s"(bv_), "+s"(ba));
+  auto tile_ptr = [bq, bk, bv_, ba, tq, tb](int t) -> const char* {
     if (t < 3 * tq) {
       const int which = t / tq;
-      return (const char*)(which == 0 ? L.pq : (which == 1 ? L.pk : L.pv)) + (size_t)(t - which * tq) * tb;
+      return (which == 0 ? bq : (which == 1 ? bk : bv_)) + (size_t)(t - which * tq) * tb;
     }
-    return (const char*)L.pa + (size_t)(t - 3 * tq) * tb;
+    return ba + (size_t)(t - 3 * tq) * tb;
   };
   if ((int)blockIdx.x >= ntiles) return;
   auto ptr = [&](int i) { return tile_ptr(blockIdx.x + i * gridDim.x); };
@@ -1090,6 +1134,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_qkv(Dims D, LayerPtrs L, RowMa
   }
   const int sq0 = min((int)threadIdx.x, rm.nseq - 1);
   const int exv = ws.exited[sq0], ebv = ws.exitb[sq0];
+  const float asv = (io.arla_sig ? io.arla_sig : ws.arla_sig)[sq0];   // unconditional: used only with the router
   const float* rows[MT];
 #pragma unroll
   for (int m = 0; m < MT; ++m) rows[m] = ws.X + (size_t)min(m, rm.M - 1) * D.d;
@@ -1108,18 +1153,22 @@ __global__ __launch_bounds__(kGemvThreads) void k_qkv(Dims D, LayerPtrs L, RowMa
   if (threadIdx.x < rm.nseq) {
     ex_in[threadIdx.x] = exv;
     eb_in[threadIdx.x] = ebv;
+    asig_s[threadIdx.x] = asv;
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    gate_logic(D, rm, ex_in, eb_in, io, layer, ssum, reinit_s, exited_s, exitb_s, sig_s);
-    for (int m = 0; m < rm.M; ++m) {
-      const int sq = rml.seq[m];
-      int src = m;
-      if (rml.fast[m] && reinit_s[sq]) src = rml.slow_of[m];
-      src_s[m] = src;
-      xrow_s[m] = ws.X + (size_t)src * D.d;
-      inv_rms[m] = rsqrtf(ssum[src * 4] / D.d + D.eps);
-    }
+  // one thread per sequence, then one per row (serial loops of dependent LDS
+  // reads on one thread took microseconds)
+  if (threadIdx.x < rm.nseq)
+    gate_logic(D, rml, ex_in, eb_in, io, layer, ssum, asig_s, reinit_s, exited_s, exitb_s, sig_s, threadIdx.x);
+  __syncthreads();
+  if (threadIdx.x < rm.M) {
+    const int m = threadIdx.x;
+    const int sq = rml.seq[m];
+    int src = m;
+    if (rml.fast[m] && reinit_s[sq]) src = rml.slow_of[m];
+    src_s[m] = src;
+    xrow_s[m] = ws.X + (size_t)src * D.d;
+    inv_rms[m] = rsqrtf(ssum[src * 4] / D.d + D.eps);
   }
   __syncthreads();
   if (blockIdx.x == 0 && threadIdx.x < rm.nseq) {
@@ -1554,9 +1603,9 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn(Dims D, LayerPtrs L, RowM
 // ============================================================================
 // Kernel: output projection + residual add (+ adapter on the fast row);
 // partial sums for the gate/up prologue.  Persistent tile GEMV, grid <= d/16.
-// The 2-row class issues its epilogue operands for the workgroup's first tile
-// (old residual values, the B_o rows, the A_g/A_u columns and gains) before
-// the weights, so the epilogue waits for nothing but the reduction.
+// The epilogue operands of the workgroup's first tile (old residual values,
+// the B_o rows, the A_g/A_u columns and gains, the exit flags) are issued
+// before the weights, so that epilogue waits for nothing but the reduction.
 // ============================================================================
 template <int WB, int MT>
 __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int layer) {
@@ -1566,12 +1615,11 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
   __shared__ float y[256];
   __shared__ float uo_s[kMaxRows * kMaxRank];
   __shared__ float newx[256];
-  __shared__ float xo_s[kMaxRows * 16];      // first tile: X of every row (PRE)
-  __shared__ float bo_s[16 * kMaxRank];      // first tile: B_o rows (PRE)
-  __shared__ float agu_s[2 * kMaxRank * 16]; // first tile: A_g, A_u columns times g_mlp (PRE)
+  __shared__ float xo_s[kMaxRows * 16];      // first tile: X of every row
+  __shared__ float bo_s[16 * kMaxRank];      // first tile: B_o rows
+  __shared__ float agu_s[2 * kMaxRank * 16]; // first tile: A_g, A_u columns times g_mlp
   __shared__ float ud_s[2 * kGemvThreads];   // per-head o-adapter values of the fast row (PRE)
-  __shared__ int flag_s[2 * kMaxSeq];        // exited, reinit (PRE)
-  __shared__ const float* xrow_s[kMaxRows];
+  __shared__ int flag_s[2 * kMaxSeq];        // exited, reinit
   extern __shared__ __attribute__((aligned(16))) char dyn[];
   __shared__ SkRmLds rmu;   // the row map, for per-thread indices (read after the first barrier)
   const RowMap& rml = rmu.rm;
@@ -1605,15 +1653,19 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
   const int tid = threadIdx.x;
   const int HR = D.H * D.r;
   const bool pre_uo = PRE && HR <= 2 * kGemvThreads;     // per-head values fit two per thread
-  const bool pre_agu = PRE && 2 * D.r * 16 <= kGemvThreads;
+  const bool pre_agu = 2 * D.r * 16 <= kGemvThreads;
+  // ---- everything needed before the weights: issued first, unconditional
+  // loads at clamped indices (a load under a branch, or a value consumed
+  // right away, would make the wave wait before the prime); the first
+  // tile's epilogue operands in every class ----
+  if constexpr (!PRE) tg.early_rows(rows, nullptr);
   if constexpr (PRE) {
-    // ---- everything needed before the weights: issued first, unconditional
-    // loads at clamped indices (a load under a branch, or a value consumed
-    // right away, would make the wave wait before the prime) ----
     tg.load_pieces(rows, nullptr, xp);
     const int fm = fast_m >= 0 ? fast_m : 0;
     pre[0] = ws.uo[(size_t)fm * HR + min(tid, HR - 1)];
     pre[1] = ws.uo[(size_t)fm * HR + min(tid + kGemvThreads, HR - 1)];
+  }
+  {
     const int mx = min(tid >> 4, rm.M - 1);
     pre[2] = ws.X[(size_t)mx * D.d + n00 + (tid & 15)];
     const int bq = min(tid, 16 * D.r - 1);
@@ -1630,11 +1682,12 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
   tg.prime(n_local, ptr);
   __builtin_amdgcn_sched_barrier(0);
   sk_rm_copy(rmu, rm);
-  if (threadIdx.x < rm.M) xrow_s[threadIdx.x] = ws.O + (size_t)threadIdx.x * D.qdim;
   for (int e = threadIdx.x; e < rm.M * D.r; e += kGemvThreads) uo_s[e] = 0.f;
   if constexpr (PRE) {
     ud_s[tid] = pre[0];
     ud_s[tid + kGemvThreads] = pre[1];
+  }
+  {
     if (tid < rm.M * 16) xo_s[tid] = pre[2];
     if (tid < 16 * D.r) bo_s[tid] = L.B[3] ? raw_f<WB>(praw) : 0.f;
     if (pre_agu && tid < 2 * D.r * 16) {
@@ -1653,23 +1706,19 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
         uo_s[fast_m * D.r + tid] = a;
       }
     } else if (L.A[3]) {
-      for (int m = 0; m < rm.M; ++m)
-        if (rml.fast[m]) column_sums(ws.uo + (size_t)m * D.H * D.r, D.H, D.r, D.r, uo_s + m * D.r, red);
+      fast_uo_sums(D, rml, rm.M, ws.uo, uo_s);
     }
     int sel[MT];
 #pragma unroll
     for (int m = 0; m < MT; ++m) sel[m] = m < rm.M ? m : 0;
     tg.store_pieces(xp, rows, nullptr, sel);
   } else {
-    if (L.A[3])
-      for (int m = 0; m < rm.M; ++m)
-        if (rml.fast[m]) column_sums(ws.uo + (size_t)m * D.H * D.r, D.H, D.r, D.r, uo_s + m * D.r, red);
-    tg.set_rows(xrow_s, nullptr, rm.M, D.qdim);
+    if (L.A[3]) fast_uo_sums(D, rml, rm.M, ws.uo, uo_s);
   }
   __syncthreads();
   auto epi = [&](int i, const f32x4_t& a) {
     const int t = blockIdx.x + i * gridDim.x;
-    const bool first = PRE && i == 0;   // operands already in LDS
+    const bool first = i == 0;   // operands already in LDS
     f32x4_t acc[1] = {a};
     gemv_reduce<1>(acc, rm.M, red, y);
     const int n0 = t * 16;
@@ -1740,9 +1789,9 @@ __global__ __launch_bounds__(kGemvThreads) void k_oproj(Dims D, LayerPtrs L, Row
 // ============================================================================
 // Kernel: gate/up projections (the gate and up tiles of the same 16 rows, one
 // after the other), adapter-up, SwiGLU; partial sums of the down adapter's
-// down-projection.  Persistent tile GEMV, grid <= ffn/16.  The 2-row class
-// issues the row statistics, its activation pieces and the first pair's
-// B_g, B_u rows and A_d columns before the weights.
+// down-projection.  Persistent tile GEMV, grid <= ffn/16.  The row
+// statistics and the first pair's B_g, B_u rows and A_d columns are issued
+// before the weights (the 2-row class also its activation pieces).
 // ============================================================================
 template <int WB, int MT>
 __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int layer) {
@@ -1753,9 +1802,8 @@ __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, Ro
   __shared__ float stat[kMaxRows * (1 + 2 * kMaxRank)];
   __shared__ float inv_rms[kMaxRows];
   __shared__ float act[256];
-  __shared__ float bgu_s[2 * 16 * kMaxRank];   // first pair: B_g, B_u rows (PRE)
-  __shared__ float ad_s[kMaxRank * 16];        // first pair: A_d columns (PRE)
-  __shared__ const float* xrow_s[kMaxRows];
+  __shared__ float bgu_s[2 * 16 * kMaxRank];   // first pair: B_g, B_u rows
+  __shared__ float ad_s[kMaxRank * 16];        // first pair: A_d columns
   extern __shared__ __attribute__((aligned(16))) char dyn[];
   __shared__ SkRmLds rmu;   // the row map, for per-thread indices (read after the first barrier)
   const RowMap& rml = rmu.rm;
@@ -1776,7 +1824,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, Ro
   const int PO = 1 + 2 * D.r;
   const int n00 = blockIdx.x * 16;
   const int tid = threadIdx.x;
-  const bool pre_b = PRE && 2 * 16 * D.r <= kGemvThreads;
+  const bool pre_b = 2 * 16 * D.r <= kGemvThreads;
   TG tg;
   tg.init(D.d, dyn);
   // ---- everything needed before the weights: issued first ----
@@ -1792,8 +1840,9 @@ __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, Ro
   for (int m = 0; m < MT; ++m) rows[m] = ws.X + (size_t)min(m, rm.M - 1) * D.d;
   typename TG::template Pieces<2> xp;
   uint32_t pb = 0, pa = 0;
-  if constexpr (PRE) {
-    tg.load_pieces(rows, L.mlp_norm, xp);
+  if constexpr (PRE) tg.load_pieces(rows, L.mlp_norm, xp);
+  else tg.early_rows(rows, L.mlp_norm);
+  {   // the first pair's epilogue operands (every class)
     const int bq = min(tid, 2 * 16 * D.r - 1);
     const int which = bq / (16 * D.r), rr = (bq / D.r) % 16, j = bq % D.r;
     const void* B = which ? L.B[5] : L.B[4];
@@ -1805,7 +1854,6 @@ __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, Ro
   tg.prime(n_local, ptr);
   __builtin_amdgcn_sched_barrier(0);
   sk_rm_copy(rmu, rm);
-  if (tid < rm.M) xrow_s[tid] = ws.X + (size_t)tid * D.d;
   if (tid < rm.M * PO) {
     float a = 0.f;
 #pragma unroll
@@ -1817,7 +1865,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, Ro
     const bool has = which ? (L.B[5] && L.A[5]) : (L.B[4] && L.A[4]);
     bgu_s[tid] = has ? raw_f<WB>(pb) : 0.f;
   }
-  if (PRE && tid < D.r * 16) ad_s[tid] = L.A[6] ? raw_f<WB>(pa) : 0.f;
+  if (tid < D.r * 16) ad_s[tid] = L.A[6] ? raw_f<WB>(pa) : 0.f;
   __syncthreads();
   if (tid < rm.M) inv_rms[tid] = rsqrtf(stat[tid * PO] / D.d + D.eps);
   if constexpr (PRE) {
@@ -1825,8 +1873,6 @@ __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, Ro
 #pragma unroll
     for (int m = 0; m < MT; ++m) sel[m] = m < rm.M ? m : 0;
     tg.store_pieces(xp, rows, L.mlp_norm, sel);
-  } else {
-    tg.set_rows(xrow_s, L.mlp_norm, rm.M, D.d);
   }
   __syncthreads();
   f32x4_t acc_g = {0.f, 0.f, 0.f, 0.f};
@@ -1836,7 +1882,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_gateup(Dims D, LayerPtrs L, Ro
       return;
     }
     const int t = blockIdx.x + (i >> 1) * gridDim.x;
-    const bool first = PRE && i == 1;
+    const bool first = i == 1;
     f32x4_t acc[2] = {acc_g, a};
     gemv_reduce<2>(acc, rm.M, red, y);
     const int n0 = t * 16;
@@ -1909,9 +1955,9 @@ __device__ void rows_unchanged_stats(const Dims& D, const RowMap& rm, const WS& 
 // ============================================================================
 // Kernel: down projection + residual add (+ adapter); partial sums for the
 // next layer's norm and the exit signal.  Persistent tile GEMV, grid <= d/16.
-// The 2-row class issues the adapter sums, its activation pieces and the
-// first tile's residual values, fast-row inputs and B_d rows before the
-// weights.
+// The adapter sums and the first tile's residual values, fast-row inputs and
+// B_d rows are issued before the weights (the 2-row class also its
+// activation pieces).
 // ============================================================================
 template <int WB, int MT>
 __global__ __launch_bounds__(kGemvThreads) void k_down(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, int layer) {
@@ -1921,10 +1967,9 @@ __global__ __launch_bounds__(kGemvThreads) void k_down(Dims D, LayerPtrs L, RowM
   __shared__ float y[256];
   __shared__ float ud[kMaxRows * kMaxRank];
   __shared__ float newx[256], pin_s[256];
-  __shared__ float xo_s[kMaxRows * 16], pino_s[kMaxRows * 16];   // first tile (PRE)
-  __shared__ float bd_s[16 * kMaxRank];                          // first tile: B_d rows (PRE)
-  __shared__ int ex_s[kMaxSeq];                                  // exited (PRE)
-  __shared__ const float* xrow_s[kMaxRows];
+  __shared__ float xo_s[kMaxRows * 16], pino_s[kMaxRows * 16];   // first tile
+  __shared__ float bd_s[16 * kMaxRank];                          // first tile: B_d rows
+  __shared__ int ex_s[kMaxSeq];                                  // exited
   extern __shared__ __attribute__((aligned(16))) char dyn[];
   __shared__ SkRmLds rmu;   // the row map, for per-thread indices (read after the first barrier)
   const RowMap& rml = rmu.rm;
@@ -1961,8 +2006,9 @@ __global__ __launch_bounds__(kGemvThreads) void k_down(Dims D, LayerPtrs L, RowM
   float px = 0.f, pp = 0.f;
   uint32_t pb = 0;
   int pe = 0;
-  if constexpr (PRE) {
-    tg.load_pieces(rows, nullptr, xp);
+  if constexpr (PRE) tg.load_pieces(rows, nullptr, xp);
+  else tg.early_rows(rows, nullptr);
+  {   // the first tile's epilogue operands (every class)
     const int m = min(tid >> 4, rm.M - 1);
     px = ws.X[(size_t)m * D.d + n00 + (tid & 15)];
     pp = ws.PIN[(size_t)m * D.d + n00 + (tid & 15)];
@@ -1974,17 +2020,16 @@ __global__ __launch_bounds__(kGemvThreads) void k_down(Dims D, LayerPtrs L, RowM
   tg.prime(n_local, ptr);
   __builtin_amdgcn_sched_barrier(0);
   sk_rm_copy(rmu, rm);
-  if (tid < rm.M) xrow_s[tid] = ws.ACT + (size_t)tid * D.F;
   if (tid < rm.M * D.r) {
     float a = 0.f;
 #pragma unroll
     for (int b = 0; b < kBins; ++b) a += uv[b];
     ud[tid] = a;
   }
-  if constexpr (PRE) {
+  {
     if (tid < rm.M * 16) {
       xo_s[tid] = px;
-      pino_s[tid] = rsel(rm.fast, tid >> 4) ? pp : 0.f;
+      pino_s[tid] = pp;   // used for fast rows only
     }
     if (tid < 16 * D.r) bd_s[tid] = (L.B[6] && L.A[6]) ? raw_f<WB>(pb) : 0.f;
     if (tid < rm.nseq) ex_s[tid] = pe;
@@ -1995,12 +2040,10 @@ __global__ __launch_bounds__(kGemvThreads) void k_down(Dims D, LayerPtrs L, RowM
 #pragma unroll
     for (int m = 0; m < MT; ++m) sel[m] = m < rm.M ? m : 0;
     tg.store_pieces(xp, rows, nullptr, sel);
-  } else {
-    tg.set_rows(xrow_s, nullptr, rm.M, D.F);
   }
   auto epi = [&](int i, const f32x4_t& a) {
     const int t = blockIdx.x + i * gridDim.x;
-    const bool first = PRE && i == 0;
+    const bool first = i == 0;
     f32x4_t acc[1] = {a};
     gemv_reduce<1>(acc, rm.M, red, y);
     const int n0 = t * 16;
@@ -2096,20 +2139,20 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
   }
   if (threadIdx.x < rm.nseq) ex_in[threadIdx.x] = exv;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    // rows fed to the head
-    int nh = 0;
-    if (rm.head_all) {
-      for (int m = 0; m < rm.M; ++m) hrow[nh++] = m;
-    } else {
-      for (int sq = 0; sq < rm.nseq; ++sq) {
-        const int f = rm.first[sq], c = rm.cnt[sq];
-        int pick = f;                       // slow row
-        if (rm.fast[f + c - 1] && (ex_in[sq] || rm.slow_of[f + c - 1] < 0)) pick = f + c - 1;
-        hrow[nh++] = pick;
-      }
+  // rows fed to the head: every row of a chunk, else one per sequence (one
+  // thread each: a serial loop of dependent LDS reads took microseconds)
+  if (rm.head_all) {
+    if (threadIdx.x < rm.M) hrow[threadIdx.x] = threadIdx.x;
+    if (threadIdx.x == 0) nh_s = rm.M;
+  } else {
+    const int sq = threadIdx.x;
+    if (sq < rm.nseq) {
+      const int f = rml.first[sq], c = rml.cnt[sq];
+      int pick = f;                       // slow row
+      if (rml.fast[f + c - 1] && (ex_in[sq] || rml.slow_of[f + c - 1] < 0)) pick = f + c - 1;
+      hrow[sq] = pick;
     }
-    nh_s = nh;
+    if (threadIdx.x == 0) nh_s = rm.nseq;
   }
   __syncthreads();
   if (threadIdx.x < nh_s) {
@@ -2193,7 +2236,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
   }
   // decode step / draft step
   for (int sq = threadIdx.x; sq < rm.nseq; sq += kGemvThreads) {
-    const int f = rm.first[sq] + rm.cnt[sq] - 1;
+    const int f = rml.first[sq] + rml.cnt[sq] - 1;
     io.next_token[sq + io.draft_slot] = best_s[sq];
     const int t = io.positions[sq] + rm.pos_offset;
     if (rml.slow_of[f] >= 0 || !rml.fast[f]) kv.seq_lens[sq] = t + 1;
@@ -2209,7 +2252,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
   if (io.signal_out) {
     for (int q = threadIdx.x; q < rm.nseq * D.n_layers; q += kGemvThreads) {
       const int sq = q / D.n_layers, l = q % D.n_layers;
-      const int f = rm.first[sq] + rm.cnt[sq] - 1;
+      const int f = rml.first[sq] + rml.cnt[sq] - 1;
       float v = ws.sig[q];
       // layers after an exit were not run
       if (!rml.fast[f] || rml.slow_of[f] < 0 || (ws.exited[sq] && l >= ws.exitb[sq])) v = 0.f;
@@ -2219,7 +2262,7 @@ __global__ __launch_bounds__(kGemvThreads) void k_head(Dims D, const void* lm_he
   if (io.h_out || io.p_out) {
     for (int q = threadIdx.x; q < rm.nseq * D.d; q += kGemvThreads) {
       const int sq = q / D.d, i = q % D.d;
-      const int f = rm.first[sq], c = rm.cnt[sq];
+      const int f = rml.first[sq], c = rml.cnt[sq];
       if (io.h_out) io.h_out[q] = ws.X[(size_t)f * D.d + i];
       if (io.p_out) io.p_out[q] = ws.X[(size_t)(f + c - 1) * D.d + i];
     }
