@@ -315,13 +315,13 @@ def test_draft_and_verify(name, gamma, exit_layer):
 
 
 @pytest.mark.parametrize("name", CASES)
-@pytest.mark.parametrize("chunks,B", [("1", 3), ("2", 3), ("1", 8)])
+@pytest.mark.parametrize("chunks,B", [("1", 3), ("2", 3), ("4", 3), ("1", 8)])
 def test_batched_dual_step(name, chunks, B, monkeypatch):
     """Three (eight) sequences with different context lengths decoded
-    together (two rows each: the batched short-chain attention with one or
-    two 128-token chunks per split, and the 8-row (16-row) tile GEMVs): every
-    sequence's logits, h, p, signal, token and cache entry match the oracle
-    step by step."""
+    together (two rows each: the batched short-chain attention with one, two
+    or four 128-token chunks per split, and the 8-row (16-row) tile GEMVs):
+    every sequence's logits, h, p, signal, token and cache entry match the
+    oracle step by step."""
     monkeypatch.setenv("M2R2_ATTN_CHUNKS", chunks)
     cfg = synth.CONFIGS[name]
     w = synth.make_weights(cfg)
