@@ -1218,7 +1218,8 @@ __device__ __forceinline__ float proj_elem(const Dims& D, const LayerPtrs& L, co
 }
 
 // Fill out[R][hd] with q (which=0) or k (which=1) after RoPE, or v (which=2).
-__device__ void head_vectors(const Dims& D, const LayerPtrs& L, const RowMap& rm, const WS& ws, const StepIO& io,
+__device__ __forceinline__ void head_vectors(const Dims& D, const LayerPtrs& L, const RowMap& rm, const WS& ws,
+                                             const StepIO& io,
                              int first, int R, int which, int h, float* out) {
   const int hd = D.hd, half = hd / 2;
   for (int e = threadIdx.x; e < R * hd; e += kAttnThreads) {
@@ -1297,7 +1298,7 @@ __device__ __forceinline__ float* att_part(const WS& ws, const Dims& D, int s, i
 // Merge the partials of one (sequence, head): the output o of every row and,
 // for fast rows, the o-adapter down-projection of that head.  The partials
 // were written by other workgroups: device-coherent loads.
-__device__ void attn_merge(const Dims& D, const RowMap& rm, const WS& ws, int s, int h, int n_split) {
+__device__ __forceinline__ void attn_merge(const Dims& D, const RowMap& rm, const WS& ws, int s, int h, int n_split) {
   __shared__ float stat[kMaxRows * 64 * 2];   // m, l of every split (n_split + 1 <= 64)
   __shared__ float wgt[kMaxRows * 64];
   __shared__ float linv[kMaxRows];
@@ -1356,9 +1357,13 @@ template <int KB, int HD>
 __global__ __launch_bounds__(kAttnThreads) void k_attn(Dims D, LayerPtrs L, RowMap rm, WS ws, StepIO io, KVPtrs kv,
                                                        int layer, int n_split) {
   extern __shared__ float sm[];
+  __shared__ SkRmLds rmu;   // the row map in LDS: the helpers index it per thread
+  const RowMap& rml = rmu.rm;
+  sk_rm_copy(rmu, rm);
+  __syncthreads();
   constexpr int DPL = HD / 4;             // dims per lane (4 lanes per token)
   const int split = blockIdx.x, h = blockIdx.y, s = blockIdx.z;
-  const int hd = HD, R = rm.cnt[s], first = rm.first[s];
+  const int hd = HD, R = rml.cnt[s], first = rml.first[s];
   const float scale = rsqrtf((float)hd);
   float* q = sm;                           // [R][hd]
   float* kx = q + kMaxRows * kMaxHeadDim;  // [R][hd]
@@ -1376,13 +1381,13 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn(Dims D, LayerPtrs L, RowM
 
   if (own) {
     // ---- the rows' own keys and the cache writes -------------------------------
-    head_vectors(D, L, rm, ws, io, first, R, 1, h, kx);
-    head_vectors(D, L, rm, ws, io, first, R, 2, h, vx);
+    head_vectors(D, L, rml, ws, io, first, R, 1, h, kx);
+    head_vectors(D, L, rml, ws, io, first, R, 2, h, vx);
     for (int e = threadIdx.x; e < R * hd; e += kAttnThreads) {
       const int i = e / hd, d = e % hd;
-      if (!rm.wr[first + i]) continue;
+      if (!rml.wr[first + i]) continue;
       bool ok;
-      const size_t ix = kv_index(kv, D, layer, s, ctx + rm.idx[first + i], h, d, ok);
+      const size_t ix = kv_index(kv, D, layer, s, ctx + rml.idx[first + i], h, d, ok);
       if (!ok) { atomicOr(ws.err, 2); continue; }
       if (KB) {
         ((uint16_t*)kv.k)[ix] = (uint16_t)f32_to_bf16_bits(kx[e]);
@@ -1393,7 +1398,7 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn(Dims D, LayerPtrs L, RowM
       }
     }
     if (!frozen) {
-      head_vectors(D, L, rm, ws, io, first, R, 0, h, q);
+      head_vectors(D, L, rml, ws, io, first, R, 0, h, q);
       // a slow row sees the chunk's slow rows up to itself (as stored in the
       // cache); a fast row sees only its own exact key/value
       float* ownsc = sc;   // [R][R]
@@ -1401,12 +1406,12 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn(Dims D, LayerPtrs L, RowM
         const int i = e / R, jj = e % R;
         const int mi = first + i, mj = first + jj;
         bool vis;
-        if (rm.fast[mi]) vis = (jj == i);
-        else vis = !rm.fast[mj] && rm.idx[mj] <= rm.idx[mi];
+        if (rml.fast[mi]) vis = (jj == i);
+        else vis = !rml.fast[mj] && rml.idx[mj] <= rml.idx[mi];
         float p = -INFINITY;
         if (vis) {
           p = 0.f;
-          const bool rnd = !rm.fast[mi];
+          const bool rnd = !rml.fast[mi];
           for (int d = 0; d < hd; ++d) {
             const float kk = rnd ? kv_round(kx[jj * hd + d], KB) : kx[jj * hd + d];
             p += q[i * hd + d] * kk;
@@ -1432,7 +1437,7 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn(Dims D, LayerPtrs L, RowM
       __syncthreads();
       for (int e = threadIdx.x; e < R * hd; e += kAttnThreads) {
         const int i = e / hd, d = e % hd;
-        const bool rnd = !rm.fast[first + i];
+        const bool rnd = !rml.fast[first + i];
         float a = 0.f;
         for (int jj = 0; jj < R; ++jj) {
           const float w = ownsc[i * R + jj];
@@ -1459,7 +1464,7 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn(Dims D, LayerPtrs L, RowM
       kv_row_load<KB, HD>(kv.k, base, ok && j < nt, kpf[it]);
       kv_row_load<KB, HD>(kv.v, base, ok && j < nt, vpf[it]);
     }
-    head_vectors(D, L, rm, ws, io, first, R, 0, h, q);
+    head_vectors(D, L, rml, ws, io, first, R, 0, h, q);
     if (per * R > kScoreCap) {             // the host sizes splits so that this cannot happen
       if (threadIdx.x == 0) atomicOr(ws.err, 4);
       store = false;
@@ -1561,7 +1566,7 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn(Dims D, LayerPtrs L, RowM
     constexpr int PCS = HD / 8;
     float* up = redp;
     for (int i0 = 0; i0 < R; ++i0) {
-      if (!rm.fast[first + i0] || !L.A[3]) {
+      if (!rml.fast[first + i0] || !L.A[3]) {
         for (int j = threadIdx.x; j < D.r; j += kAttnThreads) uacc_s[i0 * D.r + j] = 0.f;
         continue;
       }
@@ -1597,7 +1602,7 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn(Dims D, LayerPtrs L, RowM
   // every workgroup of the (sequence, head) counts in; the last one merges
   if (!arrive_last(&ws.att_cnt[s * D.H + h], n_split + 1, &last_flag)) return;
   if (frozen) return;
-  attn_merge(D, rm, ws, s, h, n_split);
+  attn_merge(D, rml, ws, s, h, n_split);
 }
 
 // ============================================================================
