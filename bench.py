@@ -184,7 +184,8 @@ def cpu_baseline(cfg, weights, ctx: int, budget_s: float, *, seqs: int = 1):
     import synth
     from oracle import Oracle, KVCache
     orc = Oracle(cfg, weights, np.float32)
-    cache = KVCache(cfg, ctx + 64, np.float32)
+    room = 256   # decode steps the cache has room for (each step appends one position)
+    cache = KVCache(cfg, ctx + room, np.float32)
     kvs = synth.synthetic_kv(cfg, ctx)
     for l, (K, V) in kvs.items():
         cache.load(l, K, V)
@@ -196,7 +197,7 @@ def cpu_baseline(cfg, weights, ctx: int, budget_s: float, *, seqs: int = 1):
         tok = r.token
         n += 1
         el = time.perf_counter() - t0
-        if el >= budget_s or n >= 4096:
+        if el >= budget_s or n >= room:
             break
     what = f"one of the {seqs} sequences' " if seqs > 1 else ""
     return _cpu_line(n / el, "tokens/s", f"{n} dual-stream decode steps of {what}the same model in float32 NumPy at "
