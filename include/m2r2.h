@@ -246,7 +246,10 @@ M2R2_API void m2r2_destroy(m2r2_ctx* ctx);
  * replacement is least-recently-used, with the experts needed now and those
  * predicted for the layer protected from eviction (M2R2_MOE_FIXED: no
  * replacement).  The call returns once the last layer's experts are
- * enqueued. */
+ * enqueued.  With as many slots as experts under M2R2_MOE_ON_DEMAND (every
+ * expert resident, nothing to decide) the call waits for no routing: the
+ * experts are taken from their slots on the device and the whole token is
+ * enqueued at once. */
 M2R2_API m2r2_status m2r2_decode_step(m2r2_ctx* ctx, int32_t batch, int32_t dual, const int32_t* tokens_d,
                                       int32_t* positions_d, const m2r2_kv* kv, const m2r2_exit* ex,
                                       const m2r2_step_out* out, hipStream_t stream);
@@ -394,7 +397,9 @@ M2R2_API m2r2_status m2r2_prefetch_experts(m2r2_ctx* ctx, int32_t layer, const i
  * 0 least recently used -- and zero the statistics.  Synchronous. */
 M2R2_API m2r2_status m2r2_moe_reset(m2r2_ctx* ctx);
 
-/* Counters since the last reset. */
+/* Counters since the last reset.  With as many slots as experts under the
+ * on-demand policy, tokens are enqueued whole (no host wait for routing) and
+ * their hits are counted on the device: the call then waits for the device. */
 M2R2_API m2r2_status m2r2_moe_stats(m2r2_ctx* ctx, m2r2_moe_counters* out);
 
 /* Host-only replay of a cache policy on a routing trace, with no copies:

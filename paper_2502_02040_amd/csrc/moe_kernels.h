@@ -72,64 +72,60 @@ constexpr int kHostWords = 64;
 // largest probabilities (ties to the lower id) and their unrenormalised
 // weights.  Tasks 1, 2 are predictions: top-k of the logits.  Nothing is
 // chosen once the sequence has exited.  The ids are also written to mapped
-// host memory, then `seq` with release semantics at system scope.
+// host memory (when given), then `seq` with release semantics at system scope.
+// Wave t takes task t: every logit is ranked at once against the task's
+// logits in LDS (its place in the order larger value first, then lower id),
+// and a logit of rank < k is chosen at that rank (a NaN ranks as -inf).
 __global__ __launch_bounds__(256) void k_topk(int E, int K, const float* logits, int route, int n_pred, MoePtrs mp,
                                               WS ws, int* slow_out, int* pred_out, int seq) {
   __shared__ int chosen[3][kMaxTopK];
   __shared__ float pr[kMaxTopK];
+  __shared__ float lv[3][kMaxExperts];
   const bool exited = ws.exited[0] != 0;
   if (exited) { route = 0; n_pred = 0; }
-  // wave t takes task t; lane l holds experts l, l+64, l+128, l+192
+  // lane l holds experts l, l+64, l+128, l+192
   constexpr int J = kMaxExperts / 64;
   const int lane = threadIdx.x & 63, t = threadIdx.x >> 6;
-  if (t < 3) {
-    const bool active = t == 0 ? route != 0 : (t - 1) < n_pred;
-    if (active) {
-      float v[J];
+  const bool active = t < 3 && (t == 0 ? route != 0 : (t - 1) < n_pred);
+  float v[J];
+  float mx = -INFINITY, sum = 1.f;
+  if (active) {
 #pragma unroll
-      for (int j = 0; j < J; ++j) v[j] = lane + 64 * j < E ? logits[t * E + lane + 64 * j] : -INFINITY;
+    for (int j = 0; j < J; ++j) {
+      const int e = lane + 64 * j;
+      const float x = e < E ? logits[t * E + e] : -INFINITY;
+      v[j] = x == x ? x : -INFINITY;
+      lv[t][e] = v[j];
+    }
+    if (t == 0) {
       float lm = v[0];
 #pragma unroll
       for (int j = 1; j < J; ++j) lm = fmaxf(lm, v[j]);
-      const float mx = wave_max(lm);
-      float sum = 1.f;
-      if (t == 0) {
-        float se = 0.f;
+      mx = wave_max(lm);
+      float se = 0.f;
 #pragma unroll
-        for (int j = 0; j < J; ++j)
-          if (lane + 64 * j < E) se += __expf(v[j] - mx);
-        sum = wave_sum(se);
-      }
-      // K rounds of a wave-wide arg-max (larger logit, then lower id)
-      unsigned taken = 0;
-      for (int k = 0; k < K; ++k) {
-        float bv = -INFINITY;
-        int bi = 0x7fffffff;
+      for (int j = 0; j < J; ++j)
+        if (lane + 64 * j < E) se += __expf(v[j] - mx);
+      sum = wave_sum(se);
+    }
+  }
+  if (t < 3 && lane < K) chosen[t][lane] = -1;
+  __syncthreads();
+  if (active) {
 #pragma unroll
-        for (int j = 0; j < J; ++j) {
-          const int e = lane + 64 * j;
-          if (e < E && !((taken >> j) & 1u) && (v[j] > bv || (v[j] == bv && e < bi))) {
-            bv = v[j];
-            bi = e;
-          }
+    for (int j = 0; j < J; ++j) {
+      const int e = lane + 64 * j;
+      if (e < E) {
+        int rk = 0;
+        for (int e2 = 0; e2 < E; ++e2) {
+          const float w = lv[t][e2];
+          rk += (w > v[j] || (w == v[j] && e2 < e)) ? 1 : 0;
         }
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) {
-          const float ov = __shfl_xor(bv, off);
-          const int oi = __shfl_xor(bi, off);
-          if (ov > bv || (ov == bv && oi < bi)) {
-            bv = ov;
-            bi = oi;
-          }
-        }
-        if ((bi & 63) == lane) taken |= 1u << (bi >> 6);
-        if (lane == 0) {
-          chosen[t][k] = bi;
-          if (t == 0) pr[k] = __expf(bv - mx) / sum;
+        if (rk < K) {
+          chosen[t][rk] = e;
+          if (t == 0) pr[rk] = __expf(v[j] - mx) / sum;
         }
       }
-    } else if (lane < K) {
-      chosen[t][lane] = -1;
     }
   }
   __syncthreads();
@@ -259,13 +255,16 @@ __global__ __launch_bounds__(64) void k_tab_set(int* tab, TabUpdates u) {
 
 // Kernel: gate/up of the chosen experts for the slow row, SwiGLU, times the
 // router probability.  grid = K * F_e/16, block = 512.
+// With every expert resident (`hits` non-null) the first workgroup also
+// counts the layer's K cache hits on the device.
 template <int WB, bool SPEC = false>
 __global__ __launch_bounds__(kGemvThreads) void k_moe_gateup(Dims D, int Fe, int K, ExpertSlots es, int slow_row,
                                                              const float* mlp_norm, int layer, MoePtrs mp, WS ws,
-                                                             SlotTable stab) {
+                                                             SlotTable stab, unsigned long long* hits = nullptr) {
   int sslot = 0;
   if constexpr (SPEC)
     if (!spec_slot(stab, mp, ws, layer, K, sslot)) return;
+  if (hits && blockIdx.x == 0 && threadIdx.x == 0) atomicAdd(hits, (unsigned long long)K);
   __shared__ float red[kGemvWaves * 512];
   __shared__ float y[512];
   __shared__ const float* xrow_s[kMaxRows];
@@ -299,12 +298,34 @@ __global__ __launch_bounds__(kGemvThreads) void k_moe_gateup(Dims D, int Fe, int
 // (the K experts' matrices form one reduction of length K*F_e over the
 // probability-weighted activations), then the slow row's partial sums for the
 // next layer's norm.  grid = d/16, block = 512.
+// `stats_on_exit`: once the sequence has exited, the first workgroup adds the
+// slow row's sum of squares for the next layer instead (k_row_stats' work,
+// for a token enqueued without the host seeing the exit).
 template <int WB, bool SPEC = false>
 __global__ __launch_bounds__(kGemvThreads) void k_moe_down(Dims D, int Fe, int K, ExpertSlots es, int slow_row,
-                                                           int layer, MoePtrs mp, WS ws, SlotTable stab) {
+                                                           int layer, MoePtrs mp, WS ws, SlotTable stab,
+                                                           int stats_on_exit = 0) {
   int sslot = 0;
   if constexpr (SPEC)
-    if (!spec_slot(stab, mp, ws, layer, K, sslot)) return;
+    if (!spec_slot(stab, mp, ws, layer, K, sslot)) {
+      if (stats_on_exit && ws.exited[0] && blockIdx.x == 0) {
+        __shared__ float sred[kGemvWaves];
+        float ss = 0.f;
+        for (int i = threadIdx.x; i < D.d; i += kGemvThreads) {
+          const float x = ws.X[(size_t)slow_row * D.d + i];
+          ss += x * x;
+        }
+        ss = wave_sum(ss);
+        if ((threadIdx.x & 63) == 0) sred[threadIdx.x >> 6] = ss;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+          float a = 0.f;
+          for (int w = 0; w < kGemvWaves; ++w) a += sred[w];
+          add_agent(bin_d_at(ws, layer + 1, 0, slow_row), a);
+        }
+      }
+      return;
+    }
   __shared__ float red[kGemvWaves * 256];
   __shared__ float y[256];
   __shared__ float newx[16];

@@ -113,7 +113,7 @@ struct Layout {
   int pk_so_w, pk_sgu_w;
   // mixture of experts: router logits, choices, probabilities, activations,
   // and the expert cache ([n_layers][slots] slots of expert_stride bytes)
-  size_t moe_logits, moe_sel, moe_prob, moe_act, moe_slots, moe_tab;
+  size_t moe_logits, moe_sel, moe_prob, moe_act, moe_slots, moe_tab, moe_hits;
   size_t expert_bytes, expert_stride;
   int TD, TF, TV, S_max;
   size_t sk_slots;                       // partial-sum slots of the stream-K GEMVs
@@ -288,6 +288,7 @@ Layout make_layout(const m2r2_config& c, int max_batch, int max_chunk, int max_c
     L.expert_stride = (L.expert_bytes + 255) & ~(size_t)255;
     L.moe_slots = take(L.expert_stride * c.n_layers * c.expert_slots);
     L.moe_tab = take(sizeof(int) * c.n_layers * c.n_experts);
+    L.moe_hits = take(sizeof(unsigned long long));
   }
   L.total = off;
   return L;
@@ -374,6 +375,11 @@ struct MoeState {
   std::vector<int> tab_idx, tab_val;   // updates still to enqueue
   struct Pending { int l, slot, e; };
   std::vector<Pending> pend;        // copies published once they are complete
+  // a cache of E slots under the LRU policy holds every expert: tokens are
+  // enqueued whole, without waiting for any routing, and the expert kernel
+  // counts the hits on the device
+  unsigned long long* hits_d = nullptr;
+  bool hits_dev_used = false;       // hits_d may be non-zero
 };
 
 struct m2r2_ctx {
@@ -1238,6 +1244,15 @@ m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVP
   const Grids G = grids<WB, MT>(c);
   const int tiles = (M.E + 15) / 16;
   float* logits = (float*)M.mp.logits;
+  // every expert of every layer resident and published: nothing the host
+  // would decide depends on the routing (the LRU policy only counts hits)
+  tab_publish_done(M);
+  const bool resident = M.spec && M.C == M.E && M.policy == M2R2_MOE_ON_DEMAND && M.pend.empty() &&
+                        std::all_of(M.tab.begin(), M.tab.end(), [](int v) { return v >= 0; });
+  if (resident) {
+    HIP_TRY(tab_flush(c, st));
+    M.hits_dev_used = true;
+  }
   for (int l = 0; l < D.n_layers; ++l) {
     const LayerPtrs& L = c->layers[l];
     if (c->rw_on) {
@@ -1268,10 +1283,24 @@ m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVP
     int* slow_out = out->slow_experts_d ? out->slow_experts_d + l * M.K : nullptr;
     int* pred_out = (out->pred_experts_d && n_pred) ? out->pred_experts_d + (prev ? l + 1 : 2 * l + 2) * M.K
                                                     : nullptr;
-    const int seq = ++M.seq;
-    TIMED(10, (k_topk<<<1, 256, 0, st>>>(M.E, M.K, logits, 1, n_pred, M.mp, c->ws, slow_out, pred_out, seq)));
+    const int seq = resident ? 0 : ++M.seq;
+    MoePtrs mpk = M.mp;
+    if (resident) mpk.sel_host = nullptr;   // no host reads this layer's routing
+    TIMED(10, (k_topk<<<1, 256, 0, st>>>(M.E, M.K, logits, 1, n_pred, mpk, c->ws, slow_out, pred_out, seq)));
     HIP_TRY(hipGetLastError());
     const SlotTable stab{M.tab_d, M.slots_d, M.stride, M.E, M.C};
+    if (resident) {
+      // the experts from the table; an exited row's statistics from the down kernel
+      TIMED(8, (k_moe_gateup<WB, true><<<M.K * (M.Fe / 16), kGemvThreads, gl, st>>>(D, M.Fe, M.K, ExpertSlots{}, 0,
+                                                                                   L.mlp_norm, l, M.mp, c->ws, stab,
+                                                                                   M.hits_d)));
+      TIMED(9, (k_moe_down<WB, true><<<c->lay.TD, kGemvThreads, gl, st>>>(D, M.Fe, M.K, ExpertSlots{}, 0, l, M.mp,
+                                                                         c->ws, stab, 1)));
+      HIP_TRY(hipGetLastError());
+      HIP_TRY(hipEventRecord(M.layer_done[l], st));
+      M.layer_done_rec[l] = 1;
+      continue;
+    }
     if (M.spec) {
       // the experts from the slots the table publishes, without waiting for
       // the host (they return at once if a chosen expert is not published)
@@ -1426,6 +1455,9 @@ hipError_t moe_warm(m2r2_ctx* c) {
   M.tab_val.clear();
   M.pend.clear();
   if (e == hipSuccess) e = hipMemcpy(M.tab_d, M.tab.data(), sizeof(int) * M.tab.size(), hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemset(M.hits_d, 0, sizeof(unsigned long long));
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  M.hits_dev_used = false;
   return e;
 }
 
@@ -1617,6 +1649,7 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
     M.store_h = (const char*)w->experts_h;
     M.slots_d = b + lay.moe_slots;
     M.tab_d = (int*)(b + lay.moe_tab);
+    M.hits_d = (unsigned long long*)(b + lay.moe_hits);
     M.mp.logits = (const float*)(b + lay.moe_logits);
     M.mp.sel = (int*)(b + lay.moe_sel);
     M.mp.prob = (float*)(b + lay.moe_prob);
@@ -2049,6 +2082,12 @@ M2R2_API m2r2_status m2r2_moe_stats(m2r2_ctx* c, m2r2_moe_counters* out) {
   if (!c || !out) return fail(M2R2_E_INVALID, "NULL argument");
   if (!c->moe.on) return fail(M2R2_E_STATE, "not a mixture-of-experts context");
   fill_stats(c->moe.pol.counters(), out);
+  if (c->moe.hits_dev_used) {   // hits counted by the expert kernels of resident tokens
+    unsigned long long h = 0;
+    HIP_TRY(hipDeviceSynchronize());
+    HIP_TRY(hipMemcpy(&h, c->moe.hits_d, sizeof h, hipMemcpyDeviceToHost));
+    out->hits += (int64_t)h;
+  }
   out->h2d_bytes = c->moe.h2d_bytes;
   out->copy_waits = c->moe.copy_waits;
   out->host_wait_ns = c->moe.host_wait_ns;

@@ -146,11 +146,37 @@ def test_moe_dual_step_observe(name, slots):
 
 
 @pytest.mark.parametrize("name", ["small_moe_f32", "small_moe_rw"])
-def test_moe_exit_mode_fills_skipped_layers(name):
-    p = MoePair(name, slots=4)
+@pytest.mark.parametrize("resident", [False, True])
+def test_moe_exit_mode_fills_skipped_layers(name, resident):
+    """EXIT mode: the layers after the exit run no MLP and still fill their
+    cache entries.  With every expert resident the host never sees the exit
+    (the token is enqueued whole): the expert kernels skip themselves and the
+    down projection's launch adds the slow row's statistics instead."""
+    cfg = synth.CONFIGS[name]
+    p = MoePair(name, slots=cfg.n_experts if resident else 4, policy="on_demand" if resident else "ahead_of_time")
     t, slow_tr, _, _ = p.run(6, mode="exit", gates=[2], tau=-1.0)
     assert t.steps == 6 and t.compared >= 6
     assert all(np.all(s[2:] == -1) for s in slow_tr)
+    if resident:
+        st = p.model.moe_stats()
+        assert st["hits"] == 6 * 2 * cfg.top_k and st["misses"] == 0 and st["host_wait_ns"] == 0
+
+
+@pytest.mark.parametrize("name", ["small_moe", "small_moe_f32", "small_moe_rw"])
+def test_resident_cache_enqueues_whole_tokens(name):
+    """As many slots as experts under the LRU policy: every expert is taken
+    from its slot on the device and the host never waits for routing.  The
+    outputs match the oracle, and the hits the expert kernels count equal the
+    routed layers times top_k."""
+    cfg = synth.CONFIGS[name]
+    p = MoePair(name, slots=cfg.n_experts, policy="on_demand")
+    t, slow_tr, *_ = p.run(8, mode="observe", gates=list(range(1, cfg.n_layers)), tau=0.9)
+    assert t.steps >= 6 and t.compared >= 6 * t.steps
+    st = p.model.moe_stats()
+    routed = sum(int(np.sum(s[:, 0] >= 0)) for s in slow_tr)
+    assert routed == len(slow_tr) * cfg.n_layers
+    assert st["hits"] == routed * cfg.top_k
+    assert st["misses"] == 0 and st["loads"] == 0 and st["host_wait_ns"] == 0
 
 
 def test_moe_previous_layer_predictions_match_oracle():
