@@ -33,16 +33,18 @@ struct RouterTask {
   float* out;             // [E]
 };
 
-template <int WB>
-__global__ __launch_bounds__(kGemvThreads) void k_router(Dims D, int E, RouterTask t0, RouterTask t1, RouterTask t2,
-                                                         int n_tasks, WS ws) {
+// One 16-row tile of one task (workgroup `b` of tiles x n_tasks); AGENT: the
+// logits are stored at agent scope (read by another workgroup of the launch).
+template <int WB, bool AGENT>
+__device__ __forceinline__ void router_tile(const Dims& D, int E, const RouterTask& t0, const RouterTask& t1,
+                                            const RouterTask& t2, int n_tasks, const WS& ws, int b) {
   __shared__ float red[kGemvWaves * 256];
   __shared__ float y[256];
   __shared__ const float* xrow_s[kMaxRows];
   __shared__ float inv_rms;
   extern __shared__ __attribute__((aligned(16))) char dyn[];
   const int tiles = (E + 15) / 16;
-  const int task = blockIdx.x / tiles, tile = blockIdx.x % tiles;
+  const int task = b / tiles, tile = b % tiles;
   if (task >= n_tasks) return;
   const RouterTask T = task == 0 ? t0 : (task == 1 ? t1 : t2);
   const void* wrow[1] = {(const char*)T.packed + (size_t)tile * 16 * D.d * (WB ? 2 : 4)};
@@ -59,7 +61,18 @@ __global__ __launch_bounds__(kGemvThreads) void k_router(Dims D, int E, RouterTa
   f32x4_t acc[1];
   gw.run(xrow_s, T.gain, 1, dyn, acc);
   gemv_reduce<1>(acc, 1, red, y);
-  if (threadIdx.x < 16 && tile * 16 + (int)threadIdx.x < E) T.out[tile * 16 + threadIdx.x] = y[threadIdx.x] * inv_rms;
+  if (threadIdx.x < 16 && tile * 16 + (int)threadIdx.x < E) {
+    float* o = T.out + tile * 16 + threadIdx.x;
+    const float v = y[threadIdx.x] * inv_rms;
+    if constexpr (AGENT) st_agent(o, v);
+    else *o = v;
+  }
+}
+
+template <int WB>
+__global__ __launch_bounds__(kGemvThreads) void k_router(Dims D, int E, RouterTask t0, RouterTask t1, RouterTask t2,
+                                                         int n_tasks, WS ws) {
+  router_tile<WB, false>(D, E, t0, t1, t2, n_tasks, ws, blockIdx.x);
 }
 
 // Words of the mapped host block that k_topk fills.
@@ -76,8 +89,11 @@ constexpr int kHostWords = 64;
 // Wave t takes task t: every logit is ranked at once against the task's
 // logits in LDS (its place in the order larger value first, then lower id),
 // and a logit of rank < k is chosen at that rank (a NaN ranks as -inf).
-__global__ __launch_bounds__(256) void k_topk(int E, int K, const float* logits, int route, int n_pred, MoePtrs mp,
-                                              WS ws, int* slow_out, int* pred_out, int seq) {
+// AGENT: the logits were stored by other workgroups of the same launch.  Run
+// by a whole workgroup of at least 256 threads.
+template <bool AGENT>
+__device__ __forceinline__ void topk_body(int E, int K, const float* logits, int route, int n_pred, const MoePtrs& mp,
+                                          const WS& ws, int* slow_out, int* pred_out, int seq) {
   __shared__ int chosen[3][kMaxTopK];
   __shared__ float pr[kMaxTopK];
   __shared__ float lv[3][kMaxExperts];
@@ -93,7 +109,7 @@ __global__ __launch_bounds__(256) void k_topk(int E, int K, const float* logits,
 #pragma unroll
     for (int j = 0; j < J; ++j) {
       const int e = lane + 64 * j;
-      const float x = e < E ? logits[t * E + e] : -INFINITY;
+      const float x = e < E ? (AGENT ? ld_agent(logits + t * E + e) : logits[t * E + e]) : -INFINITY;
       v[j] = x == x ? x : -INFINITY;
       lv[t][e] = v[j];
     }
@@ -152,16 +168,23 @@ __global__ __launch_bounds__(256) void k_topk(int E, int K, const float* logits,
     if (i == 0) __hip_atomic_store(&mp.sel_host[kHostSeq], seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
   }
 }
+__global__ __launch_bounds__(256) void k_topk(int E, int K, const float* logits, int route, int n_pred, MoePtrs mp,
+                                              WS ws, int* slow_out, int* pred_out, int seq) {
+  topk_body<false>(E, K, logits, route, n_pred, mp, ws, slow_out, pred_out, seq);
+}
 
 // Kernel: the fast row's MLP of a mixture-of-experts layer, the rank-r
 // adapter alone: p += (rms(p) * g_mlp . A_m^T) B_m^T, with the adapter-down
 // sums taken from the bins of the o projection; then the partial sums of
 // the next layer's norm and of the exit signal.  grid = ceil(d/256), block = 256.
-__global__ __launch_bounds__(256) void k_fast_mlp(Dims D, RowMap rm, LayerPtrs L, int layer, WS ws) {
+// Block `blk` of the fast row's MLP (T threads per block).
+template <int T>
+__device__ __forceinline__ void fast_mlp_block(const Dims& D, const RowMap& rm, const LayerPtrs& L, int layer,
+                                               const WS& ws, int blk) {
   __shared__ float um[kMaxRank];
-  __shared__ float red[4];
-  const int nn = blockIdx.x * 256 + threadIdx.x;
-  const int bin = blockIdx.x % kBins;
+  __shared__ float red[T / 64];
+  const int nn = blk * T + threadIdx.x;
+  const int bin = blk % kBins;
   for (int m = 0; m < rm.M; ++m) {
     if (!rm.fast[m]) continue;
     const bool ex = ws.exited[rm.seq[m]] != 0;
@@ -193,6 +216,31 @@ __global__ __launch_bounds__(256) void k_fast_mlp(Dims D, RowMap rm, LayerPtrs L
     }
     __syncthreads();
   }
+}
+__global__ __launch_bounds__(256) void k_fast_mlp(Dims D, RowMap rm, LayerPtrs L, int layer, WS ws) {
+  fast_mlp_block<256>(D, rm, L, layer, ws, blockIdx.x);
+}
+
+// Kernel: the router tiles of up to three tasks (tiles x n_tasks workgroups,
+// as k_router), then, in the last of them to finish, the top-k of every task
+// (k_topk's work; `cnt` counts the arrivals and is left at zero).  With
+// `fmlp_blocks` > 0 the workgroups after the router tiles run the fast row's
+// MLP (k_fast_mlp's work): only when no task reads the fast row.
+// grid = tiles x n_tasks + fmlp_blocks, block = 512.
+template <int WB>
+__global__ __launch_bounds__(kGemvThreads) void k_route(Dims D, int E, RouterTask t0, RouterTask t1, RouterTask t2,
+                                                        int n_tasks, WS ws, int K, MoePtrs mp, int* slow_out,
+                                                        int* pred_out, int seq, uint32_t* cnt, RowMap rm, LayerPtrs L,
+                                                        int layer) {
+  __shared__ int last;
+  const int nr = ((E + 15) / 16) * n_tasks;
+  if ((int)blockIdx.x >= nr) {
+    fast_mlp_block<kGemvThreads>(D, rm, L, layer, ws, (int)blockIdx.x - nr);
+    return;
+  }
+  router_tile<WB, true>(D, E, t0, t1, t2, n_tasks, ws, blockIdx.x);
+  if (!arrive_last(cnt, (uint32_t)nr, &last)) return;
+  topk_body<true>(E, K, t0.out, 1, n_tasks - 1, mp, ws, slow_out, pred_out, seq);
 }
 
 // Kernel: sum of squares of residual row `row` into the bins entering layer

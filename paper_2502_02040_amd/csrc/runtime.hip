@@ -288,7 +288,7 @@ Layout make_layout(const m2r2_config& c, int max_batch, int max_chunk, int max_c
     L.expert_stride = (L.expert_bytes + 255) & ~(size_t)255;
     L.moe_slots = take(L.expert_stride * c.n_layers * c.expert_slots);
     L.moe_tab = take(sizeof(int) * c.n_layers * c.n_experts);
-    L.moe_hits = take(sizeof(unsigned long long));
+    L.moe_hits = take(256);   // device hit counter (offset 0), arrival counter of k_route (offset 128)
   }
   L.total = off;
   return L;
@@ -380,6 +380,7 @@ struct MoeState {
   // counts the hits on the device
   unsigned long long* hits_d = nullptr;
   bool hits_dev_used = false;       // hits_d may be non-zero
+  uint32_t* route_cnt_d = nullptr;  // arrivals of the router workgroups (k_route), zero between launches
 };
 
 struct m2r2_ctx {
@@ -1266,7 +1267,6 @@ m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVP
       TIMED(1, (k_attn<KB, HD><<<dim3(S + 1, D.H, 1), kAttnThreads, smem, st>>>(D, L, rm, c->ws, io, kv, l, S)));
       TIMED(2, (k_oproj<WB, MT><<<G.o, kGemvThreads, G.l_q, st>>>(D, L, rm, c->ws, io, l)));
     }
-    if (dual) TIMED(10, (k_fast_mlp<<<(D.d + 255) / 256, 256, 0, st>>>(D, rm, L, l, c->ws)));
     // routing of the slow row, predictions for layers 2l+2 and 2l+3 from the fast row
     RouterTask t[3] = {};
     t[0] = RouterTask{M.router[l], L.mlp_norm, 0, 0, l, logits};
@@ -1278,15 +1278,20 @@ m2r2_status run_moe_t(m2r2_ctx* c, const RowMap& rm, const StepIO& io, const KVP
     // slow-row vector that layer l routes
     if (prev && l + 1 < D.n_layers)
       t[1 + n_pred++] = RouterTask{M.router[l + 1], c->layers[l + 1].mlp_norm, 0, 0, l, logits + M.E};
-    TIMED(10, (k_router<WB><<<tiles * (1 + n_pred), kGemvThreads, gl, st>>>(D, M.E, t[0], t[1], t[2], 1 + n_pred,
-                                                                          c->ws)));
+    // the fast row's MLP runs inside the routing launch unless a prediction
+    // task reads the fast row it produces
+    const int fmlp_blocks = dual && n_pred == 0 ? (D.d + kGemvThreads - 1) / kGemvThreads : 0;
+    if (dual && !fmlp_blocks) TIMED(10, (k_fast_mlp<<<(D.d + 255) / 256, 256, 0, st>>>(D, rm, L, l, c->ws)));
     int* slow_out = out->slow_experts_d ? out->slow_experts_d + l * M.K : nullptr;
     int* pred_out = (out->pred_experts_d && n_pred) ? out->pred_experts_d + (prev ? l + 1 : 2 * l + 2) * M.K
                                                     : nullptr;
     const int seq = resident ? 0 : ++M.seq;
     MoePtrs mpk = M.mp;
     if (resident) mpk.sel_host = nullptr;   // no host reads this layer's routing
-    TIMED(10, (k_topk<<<1, 256, 0, st>>>(M.E, M.K, logits, 1, n_pred, mpk, c->ws, slow_out, pred_out, seq)));
+    // router tiles, then the top-k in the last of them to finish
+    TIMED(10, (k_route<WB><<<tiles * (1 + n_pred) + fmlp_blocks, kGemvThreads, gl, st>>>(
+                  D, M.E, t[0], t[1], t[2], 1 + n_pred, c->ws, M.K, mpk, slow_out, pred_out, seq, M.route_cnt_d, rm, L,
+                  l)));
     HIP_TRY(hipGetLastError());
     const SlotTable stab{M.tab_d, M.slots_d, M.stride, M.E, M.C};
     if (resident) {
@@ -1421,7 +1426,8 @@ template <int WB>
 hipError_t set_moe_lds_limits() {
   const int bytes = gemv_lds_bytes(WB, 2);
   hipError_t e = hipSuccess;
-  const void* fns[] = {(const void*)k_router<WB>, (const void*)k_moe_gateup<WB>, (const void*)k_moe_down<WB>,
+  const void* fns[] = {(const void*)k_router<WB>, (const void*)k_route<WB>, (const void*)k_moe_gateup<WB>,
+                       (const void*)k_moe_down<WB>,
                        (const void*)k_moe_gateup<WB, true>, (const void*)k_moe_down<WB, true>};
   for (const void* f : fns) {
     hipError_t r = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
@@ -1455,7 +1461,7 @@ hipError_t moe_warm(m2r2_ctx* c) {
   M.tab_val.clear();
   M.pend.clear();
   if (e == hipSuccess) e = hipMemcpy(M.tab_d, M.tab.data(), sizeof(int) * M.tab.size(), hipMemcpyHostToDevice);
-  if (e == hipSuccess) e = hipMemset(M.hits_d, 0, sizeof(unsigned long long));
+  if (e == hipSuccess) e = hipMemset(M.hits_d, 0, 256);   // (and the router arrival counter)
   if (e == hipSuccess) e = hipDeviceSynchronize();
   M.hits_dev_used = false;
   return e;
@@ -1650,6 +1656,7 @@ M2R2_API m2r2_status m2r2_create(const m2r2_config* cfg, const m2r2_weights* w, 
     M.slots_d = b + lay.moe_slots;
     M.tab_d = (int*)(b + lay.moe_tab);
     M.hits_d = (unsigned long long*)(b + lay.moe_hits);
+    M.route_cnt_d = (uint32_t*)(b + lay.moe_hits + 128);
     M.mp.logits = (const float*)(b + lay.moe_logits);
     M.mp.sel = (int*)(b + lay.moe_sel);
     M.mp.prob = (float*)(b + lay.moe_prob);
