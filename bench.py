@@ -313,17 +313,31 @@ def _prefill(model, prompt, pos, desc, dev):
     return targets[i:i + 1].clone()
 
 
-def _time_graph(g, stream, steps):
+def _time_graph(g, stream, steps, per_step=None):
+    """Milliseconds of `steps` back-to-back replays of the graph, from HIP
+    events on its stream; with `per_step` (a list) an event is also recorded
+    after every replay and the single replays' durations are appended."""
     import torch
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1 if per_step is not None else 2)]
     torch.cuda.synchronize()
     with torch.cuda.stream(stream):
-        e0.record(stream)
-        for _ in range(steps):
+        ev[0].record(stream)
+        for i in range(steps):
             g.replay()
-        e1.record(stream)
+            if per_step is not None:
+                ev[i + 1].record(stream)
+        if per_step is None:
+            ev[1].record(stream)
     torch.cuda.synchronize()
-    return e0.elapsed_time(e1)
+    if per_step is not None:
+        per_step.extend(ev[i].elapsed_time(ev[i + 1]) for i in range(steps))
+    return ev[0].elapsed_time(ev[-1])
+
+
+def _pcts(xs):
+    """p10 / p50 / p90 of per-step milliseconds."""
+    import numpy as np
+    return {k: round(float(np.percentile(xs, q)), 5) for k, q in (("p10", 10), ("p50", 50), ("p90", 90))}
 
 
 def _kernel_avg_ms(model, kernel, stream, fn, reps):
@@ -383,7 +397,8 @@ def run_dense(args) -> int:
     setup_s = time.perf_counter() - t_setup
 
     ctx0 = int(pos.item())
-    ms = _time_graph(g, stream, args.steps)
+    per = []
+    ms = _time_graph(g, stream, args.steps, per)
     ms_step = ms / args.steps
     ctx_mean = ctx0 + (args.steps - 1) / 2.0
 
@@ -415,7 +430,7 @@ def run_dense(args) -> int:
 
     cpu = cpu_baseline(cfg, weights, args.ctx, args.cpu_budget) if args.cpu_budget > 0 else None
     _line(value=round(1000.0 / ms_step, 3), unit="tokens/s", steps=args.steps, warmup=args.warmup,
-          ms_per_step=round(ms_step, 5), dtype="bf16" if cfg.wdtype == "bf16" else "f32",
+          ms_per_step=round(ms_step, 5), ms_per_step_pcts=_pcts(per), dtype="bf16" if cfg.wdtype == "bf16" else "f32",
           config={"workload": f"{'dual' if dual else 'single'}-stream decode step, {cfg.name}-shaped "
                               f"{cfg.n_layers}L d{cfg.d_model} {cfg.n_heads}x{cfg.head_dim} ffn{cfg.ffn} "
                               f"vocab{cfg.vocab} rank{cfg.rank}, {cfg.wdtype} weights/KV, batch 1, "
@@ -476,7 +491,8 @@ def run_batch(args) -> int:
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t_setup
     ctx0 = int(pos[0].item())
-    ms = _time_graph(g, stream, args.steps)
+    per = []
+    ms = _time_graph(g, stream, args.steps, per)
     ms_step = ms / args.steps
     ctx_mean = ctx0 + (args.steps - 1) / 2.0
     k_avg_ms, k_n = _kernel_avg_ms(model, "attn", stream, step, args.kernel_reps)
@@ -493,7 +509,7 @@ def run_batch(args) -> int:
     cpu = cpu_baseline(cfg, synth.make_weights(cfg), ctx, args.cpu_budget, seqs=B) if args.cpu_budget > 0 else None
     _line(metric="batched decode tokens/s (aggregate) + achieved HBM GB/s of the dual-stream step",
           value=round(B * 1000.0 / ms_step, 3), unit="tokens/s", steps=args.steps, warmup=args.warmup,
-          ms_per_step=round(ms_step, 5), dtype="bf16" if cfg.wdtype == "bf16" else "f32",
+          ms_per_step=round(ms_step, 5), ms_per_step_pcts=_pcts(per), dtype="bf16" if cfg.wdtype == "bf16" else "f32",
           config={"workload": f"{'dual' if dual else 'single'}-stream decode step, {cfg.name}-shaped model, batch {B}, "
                               f"paged KV context {ctx} per sequence (block 16, shuffled table, seeded N(0,1) "
                               f"content), HIP graph replay", "batch": B, "kv_context": ctx, "dual_stream": dual},
