@@ -55,17 +55,6 @@ __device__ __forceinline__ float4 ld4(const float* p) { return *(const float4*)p
 // ----------------------------------------------------------------------------
 // Wave reductions (64 lanes)
 // ----------------------------------------------------------------------------
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
-}
-
 // Lane exchanges inside a row of 16 lanes through DPP (a VALU operand
 // modifier; __shfl_xor compiles to ds_bpermute, an LDS round trip).
 template <int CTRL>
@@ -89,6 +78,31 @@ __device__ __forceinline__ float row_sum16(float v) {
 __device__ __forceinline__ float row_sum_stride4(float v) {
   v += dpp_f<kDppRowRor8>(v);
   return v + dpp_f<kDppRowRor4>(v);
+}
+// maximum over the 16 lanes of a row (a lane whose source is disabled keeps
+// its own value)
+template <int CTRL>
+__device__ __forceinline__ float dpp_keep(float v) {
+  const int b = __builtin_bit_cast(int, v);
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(b, b, CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float row_max16(float v) {
+  v = fmaxf(v, dpp_keep<kDppQuadXor1>(v));
+  v = fmaxf(v, dpp_keep<kDppQuadXor2>(v));
+  v = fmaxf(v, dpp_keep<kDppRowHalfMirror>(v));
+  return fmaxf(v, dpp_keep<kDppRowMirror>(v));
+}
+// Sum and maximum over the 64 lanes (every lane gets it): the rows of 16 by
+// DPP, then two lane exchanges across rows.
+__device__ __forceinline__ float wave_sum(float v) {
+  v = row_sum16(v);
+  v += __shfl_xor(v, 16);
+  return v + __shfl_xor(v, 32);
+}
+__device__ __forceinline__ float wave_max(float v) {
+  v = row_max16(v);
+  v = fmaxf(v, __shfl_xor(v, 16));
+  return fmaxf(v, __shfl_xor(v, 32));
 }
 
 // Block-wide sum of one value per thread; `red` holds blockDim/64 floats.

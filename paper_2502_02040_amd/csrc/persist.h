@@ -156,8 +156,10 @@ __device__ __forceinline__ void pk_slot_sum(const float* slots, int G, int C, fl
   for (int i = 1; i < NL; ++i) {
     a.x += v[i].x; a.y += v[i].y; a.z += v[i].z; a.w += v[i].w;
   }
+  // within a row of 16 lanes by DPP, across rows by lane exchanges
+  a.x = row_sum16(a.x); a.y = row_sum16(a.y); a.z = row_sum16(a.z); a.w = row_sum16(a.w);
   const int tl = tpc < 64 ? tpc : 64;
-  for (int o = tl / 2; o >= 1; o >>= 1) {
+  for (int o = 16; o < tl; o <<= 1) {
     a.x += __shfl_xor(a.x, o);
     a.y += __shfl_xor(a.y, o);
     a.z += __shfl_xor(a.z, o);
