@@ -67,9 +67,9 @@ struct PkArgs {
   WS ws;
   StepIO io;
   KVPtrs kv;
-  float* sd;                 // [G][kPkSdW] rows' x^2, pin.x, pin^2 leaving the down projection
-  float* so;                 // [G][so_w]   x^2 of rows 0, 1 after the o projection; gate, up adapter-down (fast row)
-  float* sgu;                // [G][sgu_w]  down adapter-down of the fast row
+  float* sd;                 // [kPkSdW/4][G][4] rows' x^2, pin.x, pin^2 leaving the down projection
+  float* so;                 // [so_w/4][G][4] x^2 of rows 0, 1 after the o projection; gate, up adapter-down (fast row)
+  float* sgu;                // [sgu_w/4][G][4] down adapter-down of the fast row
   PkBar bar;                 // grid barrier: group counters and flags, zero at launch, reset by the last workgroup
   int n_layers_run;
   int S;                     // attention splits per head
@@ -135,9 +135,14 @@ __device__ __forceinline__ void pk_wait(const PkBar& b, uint32_t epoch, int* err
   __syncthreads();
 }
 
-// out[0..C) = sum over the G workgroup slots of slots[s * C + c], in one fixed
-// order (the same in every workgroup and every run).  C is a multiple of 4,
-// at most 64.  red holds kPkWaves float4.  Ends with a workgroup barrier.
+// out[0..C) = sum over the G workgroup slots of column c, in one fixed order
+// (the same in every workgroup and every run).  C is a multiple of 4, at most
+// 64.  Layout: with T (the workgroup slots) column c of slot s at
+// ((c / 4) G + s) 4 + c % 4, so that the lanes of a wave read consecutive
+// slots' float4 from one contiguous run (a slot per 16 bytes, not one cache
+// line per lane); without T at s C + c.  red holds kPkWaves float4.  Ends
+// with a workgroup barrier.
+template <bool T>
 __device__ __forceinline__ void pk_slot_sum(const float* slots, int G, int C, float* red, float* out) {
   const int C4 = C / 4;
   int tpc = 1;   // threads per float4 column: a power of two, at least 32 for C <= 64
@@ -149,7 +154,7 @@ __device__ __forceinline__ void pk_slot_sum(const float* slots, int G, int C, fl
 #pragma unroll
   for (int i = 0; i < NL; ++i) {
     const int s = j + i * tpc;
-    v[i] = (c < C4 && s < G) ? pk_ld4(rs, (s * C + 4 * c) * 4) : make_float4(0.f, 0.f, 0.f, 0.f);
+    v[i] = (c < C4 && s < G) ? pk_ld4(rs, (T ? (c * G + s) * 4 : s * C + 4 * c) * 4) : make_float4(0.f, 0.f, 0.f, 0.f);
   }
   float4 a = v[0];
 #pragma unroll
@@ -202,10 +207,14 @@ __device__ __forceinline__ void pk_load_rows(const float* base, int off0, int of
 // Sum over the workgroup of one value per wave lane (lane i of every wave
 // holds value i, i < n) into the G-slot array `slot` at [blockIdx][o + i],
 // with agent-scope stores.
+// Column k of this workgroup's slot in a [C/4][G][4] slot array.
+__device__ __forceinline__ float* pk_slot_at(float* slots, int k) {
+  return slots + (((size_t)(k >> 2) * gridDim.x + blockIdx.x) << 2) + (k & 3);
+}
 template <int NW>
-__device__ __forceinline__ void pk_wg_store(float v, int n, float* scratch, float* tot, float* slot) {
+__device__ __forceinline__ void pk_wg_store(float v, int n, float* scratch, float* tot, float* slots, int k0) {
   rw_wg_sum<NW>(v, n, scratch, tot);
-  if ((int)threadIdx.x < n) st_agent(slot + threadIdx.x, tot[threadIdx.x]);
+  if ((int)threadIdx.x < n) st_agent(pk_slot_at(slots, k0 + (int)threadIdx.x), tot[threadIdx.x]);
 }
 
 // ---------------------------------------------------------------------------
@@ -570,7 +579,7 @@ __device__ __forceinline__ void pk_phase_qkv(int l, uint32_t& target, PkShared& 
         __syncthreads();
       } else {
         pk_load_rows<PM>(P.ws.X, 0, (M > 1 ? 1 : 0) * d, attn_norm, d, xp);
-        pk_slot_sum(P.sd, G, kPkSdW, sh.red, sh.ssum);
+        pk_slot_sum<true>(P.sd, G, kPkSdW, sh.red, sh.ssum);
       }
       int newly = 0;
       if (tid == 0) {
@@ -1043,14 +1052,13 @@ __device__ __forceinline__ void pk_phase_o(int l, uint32_t& target, PkShared& sh
       RwPieces<PM> xp;
       pk_load_rows<PM>(P.ws.O, 0, (M > 1 ? 1 : 0) * qd, nullptr, qd, xp);
       if (fm >= 0 && has_o) {
-        pk_slot_sum(P.ws.uo + (size_t)fm * D.H * r, D.H, r, sh.red, sh.stat);
+        pk_slot_sum<false>(P.ws.uo + (size_t)fm * D.H * r, D.H, r, sh.red, sh.stat);
       }
       rw_store_pieces<false, PM, kPkThreads>(xp, qd, pk_dyn);
       st.template run<true>(row_ptr, u0, u1, pk_dyn, qd, epi, ops);
-      float* slot = P.so + (size_t)blockIdx.x * P.so_w;
-      pk_wg_store<kPkWaves>(epi.accx, 2, sh.wsum, sh.tot, slot);
-      pk_wg_store<kPkWaves>(fm >= 0 ? epi.accf : 0.f, 2 * r, sh.wsum, sh.tot, slot + 2);
-      if (tid >= 2 + 2 * r && tid < P.so_w) st_agent(slot + tid, 0.f);   // the slot's padding
+      pk_wg_store<kPkWaves>(epi.accx, 2, sh.wsum, sh.tot, P.so, 0);
+      pk_wg_store<kPkWaves>(fm >= 0 ? epi.accf : 0.f, 2 * r, sh.wsum, sh.tot, P.so, 2);
+      if (tid >= 2 + 2 * r && tid < P.so_w) st_agent(pk_slot_at(P.so, tid), 0.f);   // the slot's padding
       pk_arrive(P.bar, target + 1);
     }
 
@@ -1088,11 +1096,11 @@ __device__ __forceinline__ void pk_phase_gu(int l, uint32_t& target, PkShared& s
       constexpr int PM = RwPM<WB, CD::NCH, CD::NS, kPkThreads>::value;
       RwPieces<PM> xp;
       pk_load_rows<PM>(P.ws.X, 0, (M > 1 ? 1 : 0) * d, mlp_norm, d, xp);
-      pk_slot_sum(P.so, G, P.so_w, sh.red, sh.stat);
+      pk_slot_sum<true>(P.so, G, P.so_w, sh.red, sh.stat);
       if (tid < 2) sh.inv_rms[tid] = rsqrtf(sh.stat[min(tid, M - 1)] / d + D.eps);
       rw_store_pieces<true, PM, kPkThreads>(xp, d, pk_dyn);
       st.template run<true>(row_ptr, u0, u1, pk_dyn, d, epi, ops);
-      pk_wg_store<kPkWaves>(fm >= 0 ? epi.accf : 0.f, r, sh.wsum, sh.tot, P.sgu + (size_t)blockIdx.x * P.sgu_w);
+      pk_wg_store<kPkWaves>(fm >= 0 ? epi.accf : 0.f, r, sh.wsum, sh.tot, P.sgu, 0);
       pk_arrive(P.bar, target + 1);
     }
 
@@ -1124,10 +1132,10 @@ __device__ __forceinline__ void pk_phase_dn(int l, uint32_t& target, PkShared& s
       constexpr int PM = RwPM<WB, CF::NCH, CF::NS, kPkThreads>::value;
       RwPieces<PM> xp;
       pk_load_rows<PM>(P.ws.ACT, 0, (M > 1 ? 1 : 0) * D.F, nullptr, D.F, xp);
-      if (fm >= 0 && hd_ad) pk_slot_sum(P.sgu, G, P.sgu_w, sh.red, sh.stat);
+      if (fm >= 0 && hd_ad) pk_slot_sum<true>(P.sgu, G, P.sgu_w, sh.red, sh.stat);
       rw_store_pieces<false, PM, kPkThreads>(xp, D.F, pk_dyn);
       st.template run<true>(row_ptr, u0, u1, pk_dyn, D.F, epi, ops);
-      pk_wg_store<kPkWaves>(epi.acc, kPkSdW, sh.wsum, sh.tot, P.sd + (size_t)blockIdx.x * kPkSdW);
+      pk_wg_store<kPkWaves>(epi.acc, kPkSdW, sh.wsum, sh.tot, P.sd, 0);
       pk_arrive(P.bar, target + 1);
     }
 }
@@ -1156,7 +1164,7 @@ __device__ __forceinline__ void pk_phase_head(int l, uint32_t& target, PkShared&
     constexpr int PM = RwPM<WB, CD::NCH, CD::NS, kPkThreads>::value;
     RwPieces<PM> xp;
     pk_load_rows<PM>(P.ws.X, 0, (M > 1 ? 1 : 0) * d, P.final_norm, d, xp);
-    pk_slot_sum(P.sd, G, kPkSdW, sh.red, sh.ssum);
+    pk_slot_sum<true>(P.sd, G, kPkSdW, sh.red, sh.ssum);
     if (tid == 0) {
       // the row fed to the head: the slow row, or the fast row when it exited
       // at a gate or runs alone (a draft)
