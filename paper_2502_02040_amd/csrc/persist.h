@@ -145,8 +145,8 @@ __device__ __forceinline__ void pk_wait(const PkBar& b, uint32_t epoch, int* err
 template <bool T>
 __device__ __forceinline__ void pk_slot_sum(const float* slots, int G, int C, float* red, float* out) {
   const int C4 = C / 4;
-  int tpc = 1;   // threads per float4 column: a power of two, at least 32 for C <= 64
-  while (tpc < 256 && 2 * tpc * C4 <= kPkThreads) tpc *= 2;
+  int tpc = 1;   // threads per float4 column: a power of two, 32 or 64 for C <= 64 (no cross-wave step)
+  while (tpc < 64 && 2 * tpc * C4 <= kPkThreads) tpc *= 2;
   const int t = threadIdx.x, c = t / tpc, j = t % tpc;
   const __amdgpu_buffer_rsrc_t rs = pk_rsrc(slots);
   constexpr int NL = kPkMaxWG / 32;
