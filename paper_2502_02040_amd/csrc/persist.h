@@ -523,6 +523,20 @@ __device__ __forceinline__ void pk_phase_qkv(int l, uint32_t& target, PkShared& 
       PkQkvEpi epi{M, sh.src, sh.inv_rms, P.ws.QKV, nqkv, qd, r, (int)hasA[0] | ((int)hasA[1] << 1) | ((int)hasA[2] << 2)};
       PkQkvEpi::Ops ops[decltype(st)::P];
       st.begin_all(row_ptr, u0, u1, epi, ops);
+      // gate inputs that do not depend on the layer's statistics, read while
+      // the barrier is pending (one sequence: its last row is the fast row)
+      int g_f = 0, g_fast = 0, g_slow = -1, g_r0 = 0, g_r1 = 0;
+      if (tid == 0) {
+        g_f = rml.first[0] + rml.cnt[0] - 1;
+        g_fast = rml.fast[g_f];
+        g_slow = rml.slow_of[g_f];
+        g_r0 = rml.fast[0] ? rml.slow_of[0] : 0;
+        g_r1 = rml.fast[M - 1] ? rml.slow_of[M - 1] : M - 1;
+      }
+      const bool g_gate = is_gate(P.io, l);
+      const int g_mode = P.io.mode;
+      const float g_tau = P.io.tau;
+      const float* g_asig = P.io.arla_sig;
       if (l > 0) {
         target += 1;
         pk_wait(P.bar, target, P.ws.err, &sh.broken);
@@ -583,22 +597,33 @@ __device__ __forceinline__ void pk_phase_qkv(int l, uint32_t& target, PkShared& 
       }
       int newly = 0;
       if (tid == 0) {
-        int exi[2] = {sh.ex, sh.ex}, ebi[2] = {sh.eb, sh.eb}, ri[2] = {0, 0}, exo[2] = {0, 0}, ebo[2] = {0, 0};
-        float sg[2] = {0.f, 0.f};
-        sk_gate_logic(D, rml, exi, ebi, P.io, l, sh.ssum, ri, exo, ebo, sg);
-        newly = exo[0] && !sh.ex;
-        sh.ri = ri[0];
-        sh.ex = exo[0];
-        sh.eb = ebo[0];
-        if (blockIdx.x == 0 && l > 0) st_agent(&P.ws.sig[l - 1], sg[0]);
-#pragma unroll
-        for (int m = 0; m < 2; ++m) {
-          const int mm = min(m, M - 1);
-          int src = mm;
-          if (rml.fast[mm] && ri[0]) src = rml.slow_of[mm];
-          sh.src[m] = src;
-          sh.inv_rms[m] = rsqrtf(sh.ssum[src * 4] / d + D.eps);
+        // the gate rule of sk_gate_logic for the one sequence: the exit signal
+        // (cosine of the fast row's update, or the router score) decides at a
+        // gate; a gate that does not exit re-initialises the fast row
+        int ex = sh.ex, eb = sh.eb, ri = 0;
+        float sg = 0.f;
+        if (l > 0 && g_fast) {
+          const float dot = sh.ssum[g_f * 4 + 1], pin2 = sh.ssum[g_f * 4 + 2], pp = sh.ssum[g_f * 4 + 0];
+          sg = dot * rsqrtf(fmaxf(pin2 * pp, 1e-30f));
+          if (g_asig && g_gate) sg = g_asig[0];
+          if (!ex && g_mode != EX_OFF && g_gate && g_slow >= 0) {
+            const bool fired = sg >= g_tau;
+            if (fired && eb == D.n_layers) eb = l;
+            if (g_mode == EX_EXIT && fired) ex = 1;
+            else ri = 1;
+          }
         }
+        newly = ex && !sh.ex;
+        sh.ri = ri;
+        sh.ex = ex;
+        sh.eb = eb;
+        if (blockIdx.x == 0 && l > 0) st_agent(&P.ws.sig[l - 1], sg);
+        // the rows' norm sources: a re-initialised fast row takes its slow row's
+        const int s0 = ri ? g_r0 : 0, s1 = ri ? g_r1 : M - 1;
+        sh.src[0] = s0;
+        sh.src[1] = s1;
+        sh.inv_rms[0] = rsqrtf(sh.ssum[s0 * 4] / d + D.eps);
+        sh.inv_rms[1] = rsqrtf(sh.ssum[s1 * 4] / d + D.eps);
         sh.last_flag = newly;
       }
       __syncthreads();
